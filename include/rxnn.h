@@ -1,0 +1,223 @@
+/*
+ * rxnn.h -- C ABI of the MI355X (gfx950) Fast Crossbar Model library.
+ *
+ * The library evaluates DNN layers on simulated resistive crossbars the way
+ * the Fast Crossbar Model (FCM) of RxNN (arXiv 1809.00072) defines it:
+ *
+ *   phase 1, model generation (Sec. V-A, generator steps 1-3):
+ *     the P x Q weight matrix is cut into M x N crossbar tiles (zero padded),
+ *     every tile becomes one or more conductance arrays (a differential pair
+ *     per weight slice), and every array's conductances G become the
+ *     equivalent non-ideal conductance matrix G' of the resistive network
+ *     with driver, wire and sense resistances (Sec. V-B, Eqs. 2-14).
+ *   phase 2, evaluation (Sec. V-A "peripheral models", Eq. 14, Sec. VI):
+ *     DAC transfer of the layer inputs, I = V . G' per array, ADC transfer
+ *     and quantisation, and digital accumulation of the codes over row tiles,
+ *     slices and the differential pair.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * - Device pointers are HIP device memory of the current device (e.g. the
+ *   data_ptr() of a torch tensor on "cuda"); host pointers are ordinary host
+ *   memory.  Every array is dense and row-major unless stated.
+ * - `stream` is a hipStream_t passed as void* (NULL = the null stream).
+ *   Every call is asynchronous and stream ordered unless stated: the caller
+ *   keeps its inputs alive and its outputs untouched until the stream has
+ *   reached the call.
+ * - Calls on one rxnn_layer are not thread safe and must be ordered on one
+ *   stream: the layer owns a scratch workspace that its calls reuse.
+ * - No exception crosses the ABI.  Arguments are validated before any launch;
+ *   a failure returns a negative rxnn_status and leaves a message that
+ *   rxnn_last_error() returns (per thread).  HIP failures map to RXNN_EHIP.
+ *
+ * Tile-local orientation (the reading of Eqs. 2-8): row 0 of a tile is the
+ * paper's row 1, the row farthest from the sense amplifiers; column 0 is the
+ * paper's column 1, the column nearest the row drivers.
+ */
+#ifndef RXNN_H
+#define RXNN_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  RXNN_OK = 0,
+  RXNN_EINVAL = -1,       /* an argument is out of range or inconsistent      */
+  RXNN_ENOMEM = -2,       /* a device allocation failed                       */
+  RXNN_EHIP = -3,         /* a HIP runtime call failed                        */
+  RXNN_EUNSUPPORTED = -4  /* valid, but not supported by this build           */
+} rxnn_status;
+
+/* Opaque handle of one mapped layer: owns the tiled G' buffer on the device. */
+typedef struct rxnn_layer rxnn_layer;
+
+/*
+ * Crossbar and device parameters (Sec. III, IV-A, V-A generator steps 1-2).
+ *
+ * rows, cols       crossbar size M x N, each 1..64 in this build (1..256 are
+ *                  valid; sizes above 64 return RXNN_EUNSUPPORTED).
+ * g_min, g_max     conductance range of one device in siemens, 0 < g_min < g_max.
+ * r_driver         Thevenin resistance of each row driver (ohm, >= 0).  It sits
+ *                  in series with the first row-wire segment, so the
+ *                  load-dependent DAC output of Sec. IV-A is part of G'.
+ * r_sense          sense resistance between each column's last node and the
+ *                  virtual ground (ohm, >= 0).
+ * r_row, r_col     resistance of one row-wire / column-wire segment (ohm, >= 0).
+ * weight_bits      0: continuous conductances; else the magnitude |w| is
+ *                  quantised to 2^weight_bits - 1 levels (1..16).
+ * bits_per_slice   0: one slice of weight_bits bits; else the level is cut
+ *                  into weight_bits / bits_per_slice slices of that many bits,
+ *                  each on its own differential pair (shift-and-add).
+ * w_max            |w| that maps to g_max; <= 0 means max|W| of the layer,
+ *                  computed on the device at mapping time.
+ * variation        reserved for per-device variation factors; must be NULL.
+ *
+ * Mapping of one weight w (fp64):
+ *   continuous: G+ = g_min + s_w max(w,0), G- = g_min + s_w max(-w,0),
+ *               s_w = (g_max - g_min) / w_max.
+ *   quantised:  q = min(L_w, rint(|w| * (L_w / w_max))), L_w = 2^weight_bits - 1,
+ *               slice s digit d_s = (q >> (b_s s)) & (2^b_s - 1); the side of
+ *               sign(w) gets g_min + d_s dG, the other side g_min,
+ *               dG = (g_max - g_min) / (2^b_s - 1).
+ * Arrays at one tile position are ordered a = 2 s + side (side 0 = positive,
+ * slice 0 least significant); array a carries the digital weight
+ * (side ? -1 : +1) * 2^(b_s s).  Zero-padded positions hold weight 0, i.e.
+ * devices at g_min that still load the network.
+ */
+typedef struct {
+  int32_t rows, cols;
+  double g_min, g_max;
+  double r_driver, r_sense, r_row, r_col;
+  int32_t weight_bits;
+  int32_t bits_per_slice;
+  double w_max;
+  const float* variation;
+} rxnn_xbar_params;
+
+/*
+ * Peripheral (DAC / ADC) parameters (Sec. IV-A "non-ideal DAC", Sec. V-A
+ * "peripheral models"; the curves are a stated reading of a figure that the
+ * paper's text does not reproduce).  phi_b(u) = u - b u (1 - u).
+ *
+ * DAC (dac_bits 1..8): code c = clamp(rint(fp32(x) * s_in), 0, L) with
+ *   s_in = fp32(L / x_max), L = 2^dac_bits - 1, one fp32 multiply rounded to
+ *   nearest even; row voltage V = fp32(v_read * phi_{dac_bend}(c / L)).
+ *   dac_bits = 0: ideal DAC, V = max(x, 0) * fp32(v_read / x_max).
+ * ADC (adc_bits 1..8): I_FS = v_read * M * g_max, L = 2^adc_bits - 1,
+ *   thresholds t_k = fp32(I_FS * phi_{adc_bend}((k - 1/2) / L)), k = 1..L;
+ *   code = #{k : fp32(I) >= t_k}.  adc_bits = 0: ideal ADC (the current
+ *   itself is accumulated).
+ * x_max > 0, v_read > 0, 0 <= dac_bend < 1, |adc_bend| <= 0.5.
+ *
+ * Output scale: with the quantising ADC, Y = fp32(acc) * fp32(LSB / (s_v s_w'))
+ * where acc = sum over row tiles and arrays of weight(a) * code, LSB = I_FS / L,
+ * s_v = v_read / x_max and s_w' = s_w (continuous) or dG L_w / w_max
+ * (quantised).  With the ideal ADC, Y = sum weight(a) I / (s_v s_w').
+ */
+typedef struct {
+  int32_t dac_bits;
+  double x_max, v_read, dac_bend;
+  int32_t adc_bits;
+  double adc_bend;
+} rxnn_periph_params;
+
+/* Convolution shape: input NCHW n x c_in x h x w, weight c_out x c_in x kh x kw,
+ * square stride and zero padding. */
+typedef struct {
+  int32_t n, c_in, h, w, c_out, kh, kw, stride, pad;
+} rxnn_conv_desc;
+
+/*
+ * Phase 1, model generation (Sec. V-A generator steps 1-3; G -> G' is the
+ * network of Sec. V-B solved exactly).
+ *   params  host pointer, copied.
+ *   W       device, fp32 P x Q row-major (P layer inputs, Q layer outputs),
+ *           read on `stream`, not retained.  For torch.nn.Linear pass
+ *           weight.t().contiguous(); for a conv pass weight.reshape(c_out,-1)
+ *           transposed.
+ *   out     receives the new handle; free it with rxnn_free_layer.
+ * G' is built in fp64 and stored as fp32.  Returns RXNN_EINVAL for a bad
+ * argument, RXNN_EUNSUPPORTED for sizes beyond this build, RXNN_ENOMEM.
+ */
+rxnn_status rxnn_map_layer(const rxnn_xbar_params* params, const float* W,
+                           int64_t P, int64_t Q, void* stream, rxnn_layer** out);
+
+/*
+ * Phase 1 again for new weights of the same shape: rebuilds every array's G'
+ * of `layer` in place from W (device fp32 P x Q, as for rxnn_map_layer), with
+ * the parameters the layer was mapped with (w_max recomputed from W when it
+ * was not fixed).  Allocates nothing; stream ordered.  Used where the model
+ * is regenerated every step (re-training with the crossbar in the loop).
+ */
+rxnn_status rxnn_remap_layer(rxnn_layer* layer, const float* W, void* stream);
+
+/*
+ * Phase 2 for a fully connected layer: DAC -> V . G' (Eq. 14) -> ADC ->
+ * accumulation over row tiles and arrays -> scale.
+ *   X  device fp32 B x P row-major; Y  device fp32 B x Q row-major.
+ *   B >= 0 (B = 0 is a no-op).
+ */
+rxnn_status rxnn_crossbar_vmm(const rxnn_layer* layer, const rxnn_periph_params* periph,
+                              const float* X, int64_t B, float* Y, void* stream);
+
+/*
+ * Phase 2 for a convolution evaluated as a matrix product over unrolled
+ * patches (Sec. VI): patch column k = (ci kh + ky) kw + kx, patch row
+ * bv = (n H_out + oy) W_out + ox, padded pixels are 0.  The layer must have
+ * been mapped with P = c_in kh kw and Q = c_out.
+ *   X  device fp32 NCHW input; Y  device fp32 NCHW output n x c_out x H_out x W_out.
+ */
+rxnn_status rxnn_conv_layer(const rxnn_layer* layer, const rxnn_periph_params* periph,
+                            const rxnn_conv_desc* conv, const float* X, float* Y,
+                            void* stream);
+
+/*
+ * Parity/debug exports.
+ * rxnn_get_gprime copies the M x N fp32 G' of array `array` at tile
+ *   (row_tile, col_tile) to host memory `host_out` (row-major, G'[i][j] = the
+ *   column-j current for 1 V on row i).  It synchronises the device.
+ * rxnn_set_gprime overwrites that array's G' from host memory (synchronous);
+ *   for tests that feed a known G' to the evaluation kernels.
+ * rxnn_vmm_debug runs rxnn_crossbar_vmm and also writes, for every row tile r,
+ *   column tile c and array a, the fp32 pre-ADC currents and the ADC codes:
+ *   I_preadc and codes are device buffers laid out [R][C][A][B][N] (either may
+ *   be NULL).  Codes are 0 with the ideal ADC.
+ * rxnn_layer_info returns P, Q, M, N, R, C, A (host pointer to 7 int64).
+ * rxnn_layer_wmax returns the w_max the layer was mapped with (synchronises).
+ */
+rxnn_status rxnn_get_gprime(const rxnn_layer* layer, int64_t row_tile, int64_t col_tile,
+                            int64_t array, float* host_out);
+rxnn_status rxnn_set_gprime(rxnn_layer* layer, int64_t row_tile, int64_t col_tile,
+                            int64_t array, const float* host_in);
+rxnn_status rxnn_vmm_debug(const rxnn_layer* layer, const rxnn_periph_params* periph,
+                           const float* X, int64_t B, float* Y, float* I_preadc,
+                           int32_t* codes, void* stream);
+rxnn_status rxnn_layer_info(const rxnn_layer* layer, int64_t* info7);
+rxnn_status rxnn_layer_wmax(const rxnn_layer* layer, double* w_max);
+
+/* Releases the handle and its device memory (synchronises its device).
+ * NULL and already released handles are ignored. */
+void rxnn_free_layer(rxnn_layer* layer);
+
+/*
+ * Kernel timing, for measurement: when enabled, the library brackets each
+ * kernel it launches with HIP events on the launch stream and accumulates
+ * the elapsed time per kernel name ("xbar_vmm", "gprime_build", "dac_im2col",
+ * "wmax", "finish").  rxnn_profile_read synchronises, folds pending events
+ * into the totals and returns total milliseconds and launch count.
+ */
+rxnn_status rxnn_profile_enable(int32_t on);
+rxnn_status rxnn_profile_reset(void);
+rxnn_status rxnn_profile_read(const char* kernel, double* total_ms, int64_t* count);
+
+const char* rxnn_status_string(rxnn_status status);
+const char* rxnn_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* RXNN_H */

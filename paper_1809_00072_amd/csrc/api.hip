@@ -1,0 +1,564 @@
+// C ABI of librxnn: argument validation, layer handles, workspaces, launches
+// and optional kernel timing.  The kernels live in gprime.hip (model
+// generation), vmm.hip (evaluation) and im2col.hip (patch unrolling + DAC).
+
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <map>
+#include <mutex>
+#include <set>
+#include <string>
+#include <vector>
+
+#include "common.h"
+
+using namespace rxnn;
+
+namespace {
+
+thread_local std::string g_err;
+std::mutex g_mu;
+std::set<const rxnn_layer*> g_live;
+
+rxnn_status fail(rxnn_status st, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+rxnn_status fail(rxnn_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return st;
+}
+
+#define HIP_TRY(expr)                                                                        \
+  do {                                                                                       \
+    hipError_t e_ = (expr);                                                                  \
+    if (e_ != hipSuccess)                                                                    \
+      return fail(RXNN_EHIP, "%s failed: %s", #expr, hipGetErrorString(e_));                 \
+  } while (0)
+
+bool finite_nonneg(double v) { return isfinite(v) && v >= 0.0; }
+
+int64_t round_up(int64_t v, int64_t m) { return (v + m - 1) / m * m; }
+
+bool live(const rxnn_layer* L) {
+  if (!L) return false;
+  std::lock_guard<std::mutex> g(g_mu);
+  return g_live.count(L) && L->magic == kLayerMagic;
+}
+
+// Makes the layer's device current for the scope of a call.
+struct DeviceGuard {
+  int prev = -1;
+  bool ok = true;
+  explicit DeviceGuard(int dev) {
+    if (hipGetDevice(&prev) != hipSuccess) { ok = false; return; }
+    if (prev != dev && hipSetDevice(dev) != hipSuccess) ok = false;
+  }
+  ~DeviceGuard() {
+    int cur;
+    if (prev >= 0 && hipGetDevice(&cur) == hipSuccess && cur != prev) (void)hipSetDevice(prev);
+  }
+};
+
+rxnn_status check_xbar(const rxnn_xbar_params* p) {
+  if (!p) return fail(RXNN_EINVAL, "params is NULL");
+  if (p->rows < 1 || p->cols < 1)
+    return fail(RXNN_EINVAL, "crossbar size %dx%d must be positive", p->rows, p->cols);
+  if (p->rows > 256 || p->cols > 256)
+    return fail(RXNN_EINVAL, "crossbar size %dx%d exceeds 256", p->rows, p->cols);
+  if (p->rows > kMaxXbar || p->cols > kMaxXbar)
+    return fail(RXNN_EUNSUPPORTED, "crossbar size %dx%d exceeds %d in this build", p->rows,
+                p->cols, kMaxXbar);
+  if (!(isfinite(p->g_min) && p->g_min > 0.0 && isfinite(p->g_max) && p->g_max > p->g_min))
+    return fail(RXNN_EINVAL, "need 0 < g_min < g_max (got %g, %g)", p->g_min, p->g_max);
+  if (!finite_nonneg(p->r_driver) || !finite_nonneg(p->r_sense) || !finite_nonneg(p->r_row) ||
+      !finite_nonneg(p->r_col))
+    return fail(RXNN_EINVAL, "resistances must be finite and >= 0");
+  if (p->weight_bits < 0 || p->weight_bits > 16)
+    return fail(RXNN_EINVAL, "weight_bits %d not in 0..16", p->weight_bits);
+  if (p->weight_bits == 0 && p->bits_per_slice != 0)
+    return fail(RXNN_EINVAL, "bits_per_slice needs weight_bits > 0");
+  if (p->bits_per_slice < 0 || p->bits_per_slice > p->weight_bits)
+    return fail(RXNN_EINVAL, "bits_per_slice %d not in 0..weight_bits", p->bits_per_slice);
+  if (p->bits_per_slice > 0 && p->weight_bits % p->bits_per_slice)
+    return fail(RXNN_EINVAL, "weight_bits %d is not a multiple of bits_per_slice %d",
+                p->weight_bits, p->bits_per_slice);
+  if (!isfinite(p->w_max)) return fail(RXNN_EINVAL, "w_max must be finite");
+  if (p->w_max > 3.0e38) return fail(RXNN_EINVAL, "w_max exceeds the fp32 range");
+  if (p->variation)
+    return fail(RXNN_EUNSUPPORTED, "per-device variation is not supported by this build");
+  return RXNN_OK;
+}
+
+rxnn_status make_periph(const rxnn_periph_params* pp, const MapScalars& ms, PeriphScalars* out) {
+  if (!pp) return fail(RXNN_EINVAL, "periph is NULL");
+  if (pp->dac_bits < 0 || pp->dac_bits > kMaxBits)
+    return fail(RXNN_EINVAL, "dac_bits %d not in 0..%d", pp->dac_bits, kMaxBits);
+  if (pp->adc_bits < 0 || pp->adc_bits > kMaxBits)
+    return fail(RXNN_EINVAL, "adc_bits %d not in 0..%d", pp->adc_bits, kMaxBits);
+  if (!(isfinite(pp->x_max) && pp->x_max > 0.0))
+    return fail(RXNN_EINVAL, "x_max must be finite and > 0");
+  if (!(isfinite(pp->v_read) && pp->v_read > 0.0))
+    return fail(RXNN_EINVAL, "v_read must be finite and > 0");
+  if (!(isfinite(pp->dac_bend) && pp->dac_bend >= 0.0 && pp->dac_bend < 1.0))
+    return fail(RXNN_EINVAL, "dac_bend must be in [0, 1)");
+  if (!(isfinite(pp->adc_bend) && fabs(pp->adc_bend) <= 0.5))
+    return fail(RXNN_EINVAL, "|adc_bend| must be <= 0.5");
+  PeriphScalars ps;
+  memset(&ps, 0, sizeof ps);
+  ps.dac_bits = pp->dac_bits;
+  ps.adc_bits = pp->adc_bits;
+  ps.dac_levels = (1 << pp->dac_bits) - 1;
+  ps.adc_levels = (1 << pp->adc_bits) - 1;
+  ps.v_read = pp->v_read;
+  ps.dac_bend = pp->dac_bend;
+  ps.adc_bend = pp->adc_bend;
+  ps.dac_s_in = pp->dac_bits ? (float)((double)ps.dac_levels / pp->x_max) : 0.0f;
+  ps.s_v_ideal = (float)(pp->v_read / pp->x_max);
+  ps.s_v = pp->v_read / pp->x_max;
+  ps.i_fs = pp->v_read * (double)ms.M * ms.g_max;
+  if (pp->adc_bits) {
+    ps.lsb = ps.i_fs / (double)ps.adc_levels;
+    // bucket width <= a quarter of the smallest threshold spacing
+    // (1 - |bend|) I_FS / L, so a bucket's code is within one of the exact one
+    const double need = 4.0 * ps.adc_levels / (1.0 - fabs(pp->adc_bend));
+    int nb = 16;
+    while (nb < need) nb <<= 1;
+    if (nb > kMaxBuckets) return fail(RXNN_EINVAL, "ADC bucket table too large");
+    ps.n_buckets = nb;
+    ps.bucket_inv_w = (float)((double)nb / ps.i_fs);
+    ps.bucket_w = ps.i_fs / (double)nb;
+  }
+  *out = ps;
+  return RXNN_OK;
+}
+
+// ---- kernel timing ------------------------------------------------------------
+struct Pending {
+  std::string name;
+  hipEvent_t a, b;
+};
+bool g_prof = false;
+std::vector<Pending> g_pending;
+std::map<std::string, std::pair<double, int64_t>> g_prof_tot;
+
+rxnn_status grow_ws(rxnn_layer* L, size_t bytes) {
+  if (L->ws_bytes >= bytes) return RXNN_OK;
+  if (L->ws) HIP_TRY(hipFree(L->ws));
+  L->ws = nullptr;
+  L->ws_bytes = 0;
+  void* p = nullptr;
+  if (hipMalloc(&p, bytes) != hipSuccess) {
+    (void)hipGetLastError();
+    return fail(RXNN_ENOMEM, "cannot allocate %zu bytes of workspace", bytes);
+  }
+  L->ws = p;
+  L->ws_bytes = bytes;
+  return RXNN_OK;
+}
+
+// Largest |acc| = R * L_adc * sum_s 2^(b_s s) must fit int32.
+rxnn_status check_acc_range(const MapScalars& ms, const PeriphScalars& ps) {
+  if (!ps.adc_bits) return RXNN_OK;
+  double w = 0.0;
+  for (int s = 0; s < ms.n_slices; ++s) w += ldexp(1.0, ms.slice_bits * s);
+  const double mx = (double)ms.R * ps.adc_levels * w;
+  if (mx >= 2147483647.0)
+    return fail(RXNN_EUNSUPPORTED, "accumulated codes can reach %.3g, beyond int32", mx);
+  return RXNN_OK;
+}
+
+rxnn_status run_vmm(const rxnn_layer* L, const PeriphScalars& ps, const void* X, bool codes,
+                    int64_t ldx, int64_t Bv, float* Y, int64_t hw_out, float* dbgI,
+                    int32_t* dbgC, hipStream_t s, int32_t* iacc_ws) {
+  const MapScalars& ms = L->ms;
+  const int splits = (dbgI || dbgC) ? 1 : choose_splits(ms, ps, Bv);
+  VmmLaunch vl;
+  vl.X = X;
+  vl.x_codes = codes;
+  vl.ldx = ldx;
+  vl.Bv = Bv;
+  vl.Y = Y;
+  vl.hw_out = hw_out;
+  vl.iacc = nullptr;
+  vl.dbg_I = dbgI;
+  vl.dbg_code = dbgC;
+  if (splits > 1) {
+    vl.iacc = iacc_ws;
+    ProfScope z("fill", s);
+    HIP_TRY(launch_fill_u32((unsigned*)iacc_ws, Bv * ms.Q, 0u, s));
+  }
+  {
+    ProfScope t("xbar_vmm", s);
+    HIP_TRY(launch_xbar_vmm(ms, ps, L->gpt, vl, splits, s));
+  }
+  if (splits > 1) {
+    ProfScope t("finish", s);
+    HIP_TRY(launch_finish(ms, ps, iacc_ws, Bv, Y, hw_out, s));
+  }
+  return RXNN_OK;
+}
+
+rxnn_status vmm_common(const rxnn_layer* layer, const rxnn_periph_params* periph,
+                       const float* X, int64_t B, float* Y, float* dbgI, int32_t* dbgC,
+                       void* stream) {
+  if (!live(layer)) return fail(RXNN_EINVAL, "invalid or released layer handle");
+  if (B < 0) return fail(RXNN_EINVAL, "B must be >= 0");
+  if (B > 0 && (!X || !Y)) return fail(RXNN_EINVAL, "X and Y must not be NULL");
+  rxnn_layer* L = const_cast<rxnn_layer*>(layer);
+  PeriphScalars ps;
+  rxnn_status st = make_periph(periph, L->ms, &ps);
+  if (st) return st;
+  if ((st = check_acc_range(L->ms, ps))) return st;
+  if (B == 0) return RXNN_OK;
+  DeviceGuard dg(L->device);
+  if (!dg.ok) return fail(RXNN_EHIP, "cannot select the layer's device");
+  hipStream_t s = (hipStream_t)stream;
+  int32_t* iacc = nullptr;
+  if (!(dbgI || dbgC) && choose_splits(L->ms, ps, B) > 1) {
+    if ((st = grow_ws(L, (size_t)B * L->ms.Q * sizeof(int32_t)))) return st;
+    iacc = (int32_t*)L->ws;
+  }
+  return run_vmm(L, ps, X, false, L->ms.P, B, Y, 0, dbgI, dbgC, s, iacc);
+}
+
+// w_max (fixed or reduced from W) followed by the G' build of every array.
+hipError_t build_gprime(rxnn_layer* L, const float* W, hipStream_t s) {
+  const MapScalars& ms = L->ms;
+  hipError_t e = hipSuccess;
+  {
+    ProfScope t("wmax", s);
+    if (ms.wmax_fixed > 0.0f) {
+      e = launch_fill_u32((unsigned*)L->d_wmax, 1, __builtin_bit_cast(unsigned, ms.wmax_fixed), s);
+    } else {
+      e = launch_fill_u32((unsigned*)L->d_wmax, 1, 0u, s);
+      if (e == hipSuccess) e = launch_absmax(W, ms.P * ms.Q, (unsigned*)L->d_wmax, s);
+    }
+  }
+  if (e == hipSuccess) {
+    ProfScope t("gprime_build", s);
+    e = launch_gprime_build(ms, W, L->gpt, s);
+  }
+  return e;
+}
+
+}  // namespace
+
+namespace rxnn {
+
+ProfScope::ProfScope(const char* name, hipStream_t s) : name_(name), s_(s), on_(false) {
+  if (!g_prof) return;
+  if (hipEventCreate(&a_) != hipSuccess) return;
+  if (hipEventCreate(&b_) != hipSuccess) { (void)hipEventDestroy(a_); return; }
+  if (hipEventRecord(a_, s_) != hipSuccess) {
+    (void)hipEventDestroy(a_);
+    (void)hipEventDestroy(b_);
+    return;
+  }
+  on_ = true;
+}
+
+ProfScope::~ProfScope() {
+  if (!on_) return;
+  if (hipEventRecord(b_, s_) != hipSuccess) {
+    (void)hipEventDestroy(a_);
+    (void)hipEventDestroy(b_);
+    return;
+  }
+  std::lock_guard<std::mutex> g(g_mu);
+  g_pending.push_back(Pending{name_, a_, b_});
+}
+
+}  // namespace rxnn
+
+extern "C" {
+
+const char* rxnn_status_string(rxnn_status st) {
+  switch (st) {
+    case RXNN_OK: return "ok";
+    case RXNN_EINVAL: return "invalid argument";
+    case RXNN_ENOMEM: return "out of device memory";
+    case RXNN_EHIP: return "HIP runtime error";
+    case RXNN_EUNSUPPORTED: return "unsupported by this build";
+  }
+  return "unknown status";
+}
+
+const char* rxnn_last_error(void) { return g_err.c_str(); }
+
+rxnn_status rxnn_map_layer(const rxnn_xbar_params* params, const float* W, int64_t P, int64_t Q,
+                           void* stream, rxnn_layer** out) {
+  if (!out) return fail(RXNN_EINVAL, "out is NULL");
+  *out = nullptr;
+  rxnn_status st = check_xbar(params);
+  if (st) return st;
+  if (P < 1 || Q < 1) return fail(RXNN_EINVAL, "P and Q must be >= 1");
+  if (P > (int64_t)1 << 31 || Q > (int64_t)1 << 31)
+    return fail(RXNN_EINVAL, "P and Q must be <= 2^31");
+  if (!W) return fail(RXNN_EINVAL, "W is NULL");
+  MapScalars ms;
+  memset(&ms, 0, sizeof ms);
+  ms.M = params->rows;
+  ms.N = params->cols;
+  ms.P = P;
+  ms.Q = Q;
+  ms.R = (int)((P + ms.M - 1) / ms.M);
+  ms.C = (int)((Q + ms.N - 1) / ms.N);
+  ms.weight_bits = params->weight_bits;
+  ms.slice_bits = params->weight_bits
+                      ? (params->bits_per_slice ? params->bits_per_slice : params->weight_bits)
+                      : 0;
+  ms.n_slices = params->weight_bits ? params->weight_bits / ms.slice_bits : 1;
+  if (ms.slice_bits * (ms.n_slices - 1) > 24)
+    return fail(RXNN_EUNSUPPORTED, "slice weights beyond 2^24 are not supported");
+  ms.A = 2 * ms.n_slices;
+  ms.Mp = (int)round_up(ms.M, 16);
+  ms.Np = (int)round_up(ms.N, 16);
+  ms.g_min = params->g_min;
+  ms.g_max = params->g_max;
+  ms.r_driver = params->r_driver;
+  ms.r_sense = params->r_sense;
+  ms.r_row = params->r_row;
+  ms.r_col = params->r_col;
+  if (ms.slice_bits == 0) {
+    ms.sw_num = ms.g_max - ms.g_min;
+  } else {
+    const double dG = (ms.g_max - ms.g_min) / (double)((1 << ms.slice_bits) - 1);
+    ms.sw_num = dG * (double)((1 << ms.weight_bits) - 1);
+  }
+  ms.wmax_fixed = params->w_max > 0.0 ? (float)params->w_max : 0.0f;
+  if (params->w_max > 0.0 && !(ms.wmax_fixed > 0.0f))
+    return fail(RXNN_EINVAL, "w_max underflows fp32");
+
+  int dev;
+  HIP_TRY(hipGetDevice(&dev));
+  const size_t gbytes = (size_t)ms.C * ms.R * ms.A * ms.Np * ms.Mp * sizeof(float);
+  rxnn_layer* L = new (std::nothrow) rxnn_layer();
+  if (!L) return fail(RXNN_ENOMEM, "host allocation failed");
+  memset(L, 0, sizeof *L);
+  L->device = dev;
+  L->params = *params;
+  if (hipMalloc((void**)&L->gpt, gbytes) != hipSuccess) {
+    (void)hipGetLastError();
+    delete L;
+    return fail(RXNN_ENOMEM, "cannot allocate %zu bytes for G'", gbytes);
+  }
+  if (hipMalloc((void**)&L->d_wmax, 256) != hipSuccess) {
+    (void)hipGetLastError();
+    (void)hipFree(L->gpt);
+    delete L;
+    return fail(RXNN_ENOMEM, "cannot allocate w_max");
+  }
+  ms.d_wmax = L->d_wmax;
+  L->ms = ms;
+  L->magic = kLayerMagic;
+  hipError_t e = build_gprime(L, W, (hipStream_t)stream);
+  if (e != hipSuccess) {
+    (void)hipFree(L->gpt);
+    (void)hipFree(L->d_wmax);
+    delete L;
+    return fail(RXNN_EHIP, "mapping launch failed: %s", hipGetErrorString(e));
+  }
+  {
+    std::lock_guard<std::mutex> g(g_mu);
+    g_live.insert(L);
+  }
+  *out = L;
+  return RXNN_OK;
+}
+
+rxnn_status rxnn_remap_layer(rxnn_layer* layer, const float* W, void* stream) {
+  if (!live(layer)) return fail(RXNN_EINVAL, "invalid or released layer handle");
+  if (!W) return fail(RXNN_EINVAL, "W is NULL");
+  DeviceGuard dg(layer->device);
+  if (!dg.ok) return fail(RXNN_EHIP, "cannot select the layer's device");
+  hipError_t e = build_gprime(layer, W, (hipStream_t)stream);
+  if (e != hipSuccess) return fail(RXNN_EHIP, "mapping launch failed: %s", hipGetErrorString(e));
+  return RXNN_OK;
+}
+
+rxnn_status rxnn_crossbar_vmm(const rxnn_layer* layer, const rxnn_periph_params* periph,
+                              const float* X, int64_t B, float* Y, void* stream) {
+  return vmm_common(layer, periph, X, B, Y, nullptr, nullptr, stream);
+}
+
+rxnn_status rxnn_vmm_debug(const rxnn_layer* layer, const rxnn_periph_params* periph,
+                           const float* X, int64_t B, float* Y, float* I_preadc, int32_t* codes,
+                           void* stream) {
+  return vmm_common(layer, periph, X, B, Y, I_preadc, codes, stream);
+}
+
+rxnn_status rxnn_conv_layer(const rxnn_layer* layer, const rxnn_periph_params* periph,
+                            const rxnn_conv_desc* conv, const float* X, float* Y,
+                            void* stream) {
+  if (!live(layer)) return fail(RXNN_EINVAL, "invalid or released layer handle");
+  if (!conv) return fail(RXNN_EINVAL, "conv is NULL");
+  const rxnn_conv_desc cd = *conv;
+  if (cd.n < 0 || cd.c_in < 1 || cd.h < 1 || cd.w < 1 || cd.c_out < 1 || cd.kh < 1 ||
+      cd.kw < 1 || cd.stride < 1 || cd.pad < 0)
+    return fail(RXNN_EINVAL, "invalid convolution shape");
+  if (cd.h + 2 * cd.pad < cd.kh || cd.w + 2 * cd.pad < cd.kw)
+    return fail(RXNN_EINVAL, "kernel larger than the padded input");
+  rxnn_layer* L = const_cast<rxnn_layer*>(layer);
+  const MapScalars& ms = L->ms;
+  if (ms.P != (int64_t)cd.c_in * cd.kh * cd.kw || ms.Q != cd.c_out)
+    return fail(RXNN_EINVAL, "layer is %lldx%lld but the convolution needs %lldx%d",
+                (long long)ms.P, (long long)ms.Q, (long long)cd.c_in * cd.kh * cd.kw, cd.c_out);
+  PeriphScalars ps;
+  rxnn_status st = make_periph(periph, ms, &ps);
+  if (st) return st;
+  if ((st = check_acc_range(ms, ps))) return st;
+  const int64_t ho = (cd.h + 2 * cd.pad - cd.kh) / cd.stride + 1;
+  const int64_t wo = (cd.w + 2 * cd.pad - cd.kw) / cd.stride + 1;
+  const int64_t Bv = (int64_t)cd.n * ho * wo;
+  if (Bv == 0) return RXNN_OK;
+  if (!X || !Y) return fail(RXNN_EINVAL, "X and Y must not be NULL");
+  DeviceGuard dg(L->device);
+  if (!dg.ok) return fail(RXNN_EHIP, "cannot select the layer's device");
+  hipStream_t s = (hipStream_t)stream;
+  const bool codes = ps.dac_bits > 0;
+  const int64_t ldk = round_up(ms.P, 16);
+  const int splits = choose_splits(ms, ps, Bv);
+  const size_t acc_bytes = splits > 1 ? (size_t)round_up(Bv * ms.Q * 4, 256) : 0;
+  const size_t col_bytes = (size_t)Bv * ldk * (codes ? 1 : 4);
+  if ((st = grow_ws(L, acc_bytes + col_bytes))) return st;
+  char* base = (char*)L->ws;
+  void* cols = base + acc_bytes;
+  {
+    ProfScope t("dac_im2col", s);
+    HIP_TRY(launch_dac_im2col(cd, ps, X, cols, codes, ldk, s));
+  }
+  return run_vmm(L, ps, cols, codes, ldk, Bv, Y, ho * wo, nullptr, nullptr, s,
+                 splits > 1 ? (int32_t*)base : nullptr);
+}
+
+rxnn_status rxnn_get_gprime(const rxnn_layer* layer, int64_t row_tile, int64_t col_tile,
+                            int64_t array, float* host_out) {
+  if (!live(layer)) return fail(RXNN_EINVAL, "invalid or released layer handle");
+  const MapScalars& ms = layer->ms;
+  if (row_tile < 0 || row_tile >= ms.R || col_tile < 0 || col_tile >= ms.C || array < 0 ||
+      array >= ms.A)
+    return fail(RXNN_EINVAL, "tile (%lld, %lld, %lld) out of range", (long long)row_tile,
+                (long long)col_tile, (long long)array);
+  if (!host_out) return fail(RXNN_EINVAL, "host_out is NULL");
+  DeviceGuard dg(layer->device);
+  if (!dg.ok) return fail(RXNN_EHIP, "cannot select the layer's device");
+  std::vector<float> t((size_t)ms.Np * ms.Mp);
+  const int64_t arr = (col_tile * ms.R + row_tile) * ms.A + array;
+  HIP_TRY(hipDeviceSynchronize());
+  HIP_TRY(hipMemcpy(t.data(), layer->gpt + arr * ms.Np * ms.Mp, t.size() * sizeof(float),
+                    hipMemcpyDeviceToHost));
+  for (int i = 0; i < ms.M; ++i)
+    for (int j = 0; j < ms.N; ++j) host_out[(size_t)i * ms.N + j] = t[(size_t)j * ms.Mp + i];
+  return RXNN_OK;
+}
+
+rxnn_status rxnn_set_gprime(rxnn_layer* layer, int64_t row_tile, int64_t col_tile, int64_t array,
+                            const float* host_in) {
+  if (!live(layer)) return fail(RXNN_EINVAL, "invalid or released layer handle");
+  const MapScalars& ms = layer->ms;
+  if (row_tile < 0 || row_tile >= ms.R || col_tile < 0 || col_tile >= ms.C || array < 0 ||
+      array >= ms.A)
+    return fail(RXNN_EINVAL, "tile (%lld, %lld, %lld) out of range", (long long)row_tile,
+                (long long)col_tile, (long long)array);
+  if (!host_in) return fail(RXNN_EINVAL, "host_in is NULL");
+  DeviceGuard dg(layer->device);
+  if (!dg.ok) return fail(RXNN_EHIP, "cannot select the layer's device");
+  std::vector<float> t((size_t)ms.Np * ms.Mp, 0.0f);
+  for (int i = 0; i < ms.M; ++i)
+    for (int j = 0; j < ms.N; ++j) t[(size_t)j * ms.Mp + i] = host_in[(size_t)i * ms.N + j];
+  const int64_t arr = (col_tile * ms.R + row_tile) * ms.A + array;
+  HIP_TRY(hipDeviceSynchronize());
+  HIP_TRY(hipMemcpy(layer->gpt + arr * ms.Np * ms.Mp, t.data(), t.size() * sizeof(float),
+                    hipMemcpyHostToDevice));
+  return RXNN_OK;
+}
+
+rxnn_status rxnn_layer_info(const rxnn_layer* layer, int64_t* info7) {
+  if (!live(layer)) return fail(RXNN_EINVAL, "invalid or released layer handle");
+  if (!info7) return fail(RXNN_EINVAL, "info is NULL");
+  const MapScalars& ms = layer->ms;
+  const int64_t v[7] = {ms.P, ms.Q, ms.M, ms.N, ms.R, ms.C, ms.A};
+  memcpy(info7, v, sizeof v);
+  return RXNN_OK;
+}
+
+rxnn_status rxnn_layer_wmax(const rxnn_layer* layer, double* w_max) {
+  if (!live(layer)) return fail(RXNN_EINVAL, "invalid or released layer handle");
+  if (!w_max) return fail(RXNN_EINVAL, "w_max is NULL");
+  DeviceGuard dg(layer->device);
+  if (!dg.ok) return fail(RXNN_EHIP, "cannot select the layer's device");
+  float v = 0.0f;
+  HIP_TRY(hipDeviceSynchronize());
+  HIP_TRY(hipMemcpy(&v, layer->d_wmax, sizeof v, hipMemcpyDeviceToHost));
+  *w_max = (double)v;
+  return RXNN_OK;
+}
+
+void rxnn_free_layer(rxnn_layer* layer) {
+  {
+    std::lock_guard<std::mutex> g(g_mu);
+    if (!layer || !g_live.count(layer)) return;
+    g_live.erase(layer);
+  }
+  DeviceGuard dg(layer->device);
+  (void)hipDeviceSynchronize();
+  (void)hipFree(layer->gpt);
+  (void)hipFree(layer->d_wmax);
+  if (layer->ws) (void)hipFree(layer->ws);
+  layer->magic = 0;
+  delete layer;
+}
+
+rxnn_status rxnn_profile_enable(int32_t on) {
+  std::lock_guard<std::mutex> g(g_mu);
+  g_prof = on != 0;
+  return RXNN_OK;
+}
+
+rxnn_status rxnn_profile_reset(void) {
+  std::vector<Pending> p;
+  {
+    std::lock_guard<std::mutex> g(g_mu);
+    p.swap(g_pending);
+    g_prof_tot.clear();
+  }
+  for (auto& e : p) {
+    (void)hipEventSynchronize(e.b);
+    (void)hipEventDestroy(e.a);
+    (void)hipEventDestroy(e.b);
+  }
+  return RXNN_OK;
+}
+
+rxnn_status rxnn_profile_read(const char* kernel, double* total_ms, int64_t* count) {
+  if (!kernel || !total_ms || !count) return fail(RXNN_EINVAL, "NULL argument");
+  std::vector<Pending> p;
+  {
+    std::lock_guard<std::mutex> g(g_mu);
+    p.swap(g_pending);
+  }
+  for (auto& e : p) {
+    float ms = 0.0f;
+    HIP_TRY(hipEventSynchronize(e.b));
+    HIP_TRY(hipEventElapsedTime(&ms, e.a, e.b));
+    (void)hipEventDestroy(e.a);
+    (void)hipEventDestroy(e.b);
+    std::lock_guard<std::mutex> g(g_mu);
+    auto& t = g_prof_tot[e.name];
+    t.first += ms;
+    t.second += 1;
+  }
+  std::lock_guard<std::mutex> g(g_mu);
+  auto it = g_prof_tot.find(kernel);
+  *total_ms = it == g_prof_tot.end() ? 0.0 : it->second.first;
+  *count = it == g_prof_tot.end() ? 0 : it->second.second;
+  return RXNN_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,97 @@
+// Internal declarations shared by the HIP sources of librxnn (not part of the ABI).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/rxnn.h"
+
+namespace rxnn {
+
+constexpr uint64_t kLayerMagic = 0x52784e4e4c617972ull;  // "RxNNLayr"
+constexpr int kMaxXbar = 64;        // largest crossbar side of this build
+constexpr int kMaxBits = 8;         // largest DAC / ADC resolution
+constexpr int kMaxBuckets = 2048;   // largest ADC bucket table (u8 entries)
+
+// Scalars of one mapping, shared by the build, the evaluation and the finish
+// kernels.  w_max is either fixed by the caller (wmax_fixed > 0) or reduced on
+// the device into *d_wmax before the build runs.
+struct MapScalars {
+  int M, N, R, C, A, Mp, Np;   // crossbar, tile grid, arrays per position, padded tile
+  int64_t P, Q;
+  double g_min, g_max, r_driver, r_sense, r_row, r_col;
+  int weight_bits, slice_bits, n_slices;
+  float wmax_fixed;
+  const float* d_wmax;
+  double sw_num;               // s_w' = sw_num / w_max (siemens per unit weight)
+};
+
+// Peripheral constants prepared on the host from rxnn_periph_params; the
+// per-code tables are rebuilt from them on the device.
+struct PeriphScalars {
+  int dac_bits, adc_bits;      // 0 = ideal
+  int dac_levels, adc_levels;  // 2^bits - 1
+  float dac_s_in;              // fp32(L / x_max)
+  float s_v_ideal;             // fp32(v_read / x_max)
+  double v_read, dac_bend, adc_bend;
+  double i_fs;                 // ADC full scale, v_read * M * g_max
+  double lsb;                  // i_fs / L
+  double s_v;                  // v_read / x_max
+  int n_buckets;               // ADC bucket table size
+  float bucket_inv_w;          // fp32(n_buckets / i_fs)
+  double bucket_w;             // i_fs / n_buckets
+};
+
+}  // namespace rxnn
+
+struct rxnn_layer {
+  uint64_t magic;
+  int device;
+  rxnn_xbar_params params;
+  rxnn::MapScalars ms;
+  float* gpt;          // G' of every array, [C][R][A][Np][Mp] fp32, transposed per array
+  float* d_wmax;       // one float
+  void* ws;            // scratch of the evaluation calls
+  size_t ws_bytes;
+};
+
+namespace rxnn {
+
+// ---- launchers (each returns the hipError_t of its launch) -----------------
+
+hipError_t launch_absmax(const float* W, int64_t n, unsigned* out, hipStream_t s);
+hipError_t launch_fill_u32(unsigned* p, int64_t n, unsigned v, hipStream_t s);
+hipError_t launch_gprime_build(const MapScalars& ms, const float* W, float* gpt,
+                               hipStream_t s);
+
+struct VmmLaunch {
+  const void* X;        // fp32 rows or u8 DAC codes
+  bool x_codes;         // X holds u8 codes already passed through the DAC
+  int64_t ldx;          // row stride of X in elements
+  int64_t Bv;           // rows of the product
+  float* Y;
+  int64_t hw_out;       // 0: Y is Bv x Q row-major; > 0: NCHW with H_out W_out = hw_out
+  int32_t* iacc;        // split accumulation workspace (Bv x Q int32) or null
+  float* dbg_I;         // [R][C][A][Bv][N] or null
+  int32_t* dbg_code;    // [R][C][A][Bv][N] or null
+};
+hipError_t launch_xbar_vmm(const MapScalars& ms, const PeriphScalars& ps, const float* gpt,
+                           const VmmLaunch& vl, int splits, hipStream_t s);
+hipError_t launch_finish(const MapScalars& ms, const PeriphScalars& ps, const int32_t* iacc,
+                         int64_t Bv, float* Y, int64_t hw_out, hipStream_t s);
+int choose_splits(const MapScalars& ms, const PeriphScalars& ps, int64_t Bv);
+
+hipError_t launch_dac_im2col(const rxnn_conv_desc& cd, const PeriphScalars& ps, const float* X,
+                             void* out, bool codes, int64_t ldk, hipStream_t s);
+
+// ---- kernel timing (api.hip) ------------------------------------------------
+struct ProfScope {
+  ProfScope(const char* name, hipStream_t s);
+  ~ProfScope();
+  const char* name_;
+  hipStream_t s_;
+  hipEvent_t a_, b_;
+  bool on_;
+};
+
+}  // namespace rxnn
