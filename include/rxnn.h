@@ -57,8 +57,8 @@ typedef struct rxnn_layer rxnn_layer;
 /*
  * Crossbar and device parameters (Sec. III, IV-A, V-A generator steps 1-2).
  *
- * rows, cols       crossbar size M x N, each 1..64 in this build (1..256 are
- *                  valid; sizes above 64 return RXNN_EUNSUPPORTED).
+ * rows, cols       crossbar size M x N, each 1..256.  Sizes above 64 need
+ *                  r_row, r_col and r_sense > 0 (else RXNN_EUNSUPPORTED).
  * g_min, g_max     conductance range of one device in siemens, 0 < g_min < g_max.
  * r_driver         Thevenin resistance of each row driver (ohm, >= 0).  It sits
  *                  in series with the first row-wire segment, so the

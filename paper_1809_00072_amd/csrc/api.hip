@@ -1,6 +1,6 @@
 // C ABI of librxnn: argument validation, layer handles, workspaces, launches
 // and optional kernel timing.  The kernels live in gprime.hip (model
-// generation), vmm.hip (evaluation) and im2col.hip (patch unrolling + DAC).
+// generation) and vmm.hip (evaluation, with the convolution's patch gather).
 
 #include <math.h>
 #include <stdarg.h>
@@ -65,15 +65,19 @@ struct DeviceGuard {
   }
 };
 
+// The nested-dissection build needs finite wire, driver and sense conductances.
+bool nd_ok(const rxnn_xbar_params* p) {
+  return p->r_row > 0.0 && p->r_col > 0.0 && p->r_sense > 0.0;
+}
+
+constexpr size_t kNdBudget = (size_t)1 << 30;  // bytes of build workspace per layer
+
 rxnn_status check_xbar(const rxnn_xbar_params* p) {
   if (!p) return fail(RXNN_EINVAL, "params is NULL");
   if (p->rows < 1 || p->cols < 1)
     return fail(RXNN_EINVAL, "crossbar size %dx%d must be positive", p->rows, p->cols);
   if (p->rows > 256 || p->cols > 256)
     return fail(RXNN_EINVAL, "crossbar size %dx%d exceeds 256", p->rows, p->cols);
-  if (p->rows > kMaxXbar || p->cols > kMaxXbar)
-    return fail(RXNN_EUNSUPPORTED, "crossbar size %dx%d exceeds %d in this build", p->rows,
-                p->cols, kMaxXbar);
   if (!(isfinite(p->g_min) && p->g_min > 0.0 && isfinite(p->g_max) && p->g_max > p->g_min))
     return fail(RXNN_EINVAL, "need 0 < g_min < g_max (got %g, %g)", p->g_min, p->g_max);
   if (!finite_nonneg(p->r_driver) || !finite_nonneg(p->r_sense) || !finite_nonneg(p->r_row) ||
@@ -92,6 +96,10 @@ rxnn_status check_xbar(const rxnn_xbar_params* p) {
   if (p->w_max > 3.0e38) return fail(RXNN_EINVAL, "w_max exceeds the fp32 range");
   if (p->variation)
     return fail(RXNN_EUNSUPPORTED, "per-device variation is not supported by this build");
+  if (!nd_ok(p) && (p->rows > kMaxSweep || p->cols > kMaxSweep))
+    return fail(RXNN_EUNSUPPORTED,
+                "crossbars above %dx%d need positive wire, driver and sense resistances",
+                kMaxSweep, kMaxSweep);
   return RXNN_OK;
 }
 
@@ -173,14 +181,15 @@ rxnn_status check_acc_range(const MapScalars& ms, const PeriphScalars& ps) {
   return RXNN_OK;
 }
 
-rxnn_status run_vmm(const rxnn_layer* L, const PeriphScalars& ps, const void* X, bool codes,
-                    int64_t ldx, int64_t Bv, float* Y, int64_t hw_out, float* dbgI,
-                    int32_t* dbgC, hipStream_t s, int32_t* iacc_ws) {
+rxnn_status run_vmm(const rxnn_layer* L, const PeriphScalars& ps, const float* X,
+                    const rxnn_conv_desc* conv, int64_t ldx, int64_t Bv, float* Y,
+                    int64_t hw_out, float* dbgI, int32_t* dbgC, hipStream_t s,
+                    int32_t* iacc_ws) {
   const MapScalars& ms = L->ms;
   const int splits = (dbgI || dbgC) ? 1 : choose_splits(ms, ps, Bv);
   VmmLaunch vl;
   vl.X = X;
-  vl.x_codes = codes;
+  vl.conv = conv;
   vl.ldx = ldx;
   vl.Bv = Bv;
   vl.Y = Y;
@@ -224,7 +233,7 @@ rxnn_status vmm_common(const rxnn_layer* layer, const rxnn_periph_params* periph
     if ((st = grow_ws(L, (size_t)B * L->ms.Q * sizeof(int32_t)))) return st;
     iacc = (int32_t*)L->ws;
   }
-  return run_vmm(L, ps, X, false, L->ms.P, B, Y, 0, dbgI, dbgC, s, iacc);
+  return run_vmm(L, ps, X, nullptr, L->ms.P, B, Y, 0, dbgI, dbgC, s, iacc);
 }
 
 // w_max (fixed or reduced from W) followed by the G' build of every array.
@@ -242,7 +251,12 @@ hipError_t build_gprime(rxnn_layer* L, const float* W, hipStream_t s) {
   }
   if (e == hipSuccess) {
     ProfScope t("gprime_build", s);
-    e = launch_gprime_build(ms, W, L->gpt, s);
+    if (!L->nd_ws) return launch_gprime_build(ms, W, L->gpt, s);
+    const int64_t n_arrays = (int64_t)ms.R * ms.C * ms.A;
+    for (int64_t a0 = 0; a0 < n_arrays && e == hipSuccess; a0 += L->nd_chunk) {
+      const int64_t n = n_arrays - a0 < L->nd_chunk ? n_arrays - a0 : L->nd_chunk;
+      e = launch_nd_build(ms, W, L->gpt, a0, n, L->nd_ws, s);
+    }
   }
   return e;
 }
@@ -354,6 +368,23 @@ rxnn_status rxnn_map_layer(const rxnn_xbar_params* params, const float* W, int64
     delete L;
     return fail(RXNN_ENOMEM, "cannot allocate w_max");
   }
+  if (nd_ok(params)) {
+    int64_t si, so, sc;
+    nd_sizes(nd_side(ms.M, ms.N), ms.M, &si, &so, &sc);
+    const size_t per = (size_t)(si + so + sc) * sizeof(double);
+    const int64_t n_arrays = (int64_t)ms.R * ms.C * ms.A;
+    int64_t chunk = (int64_t)(kNdBudget / per);
+    if (chunk < 1) chunk = 1;
+    if (chunk > n_arrays) chunk = n_arrays;
+    if (hipMalloc((void**)&L->nd_ws, per * chunk) != hipSuccess) {
+      (void)hipGetLastError();
+      (void)hipFree(L->gpt);
+      (void)hipFree(L->d_wmax);
+      delete L;
+      return fail(RXNN_ENOMEM, "cannot allocate %zu bytes of build workspace", per * chunk);
+    }
+    L->nd_chunk = chunk;
+  }
   ms.d_wmax = L->d_wmax;
   L->ms = ms;
   L->magic = kLayerMagic;
@@ -361,6 +392,7 @@ rxnn_status rxnn_map_layer(const rxnn_xbar_params* params, const float* W, int64
   if (e != hipSuccess) {
     (void)hipFree(L->gpt);
     (void)hipFree(L->d_wmax);
+    if (L->nd_ws) (void)hipFree(L->nd_ws);
     delete L;
     return fail(RXNN_EHIP, "mapping launch failed: %s", hipGetErrorString(e));
   }
@@ -421,20 +453,12 @@ rxnn_status rxnn_conv_layer(const rxnn_layer* layer, const rxnn_periph_params* p
   DeviceGuard dg(L->device);
   if (!dg.ok) return fail(RXNN_EHIP, "cannot select the layer's device");
   hipStream_t s = (hipStream_t)stream;
-  const bool codes = ps.dac_bits > 0;
-  const int64_t ldk = round_up(ms.P, 16);
-  const int splits = choose_splits(ms, ps, Bv);
-  const size_t acc_bytes = splits > 1 ? (size_t)round_up(Bv * ms.Q * 4, 256) : 0;
-  const size_t col_bytes = (size_t)Bv * ldk * (codes ? 1 : 4);
-  if ((st = grow_ws(L, acc_bytes + col_bytes))) return st;
-  char* base = (char*)L->ws;
-  void* cols = base + acc_bytes;
-  {
-    ProfScope t("dac_im2col", s);
-    HIP_TRY(launch_dac_im2col(cd, ps, X, cols, codes, ldk, s));
+  int32_t* iacc = nullptr;
+  if (choose_splits(ms, ps, Bv) > 1) {
+    if ((st = grow_ws(L, (size_t)Bv * ms.Q * sizeof(int32_t)))) return st;
+    iacc = (int32_t*)L->ws;
   }
-  return run_vmm(L, ps, cols, codes, ldk, Bv, Y, ho * wo, nullptr, nullptr, s,
-                 splits > 1 ? (int32_t*)base : nullptr);
+  return run_vmm(L, ps, X, &cd, 0, Bv, Y, ho * wo, nullptr, nullptr, s, iacc);
 }
 
 rxnn_status rxnn_get_gprime(const rxnn_layer* layer, int64_t row_tile, int64_t col_tile,
@@ -511,6 +535,7 @@ void rxnn_free_layer(rxnn_layer* layer) {
   (void)hipFree(layer->gpt);
   (void)hipFree(layer->d_wmax);
   if (layer->ws) (void)hipFree(layer->ws);
+  if (layer->nd_ws) (void)hipFree(layer->nd_ws);
   layer->magic = 0;
   delete layer;
 }

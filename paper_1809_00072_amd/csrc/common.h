@@ -9,7 +9,8 @@
 namespace rxnn {
 
 constexpr uint64_t kLayerMagic = 0x52784e4e4c617972ull;  // "RxNNLayr"
-constexpr int kMaxXbar = 64;        // largest crossbar side of this build
+constexpr int kMaxXbar = 256;       // largest crossbar side
+constexpr int kMaxSweep = 64;       // largest side of the row-sweep build (zero resistances)
 constexpr int kMaxBits = 8;         // largest DAC / ADC resolution
 constexpr int kMaxBuckets = 2048;   // largest ADC bucket table (u8 entries)
 
@@ -53,6 +54,8 @@ struct rxnn_layer {
   float* d_wmax;       // one float
   void* ws;            // scratch of the evaluation calls
   size_t ws_bytes;
+  double* nd_ws;       // nested-dissection build workspace (null: row sweep)
+  int64_t nd_chunk;    // arrays built per pass over the workspace
 };
 
 namespace rxnn {
@@ -63,11 +66,15 @@ hipError_t launch_absmax(const float* W, int64_t n, unsigned* out, hipStream_t s
 hipError_t launch_fill_u32(unsigned* p, int64_t n, unsigned v, hipStream_t s);
 hipError_t launch_gprime_build(const MapScalars& ms, const float* W, float* gpt,
                                hipStream_t s);
+int nd_side(int M, int N);
+void nd_sizes(int T, int M, int64_t* in_stride, int64_t* out_stride, int64_t* scr_stride);
+hipError_t launch_nd_build(const MapScalars& ms, const float* W, float* gpt, int64_t arr0,
+                           int64_t n, double* ws, hipStream_t s);
 
 struct VmmLaunch {
-  const void* X;        // fp32 rows or u8 DAC codes
-  bool x_codes;         // X holds u8 codes already passed through the DAC
-  int64_t ldx;          // row stride of X in elements
+  const float* X;       // FC: Bv x ldx rows; conv: the NCHW input
+  const rxnn_conv_desc* conv;  // null for FC
+  int64_t ldx;          // row stride of X in elements (FC)
   int64_t Bv;           // rows of the product
   float* Y;
   int64_t hw_out;       // 0: Y is Bv x Q row-major; > 0: NCHW with H_out W_out = hw_out
@@ -80,9 +87,6 @@ hipError_t launch_xbar_vmm(const MapScalars& ms, const PeriphScalars& ps, const 
 hipError_t launch_finish(const MapScalars& ms, const PeriphScalars& ps, const int32_t* iacc,
                          int64_t Bv, float* Y, int64_t hw_out, hipStream_t s);
 int choose_splits(const MapScalars& ms, const PeriphScalars& ps, int64_t Bv);
-
-hipError_t launch_dac_im2col(const rxnn_conv_desc& cd, const PeriphScalars& ps, const float* X,
-                             void* out, bool codes, int64_t ldk, hipStream_t s);
 
 // ---- kernel timing (api.hip) ------------------------------------------------
 struct ProfScope {

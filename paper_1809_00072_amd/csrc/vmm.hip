@@ -5,16 +5,21 @@
 // One workgroup (4 waves) owns BM = 128 product rows and BN output columns of
 // one column tile, and walks every row tile r of that column tile (or a
 // contiguous share of them when the row tiles are split across workgroups).
-// For each row tile and each differential pair of arrays (+, -) of a slice:
-//   * the DAC output V (BM x 64 chunk of the tile's M inputs) is staged in LDS:
-//     inputs are read once per row tile, quantised to a code, and replaced by
-//     the DAC table entry (the table lives in LDS);
+// The work is a sequence of stages (r, pair of arrays, 64-input chunk):
+//   * the DAC output V (BM x 64) of the chunk is staged in LDS: inputs are
+//     quantised to a code and replaced by the DAC table entry (the table lives
+//     in LDS).  For a convolution the inputs are gathered straight from the
+//     NCHW tensor (patch column k = (ci kh + ky) kw + kx, patch row
+//     bv = (n H_out + oy) W_out + ox, zero outside the image): the patch
+//     matrix is never written to memory;
 //   * both arrays' G'^T chunks (BN x 64) are staged in LDS;
+//   * the global loads of stage s + 1 are issued into registers before the
+//     MFMA loop of stage s, so they are in flight while it runs;
 //   * v_mfma_f32_16x16x4f32 accumulates I for both arrays in fp32, the two
 //     arrays sharing every V operand read;
 //   * once the tile's M inputs are consumed, every current goes through the
-//     ADC (a bucket table gives a code within one of the exact one, two
-//     comparisons against the threshold table finish it) and is added to an
+//     ADC (a bucket table gives a code that is exact or one too low, one
+//     comparison with the threshold table finishes it) and is added to an
 //     int32 accumulator with the array's digital weight (+-2^(b_s s)).
 // Integer accumulation makes the result independent of the order of row
 // tiles and arrays, so splitting the row tiles over workgroups and combining
@@ -33,14 +38,20 @@ constexpr int BM = 128;       // product rows per workgroup
 constexpr int KC = 64;        // inputs (k) staged per chunk
 constexpr int LDK = KC + 4;   // LDS row stride in floats
 constexpr int NTHR = 256;
+constexpr int XPT = BM * KC / NTHR;  // V elements staged per thread
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+struct ConvGeom {
+  int c_in, h, w, kh, kw, stride, pad, ho, wo;
+};
 
 struct VmmArgs {
   MapScalars ms;
   PeriphScalars ps;
+  ConvGeom cg;
   const float* gpt;
-  const void* X;
+  const float* X;
   int64_t ldx, Bv;
   float* Y;
   int64_t hw_out;
@@ -52,20 +63,21 @@ struct VmmArgs {
 
 __device__ __forceinline__ double bend(double u, double b) { return u - (b * u) * (1.0 - u); }
 
+// bucket[b] = #{k : t_k <= (b - 1) w}: with w at most a quarter of the
+// smallest threshold spacing, the exact code is bucket[b] or bucket[b] + 1.
 __device__ __forceinline__ int adc_code(float I, const float* thr, const unsigned char* bucket,
                                         float inv_w, int nb) {
-  float t = I * inv_w;
-  int b = (int)fminf(fmaxf(t, 0.0f), (float)(nb - 1));
-  int c = bucket[b];
-  int up = I >= thr[c + 1];
-  int dn = I < thr[c];
-  return c + up - dn;
+  const float t = I * inv_w;
+  const int b = (int)fminf(fmaxf(t, 0.0f), (float)(nb - 1));
+  const int c = bucket[b];
+  return c + (I >= thr[c + 1] ? 1 : 0);
 }
 
-template <int BN, bool CODES, bool QADC, bool DEBUG>
+template <int BN, bool CONV, bool QADC, bool DEBUG>
 __global__ __launch_bounds__(NTHR, 2) void k_xbar_vmm(VmmArgs va) {
   constexpr int NT = BN / 16;   // column fragments per wave
   constexpr int MT = 2;         // row fragments per wave (32 rows)
+  constexpr int GV4 = BN / 8;   // float4 of G' staged per thread
   __shared__ __attribute__((aligned(16))) float Vs[BM * LDK];
   __shared__ __attribute__((aligned(16))) float Gs[2 * BN * LDK];
   __shared__ float lut[256];
@@ -100,7 +112,7 @@ __global__ __launch_bounds__(NTHR, 2) void k_xbar_vmm(VmmArgs va) {
     }
     __syncthreads();
     for (int b = tid; b < ps.n_buckets; b += NTHR) {
-      const double edge = (double)b * ps.bucket_w;
+      const double edge = (double)(b - 1) * ps.bucket_w;
       int lo = 0, hi = L;  // count of k in 1..L with thr[k] <= edge
       while (lo < hi) {
         const int mid = (lo + hi + 1) >> 1;
@@ -109,6 +121,140 @@ __global__ __launch_bounds__(NTHR, 2) void k_xbar_vmm(VmmArgs va) {
       bucket[b] = (unsigned char)lo;
     }
   }
+
+  // ---- per-thread staging geometry ----------------------------------------
+  // Staging loads are raw buffer loads: an SGPR descriptor, a 32-bit VGPR
+  // offset and (FC) an SGPR offset per row step, so no 64-bit address is kept
+  // per element.  Lanes whose element lies outside the input issue no load.
+  // FC: lanes run along k (coalesced rows of X).  Conv: lanes run along the
+  // product rows (consecutive output pixels), every wave shares one k.
+  const int kk_fc = tid & 63, row_fc = tid >> 6;
+  const int row_cv = tid & (BM - 1);
+  const int kk_cv = __builtin_amdgcn_readfirstlane(tid >> 7);
+  int xrow_off = 0;          // conv: element offset of (img, iy0, ix0) from the WG base
+  unsigned yok = 0, xok = 0;  // conv: bit ky (kx) set when the tap is inside the image
+  __amdgpu_buffer_rsrc_t xsrc;
+  int n_rows = (int)min((int64_t)BM, va.Bv - b0);
+  if (CONV) {
+    const int hw = va.cg.ho * va.cg.wo;
+    const int64_t chw = (int64_t)va.cg.c_in * va.cg.h * va.cg.w;
+    const int64_t img_first = b0 / hw;
+    const int64_t img_last = (b0 + n_rows - 1) / hw;
+    xsrc = __builtin_amdgcn_make_buffer_rsrc((void*)(va.X + img_first * chw), (short)0,
+                                             (int)((img_last - img_first + 1) * chw * 4),
+                                             0x00020000);
+    if (row_cv < n_rows) {
+      const int64_t bv = b0 + row_cv;
+      const int64_t img = bv / hw;
+      const int pix = (int)(bv - img * hw);
+      const int oy = pix / va.cg.wo, ox = pix - oy * va.cg.wo;
+      const int iy0 = oy * va.cg.stride - va.cg.pad;
+      const int ix0 = ox * va.cg.stride - va.cg.pad;
+      xrow_off = (int)((img - img_first) * chw) + iy0 * va.cg.w + ix0;
+      for (int t = 0; t < va.cg.kh; ++t)
+        if (iy0 + t >= 0 && iy0 + t < va.cg.h) yok |= 1u << t;
+      for (int t = 0; t < va.cg.kw; ++t)
+        if (ix0 + t >= 0 && ix0 + t < va.cg.w) xok |= 1u << t;
+    }
+  } else {
+    xsrc = __builtin_amdgcn_make_buffer_rsrc((void*)(va.X + b0 * va.ldx), (short)0,
+                                             (int)((int64_t)n_rows * va.ldx * 4), 0x00020000);
+  }
+
+  const int n_pairs = ms.A / 2;
+  const int nkc = (ms.Mp + KC - 1) / KC;
+  const int per_r = n_pairs * nkc;
+  const int n_stages = (r_end - r_begin) * per_r;
+  const int tile_elems = ms.Np * ms.Mp;
+
+  float xr[XPT];
+  f32x4 gr[GV4];
+
+  auto load_stage = [&](int s) {
+    const int r = r_begin + s / per_r;
+    const int rem = s % per_r;
+    const int ap = rem / nkc, kc0 = (rem % nkc) * KC;
+    if (ap == 0 || nkc > 1) {
+      if (CONV) {
+        const int khw = va.cg.kh * va.cg.kw;
+        const int hw_in = va.cg.h * va.cg.w;
+#pragma unroll
+        for (int it = 0; it < XPT; ++it) {
+          const int km = kc0 + kk_cv + 2 * it;
+          const int p = r * ms.M + km;
+          float x = 0.0f;
+          if (km < ms.M && p < ms.P) {
+            const int ci = p / khw, rr = p - ci * khw;
+            const int ky = rr / va.cg.kw, kx = rr - ky * va.cg.kw;
+            if ((yok >> ky) & (xok >> kx) & 1u) {
+              const int off = xrow_off + ci * hw_in + ky * va.cg.w + kx;
+              x = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(xsrc, off * 4, 0, 0));
+            }
+          }
+          xr[it] = x;
+        }
+      } else {
+        const int km = kc0 + kk_fc;
+        const int64_t p = (int64_t)r * ms.M + km;
+        const bool kok = km < ms.M && p < ms.P;
+        const int voff = (int)((row_fc * va.ldx + p) * 4);
+#pragma unroll
+        for (int it = 0; it < XPT; ++it) {
+          float x = 0.0f;
+          if (kok && row_fc + 4 * it < n_rows)
+            x = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
+                                              xsrc, voff, (int)(4 * it * va.ldx * 4), 0));
+          xr[it] = x;
+        }
+      }
+    }
+    const int64_t arr0 = ((int64_t)c * ms.R + r) * ms.A + 2 * ap;
+    __amdgpu_buffer_rsrc_t gsrc = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)(va.gpt + arr0 * tile_elems), (short)0, 2 * tile_elems * 4, 0x00020000);
+#pragma unroll
+    for (int it = 0; it < GV4; ++it) {
+      const int e4 = tid + NTHR * it;
+      const int p = e4 / (BN * (KC / 4));
+      const int rm = e4 % (BN * (KC / 4));
+      const int n = rm / (KC / 4), k4 = rm % (KC / 4);
+      const int kidx = kc0 + 4 * k4;
+      f32x4 v = f32x4{0.f, 0.f, 0.f, 0.f};
+      if (kidx < ms.Mp) {
+        const int off = (p * tile_elems + (n0 + n) * ms.Mp + 4 * k4) * 4;
+        v = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(gsrc, off, kc0 * 4, 0));
+      }
+      gr[it] = v;
+    }
+  };
+
+  auto dac = [&](float x) -> float {
+    if (ps.dac_bits > 0) {
+      const float t = rintf(x * ps.dac_s_in);
+      const int code = (int)fminf(fmaxf(t, 0.0f), (float)ps.dac_levels);
+      return lut[code];
+    }
+    return fmaxf(x, 0.0f) * ps.s_v_ideal;
+  };
+
+  auto store_stage = [&](int s) {
+    const int rem = s % per_r;
+    const int ap = rem / nkc;
+    if (ap == 0 || nkc > 1) {
+#pragma unroll
+      for (int it = 0; it < XPT; ++it) {
+        if (CONV) Vs[row_cv * LDK + kk_cv + 2 * it] = dac(xr[it]);
+        else Vs[(row_fc + 4 * it) * LDK + kk_fc] = dac(xr[it]);
+      }
+    }
+#pragma unroll
+    for (int it = 0; it < GV4; ++it) {
+      const int e4 = tid + NTHR * it;
+      const int p = e4 / (BN * (KC / 4));
+      const int rm = e4 % (BN * (KC / 4));
+      const int n = rm / (KC / 4), k4 = rm % (KC / 4);
+      *(f32x4*)&Gs[(p * BN + n) * LDK + 4 * k4] = gr[it];
+    }
+  };
 
   // ---- accumulators -----------------------------------------------------
   int32_t iacc[MT][NT][4];
@@ -119,116 +265,78 @@ __global__ __launch_bounds__(NTHR, 2) void k_xbar_vmm(VmmArgs va) {
     for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
       for (int v = 0; v < 4; ++v) { iacc[mt][nt][v] = 0; facc[mt][nt][v] = 0.0f; }
+  f32x4 acc[2][MT][NT];
 
-  const int n_pairs = ms.A / 2;
-  const int64_t tile_elems = (int64_t)ms.Np * ms.Mp;
-  const float* Xf = (const float*)va.X;
-  const unsigned char* Xc = (const unsigned char*)va.X;
-
-  for (int r = r_begin; r < r_end; ++r) {
-    for (int ap = 0; ap < n_pairs; ++ap) {
-      f32x4 acc[2][MT][NT];
+  if (n_stages > 0) load_stage(0);
+  for (int s = 0; s < n_stages; ++s) {
+    const int r = r_begin + s / per_r;
+    const int rem = s % per_r;
+    const int ap = rem / nkc, kci = rem % nkc, kc0 = kci * KC;
+    __syncthreads();
+    store_stage(s);
+    __syncthreads();
+    if (s + 1 < n_stages) load_stage(s + 1);
+    if (kci == 0) {
 #pragma unroll
       for (int p = 0; p < 2; ++p)
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
           for (int nt = 0; nt < NT; ++nt) acc[p][mt][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-      for (int kc0 = 0; kc0 < ms.Mp; kc0 += KC) {
-        const bool stage_v = (ap == 0) || (ms.Mp > KC);
-        __syncthreads();
-        if (stage_v) {
-          // V = DAC(x) for rows b0.., inputs r*M + kc0 + kk of this row tile
-          for (int e = tid; e < BM * KC; e += NTHR) {
-            const int row = e / KC, kk = e % KC;
-            const int64_t bv = b0 + row;
-            const int km = kc0 + kk;
-            const int64_t p = (int64_t)r * ms.M + km;
-            float v = 0.0f;
-            if (bv < va.Bv && km < ms.M && p < ms.P) {
-              if (CODES) {
-                v = lut[Xc[bv * va.ldx + p]];
-              } else {
-                const float x = Xf[bv * va.ldx + p];
-                if (ps.dac_bits > 0) {
-                  const float t = rintf(x * ps.dac_s_in);
-                  const int code = (int)fminf(fmaxf(t, 0.0f), (float)ps.dac_levels);
-                  v = lut[code];
-                } else {
-                  v = fmaxf(x, 0.0f) * ps.s_v_ideal;
-                }
-              }
-            }
-            Vs[row * LDK + kk] = v;
-          }
-        }
-        // G'^T chunks of arrays 2 ap and 2 ap + 1
-        for (int e = tid; e < 2 * BN * KC; e += NTHR) {
-          const int p = e / (BN * KC);
-          const int rem = e % (BN * KC);
-          const int n = rem / KC, kk = rem % KC;
-          const int64_t arr = ((int64_t)c * ms.R + r) * ms.A + 2 * ap + p;
-          float gv = 0.0f;
-          if (kc0 + kk < ms.Mp) gv = va.gpt[arr * tile_elems + (int64_t)(n0 + n) * ms.Mp + kc0 + kk];
-          Gs[(p * BN + n) * LDK + kk] = gv;
-        }
-        __syncthreads();
-
-        const int kb_end = min(KC, ms.Mp - kc0);
-        for (int kb = 0; kb < kb_end; kb += 16) {
-          f32x4 af[MT], bf[2][NT];
+    }
+    const int kb_end = min(KC, ms.Mp - kc0);
+    for (int kb = 0; kb < kb_end; kb += 16) {
+      f32x4 af[MT];
 #pragma unroll
-          for (int mt = 0; mt < MT; ++mt)
-            af[mt] = *(const f32x4*)&Vs[(wave * 32 + mt * 16 + li) * LDK + kb + 4 * g];
-#pragma unroll
-          for (int p = 0; p < 2; ++p)
-#pragma unroll
-            for (int nt = 0; nt < NT; ++nt)
-              bf[p][nt] = *(const f32x4*)&Gs[(p * BN + nt * 16 + li) * LDK + kb + 4 * g];
-#pragma unroll
-          for (int s = 0; s < 4; ++s)
-#pragma unroll
-            for (int p = 0; p < 2; ++p)
-#pragma unroll
-              for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-                for (int nt = 0; nt < NT; ++nt)
-                  acc[p][mt][nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(
-                      af[mt][s], bf[p][nt][s], acc[p][mt][nt], 0, 0, 0);
-        }
-      }
-
-      // ---- ADC and digital accumulation -----------------------------------
-      const int wpos = 1 << (ms.slice_bits * ap);
+      for (int mt = 0; mt < MT; ++mt)
+        af[mt] = *(const f32x4*)&Vs[(wave * 32 + mt * 16 + li) * LDK + kb + 4 * g];
 #pragma unroll
       for (int p = 0; p < 2; ++p) {
-        const int wgt = p ? -wpos : wpos;
+        f32x4 bf[NT];
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt)
+        for (int nt = 0; nt < NT; ++nt)
+          bf[nt] = *(const f32x4*)&Gs[(p * BN + nt * 16 + li) * LDK + kb + 4 * g];
 #pragma unroll
-          for (int nt = 0; nt < NT; ++nt)
+        for (int ss = 0; ss < 4; ++ss)
 #pragma unroll
-            for (int v = 0; v < 4; ++v) {
-              const float I = acc[p][mt][nt][v];
-              int code = 0;
-              if (QADC) {
-                code = adc_code(I, thr, bucket, ps.bucket_inv_w, ps.n_buckets);
-                iacc[mt][nt][v] += wgt * code;
-              } else {
-                facc[mt][nt][v] += (float)wgt * I;
-              }
-              if (DEBUG) {
-                const int64_t bv = b0 + wave * 32 + mt * 16 + 4 * g + v;
-                const int n = n0 + nt * 16 + li;
-                if (bv < va.Bv && n < ms.N) {
-                  const int64_t slot = (((int64_t)r * ms.C + c) * ms.A + 2 * ap + p) * va.Bv + bv;
-                  if (va.dbg_I) va.dbg_I[slot * ms.N + n] = I;
-                  if (va.dbg_code) va.dbg_code[slot * ms.N + n] = code;
-                }
+          for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+            for (int nt = 0; nt < NT; ++nt)
+              acc[p][mt][nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(
+                  af[mt][ss], bf[nt][ss], acc[p][mt][nt], 0, 0, 0);
+      }
+    }
+    if (kci != nkc - 1) continue;
+
+    // ---- ADC and digital accumulation -------------------------------------
+    const int wpos = 1 << (ms.slice_bits * ap);
+#pragma unroll
+    for (int p = 0; p < 2; ++p) {
+      const int wgt = p ? -wpos : wpos;
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+          for (int v = 0; v < 4; ++v) {
+            const float I = acc[p][mt][nt][v];
+            int code = 0;
+            if (QADC) {
+              code = adc_code(I, thr, bucket, ps.bucket_inv_w, ps.n_buckets);
+              iacc[mt][nt][v] += wgt * code;
+            } else {
+              facc[mt][nt][v] += (float)wgt * I;
+            }
+            if (DEBUG) {
+              const int64_t bv = b0 + wave * 32 + mt * 16 + 4 * g + v;
+              const int n = n0 + nt * 16 + li;
+              if (bv < va.Bv && n < ms.N) {
+                const int64_t slot = (((int64_t)r * ms.C + c) * ms.A + 2 * ap + p) * va.Bv + bv;
+                if (va.dbg_I) va.dbg_I[slot * ms.N + n] = I;
+                if (va.dbg_code) va.dbg_code[slot * ms.N + n] = code;
               }
             }
-      }
+          }
     }
   }
 
@@ -255,7 +363,7 @@ __global__ __launch_bounds__(NTHR, 2) void k_xbar_vmm(VmmArgs va) {
         }
         const float y = QADC ? (float)iacc[mt][nt][v] * scale : facc[mt][nt][v] * scale;
         if (va.hw_out > 0) {
-          const int64_t img = bv / va.hw_out, pix = bv % va.hw_out;
+          const int64_t img = bv / va.hw_out, pix = bv - img * va.hw_out;
           va.Y[(img * ms.Q + q) * va.hw_out + pix] = y;
         } else {
           va.Y[bv * ms.Q + q] = y;
@@ -263,38 +371,40 @@ __global__ __launch_bounds__(NTHR, 2) void k_xbar_vmm(VmmArgs va) {
       }
 }
 
+template <typename IDX>
 __global__ void k_finish(MapScalars ms, PeriphScalars ps, const int32_t* __restrict__ iacc,
-                         int64_t Bv, float* __restrict__ Y, int64_t hw_out) {
+                         IDX Bv, float* __restrict__ Y, IDX hw_out) {
   const double wmax = ms.wmax_fixed > 0.0f ? (double)ms.wmax_fixed : (double)*ms.d_wmax;
   float scale = 0.0f;
   if (wmax > 0.0) scale = (float)(ps.lsb / (ps.s_v * (ms.sw_num / wmax)));
-  const int64_t total = Bv * ms.Q;
-  for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < total;
-       e += (int64_t)gridDim.x * blockDim.x) {
-    const int64_t bv = e / ms.Q, q = e % ms.Q;
+  const IDX Q = (IDX)ms.Q;
+  const IDX total = Bv * Q;
+  for (IDX e = (IDX)blockIdx.x * blockDim.x + threadIdx.x; e < total;
+       e += (IDX)gridDim.x * blockDim.x) {
+    const IDX bv = e / Q, q = e - bv * Q;
     const float y = (float)iacc[e] * scale;
     if (hw_out > 0) {
-      const int64_t img = bv / hw_out, pix = bv % hw_out;
-      Y[(img * ms.Q + q) * hw_out + pix] = y;
+      const IDX img = bv / hw_out, pix = bv - img * hw_out;
+      Y[(img * Q + q) * hw_out + pix] = y;
     } else {
       Y[e] = y;
     }
   }
 }
 
-template <int BN, bool CODES, bool QADC>
+template <int BN, bool CONV, bool QADC>
 hipError_t launch_t(const VmmArgs& va, dim3 grid, hipStream_t s, bool debug) {
   if (debug)
-    hipLaunchKernelGGL((k_xbar_vmm<BN, CODES, QADC, true>), grid, dim3(NTHR), 0, s, va);
+    hipLaunchKernelGGL((k_xbar_vmm<BN, CONV, QADC, true>), grid, dim3(NTHR), 0, s, va);
   else
-    hipLaunchKernelGGL((k_xbar_vmm<BN, CODES, QADC, false>), grid, dim3(NTHR), 0, s, va);
+    hipLaunchKernelGGL((k_xbar_vmm<BN, CONV, QADC, false>), grid, dim3(NTHR), 0, s, va);
   return hipGetLastError();
 }
 
 template <int BN>
-hipError_t launch_bn(const VmmArgs& va, dim3 grid, hipStream_t s, bool codes, bool qadc,
+hipError_t launch_bn(const VmmArgs& va, dim3 grid, hipStream_t s, bool conv, bool qadc,
                      bool debug) {
-  if (codes) {
+  if (conv) {
     return qadc ? launch_t<BN, true, true>(va, grid, s, debug)
                 : launch_t<BN, true, false>(va, grid, s, debug);
   }
@@ -313,10 +423,9 @@ int pick_bn(int Np) {
 int choose_splits(const MapScalars& ms, const PeriphScalars& ps, int64_t Bv) {
   if (ps.adc_bits == 0 || ms.R < 2) return 1;
   const int64_t blocks = ((Bv + BM - 1) / BM) * (int64_t)ms.C * (ms.Np / pick_bn(ms.Np));
-  if (blocks >= 1024) return 1;
+  if (blocks >= 512) return 1;
   int64_t want = (1024 + blocks - 1) / blocks;
   if (want > ms.R) want = ms.R;
-  // equal shares of row tiles
   const int per = (int)((ms.R + want - 1) / want);
   return (ms.R + per - 1) / per;
 }
@@ -326,6 +435,19 @@ hipError_t launch_xbar_vmm(const MapScalars& ms, const PeriphScalars& ps, const 
   VmmArgs va;
   va.ms = ms;
   va.ps = ps;
+  va.cg = ConvGeom{0, 0, 0, 0, 0, 1, 0, 1, 1};
+  if (vl.conv) {
+    const rxnn_conv_desc& cd = *vl.conv;
+    va.cg.c_in = cd.c_in;
+    va.cg.h = cd.h;
+    va.cg.w = cd.w;
+    va.cg.kh = cd.kh;
+    va.cg.kw = cd.kw;
+    va.cg.stride = cd.stride;
+    va.cg.pad = cd.pad;
+    va.cg.ho = (cd.h + 2 * cd.pad - cd.kh) / cd.stride + 1;
+    va.cg.wo = (cd.w + 2 * cd.pad - cd.kw) / cd.stride + 1;
+  }
   va.gpt = gpt;
   va.X = vl.X;
   va.ldx = vl.ldx;
@@ -341,9 +463,10 @@ hipError_t launch_xbar_vmm(const MapScalars& ms, const PeriphScalars& ps, const 
             (unsigned)((ms.R + va.r_per_split - 1) / va.r_per_split));
   const bool qadc = ps.adc_bits > 0;
   const bool debug = vl.dbg_I != nullptr || vl.dbg_code != nullptr;
-  if (bn == 64) return launch_bn<64>(va, grid, s, vl.x_codes, qadc, debug);
-  if (bn == 32) return launch_bn<32>(va, grid, s, vl.x_codes, qadc, debug);
-  return launch_bn<16>(va, grid, s, vl.x_codes, qadc, debug);
+  const bool conv = vl.conv != nullptr;
+  if (bn == 64) return launch_bn<64>(va, grid, s, conv, qadc, debug);
+  if (bn == 32) return launch_bn<32>(va, grid, s, conv, qadc, debug);
+  return launch_bn<16>(va, grid, s, conv, qadc, debug);
 }
 
 hipError_t launch_finish(const MapScalars& ms, const PeriphScalars& ps, const int32_t* iacc,
@@ -351,8 +474,12 @@ hipError_t launch_finish(const MapScalars& ms, const PeriphScalars& ps, const in
   int64_t blocks = (Bv * ms.Q + 255) / 256;
   if (blocks > 8192) blocks = 8192;
   if (blocks < 1) blocks = 1;
-  hipLaunchKernelGGL(k_finish, dim3((unsigned)blocks), dim3(256), 0, s, ms, ps, iacc, Bv, Y,
-                     hw_out);
+  if (Bv * ms.Q < ((int64_t)1 << 31))
+    hipLaunchKernelGGL(k_finish<int32_t>, dim3((unsigned)blocks), dim3(256), 0, s, ms, ps, iacc,
+                       (int32_t)Bv, Y, (int32_t)hw_out);
+  else
+    hipLaunchKernelGGL(k_finish<int64_t>, dim3((unsigned)blocks), dim3(256), 0, s, ms, ps, iacc,
+                       Bv, Y, hw_out);
   return hipGetLastError();
 }
 

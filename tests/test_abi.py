@@ -55,7 +55,7 @@ FAKE = ctypes.c_void_p(0x1000)  # never dereferenced: validation fails first
     (dict(rows=0), rxnn.RXNN_EINVAL, "positive"),
     (dict(cols=-3), rxnn.RXNN_EINVAL, "positive"),
     (dict(rows=300), rxnn.RXNN_EINVAL, "256"),
-    (dict(rows=128), rxnn.RXNN_EUNSUPPORTED, "this build"),
+    (dict(rows=128, r_row=0.0), rxnn.RXNN_EUNSUPPORTED, "positive wire"),
     (dict(g_min=0.0), rxnn.RXNN_EINVAL, "g_min"),
     (dict(g_min=6e-5), rxnn.RXNN_EINVAL, "g_min"),
     (dict(r_row=-1.0), rxnn.RXNN_EINVAL, "resistances"),

@@ -115,6 +115,24 @@ def test_gprime_parity(P, Q, M, N, wire, wb, sb):
     say("gprime worst rel err %.3g" % worst)
 
 
+@pytest.mark.parametrize("P,Q,M,N,wire,arrays", [
+    (128, 128, 128, 128, 1.0, 2),      # 128 x 128 crossbars
+    (100, 200, 100, 200, 2.5, 1),      # rectangular, embedded in a 256 grid
+    (256, 256, 256, 256, 2.5, 1),      # 256 x 256 crossbars
+])
+def test_gprime_parity_large(P, Q, M, N, wire, arrays):
+    say("gprime large", P, Q, M, N, wire)
+    rng = np.random.default_rng(P + Q)
+    W = rng.normal(0, 0.05, size=(P, Q)).astype(np.float32)
+    xb = wl.xbar(M, N, wire)
+    L = rxnn.map_layer(dev(W), xb)
+    w_max = float(np.max(np.abs(W)))
+    G = omap.array_conductances(omap.tile_weights(W, xb, 0, 0), xb, w_max)
+    for a in range(arrays):
+        ref = gprime_nodal(G[a], xb["r_driver"], xb["r_sense"], xb["r_row"], xb["r_col"])
+        say("gprime large worst rel err %.3g" % check_gprime(L.gprime(0, 0, a), ref))
+
+
 @pytest.mark.parametrize("r_driver,r_sense,wire", [
     (0.0, 0.0, 0.0),          # no parasitics: G' = G exactly (Eq. 1)
     (1000.0, 0.0, 0.0),       # driver only: the DAC-load divider
@@ -166,6 +184,13 @@ def test_fc_256x128_parity():
 def test_fc_ragged(P, Q, M, N, B, dac, adc):
     W, X, xb, pp = fc_case(P, Q, M, N, B, dac=dac, adc=adc)
     compare_fc_debug(W, X, xb, pp, "fc ragged %s" % ((P, Q, M, N, B),))
+
+
+def test_fc_128x64_crossbars():
+    """M = 128 rows per crossbar: the evaluation consumes each tile's inputs in
+    two 64-deep chunks before the ADC."""
+    W, X, xb, pp = fc_case(200, 64, 128, 64, 70, dac=8, adc=8)
+    compare_fc_debug(W, X, xb, pp, "fc 128x64 crossbars")
 
 
 def test_fc_sliced_parity():
