@@ -255,7 +255,7 @@ hipError_t build_gprime(rxnn_layer* L, const float* W, hipStream_t s) {
     const int64_t n_arrays = (int64_t)ms.R * ms.C * ms.A;
     for (int64_t a0 = 0; a0 < n_arrays && e == hipSuccess; a0 += L->nd_chunk) {
       const int64_t n = n_arrays - a0 < L->nd_chunk ? n_arrays - a0 : L->nd_chunk;
-      e = launch_nd_build(ms, W, L->gpt, a0, n, L->nd_ws, s);
+      e = launch_nd_build(ms, W, L->gpt, a0, n, L->nd_bs, L->nd_ws, s);
     }
   }
   return e;
@@ -370,9 +370,11 @@ rxnn_status rxnn_map_layer(const rxnn_xbar_params* params, const float* W, int64
   }
   if (nd_ok(params)) {
     int64_t si, so, sc;
-    nd_sizes(nd_side(ms.M, ms.N), ms.M, &si, &so, &sc);
-    const size_t per = (size_t)(si + so + sc) * sizeof(double);
+    const int T = nd_side(ms.M, ms.N);
     const int64_t n_arrays = (int64_t)ms.R * ms.C * ms.A;
+    L->nd_bs = nd_block_side(T, n_arrays);
+    nd_sizes(T, ms.M, L->nd_bs, &si, &so, &sc);
+    const size_t per = (size_t)(si + so + sc) * sizeof(double);
     int64_t chunk = (int64_t)(kNdBudget / per);
     if (chunk < 1) chunk = 1;
     if (chunk > n_arrays) chunk = n_arrays;

@@ -56,6 +56,7 @@ struct rxnn_layer {
   size_t ws_bytes;
   double* nd_ws;       // nested-dissection build workspace (null: row sweep)
   int64_t nd_chunk;    // arrays built per pass over the workspace
+  int nd_bs;           // side of the blocks reduced in LDS
 };
 
 namespace rxnn {
@@ -67,9 +68,11 @@ hipError_t launch_fill_u32(unsigned* p, int64_t n, unsigned v, hipStream_t s);
 hipError_t launch_gprime_build(const MapScalars& ms, const float* W, float* gpt,
                                hipStream_t s);
 int nd_side(int M, int N);
-void nd_sizes(int T, int M, int64_t* in_stride, int64_t* out_stride, int64_t* scr_stride);
+int nd_block_side(int T, int64_t n_arrays);
+void nd_sizes(int T, int M, int bs, int64_t* in_stride, int64_t* out_stride,
+              int64_t* scr_stride);
 hipError_t launch_nd_build(const MapScalars& ms, const float* W, float* gpt, int64_t arr0,
-                           int64_t n, double* ws, hipStream_t s);
+                           int64_t n, int bs, double* ws, hipStream_t s);
 
 struct VmmLaunch {
   const float* X;       // FC: Bv x ldx rows; conv: the NCHW input

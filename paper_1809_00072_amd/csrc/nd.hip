@@ -51,14 +51,18 @@ struct NdArgs {
   double* scratch;
   int64_t in_stride, out_stride, scr_stride;  // doubles per array
   int h, w, vert;        // children size and merge direction (merge kernel)
+  int e_layout;          // largest external port count of a merge at this level
 };
 
 namespace {
 
-constexpr int SB = 16;          // side of the blocks reduced in LDS
-constexpr int NTH = 256;
-constexpr int LBUF = 6400;      // doubles per LDS level buffer
+constexpr int SBMIN = 8;        // smallest side of the blocks reduced in LDS
+constexpr int NTH = 256;        // threads of the kernels on the blocked global path
+constexpr int NTB = 1024;       // threads of the LDS-resident kernels (four waves per SIMD)
+// doubles per LDS level buffer of a bs x bs block reduction
+__host__ __device__ constexpr int lbuf(int bs) { return bs == 16 ? 6400 : 1600; }
 constexpr int KB = 16;          // pivots per elimination block
+constexpr int ULDS = 16384;     // doubles of cut rows a merge may keep in LDS
 
 __device__ __forceinline__ void ports(int i0, int j0, int h, int w, int T, int& nL, int& nR,
                                       int& nT, int& nB) {
@@ -116,6 +120,20 @@ __device__ __forceinline__ int merge_dest(int ch, int p, int i0, int j0, int h, 
   return oB + w + idx;
 }
 
+__device__ __forceinline__ int lg2ceil(int v) {
+  int l = 0;
+  while ((1 << l) < v) ++l;
+  return l;
+}
+
+// 1 / a to within an ulp or two: hardware reciprocal and two Newton steps.
+__device__ __forceinline__ double recip(double a) {
+  double r = __builtin_amdgcn_rcp(a);
+  r = fma(r, fma(-a, r, 1.0), r);
+  r = fma(r, fma(-a, r, 1.0), r);
+  return r;
+}
+
 __device__ __forceinline__ int nports(int i0, int j0, int h, int w, int T) {
   int a, b, c, d;
   ports(i0, j0, h, w, T, a, b, c, d);
@@ -152,11 +170,13 @@ __device__ __forceinline__ double cell_conductance(const MapScalars& ms, const f
 }
 
 // ---------------------------------------------------------------------------
-// Levels 1 x 1 .. 16 x 16 of one 16 x 16 block, in LDS.
+// Levels 1 x 1 .. SB x SB of one SB x SB block, in LDS.
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(NTH) void k_nd_block16(NdArgs na) {
-  __shared__ double bufA[LBUF];
-  __shared__ double bufB[LBUF];
+template <int SB, int NB>
+__global__ __launch_bounds__(NB) void k_nd_block(NdArgs na) {
+  __shared__ double bufA[lbuf(SB)];
+  __shared__ double bufB[lbuf(SB)];
+  __shared__ short tab[1024];
   const int tid = threadIdx.x;
   const int T = na.T;
   const int nsb = T / SB;
@@ -168,7 +188,7 @@ __global__ __launch_bounds__(NTH) void k_nd_block16(NdArgs na) {
   const double wmax = ms.wmax_fixed > 0.0f ? (double)ms.wmax_fixed : (double)*ms.d_wmax;
 
   // leaves: one cell per thread, 4 x 4 slots
-  {
+  if (tid < SB * SB) {
     const int li = tid / SB, lj = tid % SB;
     const int gi = I0 + li, gj = J0 + lj;
     const double G = cell_conductance(ms, na.W, wmax, arr, gi, gj, na.row_off);
@@ -202,47 +222,68 @@ __global__ __launch_bounds__(NTH) void k_nd_block16(NdArgs na) {
   while (h < SB || w < SB) {
     const int nh = vert ? 2 * h : h, nw = vert ? w : 2 * w;
     const int E = 2 * (nh + nw), c = vert ? w : h, ld = E + c, slot = ld * ld;
-    const int cols = SB / nw;                    // merged blocks per row of the 16 x 16 block
+    const int cols = SB / nw;                    // merged blocks per row of the block
     const int nmerge = (SB / nh) * cols;
     const int ccols = SB / w;                    // child blocks per row
-    for (int e = tid; e < nmerge * slot; e += NTH) out[e] = 0.0;
+    const int npc = ld_in;                       // child slot side
+    // destination of every child port in its merge's combined matrix
+    for (int t = tid; t < nmerge * 2 * npc; t += NB) {
+      const int m = t / (2 * npc), r2 = t - m * 2 * npc, ch = r2 >= npc ? 1 : 0;
+      const int p = r2 - ch * npc;
+      const int mi = m / cols, mj = m - mi * cols;
+      const int i0 = I0 + mi * nh, j0 = J0 + mj * nw;
+      const int np = nports((vert && ch) ? i0 + h : i0, (!vert && ch) ? j0 + w : j0, h, w, T);
+      int d = -1;
+      if (p < np) {
+        d = merge_dest(ch, p, i0, j0, h, w, vert, T);
+        d = d >= 0 ? d : E + (-1 - d);
+      }
+      tab[t] = (short)d;
+    }
+    for (int e = tid; e < nmerge * slot; e += NB) out[e] = 0.0;
     __syncthreads();
+    // child entries: consecutive threads take consecutive columns q; task
+    // spaces are padded to powers of two so that indices come from shifts
+    const int lgq = lg2ceil(npc), lgc = lg2ceil(cols), lgcc = lg2ceil(ccols);
     for (int ch = 0; ch < 2; ++ch) {
-      const int n_child = (ld_in) * (ld_in);
-      for (int e = tid; e < nmerge * n_child; e += NTH) {
-        const int m = e / n_child, rem = e % n_child;
-        const int p = rem / ld_in, q = rem % ld_in;
-        const int mi = m / cols, mj = m % cols;
-        const int i0 = I0 + mi * nh, j0 = J0 + mj * nw;
-        const int np = nports((vert && ch) ? i0 + h : i0, (!vert && ch) ? j0 + w : j0, h, w, T);
-        if (p >= np || q >= np) continue;
-        const int cm = (vert ? (mi * 2 + ch) * ccols + mj : mi * ccols + mj * 2 + ch);
-        const double v = in[cm * ld_in * ld_in + p * ld_in + q];
-        int dp = merge_dest(ch, p, i0, j0, h, w, vert, T);
-        int dq = merge_dest(ch, q, i0, j0, h, w, vert, T);
-        dp = dp >= 0 ? dp : E + (-1 - dp);
-        dq = dq >= 0 ? dq : E + (-1 - dq);
-        out[m * slot + dp * ld + dq] += v;
+      for (int t = tid; t < nmerge << (2 * lgq); t += NB) {
+        const int q = t & ((1 << lgq) - 1), p = (t >> lgq) & ((1 << lgq) - 1);
+        const int m = t >> (2 * lgq);
+        if (p >= npc || q >= npc) continue;
+        const short* dt = tab + (m * 2 + ch) * npc;
+        const int dp = dt[p], dq = dt[q];
+        if (dp < 0 || dq < 0) continue;
+        const int mi = m >> lgc, mj = m & (cols - 1);
+        const int cm = vert ? (((mi * 2 + ch) << lgcc) + mj) : ((mi << lgcc) + mj * 2 + ch);
+        out[m * slot + dp * ld + dq] += in[cm * npc * npc + p * npc + q];
       }
       __syncthreads();
     }
-    // eliminate the c shared nodes (pivot rows / columns E .. E + c - 1)
+    // eliminate the c shared nodes (pivot rows / columns E .. E + c - 1):
+    // a task is one column y of one merge over a chunk of 8 rows
+    const int lgy = lg2ceil(ld), lgx = lg2ceil((ld + 7) / 8);
     for (int k = 0; k < c; ++k) {
       const int pv = E + k;
-      // pivot row / pivot, then the rank-1 update of every other entry
-      for (int e = tid; e < nmerge * ld; e += NTH) {
-        const int m = e / ld, y = e % ld;
+      for (int t = tid; t < nmerge << (lgy + lgx); t += NB) {
+        const int y = t & ((1 << lgy) - 1);
+        const int x0 = ((t >> lgy) & ((1 << lgx) - 1)) * 8;
+        const int m = t >> (lgy + lgx);
+        if (y >= ld || y == pv || x0 >= ld) continue;
         double* A = out + m * slot;
-        if (y != pv) A[pv * ld + y] /= A[pv * ld + pv];
-      }
-      __syncthreads();
-      for (int e = tid; e < nmerge * ld * ld; e += NTH) {
-        const int m = e / (ld * ld), rem = e % (ld * ld);
-        const int x = rem / ld, y = rem % ld;
-        if (x == pv || y == pv) continue;
-        double* A = out + m * slot;
-        const double f = A[x * ld + pv];
-        if (f != 0.0) A[x * ld + y] -= f * A[pv * ld + y];
+        const double g = A[pv * ld + y] * recip(A[pv * ld + pv]);
+        if (g == 0.0) continue;
+        double axp[8], axy[8];
+#pragma unroll
+        for (int xx = 0; xx < 8; ++xx) {
+          const int x = min(x0 + xx, ld - 1);
+          axp[xx] = A[x * ld + pv];
+          axy[xx] = A[x * ld + y];
+        }
+#pragma unroll
+        for (int xx = 0; xx < 8; ++xx) {
+          const int x = x0 + xx;
+          if (x < ld && x != pv) A[x * ld + y] = axy[xx] - axp[xx] * g;
+        }
       }
       __syncthreads();
     }
@@ -255,9 +296,10 @@ __global__ __launch_bounds__(NTH) void k_nd_block16(NdArgs na) {
     vert = !vert;
   }
   // the 16 x 16 block's matrix -> global (ld 64)
-  double* dst = na.buf_out + la * na.out_stride + (int64_t)sb * 64 * 64;
-  for (int e = tid; e < 64 * 64; e += NTH) {
-    const int p = e / 64, q = e % 64;
+  constexpr int EO = 4 * SB;   // ports of an interior SB x SB block
+  double* dst = na.buf_out + la * na.out_stride + (int64_t)sb * EO * EO;
+  for (int e = tid; e < EO * EO; e += NB) {
+    const int p = e / EO, q = e % EO;
     dst[e] = (p < ld_in && q < ld_in) ? in[p * ld_in + q] : 0.0;
   }
 }
@@ -367,9 +409,54 @@ __device__ void eliminate(double* cut, int c, int E, int ldc, double* ext, int l
   }
 }
 
+// Pivot-by-pivot elimination of the c cut rows U (row stride ldu, c cut
+// columns then E external columns) held in LDS, followed by Z = D^-1/2 U_ext:
+// afterwards the Schur complement of the externals is ext - Z^T Z.
+// Pivot-by-pivot elimination of the c cut rows U (row stride ldu, c cut
+// columns then E external columns) held in LDS, followed by Z = D^-1/2 U_ext:
+// afterwards the Schur complement of the externals is ext - Z^T Z.  A task is
+// one column over a chunk of 8 rows, its loads issued before its stores.
+template <int NT>
+__device__ void eliminate_lds(double* U, int c, int E, int ldu, double* isq) {
+  const int tid = threadIdx.x;
+  const int lgy = lg2ceil(c + E);
+  for (int k = 0; k < c; ++k) {
+    const double inv = recip(U[k * ldu + k]);
+    const int nxc = (c - k - 1 + 7) / 8;
+    for (int t = tid; t < nxc << lgy; t += NT) {
+      const int y = t & ((1 << lgy) - 1);
+      if (y <= k || y >= c + E) continue;
+      const int x0 = k + 1 + (t >> lgy) * 8;
+      const double uky = U[k * ldu + y] * inv;
+      double uxk[8], uxy[8];
+#pragma unroll
+      for (int xx = 0; xx < 8; ++xx) {
+        const int x = min(x0 + xx, c - 1);
+        uxk[xx] = U[x * ldu + k];
+        uxy[xx] = U[x * ldu + y];
+      }
+#pragma unroll
+      for (int xx = 0; xx < 8; ++xx)
+        if (x0 + xx < c) U[(x0 + xx) * ldu + y] = uxy[xx] - uxk[xx] * uky;
+    }
+    __syncthreads();
+  }
+  for (int t = tid; t < c; t += NT) isq[t] = 1.0 / sqrt(U[t * ldu + t]);
+  __syncthreads();
+  const int lge = lg2ceil(E);
+  for (int t = tid; t < c << lge; t += NT) {
+    const int k = t >> lge, y = t & ((1 << lge) - 1);
+    if (y < E) U[k * ldu + c + y] *= isq[k];
+  }
+  __syncthreads();
+}
+
 // One merge of two h x w blocks (children in buf_in, result to buf_out).
-__global__ __launch_bounds__(NTH) void k_nd_merge(NdArgs na) {
-  __shared__ double lds[KB * KB + 2 * KB * 64];
+template <bool LDSP, int NT>
+__global__ __launch_bounds__(NT) void k_nd_merge(NdArgs na) {
+  extern __shared__ double lds[];   // cut rows (LDS path) or the blocked path's panels
+  __shared__ short tab[2 * 1024];   // children of a 256 x 256 grid have up to 768 ports
+  __shared__ double isq[256];
   const int tid = threadIdx.x;
   const int T = na.T, h = na.h, w = na.w;
   const bool vert = na.vert != 0;
@@ -380,35 +467,105 @@ __global__ __launch_bounds__(NTH) void k_nd_merge(NdArgs na) {
   const int mi = m / cols, mj = m % cols;
   const int i0 = mi * nh, j0 = mj * nw;
   const int Emax = 2 * (nh + nw), c = vert ? w : h;
+  const int E = nports(i0, j0, nh, nw, T);
   const int Ein = 2 * (h + w);
   const int ccols = T / w;
-  const int ldc = c + Emax;
   double* ext = na.buf_out + la * na.out_stride + (int64_t)m * Emax * Emax;
-  double* cut = na.scratch + la * na.scr_stride + (int64_t)m * c * ldc;
-  for (int e = tid; e < Emax * Emax; e += NTH) ext[e] = 0.0;
-  for (int e = tid; e < c * ldc; e += NTH) cut[e] = 0.0;
+  const int ldc = LDSP ? c + na.e_layout : c + Emax;
+  double* cut = LDSP ? lds : na.scratch + la * na.scr_stride + (int64_t)m * c * ldc;
+  for (int t = tid; t < 2 * Ein; t += NT) {
+    const int ch = t / Ein, p = t - ch * Ein;
+    const int ci = (vert && ch) ? i0 + h : i0, cj = (!vert && ch) ? j0 + w : j0;
+    tab[t] = (short)(p < nports(ci, cj, h, w, T) ? merge_dest(ch, p, i0, j0, h, w, vert, T)
+                                                 : -1000);
+  }
+  {
+    const int lge = lg2ceil(E);
+    for (int e = tid; e < E << lge; e += NT) {
+      const int y = e & ((1 << lge) - 1);
+      if (y < E) ext[(e >> lge) * Emax + y] = 0.0;
+    }
+  }
+  for (int e = tid; e < c * ldc; e += NT) cut[e] = 0.0;
   __syncthreads();
   for (int ch = 0; ch < 2; ++ch) {
-    const int ci = (vert && ch) ? i0 + h : i0, cj = (!vert && ch) ? j0 + w : j0;
-    const int np = nports(ci, cj, h, w, T);
     const int cm = vert ? (mi * 2 + ch) * ccols + mj : mi * ccols + mj * 2 + ch;
     const double* Yc = na.buf_in + la * na.in_stride + (int64_t)cm * Ein * Ein;
-    for (int e = tid; e < np * np; e += NTH) {
-      const int p = e / np, q = e % np;
-      const double v = Yc[p * Ein + q];
-      const int dp = merge_dest(ch, p, i0, j0, h, w, vert, T);
-      const int dq = merge_dest(ch, q, i0, j0, h, w, vert, T);
-      if (dp >= 0 && dq >= 0) ext[dp * Emax + dq] += v;
-      else if (dp < 0) cut[(-1 - dp) * ldc + (dq < 0 ? (-1 - dq) : c + dq)] += v;
+    const short* dt = tab + ch * Ein;
+    const int lgi = lg2ceil(Ein);
+    for (int t0 = tid; t0 < Ein << lgi; t0 += 8 * NT) {
+      double v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int t = min(t0 + u * NT, (Ein << lgi) - 1);
+        const int p = t >> lgi, q = min(t & ((1 << lgi) - 1), Ein - 1);
+        v[u] = Yc[p * Ein + q];
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int t = t0 + u * NT;
+        if (t >= Ein << lgi) continue;
+        const int p = t >> lgi, q = t & ((1 << lgi) - 1);
+        if (q >= Ein) continue;
+        const int dp = dt[p], dq = dt[q];
+        if (dp == -1000 || dq == -1000) continue;
+        if (dp >= 0) {
+          if (dq >= 0) ext[dp * Emax + dq] = v[u];
+        } else {
+          cut[(-1 - dp) * ldc + (dq < 0 ? (-1 - dq) : c + dq)] += v[u];
+        }
+      }
     }
     __syncthreads();
   }
-  eliminate(cut, c, nports(i0, j0, nh, nw, T), ldc, ext, Emax, lds);
+  if (!LDSP) {
+    eliminate(cut, c, E, ldc, ext, Emax, lds);
+    return;
+  }
+  eliminate_lds<NT>(cut, c, E, ldc, isq);
+  // ext -= Z^T Z, square tiles of TS x TS entries, 4 x 4 per thread
+  constexpr int TS = NT == 1024 ? 128 : 64;
+  const int rx = (tid / (TS / 4)) * 4, ry = (tid % (TS / 4)) * 4;
+  for (int tx0 = 0; tx0 < E; tx0 += TS)
+    for (int ty0 = 0; ty0 < E; ty0 += TS) {
+      double acc[4][4];
+#pragma unroll
+      for (int a = 0; a < 4; ++a)
+#pragma unroll
+        for (int b = 0; b < 4; ++b) acc[a][b] = 0.0;
+      for (int k = 0; k < c; ++k) {
+        const double* z = cut + k * ldc + c;
+        double xa[4], yb[4];
+#pragma unroll
+        for (int a = 0; a < 4; ++a) xa[a] = z[min(tx0 + rx + a, E - 1)];
+#pragma unroll
+        for (int b = 0; b < 4; ++b) yb[b] = z[min(ty0 + ry + b, E - 1)];
+#pragma unroll
+        for (int a = 0; a < 4; ++a)
+#pragma unroll
+          for (int b = 0; b < 4; ++b) acc[a][b] = fma(xa[a], yb[b], acc[a][b]);
+      }
+#pragma unroll
+      for (int a = 0; a < 4; ++a) {
+        const int x = tx0 + rx + a;
+        if (x >= E) continue;
+#pragma unroll
+        for (int b = 0; b < 4; ++b) {
+          const int y = ty0 + ry + b;
+          if (y < E) ext[x * Emax + y] -= acc[a][b];
+        }
+      }
+    }
 }
 
 // Drivers and sinks: G'^T = -(Y_sL (Y_LL + g_d I)^-1 g_d E), written as fp32.
-__global__ __launch_bounds__(NTH) void k_nd_final(NdArgs na) {
-  __shared__ double lds[KB * KB + 2 * KB * 64];
+// Externals: the M source terminals t, then the T sink terminals s; cut: the
+// T row-input nodes.  Only the (s, t) block of the result is needed.
+template <bool LDSP>
+__global__ __launch_bounds__(LDSP ? NTB : NTH) void k_nd_final(NdArgs na) {
+  constexpr int NT = LDSP ? NTB : NTH;
+  extern __shared__ double lds[];
+  __shared__ double isq[256];
   const int tid = threadIdx.x;
   const int T = na.T, M = na.ms.M, N = na.ms.N;
   const int64_t la = blockIdx.x;
@@ -416,40 +573,64 @@ __global__ __launch_bounds__(NTH) void k_nd_final(NdArgs na) {
   const double* Y = na.buf_in + la * na.in_stride;
   const int E = M + T, c = T, ldc = c + E;
   double* ext = na.scratch + la * na.scr_stride;
-  double* cut = ext + (int64_t)E * E;
-  // ports of the whole grid: L (T) then B (T); externals: sources t (M), sinks s (T)
-  for (int e = tid; e < E * E; e += NTH) {
-    const int x = e / E, y = e % E;
-    double v = 0.0;
-    if (x < M && y < M) v = (x == y) ? na.g_d : 0.0;
-    else if (x >= M && y >= M) v = Y[(T + x - M) * Ein + (T + y - M)];
-    ext[e] = v;
+  double* cut = LDSP ? lds : ext + (int64_t)E * E;
+  if (!LDSP) {
+    for (int e = tid; e < E * E; e += NT) {
+      const int x = e / E, y = e % E;
+      double v = 0.0;
+      if (x < M && y < M) v = (x == y) ? na.g_d : 0.0;
+      else if (x >= M && y >= M) v = Y[(T + x - M) * Ein + (T + y - M)];
+      ext[e] = v;
+    }
   }
-  for (int e = tid; e < c * ldc; e += NTH) {
-    const int i = e / ldc, y = e % ldc;
+  const int lgl = lg2ceil(ldc);
+  for (int e = tid; e < c << lgl; e += NT) {
+    const int i = e >> lgl, y = e & ((1 << lgl) - 1);
+    if (y >= ldc) continue;
     double v;
     if (y < c) v = Y[i * Ein + y] + (i == y ? na.g_d : 0.0);
     else if (y < c + M) v = (i == na.row_off + (y - c)) ? -na.g_d : 0.0;
     else v = Y[i * Ein + T + (y - c - M)];
-    cut[e] = v;
+    cut[i * ldc + y] = v;
   }
   __syncthreads();
-  eliminate(cut, c, E, ldc, ext, E, lds);
   const int64_t arr = na.arr0 + la;
   float* out = na.gpt + arr * (int64_t)na.ms.Np * na.ms.Mp;
-  for (int e = tid; e < na.ms.Np * na.ms.Mp; e += NTH) {
-    const int j = e / na.ms.Mp, k = e % na.ms.Mp;
-    out[e] = (j < N && k < M) ? (float)(-ext[(int64_t)(M + j) * E + k]) : 0.0f;
+  if (!LDSP) {
+    eliminate(cut, c, E, ldc, ext, E, lds);
+    for (int e = tid; e < na.ms.Np * na.ms.Mp; e += NT) {
+      const int j = e / na.ms.Mp, k = e % na.ms.Mp;
+      out[e] = (j < N && k < M) ? (float)(-ext[(int64_t)(M + j) * E + k]) : 0.0f;
+    }
+    return;
+  }
+  eliminate_lds<NT>(cut, c, E, ldc, isq);
+  const int lgm = lg2ceil(na.ms.Mp);
+  for (int e = tid; e < na.ms.Np << lgm; e += NT) {
+    const int j = e >> lgm, k = e & ((1 << lgm) - 1);
+    if (k >= na.ms.Mp) continue;
+    double v = 0.0;
+    if (j < N && k < M)
+      for (int l = 0; l < c; ++l) v = fma(cut[l * ldc + c + M + j], cut[l * ldc + c + k], v);
+    out[j * na.ms.Mp + k] = (float)v;
   }
 }
 
 }  // namespace
 
+// Side of the blocks reduced in LDS: 8 x 8 blocks give more, smaller
+// workgroups (several per CU) when the arrays of a chunk alone would not fill
+// the device; 16 x 16 blocks need fewer merge passes.
+int nd_block_side(int T, int64_t n_arrays) {
+  return (n_arrays * (T / 16) * (T / 16) < 1024) ? 8 : 16;
+}
+
 // Doubles of workspace one array needs (level buffers in, out, scratch).
-void nd_sizes(int T, int M, int64_t* in_stride, int64_t* out_stride, int64_t* scr_stride) {
-  int64_t lvl = (int64_t)(T / SB) * (T / SB) * 64 * 64;
+void nd_sizes(int T, int M, int bs, int64_t* in_stride, int64_t* out_stride,
+              int64_t* scr_stride) {
+  int64_t lvl = (int64_t)(T / bs) * (T / bs) * (4 * bs) * (4 * bs);
   int64_t scr = 0;
-  int h = SB, w = SB;
+  int h = bs, w = bs;
   bool vert = true;
   while (h < T || w < T) {
     const int nh = vert ? 2 * h : h, nw = vert ? w : 2 * w;
@@ -470,15 +651,30 @@ void nd_sizes(int T, int M, int64_t* in_stride, int64_t* out_stride, int64_t* sc
 }
 
 int nd_side(int M, int N) {
-  int T = SB;
+  int T = 16;
   while (T < M || T < N) T *= 2;
   return T;
 }
 
+static bool g_nd_attr = false;
+
 // Builds G' of arrays [arr0, arr0 + n) with the workspace ws (ping-pong
 // level buffers and scratch, sized by nd_sizes for one array, times n).
 hipError_t launch_nd_build(const MapScalars& ms, const float* W, float* gpt, int64_t arr0,
-                           int64_t n, double* ws, hipStream_t s) {
+                           int64_t n, int bs, double* ws, hipStream_t s) {
+  if (!g_nd_attr) {
+    const int mx = ULDS * (int)sizeof(double);
+    hipError_t e0 = hipFuncSetAttribute((const void*)k_nd_merge<true, NTB>,
+                                        hipFuncAttributeMaxDynamicSharedMemorySize, mx);
+    if (e0 == hipSuccess)
+      e0 = hipFuncSetAttribute((const void*)k_nd_merge<true, NTH>,
+                               hipFuncAttributeMaxDynamicSharedMemorySize, mx);
+    if (e0 == hipSuccess)
+      e0 = hipFuncSetAttribute((const void*)k_nd_final<true>,
+                               hipFuncAttributeMaxDynamicSharedMemorySize, mx);
+    if (e0 != hipSuccess) return e0;
+    g_nd_attr = true;
+  }
   NdArgs na;
   na.ms = ms;
   na.W = W;
@@ -491,22 +687,25 @@ hipError_t launch_nd_build(const MapScalars& ms, const float* W, float* gpt, int
   na.g_s = 1.0 / ms.r_sense;
   na.g_d = 1.0 / (ms.r_driver + ms.r_row);
   int64_t si, so, sc;
-  nd_sizes(na.T, ms.M, &si, &so, &sc);
+  nd_sizes(na.T, ms.M, bs, &si, &so, &sc);
   double* bufA = ws;
   double* bufB = ws + n * si;
   na.scratch = ws + n * (si + so);
   na.in_stride = si;
   na.out_stride = so;
   na.scr_stride = sc;
-  const int nsb = na.T / SB;
+  const int nsb = na.T / bs;
   na.buf_in = nullptr;
   na.buf_out = bufA;
-  hipLaunchKernelGGL(k_nd_block16, dim3((unsigned)(n * nsb * nsb)), dim3(NTH), 0, s, na);
+  if (bs == 8)
+    hipLaunchKernelGGL((k_nd_block<8, NTH>), dim3((unsigned)(n * nsb * nsb)), dim3(NTH), 0, s, na);
+  else
+    hipLaunchKernelGGL((k_nd_block<16, NTB>), dim3((unsigned)(n * nsb * nsb)), dim3(NTB), 0, s, na);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   double* cur = bufA;
   double* nxt = bufB;
-  int h = SB, w = SB;
+  int h = bs, w = bs;
   bool vert = true;
   while (h < na.T || w < na.T) {
     const int nh = vert ? 2 * h : h, nw = vert ? w : 2 * w;
@@ -516,7 +715,25 @@ hipError_t launch_nd_build(const MapScalars& ms, const float* W, float* gpt, int
     na.h = h;
     na.w = w;
     na.vert = vert ? 1 : 0;
-    hipLaunchKernelGGL(k_nd_merge, dim3((unsigned)(n * nmerge)), dim3(NTH), 0, s, na);
+    int e_layout = 0;
+    for (int bi = 0; bi < na.T / nh; ++bi)
+      for (int bj = 0; bj < na.T / nw; ++bj) {
+        const int e_b = nh + ((bj + 1) * nw < na.T ? nh : 0) + (bi > 0 ? nw : 0) + nw;
+        e_layout = e_layout > e_b ? e_layout : e_b;
+      }
+    na.e_layout = e_layout;
+    const int c = vert ? w : h;
+    const int64_t u = (int64_t)c * (c + e_layout);
+    const unsigned nwg = (unsigned)(n * nmerge);
+    if (u <= ULDS && c <= 16)
+      hipLaunchKernelGGL((k_nd_merge<true, NTH>), dim3(nwg), dim3(NTH),
+                         (unsigned)(u * sizeof(double)), s, na);
+    else if (u <= ULDS)
+      hipLaunchKernelGGL((k_nd_merge<true, NTB>), dim3(nwg), dim3(NTB),
+                         (unsigned)(u * sizeof(double)), s, na);
+    else
+      hipLaunchKernelGGL((k_nd_merge<false, NTH>), dim3(nwg), dim3(NTH),
+                         (unsigned)((KB * KB + 2 * KB * 64) * sizeof(double)), s, na);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
     double* t = cur;
@@ -527,7 +744,13 @@ hipError_t launch_nd_build(const MapScalars& ms, const float* W, float* gpt, int
     vert = !vert;
   }
   na.buf_in = cur;
-  hipLaunchKernelGGL(k_nd_final, dim3((unsigned)n), dim3(NTH), 0, s, na);
+  const int64_t uf = (int64_t)na.T * (na.T + ms.M + na.T);
+  if (uf <= ULDS)
+    hipLaunchKernelGGL(k_nd_final<true>, dim3((unsigned)n), dim3(NTB),
+                       (unsigned)(uf * sizeof(double)), s, na);
+  else
+    hipLaunchKernelGGL(k_nd_final<false>, dim3((unsigned)n), dim3(NTH),
+                       (unsigned)((KB * KB + 2 * KB * 64) * sizeof(double)), s, na);
   return hipGetLastError();
 }
 

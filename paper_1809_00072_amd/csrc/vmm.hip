@@ -83,6 +83,7 @@ __global__ __launch_bounds__(NTHR, 2) void k_xbar_vmm(VmmArgs va) {
   __shared__ float lut[256];
   __shared__ float thr[258];
   __shared__ unsigned char bucket[kMaxBuckets];
+  __shared__ int2 ktab[2][KC];   // conv: per stage, input offset and (ky, kx) of each k
 
   const MapScalars& ms = va.ms;
   const PeriphScalars& ps = va.ps;
@@ -176,21 +177,14 @@ __global__ __launch_bounds__(NTHR, 2) void k_xbar_vmm(VmmArgs va) {
     const int ap = rem / nkc, kc0 = (rem % nkc) * KC;
     if (ap == 0 || nkc > 1) {
       if (CONV) {
-        const int khw = va.cg.kh * va.cg.kw;
-        const int hw_in = va.cg.h * va.cg.w;
+        const int2* kt = ktab[s & 1];
 #pragma unroll
         for (int it = 0; it < XPT; ++it) {
-          const int km = kc0 + kk_cv + 2 * it;
-          const int p = r * ms.M + km;
+          const int2 e = kt[kk_cv + 2 * it];
           float x = 0.0f;
-          if (km < ms.M && p < ms.P) {
-            const int ci = p / khw, rr = p - ci * khw;
-            const int ky = rr / va.cg.kw, kx = rr - ky * va.cg.kw;
-            if ((yok >> ky) & (xok >> kx) & 1u) {
-              const int off = xrow_off + ci * hw_in + ky * va.cg.w + kx;
-              x = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(xsrc, off * 4, 0, 0));
-            }
-          }
+          if (e.x >= 0 && ((yok >> (e.y >> 8)) & (xok >> (e.y & 255)) & 1u))
+            x = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
+                                              xsrc, (xrow_off + e.x) * 4, 0, 0));
           xr[it] = x;
         }
       } else {
@@ -225,6 +219,23 @@ __global__ __launch_bounds__(NTHR, 2) void k_xbar_vmm(VmmArgs va) {
       }
       gr[it] = v;
     }
+  };
+
+  // conv: offset of input element k of stage s relative to (img, iy0, ix0)
+  auto build_ktab = [&](int s) {
+    if (!CONV || tid >= KC) return;
+    const int r = r_begin + s / per_r;
+    const int kc0 = ((s % per_r) % nkc) * KC;
+    const int km = kc0 + tid;
+    const int p = r * ms.M + km;
+    int2 e = make_int2(-1, 0);
+    if (km < ms.M && p < ms.P) {
+      const int khw = va.cg.kh * va.cg.kw;
+      const int ci = p / khw, rr = p - ci * khw;
+      const int ky = rr / va.cg.kw, kx = rr - ky * va.cg.kw;
+      e = make_int2(ci * va.cg.h * va.cg.w + ky * va.cg.w + kx, (ky << 8) | kx);
+    }
+    ktab[s & 1][tid] = e;
   };
 
   auto dac = [&](float x) -> float {
@@ -267,6 +278,8 @@ __global__ __launch_bounds__(NTHR, 2) void k_xbar_vmm(VmmArgs va) {
       for (int v = 0; v < 4; ++v) { iacc[mt][nt][v] = 0; facc[mt][nt][v] = 0.0f; }
   f32x4 acc[2][MT][NT];
 
+  if (n_stages > 0) build_ktab(0);
+  __syncthreads();
   if (n_stages > 0) load_stage(0);
   for (int s = 0; s < n_stages; ++s) {
     const int r = r_begin + s / per_r;
@@ -274,6 +287,7 @@ __global__ __launch_bounds__(NTHR, 2) void k_xbar_vmm(VmmArgs va) {
     const int ap = rem / nkc, kci = rem % nkc, kc0 = kci * KC;
     __syncthreads();
     store_stage(s);
+    if (s + 1 < n_stages) build_ktab(s + 1);
     __syncthreads();
     if (s + 1 < n_stages) load_stage(s + 1);
     if (kci == 0) {
