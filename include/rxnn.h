@@ -205,8 +205,10 @@ void rxnn_free_layer(rxnn_layer* layer);
 /*
  * Kernel timing, for measurement: when enabled, the library brackets each
  * kernel it launches with HIP events on the launch stream and accumulates
- * the elapsed time per kernel name ("xbar_vmm", "gprime_build", "dac_im2col",
- * "wmax", "finish").  rxnn_profile_read synchronises, folds pending events
+ * the elapsed time per kernel name: "wmax" (w_max reduction), "nd_block",
+ * "nd_merge", "nd_final" (G' build by nested dissection), "gprime_sweep" (G'
+ * build by the row sweep), "xbar_vmm" (evaluation), "fill" and "finish"
+ * (split accumulation).  rxnn_profile_read synchronises, folds pending events
  * into the totals and returns total milliseconds and launch count.
  */
 rxnn_status rxnn_profile_enable(int32_t on);

@@ -250,8 +250,10 @@ hipError_t build_gprime(rxnn_layer* L, const float* W, hipStream_t s) {
     }
   }
   if (e == hipSuccess) {
-    ProfScope t("gprime_build", s);
-    if (!L->nd_ws) return launch_gprime_build(ms, W, L->gpt, s);
+    if (!L->nd_ws) {
+      ProfScope t("gprime_sweep", s);
+      return launch_gprime_build(ms, W, L->gpt, s);
+    }
     const int64_t n_arrays = (int64_t)ms.R * ms.C * ms.A;
     for (int64_t a0 = 0; a0 < n_arrays && e == hipSuccess; a0 += L->nd_chunk) {
       const int64_t n = n_arrays - a0 < L->nd_chunk ? n_arrays - a0 : L->nd_chunk;

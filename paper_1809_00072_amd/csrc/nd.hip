@@ -697,10 +697,14 @@ hipError_t launch_nd_build(const MapScalars& ms, const float* W, float* gpt, int
   const int nsb = na.T / bs;
   na.buf_in = nullptr;
   na.buf_out = bufA;
-  if (bs == 8)
-    hipLaunchKernelGGL((k_nd_block<8, NTH>), dim3((unsigned)(n * nsb * nsb)), dim3(NTH), 0, s, na);
-  else
-    hipLaunchKernelGGL((k_nd_block<16, NTB>), dim3((unsigned)(n * nsb * nsb)), dim3(NTB), 0, s, na);
+  {
+    ProfScope prof("nd_block", s);
+    const dim3 grid((unsigned)(n * nsb * nsb));
+    if (bs == 8)
+      hipLaunchKernelGGL((k_nd_block<8, NTH>), grid, dim3(NTH), 0, s, na);
+    else
+      hipLaunchKernelGGL((k_nd_block<16, NTB>), grid, dim3(NTB), 0, s, na);
+  }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   double* cur = bufA;
@@ -724,16 +728,19 @@ hipError_t launch_nd_build(const MapScalars& ms, const float* W, float* gpt, int
     na.e_layout = e_layout;
     const int c = vert ? w : h;
     const int64_t u = (int64_t)c * (c + e_layout);
-    const unsigned nwg = (unsigned)(n * nmerge);
-    if (u <= ULDS && c <= 16)
-      hipLaunchKernelGGL((k_nd_merge<true, NTH>), dim3(nwg), dim3(NTH),
-                         (unsigned)(u * sizeof(double)), s, na);
-    else if (u <= ULDS)
-      hipLaunchKernelGGL((k_nd_merge<true, NTB>), dim3(nwg), dim3(NTB),
-                         (unsigned)(u * sizeof(double)), s, na);
-    else
-      hipLaunchKernelGGL((k_nd_merge<false, NTH>), dim3(nwg), dim3(NTH),
-                         (unsigned)((KB * KB + 2 * KB * 64) * sizeof(double)), s, na);
+    const dim3 grid((unsigned)(n * nmerge));
+    {
+      ProfScope prof("nd_merge", s);
+      if (u <= ULDS && c <= 16)
+        hipLaunchKernelGGL((k_nd_merge<true, NTH>), grid, dim3(NTH),
+                           (unsigned)(u * sizeof(double)), s, na);
+      else if (u <= ULDS)
+        hipLaunchKernelGGL((k_nd_merge<true, NTB>), grid, dim3(NTB),
+                           (unsigned)(u * sizeof(double)), s, na);
+      else
+        hipLaunchKernelGGL((k_nd_merge<false, NTH>), grid, dim3(NTH),
+                           (unsigned)((KB * KB + 2 * KB * 64) * sizeof(double)), s, na);
+    }
     e = hipGetLastError();
     if (e != hipSuccess) return e;
     double* t = cur;
@@ -744,13 +751,16 @@ hipError_t launch_nd_build(const MapScalars& ms, const float* W, float* gpt, int
     vert = !vert;
   }
   na.buf_in = cur;
-  const int64_t uf = (int64_t)na.T * (na.T + ms.M + na.T);
-  if (uf <= ULDS)
-    hipLaunchKernelGGL(k_nd_final<true>, dim3((unsigned)n), dim3(NTB),
-                       (unsigned)(uf * sizeof(double)), s, na);
-  else
-    hipLaunchKernelGGL(k_nd_final<false>, dim3((unsigned)n), dim3(NTH),
-                       (unsigned)((KB * KB + 2 * KB * 64) * sizeof(double)), s, na);
+  {
+    ProfScope prof("nd_final", s);
+    const int64_t uf = (int64_t)na.T * (na.T + ms.M + na.T);
+    if (uf <= ULDS)
+      hipLaunchKernelGGL(k_nd_final<true>, dim3((unsigned)n), dim3(NTB),
+                         (unsigned)(uf * sizeof(double)), s, na);
+    else
+      hipLaunchKernelGGL(k_nd_final<false>, dim3((unsigned)n), dim3(NTH),
+                         (unsigned)((KB * KB + 2 * KB * 64) * sizeof(double)), s, na);
+  }
   return hipGetLastError();
 }
 
