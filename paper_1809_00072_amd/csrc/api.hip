@@ -7,6 +7,7 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <algorithm>
 #include <map>
 #include <mutex>
 #include <set>
@@ -184,7 +185,7 @@ rxnn_status check_acc_range(const MapScalars& ms, const PeriphScalars& ps) {
 rxnn_status run_vmm(const rxnn_layer* L, const PeriphScalars& ps, const float* X,
                     const rxnn_conv_desc* conv, int64_t ldx, int64_t Bv, float* Y,
                     int64_t hw_out, float* dbgI, int32_t* dbgC, hipStream_t s,
-                    int32_t* iacc_ws) {
+                    int32_t* iacc_ws, const int2* ktab = nullptr) {
   const MapScalars& ms = L->ms;
   const int splits = (dbgI || dbgC) ? 1 : choose_splits(ms, ps, Bv);
   VmmLaunch vl;
@@ -197,6 +198,7 @@ rxnn_status run_vmm(const rxnn_layer* L, const PeriphScalars& ps, const float* X
   vl.iacc = nullptr;
   vl.dbg_I = dbgI;
   vl.dbg_code = dbgC;
+  vl.ktab = ktab;
   if (splits > 1) {
     vl.iacc = iacc_ws;
     ProfScope z("fill", s);
@@ -224,6 +226,9 @@ rxnn_status vmm_common(const rxnn_layer* layer, const rxnn_periph_params* periph
   rxnn_status st = make_periph(periph, L->ms, &ps);
   if (st) return st;
   if ((st = check_acc_range(L->ms, ps))) return st;
+  // the evaluation kernel addresses a 128-row block of X with 32-bit byte offsets
+  if (L->ms.P >= (int64_t)1 << 22)
+    return fail(RXNN_EUNSUPPORTED, "P must be below 2^22 for the evaluation kernel");
   if (B == 0) return RXNN_OK;
   DeviceGuard dg(L->device);
   if (!dg.ok) return fail(RXNN_EHIP, "cannot select the layer's device");
@@ -440,11 +445,16 @@ rxnn_status rxnn_conv_layer(const rxnn_layer* layer, const rxnn_periph_params* p
     return fail(RXNN_EINVAL, "invalid convolution shape");
   if (cd.h + 2 * cd.pad < cd.kh || cd.w + 2 * cd.pad < cd.kw)
     return fail(RXNN_EINVAL, "kernel larger than the padded input");
+  if (cd.kh > 32 || cd.kw > 32)
+    return fail(RXNN_EUNSUPPORTED, "kernel sides above 32 are not supported");
+
   rxnn_layer* L = const_cast<rxnn_layer*>(layer);
   const MapScalars& ms = L->ms;
   if (ms.P != (int64_t)cd.c_in * cd.kh * cd.kw || ms.Q != cd.c_out)
     return fail(RXNN_EINVAL, "layer is %lldx%lld but the convolution needs %lldx%d",
                 (long long)ms.P, (long long)ms.Q, (long long)cd.c_in * cd.kh * cd.kw, cd.c_out);
+  if (ms.P >= (int64_t)1 << 22)
+    return fail(RXNN_EUNSUPPORTED, "P must be below 2^22 for the evaluation kernel");
   PeriphScalars ps;
   rxnn_status st = make_periph(periph, ms, &ps);
   if (st) return st;
@@ -452,6 +462,13 @@ rxnn_status rxnn_conv_layer(const rxnn_layer* layer, const rxnn_periph_params* p
   const int64_t ho = (cd.h + 2 * cd.pad - cd.kh) / cd.stride + 1;
   const int64_t wo = (cd.w + 2 * cd.pad - cd.kw) / cd.stride + 1;
   const int64_t Bv = (int64_t)cd.n * ho * wo;
+  {
+    // the images one 128-pixel block of the evaluation kernel reads are
+    // addressed with 32-bit byte offsets
+    const int64_t span = std::min<int64_t>(cd.n, 127 / (ho * wo) + 2);
+    if ((span * cd.c_in * cd.h * cd.w + (int64_t)cd.pad * (cd.w + 1)) * 4 >= (int64_t)1 << 31)
+      return fail(RXNN_EUNSUPPORTED, "input images too large for the evaluation kernel");
+  }
   if (Bv == 0) return RXNN_OK;
   if (!X || !Y) return fail(RXNN_EINVAL, "X and Y must not be NULL");
   DeviceGuard dg(L->device);
@@ -462,7 +479,34 @@ rxnn_status rxnn_conv_layer(const rxnn_layer* layer, const rxnn_periph_params* p
     if ((st = grow_ws(L, (size_t)Bv * ms.Q * sizeof(int32_t)))) return st;
     iacc = (int32_t*)L->ws;
   }
-  return run_vmm(L, ps, X, &cd, 0, Bv, Y, ho * wo, nullptr, nullptr, s, iacc);
+  // patch-column table (per row tile and input: offset in the window, tap),
+  // rebuilt when the geometry changes; taps are numbered below 31
+  const int2* ktab = nullptr;
+  if (cd.kh * cd.kw <= 31) {
+    const int key[5] = {cd.c_in, cd.h, cd.w, cd.kh, cd.kw};
+    const int64_t n = ktab_entries(ms);
+    if (!L->ktab || memcmp(key, L->ktab_key, sizeof key) != 0) {
+      if (L->ktab_cap < n) {
+        if (L->ktab) HIP_TRY(hipFree(L->ktab));
+        L->ktab = nullptr;
+        L->ktab_cap = 0;
+        void* p = nullptr;
+        if (hipMalloc(&p, (size_t)n * sizeof(int2)) != hipSuccess) {
+          (void)hipGetLastError();
+          return fail(RXNN_ENOMEM, "cannot allocate the patch-column table");
+        }
+        L->ktab = (int2*)p;
+        L->ktab_cap = n;
+      }
+      {
+        ProfScope t("ktab", s);
+        HIP_TRY(launch_conv_ktab(ms, cd, L->ktab, s));
+      }
+      memcpy(L->ktab_key, key, sizeof key);
+    }
+    ktab = L->ktab;
+  }
+  return run_vmm(L, ps, X, &cd, 0, Bv, Y, ho * wo, nullptr, nullptr, s, iacc, ktab);
 }
 
 rxnn_status rxnn_get_gprime(const rxnn_layer* layer, int64_t row_tile, int64_t col_tile,
@@ -540,6 +584,7 @@ void rxnn_free_layer(rxnn_layer* layer) {
   (void)hipFree(layer->d_wmax);
   if (layer->ws) (void)hipFree(layer->ws);
   if (layer->nd_ws) (void)hipFree(layer->nd_ws);
+  if (layer->ktab) (void)hipFree(layer->ktab);
   layer->magic = 0;
   delete layer;
 }

@@ -57,6 +57,9 @@ struct rxnn_layer {
   double* nd_ws;       // nested-dissection build workspace (null: row sweep)
   int64_t nd_chunk;    // arrays built per pass over the workspace
   int nd_bs;           // side of the blocks reduced in LDS
+  int2* ktab;          // patch-column table of the last convolution geometry (or null)
+  int64_t ktab_cap;    // entries allocated
+  int ktab_key[5];     // c_in, h, w, kh, kw the table was built for
 };
 
 namespace rxnn {
@@ -84,9 +87,13 @@ struct VmmLaunch {
   int32_t* iacc;        // split accumulation workspace (Bv x Q int32) or null
   float* dbg_I;         // [R][C][A][Bv][N] or null
   int32_t* dbg_code;    // [R][C][A][Bv][N] or null
+  const int2* ktab;     // conv: patch-column table (kh kw <= 31) or null
 };
 hipError_t launch_xbar_vmm(const MapScalars& ms, const PeriphScalars& ps, const float* gpt,
                            const VmmLaunch& vl, int splits, hipStream_t s);
+int ktab_entries(const MapScalars& ms);
+hipError_t launch_conv_ktab(const MapScalars& ms, const rxnn_conv_desc& cd, int2* tab,
+                            hipStream_t s);
 hipError_t launch_finish(const MapScalars& ms, const PeriphScalars& ps, const int32_t* iacc,
                          int64_t Bv, float* Y, int64_t hw_out, hipStream_t s);
 int choose_splits(const MapScalars& ms, const PeriphScalars& ps, int64_t Bv);

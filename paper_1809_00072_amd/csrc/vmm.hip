@@ -39,6 +39,9 @@ constexpr int KC = 64;        // inputs (k) staged per chunk
 constexpr int LDK = KC + 4;   // LDS row stride in floats
 constexpr int NTHR = 256;
 constexpr int XPT = BM * KC / NTHR;  // V elements staged per thread
+// Buffer offset of an element that is not loaded: at or beyond the end of every
+// buffer (all are below 2^31 bytes), so the load returns 0 without a memory access.
+constexpr int kOob = (int)0x80000000u;
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
@@ -58,6 +61,7 @@ struct VmmArgs {
   int32_t* iacc;
   float* dbg_I;
   int32_t* dbg_code;
+  const int2* ktab;   // conv, kh kw <= 31: per (row tile, input) {byte offset, tap}
   int r_per_split;
 };
 
@@ -73,8 +77,11 @@ __device__ __forceinline__ int adc_code(float I, const float* thr, const unsigne
   return c + (I >= thr[c + 1] ? 1 : 0);
 }
 
-template <int BN, bool CONV, bool QADC, bool DEBUG>
+// CV: 0 fully connected; 1 convolution, patch columns decomposed in the
+// kernel; 2 convolution, patch columns read from the per-layer table.
+template <int BN, int CV, bool QADC, bool DEBUG>
 __global__ __launch_bounds__(NTHR, 2) void k_xbar_vmm(VmmArgs va) {
+  constexpr bool CONV = CV > 0;
   constexpr int NT = BN / 16;   // column fragments per wave
   constexpr int MT = 2;         // row fragments per wave (32 rows)
   constexpr int GV4 = BN / 8;   // float4 of G' staged per thread
@@ -83,7 +90,6 @@ __global__ __launch_bounds__(NTHR, 2) void k_xbar_vmm(VmmArgs va) {
   __shared__ float lut[256];
   __shared__ float thr[258];
   __shared__ unsigned char bucket[kMaxBuckets];
-  __shared__ int2 ktab[2][KC];   // conv: per stage, input offset and (ky, kx) of each k
 
   const MapScalars& ms = va.ms;
   const PeriphScalars& ps = va.ps;
@@ -131,9 +137,11 @@ __global__ __launch_bounds__(NTHR, 2) void k_xbar_vmm(VmmArgs va) {
   // product rows (consecutive output pixels), every wave shares one k.
   const int kk_fc = tid & 63, row_fc = tid >> 6;
   const int row_cv = tid & (BM - 1);
-  const int kk_cv = __builtin_amdgcn_readfirstlane(tid >> 7);
+  const int kq_cv = __builtin_amdgcn_readfirstlane(tid >> 7);  // conv: first quad of 4 k
   int xrow_off = 0;          // conv: element offset of (img, iy0, ix0) from the WG base
-  unsigned yok = 0, xok = 0;  // conv: bit ky (kx) set when the tap is inside the image
+  unsigned yok = 0, xok = 0;  // conv: bit ky (kx) set when that tap row (column) is inside the image
+  unsigned tapbad = ~0u;     // table mode: bit ky kw + kx set when that tap is outside the image
+                             // (bit 31, the table's code for a missing input, always set)
   __amdgpu_buffer_rsrc_t xsrc;
   int n_rows = (int)min((int64_t)BM, va.Bv - b0);
   if (CONV) {
@@ -141,8 +149,11 @@ __global__ __launch_bounds__(NTHR, 2) void k_xbar_vmm(VmmArgs va) {
     const int64_t chw = (int64_t)va.cg.c_in * va.cg.h * va.cg.w;
     const int64_t img_first = b0 / hw;
     const int64_t img_last = (b0 + n_rows - 1) / hw;
-    xsrc = __builtin_amdgcn_make_buffer_rsrc((void*)(va.X + img_first * chw), (short)0,
-                                             (int)((img_last - img_first + 1) * chw * 4),
+    // table mode: the descriptor starts pad (w + 1) elements before the first
+    // image, so that every lane's base offset is non-negative
+    const int64_t shift = CV == 2 ? (int64_t)va.cg.pad * (va.cg.w + 1) : 0;
+    xsrc = __builtin_amdgcn_make_buffer_rsrc((void*)(va.X + img_first * chw - shift), (short)0,
+                                             (int)(((img_last - img_first + 1) * chw + shift) * 4),
                                              0x00020000);
     if (row_cv < n_rows) {
       const int64_t bv = b0 + row_cv;
@@ -156,6 +167,13 @@ __global__ __launch_bounds__(NTHR, 2) void k_xbar_vmm(VmmArgs va) {
         if (iy0 + t >= 0 && iy0 + t < va.cg.h) yok |= 1u << t;
       for (int t = 0; t < va.cg.kw; ++t)
         if (ix0 + t >= 0 && ix0 + t < va.cg.w) xok |= 1u << t;
+      if (CV == 2) {
+        xrow_off = (xrow_off + (int)shift) * 4;   // byte offset from the shifted descriptor
+        tapbad = 1u << 31;
+        for (int ty = 0; ty < va.cg.kh; ++ty)
+          for (int tx = 0; tx < va.cg.kw; ++tx)
+            if (!((yok >> ty) & (xok >> tx) & 1u)) tapbad |= 1u << (ty * va.cg.kw + tx);
+      }
     }
   } else {
     xsrc = __builtin_amdgcn_make_buffer_rsrc((void*)(va.X + b0 * va.ldx), (short)0,
@@ -176,26 +194,71 @@ __global__ __launch_bounds__(NTHR, 2) void k_xbar_vmm(VmmArgs va) {
     const int rem = s % per_r;
     const int ap = rem / nkc, kc0 = (rem % nkc) * KC;
     if (ap == 0 || nkc > 1) {
-      if (CONV) {
-        const int2* kt = ktab[s & 1];
+      if (CV == 2) {
+        // this thread gathers k = 4 (kq_cv + 2 q) .. + 3, q = 0 .. 7, of its
+        // pixel.  The table gives, per k, the byte offset of the input element
+        // relative to the pixel's window (a scalar, the same for the wave) and
+        // its tap; a tap outside the image (or code 31, no input) turns the
+        // lane's offset out of range, so the load returns 0.
+        const int2* kt = va.ktab + (int64_t)r * (nkc * KC) + kc0 + 4 * kq_cv;
 #pragma unroll
-        for (int it = 0; it < XPT; ++it) {
-          const int2 e = kt[kk_cv + 2 * it];
-          float x = 0.0f;
-          if (e.x >= 0 && ((yok >> (e.y >> 8)) & (xok >> (e.y & 255)) & 1u))
-            x = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
-                                              xsrc, (xrow_off + e.x) * 4, 0, 0));
-          xr[it] = x;
+        for (int q = 0; q < XPT / 4; ++q)
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            const int2 e = kt[8 * q + j];
+            const int voff = (int)((((tapbad >> e.y) & 1u) << 31) | (unsigned)xrow_off);
+            xr[4 * q + j] = __builtin_bit_cast(float,
+                __builtin_amdgcn_raw_buffer_load_b32(xsrc, voff, e.x, 0));
+          }
+      } else if (CONV) {
+        // this thread gathers k = 4 (kq_cv + 2 q) .. + 3, q = 0 .. 7, of its
+        // pixel.  The tap (ky, kx) and the input offset of k advance in scalar
+        // registers (k is the same for the whole wave); an element outside the
+        // image or beyond the layer's inputs gets an out-of-range buffer offset,
+        // for which the load returns 0 without touching memory.
+        const int khw = va.cg.kh * va.cg.kw, hw_in = va.cg.h * va.cg.w;
+        const int kbase = r * ms.M + kc0;
+        const int nvalid = min(ms.M - kc0, (int)ms.P - kbase);   // valid k of this chunk
+        const int k0 = kbase + 4 * kq_cv;
+        const int ci = k0 / khw;
+        const int tap = k0 - ci * khw;
+        int ky = tap / va.cg.kw, kx = tap - ky * va.cg.kw;
+        int off = (ci * va.cg.h + ky) * va.cg.w + kx;
+        auto step = [&]() {
+          ++off;
+          if (++kx == va.cg.kw) {
+            kx = 0;
+            off += va.cg.w - va.cg.kw;
+            if (++ky == va.cg.kh) {
+              ky = 0;
+              off += hw_in - va.cg.kh * va.cg.w;
+            }
+          }
+        };
+#pragma unroll
+        for (int q = 0; q < XPT / 4; ++q) {
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            const bool kok = 4 * (kq_cv + 2 * q) + j < nvalid;
+            const bool ok = kok && (((yok >> ky) & (xok >> kx)) & 1);
+            xr[4 * q + j] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
+                xsrc, ok ? (xrow_off + off) * 4 : kOob, 0, 0));
+            step();
+          }
+#pragma unroll
+          for (int j = 0; j < 4; ++j) step();   // the other half-wave group's quad
         }
       } else {
+        // lanes along k; a lane beyond the layer's inputs gets an out-of-range
+        // offset (the load returns 0), rows beyond the batch are skipped
         const int km = kc0 + kk_fc;
-        const int64_t p = (int64_t)r * ms.M + km;
-        const bool kok = km < ms.M && p < ms.P;
-        const int voff = (int)((row_fc * va.ldx + p) * 4);
+        const int p = r * ms.M + km;
+        const bool kok = km < ms.M && p < (int)ms.P;
+        const int voff = kok ? (int)((row_fc * va.ldx + p) * 4) : kOob;
 #pragma unroll
         for (int it = 0; it < XPT; ++it) {
           float x = 0.0f;
-          if (kok && row_fc + 4 * it < n_rows)
+          if (row_fc + 4 * it < n_rows)   // uniform over the wave
             x = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
                                               xsrc, voff, (int)(4 * it * va.ldx * 4), 0));
           xr[it] = x;
@@ -212,30 +275,9 @@ __global__ __launch_bounds__(NTHR, 2) void k_xbar_vmm(VmmArgs va) {
       const int rm = e4 % (BN * (KC / 4));
       const int n = rm / (KC / 4), k4 = rm % (KC / 4);
       const int kidx = kc0 + 4 * k4;
-      f32x4 v = f32x4{0.f, 0.f, 0.f, 0.f};
-      if (kidx < ms.Mp) {
-        const int off = (p * tile_elems + (n0 + n) * ms.Mp + 4 * k4) * 4;
-        v = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(gsrc, off, kc0 * 4, 0));
-      }
-      gr[it] = v;
+      const int off = kidx < ms.Mp ? (p * tile_elems + (n0 + n) * ms.Mp + kidx) * 4 : kOob;
+      gr[it] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(gsrc, off, 0, 0));
     }
-  };
-
-  // conv: offset of input element k of stage s relative to (img, iy0, ix0)
-  auto build_ktab = [&](int s) {
-    if (!CONV || tid >= KC) return;
-    const int r = r_begin + s / per_r;
-    const int kc0 = ((s % per_r) % nkc) * KC;
-    const int km = kc0 + tid;
-    const int p = r * ms.M + km;
-    int2 e = make_int2(-1, 0);
-    if (km < ms.M && p < ms.P) {
-      const int khw = va.cg.kh * va.cg.kw;
-      const int ci = p / khw, rr = p - ci * khw;
-      const int ky = rr / va.cg.kw, kx = rr - ky * va.cg.kw;
-      e = make_int2(ci * va.cg.h * va.cg.w + ky * va.cg.w + kx, (ky << 8) | kx);
-    }
-    ktab[s & 1][tid] = e;
   };
 
   auto dac = [&](float x) -> float {
@@ -251,10 +293,14 @@ __global__ __launch_bounds__(NTHR, 2) void k_xbar_vmm(VmmArgs va) {
     const int rem = s % per_r;
     const int ap = rem / nkc;
     if (ap == 0 || nkc > 1) {
+      if (CONV) {
 #pragma unroll
-      for (int it = 0; it < XPT; ++it) {
-        if (CONV) Vs[row_cv * LDK + kk_cv + 2 * it] = dac(xr[it]);
-        else Vs[(row_fc + 4 * it) * LDK + kk_fc] = dac(xr[it]);
+        for (int q = 0; q < XPT / 4; ++q)
+          *(f32x4*)&Vs[row_cv * LDK + 4 * (kq_cv + 2 * q)] =
+              f32x4{dac(xr[4 * q]), dac(xr[4 * q + 1]), dac(xr[4 * q + 2]), dac(xr[4 * q + 3])};
+      } else {
+#pragma unroll
+        for (int it = 0; it < XPT; ++it) Vs[(row_fc + 4 * it) * LDK + kk_fc] = dac(xr[it]);
       }
     }
 #pragma unroll
@@ -278,7 +324,6 @@ __global__ __launch_bounds__(NTHR, 2) void k_xbar_vmm(VmmArgs va) {
       for (int v = 0; v < 4; ++v) { iacc[mt][nt][v] = 0; facc[mt][nt][v] = 0.0f; }
   f32x4 acc[2][MT][NT];
 
-  if (n_stages > 0) build_ktab(0);
   __syncthreads();
   if (n_stages > 0) load_stage(0);
   for (int s = 0; s < n_stages; ++s) {
@@ -287,7 +332,6 @@ __global__ __launch_bounds__(NTHR, 2) void k_xbar_vmm(VmmArgs va) {
     const int ap = rem / nkc, kci = rem % nkc, kc0 = kci * KC;
     __syncthreads();
     store_stage(s);
-    if (s + 1 < n_stages) build_ktab(s + 1);
     __syncthreads();
     if (s + 1 < n_stages) load_stage(s + 1);
     if (kci == 0) {
@@ -406,24 +450,48 @@ __global__ void k_finish(MapScalars ms, PeriphScalars ps, const int32_t* __restr
   }
 }
 
-template <int BN, bool CONV, bool QADC>
+template <int BN, int CV, bool QADC>
 hipError_t launch_t(const VmmArgs& va, dim3 grid, hipStream_t s, bool debug) {
   if (debug)
-    hipLaunchKernelGGL((k_xbar_vmm<BN, CONV, QADC, true>), grid, dim3(NTHR), 0, s, va);
+    hipLaunchKernelGGL((k_xbar_vmm<BN, CV, QADC, true>), grid, dim3(NTHR), 0, s, va);
   else
-    hipLaunchKernelGGL((k_xbar_vmm<BN, CONV, QADC, false>), grid, dim3(NTHR), 0, s, va);
+    hipLaunchKernelGGL((k_xbar_vmm<BN, CV, QADC, false>), grid, dim3(NTHR), 0, s, va);
   return hipGetLastError();
 }
 
 template <int BN>
-hipError_t launch_bn(const VmmArgs& va, dim3 grid, hipStream_t s, bool conv, bool qadc,
+hipError_t launch_bn(const VmmArgs& va, dim3 grid, hipStream_t s, int cv, bool qadc,
                      bool debug) {
-  if (conv) {
-    return qadc ? launch_t<BN, true, true>(va, grid, s, debug)
-                : launch_t<BN, true, false>(va, grid, s, debug);
+  if (cv == 2) {
+    return qadc ? launch_t<BN, 2, true>(va, grid, s, debug)
+                : launch_t<BN, 2, false>(va, grid, s, debug);
   }
-  return qadc ? launch_t<BN, false, true>(va, grid, s, debug)
-              : launch_t<BN, false, false>(va, grid, s, debug);
+  if (cv == 1) {
+    return qadc ? launch_t<BN, 1, true>(va, grid, s, debug)
+                : launch_t<BN, 1, false>(va, grid, s, debug);
+  }
+  return qadc ? launch_t<BN, 0, true>(va, grid, s, debug)
+              : launch_t<BN, 0, false>(va, grid, s, debug);
+}
+
+// Table of the patch columns of a convolution, per row tile r and tile input
+// kk < nkc KC: {byte offset of input p = r M + kk relative to the window of
+// an output pixel, tap ky kw + kx}; kk >= M or p >= P gets tap 31 (no input).
+__global__ void k_conv_ktab(MapScalars ms, ConvGeom cg, int kcp, int2* tab) {
+  const int64_t n = (int64_t)ms.R * kcp;
+  const int khw = cg.kh * cg.kw;
+  for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < n;
+       e += (int64_t)gridDim.x * blockDim.x) {
+    const int r = (int)(e / kcp), kk = (int)(e - (int64_t)r * kcp);
+    const int64_t p = (int64_t)r * ms.M + kk;
+    int2 v = make_int2(0, 31);
+    if (kk < ms.M && p < ms.P) {
+      const int ci = (int)(p / khw), tap = (int)(p - (int64_t)ci * khw);
+      const int ky = tap / cg.kw, kx = tap - ky * cg.kw;
+      v = make_int2(((ci * cg.h + ky) * cg.w + kx) * 4, tap);
+    }
+    tab[e] = v;
+  }
 }
 
 int pick_bn(int Np) {
@@ -477,10 +545,24 @@ hipError_t launch_xbar_vmm(const MapScalars& ms, const PeriphScalars& ps, const 
             (unsigned)((ms.R + va.r_per_split - 1) / va.r_per_split));
   const bool qadc = ps.adc_bits > 0;
   const bool debug = vl.dbg_I != nullptr || vl.dbg_code != nullptr;
-  const bool conv = vl.conv != nullptr;
-  if (bn == 64) return launch_bn<64>(va, grid, s, conv, qadc, debug);
-  if (bn == 32) return launch_bn<32>(va, grid, s, conv, qadc, debug);
-  return launch_bn<16>(va, grid, s, conv, qadc, debug);
+  const int cv = vl.conv == nullptr ? 0 : (vl.ktab ? 2 : 1);
+  va.ktab = vl.ktab;
+  if (bn == 64) return launch_bn<64>(va, grid, s, cv, qadc, debug);
+  if (bn == 32) return launch_bn<32>(va, grid, s, cv, qadc, debug);
+  return launch_bn<16>(va, grid, s, cv, qadc, debug);
+}
+
+int ktab_entries(const MapScalars& ms) { return ms.R * (((ms.Mp + KC - 1) / KC) * KC); }
+
+hipError_t launch_conv_ktab(const MapScalars& ms, const rxnn_conv_desc& cd, int2* tab,
+                            hipStream_t s) {
+  ConvGeom cg{cd.c_in, cd.h, cd.w, cd.kh, cd.kw, cd.stride, cd.pad, 0, 0};
+  const int kcp = ((ms.Mp + KC - 1) / KC) * KC;
+  const int64_t n = (int64_t)ms.R * kcp;
+  int64_t blocks = (n + 255) / 256;
+  if (blocks > 1024) blocks = 1024;
+  hipLaunchKernelGGL(k_conv_ktab, dim3((unsigned)blocks), dim3(256), 0, s, ms, cg, kcp, tab);
+  return hipGetLastError();
 }
 
 hipError_t launch_finish(const MapScalars& ms, const PeriphScalars& ps, const int32_t* iacc,
