@@ -34,12 +34,17 @@ from . import periph as pp
 from .mapping import array_weight
 
 
-def crossbar_vmm(X, layer, params, periph, rows=None, col_tiles=None, debug=False):
+def crossbar_vmm(X, layer, params, periph, rows=None, col_tiles=None, debug=False,
+                 row_tiles=None):
     """Evaluate one FC layer.  X is [B, P] fp32; returns Y [len(rows), Q].
 
     Only the column tiles in ``col_tiles`` (default: all) are computed; other
     output columns are NaN.  ``layer`` comes from ``mapping.map_layer`` and must
     hold G' for every row tile of those column tiles.
+    ``row_tiles`` (default: all) restricts the evaluation to inputs that are
+    zero outside those row tiles: every other row tile then carries V = 0,
+    hence I = 0 and code 0 (the first threshold is positive), and adds
+    nothing; this is checked, and their G' is not needed.
     With ``debug`` also returns {(r, c, a): (I fp64, codes)}.
     """
     X = np.asarray(X, dtype=np.float32)
@@ -59,9 +64,14 @@ def crossbar_vmm(X, layer, params, periph, rows=None, col_tiles=None, debug=Fals
         scale = pp.ideal_output_scale(periph, layer["s_w_eff"])
     Y = np.full((B, Q), np.nan, dtype=np.float32 if quant else np.float64)
     dbg = {}
+    if row_tiles is not None:
+        if quant:
+            assert thr[0] > 0.0
+        for r in set(range(R)) - set(row_tiles):
+            assert not V[:, r * M:(r + 1) * M].any(), "inputs outside row_tiles must be zero"
     for c in (range(C) if col_tiles is None else col_tiles):
         acc = np.zeros((B, N), dtype=np.int64 if quant else np.float64)
-        for r in range(R):
+        for r in (range(R) if row_tiles is None else sorted(row_tiles)):
             Vr = V[:, r * M:(r + 1) * M]
             for a in range(A):
                 I = Vr @ layer["gp"][(r, c)][a]
@@ -106,11 +116,17 @@ def im2col(X, conv, images=None):
     return cols.reshape(n * ho * wo, ci * kh * kw)
 
 
-def conv_layer(X, layer, params, periph, conv, images=None, col_tiles=None):
+def conv_layer(X, layer, params, periph, conv, images=None, col_tiles=None, row_tiles=None,
+               debug=False):
     """Evaluate one conv layer mapped from ``W = weight.reshape(c_out, -1).T``.
-    Returns NCHW output for the selected images."""
+    Returns NCHW output for the selected images (and with ``debug`` the
+    per-array currents and codes of ``crossbar_vmm`` over the patch rows)."""
     cols = im2col(X, conv, images)
-    Y = crossbar_vmm(cols, layer, params, periph, col_tiles=col_tiles)
+    Y = crossbar_vmm(cols, layer, params, periph, col_tiles=col_tiles, row_tiles=row_tiles,
+                     debug=debug)
+    if debug:
+        Y, dbg = Y
     n = cols.shape[0] // int(np.prod(conv_out_hw(conv)))
     ho, wo = conv_out_hw(conv)
-    return Y.reshape(n, ho, wo, -1).transpose(0, 3, 1, 2)
+    Y = Y.reshape(n, ho, wo, -1).transpose(0, 3, 1, 2)
+    return (Y, dbg) if debug else Y

@@ -25,7 +25,9 @@ Step 2 (W -> G), for a linear device between ``g_min`` and ``g_max``:
   crossbar with its own ADCs; the arrays are combined digitally with weight
   ``(+1 | -1) * 2^(s_b s)``.
 
-Step 3 (G -> G'): ``network.gprime_nodal`` per array.
+Step 3 (G -> G'): ``network.gprime_nodal`` per array, or for arrays above
+32 x 32 with positive wire and sense resistances ``network.gprime_rowsweep``
+(the same equations, eliminated row by row; the two agree to ~1e-12).
 
 Parity status: tiling and W->G are exact integer/fp64 definitions; pinned by
 the recombination identity ``sum_s 2^(s_b s) (G+_s - G-_s) = dG q sign(w)``
@@ -38,7 +40,7 @@ import math
 
 import numpy as np
 
-from .network import gprime_nodal
+from .network import gprime_nodal, gprime_rowsweep
 
 PARAM_KEYS = ("rows", "cols", "g_min", "g_max", "r_driver", "r_sense", "r_row",
               "r_col", "weight_bits", "bits_per_slice", "w_max")
@@ -124,6 +126,16 @@ def array_conductances(frag, params, w_max):
     return out
 
 
+def array_gprime(G, params):
+    """Step 3 for one array: the nodal solve, or the row sweep for large
+    arrays whose wire and sense resistances are positive."""
+    res = (params["r_driver"], params["r_sense"], params["r_row"], params["r_col"])
+    sweep_ok = params["r_row"] > 0 and params["r_col"] > 0 and params["r_sense"] > 0
+    if sweep_ok and G.shape[0] * G.shape[1] > 32 * 32:
+        return gprime_rowsweep(G, *res)
+    return gprime_nodal(G, *res)
+
+
 def map_layer(W, params, col_tiles=None, row_tiles=None):
     """Model generation for one layer (steps 1-3).
 
@@ -141,10 +153,7 @@ def map_layer(W, params, col_tiles=None, row_tiles=None):
     for c in cols:
         for r in rows:
             G = array_conductances(tile_weights(W, params, r, c), params, w_max)
-            gp[(r, c)] = np.stack([
-                gprime_nodal(G[a], params["r_driver"], params["r_sense"],
-                             params["r_row"], params["r_col"])
-                for a in range(G.shape[0])])
+            gp[(r, c)] = np.stack([array_gprime(G[a], params) for a in range(G.shape[0])])
     return {"gp": gp, "P": P, "Q": Q, "M": M, "N": N, "R": R, "C": C,
             "A": arrays_per_position(params), "w_max": w_max,
             "s_w_eff": effective_weight_scale(params, w_max)}

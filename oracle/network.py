@@ -35,11 +35,18 @@ node_voltages(G, Vin, ...)  The node voltages of the same nodal solve, used by
                        the sneak-path example of Sec. IV-A.
 gprime_paper(G, ...)   The paper's Eqs. 2-14, dense.  Pinned by the same tests
                        and against ``gprime_nodal``.
+gprime_rowsweep(G, ...)  The same nodal equations solved row by row (block
+                       tridiagonal elimination), O(M N^3): the oracle for
+                       large arrays.  Needs positive wire and sense
+                       resistances.  Pinned against ``gprime_nodal`` and the
+                       exact rational solutions, and by the network
+                       invariants at 128 x 128.
 """
 
 from __future__ import annotations
 
 import numpy as np
+import scipy.linalg as sla
 import scipy.sparse as sp
 import scipy.sparse.linalg as spla
 
@@ -236,3 +243,68 @@ def gprime_paper(G, r_driver, r_sense, r_row, r_col):
         for i in range(M):
             netmatC[:, i] += netmat[:, j * M + i]
     return netmatC.T                                         # Eq. 14
+
+
+# ---------------------------------------------------------------------------
+# Row sweep of the nodal equations (large arrays)
+# ---------------------------------------------------------------------------
+
+def gprime_rowsweep(G, r_driver, r_sense, r_row, r_col):
+    """G' from the KCL equations of ``_solve_nodal``, eliminated one row at a
+    time.
+
+    Row i's nodes a[i, :] form a chain: KCL there reads
+    ``T_i a_i = g_in Vin_i e_0 + D_i b_i`` with ``D_i = diag(G[i, :])`` and
+    ``T_i`` the chain's tridiagonal conductance matrix (``g_in = 1 / (r_driver
+    + r_row)`` to the source at node 0, ``1 / r_row`` between neighbours) plus
+    ``D_i``.  Substituting ``a_i`` into KCL at the column nodes b[i, :] leaves
+    a block tridiagonal system in the b rows:
+
+        ``(S_i + g_col n_i I + [i = M-1] g_sense I) b_i - g_col b_(i-1)
+          - g_col b_(i+1) = f_i Vin_i``
+
+    with ``S_i = D_i - D_i T_i^-1 D_i``, ``f_i = g_in D_i T_i^-1 e_0`` and
+    ``n_i`` the number of column segments at row i.  Forward elimination over
+    the rows carries every source pattern ``Vin = e_k`` at once; the last row
+    gives ``G'[k, j] = b_(M-1, j) / r_sense``.  fp64, M x N.
+    """
+    G = np.asarray(G, dtype=np.float64)
+    M, N = G.shape
+    if np.any(G <= 0):
+        raise ValueError("device conductances must be positive")
+    if not (r_row > 0 and r_col > 0 and r_sense > 0 and r_driver >= 0):
+        raise ValueError("the row sweep needs positive wire and sense resistances")
+    g_in, g_r, g_c, g_s = 1.0 / (r_driver + r_row), 1.0 / r_row, 1.0 / r_col, 1.0 / r_sense
+    # chain conductance matrix of one row without the devices, in the banded
+    # storage of scipy.linalg.solve_banded: (upper, diagonal, lower)
+    lap_diag = np.zeros(N)
+    lap_diag[0] += g_in
+    lap_diag[:-1] += g_r
+    lap_diag[1:] += g_r
+    band = np.zeros((3, N))
+    band[0, 1:] = -g_r
+    band[2, :-1] = -g_r
+    rhs_e0 = np.zeros((N, N + 1))
+    A_prev_inv = None
+    rhs = None          # N x M: the eliminated right-hand side of every pattern
+    for i in range(M):
+        band[1] = lap_diag + G[i]
+        rhs_e0[:, :N] = np.diag(G[i])
+        rhs_e0[:, N] = 0.0
+        rhs_e0[0, N] = 1.0
+        sol = sla.solve_banded((1, 1), band, rhs_e0)     # T_i^-1 [D_i | e_0]
+        S = np.diag(G[i]) - G[i][:, None] * sol[:, :N]
+        f = g_in * (G[i] * sol[:, N])
+        n_seg = (1 if i > 0 else 0) + (1 if i + 1 < M else 0)
+        A = S + g_c * n_seg * np.eye(N)
+        if i == M - 1:
+            A += g_s * np.eye(N)
+        r_i = np.zeros((N, M))
+        r_i[:, i] = f
+        if i > 0:
+            A = A - g_c * g_c * A_prev_inv
+            r_i = r_i + g_c * (A_prev_inv @ rhs)
+        A_prev_inv = np.linalg.inv(A)
+        rhs = r_i
+    b_last = A_prev_inv @ rhs            # N x M: b[M-1, j] for pattern e_k
+    return (g_s * b_last).T

@@ -96,9 +96,11 @@ __global__ __launch_bounds__(NTHR, 2) void k_xbar_vmm(VmmArgs va) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int g = lane >> 4, li = lane & 15;
   const int64_t b0 = (int64_t)blockIdx.x * BM;
+  // column blocks: every block of a full column tile, and of the last tile
+  // only those that hold real output columns (padded columns are discarded)
   const int nblk_per_tile = ms.Np / BN;
-  const int c = blockIdx.y / nblk_per_tile;
-  const int n0 = (blockIdx.y % nblk_per_tile) * BN;
+  const int c = min((int)blockIdx.y / nblk_per_tile, ms.C - 1);
+  const int n0 = ((int)blockIdx.y - c * nblk_per_tile) * BN;
   const int r_begin = blockIdx.z * va.r_per_split;
   const int r_end = min(ms.R, r_begin + va.r_per_split);
 
@@ -181,19 +183,32 @@ __global__ __launch_bounds__(NTHR, 2) void k_xbar_vmm(VmmArgs va) {
   }
 
   const int n_pairs = ms.A / 2;
+  // Stages run over (row tile, pair, chunk).  Chunks that hold only padded
+  // inputs (V = 0) are skipped: only the last row tile has them.
   const int nkc = (ms.Mp + KC - 1) / KC;
+  const int nkc_last = min(nkc, (int)((ms.P - (int64_t)(ms.R - 1) * ms.M + KC - 1) / KC));
   const int per_r = n_pairs * nkc;
-  const int n_stages = (r_end - r_begin) * per_r;
+  const int n_stages = r_end == ms.R ? (r_end - 1 - r_begin) * per_r + n_pairs * nkc_last
+                                     : (r_end - r_begin) * per_r;
+  // stage s -> row tile r, pair ap, chunk kci of the nk chunks of r
+  auto decode = [&](int s, int& r, int& ap, int& kci, int& nk) {
+    const int rr = s / per_r;
+    const int rem = s - rr * per_r;
+    r = r_begin + rr;
+    nk = r == ms.R - 1 ? nkc_last : nkc;
+    ap = rem / nk;
+    kci = rem - ap * nk;
+  };
   const int tile_elems = ms.Np * ms.Mp;
 
   float xr[XPT];
   f32x4 gr[GV4];
 
   auto load_stage = [&](int s) {
-    const int r = r_begin + s / per_r;
-    const int rem = s % per_r;
-    const int ap = rem / nkc, kc0 = (rem % nkc) * KC;
-    if (ap == 0 || nkc > 1) {
+    int r, ap, kci, nk;
+    decode(s, r, ap, kci, nk);
+    const int kc0 = kci * KC;
+    if (ap == 0 || nk > 1) {
       if (CV == 2) {
         // this thread gathers k = 4 (kq_cv + 2 q) .. + 3, q = 0 .. 7, of its
         // pixel.  The table gives, per k, the byte offset of the input element
@@ -290,9 +305,9 @@ __global__ __launch_bounds__(NTHR, 2) void k_xbar_vmm(VmmArgs va) {
   };
 
   auto store_stage = [&](int s) {
-    const int rem = s % per_r;
-    const int ap = rem / nkc;
-    if (ap == 0 || nkc > 1) {
+    int r, ap, kci, nk;
+    decode(s, r, ap, kci, nk);
+    if (ap == 0 || nk > 1) {
       if (CONV) {
 #pragma unroll
         for (int q = 0; q < XPT / 4; ++q)
@@ -327,9 +342,9 @@ __global__ __launch_bounds__(NTHR, 2) void k_xbar_vmm(VmmArgs va) {
   __syncthreads();
   if (n_stages > 0) load_stage(0);
   for (int s = 0; s < n_stages; ++s) {
-    const int r = r_begin + s / per_r;
-    const int rem = s % per_r;
-    const int ap = rem / nkc, kci = rem % nkc, kc0 = kci * KC;
+    int r, ap, kci, nk;
+    decode(s, r, ap, kci, nk);
+    const int kc0 = kci * KC;
     __syncthreads();
     store_stage(s);
     __syncthreads();
@@ -364,7 +379,7 @@ __global__ __launch_bounds__(NTHR, 2) void k_xbar_vmm(VmmArgs va) {
                   af[mt][ss], bf[nt][ss], acc[p][mt][nt], 0, 0, 0);
       }
     }
-    if (kci != nkc - 1) continue;
+    if (kci != nk - 1) continue;
 
     // ---- ADC and digital accumulation -------------------------------------
     const int wpos = 1 << (ms.slice_bits * ap);
@@ -504,7 +519,10 @@ int pick_bn(int Np) {
 
 int choose_splits(const MapScalars& ms, const PeriphScalars& ps, int64_t Bv) {
   if (ps.adc_bits == 0 || ms.R < 2) return 1;
-  const int64_t blocks = ((Bv + BM - 1) / BM) * (int64_t)ms.C * (ms.Np / pick_bn(ms.Np));
+  const int bn = pick_bn(ms.Np);
+  const int64_t col_blocks = (int64_t)(ms.C - 1) * (ms.Np / bn) +
+                             (ms.Q - (int64_t)(ms.C - 1) * ms.N + bn - 1) / bn;
+  const int64_t blocks = ((Bv + BM - 1) / BM) * col_blocks;
   if (blocks >= 512) return 1;
   int64_t want = (1024 + blocks - 1) / blocks;
   if (want > ms.R) want = ms.R;
@@ -541,10 +559,13 @@ hipError_t launch_xbar_vmm(const MapScalars& ms, const PeriphScalars& ps, const 
   va.dbg_code = vl.dbg_code;
   va.r_per_split = (ms.R + splits - 1) / splits;
   const int bn = pick_bn(ms.Np);
-  dim3 grid((unsigned)((vl.Bv + BM - 1) / BM), (unsigned)(ms.C * (ms.Np / bn)),
+  // the debug entry reports the currents of every column, padded ones included
+  const bool debug = vl.dbg_I != nullptr || vl.dbg_code != nullptr;
+  const int64_t q_last = ms.Q - (int64_t)(ms.C - 1) * ms.N;   // real columns of the last tile
+  const int blk_last = debug ? ms.Np / bn : (int)((q_last + bn - 1) / bn);
+  dim3 grid((unsigned)((vl.Bv + BM - 1) / BM), (unsigned)((ms.C - 1) * (ms.Np / bn) + blk_last),
             (unsigned)((ms.R + va.r_per_split - 1) / va.r_per_split));
   const bool qadc = ps.adc_bits > 0;
-  const bool debug = vl.dbg_I != nullptr || vl.dbg_code != nullptr;
   const int cv = vl.conv == nullptr ? 0 : (vl.ktab ? 2 : 1);
   va.ktab = vl.ktab;
   if (bn == 64) return launch_bn<64>(va, grid, s, cv, qadc, debug);

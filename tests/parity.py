@@ -2,8 +2,8 @@
 
 * G' per element: relative error <= GP_RTOL (fp64 build rounded to fp32).
 * Pre-ADC currents: relative error <= I_RTOL.  V >= 0 and G' >= 0, so no
-  cancellation happens inside a current; fp32 accumulation over M <= 64 terms
-  stays far below this bound.
+  cancellation happens inside a current; fp32 accumulation over M <= 256
+  terms (worst case about M 2^-24 = 1.5e-5) stays below this bound.
 * ADC codes: identical, except a fraction <= FLIP_FRAC of codes that differ
   by exactly one, and only where the oracle current lies within I_RTOL of the
   threshold separating the two codes (fp32 rounding of a current that sits on
@@ -60,6 +60,39 @@ def check_codes(codes_gpu, codes_oracle, I_oracle, thresholds, max_frac=FLIP_FRA
     frac = n / max(codes_oracle.size, 1)
     assert frac <= max_frac, f"{frac:.3g} of codes flipped"
     return flip
+
+
+def check_outputs_by_codes(Y_gpu, dbg, weights, thresholds, scale,
+                           max_frac=FLIP_FRAC, rtol=I_RTOL):
+    """Layer outputs of the production path against the oracle's per-array
+    currents and codes (``dbg`` = {(r, a): (I [S, n], code [S, n])} for the
+    sampled outputs).
+
+    The GPU output is fp32(acc) * scale with an integer acc, so acc is read
+    back exactly.  acc_gpu - acc_oracle must be explained by codes at a
+    threshold: its magnitude is at most the summed |weight| of the oracle
+    codes whose current lies within rtol of a threshold.  Every nonzero
+    difference needs at least one flip, so their count must stay within
+    max_frac of the codes behind the sample."""
+    Y_gpu = np.asarray(Y_gpu, dtype=np.float32)
+    t = np.asarray(thresholds, dtype=np.float64)
+    acc_o = 0
+    slack = 0
+    n_codes = 0
+    for (r, a), (I, code) in dbg.items():
+        acc_o = acc_o + weights[a] * code.astype(np.int64)
+        k = np.clip(np.searchsorted(t, I), 1, len(t) - 1)      # nearest thresholds
+        near = np.minimum(np.abs(I - t[k - 1]), np.abs(I - t[k])) <= rtol * np.abs(I)
+        slack = slack + abs(int(weights[a])) * near
+        n_codes += I.size
+    acc_g = np.rint(Y_gpu.astype(np.float64) / float(scale)).astype(np.int64)
+    assert np.array_equal((acc_g.astype(np.float32) * np.float32(scale)), Y_gpu), \
+        "GPU output is not fp32(integer) * scale"
+    d = acc_g - acc_o
+    assert np.all(np.abs(d) <= slack), "an output differs by more than its threshold codes allow"
+    n_diff = int(np.count_nonzero(d))
+    assert n_diff <= max_frac * n_codes, f"{n_diff} differing outputs for {n_codes} codes"
+    return n_diff, n_codes
 
 
 def array_weights(A, slice_bits):

@@ -84,6 +84,11 @@ def compare_fc_debug(W, X, xb, pp, label):
     # and equal the oracle wherever no contributing code flipped
     any_flip = flipped.any(axis=(0, 2)).transpose(1, 0, 2).reshape(B, Cn * N)[:, :W.shape[1]]
     np.testing.assert_array_equal(Y[~any_flip], Yo[~any_flip])
+    # the production entry (padded chunks and column blocks skipped, row tiles
+    # possibly split) gives the same outputs bit for bit
+    say(label, "crossbar_vmm")
+    Yp = rxnn.crossbar_vmm(L, pp, dev(X)).cpu().numpy()
+    np.testing.assert_array_equal(Yp, Y)
     return L, Y, Yo
 
 
@@ -180,6 +185,8 @@ def test_fc_256x128_parity():
     (50, 40, 16, 16, 1, 8, 8),        # one row
     (90, 33, 32, 32, 257, 6, 6),      # N = 32 path, three batch blocks
     (60, 20, 13, 10, 37, 3, 5),       # N = 10 -> 16-wide path
+    (100, 70, 256, 256, 33, 8, 8),    # one 256 x 256 tile: padded chunks and column blocks
+    (300, 130, 128, 128, 20, 8, 8),   # last row tile 44 inputs, last column tile 2 outputs
 ])
 def test_fc_ragged(P, Q, M, N, B, dac, adc):
     W, X, xb, pp = fc_case(P, Q, M, N, B, dac=dac, adc=adc)
@@ -310,6 +317,8 @@ def conv_compare(cv, W, X, xb, pp, images=None, label="conv"):
     (1, 3, 10, 40, 5, 2, 2, 32, 32, 8),
     (2, 6, 7, 9, 1, 1, 0, 13, 10, 6),
     (2, 5, 9, 7, 3, 1, 1, 16, 16, 0),      # ideal DAC: fp32 patches
+    (2, 3, 20, 16, 7, 2, 3, 32, 32, 8),    # 7x7 stride 2: taps decomposed in the kernel
+    (1, 4, 12, 70, 6, 1, 2, 64, 64, 6),    # 6x6 (36 taps), padded column tile
 ])
 def test_conv_small(n, c_in, hw, c_out, k, s, p, M, N, dac):
     rng = np.random.default_rng(n * 100 + c_in)

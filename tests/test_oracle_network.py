@@ -10,7 +10,7 @@ from fractions import Fraction as Fr
 import numpy as np
 import pytest
 
-from oracle.network import gprime_nodal, gprime_paper, node_voltages
+from oracle.network import gprime_nodal, gprime_paper, gprime_rowsweep, node_voltages
 
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
 
@@ -109,7 +109,7 @@ def test_exact_rational_tiny(M, N):
     ref = np.array([[float(v) for v in row] for row in e1])
     G = np.array([[float(v) for v in row] for row in Gq])
     res = tuple(float(r) for r in RES_EXACT)
-    for fn in (gprime_nodal, gprime_paper):
+    for fn in (gprime_nodal, gprime_paper, gprime_rowsweep):
         got = fn(G, *res)
         assert np.max(np.abs(got - ref) / np.abs(ref)) < 1e-12, fn.__name__
 
@@ -161,7 +161,7 @@ def test_driver_only_is_divider(fn, Grand):
     np.testing.assert_allclose(fn(Grand, Rd, 0.0, 0.0, 0.0), want, rtol=1e-13)
 
 
-@pytest.mark.parametrize("fn", [gprime_nodal, gprime_paper])
+@pytest.mark.parametrize("fn", [gprime_nodal, gprime_paper, gprime_rowsweep])
 def test_one_by_one(fn):
     G = np.array([[3.3e-5]])
     # a 1x1 array has no column segment: source, R_d + r_row, device, R_sense
@@ -230,14 +230,14 @@ def _column_ladder(Gs, rd, rr, rc, rs):
     return out
 
 
-@pytest.mark.parametrize("fn", [gprime_nodal, gprime_paper])
+@pytest.mark.parametrize("fn", [gprime_nodal, gprime_paper, gprime_rowsweep])
 def test_row_ladder(fn):
     Gs = np.random.default_rng(3).uniform(5e-6, 5e-5, 9)
     got = fn(Gs[None, :], 1000.0, 800.0, 2.5, 77.0)    # r_col unused for M = 1
     np.testing.assert_allclose(got, _row_ladder(Gs, 1000.0, 2.5, 800.0), rtol=1e-12)
 
 
-@pytest.mark.parametrize("fn", [gprime_nodal, gprime_paper])
+@pytest.mark.parametrize("fn", [gprime_nodal, gprime_paper, gprime_rowsweep])
 def test_column_ladder(fn):
     Gs = np.random.default_rng(4).uniform(5e-6, 5e-5, 8)
     got = fn(Gs[:, None], 1000.0, 900.0, 2.5, 30.0)
@@ -249,6 +249,40 @@ def test_nodal_matches_paper_32x32():
     a = gprime_nodal(G, 1000.0, 1000.0, 2.5, 2.5)
     b = gprime_paper(G, 1000.0, 1000.0, 2.5, 2.5)
     assert np.max(np.abs(a - b) / a) < 1e-11
+
+
+@pytest.mark.parametrize("M,N,res", [
+    (1, 17, (1000.0, 1000.0, 2.5, 2.5)),
+    (19, 1, (1000.0, 1000.0, 2.5, 2.5)),
+    (13, 29, (1000.0, 1000.0, 2.5, 2.5)),
+    (40, 33, (0.0, 1000.0, 1.0, 5.0)),
+    (64, 64, (1000.0, 1000.0, 1.0, 1.0)),
+])
+def test_rowsweep_matches_nodal(M, N, res):
+    """The row sweep (large-array oracle) solves the same KCL equations as the
+    nodal solve by a different elimination."""
+    G = np.random.default_rng(M * 100 + N).uniform(5e-6, 5e-5, size=(M, N))
+    a = gprime_nodal(G, *res)
+    b = gprime_rowsweep(G, *res)
+    assert np.max(np.abs(a - b) / a) < 1e-9
+
+
+def test_rowsweep_rejects_zero_wire():
+    with pytest.raises(ValueError):
+        gprime_rowsweep(np.full((3, 3), 1e-5), 1000.0, 1000.0, 0.0, 2.5)
+
+
+def test_rowsweep_invariants_128():
+    """At 128 x 128 (the size of the stacked workloads): positivity, the row
+    and column sum bounds, and Rayleigh monotonicity of 1^T G' 1 in the wire
+    resistance."""
+    G = np.random.default_rng(13).uniform(5e-6, 5e-5, size=(128, 128))
+    gp = gprime_rowsweep(G, 1000.0, 1000.0, 1.0, 1.0)
+    assert np.all(gp > 0)
+    assert np.all(gp.sum(axis=1) <= G.sum(axis=1))
+    assert np.all(gp.sum(axis=0) <= G.sum(axis=0))
+    gp2 = gprime_rowsweep(G, 1000.0, 1000.0, 2.5, 2.5)
+    assert gp2.sum() < gp.sum()
 
 
 # ---------------------------------------------------------------------------
