@@ -133,11 +133,12 @@ rxnn_status make_periph(const rxnn_periph_params* pp, const MapScalars& ms, Peri
   ps.i_fs = pp->v_read * (double)ms.M * ms.g_max;
   if (pp->adc_bits) {
     ps.lsb = ps.i_fs / (double)ps.adc_levels;
-    // bucket width <= a quarter of the smallest threshold spacing
-    // (1 - |bend|) I_FS / L, so a bucket's code is within one of the exact one
-    const double need = 4.0 * ps.adc_levels / (1.0 - fabs(pp->adc_bend));
-    int nb = 16;
-    while (nb < need) nb <<= 1;
+    // bucket width w <= 1 / 3.25 of the smallest threshold spacing
+    // (1 - |bend|) I_FS / L: a current rounded into a neighbouring bucket
+    // still leaves at most one threshold between the bucket's lower edge and
+    // the current, so the bucket's code is exact or one too low
+    const double need = 3.25 * ps.adc_levels / (1.0 - fabs(pp->adc_bend));
+    const int nb = (int)ceil(need) < 16 ? 16 : (int)ceil(need);
     if (nb > kMaxBuckets) return fail(RXNN_EINVAL, "ADC bucket table too large");
     ps.n_buckets = nb;
     ps.bucket_inv_w = (float)((double)nb / ps.i_fs);
@@ -185,11 +186,31 @@ rxnn_status check_acc_range(const MapScalars& ms, const PeriphScalars& ps) {
 rxnn_status run_vmm(const rxnn_layer* L, const PeriphScalars& ps, const float* X,
                     const rxnn_conv_desc* conv, int64_t ldx, int64_t Bv, float* Y,
                     int64_t hw_out, float* dbgI, int32_t* dbgC, hipStream_t s,
-                    int32_t* iacc_ws, const int2* ktab = nullptr) {
+                    int32_t* iacc_ws, const int* ktab = nullptr) {
   const MapScalars& ms = L->ms;
   const int splits = (dbgI || dbgC) ? 1 : choose_splits(ms, ps, Bv);
+  // DAC of every input into the layer's V buffer (padded for a convolution)
+  const int64_t n_v = dac_elems(conv, Bv, ldx);
+  if ((size_t)n_v * sizeof(float) > L->vbuf_bytes) {
+    rxnn_layer* Lm = const_cast<rxnn_layer*>(L);
+    if (Lm->vbuf) HIP_TRY(hipFree(Lm->vbuf));
+    Lm->vbuf = nullptr;
+    Lm->vbuf_bytes = 0;
+    void* p = nullptr;
+    if (hipMalloc(&p, (size_t)n_v * sizeof(float)) != hipSuccess) {
+      (void)hipGetLastError();
+      return fail(RXNN_ENOMEM, "cannot allocate %zu bytes for the DAC output",
+                  (size_t)n_v * sizeof(float));
+    }
+    Lm->vbuf = (float*)p;
+    Lm->vbuf_bytes = (size_t)n_v * sizeof(float);
+  }
+  {
+    ProfScope t("dac", s);
+    HIP_TRY(launch_dac(ps, conv, X, L->vbuf, n_v, s));
+  }
   VmmLaunch vl;
-  vl.X = X;
+  vl.V = L->vbuf;
   vl.conv = conv;
   vl.ldx = ldx;
   vl.Bv = Bv;
@@ -445,8 +466,6 @@ rxnn_status rxnn_conv_layer(const rxnn_layer* layer, const rxnn_periph_params* p
     return fail(RXNN_EINVAL, "invalid convolution shape");
   if (cd.h + 2 * cd.pad < cd.kh || cd.w + 2 * cd.pad < cd.kw)
     return fail(RXNN_EINVAL, "kernel larger than the padded input");
-  if (cd.kh > 32 || cd.kw > 32)
-    return fail(RXNN_EUNSUPPORTED, "kernel sides above 32 are not supported");
 
   rxnn_layer* L = const_cast<rxnn_layer*>(layer);
   const MapScalars& ms = L->ms;
@@ -466,7 +485,8 @@ rxnn_status rxnn_conv_layer(const rxnn_layer* layer, const rxnn_periph_params* p
     // the images one 128-pixel block of the evaluation kernel reads are
     // addressed with 32-bit byte offsets
     const int64_t span = std::min<int64_t>(cd.n, 127 / (ho * wo) + 2);
-    if ((span * cd.c_in * cd.h * cd.w + (int64_t)cd.pad * (cd.w + 1)) * 4 >= (int64_t)1 << 31)
+    if (span * cd.c_in * (cd.h + 2 * (int64_t)cd.pad) * (cd.w + 2 * (int64_t)cd.pad) * 4 >=
+        (int64_t)1 << 31)
       return fail(RXNN_EUNSUPPORTED, "input images too large for the evaluation kernel");
   }
   if (Bv == 0) return RXNN_OK;
@@ -479,11 +499,10 @@ rxnn_status rxnn_conv_layer(const rxnn_layer* layer, const rxnn_periph_params* p
     if ((st = grow_ws(L, (size_t)Bv * ms.Q * sizeof(int32_t)))) return st;
     iacc = (int32_t*)L->ws;
   }
-  // patch-column table (per row tile and input: offset in the window, tap),
-  // rebuilt when the geometry changes; taps are numbered below 31
-  const int2* ktab = nullptr;
-  if (cd.kh * cd.kw <= 31) {
-    const int key[5] = {cd.c_in, cd.h, cd.w, cd.kh, cd.kw};
+  // patch-column table (per row tile and input: byte offset in the window of
+  // the padded input), rebuilt when the geometry changes
+  {
+    const int key[6] = {cd.c_in, cd.h, cd.w, cd.kh, cd.kw, cd.pad};
     const int64_t n = ktab_entries(ms);
     if (!L->ktab || memcmp(key, L->ktab_key, sizeof key) != 0) {
       if (L->ktab_cap < n) {
@@ -491,11 +510,11 @@ rxnn_status rxnn_conv_layer(const rxnn_layer* layer, const rxnn_periph_params* p
         L->ktab = nullptr;
         L->ktab_cap = 0;
         void* p = nullptr;
-        if (hipMalloc(&p, (size_t)n * sizeof(int2)) != hipSuccess) {
+        if (hipMalloc(&p, (size_t)n * sizeof(int)) != hipSuccess) {
           (void)hipGetLastError();
           return fail(RXNN_ENOMEM, "cannot allocate the patch-column table");
         }
-        L->ktab = (int2*)p;
+        L->ktab = (int*)p;
         L->ktab_cap = n;
       }
       {
@@ -504,8 +523,8 @@ rxnn_status rxnn_conv_layer(const rxnn_layer* layer, const rxnn_periph_params* p
       }
       memcpy(L->ktab_key, key, sizeof key);
     }
-    ktab = L->ktab;
   }
+  const int* ktab = L->ktab;
   return run_vmm(L, ps, X, &cd, 0, Bv, Y, ho * wo, nullptr, nullptr, s, iacc, ktab);
 }
 
@@ -585,6 +604,7 @@ void rxnn_free_layer(rxnn_layer* layer) {
   if (layer->ws) (void)hipFree(layer->ws);
   if (layer->nd_ws) (void)hipFree(layer->nd_ws);
   if (layer->ktab) (void)hipFree(layer->ktab);
+  if (layer->vbuf) (void)hipFree(layer->vbuf);
   layer->magic = 0;
   delete layer;
 }

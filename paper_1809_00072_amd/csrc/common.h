@@ -57,9 +57,11 @@ struct rxnn_layer {
   double* nd_ws;       // nested-dissection build workspace (null: row sweep)
   int64_t nd_chunk;    // arrays built per pass over the workspace
   int nd_bs;           // side of the blocks reduced in LDS
-  int2* ktab;          // patch-column table of the last convolution geometry (or null)
+  int* ktab;           // patch-column table of the last convolution geometry (or null)
   int64_t ktab_cap;    // entries allocated
-  int ktab_key[5];     // c_in, h, w, kh, kw the table was built for
+  int ktab_key[6];     // c_in, h, w, kh, kw, pad the table was built for
+  float* vbuf;         // DAC output of the current call (padded for a convolution)
+  size_t vbuf_bytes;
 };
 
 namespace rxnn {
@@ -78,7 +80,7 @@ hipError_t launch_nd_build(const MapScalars& ms, const float* W, float* gpt, int
                            int64_t n, int bs, double* ws, hipStream_t s);
 
 struct VmmLaunch {
-  const float* X;       // FC: Bv x ldx rows; conv: the NCHW input
+  const float* V;       // DAC output: FC Bv x ldx rows; conv the padded NCHW tensor
   const rxnn_conv_desc* conv;  // null for FC
   int64_t ldx;          // row stride of X in elements (FC)
   int64_t Bv;           // rows of the product
@@ -87,13 +89,16 @@ struct VmmLaunch {
   int32_t* iacc;        // split accumulation workspace (Bv x Q int32) or null
   float* dbg_I;         // [R][C][A][Bv][N] or null
   int32_t* dbg_code;    // [R][C][A][Bv][N] or null
-  const int2* ktab;     // conv: patch-column table (kh kw <= 31) or null
+  const int* ktab;      // conv: patch-column table
 };
 hipError_t launch_xbar_vmm(const MapScalars& ms, const PeriphScalars& ps, const float* gpt,
                            const VmmLaunch& vl, int splits, hipStream_t s);
 int ktab_entries(const MapScalars& ms);
-hipError_t launch_conv_ktab(const MapScalars& ms, const rxnn_conv_desc& cd, int2* tab,
+hipError_t launch_conv_ktab(const MapScalars& ms, const rxnn_conv_desc& cd, int* tab,
                             hipStream_t s);
+int64_t dac_elems(const rxnn_conv_desc* conv, int64_t Bv, int64_t ldx);
+hipError_t launch_dac(const PeriphScalars& ps, const rxnn_conv_desc* conv, const float* X,
+                      float* V, int64_t n, hipStream_t s);
 hipError_t launch_finish(const MapScalars& ms, const PeriphScalars& ps, const int32_t* iacc,
                          int64_t Bv, float* Y, int64_t hw_out, hipStream_t s);
 int choose_splits(const MapScalars& ms, const PeriphScalars& ps, int64_t Bv);

@@ -2,25 +2,40 @@
 // Sec. VI): DAC -> I = V . G' per crossbar array -> ADC -> digital
 // accumulation over row tiles, slices and the differential pair -> scale.
 //
-// One workgroup (4 waves) owns BM = 128 product rows and BN output columns of
-// one column tile, and walks every row tile r of that column tile (or a
-// contiguous share of them when the row tiles are split across workgroups).
-// The work is a sequence of stages (r, pair of arrays, 64-input chunk):
-//   * the DAC output V (BM x 64) of the chunk is staged in LDS: inputs are
-//     quantised to a code and replaced by the DAC table entry (the table lives
-//     in LDS).  For a convolution the inputs are gathered straight from the
-//     NCHW tensor (patch column k = (ci kh + ky) kw + kx, patch row
-//     bv = (n H_out + oy) W_out + ox, zero outside the image): the patch
-//     matrix is never written to memory;
+// Two kernels per call.
+//
+// k_dac converts every layer input once into its row voltage V (the DAC
+// transfer table lives in LDS).  For a convolution it writes V into a
+// zero-bordered copy of the NCHW input (pad pixels on every side), so the
+// patch gather of the evaluation kernel needs no bounds tests: a padded pixel
+// is input 0, whose DAC output is 0 V.
+//
+// k_xbar_vmm: one workgroup (4 waves) owns BM = 128 product rows and BN
+// output columns of one column tile, and walks every row tile r of that
+// column tile (or a contiguous share of them when the row tiles are split
+// across workgroups).  The work is a sequence of stages (r, pair of arrays,
+// 64-input chunk):
+//   * the V chunk (BM x 64) is staged in LDS.  For a convolution the rows are
+//     gathered from the padded V tensor (patch column k = (ci kh + ky) kw +
+//     kx, patch row bv = (n H_out + oy) W_out + ox): a per-layer table gives
+//     the offset of column k inside a pixel's window, which is the same for
+//     the whole wave, so a gathered element costs one buffer load with a
+//     scalar offset and no vector instruction; the patch matrix is never
+//     written to memory;
 //   * both arrays' G'^T chunks (BN x 64) are staged in LDS;
 //   * the global loads of stage s + 1 are issued into registers before the
 //     MFMA loop of stage s, so they are in flight while it runs;
 //   * v_mfma_f32_16x16x4f32 accumulates I for both arrays in fp32, the two
 //     arrays sharing every V operand read;
 //   * once the tile's M inputs are consumed, every current goes through the
-//     ADC (a bucket table gives a code that is exact or one too low, one
-//     comparison with the threshold table finishes it) and is added to an
-//     int32 accumulator with the array's digital weight (+-2^(b_s s)).
+//     ADC: one LDS read of a bucket table gives the code at the bucket's
+//     lower edge and the next threshold, one comparison finishes the code,
+//     and the difference of the pair's codes is added to an int32
+//     accumulator with the pair's digital weight 2^(b_s s).
+// On gfx950 the fp32 matrix instructions and vector instructions of a SIMD
+// do not overlap, so every vector instruction in the stage loop costs matrix
+// time: the kernel keeps them to the ADC (about six per conversion) and a
+// few per stage.
 // Integer accumulation makes the result independent of the order of row
 // tiles and arrays, so splitting the row tiles over workgroups and combining
 // with int32 atomics gives bit-identical results.
@@ -46,7 +61,7 @@ constexpr int kOob = (int)0x80000000u;
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 struct ConvGeom {
-  int c_in, h, w, kh, kw, stride, pad, ho, wo;
+  int c_in, h, w, kh, kw, stride, pad, ho, wo, hp, wp;   // hp, wp: padded input sides
 };
 
 struct VmmArgs {
@@ -54,46 +69,73 @@ struct VmmArgs {
   PeriphScalars ps;
   ConvGeom cg;
   const float* gpt;
-  const float* X;
+  const float* V;       // DAC output: FC Bv x ldx; conv the padded NCHW tensor
   int64_t ldx, Bv;
   float* Y;
   int64_t hw_out;
   int32_t* iacc;
   float* dbg_I;
   int32_t* dbg_code;
-  const int2* ktab;   // conv, kh kw <= 31: per (row tile, input) {byte offset, tap}
+  const int* ktab;      // conv: per (row tile, input) byte offset inside the window
   int r_per_split;
 };
 
 __device__ __forceinline__ double bend(double u, double b) { return u - (b * u) * (1.0 - u); }
 
-// bucket[b] = #{k : t_k <= (b - 1) w}: with w at most a quarter of the
-// smallest threshold spacing, the exact code is bucket[b] or bucket[b] + 1.
-__device__ __forceinline__ int adc_code(float I, const float* thr, const unsigned char* bucket,
-                                        float inv_w, int nb) {
-  const float t = I * inv_w;
-  const int b = (int)fminf(fmaxf(t, 0.0f), (float)(nb - 1));
-  const int c = bucket[b];
-  return c + (I >= thr[c + 1] ? 1 : 0);
+// ---------------------------------------------------------------------------
+// DAC of every layer input (Sec. IV-A 'Non-ideal DAC'): code =
+// clamp(rint(x s_in), 0, L), V = fp32(v_read phi(code / L)); ideal: V =
+// max(x, 0) v_read / x_max.  Convolution inputs go to the padded layout.
+// ---------------------------------------------------------------------------
+template <bool CONV>
+__global__ __launch_bounds__(256) void k_dac(PeriphScalars ps, ConvGeom cg, const float* X,
+                                             float* V, int64_t n_out) {
+  __shared__ float lut[256];
+  if (ps.dac_bits > 0) {
+    const int L = ps.dac_levels;
+    for (int k = threadIdx.x; k <= L; k += blockDim.x)
+      lut[k] = (float)(ps.v_read * bend((double)k / (double)L, ps.dac_bend));
+  }
+  __syncthreads();
+  for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < n_out;
+       e += (int64_t)gridDim.x * blockDim.x) {
+    float x = 0.0f;
+    if (CONV) {
+      // e = ((img c_in + ci) hp + yp) wp + xp over the padded tensor
+      const int64_t row = e / cg.wp;
+      const int xp = (int)(e - row * cg.wp);
+      const int64_t plane = row / cg.hp;
+      const int yp = (int)(row - plane * cg.hp);
+      const int iy = yp - cg.pad, ix = xp - cg.pad;
+      if (iy >= 0 && iy < cg.h && ix >= 0 && ix < cg.w)
+        x = X[(plane * cg.h + iy) * cg.w + ix];
+    } else {
+      x = X[e];
+    }
+    float v;
+    if (ps.dac_bits > 0) {
+      const float t = rintf(x * ps.dac_s_in);
+      v = lut[(int)fminf(fmaxf(t, 0.0f), (float)ps.dac_levels)];
+    } else {
+      v = fmaxf(x, 0.0f) * ps.s_v_ideal;
+    }
+    V[e] = v;
+  }
 }
 
-// CV: 0 fully connected; 1 convolution, patch columns decomposed in the
-// kernel; 2 convolution, patch columns read from the per-layer table.
-template <int BN, int CV, bool QADC, bool DEBUG>
+template <int BN, bool CONV, bool QADC, bool DEBUG>
 __global__ __launch_bounds__(NTHR, 2) void k_xbar_vmm(VmmArgs va) {
-  constexpr bool CONV = CV > 0;
   constexpr int NT = BN / 16;   // column fragments per wave
   constexpr int MT = 2;         // row fragments per wave (32 rows)
   constexpr int GV4 = BN / 8;   // float4 of G' staged per thread
   __shared__ __attribute__((aligned(16))) float Vs[BM * LDK];
   __shared__ __attribute__((aligned(16))) float Gs[2 * BN * LDK];
-  __shared__ float lut[256];
-  __shared__ float thr[258];
-  __shared__ unsigned char bucket[kMaxBuckets];
+  extern __shared__ float2 adct[];   // ADC table, n_buckets + 2 entries
 
   const MapScalars& ms = va.ms;
   const PeriphScalars& ps = va.ps;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int g = lane >> 4, li = lane & 15;
   const int64_t b0 = (int64_t)blockIdx.x * BM;
   // column blocks: every block of a full column tile, and of the last tile
@@ -104,13 +146,15 @@ __global__ __launch_bounds__(NTHR, 2) void k_xbar_vmm(VmmArgs va) {
   const int r_begin = blockIdx.z * va.r_per_split;
   const int r_end = min(ms.R, r_begin + va.r_per_split);
 
-  // ---- DAC and ADC tables (fp64 formulas, rounded to fp32) ----------------
-  if (ps.dac_bits > 0) {
-    const int L = ps.dac_levels;
-    for (int k = tid; k <= L; k += NTHR)
-      lut[k] = (float)(ps.v_read * bend((double)k / (double)L, ps.dac_bend));
-  }
+  // ---- ADC table ------------------------------------------------------------
+  // Thresholds t_1 .. t_L = fp32(I_FS phi((k - 1/2) / L)) (fp64 formula), held
+  // in the G' space until staging starts.  Entry b: c = #{k : t_k <= (b - 1) w}
+  // and t_{c+1}.  The bucket width w is at most 1 / 3.25 of the smallest
+  // threshold spacing: I / w rounded in fp32 lands in bucket floor(I / w) or a
+  // neighbour, which leaves at most one threshold between the entry's edge
+  // and I, so code(I) = c + (I >= t_{c+1}).
   if (QADC) {
+    float* thr = Gs;
     const int L = ps.adc_levels;
     for (int k = tid; k <= L + 1; k += NTHR) {
       float t;
@@ -120,65 +164,46 @@ __global__ __launch_bounds__(NTHR, 2) void k_xbar_vmm(VmmArgs va) {
       thr[k] = t;
     }
     __syncthreads();
-    for (int b = tid; b < ps.n_buckets; b += NTHR) {
+    for (int b = tid; b < ps.n_buckets + 2; b += NTHR) {
       const double edge = (double)(b - 1) * ps.bucket_w;
-      int lo = 0, hi = L;  // count of k in 1..L with thr[k] <= edge
+      int lo = 0, hi = L;
       while (lo < hi) {
         const int mid = (lo + hi + 1) >> 1;
         if ((double)thr[mid] <= edge) lo = mid; else hi = mid - 1;
       }
-      bucket[b] = (unsigned char)lo;
+      adct[b] = make_float2(__int_as_float(lo), thr[lo + 1]);
     }
   }
 
   // ---- per-thread staging geometry ----------------------------------------
   // Staging loads are raw buffer loads: an SGPR descriptor, a 32-bit VGPR
-  // offset and (FC) an SGPR offset per row step, so no 64-bit address is kept
-  // per element.  Lanes whose element lies outside the input issue no load.
-  // FC: lanes run along k (coalesced rows of X).  Conv: lanes run along the
-  // product rows (consecutive output pixels), every wave shares one k.
+  // offset and an SGPR offset.  FC: lanes run along k (coalesced rows of V),
+  // the SGPR offset steps the rows.  Conv: lanes run along the product rows
+  // (consecutive output pixels) and every wave shares one k, whose window
+  // offset is the SGPR offset.
   const int kk_fc = tid & 63, row_fc = tid >> 6;
   const int row_cv = tid & (BM - 1);
   const int kq_cv = __builtin_amdgcn_readfirstlane(tid >> 7);  // conv: first quad of 4 k
-  int xrow_off = 0;          // conv: element offset of (img, iy0, ix0) from the WG base
-  unsigned yok = 0, xok = 0;  // conv: bit ky (kx) set when that tap row (column) is inside the image
-  unsigned tapbad = ~0u;     // table mode: bit ky kw + kx set when that tap is outside the image
-                             // (bit 31, the table's code for a missing input, always set)
+  int xbase = 0;             // conv: byte offset of the pixel's window origin
   __amdgpu_buffer_rsrc_t xsrc;
-  int n_rows = (int)min((int64_t)BM, va.Bv - b0);
+  const int n_rows = (int)min((int64_t)BM, va.Bv - b0);
   if (CONV) {
     const int hw = va.cg.ho * va.cg.wo;
-    const int64_t chw = (int64_t)va.cg.c_in * va.cg.h * va.cg.w;
+    const int64_t chw = (int64_t)va.cg.c_in * va.cg.hp * va.cg.wp;
     const int64_t img_first = b0 / hw;
     const int64_t img_last = (b0 + n_rows - 1) / hw;
-    // table mode: the descriptor starts pad (w + 1) elements before the first
-    // image, so that every lane's base offset is non-negative
-    const int64_t shift = CV == 2 ? (int64_t)va.cg.pad * (va.cg.w + 1) : 0;
-    xsrc = __builtin_amdgcn_make_buffer_rsrc((void*)(va.X + img_first * chw - shift), (short)0,
-                                             (int)(((img_last - img_first + 1) * chw + shift) * 4),
+    xsrc = __builtin_amdgcn_make_buffer_rsrc((void*)(va.V + img_first * chw), (short)0,
+                                             (int)((img_last - img_first + 1) * chw * 4),
                                              0x00020000);
-    if (row_cv < n_rows) {
-      const int64_t bv = b0 + row_cv;
-      const int64_t img = bv / hw;
-      const int pix = (int)(bv - img * hw);
-      const int oy = pix / va.cg.wo, ox = pix - oy * va.cg.wo;
-      const int iy0 = oy * va.cg.stride - va.cg.pad;
-      const int ix0 = ox * va.cg.stride - va.cg.pad;
-      xrow_off = (int)((img - img_first) * chw) + iy0 * va.cg.w + ix0;
-      for (int t = 0; t < va.cg.kh; ++t)
-        if (iy0 + t >= 0 && iy0 + t < va.cg.h) yok |= 1u << t;
-      for (int t = 0; t < va.cg.kw; ++t)
-        if (ix0 + t >= 0 && ix0 + t < va.cg.w) xok |= 1u << t;
-      if (CV == 2) {
-        xrow_off = (xrow_off + (int)shift) * 4;   // byte offset from the shifted descriptor
-        tapbad = 1u << 31;
-        for (int ty = 0; ty < va.cg.kh; ++ty)
-          for (int tx = 0; tx < va.cg.kw; ++tx)
-            if (!((yok >> ty) & (xok >> tx) & 1u)) tapbad |= 1u << (ty * va.cg.kw + tx);
-      }
-    }
+    // rows past the batch read the last real row (their outputs are dropped)
+    const int64_t bv = b0 + min(row_cv, n_rows - 1);
+    const int64_t img = bv / hw;
+    const int pix = (int)(bv - img * hw);
+    const int oy = pix / va.cg.wo, ox = pix - oy * va.cg.wo;
+    xbase = (int)(((img - img_first) * chw + (int64_t)oy * va.cg.stride * va.cg.wp +
+                   (int64_t)ox * va.cg.stride) * 4);
   } else {
-    xsrc = __builtin_amdgcn_make_buffer_rsrc((void*)(va.X + b0 * va.ldx), (short)0,
+    xsrc = __builtin_amdgcn_make_buffer_rsrc((void*)(va.V + b0 * va.ldx), (short)0,
                                              (int)((int64_t)n_rows * va.ldx * 4), 0x00020000);
   }
 
@@ -190,6 +215,7 @@ __global__ __launch_bounds__(NTHR, 2) void k_xbar_vmm(VmmArgs va) {
   const int per_r = n_pairs * nkc;
   const int n_stages = r_end == ms.R ? (r_end - 1 - r_begin) * per_r + n_pairs * nkc_last
                                      : (r_end - r_begin) * per_r;
+  const int tile_elems = ms.Np * ms.Mp;
   // stage s -> row tile r, pair ap, chunk kci of the nk chunks of r
   auto decode = [&](int s, int& r, int& ap, int& kci, int& nk) {
     const int rr = s / per_r;
@@ -199,7 +225,6 @@ __global__ __launch_bounds__(NTHR, 2) void k_xbar_vmm(VmmArgs va) {
     ap = rem / nk;
     kci = rem - ap * nk;
   };
-  const int tile_elems = ms.Np * ms.Mp;
 
   float xr[XPT];
   f32x4 gr[GV4];
@@ -209,63 +234,20 @@ __global__ __launch_bounds__(NTHR, 2) void k_xbar_vmm(VmmArgs va) {
     decode(s, r, ap, kci, nk);
     const int kc0 = kci * KC;
     if (ap == 0 || nk > 1) {
-      if (CV == 2) {
+      if (CONV) {
         // this thread gathers k = 4 (kq_cv + 2 q) .. + 3, q = 0 .. 7, of its
-        // pixel.  The table gives, per k, the byte offset of the input element
-        // relative to the pixel's window (a scalar, the same for the wave) and
-        // its tap; a tap outside the image (or code 31, no input) turns the
-        // lane's offset out of range, so the load returns 0.
-        const int2* kt = va.ktab + (int64_t)r * (nkc * KC) + kc0 + 4 * kq_cv;
+        // pixel; table entries of missing inputs point at the window origin
+        // and are zeroed when staged
+        const int* kt = va.ktab + (int64_t)r * (nkc * KC) + kc0 + 4 * kq_cv;
 #pragma unroll
         for (int q = 0; q < XPT / 4; ++q)
 #pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            const int2 e = kt[8 * q + j];
-            const int voff = (int)((((tapbad >> e.y) & 1u) << 31) | (unsigned)xrow_off);
-            xr[4 * q + j] = __builtin_bit_cast(float,
-                __builtin_amdgcn_raw_buffer_load_b32(xsrc, voff, e.x, 0));
-          }
-      } else if (CONV) {
-        // this thread gathers k = 4 (kq_cv + 2 q) .. + 3, q = 0 .. 7, of its
-        // pixel.  The tap (ky, kx) and the input offset of k advance in scalar
-        // registers (k is the same for the whole wave); an element outside the
-        // image or beyond the layer's inputs gets an out-of-range buffer offset,
-        // for which the load returns 0 without touching memory.
-        const int khw = va.cg.kh * va.cg.kw, hw_in = va.cg.h * va.cg.w;
-        const int kbase = r * ms.M + kc0;
-        const int nvalid = min(ms.M - kc0, (int)ms.P - kbase);   // valid k of this chunk
-        const int k0 = kbase + 4 * kq_cv;
-        const int ci = k0 / khw;
-        const int tap = k0 - ci * khw;
-        int ky = tap / va.cg.kw, kx = tap - ky * va.cg.kw;
-        int off = (ci * va.cg.h + ky) * va.cg.w + kx;
-        auto step = [&]() {
-          ++off;
-          if (++kx == va.cg.kw) {
-            kx = 0;
-            off += va.cg.w - va.cg.kw;
-            if (++ky == va.cg.kh) {
-              ky = 0;
-              off += hw_in - va.cg.kh * va.cg.w;
-            }
-          }
-        };
-#pragma unroll
-        for (int q = 0; q < XPT / 4; ++q) {
-#pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            const bool kok = 4 * (kq_cv + 2 * q) + j < nvalid;
-            const bool ok = kok && (((yok >> ky) & (xok >> kx)) & 1);
+          for (int j = 0; j < 4; ++j)
             xr[4 * q + j] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
-                xsrc, ok ? (xrow_off + off) * 4 : kOob, 0, 0));
-            step();
-          }
-#pragma unroll
-          for (int j = 0; j < 4; ++j) step();   // the other half-wave group's quad
-        }
+                xsrc, xbase, kt[8 * q + j], 0));
       } else {
-        // lanes along k; a lane beyond the layer's inputs gets an out-of-range
-        // offset (the load returns 0), rows beyond the batch are skipped
+        // a lane beyond the layer's inputs gets an out-of-range offset (the
+        // load returns 0), rows beyond the batch are skipped
         const int km = kc0 + kk_fc;
         const int p = r * ms.M + km;
         const bool kok = km < ms.M && p < (int)ms.P;
@@ -295,27 +277,29 @@ __global__ __launch_bounds__(NTHR, 2) void k_xbar_vmm(VmmArgs va) {
     }
   };
 
-  auto dac = [&](float x) -> float {
-    if (ps.dac_bits > 0) {
-      const float t = rintf(x * ps.dac_s_in);
-      const int code = (int)fminf(fmaxf(t, 0.0f), (float)ps.dac_levels);
-      return lut[code];
-    }
-    return fmaxf(x, 0.0f) * ps.s_v_ideal;
-  };
-
   auto store_stage = [&](int s) {
     int r, ap, kci, nk;
     decode(s, r, ap, kci, nk);
     if (ap == 0 || nk > 1) {
       if (CONV) {
+        // inputs past the tile's or the layer's end are 0 (only in a chunk
+        // that is not full, a uniform condition)
+        const int kc0 = kci * KC;
+        const int nvalid = min(ms.M - kc0, (int)(ms.P - (int64_t)r * ms.M) - kc0);
+        if (nvalid < KC) {
+#pragma unroll
+          for (int q = 0; q < XPT / 4; ++q)
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+              if (4 * (kq_cv + 2 * q) + j >= nvalid) xr[4 * q + j] = 0.0f;
+        }
 #pragma unroll
         for (int q = 0; q < XPT / 4; ++q)
           *(f32x4*)&Vs[row_cv * LDK + 4 * (kq_cv + 2 * q)] =
-              f32x4{dac(xr[4 * q]), dac(xr[4 * q + 1]), dac(xr[4 * q + 2]), dac(xr[4 * q + 3])};
+              f32x4{xr[4 * q], xr[4 * q + 1], xr[4 * q + 2], xr[4 * q + 3]};
       } else {
 #pragma unroll
-        for (int it = 0; it < XPT; ++it) Vs[(row_fc + 4 * it) * LDK + kk_fc] = dac(xr[it]);
+        for (int it = 0; it < XPT; ++it) Vs[(row_fc + 4 * it) * LDK + kk_fc] = xr[it];
       }
     }
 #pragma unroll
@@ -339,7 +323,14 @@ __global__ __launch_bounds__(NTHR, 2) void k_xbar_vmm(VmmArgs va) {
       for (int v = 0; v < 4; ++v) { iacc[mt][nt][v] = 0; facc[mt][nt][v] = 0.0f; }
   f32x4 acc[2][MT][NT];
 
-  __syncthreads();
+  const unsigned b_max = (unsigned)ps.n_buckets;
+  auto adc = [&](float I) -> int {
+    const unsigned b = min((unsigned)(I * ps.bucket_inv_w), b_max);
+    const float2 e = adct[b];
+    return __float_as_int(e.x) + (I >= e.y ? 1 : 0);
+  };
+
+  __syncthreads();   // the ADC table build used the G' space
   if (n_stages > 0) load_stage(0);
   for (int s = 0; s < n_stages; ++s) {
     int r, ap, kci, nk;
@@ -357,8 +348,7 @@ __global__ __launch_bounds__(NTHR, 2) void k_xbar_vmm(VmmArgs va) {
 #pragma unroll
           for (int nt = 0; nt < NT; ++nt) acc[p][mt][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
     }
-    const int kb_end = min(KC, ms.Mp - kc0);
-    for (int kb = 0; kb < kb_end; kb += 16) {
+    auto block = [&](int kb) {
       f32x4 af[MT];
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt)
@@ -378,39 +368,45 @@ __global__ __launch_bounds__(NTHR, 2) void k_xbar_vmm(VmmArgs va) {
               acc[p][mt][nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(
                   af[mt][ss], bf[nt][ss], acc[p][mt][nt], 0, 0, 0);
       }
-    }
+    };
+    const int kb_end = min(KC, ms.Mp - kc0);
+    for (int kb = 0; kb < kb_end; kb += 16) block(kb);
     if (kci != nk - 1) continue;
 
     // ---- ADC and digital accumulation -------------------------------------
-    const int wpos = 1 << (ms.slice_bits * ap);
+    const int sh = ms.slice_bits * ap;   // the pair's weight is +-2^sh
 #pragma unroll
-    for (int p = 0; p < 2; ++p) {
-      const int wgt = p ? -wpos : wpos;
+    for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-      for (int mt = 0; mt < MT; ++mt)
+      for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
-        for (int nt = 0; nt < NT; ++nt)
-#pragma unroll
-          for (int v = 0; v < 4; ++v) {
-            const float I = acc[p][mt][nt][v];
-            int code = 0;
-            if (QADC) {
-              code = adc_code(I, thr, bucket, ps.bucket_inv_w, ps.n_buckets);
-              iacc[mt][nt][v] += wgt * code;
-            } else {
-              facc[mt][nt][v] += (float)wgt * I;
-            }
-            if (DEBUG) {
-              const int64_t bv = b0 + wave * 32 + mt * 16 + 4 * g + v;
-              const int n = n0 + nt * 16 + li;
-              if (bv < va.Bv && n < ms.N) {
-                const int64_t slot = (((int64_t)r * ms.C + c) * ms.A + 2 * ap + p) * va.Bv + bv;
-                if (va.dbg_I) va.dbg_I[slot * ms.N + n] = I;
-                if (va.dbg_code) va.dbg_code[slot * ms.N + n] = code;
+        for (int v = 0; v < 4; ++v) {
+          const float Ip = acc[0][mt][nt][v], In = acc[1][mt][nt][v];
+          int cp = 0, cn = 0;
+          if (QADC) {
+            cp = adc(Ip);
+            cn = adc(In);
+            iacc[mt][nt][v] += (cp - cn) << sh;
+          } else {
+            facc[mt][nt][v] += (float)(1 << sh) * Ip;
+            facc[mt][nt][v] += -(float)(1 << sh) * In;
+          }
+          if (DEBUG) {
+            const int64_t bv = b0 + wave * 32 + mt * 16 + 4 * g + v;
+            const int n = n0 + nt * 16 + li;
+            if (bv < va.Bv && n < ms.N) {
+              const int64_t slot = (((int64_t)r * ms.C + c) * ms.A + 2 * ap) * va.Bv + bv;
+              if (va.dbg_I) {
+                va.dbg_I[slot * ms.N + n] = Ip;
+                va.dbg_I[(slot + va.Bv) * ms.N + n] = In;
+              }
+              if (va.dbg_code) {
+                va.dbg_code[slot * ms.N + n] = cp;
+                va.dbg_code[(slot + va.Bv) * ms.N + n] = cn;
               }
             }
           }
-    }
+        }
   }
 
   // ---- output ---------------------------------------------------------------
@@ -465,54 +461,83 @@ __global__ void k_finish(MapScalars ms, PeriphScalars ps, const int32_t* __restr
   }
 }
 
-template <int BN, int CV, bool QADC>
-hipError_t launch_t(const VmmArgs& va, dim3 grid, hipStream_t s, bool debug) {
-  if (debug)
-    hipLaunchKernelGGL((k_xbar_vmm<BN, CV, QADC, true>), grid, dim3(NTHR), 0, s, va);
-  else
-    hipLaunchKernelGGL((k_xbar_vmm<BN, CV, QADC, false>), grid, dim3(NTHR), 0, s, va);
-  return hipGetLastError();
-}
-
-template <int BN>
-hipError_t launch_bn(const VmmArgs& va, dim3 grid, hipStream_t s, int cv, bool qadc,
-                     bool debug) {
-  if (cv == 2) {
-    return qadc ? launch_t<BN, 2, true>(va, grid, s, debug)
-                : launch_t<BN, 2, false>(va, grid, s, debug);
-  }
-  if (cv == 1) {
-    return qadc ? launch_t<BN, 1, true>(va, grid, s, debug)
-                : launch_t<BN, 1, false>(va, grid, s, debug);
-  }
-  return qadc ? launch_t<BN, 0, true>(va, grid, s, debug)
-              : launch_t<BN, 0, false>(va, grid, s, debug);
-}
-
 // Table of the patch columns of a convolution, per row tile r and tile input
-// kk < nkc KC: {byte offset of input p = r M + kk relative to the window of
-// an output pixel, tap ky kw + kx}; kk >= M or p >= P gets tap 31 (no input).
-__global__ void k_conv_ktab(MapScalars ms, ConvGeom cg, int kcp, int2* tab) {
+// kk < nkc KC: byte offset of input p = r M + kk inside an output pixel's
+// window of the padded input; an input past the tile or the layer gets 0 (it
+// is zeroed when staged).
+__global__ void k_conv_ktab(MapScalars ms, ConvGeom cg, int kcp, int* tab) {
   const int64_t n = (int64_t)ms.R * kcp;
   const int khw = cg.kh * cg.kw;
   for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < n;
        e += (int64_t)gridDim.x * blockDim.x) {
     const int r = (int)(e / kcp), kk = (int)(e - (int64_t)r * kcp);
     const int64_t p = (int64_t)r * ms.M + kk;
-    int2 v = make_int2(0, 31);
+    int v = 0;
     if (kk < ms.M && p < ms.P) {
       const int ci = (int)(p / khw), tap = (int)(p - (int64_t)ci * khw);
       const int ky = tap / cg.kw, kx = tap - ky * cg.kw;
-      v = make_int2(((ci * cg.h + ky) * cg.w + kx) * 4, tap);
+      v = ((ci * cg.hp + ky) * cg.wp + kx) * 4;
     }
     tab[e] = v;
   }
+}
+
+// The ADC table is dynamic LDS (up to kMaxBuckets + 2 entries of 8 bytes);
+// the limit is raised once per instantiation.
+template <typename K>
+hipError_t allow_adc_table(K kernel) {
+  return hipFuncSetAttribute(reinterpret_cast<const void*>(kernel),
+                             hipFuncAttributeMaxDynamicSharedMemorySize,
+                             (kMaxBuckets + 2) * (int)sizeof(float2));
+}
+
+template <int BN, bool CONV, bool QADC, bool DEBUG>
+hipError_t launch_one(const VmmArgs& va, dim3 grid, hipStream_t s) {
+  auto kern = k_xbar_vmm<BN, CONV, QADC, DEBUG>;
+  static const hipError_t attr = allow_adc_table(kern);
+  if (attr != hipSuccess) return attr;
+  const size_t shm = QADC ? (size_t)(va.ps.n_buckets + 2) * sizeof(float2) : 0;
+  hipLaunchKernelGGL(kern, grid, dim3(NTHR), shm, s, va);
+  return hipGetLastError();
+}
+
+template <int BN, bool CONV, bool QADC>
+hipError_t launch_t(const VmmArgs& va, dim3 grid, hipStream_t s, bool debug) {
+  return debug ? launch_one<BN, CONV, QADC, true>(va, grid, s)
+               : launch_one<BN, CONV, QADC, false>(va, grid, s);
+}
+
+template <int BN>
+hipError_t launch_bn(const VmmArgs& va, dim3 grid, hipStream_t s, bool conv, bool qadc,
+                     bool debug) {
+  if (conv) {
+    return qadc ? launch_t<BN, true, true>(va, grid, s, debug)
+                : launch_t<BN, true, false>(va, grid, s, debug);
+  }
+  return qadc ? launch_t<BN, false, true>(va, grid, s, debug)
+              : launch_t<BN, false, false>(va, grid, s, debug);
 }
 
 int pick_bn(int Np) {
   if (Np % 64 == 0) return 64;
   if (Np % 32 == 0) return 32;
   return 16;
+}
+
+ConvGeom conv_geom(const rxnn_conv_desc& cd) {
+  ConvGeom cg;
+  cg.c_in = cd.c_in;
+  cg.h = cd.h;
+  cg.w = cd.w;
+  cg.kh = cd.kh;
+  cg.kw = cd.kw;
+  cg.stride = cd.stride;
+  cg.pad = cd.pad;
+  cg.ho = (cd.h + 2 * cd.pad - cd.kh) / cd.stride + 1;
+  cg.wo = (cd.w + 2 * cd.pad - cd.kw) / cd.stride + 1;
+  cg.hp = cd.h + 2 * cd.pad;
+  cg.wp = cd.w + 2 * cd.pad;
+  return cg;
 }
 
 }  // namespace
@@ -530,26 +555,33 @@ int choose_splits(const MapScalars& ms, const PeriphScalars& ps, int64_t Bv) {
   return (ms.R + per - 1) / per;
 }
 
+int64_t dac_elems(const rxnn_conv_desc* conv, int64_t Bv, int64_t ldx) {
+  if (!conv) return Bv * ldx;
+  return (int64_t)conv->n * conv->c_in * (conv->h + 2 * conv->pad) * (conv->w + 2 * conv->pad);
+}
+
+hipError_t launch_dac(const PeriphScalars& ps, const rxnn_conv_desc* conv, const float* X,
+                      float* V, int64_t n, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  int64_t blocks = (n + 255) / 256;
+  if (blocks > 16384) blocks = 16384;
+  if (conv)
+    hipLaunchKernelGGL(k_dac<true>, dim3((unsigned)blocks), dim3(256), 0, s, ps,
+                       conv_geom(*conv), X, V, n);
+  else
+    hipLaunchKernelGGL(k_dac<false>, dim3((unsigned)blocks), dim3(256), 0, s, ps, ConvGeom{},
+                       X, V, n);
+  return hipGetLastError();
+}
+
 hipError_t launch_xbar_vmm(const MapScalars& ms, const PeriphScalars& ps, const float* gpt,
                            const VmmLaunch& vl, int splits, hipStream_t s) {
   VmmArgs va;
   va.ms = ms;
   va.ps = ps;
-  va.cg = ConvGeom{0, 0, 0, 0, 0, 1, 0, 1, 1};
-  if (vl.conv) {
-    const rxnn_conv_desc& cd = *vl.conv;
-    va.cg.c_in = cd.c_in;
-    va.cg.h = cd.h;
-    va.cg.w = cd.w;
-    va.cg.kh = cd.kh;
-    va.cg.kw = cd.kw;
-    va.cg.stride = cd.stride;
-    va.cg.pad = cd.pad;
-    va.cg.ho = (cd.h + 2 * cd.pad - cd.kh) / cd.stride + 1;
-    va.cg.wo = (cd.w + 2 * cd.pad - cd.kw) / cd.stride + 1;
-  }
+  va.cg = vl.conv ? conv_geom(*vl.conv) : ConvGeom{0, 0, 0, 0, 0, 1, 0, 1, 1, 0, 0};
   va.gpt = gpt;
-  va.X = vl.X;
+  va.V = vl.V;
   va.ldx = vl.ldx;
   va.Bv = vl.Bv;
   va.Y = vl.Y;
@@ -557,6 +589,7 @@ hipError_t launch_xbar_vmm(const MapScalars& ms, const PeriphScalars& ps, const 
   va.iacc = vl.iacc;
   va.dbg_I = vl.dbg_I;
   va.dbg_code = vl.dbg_code;
+  va.ktab = vl.ktab;
   va.r_per_split = (ms.R + splits - 1) / splits;
   const int bn = pick_bn(ms.Np);
   // the debug entry reports the currents of every column, padded ones included
@@ -566,23 +599,22 @@ hipError_t launch_xbar_vmm(const MapScalars& ms, const PeriphScalars& ps, const 
   dim3 grid((unsigned)((vl.Bv + BM - 1) / BM), (unsigned)((ms.C - 1) * (ms.Np / bn) + blk_last),
             (unsigned)((ms.R + va.r_per_split - 1) / va.r_per_split));
   const bool qadc = ps.adc_bits > 0;
-  const int cv = vl.conv == nullptr ? 0 : (vl.ktab ? 2 : 1);
-  va.ktab = vl.ktab;
-  if (bn == 64) return launch_bn<64>(va, grid, s, cv, qadc, debug);
-  if (bn == 32) return launch_bn<32>(va, grid, s, cv, qadc, debug);
-  return launch_bn<16>(va, grid, s, cv, qadc, debug);
+  const bool conv = vl.conv != nullptr;
+  if (bn == 64) return launch_bn<64>(va, grid, s, conv, qadc, debug);
+  if (bn == 32) return launch_bn<32>(va, grid, s, conv, qadc, debug);
+  return launch_bn<16>(va, grid, s, conv, qadc, debug);
 }
 
 int ktab_entries(const MapScalars& ms) { return ms.R * (((ms.Mp + KC - 1) / KC) * KC); }
 
-hipError_t launch_conv_ktab(const MapScalars& ms, const rxnn_conv_desc& cd, int2* tab,
+hipError_t launch_conv_ktab(const MapScalars& ms, const rxnn_conv_desc& cd, int* tab,
                             hipStream_t s) {
-  ConvGeom cg{cd.c_in, cd.h, cd.w, cd.kh, cd.kw, cd.stride, cd.pad, 0, 0};
   const int kcp = ((ms.Mp + KC - 1) / KC) * KC;
   const int64_t n = (int64_t)ms.R * kcp;
   int64_t blocks = (n + 255) / 256;
   if (blocks > 1024) blocks = 1024;
-  hipLaunchKernelGGL(k_conv_ktab, dim3((unsigned)blocks), dim3(256), 0, s, ms, cg, kcp, tab);
+  hipLaunchKernelGGL(k_conv_ktab, dim3((unsigned)blocks), dim3(256), 0, s, ms, conv_geom(cd),
+                     kcp, tab);
   return hipGetLastError();
 }
 
