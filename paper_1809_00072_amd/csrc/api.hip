@@ -186,11 +186,19 @@ rxnn_status check_acc_range(const MapScalars& ms, const PeriphScalars& ps) {
 rxnn_status run_vmm(const rxnn_layer* L, const PeriphScalars& ps, const float* X,
                     const rxnn_conv_desc* conv, int64_t ldx, int64_t Bv, float* Y,
                     int64_t hw_out, float* dbgI, int32_t* dbgC, hipStream_t s,
-                    int32_t* iacc_ws, const int* ktab = nullptr) {
+                    const int* ktab = nullptr) {
   const MapScalars& ms = L->ms;
-  const int splits = (dbgI || dbgC) ? 1 : choose_splits(ms, ps, Bv);
+  VmmPlan plan{0, 0, 0};
+  if (!(dbgI || dbgC)) plan = vmm_plan(ms, ps, Bv, conv != nullptr);
+  const int workers = plan.workers;
+  int32_t* iacc_ws = nullptr;
+  if (workers > 0) {
+    rxnn_status st = grow_ws(const_cast<rxnn_layer*>(L), (size_t)Bv * ms.Q * sizeof(int32_t));
+    if (st) return st;
+    iacc_ws = (int32_t*)L->ws;
+  }
   // DAC of every input into the layer's V buffer (padded for a convolution)
-  const int64_t n_v = dac_elems(conv, Bv, ldx);
+  const int64_t n_v = dac_elems(ms, conv, Bv);
   if ((size_t)n_v * sizeof(float) > L->vbuf_bytes) {
     rxnn_layer* Lm = const_cast<rxnn_layer*>(L);
     if (Lm->vbuf) HIP_TRY(hipFree(Lm->vbuf));
@@ -207,12 +215,13 @@ rxnn_status run_vmm(const rxnn_layer* L, const PeriphScalars& ps, const float* X
   }
   {
     ProfScope t("dac", s);
-    HIP_TRY(launch_dac(ps, conv, X, L->vbuf, n_v, s));
+    HIP_TRY(launch_dac(ms, ps, conv, X, Bv, L->vbuf, s));
   }
   VmmLaunch vl;
   vl.V = L->vbuf;
   vl.conv = conv;
-  vl.ldx = ldx;
+  vl.ldx = conv ? 0 : fc_ldv(ms);
+  (void)ldx;
   vl.Bv = Bv;
   vl.Y = Y;
   vl.hw_out = hw_out;
@@ -220,18 +229,19 @@ rxnn_status run_vmm(const rxnn_layer* L, const PeriphScalars& ps, const float* X
   vl.dbg_I = dbgI;
   vl.dbg_code = dbgC;
   vl.ktab = ktab;
-  if (splits > 1) {
+  if (workers > 0) {
     vl.iacc = iacc_ws;
     ProfScope z("fill", s);
-    HIP_TRY(launch_fill_u32((unsigned*)iacc_ws, Bv * ms.Q, 0u, s));
+    HIP_TRY(launch_fill_u32((unsigned*)iacc_ws + plan.row0 * ms.Q, (Bv - plan.row0) * ms.Q, 0u,
+                            s));
   }
   {
     ProfScope t("xbar_vmm", s);
-    HIP_TRY(launch_xbar_vmm(ms, ps, L->gpt, vl, splits, s));
+    HIP_TRY(launch_xbar_vmm(ms, ps, L->gpt, vl, plan, s));
   }
-  if (splits > 1) {
+  if (workers > 0) {
     ProfScope t("finish", s);
-    HIP_TRY(launch_finish(ms, ps, iacc_ws, Bv, Y, hw_out, s));
+    HIP_TRY(launch_finish(ms, ps, iacc_ws, plan.row0, Bv, Y, hw_out, s));
   }
   return RXNN_OK;
 }
@@ -254,12 +264,7 @@ rxnn_status vmm_common(const rxnn_layer* layer, const rxnn_periph_params* periph
   DeviceGuard dg(L->device);
   if (!dg.ok) return fail(RXNN_EHIP, "cannot select the layer's device");
   hipStream_t s = (hipStream_t)stream;
-  int32_t* iacc = nullptr;
-  if (!(dbgI || dbgC) && choose_splits(L->ms, ps, B) > 1) {
-    if ((st = grow_ws(L, (size_t)B * L->ms.Q * sizeof(int32_t)))) return st;
-    iacc = (int32_t*)L->ws;
-  }
-  return run_vmm(L, ps, X, nullptr, L->ms.P, B, Y, 0, dbgI, dbgC, s, iacc);
+  return run_vmm(L, ps, X, nullptr, L->ms.P, B, Y, 0, dbgI, dbgC, s);
 }
 
 // w_max (fixed or reduced from W) followed by the G' build of every array.
@@ -494,11 +499,6 @@ rxnn_status rxnn_conv_layer(const rxnn_layer* layer, const rxnn_periph_params* p
   DeviceGuard dg(L->device);
   if (!dg.ok) return fail(RXNN_EHIP, "cannot select the layer's device");
   hipStream_t s = (hipStream_t)stream;
-  int32_t* iacc = nullptr;
-  if (choose_splits(ms, ps, Bv) > 1) {
-    if ((st = grow_ws(L, (size_t)Bv * ms.Q * sizeof(int32_t)))) return st;
-    iacc = (int32_t*)L->ws;
-  }
   // patch-column table (per row tile and input: byte offset in the window of
   // the padded input), rebuilt when the geometry changes
   {
@@ -525,7 +525,7 @@ rxnn_status rxnn_conv_layer(const rxnn_layer* layer, const rxnn_periph_params* p
     }
   }
   const int* ktab = L->ktab;
-  return run_vmm(L, ps, X, &cd, 0, Bv, Y, ho * wo, nullptr, nullptr, s, iacc, ktab);
+  return run_vmm(L, ps, X, &cd, 0, Bv, Y, ho * wo, nullptr, nullptr, s, ktab);
 }
 
 rxnn_status rxnn_get_gprime(const rxnn_layer* layer, int64_t row_tile, int64_t col_tile,

@@ -80,7 +80,7 @@ hipError_t launch_nd_build(const MapScalars& ms, const float* W, float* gpt, int
                            int64_t n, int bs, double* ws, hipStream_t s);
 
 struct VmmLaunch {
-  const float* V;       // DAC output: FC Bv x ldx rows; conv the padded NCHW tensor
+  const float* V;       // DAC output: FC Bv x ldx rows (ldx = fc_ldv); conv the padded NCHW tensor
   const rxnn_conv_desc* conv;  // null for FC
   int64_t ldx;          // row stride of X in elements (FC)
   int64_t Bv;           // rows of the product
@@ -91,17 +91,30 @@ struct VmmLaunch {
   int32_t* dbg_code;    // [R][C][A][Bv][N] or null
   const int* ktab;      // conv: patch-column table
 };
+// Schedule of the evaluation kernel.  workers = 0: one workgroup per tile.
+// workers > 0: persistent workgroups; tiles [0, dp_tiles) are whole-tile work,
+// the rest (output rows [row0, Bv)) is shared by (tile, row tile) units that
+// accumulate in the int32 workspace (zeroed first, converted by finish).
+struct VmmPlan {
+  int workers;
+  int64_t dp_tiles;
+  int64_t row0;
+};
 hipError_t launch_xbar_vmm(const MapScalars& ms, const PeriphScalars& ps, const float* gpt,
-                           const VmmLaunch& vl, int splits, hipStream_t s);
+                           const VmmLaunch& vl, const VmmPlan& plan, hipStream_t s);
 int ktab_entries(const MapScalars& ms);
 hipError_t launch_conv_ktab(const MapScalars& ms, const rxnn_conv_desc& cd, int* tab,
                             hipStream_t s);
-int64_t dac_elems(const rxnn_conv_desc* conv, int64_t Bv, int64_t ldx);
-hipError_t launch_dac(const PeriphScalars& ps, const rxnn_conv_desc* conv, const float* X,
-                      float* V, int64_t n, hipStream_t s);
+// DAC output: FC rows of fc_ldv(ms) floats (zero past P); conv the input with
+// pad pixels on every side
+int64_t fc_ldv(const MapScalars& ms);
+int64_t dac_elems(const MapScalars& ms, const rxnn_conv_desc* conv, int64_t Bv);
+hipError_t launch_dac(const MapScalars& ms, const PeriphScalars& ps,
+                      const rxnn_conv_desc* conv, const float* X, int64_t Bv, float* V,
+                      hipStream_t s);
 hipError_t launch_finish(const MapScalars& ms, const PeriphScalars& ps, const int32_t* iacc,
-                         int64_t Bv, float* Y, int64_t hw_out, hipStream_t s);
-int choose_splits(const MapScalars& ms, const PeriphScalars& ps, int64_t Bv);
+                         int64_t row0, int64_t Bv, float* Y, int64_t hw_out, hipStream_t s);
+VmmPlan vmm_plan(const MapScalars& ms, const PeriphScalars& ps, int64_t Bv, bool conv);
 
 // ---- kernel timing (api.hip) ------------------------------------------------
 struct ProfScope {

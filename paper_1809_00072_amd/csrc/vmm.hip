@@ -69,7 +69,7 @@ struct VmmArgs {
   PeriphScalars ps;
   ConvGeom cg;
   const float* gpt;
-  const float* V;       // DAC output: FC Bv x ldx; conv the padded NCHW tensor
+  const float* V;       // DAC output: FC Bv x ldx (zero past P); conv the padded NCHW tensor
   int64_t ldx, Bv;
   float* Y;
   int64_t hw_out;
@@ -77,16 +77,33 @@ struct VmmArgs {
   float* dbg_I;
   int32_t* dbg_code;
   const int* ktab;      // conv: per (row tile, input) byte offset inside the window
-  int r_per_split;
+  int n_cb;             // column blocks (tiles along y)
+  int workers;          // 0: one workgroup per tile; > 0: persistent workgroups
+  int64_t dp_tiles;     // persistent: tiles [0, dp_tiles) are whole-tile work (direct
+                        // writes); the rest is shared evenly by (tile, row tile) units
+                        // accumulated with int32 atomics
 };
 
 __device__ __forceinline__ double bend(double u, double b) { return u - (b * u) * (1.0 - u); }
+
+// Buffer descriptor of a workgroup-uniform range; readfirstlane keeps it in
+// scalar registers (a descriptor the compiler cannot prove uniform costs a
+// loop over the distinct values at every load).
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t uniform_rsrc(const void* p, int64_t bytes) {
+  const uint64_t a = (uint64_t)p;
+  const uint64_t au = ((uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((int)(a >> 32)) << 32) |
+                      (uint32_t)__builtin_amdgcn_readfirstlane((int)a);
+  return __builtin_amdgcn_make_buffer_rsrc((void*)au, (short)0,
+                                           __builtin_amdgcn_readfirstlane((int)bytes), 0x00020000);
+}
 
 // ---------------------------------------------------------------------------
 // DAC of every layer input (Sec. IV-A 'Non-ideal DAC'): code =
 // clamp(rint(x s_in), 0, L), V = fp32(v_read phi(code / L)); ideal: V =
 // max(x, 0) v_read / x_max.  Convolution inputs go to the padded layout.
 // ---------------------------------------------------------------------------
+// n_out: rows Bv (FC; cg.c_in = P, cg.wp = row stride of V) or planes n c_in
+// (convolution)
 template <bool CONV>
 __global__ __launch_bounds__(256) void k_dac(PeriphScalars ps, ConvGeom cg, const float* X,
                                              float* V, int64_t n_out) {
@@ -97,29 +114,34 @@ __global__ __launch_bounds__(256) void k_dac(PeriphScalars ps, ConvGeom cg, cons
       lut[k] = (float)(ps.v_read * bend((double)k / (double)L, ps.dac_bend));
   }
   __syncthreads();
-  for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < n_out;
-       e += (int64_t)gridDim.x * blockDim.x) {
-    float x = 0.0f;
-    if (CONV) {
-      // e = ((img c_in + ci) hp + yp) wp + xp over the padded tensor
-      const int64_t row = e / cg.wp;
-      const int xp = (int)(e - row * cg.wp);
-      const int64_t plane = row / cg.hp;
-      const int yp = (int)(row - plane * cg.hp);
-      const int iy = yp - cg.pad, ix = xp - cg.pad;
-      if (iy >= 0 && iy < cg.h && ix >= 0 && ix < cg.w)
-        x = X[(plane * cg.h + iy) * cg.w + ix];
-    } else {
-      x = X[e];
-    }
-    float v;
+  auto dac = [&](float x) -> float {
     if (ps.dac_bits > 0) {
       const float t = rintf(x * ps.dac_s_in);
-      v = lut[(int)fminf(fmaxf(t, 0.0f), (float)ps.dac_levels)];
-    } else {
-      v = fmaxf(x, 0.0f) * ps.s_v_ideal;
+      return lut[(int)fminf(fmaxf(t, 0.0f), (float)ps.dac_levels)];
     }
-    V[e] = v;
+    return fmaxf(x, 0.0f) * ps.s_v_ideal;
+  };
+  if (CONV) {
+    // planes (img, ci) over blockIdx.y; threads stride over the padded plane
+    const int plane_p = cg.hp * cg.wp;
+    for (int64_t plane = blockIdx.y; plane < n_out; plane += gridDim.y) {
+      const float* Xp = X + plane * cg.h * cg.w;
+      float* Vp = V + plane * plane_p;
+      for (int e = blockIdx.x * blockDim.x + threadIdx.x; e < plane_p;
+           e += gridDim.x * blockDim.x) {
+        const int yp = e / cg.wp, xp = e - yp * cg.wp;
+        const int iy = yp - cg.pad, ix = xp - cg.pad;
+        float x = 0.0f;
+        if (iy >= 0 && iy < cg.h && ix >= 0 && ix < cg.w) x = Xp[iy * cg.w + ix];
+        Vp[e] = dac(x);
+      }
+    }
+  } else {
+    // rows b over blockIdx.y: V[b][p] = DAC(X[b][p]) for p < P, 0 up to ldv
+    const int P = cg.c_in, ldv = cg.wp;
+    for (int64_t b = blockIdx.y; b < n_out; b += gridDim.y)
+      for (int p = blockIdx.x * blockDim.x + threadIdx.x; p < ldv; p += gridDim.x * blockDim.x)
+        V[b * ldv + p] = p < P ? dac(X[b * P + p]) : 0.0f;
   }
 }
 
@@ -137,14 +159,7 @@ __global__ __launch_bounds__(NTHR, 2) void k_xbar_vmm(VmmArgs va) {
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int g = lane >> 4, li = lane & 15;
-  const int64_t b0 = (int64_t)blockIdx.x * BM;
-  // column blocks: every block of a full column tile, and of the last tile
-  // only those that hold real output columns (padded columns are discarded)
   const int nblk_per_tile = ms.Np / BN;
-  const int c = min((int)blockIdx.y / nblk_per_tile, ms.C - 1);
-  const int n0 = ((int)blockIdx.y - c * nblk_per_tile) * BN;
-  const int r_begin = blockIdx.z * va.r_per_split;
-  const int r_end = min(ms.R, r_begin + va.r_per_split);
 
   // ---- ADC table ------------------------------------------------------------
   // Thresholds t_1 .. t_L = fp32(I_FS phi((k - 1/2) / L)) (fp64 formula), held
@@ -175,16 +190,37 @@ __global__ __launch_bounds__(NTHR, 2) void k_xbar_vmm(VmmArgs va) {
     }
   }
 
+  const unsigned b_max = (unsigned)ps.n_buckets;
+  auto adc = [&](float I) -> int {
+    const unsigned b = min((unsigned)(I * ps.bucket_inv_w), b_max);
+    const float2 e = adct[b];
+    return __float_as_int(e.x) + (I >= e.y ? 1 : 0);
+  };
+  __syncthreads();   // the ADC table build used the G' space
+
+  // One tile: product rows [b0, b0 + BM) x columns [n0, n0 + BN) of column
+  // tile c, row tiles [r_begin, r_end).
+  auto run_tile = [&](int64_t b0_in, int c_in, int n0_in, int r_begin_in, int r_end_in,
+                      bool atomic) __attribute__((always_inline)) {
+  // the tile parameters are the same for the whole workgroup; readfirstlane
+  // lets the compiler keep everything derived from them in scalar registers
+  const int64_t b0 = (int64_t)__builtin_amdgcn_readfirstlane((int)(b0_in >> 32)) << 32 |
+                     (uint32_t)__builtin_amdgcn_readfirstlane((int)b0_in);
+  const int c = __builtin_amdgcn_readfirstlane(c_in);
+  const int n0 = __builtin_amdgcn_readfirstlane(n0_in);
+  const int r_begin = __builtin_amdgcn_readfirstlane(r_begin_in);
+  const int r_end = __builtin_amdgcn_readfirstlane(r_end_in);
   // ---- per-thread staging geometry ----------------------------------------
   // Staging loads are raw buffer loads: an SGPR descriptor, a 32-bit VGPR
   // offset and an SGPR offset.  FC: lanes run along k (coalesced rows of V),
   // the SGPR offset steps the rows.  Conv: lanes run along the product rows
   // (consecutive output pixels) and every wave shares one k, whose window
   // offset is the SGPR offset.
-  const int kk_fc = tid & 63, row_fc = tid >> 6;
+  const int k4_fc = tid & 15, row_fc = tid >> 4;   // FC: 4 inputs of rows row_fc + 16 i
   const int row_cv = tid & (BM - 1);
   const int kq_cv = __builtin_amdgcn_readfirstlane(tid >> 7);  // conv: first quad of 4 k
   int xbase = 0;             // conv: byte offset of the pixel's window origin
+  int fc_off[XPT / 4];       // FC: byte offsets of this thread's rows
   __amdgpu_buffer_rsrc_t xsrc;
   const int n_rows = (int)min((int64_t)BM, va.Bv - b0);
   if (CONV) {
@@ -192,9 +228,7 @@ __global__ __launch_bounds__(NTHR, 2) void k_xbar_vmm(VmmArgs va) {
     const int64_t chw = (int64_t)va.cg.c_in * va.cg.hp * va.cg.wp;
     const int64_t img_first = b0 / hw;
     const int64_t img_last = (b0 + n_rows - 1) / hw;
-    xsrc = __builtin_amdgcn_make_buffer_rsrc((void*)(va.V + img_first * chw), (short)0,
-                                             (int)((img_last - img_first + 1) * chw * 4),
-                                             0x00020000);
+    xsrc = uniform_rsrc(va.V + img_first * chw, (img_last - img_first + 1) * chw * 4);
     // rows past the batch read the last real row (their outputs are dropped)
     const int64_t bv = b0 + min(row_cv, n_rows - 1);
     const int64_t img = bv / hw;
@@ -203,8 +237,10 @@ __global__ __launch_bounds__(NTHR, 2) void k_xbar_vmm(VmmArgs va) {
     xbase = (int)(((img - img_first) * chw + (int64_t)oy * va.cg.stride * va.cg.wp +
                    (int64_t)ox * va.cg.stride) * 4);
   } else {
-    xsrc = __builtin_amdgcn_make_buffer_rsrc((void*)(va.V + b0 * va.ldx), (short)0,
-                                             (int)((int64_t)n_rows * va.ldx * 4), 0x00020000);
+    xsrc = uniform_rsrc(va.V + b0 * va.ldx, (int64_t)n_rows * va.ldx * 4);
+#pragma unroll
+    for (int it = 0; it < XPT / 4; ++it)
+      fc_off[it] = (int)(((row_fc + 16 * it) * va.ldx + 4 * k4_fc) * 4);
   }
 
   const int n_pairs = ms.A / 2;
@@ -238,7 +274,7 @@ __global__ __launch_bounds__(NTHR, 2) void k_xbar_vmm(VmmArgs va) {
         // this thread gathers k = 4 (kq_cv + 2 q) .. + 3, q = 0 .. 7, of its
         // pixel; table entries of missing inputs point at the window origin
         // and are zeroed when staged
-        const int* kt = va.ktab + (int64_t)r * (nkc * KC) + kc0 + 4 * kq_cv;
+        const int* kt = va.ktab + __builtin_amdgcn_readfirstlane(r * (nkc * KC) + kc0 + 4 * kq_cv);
 #pragma unroll
         for (int q = 0; q < XPT / 4; ++q)
 #pragma unroll
@@ -246,25 +282,23 @@ __global__ __launch_bounds__(NTHR, 2) void k_xbar_vmm(VmmArgs va) {
             xr[4 * q + j] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
                 xsrc, xbase, kt[8 * q + j], 0));
       } else {
-        // a lane beyond the layer's inputs gets an out-of-range offset (the
-        // load returns 0), rows beyond the batch are skipped
-        const int km = kc0 + kk_fc;
-        const int p = r * ms.M + km;
-        const bool kok = km < ms.M && p < (int)ms.P;
-        const int voff = kok ? (int)((row_fc * va.ldx + p) * 4) : kOob;
+        // 16 bytes per lane; V is zero past P, inputs past the tile's M meet
+        // zero G' rows or G' loads past the tile; rows past the batch are
+        // beyond the descriptor and read 0
+        const int soff = __builtin_amdgcn_readfirstlane((r * ms.M + kc0) * 4);
 #pragma unroll
-        for (int it = 0; it < XPT; ++it) {
-          float x = 0.0f;
-          if (row_fc + 4 * it < n_rows)   // uniform over the wave
-            x = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
-                                              xsrc, voff, (int)(4 * it * va.ldx * 4), 0));
-          xr[it] = x;
+        for (int it = 0; it < XPT / 4; ++it) {
+          const f32x4 x4 = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(
+              xsrc, fc_off[it], soff, 0));
+          xr[4 * it] = x4[0];
+          xr[4 * it + 1] = x4[1];
+          xr[4 * it + 2] = x4[2];
+          xr[4 * it + 3] = x4[3];
         }
       }
     }
     const int64_t arr0 = ((int64_t)c * ms.R + r) * ms.A + 2 * ap;
-    __amdgpu_buffer_rsrc_t gsrc = __builtin_amdgcn_make_buffer_rsrc(
-        (void*)(va.gpt + arr0 * tile_elems), (short)0, 2 * tile_elems * 4, 0x00020000);
+    __amdgpu_buffer_rsrc_t gsrc = uniform_rsrc(va.gpt + arr0 * tile_elems, (int64_t)2 * tile_elems * 4);
 #pragma unroll
     for (int it = 0; it < GV4; ++it) {
       const int e4 = tid + NTHR * it;
@@ -299,7 +333,9 @@ __global__ __launch_bounds__(NTHR, 2) void k_xbar_vmm(VmmArgs va) {
               f32x4{xr[4 * q], xr[4 * q + 1], xr[4 * q + 2], xr[4 * q + 3]};
       } else {
 #pragma unroll
-        for (int it = 0; it < XPT; ++it) Vs[(row_fc + 4 * it) * LDK + kk_fc] = xr[it];
+        for (int it = 0; it < XPT / 4; ++it)
+          *(f32x4*)&Vs[(row_fc + 16 * it) * LDK + 4 * k4_fc] =
+              f32x4{xr[4 * it], xr[4 * it + 1], xr[4 * it + 2], xr[4 * it + 3]};
       }
     }
 #pragma unroll
@@ -323,14 +359,6 @@ __global__ __launch_bounds__(NTHR, 2) void k_xbar_vmm(VmmArgs va) {
       for (int v = 0; v < 4; ++v) { iacc[mt][nt][v] = 0; facc[mt][nt][v] = 0.0f; }
   f32x4 acc[2][MT][NT];
 
-  const unsigned b_max = (unsigned)ps.n_buckets;
-  auto adc = [&](float I) -> int {
-    const unsigned b = min((unsigned)(I * ps.bucket_inv_w), b_max);
-    const float2 e = adct[b];
-    return __float_as_int(e.x) + (I >= e.y ? 1 : 0);
-  };
-
-  __syncthreads();   // the ADC table build used the G' space
   if (n_stages > 0) load_stage(0);
   for (int s = 0; s < n_stages; ++s) {
     int r, ap, kci, nk;
@@ -416,49 +444,133 @@ __global__ __launch_bounds__(NTHR, 2) void k_xbar_vmm(VmmArgs va) {
     const double s_w_eff = ms.sw_num / wmax;
     scale = QADC ? (float)(ps.lsb / (ps.s_v * s_w_eff)) : (float)(1.0 / (ps.s_v * s_w_eff));
   }
+  // Y is Bv x Q, or NCHW with H_out W_out = hw_out: the element of (bv, q)
+  // is row_base(bv) + q times the column stride.  The int32 workspace is
+  // Bv x Q (lanes along q: coalesced atomics).
+  const int64_t qstride = va.hw_out > 0 ? va.hw_out : 1;
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt)
+    for (int v = 0; v < 4; ++v) {
+      const int64_t bv = b0 + wave * 32 + mt * 16 + 4 * g + v;
+      if (bv >= va.Bv) continue;
+      int64_t row_base;
+      if (va.hw_out > 0) {
+        const int64_t img = bv / va.hw_out;
+        row_base = img * ms.Q * va.hw_out + (bv - img * va.hw_out);
+      } else {
+        row_base = bv * ms.Q;
+      }
 #pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        const int64_t bv = b0 + wave * 32 + mt * 16 + 4 * g + v;
+      for (int nt = 0; nt < NT; ++nt) {
         const int n = n0 + nt * 16 + li;
         const int64_t q = (int64_t)c * ms.N + n;
-        if (bv >= va.Bv || n >= ms.N || q >= ms.Q) continue;
-        if (va.iacc) {
+        if (n >= ms.N || q >= ms.Q) continue;
+        const int64_t e = row_base + q * qstride;
+        if (atomic) {
           atomicAdd(&va.iacc[bv * ms.Q + q], iacc[mt][nt][v]);
-          continue;
-        }
-        const float y = QADC ? (float)iacc[mt][nt][v] * scale : facc[mt][nt][v] * scale;
-        if (va.hw_out > 0) {
-          const int64_t img = bv / va.hw_out, pix = bv - img * va.hw_out;
-          va.Y[(img * ms.Q + q) * va.hw_out + pix] = y;
         } else {
-          va.Y[bv * ms.Q + q] = y;
+          va.Y[e] = QADC ? (float)iacc[mt][nt][v] * scale : facc[mt][nt][v] * scale;
         }
       }
+    }
+  };
+
+  auto tile_at = [&](int bx, int cb, int r_begin, int r_end, bool atomic)
+                     __attribute__((always_inline)) {
+    // column blocks: every block of a full column tile, and of the last tile
+    // only those that hold real output columns (padded columns are discarded)
+    const int c = min(cb / nblk_per_tile, ms.C - 1);
+    run_tile((int64_t)bx * BM, c, (cb - c * nblk_per_tile) * BN, r_begin, r_end, atomic);
+  };
+  // One workgroup per tile, or persistent workers: worker w first takes the
+  // whole tiles w, w + W, ... below dp_tiles (the full rounds of the GPU), then
+  // the units (tile, row tile) of the remaining tiles in the range
+  // [U w / W, U (w + 1) / W) (tile-major), which may cover parts of tiles.
+  int64_t u, u1, t_dp, dp_end;
+  bool shared_units = false;
+  if (va.workers == 0) {
+    u = ((int64_t)blockIdx.x * va.n_cb + blockIdx.y) * ms.R;
+    u1 = u + ms.R;
+    t_dp = dp_end = 0;
+  } else {
+    const int64_t n_tiles = (int64_t)((va.Bv + BM - 1) / BM) * va.n_cb;
+    const int64_t U = (n_tiles - va.dp_tiles) * ms.R;
+    u = va.dp_tiles * ms.R + U * blockIdx.x / va.workers;
+    u1 = va.dp_tiles * ms.R + U * (blockIdx.x + 1) / va.workers;
+    t_dp = blockIdx.x;
+    dp_end = va.dp_tiles;
+    shared_units = true;
+  }
+  for (;;) {
+    int64_t t;
+    int r0, r1;
+    bool atomic;
+    if (t_dp < dp_end) {
+      t = t_dp;
+      r0 = 0;
+      r1 = ms.R;
+      atomic = false;
+      t_dp += va.workers;
+    } else if (u < u1) {
+      t = u / ms.R;
+      r0 = (int)(u - t * ms.R);
+      r1 = (int)min((int64_t)ms.R, r0 + (u1 - u));
+      atomic = shared_units;
+      u += r1 - r0;
+    } else {
+      break;
+    }
+    tile_at((int)(t / va.n_cb), (int)(t % va.n_cb), r0, r1, atomic);
+  }
 }
 
-template <typename IDX>
-__global__ void k_finish(MapScalars ms, PeriphScalars ps, const int32_t* __restrict__ iacc,
-                         IDX Bv, float* __restrict__ Y, IDX hw_out) {
+// Y = fp32(acc) * scale_out from the Bv x Q int32 workspace: FC (Y has the
+// same layout) elementwise.
+__global__ __launch_bounds__(256) void k_finish(MapScalars ms, PeriphScalars ps,
+                                                const int32_t* __restrict__ iacc,
+                                                float* __restrict__ Y, int64_t n) {
   const double wmax = ms.wmax_fixed > 0.0f ? (double)ms.wmax_fixed : (double)*ms.d_wmax;
   float scale = 0.0f;
   if (wmax > 0.0) scale = (float)(ps.lsb / (ps.s_v * (ms.sw_num / wmax)));
-  const IDX Q = (IDX)ms.Q;
-  const IDX total = Bv * Q;
-  for (IDX e = (IDX)blockIdx.x * blockDim.x + threadIdx.x; e < total;
-       e += (IDX)gridDim.x * blockDim.x) {
-    const IDX bv = e / Q, q = e - bv * Q;
-    const float y = (float)iacc[e] * scale;
-    if (hw_out > 0) {
-      const IDX img = bv / hw_out, pix = bv - img * hw_out;
-      Y[(img * Q + q) * hw_out + pix] = y;
-    } else {
-      Y[e] = y;
+  const int64_t n4 = n >> 2;
+  const int4* a4 = reinterpret_cast<const int4*>(iacc);
+  float4* y4 = reinterpret_cast<float4*>(Y);
+  const bool aligned = ((uintptr_t)Y & 15) == 0;
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (aligned) {
+    for (; e < n4; e += stride) {
+      const int4 a = a4[e];
+      y4[e] = make_float4((float)a.x * scale, (float)a.y * scale, (float)a.z * scale,
+                          (float)a.w * scale);
     }
+    e = 4 * n4 + (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   }
+  for (; e < n; e += stride) Y[e] = (float)iacc[e] * scale;
+}
+
+// Convolution: 64 x 64 blocks of the workspace go through LDS, so that both
+// the Bv x Q reads and the NCHW writes are coalesced.
+__global__ __launch_bounds__(256) void k_finish_nchw(MapScalars ms, PeriphScalars ps,
+                                                     const int32_t* __restrict__ iacc,
+                                                     float* __restrict__ Y, int64_t row0,
+                                                     int64_t Bv, int64_t hw) {
+  __shared__ int32_t tile[64][65];
+  const double wmax = ms.wmax_fixed > 0.0f ? (double)ms.wmax_fixed : (double)*ms.d_wmax;
+  float scale = 0.0f;
+  if (wmax > 0.0) scale = (float)(ps.lsb / (ps.s_v * (ms.sw_num / wmax)));
+  const int64_t bv0 = row0 + (int64_t)blockIdx.x * 64;
+  const int64_t q0 = (int64_t)blockIdx.y * 64;
+  const int t = threadIdx.x & 63, u = threadIdx.x >> 6;
+  for (int i = u; i < 64; i += 4)
+    if (bv0 + i < Bv && q0 + t < ms.Q) tile[i][t] = iacc[(bv0 + i) * ms.Q + q0 + t];
+  __syncthreads();
+  const int64_t bv = bv0 + t;
+  if (bv >= Bv) return;
+  const int64_t img = bv / hw, pix = bv - img * hw;
+  for (int i = u; i < 64; i += 4)
+    if (q0 + i < ms.Q) Y[(img * ms.Q + q0 + i) * hw + pix] = (float)tile[t][i] * scale;
 }
 
 // Table of the patch columns of a convolution, per row tile r and tile input
@@ -524,6 +636,37 @@ int pick_bn(int Np) {
   return 16;
 }
 
+// Column blocks of the grid: every block of a full column tile, and of the
+// last tile only those holding real outputs (all of them for the debug entry,
+// which reports the padded columns' currents too).
+int col_blocks(const MapScalars& ms, int bn, bool debug) {
+  const int64_t q_last = ms.Q - (int64_t)(ms.C - 1) * ms.N;
+  const int blk_last = debug ? ms.Np / bn : (int)((q_last + bn - 1) / bn);
+  return (ms.C - 1) * (ms.Np / bn) + blk_last;
+}
+
+// Workgroups of the quantising evaluation kernel resident on the device at once.
+template <int BN, bool CONV>
+int64_t slots_t(const PeriphScalars& ps) {
+  int dev = 0, cus = 0, per_cu = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return 0;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+    return 0;
+  auto kern = k_xbar_vmm<BN, CONV, true, false>;
+  if (allow_adc_table(kern) != hipSuccess) return 0;
+  const size_t shm = (size_t)(ps.n_buckets + 2) * sizeof(float2);
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void*>(kern),
+                                                   NTHR, shm) != hipSuccess)
+    return 0;
+  return (int64_t)cus * per_cu;
+}
+
+int64_t slots_for(int bn, bool conv, const PeriphScalars& ps) {
+  if (bn == 64) return conv ? slots_t<64, true>(ps) : slots_t<64, false>(ps);
+  if (bn == 32) return conv ? slots_t<32, true>(ps) : slots_t<32, false>(ps);
+  return conv ? slots_t<16, true>(ps) : slots_t<16, false>(ps);
+}
+
 ConvGeom conv_geom(const rxnn_conv_desc& cd) {
   ConvGeom cg;
   cg.c_in = cd.c_in;
@@ -542,40 +685,63 @@ ConvGeom conv_geom(const rxnn_conv_desc& cd) {
 
 }  // namespace
 
-int choose_splits(const MapScalars& ms, const PeriphScalars& ps, int64_t Bv) {
-  if (ps.adc_bits == 0 || ms.R < 2) return 1;
+VmmPlan vmm_plan(const MapScalars& ms, const PeriphScalars& ps, int64_t Bv, bool conv) {
+  VmmPlan pl{0, 0, 0};
+  // fp32 accumulation (ideal ADC) keeps one workgroup per tile: a fixed order
+  if (ps.adc_bits == 0 || ms.R < 2 || Bv <= 0) return pl;
   const int bn = pick_bn(ms.Np);
-  const int64_t col_blocks = (int64_t)(ms.C - 1) * (ms.Np / bn) +
-                             (ms.Q - (int64_t)(ms.C - 1) * ms.N + bn - 1) / bn;
-  const int64_t blocks = ((Bv + BM - 1) / BM) * col_blocks;
-  if (blocks >= 512) return 1;
-  int64_t want = (1024 + blocks - 1) / blocks;
-  if (want > ms.R) want = ms.R;
-  const int per = (int)((ms.R + want - 1) / want);
-  return (ms.R + per - 1) / per;
+  const int n_cb = col_blocks(ms, bn, false);
+  const int64_t tiles = ((Bv + BM - 1) / BM) * n_cb;
+  const int64_t slots = slots_for(bn, conv, ps);
+  if (slots <= 0) return pl;
+  // one workgroup per tile fills the last round of the GPU only partly; when
+  // that wastes more than 10 %, the full rounds stay whole-tile work and the
+  // remaining tiles are shared evenly by (tile, row tile) units
+  const int64_t rounds = (tiles + slots - 1) / slots;
+  if ((double)tiles >= 0.9 * (double)(rounds * slots)) return pl;
+  const int64_t dp = ((tiles / slots) * slots / n_cb) * n_cb;   // whole row blocks
+  const int64_t units = (tiles - dp) * ms.R;
+  pl.workers = (int)(units + dp < slots ? units + dp : slots);
+  pl.dp_tiles = dp;
+  pl.row0 = (dp / n_cb) * BM;
+  return pl;
 }
 
-int64_t dac_elems(const rxnn_conv_desc* conv, int64_t Bv, int64_t ldx) {
-  if (!conv) return Bv * ldx;
+int64_t fc_ldv(const MapScalars& ms) {
+  return ((int64_t)ms.R * ms.M + KC + 3) / 4 * 4;
+}
+
+int64_t dac_elems(const MapScalars& ms, const rxnn_conv_desc* conv, int64_t Bv) {
+  if (!conv) return Bv * fc_ldv(ms);
   return (int64_t)conv->n * conv->c_in * (conv->h + 2 * conv->pad) * (conv->w + 2 * conv->pad);
 }
 
-hipError_t launch_dac(const PeriphScalars& ps, const rxnn_conv_desc* conv, const float* X,
-                      float* V, int64_t n, hipStream_t s) {
-  if (n <= 0) return hipSuccess;
-  int64_t blocks = (n + 255) / 256;
-  if (blocks > 16384) blocks = 16384;
-  if (conv)
-    hipLaunchKernelGGL(k_dac<true>, dim3((unsigned)blocks), dim3(256), 0, s, ps,
-                       conv_geom(*conv), X, V, n);
-  else
-    hipLaunchKernelGGL(k_dac<false>, dim3((unsigned)blocks), dim3(256), 0, s, ps, ConvGeom{},
-                       X, V, n);
+hipError_t launch_dac(const MapScalars& ms, const PeriphScalars& ps,
+                      const rxnn_conv_desc* conv, const float* X, int64_t Bv, float* V,
+                      hipStream_t s) {
+  if (Bv <= 0) return hipSuccess;
+  if (conv) {
+    const ConvGeom cg = conv_geom(*conv);
+    const int64_t planes = (int64_t)conv->n * conv->c_in;
+    const int per_plane = (cg.hp * cg.wp + 255) / 256;
+    hipLaunchKernelGGL(k_dac<true>, dim3((unsigned)(per_plane < 64 ? per_plane : 64),
+                                         (unsigned)(planes < 32768 ? planes : 32768)),
+                       dim3(256), 0, s, ps, cg, X, V, planes);
+  } else {
+    ConvGeom cg{};
+    cg.c_in = (int)ms.P;
+    cg.wp = (int)fc_ldv(ms);
+    const int per_row = (cg.wp + 255) / 256;
+    hipLaunchKernelGGL(k_dac<false>, dim3((unsigned)(per_row < 64 ? per_row : 64),
+                                          (unsigned)(Bv < 32768 ? Bv : 32768)),
+                       dim3(256), 0, s, ps, cg, X, V, Bv);
+  }
   return hipGetLastError();
 }
 
 hipError_t launch_xbar_vmm(const MapScalars& ms, const PeriphScalars& ps, const float* gpt,
-                           const VmmLaunch& vl, int splits, hipStream_t s) {
+                           const VmmLaunch& vl, const VmmPlan& plan, hipStream_t s) {
+  const int workers = plan.workers;
   VmmArgs va;
   va.ms = ms;
   va.ps = ps;
@@ -590,14 +756,13 @@ hipError_t launch_xbar_vmm(const MapScalars& ms, const PeriphScalars& ps, const 
   va.dbg_I = vl.dbg_I;
   va.dbg_code = vl.dbg_code;
   va.ktab = vl.ktab;
-  va.r_per_split = (ms.R + splits - 1) / splits;
   const int bn = pick_bn(ms.Np);
-  // the debug entry reports the currents of every column, padded ones included
   const bool debug = vl.dbg_I != nullptr || vl.dbg_code != nullptr;
-  const int64_t q_last = ms.Q - (int64_t)(ms.C - 1) * ms.N;   // real columns of the last tile
-  const int blk_last = debug ? ms.Np / bn : (int)((q_last + bn - 1) / bn);
-  dim3 grid((unsigned)((vl.Bv + BM - 1) / BM), (unsigned)((ms.C - 1) * (ms.Np / bn) + blk_last),
-            (unsigned)((ms.R + va.r_per_split - 1) / va.r_per_split));
+  va.n_cb = col_blocks(ms, bn, debug);
+  va.workers = workers;
+  va.dp_tiles = plan.dp_tiles;
+  const dim3 grid = workers > 0 ? dim3((unsigned)workers)
+                                : dim3((unsigned)((vl.Bv + BM - 1) / BM), (unsigned)va.n_cb);
   const bool qadc = ps.adc_bits > 0;
   const bool conv = vl.conv != nullptr;
   if (bn == 64) return launch_bn<64>(va, grid, s, conv, qadc, debug);
@@ -619,16 +784,20 @@ hipError_t launch_conv_ktab(const MapScalars& ms, const rxnn_conv_desc& cd, int*
 }
 
 hipError_t launch_finish(const MapScalars& ms, const PeriphScalars& ps, const int32_t* iacc,
-                         int64_t Bv, float* Y, int64_t hw_out, hipStream_t s) {
-  int64_t blocks = (Bv * ms.Q + 255) / 256;
-  if (blocks > 8192) blocks = 8192;
+                         int64_t row0, int64_t Bv, float* Y, int64_t hw_out, hipStream_t s) {
+  if (Bv <= row0) return hipSuccess;
+  if (hw_out > 0) {
+    const dim3 grid((unsigned)((Bv - row0 + 63) / 64), (unsigned)((ms.Q + 63) / 64));
+    hipLaunchKernelGGL(k_finish_nchw, grid, dim3(256), 0, s, ms, ps, iacc, Y, row0, Bv, hw_out);
+    return hipGetLastError();
+  }
+  iacc += row0 * ms.Q;
+  Y += row0 * ms.Q;
+  const int64_t n = (Bv - row0) * ms.Q;
+  int64_t blocks = (n / 4 + 255) / 256;
+  if (blocks > 4096) blocks = 4096;
   if (blocks < 1) blocks = 1;
-  if (Bv * ms.Q < ((int64_t)1 << 31))
-    hipLaunchKernelGGL(k_finish<int32_t>, dim3((unsigned)blocks), dim3(256), 0, s, ms, ps, iacc,
-                       (int32_t)Bv, Y, (int32_t)hw_out);
-  else
-    hipLaunchKernelGGL(k_finish<int64_t>, dim3((unsigned)blocks), dim3(256), 0, s, ms, ps, iacc,
-                       Bv, Y, hw_out);
+  hipLaunchKernelGGL(k_finish, dim3((unsigned)blocks), dim3(256), 0, s, ms, ps, iacc, Y, n);
   return hipGetLastError();
 }
 
