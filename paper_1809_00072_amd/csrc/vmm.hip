@@ -274,7 +274,11 @@ __global__ __launch_bounds__(NTHR, 2) void k_xbar_vmm(VmmArgs va) {
         // this thread gathers k = 4 (kq_cv + 2 q) .. + 3, q = 0 .. 7, of its
         // pixel; table entries of missing inputs point at the window origin
         // and are zeroed when staged
-        const int* kt = va.ktab + __builtin_amdgcn_readfirstlane(r * (nkc * KC) + kc0 + 4 * kq_cv);
+        // the table is read-only for the kernel: reading it through the
+        // constant address space gives scalar loads
+        typedef const __attribute__((address_space(4))) int cint4;
+        cint4* kt = (cint4*)(uintptr_t)(va.ktab + __builtin_amdgcn_readfirstlane(
+                                                    r * (nkc * KC) + kc0 + 4 * kq_cv));
 #pragma unroll
         for (int q = 0; q < XPT / 4; ++q)
 #pragma unroll
