@@ -9,6 +9,20 @@ ADC, 1 kOhm driver and sense, 2.5 Ohm wire segments).
 
 Prints one JSON line.  Kernel durations come from HIP events that the
 library records around each of its launches on the launch stream.
+
+--workload selects one of the other workloads instead (each prints its own
+line; the default is the convolution above):
+  fc256      FC 256 -> 128, batch 16, 64 x 64 crossbars (launch bound);
+  resnet18   the 21 layers of a ResNet-18 shaped stack, 128 x 128 crossbars,
+             wire 1 Ohm, batch 64, each layer on its own seeded input; a step
+             evaluates every layer (G' mapped once);
+  vgg16fc    the VGG-16 shaped FC head 25088 -> 4096 -> 4096 -> 1000, batch
+             256, 8-bit weights in four 2-bit slices; a step evaluates the
+             three layers;
+  resnet50   the 54 layers of a ResNet-50 shaped stack, batch 128, crossbar
+             side --crossbar (32 / 64 / 128 / 256), wire --wire; a step
+             perturbs every layer's weights, rebuilds G' and evaluates it
+             (reported: the whole step and the evaluation alone).
 """
 
 from __future__ import annotations
@@ -24,6 +38,11 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 FP32_MFMA_PEAK_TFLOPS = 157.3   # MI355X dense fp32 matrix
+# HBM bytes per launch of k_xbar_vmm on the convolution workload, from the
+# FETCH_SIZE / WRITE_SIZE counters of this kernel version, each scaled by what
+# the counter reads for a plain 2 GiB copy (fetch x 2.000, write x 1.000);
+# the summary and its commands are in the repository's profiles folder
+VMM_TRAFFIC_BYTES = 2.0 * 29888 * 1024 + 48362 * 1024
 FP64_PEAK_TFLOPS = 78.6         # MI355X fp64 (vector and matrix)
 HBM_PEAK_GBS = 8000.0
 
@@ -79,6 +98,175 @@ def cpu_baseline(work):
                       % (lay["R"] * lay["C"] * lay["A"], t1 - t0, work["conv"]["n"], t2 - t1)}
 
 
+KERNEL_NAMES = ("wmax", "nd_block", "nd_merge", "nd_final", "gprime_sweep", "dac", "ktab",
+                "fill", "xbar_vmm", "finish")
+
+
+def read_kernels(rxnn, steps):
+    kern = {}
+    for name in KERNEL_NAMES:
+        tot, cnt = rxnn.profile_read(name)
+        if cnt:
+            kern[name] = {"avg_us": 1e3 * tot / cnt, "launches": cnt,
+                          "us_per_step": 1e3 * tot / steps}
+    return kern
+
+
+def copy_probe(torch, dev):
+    """A plain elementwise copy of known size, for scaling HBM byte counters.
+    The 2 GiB source is written first and then a 1 GiB buffer, so that
+    little of the source is left in the 256 MB last-level cache."""
+    n = 512 << 20
+    a = torch.rand(n, device=dev)
+    flush = torch.empty(256 << 20, device=dev)
+    flush.fill_(1.0)
+    b = torch.empty_like(a)
+    torch.mul(a, 1.0, out=b)
+    torch.cuda.synchronize()
+    print("[bench] copy probe: %d bytes read, %d bytes written" % (4 * n, 4 * n),
+          file=sys.stderr, flush=True)
+
+
+def bench_fc256(args):
+    """FC 256 -> 128, batch 16 (launch bound; absolute time only)."""
+    import torch
+    from paper_1809_00072_amd import rxnn, workloads as wl
+    rxnn.load()
+    w = wl.fc_256x128()
+    dev = torch.device("cuda:0")
+    Wd = torch.from_numpy(w["W"]).to(dev)
+    Xd = torch.from_numpy(w["X"]).to(dev)
+    L = rxnn.map_layer(Wd, w["xbar"])
+    Y = rxnn.crossbar_vmm(L, w["periph"], Xd)
+    stream = torch.cuda.current_stream()
+    for _ in range(args.warmup):
+        rxnn.crossbar_vmm(L, w["periph"], Xd, Y, stream)
+    torch.cuda.synchronize()
+    rxnn.profile_reset()
+    rxnn.profile_enable(True)
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ev0.record(stream)
+    for _ in range(args.steps):
+        rxnn.crossbar_vmm(L, w["periph"], Xd, Y, stream)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    rxnn.profile_enable(False)
+    ms = ev0.elapsed_time(ev1) / args.steps
+    macs = wl.alg_macs(w)
+    out = {"metric": "non-ideal crossbar MACs/sec per layer", "value": macs / (ms * 1e-3),
+           "unit": "MAC/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+           "ms_per_step": ms, "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+           "dtype": "f32", "data": "synthetic",
+           "config": {"workload": "fc256->128, batch 16, 64x64 crossbars, 4-bit DAC / 8-bit ADC; "
+                                  "step = evaluation (launch bound)", "alg_macs_per_step": macs},
+           "kernels": read_kernels(rxnn, args.steps)}
+    L.free()
+    print(json.dumps(out), flush=True)
+
+
+def bench_stack(args):
+    """Every layer of a stacked workload, standalone on its seeded input."""
+    import numpy as np
+    import torch
+    from paper_1809_00072_amd import rxnn, workloads as wl
+    rxnn.load()
+    assert torch.cuda.is_available(), "bench.py needs the HIP device"
+    dev = torch.device("cuda:0")
+    cfg = args.workload
+    n_layers = {"resnet18": len(wl.resnet18_layers()), "vgg16fc": len(wl.vgg16_fc_layers()),
+                "resnet50": len(wl.resnet50_layers())}[cfg]
+    rebuild = cfg == "resnet50"
+    layers = []
+    print("[bench] %s: generating %d layers" % (cfg, n_layers), file=sys.stderr, flush=True)
+    for l in range(n_layers):
+        w = wl.stack_layer(cfg, l, crossbar=args.crossbar if rebuild else None,
+                           wire=args.wire if rebuild else None)
+        Wd = torch.from_numpy(w["W"]).to(dev)
+        Xd = torch.from_numpy(w["X"]).to(dev)
+        L = rxnn.map_layer(Wd, w["xbar"])
+        if w["kind"] == "conv":
+            Y = rxnn.conv_layer(L, w["periph"], w["conv"], Xd)
+        else:
+            Y = rxnn.crossbar_vmm(L, w["periph"], Xd)
+        ent = {"w": w, "L": L, "X": Xd, "Y": Y, "W": Wd, "Wt": []}
+        if rebuild:
+            # model-in-the-loop update of every step: W + 1e-3 sigma eps_t
+            sigma = float(np.sqrt(2.0 / w["W"].shape[0]))
+            for t in range(args.warmup + args.steps):
+                g = torch.Generator(device=dev).manual_seed(3000 + t)
+                eps = torch.randn(Wd.shape, generator=g, device=dev)
+                ent["Wt"].append(Wd + 1e-3 * sigma * eps)
+        del w["X"]
+        layers.append(ent)
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+
+    def evaluate(e):
+        w = e["w"]
+        if w["kind"] == "conv":
+            rxnn.conv_layer(e["L"], w["periph"], w["conv"], e["X"], e["Y"], stream)
+        else:
+            rxnn.crossbar_vmm(e["L"], w["periph"], e["X"], e["Y"], stream)
+
+    def step(t):
+        for e in layers:
+            if rebuild:
+                rxnn.remap_layer(e["L"], e["Wt"][t], stream)
+            evaluate(e)
+
+    for t in range(args.warmup):
+        step(t)
+    torch.cuda.synchronize()
+    rxnn.profile_reset()
+    rxnn.profile_enable(True)
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ev0.record(stream)
+    for t in range(args.steps):
+        step(args.warmup + t)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    rxnn.profile_enable(False)
+    step_ms = ev0.elapsed_time(ev1) / args.steps
+    kern = read_kernels(rxnn, args.steps)
+    # evaluation alone (G' kept)
+    ev0.record(stream)
+    for _ in range(args.steps):
+        for e in layers:
+            evaluate(e)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    eval_ms = ev0.elapsed_time(ev1) / args.steps
+    macs = wl.stack_alg_macs(cfg)
+    vmm_us = sum(kern[k]["us_per_step"] for k in ("xbar_vmm",) if k in kern)
+    ach = 2.0 * macs / (vmm_us * 1e-6) / 1e12
+    desc = {"resnet18": "ResNet-18 shaped stack (21 layers), batch 64, 128x128 crossbars, "
+                        "wire 1 ohm, 8-bit DAC/ADC; step = evaluation of every layer",
+            "vgg16fc": "VGG-16 shaped FC head 25088->4096->4096->1000, batch 256, 64x64 "
+                       "crossbars, 8-bit weights in 4x2-bit slices, 8-bit DAC/ADC; step = "
+                       "evaluation of the three layers",
+            "resnet50": "ResNet-50 shaped stack (54 layers), batch 128, %dx%d crossbars, wire "
+                        "%g ohm, 8-bit DAC/ADC; step = weight update + G' rebuild + evaluation "
+                        "of every layer" % (args.crossbar, args.crossbar, args.wire)}[cfg]
+    value_ms = step_ms
+    out = {
+        "metric": "non-ideal crossbar MACs/sec per layer",
+        "value": macs / (value_ms * 1e-3),
+        "unit": "MAC/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": value_ms, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "config": {"workload": desc, "alg_macs_per_step": macs,
+                   "arrays": int(sum(e["L"].R * e["L"].C * e["L"].A for e in layers))},
+        "roofline": {"kernel": "k_xbar_vmm (all layers)", "bound": "mfma", "achieved": ach,
+                     "peak": FP32_MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
+                     "frac": ach / FP32_MFMA_PEAK_TFLOPS, "traffic": None},
+        "eval_only": {"ms": eval_ms, "value": macs / (eval_ms * 1e-3), "unit": "MAC/s"},
+        "kernels": kern,
+    }
+    for e in layers:
+        e["L"].free()
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -86,12 +274,20 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-probe", action="store_true",
-                    help="also run a plain 256 MiB copy kernel (counter calibration)")
+                    help="also run a plain 2 GiB copy kernel (counter calibration)")
+    ap.add_argument("--workload", default="conv3x3",
+                    choices=["conv3x3", "fc256", "resnet18", "vgg16fc", "resnet50"])
+    ap.add_argument("--crossbar", type=int, default=256, help="resnet50: crossbar side")
+    ap.add_argument("--wire", type=float, default=2.5, help="resnet50: wire resistance (Ohm)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU: the crossbar path is built and measured on a "
               "single MI355X; --gpus %d is not supported" % args.gpus, file=sys.stderr)
         sys.exit(2)
+    if args.workload in ("resnet18", "vgg16fc", "resnet50"):
+        return bench_stack(args)
+    if args.workload == "fc256":
+        return bench_fc256(args)
 
     import numpy as np
     import torch
@@ -137,13 +333,7 @@ def main():
     wall = time.perf_counter() - w0
     rxnn.profile_enable(False)
     step_ms = ev0.elapsed_time(ev1) / args.steps
-    kern = {}
-    for name in ("wmax", "nd_block", "nd_merge", "nd_final", "gprime_sweep", "xbar_vmm",
-                 "fill", "finish"):
-        tot, cnt = rxnn.profile_read(name)
-        if cnt:
-            kern[name] = {"avg_us": 1e3 * tot / cnt, "launches": cnt,
-                          "us_per_step": 1e3 * tot / args.steps}
+    kern = read_kernels(rxnn, args.steps)
     print("[bench] timed %d steps: %.3f ms/step" % (args.steps, step_ms), file=sys.stderr,
           flush=True)
 
@@ -161,7 +351,7 @@ def main():
     ach = 2.0 * macs / (vmm_us * 1e-6) / 1e12
     roof = {"kernel": "k_xbar_vmm", "bound": "mfma", "achieved": ach,
             "peak": FP32_MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
-            "frac": ach / FP32_MFMA_PEAK_TFLOPS, "traffic": None}
+            "frac": ach / FP32_MFMA_PEAK_TFLOPS, "traffic": VMM_TRAFFIC_BYTES}
     build_us = sum(kern[k]["us_per_step"] for k in ("nd_block", "nd_merge", "nd_final",
                                                      "gprime_sweep") if k in kern)
     b_ach = n_arrays * build_flops(L.M, L.N) / (build_us * 1e-6) / 1e12
@@ -169,14 +359,7 @@ def main():
              "peak": FP64_PEAK_TFLOPS, "unit": "TFLOP/s", "frac": b_ach / FP64_PEAK_TFLOPS}
 
     if args.copy_probe:
-        # a plain elementwise copy of known size, for scaling HBM byte counters
-        n = 64 << 20
-        a = torch.rand(n, device=dev)
-        b = torch.empty_like(a)
-        torch.mul(a, 1.0, out=b)
-        torch.cuda.synchronize()
-        print("[bench] copy probe: %d bytes read, %d bytes written" % (4 * n, 4 * n),
-              file=sys.stderr, flush=True)
+        copy_probe(torch, dev)
 
     out = {
         "metric": "non-ideal crossbar MACs/sec per layer",
