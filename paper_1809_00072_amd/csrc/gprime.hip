@@ -239,13 +239,19 @@ __global__ __launch_bounds__(TG* TG) void k_gprime_build(MapScalars ms, const fl
     }
 }
 
-__global__ void k_absmax(const float* __restrict__ W, int64_t n, unsigned* out) {
+// max |W| as the bit pattern of a non-negative float (ordered like the
+// value): wave then workgroup reduction, one atomic per workgroup
+__global__ __launch_bounds__(256) void k_absmax(const float* __restrict__ W, int64_t n,
+                                                unsigned* out) {
+  __shared__ unsigned wm[4];
   unsigned m = 0;
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
        i += (int64_t)gridDim.x * blockDim.x)
     m = max(m, __float_as_uint(fabsf(W[i])));
   for (int off = 32; off > 0; off >>= 1) m = max(m, (unsigned)__shfl_xor((int)m, off, 64));
-  if ((threadIdx.x & 63) == 0) atomicMax(out, m);
+  if ((threadIdx.x & 63) == 0) wm[threadIdx.x >> 6] = m;
+  __syncthreads();
+  if (threadIdx.x == 0) atomicMax(out, max(max(wm[0], wm[1]), max(wm[2], wm[3])));
 }
 
 __global__ void k_fill_u32(unsigned* p, int64_t n, unsigned v) {
@@ -257,8 +263,8 @@ __global__ void k_fill_u32(unsigned* p, int64_t n, unsigned v) {
 }  // namespace
 
 hipError_t launch_absmax(const float* W, int64_t n, unsigned* out, hipStream_t s) {
-  int64_t blocks = (n + 255) / 256;
-  if (blocks > 4096) blocks = 4096;
+  int64_t blocks = (n + 4095) / 4096;   // at least 16 elements per thread
+  if (blocks > 512) blocks = 512;
   if (blocks < 1) blocks = 1;
   hipLaunchKernelGGL(k_absmax, dim3((unsigned)blocks), dim3(256), 0, s, W, n, out);
   return hipGetLastError();

@@ -122,13 +122,12 @@ __global__ __launch_bounds__(256) void k_dac(PeriphScalars ps, ConvGeom cg, cons
     return fmaxf(x, 0.0f) * ps.s_v_ideal;
   };
   if (CONV) {
-    // planes (img, ci) over blockIdx.y; threads stride over the padded plane
+    // planes (img, ci) over the blocks; threads stride over the padded plane
     const int plane_p = cg.hp * cg.wp;
-    for (int64_t plane = blockIdx.y; plane < n_out; plane += gridDim.y) {
+    for (int64_t plane = blockIdx.x; plane < n_out; plane += gridDim.x) {
       const float* Xp = X + plane * cg.h * cg.w;
       float* Vp = V + plane * plane_p;
-      for (int e = blockIdx.x * blockDim.x + threadIdx.x; e < plane_p;
-           e += gridDim.x * blockDim.x) {
+      for (int e = threadIdx.x; e < plane_p; e += blockDim.x) {
         const int yp = e / cg.wp, xp = e - yp * cg.wp;
         const int iy = yp - cg.pad, ix = xp - cg.pad;
         float x = 0.0f;
@@ -139,8 +138,8 @@ __global__ __launch_bounds__(256) void k_dac(PeriphScalars ps, ConvGeom cg, cons
   } else {
     // rows b over blockIdx.y: V[b][p] = DAC(X[b][p]) for p < P, 0 up to ldv
     const int P = cg.c_in, ldv = cg.wp;
-    for (int64_t b = blockIdx.y; b < n_out; b += gridDim.y)
-      for (int p = blockIdx.x * blockDim.x + threadIdx.x; p < ldv; p += gridDim.x * blockDim.x)
+    for (int64_t b = blockIdx.x; b < n_out; b += gridDim.x)
+      for (int p = threadIdx.x; p < ldv; p += blockDim.x)
         V[b * ldv + p] = p < P ? dac(X[b * P + p]) : 0.0f;
   }
 }
@@ -727,18 +726,14 @@ hipError_t launch_dac(const MapScalars& ms, const PeriphScalars& ps,
   if (conv) {
     const ConvGeom cg = conv_geom(*conv);
     const int64_t planes = (int64_t)conv->n * conv->c_in;
-    const int per_plane = (cg.hp * cg.wp + 255) / 256;
-    hipLaunchKernelGGL(k_dac<true>, dim3((unsigned)(per_plane < 64 ? per_plane : 64),
-                                         (unsigned)(planes < 32768 ? planes : 32768)),
-                       dim3(256), 0, s, ps, cg, X, V, planes);
+    hipLaunchKernelGGL(k_dac<true>, dim3((unsigned)(planes < 8192 ? planes : 8192)), dim3(256),
+                       0, s, ps, cg, X, V, planes);
   } else {
     ConvGeom cg{};
     cg.c_in = (int)ms.P;
     cg.wp = (int)fc_ldv(ms);
-    const int per_row = (cg.wp + 255) / 256;
-    hipLaunchKernelGGL(k_dac<false>, dim3((unsigned)(per_row < 64 ? per_row : 64),
-                                          (unsigned)(Bv < 32768 ? Bv : 32768)),
-                       dim3(256), 0, s, ps, cg, X, V, Bv);
+    hipLaunchKernelGGL(k_dac<false>, dim3((unsigned)(Bv < 8192 ? Bv : 8192)), dim3(256), 0, s,
+                       ps, cg, X, V, Bv);
   }
   return hipGetLastError();
 }
