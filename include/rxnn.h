@@ -159,6 +159,10 @@ rxnn_status rxnn_remap_layer(rxnn_layer* layer, const float* W, void* stream);
  * accumulation over row tiles and arrays -> scale.
  *   X  device fp32 B x P row-major; Y  device fp32 B x Q row-major.
  *   B >= 0 (B = 0 is a no-op).
+ * The layer keeps a DAC output buffer (B x (R M + 64) floats) and, when the
+ * evaluation is shared across persistent workgroups, an int32 B x Q
+ * workspace; both grow on demand (RXNN_ENOMEM when they cannot).
+ * RXNN_EUNSUPPORTED when P >= 2^22 (32-bit buffer offsets).
  */
 rxnn_status rxnn_crossbar_vmm(const rxnn_layer* layer, const rxnn_periph_params* periph,
                               const float* X, int64_t B, float* Y, void* stream);
@@ -169,6 +173,11 @@ rxnn_status rxnn_crossbar_vmm(const rxnn_layer* layer, const rxnn_periph_params*
  * bv = (n H_out + oy) W_out + ox, padded pixels are 0.  The layer must have
  * been mapped with P = c_in kh kw and Q = c_out.
  *   X  device fp32 NCHW input; Y  device fp32 NCHW output n x c_out x H_out x W_out.
+ * The patch matrix is never written: the layer keeps a DAC output buffer
+ * (the input with pad zero pixels on every side), a table of patch-column
+ * offsets (rebuilt when the geometry changes) and, as for the FC entry, an
+ * int32 workspace when needed.  RXNN_EUNSUPPORTED when P >= 2^22 or when
+ * the padded images one 128-pixel block touches exceed 2 GiB.
  */
 rxnn_status rxnn_conv_layer(const rxnn_layer* layer, const rxnn_periph_params* periph,
                             const rxnn_conv_desc* conv, const float* X, float* Y,
@@ -207,8 +216,9 @@ void rxnn_free_layer(rxnn_layer* layer);
  * kernel it launches with HIP events on the launch stream and accumulates
  * the elapsed time per kernel name: "wmax" (w_max reduction), "nd_block",
  * "nd_merge", "nd_final" (G' build by nested dissection), "gprime_sweep" (G'
- * build by the row sweep), "xbar_vmm" (evaluation), "fill" and "finish"
- * (split accumulation).  rxnn_profile_read synchronises, folds pending events
+ * build by the row sweep), "dac" (DAC of the inputs), "ktab" (patch-column
+ * table), "xbar_vmm" (evaluation), "fill" and "finish" (workspace of the
+ * shared tiles).  rxnn_profile_read synchronises, folds pending events
  * into the totals and returns total milliseconds and launch count.
  */
 rxnn_status rxnn_profile_enable(int32_t on);
