@@ -451,12 +451,93 @@ __device__ void eliminate_lds(double* U, int c, int E, int ldu, double* isq) {
   __syncthreads();
 }
 
+// The same elimination in blocks of PB pivots: the pivot rows of a block are
+// eliminated among themselves, every later row then gets its PB multipliers
+// from its own entries in the block's columns, and one pass applies the
+// rank-PB update to the trailing rows.  The trailing matrix is read and
+// written once per block instead of once per pivot (the rank-1 form is bound
+// by that LDS traffic).  aux: LDS scratch of 4 (c + 1) doubles.
+template <int NT>
+__device__ void eliminate_lds_blocked(double* U, int c, int E, int ldu, double* isq,
+                                      double* aux) {
+  constexpr int PB = 4;
+  const int tid = threadIdx.x;
+  const int ncol = c + E;
+  const int lgy = lg2ceil(ncol);
+  double* lm = aux;               // multipliers, PB per row
+  double* inv = aux + PB * c;     // pivot reciprocals of the block
+  for (int k0 = 0; k0 < c; k0 += PB) {
+    const int kb = min(PB, c - k0);
+    // pivot rows of the block, among themselves
+    for (int i = 0; i < kb; ++i) {
+      const int k = k0 + i;
+      const double ik = recip(U[k * ldu + k]);
+      if (tid == 0) inv[i] = ik;
+      const int nr = kb - 1 - i;   // later rows of the block
+      for (int t = tid; t < nr << lgy; t += NT) {
+        const int y = t & ((1 << lgy) - 1);
+        if (y <= k || y >= ncol) continue;
+        const int x = k + 1 + (t >> lgy);
+        U[x * ldu + y] -= U[x * ldu + k] * ik * U[k * ldu + y];
+      }
+      __syncthreads();
+    }
+    const int r0 = k0 + kb;
+    // multipliers of the trailing rows
+    for (int x = r0 + tid; x < c; x += NT) {
+      double l[PB];
+#pragma unroll
+      for (int i = 0; i < PB; ++i) {
+        if (i >= kb) break;
+        double t = U[x * ldu + k0 + i];
+        for (int j = 0; j < i; ++j) t -= l[j] * U[(k0 + j) * ldu + k0 + i];
+        l[i] = t * inv[i];
+        lm[x * PB + i] = l[i];
+      }
+    }
+    __syncthreads();
+    // rank-kb update of the trailing rows, 8-row chunks per task
+    const int nxc = (c - r0 + 7) / 8;
+    for (int t = tid; t < nxc << lgy; t += NT) {
+      const int y = t & ((1 << lgy) - 1);
+      if (y < r0 || y >= ncol) continue;
+      const int x0 = r0 + (t >> lgy) * 8;
+      double p[PB];
+#pragma unroll
+      for (int i = 0; i < PB; ++i) p[i] = i < kb ? U[(k0 + i) * ldu + y] : 0.0;
+      double u[8];
+#pragma unroll
+      for (int xx = 0; xx < 8; ++xx) u[xx] = U[min(x0 + xx, c - 1) * ldu + y];
+#pragma unroll
+      for (int xx = 0; xx < 8; ++xx) {
+        const int x = x0 + xx;
+        if (x >= c) continue;
+        double v = u[xx];
+#pragma unroll
+        for (int i = 0; i < PB; ++i)
+          if (i < kb) v -= lm[x * PB + i] * p[i];
+        U[x * ldu + y] = v;
+      }
+    }
+    __syncthreads();
+  }
+  for (int t = tid; t < c; t += NT) isq[t] = 1.0 / sqrt(U[t * ldu + t]);
+  __syncthreads();
+  const int lge = lg2ceil(E);
+  for (int t = tid; t < c << lge; t += NT) {
+    const int k = t >> lge, y = t & ((1 << lge) - 1);
+    if (y < E) U[k * ldu + c + y] *= isq[k];
+  }
+  __syncthreads();
+}
+
 // One merge of two h x w blocks (children in buf_in, result to buf_out).
 template <bool LDSP, int NT>
 __global__ __launch_bounds__(NT) void k_nd_merge(NdArgs na) {
   extern __shared__ double lds[];   // cut rows (LDS path) or the blocked path's panels
   __shared__ short tab[2 * 1024];   // children of a 256 x 256 grid have up to 768 ports
   __shared__ double isq[256];
+  __shared__ double aux[4 * 257];
   const int tid = threadIdx.x;
   const int T = na.T, h = na.h, w = na.w;
   const bool vert = na.vert != 0;
@@ -522,7 +603,7 @@ __global__ __launch_bounds__(NT) void k_nd_merge(NdArgs na) {
     eliminate(cut, c, E, ldc, ext, Emax, lds);
     return;
   }
-  eliminate_lds<NT>(cut, c, E, ldc, isq);
+  eliminate_lds_blocked<NT>(cut, c, E, ldc, isq, aux);
   // ext -= Z^T Z, square tiles of TS x TS entries, 4 x 4 per thread
   constexpr int TS = NT == 1024 ? 128 : 64;
   const int rx = (tid / (TS / 4)) * 4, ry = (tid % (TS / 4)) * 4;
@@ -566,6 +647,7 @@ __global__ __launch_bounds__(LDSP ? NTB : NTH) void k_nd_final(NdArgs na) {
   constexpr int NT = LDSP ? NTB : NTH;
   extern __shared__ double lds[];
   __shared__ double isq[256];
+  __shared__ double aux[4 * 257];
   const int tid = threadIdx.x;
   const int T = na.T, M = na.ms.M, N = na.ms.N;
   const int64_t la = blockIdx.x;
@@ -604,7 +686,7 @@ __global__ __launch_bounds__(LDSP ? NTB : NTH) void k_nd_final(NdArgs na) {
     }
     return;
   }
-  eliminate_lds<NT>(cut, c, E, ldc, isq);
+  eliminate_lds_blocked<NT>(cut, c, E, ldc, isq, aux);
   const int lgm = lg2ceil(na.ms.Mp);
   for (int e = tid; e < na.ms.Np << lgm; e += NT) {
     const int j = e >> lgm, k = e & ((1 << lgm) - 1);
