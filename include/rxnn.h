@@ -217,8 +217,9 @@ void rxnn_free_layer(rxnn_layer* layer);
  * the elapsed time per kernel name: "wmax" (w_max reduction), "nd_block",
  * "nd_merge", "nd_final" (G' build by nested dissection), "gprime_sweep" (G'
  * build by the row sweep), "dac" (DAC of the inputs), "ktab" (patch-column
- * table), "xbar_vmm" (evaluation), "fill" and "finish" (workspace of the
- * shared tiles).  rxnn_profile_read synchronises, folds pending events
+ * table), "xbar_vmm" (evaluation), "fill" (clearing of a new evaluation
+ * workspace) and "finish" (workspace of the shared tiles to Y, which also
+ * leaves the workspace zeroed).  rxnn_profile_read synchronises, folds pending events
  * into the totals and returns total milliseconds and launch count.
  */
 rxnn_status rxnn_profile_enable(int32_t on);

@@ -169,6 +169,7 @@ rxnn_status grow_ws(rxnn_layer* L, size_t bytes) {
   }
   L->ws = p;
   L->ws_bytes = bytes;
+  L->ws_dirty = true;
   return RXNN_OK;
 }
 
@@ -229,11 +230,18 @@ rxnn_status run_vmm(const rxnn_layer* L, const PeriphScalars& ps, const float* X
   vl.dbg_I = dbgI;
   vl.dbg_code = dbgC;
   vl.ktab = ktab;
+  // The shared-tile units add into a zeroed workspace.  The finish kernel
+  // zeroes again every word it reads, and no other word is ever written, so
+  // the workspace is cleared only when new or after a call that did not end.
+  rxnn_layer* Lw = const_cast<rxnn_layer*>(L);
   if (workers > 0) {
     vl.iacc = iacc_ws;
-    ProfScope z("fill", s);
-    HIP_TRY(launch_fill_u32((unsigned*)iacc_ws + plan.row0 * ms.Q, (Bv - plan.row0) * ms.Q, 0u,
-                            s));
+    if (Lw->ws_dirty) {
+      ProfScope z("fill", s);
+      HIP_TRY(launch_fill_u32((unsigned*)Lw->ws, (int64_t)(Lw->ws_bytes / sizeof(unsigned)), 0u,
+                              s));
+    }
+    Lw->ws_dirty = true;   // until the finish kernel has been launched
   }
   {
     ProfScope t("xbar_vmm", s);
@@ -242,6 +250,7 @@ rxnn_status run_vmm(const rxnn_layer* L, const PeriphScalars& ps, const float* X
   if (workers > 0) {
     ProfScope t("finish", s);
     HIP_TRY(launch_finish(ms, ps, iacc_ws, plan.row0, Bv, Y, hw_out, s));
+    Lw->ws_dirty = false;
   }
   return RXNN_OK;
 }

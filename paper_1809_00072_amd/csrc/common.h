@@ -54,6 +54,7 @@ struct rxnn_layer {
   float* d_wmax;       // one float
   void* ws;            // scratch of the evaluation calls
   size_t ws_bytes;
+  bool ws_dirty;       // ws may hold non-zero words (new, or a call did not finish)
   double* nd_ws;       // nested-dissection build workspace (null: row sweep)
   int64_t nd_chunk;    // arrays built per pass over the workspace
   int nd_bs;           // side of the blocks reduced in LDS
@@ -112,7 +113,7 @@ int64_t dac_elems(const MapScalars& ms, const rxnn_conv_desc* conv, int64_t Bv);
 hipError_t launch_dac(const MapScalars& ms, const PeriphScalars& ps,
                       const rxnn_conv_desc* conv, const float* X, int64_t Bv, float* V,
                       hipStream_t s);
-hipError_t launch_finish(const MapScalars& ms, const PeriphScalars& ps, const int32_t* iacc,
+hipError_t launch_finish(const MapScalars& ms, const PeriphScalars& ps, int32_t* iacc,
                          int64_t row0, int64_t Bv, float* Y, int64_t hw_out, hipStream_t s);
 VmmPlan vmm_plan(const MapScalars& ms, const PeriphScalars& ps, int64_t Bv, bool conv);
 

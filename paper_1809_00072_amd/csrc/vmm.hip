@@ -531,13 +531,13 @@ __global__ __launch_bounds__(NTHR, 2) void k_xbar_vmm(VmmArgs va) {
 // Y = fp32(acc) * scale_out from the Bv x Q int32 workspace: FC (Y has the
 // same layout) elementwise.
 __global__ __launch_bounds__(256) void k_finish(MapScalars ms, PeriphScalars ps,
-                                                const int32_t* __restrict__ iacc,
+                                                int32_t* __restrict__ iacc,
                                                 float* __restrict__ Y, int64_t n) {
   const double wmax = ms.wmax_fixed > 0.0f ? (double)ms.wmax_fixed : (double)*ms.d_wmax;
   float scale = 0.0f;
   if (wmax > 0.0) scale = (float)(ps.lsb / (ps.s_v * (ms.sw_num / wmax)));
   const int64_t n4 = n >> 2;
-  const int4* a4 = reinterpret_cast<const int4*>(iacc);
+  int4* a4 = reinterpret_cast<int4*>(iacc);
   float4* y4 = reinterpret_cast<float4*>(Y);
   const bool aligned = ((uintptr_t)Y & 15) == 0;
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
@@ -545,18 +545,22 @@ __global__ __launch_bounds__(256) void k_finish(MapScalars ms, PeriphScalars ps,
   if (aligned) {
     for (; e < n4; e += stride) {
       const int4 a = a4[e];
+      a4[e] = make_int4(0, 0, 0, 0);   // the workspace is left zeroed for the next call
       y4[e] = make_float4((float)a.x * scale, (float)a.y * scale, (float)a.z * scale,
                           (float)a.w * scale);
     }
     e = 4 * n4 + (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   }
-  for (; e < n; e += stride) Y[e] = (float)iacc[e] * scale;
+  for (; e < n; e += stride) {
+    Y[e] = (float)iacc[e] * scale;
+    iacc[e] = 0;
+  }
 }
 
 // Convolution: 64 x 64 blocks of the workspace go through LDS, so that both
 // the Bv x Q reads and the NCHW writes are coalesced.
 __global__ __launch_bounds__(256) void k_finish_nchw(MapScalars ms, PeriphScalars ps,
-                                                     const int32_t* __restrict__ iacc,
+                                                     int32_t* __restrict__ iacc,
                                                      float* __restrict__ Y, int64_t row0,
                                                      int64_t Bv, int64_t hw) {
   __shared__ int32_t tile[64][65];
@@ -567,7 +571,10 @@ __global__ __launch_bounds__(256) void k_finish_nchw(MapScalars ms, PeriphScalar
   const int64_t q0 = (int64_t)blockIdx.y * 64;
   const int t = threadIdx.x & 63, u = threadIdx.x >> 6;
   for (int i = u; i < 64; i += 4)
-    if (bv0 + i < Bv && q0 + t < ms.Q) tile[i][t] = iacc[(bv0 + i) * ms.Q + q0 + t];
+    if (bv0 + i < Bv && q0 + t < ms.Q) {
+      tile[i][t] = iacc[(bv0 + i) * ms.Q + q0 + t];
+      iacc[(bv0 + i) * ms.Q + q0 + t] = 0;   // left zeroed for the next call
+    }
   __syncthreads();
   const int64_t bv = bv0 + t;
   if (bv >= Bv) return;
@@ -782,7 +789,7 @@ hipError_t launch_conv_ktab(const MapScalars& ms, const rxnn_conv_desc& cd, int*
   return hipGetLastError();
 }
 
-hipError_t launch_finish(const MapScalars& ms, const PeriphScalars& ps, const int32_t* iacc,
+hipError_t launch_finish(const MapScalars& ms, const PeriphScalars& ps, int32_t* iacc,
                          int64_t row0, int64_t Bv, float* Y, int64_t hw_out, hipStream_t s) {
   if (Bv <= row0) return hipSuccess;
   if (hw_out > 0) {

@@ -233,6 +233,21 @@ def test_fc_split_matches_unsplit():
     np.testing.assert_array_equal(Ys, Yd)
 
 
+def test_fc_workspace_reuse():
+    """The shared-tile workspace is cleared once and left zeroed by each call:
+    calls of several batch sizes on one layer (smaller, then larger than the
+    workspace) each equal the debug run, which uses no workspace, bit for bit."""
+    W, X, xb, pp = fc_case(1200, 40, 16, 16, 40, dac=6, adc=8, seed=11)
+    say("fc workspace reuse map")
+    L = rxnn.map_layer(dev(W), xb)
+    for B in (20, 7, 40, 20, 1):
+        say("fc workspace reuse B=%d" % B)
+        Yd = rxnn.vmm_debug(L, pp, dev(X[:B]))[0].cpu().numpy()
+        Yp = rxnn.crossbar_vmm(L, pp, dev(X[:B])).cpu().numpy()
+        np.testing.assert_array_equal(Yp, Yd)
+    L.free()
+
+
 def test_fc_batch_zero():
     W, X, xb, pp = fc_case(40, 20, 16, 16, 4)
     say("fc B=0")
@@ -337,3 +352,25 @@ def test_conv3x3_64_56_b32_sampled():
     w = wl.conv3x3_64_56()
     conv_compare(w["conv"], w["W"], w["X"], w["xbar"], w["periph"], images=[0, 31],
                  label="conv3x3 64->64 56x56 b32")
+
+
+def test_conv3x3_workspace_reuse():
+    """Repeated calls on the benchmarked layer (whole-tile rounds plus shared
+    tiles): the images are independent, so a call on the first 5 images
+    equals those images of the full call, and a repeated full call equals the
+    first one bit for bit."""
+    w = wl.conv3x3_64_56()
+    cv = dict(w["conv"])
+    say("conv3x3 workspace reuse map")
+    L = rxnn.map_layer(dev(w["W"]), w["xbar"])
+    X = dev(w["X"])
+    say("conv3x3 workspace reuse n=%d" % cv["n"])
+    Y0 = rxnn.conv_layer(L, w["periph"], cv, X).cpu().numpy()
+    cs = dict(cv, n=5)
+    say("conv3x3 workspace reuse n=5")
+    Y1 = rxnn.conv_layer(L, w["periph"], cs, X[:5].contiguous()).cpu().numpy()
+    np.testing.assert_array_equal(Y1, Y0[:5])
+    say("conv3x3 workspace reuse n=%d again" % cv["n"])
+    Y2 = rxnn.conv_layer(L, w["periph"], cv, X).cpu().numpy()
+    np.testing.assert_array_equal(Y2, Y0)
+    L.free()
