@@ -143,7 +143,7 @@ def bench_fc256(args):
         rxnn.crossbar_vmm(L, w["periph"], Xd, Y, stream)
     torch.cuda.synchronize()
     rxnn.profile_reset()
-    rxnn.profile_enable(True)
+    rxnn.profile_enable(2)
     ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     ev0.record(stream)
     for _ in range(args.steps):
@@ -233,8 +233,10 @@ def bench_stack(args):
     for t in range(args.warmup):
         step(t)
     torch.cuda.synchronize()
+    # timed steps: only the evaluation kernel carries timing events (an event
+    # pair around every launch would leave the GPU idle between kernels)
     rxnn.profile_reset()
-    rxnn.profile_enable(True)
+    rxnn.profile_enable(2)
     ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     ev0.record(stream)
     for t in range(args.steps):
@@ -243,11 +245,19 @@ def bench_stack(args):
     torch.cuda.synchronize()
     rxnn.profile_enable(False)
     step_ms = ev0.elapsed_time(ev1) / args.steps
+    # per-kernel breakdown: the same steps again (same weights), every launch timed
+    if rebuild or args.breakdown:
+        rxnn.profile_reset()
+        rxnn.profile_enable(1)
+        for t in range(args.steps):
+            step(args.warmup + t)
+        torch.cuda.synchronize()
+        rxnn.profile_enable(False)
     kern = read_kernels(rxnn, args.steps)
     # evaluation alone (G' kept); the evaluation kernel's roofline is taken
     # here, where no rebuild of another layer shares the GPU with it
     rxnn.profile_reset()
-    rxnn.profile_enable(True)
+    rxnn.profile_enable(2)
     ev0.record(stream)
     for _ in range(args.steps):
         for e in layers:
@@ -301,6 +311,8 @@ def main():
                     choices=["conv3x3", "fc256", "resnet18", "vgg16fc", "resnet50"])
     ap.add_argument("--crossbar", type=int, default=256, help="resnet50: crossbar side")
     ap.add_argument("--wire", type=float, default=2.5, help="resnet50: wire resistance (Ohm)")
+    ap.add_argument("--breakdown", action="store_true",
+                    help="stacks without rebuild: also time every launch in a second pass")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU: the crossbar path is built and measured on a "
@@ -341,9 +353,11 @@ def main():
         step()
     torch.cuda.synchronize()
 
-    # timed region: K whole steps, kernel events recorded by the library
+    # timed region: K whole steps; the library brackets the evaluation kernel
+    # with HIP events on the launch stream (level 2: the other launches stay
+    # back to back, an event pair around each would idle the GPU between them)
     rxnn.profile_reset()
-    rxnn.profile_enable(True)
+    rxnn.profile_enable(2)
     ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     w0 = time.perf_counter()
@@ -355,9 +369,17 @@ def main():
     wall = time.perf_counter() - w0
     rxnn.profile_enable(False)
     step_ms = ev0.elapsed_time(ev1) / args.steps
-    kern = read_kernels(rxnn, args.steps)
+    vmm_timed = read_kernels(rxnn, args.steps)["xbar_vmm"]
     print("[bench] timed %d steps: %.3f ms/step" % (args.steps, step_ms), file=sys.stderr,
           flush=True)
+    # per-kernel breakdown: K more identical steps with every launch timed
+    rxnn.profile_reset()
+    rxnn.profile_enable(1)
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    rxnn.profile_enable(False)
+    kern = read_kernels(rxnn, args.steps)
 
     # evaluation only (G' kept): the paper's phase 2
     torch.cuda.synchronize()
@@ -368,8 +390,8 @@ def main():
     torch.cuda.synchronize()
     eval_ms = ev0.elapsed_time(ev1) / args.steps
 
-    # the dominant single kernel is the evaluation kernel
-    vmm_us = kern["xbar_vmm"]["avg_us"]
+    # the dominant single kernel is the evaluation kernel (timed in the timed region)
+    vmm_us = vmm_timed["avg_us"]
     ach = 2.0 * macs / (vmm_us * 1e-6) / 1e12
     roof = {"kernel": "k_xbar_vmm", "bound": "mfma", "achieved": ach,
             "peak": FP32_MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
@@ -406,6 +428,7 @@ def main():
         "build": build,
         "eval_only": {"ms": eval_ms, "value": macs / (eval_ms * 1e-3), "unit": "MAC/s"},
         "kernels": kern,
+        "kernels_pass": "a second pass of the same steps with every launch timed",
         "wall_s_timed": wall,
     }
     if not args.no_cpu_baseline:

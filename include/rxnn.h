@@ -212,9 +212,12 @@ rxnn_status rxnn_layer_wmax(const rxnn_layer* layer, double* w_max);
 void rxnn_free_layer(rxnn_layer* layer);
 
 /*
- * Kernel timing, for measurement: when enabled, the library brackets each
- * kernel it launches with HIP events on the launch stream and accumulates
- * the elapsed time per kernel name: "wmax" (w_max reduction), "nd_block",
+ * Kernel timing, for measurement.  rxnn_profile_enable(1): the library
+ * brackets each kernel it launches with HIP events on the launch stream;
+ * rxnn_profile_enable(2): only the evaluation kernel ("xbar_vmm"), which
+ * keeps the other launches back to back (an event pair leaves the GPU idle
+ * for several microseconds); 0 switches timing off, any other level is
+ * RXNN_EINVAL.  The elapsed time is accumulated per kernel name: "wmax" (w_max reduction), "nd_block",
  * "nd_merge", "nd_final" (G' build by nested dissection), "gprime_sweep" (G'
  * build by the row sweep), "dac" (DAC of the inputs), "ktab" (patch-column
  * table), "xbar_vmm" (evaluation), "fill" (clearing of a new evaluation

@@ -153,7 +153,7 @@ struct Pending {
   std::string name;
   hipEvent_t a, b;
 };
-bool g_prof = false;
+int g_prof = 0;   // 0 off, 1 every kernel, 2 the evaluation kernel only
 std::vector<Pending> g_pending;
 std::map<std::string, std::pair<double, int64_t>> g_prof_tot;
 
@@ -308,9 +308,13 @@ hipError_t build_gprime(rxnn_layer* L, const float* W, hipStream_t s) {
 namespace rxnn {
 
 ProfScope::ProfScope(const char* name, hipStream_t s) : name_(name), s_(s), on_(false) {
-  if (!g_prof) return;
-  if (hipEventCreate(&a_) != hipSuccess) return;
-  if (hipEventCreate(&b_) != hipSuccess) { (void)hipEventDestroy(a_); return; }
+  if (!g_prof || (g_prof == 2 && strcmp(name, "xbar_vmm") != 0)) return;
+  // no system-scope fence: a timing event then costs no cache flush on the GPU
+  if (hipEventCreateWithFlags(&a_, hipEventDisableSystemFence) != hipSuccess) return;
+  if (hipEventCreateWithFlags(&b_, hipEventDisableSystemFence) != hipSuccess) {
+    (void)hipEventDestroy(a_);
+    return;
+  }
   if (hipEventRecord(a_, s_) != hipSuccess) {
     (void)hipEventDestroy(a_);
     (void)hipEventDestroy(b_);
@@ -619,8 +623,9 @@ void rxnn_free_layer(rxnn_layer* layer) {
 }
 
 rxnn_status rxnn_profile_enable(int32_t on) {
+  if (on < 0 || on > 2) return fail(RXNN_EINVAL, "profile level must be 0, 1 or 2");
   std::lock_guard<std::mutex> g(g_mu);
-  g_prof = on != 0;
+  g_prof = on;
   return RXNN_OK;
 }
 

@@ -56,13 +56,11 @@ struct NdArgs {
 
 namespace {
 
-constexpr int SBMIN = 8;        // smallest side of the blocks reduced in LDS
 constexpr int NTH = 256;        // threads of the kernels on the blocked global path
-constexpr int NTB = 1024;       // threads of the LDS-resident kernels (four waves per SIMD)
+constexpr int NTB = 1024;       // threads of the 16 x 16 block kernel
 // doubles per LDS level buffer of a bs x bs block reduction
 __host__ __device__ constexpr int lbuf(int bs) { return bs == 16 ? 6400 : 1600; }
 constexpr int KB = 16;          // pivots per elimination block
-constexpr int ULDS = 16384;     // doubles of cut rows a merge may keep in LDS
 
 __device__ __forceinline__ void ports(int i0, int j0, int h, int w, int T, int& nL, int& nR,
                                       int& nT, int& nB) {
@@ -409,135 +407,12 @@ __device__ void eliminate(double* cut, int c, int E, int ldc, double* ext, int l
   }
 }
 
-// Pivot-by-pivot elimination of the c cut rows U (row stride ldu, c cut
-// columns then E external columns) held in LDS, followed by Z = D^-1/2 U_ext:
-// afterwards the Schur complement of the externals is ext - Z^T Z.
-// Pivot-by-pivot elimination of the c cut rows U (row stride ldu, c cut
-// columns then E external columns) held in LDS, followed by Z = D^-1/2 U_ext:
-// afterwards the Schur complement of the externals is ext - Z^T Z.  A task is
-// one column over a chunk of 8 rows, its loads issued before its stores.
-template <int NT>
-__device__ void eliminate_lds(double* U, int c, int E, int ldu, double* isq) {
-  const int tid = threadIdx.x;
-  const int lgy = lg2ceil(c + E);
-  for (int k = 0; k < c; ++k) {
-    const double inv = recip(U[k * ldu + k]);
-    const int nxc = (c - k - 1 + 7) / 8;
-    for (int t = tid; t < nxc << lgy; t += NT) {
-      const int y = t & ((1 << lgy) - 1);
-      if (y <= k || y >= c + E) continue;
-      const int x0 = k + 1 + (t >> lgy) * 8;
-      const double uky = U[k * ldu + y] * inv;
-      double uxk[8], uxy[8];
-#pragma unroll
-      for (int xx = 0; xx < 8; ++xx) {
-        const int x = min(x0 + xx, c - 1);
-        uxk[xx] = U[x * ldu + k];
-        uxy[xx] = U[x * ldu + y];
-      }
-#pragma unroll
-      for (int xx = 0; xx < 8; ++xx)
-        if (x0 + xx < c) U[(x0 + xx) * ldu + y] = uxy[xx] - uxk[xx] * uky;
-    }
-    __syncthreads();
-  }
-  for (int t = tid; t < c; t += NT) isq[t] = 1.0 / sqrt(U[t * ldu + t]);
-  __syncthreads();
-  const int lge = lg2ceil(E);
-  for (int t = tid; t < c << lge; t += NT) {
-    const int k = t >> lge, y = t & ((1 << lge) - 1);
-    if (y < E) U[k * ldu + c + y] *= isq[k];
-  }
-  __syncthreads();
-}
-
-// The same elimination in blocks of PB pivots: the pivot rows of a block are
-// eliminated among themselves, every later row then gets its PB multipliers
-// from its own entries in the block's columns, and one pass applies the
-// rank-PB update to the trailing rows.  The trailing matrix is read and
-// written once per block instead of once per pivot (the rank-1 form is bound
-// by that LDS traffic).  aux: LDS scratch of 4 (c + 1) doubles.
-template <int NT>
-__device__ void eliminate_lds_blocked(double* U, int c, int E, int ldu, double* isq,
-                                      double* aux) {
-  constexpr int PB = 4;
-  const int tid = threadIdx.x;
-  const int ncol = c + E;
-  const int lgy = lg2ceil(ncol);
-  double* lm = aux;               // multipliers, PB per row
-  double* inv = aux + PB * c;     // pivot reciprocals of the block
-  for (int k0 = 0; k0 < c; k0 += PB) {
-    const int kb = min(PB, c - k0);
-    // pivot rows of the block, among themselves
-    for (int i = 0; i < kb; ++i) {
-      const int k = k0 + i;
-      const double ik = recip(U[k * ldu + k]);
-      if (tid == 0) inv[i] = ik;
-      const int nr = kb - 1 - i;   // later rows of the block
-      for (int t = tid; t < nr << lgy; t += NT) {
-        const int y = t & ((1 << lgy) - 1);
-        if (y <= k || y >= ncol) continue;
-        const int x = k + 1 + (t >> lgy);
-        U[x * ldu + y] -= U[x * ldu + k] * ik * U[k * ldu + y];
-      }
-      __syncthreads();
-    }
-    const int r0 = k0 + kb;
-    // multipliers of the trailing rows
-    for (int x = r0 + tid; x < c; x += NT) {
-      double l[PB];
-#pragma unroll
-      for (int i = 0; i < PB; ++i) {
-        if (i >= kb) break;
-        double t = U[x * ldu + k0 + i];
-        for (int j = 0; j < i; ++j) t -= l[j] * U[(k0 + j) * ldu + k0 + i];
-        l[i] = t * inv[i];
-        lm[x * PB + i] = l[i];
-      }
-    }
-    __syncthreads();
-    // rank-kb update of the trailing rows, 8-row chunks per task
-    const int nxc = (c - r0 + 7) / 8;
-    for (int t = tid; t < nxc << lgy; t += NT) {
-      const int y = t & ((1 << lgy) - 1);
-      if (y < r0 || y >= ncol) continue;
-      const int x0 = r0 + (t >> lgy) * 8;
-      double p[PB];
-#pragma unroll
-      for (int i = 0; i < PB; ++i) p[i] = i < kb ? U[(k0 + i) * ldu + y] : 0.0;
-      double u[8];
-#pragma unroll
-      for (int xx = 0; xx < 8; ++xx) u[xx] = U[min(x0 + xx, c - 1) * ldu + y];
-#pragma unroll
-      for (int xx = 0; xx < 8; ++xx) {
-        const int x = x0 + xx;
-        if (x >= c) continue;
-        double v = u[xx];
-#pragma unroll
-        for (int i = 0; i < PB; ++i)
-          if (i < kb) v -= lm[x * PB + i] * p[i];
-        U[x * ldu + y] = v;
-      }
-    }
-    __syncthreads();
-  }
-  for (int t = tid; t < c; t += NT) isq[t] = 1.0 / sqrt(U[t * ldu + t]);
-  __syncthreads();
-  const int lge = lg2ceil(E);
-  for (int t = tid; t < c << lge; t += NT) {
-    const int k = t >> lge, y = t & ((1 << lge) - 1);
-    if (y < E) U[k * ldu + c + y] *= isq[k];
-  }
-  __syncthreads();
-}
-
-// One merge of two h x w blocks (children in buf_in, result to buf_out).
-template <bool LDSP, int NT>
-__global__ __launch_bounds__(NT) void k_nd_merge(NdArgs na) {
-  extern __shared__ double lds[];   // cut rows (LDS path) or the blocked path's panels
+// One merge of two h x w blocks (children in buf_in, result to buf_out) with
+// the cut rows in global memory: merges with more than 64 cut nodes.
+__global__ __launch_bounds__(NTH) void k_nd_merge(NdArgs na) {
+  constexpr int NT = NTH;
+  extern __shared__ double lds[];   // the blocked elimination's panels
   __shared__ short tab[2 * 1024];   // children of a 256 x 256 grid have up to 768 ports
-  __shared__ double isq[256];
-  __shared__ double aux[4 * 257];
   const int tid = threadIdx.x;
   const int T = na.T, h = na.h, w = na.w;
   const bool vert = na.vert != 0;
@@ -552,8 +427,8 @@ __global__ __launch_bounds__(NT) void k_nd_merge(NdArgs na) {
   const int Ein = 2 * (h + w);
   const int ccols = T / w;
   double* ext = na.buf_out + la * na.out_stride + (int64_t)m * Emax * Emax;
-  const int ldc = LDSP ? c + na.e_layout : c + Emax;
-  double* cut = LDSP ? lds : na.scratch + la * na.scr_stride + (int64_t)m * c * ldc;
+  const int ldc = c + Emax;
+  double* cut = na.scratch + la * na.scr_stride + (int64_t)m * c * ldc;
   for (int t = tid; t < 2 * Ein; t += NT) {
     const int ch = t / Ein, p = t - ch * Ein;
     const int ci = (vert && ch) ? i0 + h : i0, cj = (!vert && ch) ? j0 + w : j0;
@@ -599,55 +474,15 @@ __global__ __launch_bounds__(NT) void k_nd_merge(NdArgs na) {
     }
     __syncthreads();
   }
-  if (!LDSP) {
-    eliminate(cut, c, E, ldc, ext, Emax, lds);
-    return;
-  }
-  eliminate_lds_blocked<NT>(cut, c, E, ldc, isq, aux);
-  // ext -= Z^T Z, square tiles of TS x TS entries, 4 x 4 per thread
-  constexpr int TS = NT == 1024 ? 128 : 64;
-  const int rx = (tid / (TS / 4)) * 4, ry = (tid % (TS / 4)) * 4;
-  for (int tx0 = 0; tx0 < E; tx0 += TS)
-    for (int ty0 = 0; ty0 < E; ty0 += TS) {
-      double acc[4][4];
-#pragma unroll
-      for (int a = 0; a < 4; ++a)
-#pragma unroll
-        for (int b = 0; b < 4; ++b) acc[a][b] = 0.0;
-      for (int k = 0; k < c; ++k) {
-        const double* z = cut + k * ldc + c;
-        double xa[4], yb[4];
-#pragma unroll
-        for (int a = 0; a < 4; ++a) xa[a] = z[min(tx0 + rx + a, E - 1)];
-#pragma unroll
-        for (int b = 0; b < 4; ++b) yb[b] = z[min(ty0 + ry + b, E - 1)];
-#pragma unroll
-        for (int a = 0; a < 4; ++a)
-#pragma unroll
-          for (int b = 0; b < 4; ++b) acc[a][b] = fma(xa[a], yb[b], acc[a][b]);
-      }
-#pragma unroll
-      for (int a = 0; a < 4; ++a) {
-        const int x = tx0 + rx + a;
-        if (x >= E) continue;
-#pragma unroll
-        for (int b = 0; b < 4; ++b) {
-          const int y = ty0 + ry + b;
-          if (y < E) ext[x * Emax + y] -= acc[a][b];
-        }
-      }
-    }
+  eliminate(cut, c, E, ldc, ext, Emax, lds);
 }
 
 // Drivers and sinks: G'^T = -(Y_sL (Y_LL + g_d I)^-1 g_d E), written as fp32.
 // Externals: the M source terminals t, then the T sink terminals s; cut: the
 // T row-input nodes.  Only the (s, t) block of the result is needed.
-template <bool LDSP>
-__global__ __launch_bounds__(LDSP ? NTB : NTH) void k_nd_final(NdArgs na) {
-  constexpr int NT = LDSP ? NTB : NTH;
+__global__ __launch_bounds__(NTH) void k_nd_final(NdArgs na) {
+  constexpr int NT = NTH;
   extern __shared__ double lds[];
-  __shared__ double isq[256];
-  __shared__ double aux[4 * 257];
   const int tid = threadIdx.x;
   const int T = na.T, M = na.ms.M, N = na.ms.N;
   const int64_t la = blockIdx.x;
@@ -655,15 +490,13 @@ __global__ __launch_bounds__(LDSP ? NTB : NTH) void k_nd_final(NdArgs na) {
   const double* Y = na.buf_in + la * na.in_stride;
   const int E = M + T, c = T, ldc = c + E;
   double* ext = na.scratch + la * na.scr_stride;
-  double* cut = LDSP ? lds : ext + (int64_t)E * E;
-  if (!LDSP) {
-    for (int e = tid; e < E * E; e += NT) {
-      const int x = e / E, y = e % E;
-      double v = 0.0;
-      if (x < M && y < M) v = (x == y) ? na.g_d : 0.0;
-      else if (x >= M && y >= M) v = Y[(T + x - M) * Ein + (T + y - M)];
-      ext[e] = v;
-    }
+  double* cut = ext + (int64_t)E * E;
+  for (int e = tid; e < E * E; e += NT) {
+    const int x = e / E, y = e % E;
+    double v = 0.0;
+    if (x < M && y < M) v = (x == y) ? na.g_d : 0.0;
+    else if (x >= M && y >= M) v = Y[(T + x - M) * Ein + (T + y - M)];
+    ext[e] = v;
   }
   const int lgl = lg2ceil(ldc);
   for (int e = tid; e < c << lgl; e += NT) {
@@ -678,23 +511,296 @@ __global__ __launch_bounds__(LDSP ? NTB : NTH) void k_nd_final(NdArgs na) {
   __syncthreads();
   const int64_t arr = na.arr0 + la;
   float* out = na.gpt + arr * (int64_t)na.ms.Np * na.ms.Mp;
-  if (!LDSP) {
-    eliminate(cut, c, E, ldc, ext, E, lds);
-    for (int e = tid; e < na.ms.Np * na.ms.Mp; e += NT) {
-      const int j = e / na.ms.Mp, k = e % na.ms.Mp;
-      out[e] = (j < N && k < M) ? (float)(-ext[(int64_t)(M + j) * E + k]) : 0.0f;
+  eliminate(cut, c, E, ldc, ext, E, lds);
+  for (int e = tid; e < na.ms.Np * na.ms.Mp; e += NT) {
+    const int j = e / na.ms.Mp, k = e % na.ms.Mp;
+    out[e] = (j < N && k < M) ? (float)(-ext[(int64_t)(M + j) * E + k]) : 0.0f;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Merges and the final step with at most 64 cut nodes: the elimination runs
+// in registers.  Lane x of every wave holds cut row x; wave w holds the
+// columns w, w + NW, w + 2 NW, ... of the combined matrix (the c cut columns,
+// then the E external columns).  Pivot k needs row k in every column, which
+// lane k of the same wave holds (a lane read, no LDS), and the multipliers
+// l_x = U[x][k] / U[k][k] of column k, which the wave holding column k
+// publishes through LDS: one barrier per pivot.  The eliminated rows, scaled
+// by D^-1/2, leave as Zt (E x c, row-major) for the Schur update
+// ext - Zt Zt^T, which k_nd_schur computes on 64 x 64 tiles over many
+// workgroups.
+// ---------------------------------------------------------------------------
+constexpr int MAXSLOT = 512;    // cut + external slots of a merge with c <= 64
+
+__device__ __forceinline__ double readlane_d(double v, int l) {
+  const unsigned long long b = __builtin_bit_cast(unsigned long long, v);
+  const unsigned lo = (unsigned)__builtin_amdgcn_readlane((int)(unsigned)b, l);
+  const unsigned hi = (unsigned)__builtin_amdgcn_readlane((int)(unsigned)(b >> 32), l);
+  return __builtin_bit_cast(double, ((unsigned long long)hi << 32) | lo);
+}
+
+// Geometry of merge `m` of the level described by na (children h x w).
+struct MergeGeom {
+  int64_t la;
+  int m, mi, mj, i0, j0, c, E, Emax, Ein, cm0, cm1;
+};
+
+__device__ __forceinline__ MergeGeom merge_geom(const NdArgs& na, int64_t blk) {
+  MergeGeom g;
+  const int T = na.T, h = na.h, w = na.w;
+  const bool vert = na.vert != 0;
+  const int nh = vert ? 2 * h : h, nw = vert ? w : 2 * w;
+  const int cols = T / nw, nmerge = (T / nh) * cols;
+  g.la = blk / nmerge;
+  g.m = (int)(blk % nmerge);
+  g.mi = g.m / cols;
+  g.mj = g.m % cols;
+  g.i0 = g.mi * nh;
+  g.j0 = g.mj * nw;
+  g.Emax = 2 * (nh + nw);
+  g.c = vert ? w : h;
+  g.E = nports(g.i0, g.j0, nh, nw, T);
+  g.Ein = 2 * (h + w);
+  const int ccols = T / w;
+  g.cm0 = vert ? (g.mi * 2) * ccols + g.mj : g.mi * ccols + g.mj * 2;
+  g.cm1 = vert ? (g.mi * 2 + 1) * ccols + g.mj : g.mi * ccols + g.mj * 2 + 1;
+  return g;
+}
+
+// invt[ch][slot]: the port of child ch that lands on merged slot `slot`
+// (cut node k -> slot k, external port d -> slot c + d), or -1.
+__device__ void inverse_tables(const NdArgs& na, const MergeGeom& g, short (*invt)[MAXSLOT],
+                               int NT) {
+  const int tid = threadIdx.x;
+  const bool vert = na.vert != 0;
+  for (int t = tid; t < 2 * MAXSLOT; t += NT) invt[t / MAXSLOT][t % MAXSLOT] = -1;
+  __syncthreads();
+  for (int t = tid; t < 2 * g.Ein; t += NT) {
+    const int ch = t / g.Ein, p = t - ch * g.Ein;
+    const int ci = (vert && ch) ? g.i0 + na.h : g.i0, cj = (!vert && ch) ? g.j0 + na.w : g.j0;
+    if (p < nports(ci, cj, na.h, na.w, na.T)) {
+      const int d = merge_dest(ch, p, g.i0, g.j0, na.h, na.w, vert, na.T);
+      invt[ch][d >= 0 ? g.c + d : -1 - d] = (short)p;
+    }
+  }
+  __syncthreads();
+}
+
+template <int C, int NW, int CPT, bool FINAL>
+__global__ __launch_bounds__(64 * NW) void k_nd_cut(NdArgs na) {
+  constexpr int NT = 64 * NW;
+  static_assert(C <= 64, "one cut row per lane");
+  __shared__ short invt[2][MAXSLOT];
+  __shared__ double colb[2][64];
+  __shared__ double dg[64];
+  // final step: the eliminated rows' sink and source columns for G'
+  __shared__ double zs[FINAL ? C : 1][FINAL ? 64 + 2 : 1];
+  __shared__ double zq[FINAL ? C : 1][FINAL ? 64 + 2 : 1];
+  const int lane = threadIdx.x & 63;
+  const int wv = threadIdx.x >> 6;
+  const int T = na.T;
+  int E, ncol;
+  int64_t la;
+  double* zt = nullptr;
+  double U[CPT];
+  if (FINAL) {
+    la = blockIdx.x;
+    E = na.ms.M + T;
+    ncol = C + E;
+    const int Ein = 4 * T, M = na.ms.M;
+    const double* Y = na.buf_in + la * na.in_stride;
+    const int x = lane;
+#pragma unroll
+    for (int j = 0; j < CPT; ++j) {
+      const int y = wv + NW * j;
+      double v = 0.0;
+      if (x < C && y < ncol) {
+        if (y < C) v = Y[y * Ein + x] + (x == y ? na.g_d : 0.0);
+        else if (y < C + M) v = (x == na.row_off + (y - C)) ? -na.g_d : 0.0;
+        else v = Y[(T + (y - C - M)) * Ein + x];
+      }
+      U[j] = v;
+    }
+  } else {
+    const MergeGeom g = merge_geom(na, blockIdx.x);
+    inverse_tables(na, g, invt, NT);
+    la = g.la;
+    E = g.E;
+    ncol = C + E;
+    zt = na.scratch + la * na.scr_stride + (int64_t)g.m * g.Emax * C;
+    const double* Y0 = na.buf_in + la * na.in_stride + (int64_t)g.cm0 * g.Ein * g.Ein;
+    const double* Y1 = na.buf_in + la * na.in_stride + (int64_t)g.cm1 * g.Ein * g.Ein;
+    const int x = lane;
+    const int pa0 = x < C ? invt[0][x] : -1, pa1 = x < C ? invt[1][x] : -1;
+    // the children's matrices are symmetric: row pb, column pa is read so
+    // that consecutive lanes read consecutive ports
+#pragma unroll
+    for (int j = 0; j < CPT; ++j) {
+      const int y = wv + NW * j;
+      double v = 0.0;
+      if (y < ncol) {
+        const int pb0 = invt[0][y], pb1 = invt[1][y];
+        if (pa0 >= 0 && pb0 >= 0) v += Y0[pb0 * g.Ein + pa0];
+        if (pa1 >= 0 && pb1 >= 0) v += Y1[pb1 * g.Ein + pa1];
+      }
+      U[j] = v;
+    }
+  }
+  // Pivot k: the wave holding column k + 1 (slot (k + 1) / NW of wave
+  // (k + 1) % NW, both fixed once the loop is unrolled) first applies pivot k
+  // to that column and publishes its multipliers, then every wave applies
+  // pivot k to the rest of its columns.
+  if (wv == 0) {
+    const double piv = readlane_d(U[0], 0);
+    colb[0][lane] = (lane > 0 && lane < C) ? U[0] * recip(piv) : 0.0;
+    if (lane == 0) dg[0] = piv;
+  }
+#pragma clang loop unroll(full)
+  for (int k = 0; k < C; ++k) {
+    __syncthreads();
+    const double l = colb[k & 1][lane];
+    const int w1 = (k + 1) % NW, j1 = (k + 1) / NW;
+    if (k + 1 < C && wv == w1) {
+      U[j1] = fma(-l, readlane_d(U[j1], k), U[j1]);
+      const double piv = readlane_d(U[j1], k + 1);
+      colb[(k + 1) & 1][lane] = (lane > k + 1 && lane < C) ? U[j1] * recip(piv) : 0.0;
+      if (lane == 0) dg[k + 1] = piv;
+    }
+#pragma clang loop unroll(full)
+    for (int j = 0; j < CPT; ++j) {
+      if (NW * j + NW - 1 <= k) continue;          // every column of this slot is done
+      const int y = wv + NW * j;
+      if (y <= k || y >= ncol) continue;
+      if (k + 1 < C && j == j1 && wv == w1) continue;   // column k + 1, done above
+      U[j] = fma(-l, readlane_d(U[j], k), U[j]);
+    }
+  }
+  __syncthreads();
+  const double isq = lane < C ? 1.0 / sqrt(dg[lane]) : 0.0;
+  if (!FINAL) {
+    // Zt[y - C][x] = U[x][y] / sqrt(D_x) for the external columns
+    if (lane < C) {
+#pragma unroll
+      for (int j = 0; j < CPT; ++j) {
+        const int y = wv + NW * j;
+        if (y >= C && y < ncol) zt[(int64_t)(y - C) * C + lane] = U[j] * isq;
+      }
     }
     return;
   }
-  eliminate_lds_blocked<NT>(cut, c, E, ldc, isq, aux);
-  const int lgm = lg2ceil(na.ms.Mp);
-  for (int e = tid; e < na.ms.Np << lgm; e += NT) {
-    const int j = e >> lgm, k = e & ((1 << lgm) - 1);
-    if (k >= na.ms.Mp) continue;
-    double v = 0.0;
-    if (j < N && k < M)
-      for (int l = 0; l < c; ++l) v = fma(cut[l * ldc + c + M + j], cut[l * ldc + c + k], v);
-    out[j * na.ms.Mp + k] = (float)v;
+  // G'[j][k] = sum_x Z[x][sink j] Z[x][source k]
+  const int M = na.ms.M, N = na.ms.N;
+  if (lane < C) {
+#pragma unroll
+    for (int j = 0; j < CPT; ++j) {
+      const int y = wv + NW * j;
+      if (y >= C && y < C + M && y - C < 64) zq[lane][y - C] = U[j] * isq;
+      if (y >= C + M && y < ncol && y - C - M < 64) zs[lane][y - C - M] = U[j] * isq;
+    }
+  }
+  __syncthreads();
+  const int64_t arr = na.arr0 + la;
+  float* out = na.gpt + arr * (int64_t)na.ms.Np * na.ms.Mp;
+  const int Np = na.ms.Np, Mp = na.ms.Mp;
+  if (threadIdx.x < 256) {
+    const int tx = threadIdx.x >> 4, ty = threadIdx.x & 15;
+    double acc[4][4];
+#pragma unroll
+    for (int a = 0; a < 4; ++a)
+#pragma unroll
+      for (int b = 0; b < 4; ++b) acc[a][b] = 0.0;
+#pragma unroll 4
+    for (int x = 0; x < C; ++x) {
+      double sa[4], qb[4];
+#pragma unroll
+      for (int a = 0; a < 4; ++a) sa[a] = zs[x][4 * tx + a];
+#pragma unroll
+      for (int b = 0; b < 4; ++b) qb[b] = zq[x][4 * ty + b];
+#pragma unroll
+      for (int a = 0; a < 4; ++a)
+#pragma unroll
+        for (int b = 0; b < 4; ++b) acc[a][b] = fma(sa[a], qb[b], acc[a][b]);
+    }
+#pragma unroll
+    for (int a = 0; a < 4; ++a) {
+      const int j = 4 * tx + a;
+      if (j >= Np) continue;
+#pragma unroll
+      for (int b = 0; b < 4; ++b) {
+        const int k = 4 * ty + b;
+        if (k < Mp) out[j * Mp + k] = (j < N && k < M) ? (float)acc[a][b] : 0.0f;
+      }
+    }
+  }
+}
+
+// ext = V - Zt Zt^T on one 64 x 64 tile of one merge (V: the children's
+// external-external entries).
+__global__ __launch_bounds__(256) void k_nd_schur(NdArgs na) {
+  constexpr int KC = 16;
+  __shared__ short invt[2][MAXSLOT];
+  __shared__ double za[KC][64 + 2];
+  __shared__ double zb[KC][64 + 2];
+  const int tid = threadIdx.x;
+  const int nh = na.vert ? 2 * na.h : na.h, nw = na.vert ? na.w : 2 * na.w;
+  const int Emax = 2 * (nh + nw);
+  const int nt = (Emax + 63) / 64;
+  const int64_t blk = blockIdx.x / (nt * nt);
+  const MergeGeom g = merge_geom(na, blk);
+  const int c = g.c, E = g.E;
+  const int tt = (int)(blockIdx.x % (nt * nt));
+  const int x0 = (tt / nt) * 64, y0 = (tt % nt) * 64;
+  const int nrx = min(64, E - x0), nry = min(64, E - y0);
+  if (nrx <= 0 || nry <= 0) return;
+  inverse_tables(na, g, invt, 256);
+  const double* zt = na.scratch + g.la * na.scr_stride + (int64_t)g.m * Emax * c;
+  const int tx = tid >> 4, ty = tid & 15;
+  double acc[4][4];
+#pragma unroll
+  for (int a = 0; a < 4; ++a)
+#pragma unroll
+    for (int b = 0; b < 4; ++b) acc[a][b] = 0.0;
+  for (int k0 = 0; k0 < c; k0 += KC) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int e = tid + 256 * r, xx = e / KC, kk = e % KC;
+      const int k = k0 + kk;
+      za[kk][xx] = (xx < nrx && k < c) ? zt[(int64_t)(x0 + xx) * c + k] : 0.0;
+      zb[kk][xx] = (xx < nry && k < c) ? zt[(int64_t)(y0 + xx) * c + k] : 0.0;
+    }
+    __syncthreads();
+#pragma unroll 4
+    for (int kk = 0; kk < KC; ++kk) {
+      double xa[4], yb[4];
+#pragma unroll
+      for (int a = 0; a < 4; ++a) xa[a] = za[kk][4 * tx + a];
+#pragma unroll
+      for (int b = 0; b < 4; ++b) yb[b] = zb[kk][4 * ty + b];
+#pragma unroll
+      for (int a = 0; a < 4; ++a)
+#pragma unroll
+        for (int b = 0; b < 4; ++b) acc[a][b] = fma(xa[a], yb[b], acc[a][b]);
+    }
+    __syncthreads();
+  }
+  const double* Y0 = na.buf_in + g.la * na.in_stride + (int64_t)g.cm0 * g.Ein * g.Ein;
+  const double* Y1 = na.buf_in + g.la * na.in_stride + (int64_t)g.cm1 * g.Ein * g.Ein;
+  double* ext = na.buf_out + g.la * na.out_stride + (int64_t)g.m * Emax * Emax;
+#pragma unroll
+  for (int a = 0; a < 4; ++a) {
+    const int x = x0 + 4 * tx + a;
+    if (x >= E) continue;
+    const int pa0 = invt[0][c + x], pa1 = invt[1][c + x];
+#pragma unroll
+    for (int b = 0; b < 4; ++b) {
+      const int y = y0 + 4 * ty + b;
+      if (y >= E) continue;
+      const int pb0 = invt[0][c + y], pb1 = invt[1][c + y];
+      double v = 0.0;
+      if (pa0 >= 0 && pb0 >= 0) v += Y0[pa0 * g.Ein + pb0];
+      if (pa1 >= 0 && pb1 >= 0) v += Y1[pa1 * g.Ein + pb1];
+      ext[x * Emax + y] = v - acc[a][b];
+    }
   }
 }
 
@@ -738,25 +844,38 @@ int nd_side(int M, int N) {
   return T;
 }
 
-static bool g_nd_attr = false;
+// Register elimination (one cut row per lane): the cut sizes and column
+// counts that have an instantiation.  Cut sizes are powers of two.
+static bool cut_in_registers(int c, int ncol) {
+  return (c == 8 && ncol <= 64) || (c == 16 && ncol <= 128) || (c == 32 && ncol <= 256) ||
+         (c == 64 && ncol <= 448);
+}
+
+template <bool FINAL>
+static void launch_cut(const NdArgs& na, dim3 grid, int c, int ncol, hipStream_t s) {
+#define RXNN_CUT(Cv, NWv, CPTv) \
+  hipLaunchKernelGGL((k_nd_cut<Cv, NWv, CPTv, FINAL>), grid, dim3(64 * NWv), 0, s, na)
+  if constexpr (FINAL) {   // c = T, ncol = 2 T + M <= 3 T
+    if (c == 16) RXNN_CUT(16, 16, 8);
+    else if (c == 32) RXNN_CUT(32, 16, 8);
+    else RXNN_CUT(64, 16, 12);
+  } else {
+    if (c == 8) RXNN_CUT(8, 4, 16);
+    else if (c == 16) RXNN_CUT(16, 16, 8);
+    else if (c == 32 && ncol <= 128) RXNN_CUT(32, 16, 8);
+    else if (c == 32 && ncol <= 192) RXNN_CUT(32, 16, 12);
+    else if (c == 32) RXNN_CUT(32, 16, 16);
+    else if (ncol <= 192) RXNN_CUT(64, 16, 12);
+    else if (ncol <= 320) RXNN_CUT(64, 16, 20);
+    else RXNN_CUT(64, 16, 28);
+  }
+#undef RXNN_CUT
+}
 
 // Builds G' of arrays [arr0, arr0 + n) with the workspace ws (ping-pong
 // level buffers and scratch, sized by nd_sizes for one array, times n).
 hipError_t launch_nd_build(const MapScalars& ms, const float* W, float* gpt, int64_t arr0,
                            int64_t n, int bs, double* ws, hipStream_t s) {
-  if (!g_nd_attr) {
-    const int mx = ULDS * (int)sizeof(double);
-    hipError_t e0 = hipFuncSetAttribute((const void*)k_nd_merge<true, NTB>,
-                                        hipFuncAttributeMaxDynamicSharedMemorySize, mx);
-    if (e0 == hipSuccess)
-      e0 = hipFuncSetAttribute((const void*)k_nd_merge<true, NTH>,
-                               hipFuncAttributeMaxDynamicSharedMemorySize, mx);
-    if (e0 == hipSuccess)
-      e0 = hipFuncSetAttribute((const void*)k_nd_final<true>,
-                               hipFuncAttributeMaxDynamicSharedMemorySize, mx);
-    if (e0 != hipSuccess) return e0;
-    g_nd_attr = true;
-  }
   NdArgs na;
   na.ms = ms;
   na.W = W;
@@ -809,19 +928,18 @@ hipError_t launch_nd_build(const MapScalars& ms, const float* W, float* gpt, int
       }
     na.e_layout = e_layout;
     const int c = vert ? w : h;
-    const int64_t u = (int64_t)c * (c + e_layout);
     const dim3 grid((unsigned)(n * nmerge));
     {
       ProfScope prof("nd_merge", s);
-      if (u <= ULDS && c <= 16)
-        hipLaunchKernelGGL((k_nd_merge<true, NTH>), grid, dim3(NTH),
-                           (unsigned)(u * sizeof(double)), s, na);
-      else if (u <= ULDS)
-        hipLaunchKernelGGL((k_nd_merge<true, NTB>), grid, dim3(NTB),
-                           (unsigned)(u * sizeof(double)), s, na);
-      else
-        hipLaunchKernelGGL((k_nd_merge<false, NTH>), grid, dim3(NTH),
+      if (cut_in_registers(c, c + e_layout)) {
+        launch_cut<false>(na, grid, c, c + e_layout, s);
+        const int nt = (2 * (nh + nw) + 63) / 64;
+        hipLaunchKernelGGL(k_nd_schur, dim3((unsigned)(n * nmerge * nt * nt)), dim3(256), 0, s,
+                           na);
+      } else {
+        hipLaunchKernelGGL(k_nd_merge, grid, dim3(NTH),
                            (unsigned)((KB * KB + 2 * KB * 64) * sizeof(double)), s, na);
+      }
     }
     e = hipGetLastError();
     if (e != hipSuccess) return e;
@@ -835,12 +953,10 @@ hipError_t launch_nd_build(const MapScalars& ms, const float* W, float* gpt, int
   na.buf_in = cur;
   {
     ProfScope prof("nd_final", s);
-    const int64_t uf = (int64_t)na.T * (na.T + ms.M + na.T);
-    if (uf <= ULDS)
-      hipLaunchKernelGGL(k_nd_final<true>, dim3((unsigned)n), dim3(NTB),
-                         (unsigned)(uf * sizeof(double)), s, na);
-    else
-      hipLaunchKernelGGL(k_nd_final<false>, dim3((unsigned)n), dim3(NTH),
+    if (na.T <= 64 && cut_in_registers(na.T, 2 * na.T + ms.M)) {
+      launch_cut<true>(na, dim3((unsigned)n), na.T, 2 * na.T + ms.M, s);
+    } else
+      hipLaunchKernelGGL(k_nd_final, dim3((unsigned)n), dim3(NTH),
                          (unsigned)((KB * KB + 2 * KB * 64) * sizeof(double)), s, na);
   }
   return hipGetLastError();

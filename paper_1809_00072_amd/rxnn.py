@@ -250,7 +250,8 @@ def conv_layer(layer: Layer, periph, conv, X, Y=None, stream=None):
 
 
 def profile_enable(on=True):
-    _check(load().rxnn_profile_enable(1 if on else 0))
+    """on: False/0 off, True/1 every kernel, 2 the evaluation kernel only."""
+    _check(load().rxnn_profile_enable(int(on)))
 
 
 def profile_reset():
