@@ -519,24 +519,60 @@ __global__ __launch_bounds__(NTH) void k_nd_final(NdArgs na) {
 }
 
 // ---------------------------------------------------------------------------
-// Merges and the final step with at most 64 cut nodes: the elimination runs
-// in registers.  Lane x of every wave holds cut row x; wave w holds the
-// columns w, w + NW, w + 2 NW, ... of the combined matrix (the c cut columns,
-// then the E external columns).  Pivot k needs row k in every column, which
-// lane k of the same wave holds (a lane read, no LDS), and the multipliers
-// l_x = U[x][k] / U[k][k] of column k, which the wave holding column k
-// publishes through LDS: one barrier per pivot.  The eliminated rows, scaled
-// by D^-1/2, leave as Zt (E x c, row-major) for the Schur update
-// ext - Zt Zt^T, which k_nd_schur computes on 64 x 64 tiles over many
+// Merges and the final step with at most 64 cut nodes: one workgroup of
+// ceil(ncol / 64) waves per merge.  Lane y holds column y of the combined
+// matrix (the C cut columns first, then the E externals) with all C cut rows
+// in registers.  The cut block is symmetric, so row k is also column k: at
+// pivot k the cut-column lanes publish row k in LDS and every lane updates
+// its rows x > k with t = U[k][y] / U[k][k]:  U[x][y] -= U[k][x] t.  One
+// barrier per pivot, one FMA per row and pivot.  The eliminated rows, scaled
+// by D^-1/2, leave as Z (C x E, row stride Emax) for the Schur update
+// ext - Z^T Z, which k_nd_schur computes on 64 x 64 tiles over many
 // workgroups.
 // ---------------------------------------------------------------------------
 constexpr int MAXSLOT = 512;    // cut + external slots of a merge with c <= 64
 
-__device__ __forceinline__ double readlane_d(double v, int l) {
-  const unsigned long long b = __builtin_bit_cast(unsigned long long, v);
-  const unsigned lo = (unsigned)__builtin_amdgcn_readlane((int)(unsigned)b, l);
-  const unsigned hi = (unsigned)__builtin_amdgcn_readlane((int)(unsigned)(b >> 32), l);
-  return __builtin_bit_cast(double, ((unsigned long long)hi << 32) | lo);
+typedef __attribute__((address_space(3))) double lds_f64;
+typedef __attribute__((address_space(3))) short lds_i16;
+
+// Empty asm that takes rows x0 .. x0 + 7 of U (those below N) as operands:
+// their updates must be complete here and cannot be deferred past it.
+template <int N>
+__device__ __forceinline__ void pin8(double (&U)[N], int x0) {
+  double* u = U + x0;
+  if (x0 + 8 <= N) {
+    asm volatile("" : "+v"(u[0]), "+v"(u[1]), "+v"(u[2]), "+v"(u[3]), "+v"(u[4]), "+v"(u[5]),
+                 "+v"(u[6]), "+v"(u[7]));
+  } else {
+#pragma unroll
+    for (int i = 0; i < 8; ++i)
+      if (x0 + i < N) asm volatile("" : "+v"(u[i]));
+  }
+}
+
+// Buffer descriptor over [p, p + bytes) with a wave-uniform base and size:
+// loads through it take a per-lane 32-bit offset and a scalar offset, so a
+// gather of many rows holds no 64-bit address per load.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t nd_rsrc(const void* p, unsigned bytes) {
+  const uint64_t a = (uint64_t)p;
+  const uint64_t au = ((uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((int)(a >> 32)) << 32) |
+                      (uint32_t)__builtin_amdgcn_readfirstlane((int)a);
+  return __builtin_amdgcn_make_buffer_rsrc((void*)au, (short)0,
+                                           __builtin_amdgcn_readfirstlane((int)bytes), 0x00020000);
+}
+
+__device__ __forceinline__ double nd_load(__amdgpu_buffer_rsrc_t r, unsigned voff, unsigned soff) {
+  return __builtin_bit_cast(double, __builtin_amdgcn_raw_buffer_load_b64(r, voff, soff, 0));
+}
+
+// An LDS pointer the compiler cannot see through: element reads at fixed
+// indices then use the instruction's offset field instead of a register
+// holding each address.
+template <typename P>
+__device__ __forceinline__ P* opaque_lds(const void* p) {
+  unsigned a = (unsigned)(uintptr_t)(const __attribute__((address_space(3))) char*)p;
+  asm volatile("" : "+v"(a));
+  return (P*)(uintptr_t)a;
 }
 
 // Geometry of merge `m` of the level described by na (children h x w).
@@ -586,124 +622,198 @@ __device__ void inverse_tables(const NdArgs& na, const MergeGeom& g, short (*inv
   __syncthreads();
 }
 
-template <int C, int NW, int CPT, bool FINAL>
-__global__ __launch_bounds__(64 * NW) void k_nd_cut(NdArgs na) {
-  constexpr int NT = 64 * NW;
-  static_assert(C <= 64, "one cut row per lane");
+template <int C, bool FINAL>
+__global__ __launch_bounds__(512) void k_nd_cut(NdArgs na) {
+  static_assert(C <= 64, "at most 64 cut rows");
   __shared__ short invt[2][MAXSLOT];
-  __shared__ double colb[2][64];
-  __shared__ double dg[64];
+  __shared__ double rowb[2][64];
+  __shared__ double isq[64];
   // final step: the eliminated rows' sink and source columns for G'
   __shared__ double zs[FINAL ? C : 1][FINAL ? 64 + 2 : 1];
   __shared__ double zq[FINAL ? C : 1][FINAL ? 64 + 2 : 1];
-  const int lane = threadIdx.x & 63;
-  const int wv = threadIdx.x >> 6;
+  // small merges (C <= 16, at most 64 ports): Z and the Schur update stay
+  // in this workgroup
+  constexpr bool kFuse = !FINAL && C <= 16;
+  __shared__ double zl[kFuse ? C : 1][kFuse ? 64 + 2 : 1];
+  const int y = threadIdx.x;
   const int T = na.T;
-  int E, ncol;
+  int E, ncol, Emax = 0;
   int64_t la;
-  double* zt = nullptr;
-  double U[CPT];
+  double* z = nullptr;
+  double U[C];
+  MergeGeom g{};
+  const double* Y0 = nullptr;
+  const double* Y1 = nullptr;
   if (FINAL) {
     la = blockIdx.x;
     E = na.ms.M + T;
     ncol = C + E;
     const int Ein = 4 * T, M = na.ms.M;
     const double* Y = na.buf_in + la * na.in_stride;
-    const int x = lane;
+    // column of this lane in the last level's matrix (clamped: always valid)
+    const int yc = y < C ? y : (y >= C + M && y < ncol ? T + (y - C - M) : 0);
+    const __amdgpu_buffer_rsrc_t ry = nd_rsrc(Y, (unsigned)(C * Ein * 8));
 #pragma unroll
-    for (int j = 0; j < CPT; ++j) {
-      const int y = wv + NW * j;
+    for (int x = 0; x < C; ++x) {
+      const double yv = nd_load(ry, 8u * (unsigned)yc, 8u * (unsigned)(x * Ein));
       double v = 0.0;
-      if (x < C && y < ncol) {
-        if (y < C) v = Y[y * Ein + x] + (x == y ? na.g_d : 0.0);
-        else if (y < C + M) v = (x == na.row_off + (y - C)) ? -na.g_d : 0.0;
-        else v = Y[(T + (y - C - M)) * Ein + x];
+      if (y < C) v = yv + (x == y ? na.g_d : 0.0);
+      else if (y < C + M) v = (x == na.row_off + (y - C)) ? -na.g_d : 0.0;
+      else if (y < ncol) v = yv;
+      U[x] = v;
+      if ((x & 31) == 31) {   // 32 loads in flight per round trip
+        pin8(U, x - 31);
+        pin8(U, x - 23);
+        pin8(U, x - 15);
+        pin8(U, x - 7);
       }
-      U[j] = v;
     }
   } else {
-    const MergeGeom g = merge_geom(na, blockIdx.x);
-    inverse_tables(na, g, invt, NT);
+    g = merge_geom(na, blockIdx.x);
+    inverse_tables(na, g, invt, blockDim.x);
     la = g.la;
     E = g.E;
+    Emax = g.Emax;
     ncol = C + E;
-    zt = na.scratch + la * na.scr_stride + (int64_t)g.m * g.Emax * C;
-    const double* Y0 = na.buf_in + la * na.in_stride + (int64_t)g.cm0 * g.Ein * g.Ein;
-    const double* Y1 = na.buf_in + la * na.in_stride + (int64_t)g.cm1 * g.Ein * g.Ein;
-    const int x = lane;
-    const int pa0 = x < C ? invt[0][x] : -1, pa1 = x < C ? invt[1][x] : -1;
-    // the children's matrices are symmetric: row pb, column pa is read so
-    // that consecutive lanes read consecutive ports
+    z = na.scratch + la * na.scr_stride + (int64_t)g.m * g.Emax * C;
+    Y0 = na.buf_in + la * na.in_stride + (int64_t)g.cm0 * g.Ein * g.Ein;
+    Y1 = na.buf_in + la * na.in_stride + (int64_t)g.cm1 * g.Ein * g.Ein;
+    const int pb0 = y < ncol ? invt[0][y] : -1, pb1 = y < ncol ? invt[1][y] : -1;
+    const unsigned cb = (unsigned)(g.Ein * g.Ein * 8);
+    const __amdgpu_buffer_rsrc_t r0 = nd_rsrc(Y0, cb), r1 = nd_rsrc(Y1, cb);
+    const unsigned q0 = 8u * (unsigned)max(pb0, 0), q1 = 8u * (unsigned)max(pb1, 0);
+    const lds_i16* iv = opaque_lds<lds_i16>(&invt[0][0]);
+    // the row's port is uniform (a scalar offset), the column's fixed per
+    // lane; clamped ports keep every offset valid, so that all loads of a
+    // chunk are in flight together, and entries without a port are masked
 #pragma unroll
-    for (int j = 0; j < CPT; ++j) {
-      const int y = wv + NW * j;
-      double v = 0.0;
-      if (y < ncol) {
-        const int pb0 = invt[0][y], pb1 = invt[1][y];
-        if (pa0 >= 0 && pb0 >= 0) v += Y0[pb0 * g.Ein + pa0];
-        if (pa1 >= 0 && pb1 >= 0) v += Y1[pb1 * g.Ein + pa1];
+    for (int x = 0; x < C; ++x) {
+      const int pa0 = __builtin_amdgcn_readfirstlane(iv[x]);
+      const int pa1 = __builtin_amdgcn_readfirstlane(iv[MAXSLOT + x]);
+      const double v0 = nd_load(r0, q0, 8u * (unsigned)(max(pa0, 0) * g.Ein));
+      const double v1 = nd_load(r1, q1, 8u * (unsigned)(max(pa1, 0) * g.Ein));
+      U[x] = ((pa0 >= 0 && pb0 >= 0) ? v0 : 0.0) + ((pa1 >= 0 && pb1 >= 0) ? v1 : 0.0);
+      // 16 rows (32 loads) in flight per round trip
+      if ((x & 15) == 15) {
+        pin8(U, x - 15);
+        pin8(U, x - 7);
       }
-      U[j] = v;
     }
   }
-  // Pivot k: the wave holding column k + 1 (slot (k + 1) / NW of wave
-  // (k + 1) % NW, both fixed once the loop is unrolled) first applies pivot k
-  // to that column and publishes its multipliers, then every wave applies
-  // pivot k to the rest of its columns.
-  if (wv == 0) {
-    const double piv = readlane_d(U[0], 0);
-    colb[0][lane] = (lane > 0 && lane < C) ? U[0] * recip(piv) : 0.0;
-    if (lane == 0) dg[0] = piv;
-  }
+  if (y < C) rowb[0][y] = U[0];
+  const lds_f64* rbase = opaque_lds<lds_f64>(&rowb[0][0]);
 #pragma clang loop unroll(full)
   for (int k = 0; k < C; ++k) {
     __syncthreads();
-    const double l = colb[k & 1][lane];
-    const int w1 = (k + 1) % NW, j1 = (k + 1) / NW;
-    if (k + 1 < C && wv == w1) {
-      U[j1] = fma(-l, readlane_d(U[j1], k), U[j1]);
-      const double piv = readlane_d(U[j1], k + 1);
-      colb[(k + 1) & 1][lane] = (lane > k + 1 && lane < C) ? U[j1] * recip(piv) : 0.0;
-      if (lane == 0) dg[k + 1] = piv;
+    const lds_f64* rb = rbase + (k & 1) * 64;
+    const double piv = rb[k];
+    if (y == 0) isq[k] = piv;
+    const double t = U[k] * recip(piv);
+    // row k + 1 first, so that it is published early; every row is updated
+    // here (the empty asm keeps the compiler from deferring an update to the
+    // row's own pivot, which would hold every pivot row's values live)
+    if (k + 1 < C) {
+      U[k + 1] = fma(-rb[k + 1], t, U[k + 1]);
+      if (y < C) rowb[(k + 1) & 1][y] = U[k + 1];
     }
+    // chunks of 8 rows, software pipelined: the next chunk's reads are
+    // issued before this chunk's FMAs, and a fence after the FMAs pins the
+    // updated rows here
+    double ra[8], rn[8];
 #pragma clang loop unroll(full)
-    for (int j = 0; j < CPT; ++j) {
-      if (NW * j + NW - 1 <= k) continue;          // every column of this slot is done
-      const int y = wv + NW * j;
-      if (y <= k || y >= ncol) continue;
-      if (k + 1 < C && j == j1 && wv == w1) continue;   // column k + 1, done above
-      U[j] = fma(-l, readlane_d(U[j], k), U[j]);
+    for (int i = 0; i < 8; ++i) ra[i] = (k + 2 + i < C) ? rb[k + 2 + i] : 0.0;
+#pragma clang loop unroll(full)
+    for (int x0 = k + 2; x0 < C; x0 += 8) {
+#pragma clang loop unroll(full)
+      for (int i = 0; i < 8; ++i) rn[i] = (x0 + 8 + i < C) ? rb[x0 + 8 + i] : 0.0;
+#pragma clang loop unroll(full)
+      for (int i = 0; i < 8; ++i)
+        if (x0 + i < C) U[x0 + i] = fma(-ra[i], t, U[x0 + i]);
+      pin8(U, x0);
+#pragma clang loop unroll(full)
+      for (int i = 0; i < 8; ++i) ra[i] = rn[i];
     }
   }
   __syncthreads();
-  const double isq = lane < C ? 1.0 / sqrt(dg[lane]) : 0.0;
-  if (!FINAL) {
-    // Zt[y - C][x] = U[x][y] / sqrt(D_x) for the external columns
-    if (lane < C) {
+  if (y < C) isq[y] = 1.0 / sqrt(isq[y]);
+  __syncthreads();
+  const lds_f64* is = opaque_lds<lds_f64>(&isq[0]);
+  if constexpr (kFuse) {
+    if (Emax <= 64) {
+      if (y >= C && y < ncol) {
 #pragma unroll
-      for (int j = 0; j < CPT; ++j) {
-        const int y = wv + NW * j;
-        if (y >= C && y < ncol) zt[(int64_t)(y - C) * C + lane] = U[j] * isq;
+        for (int x = 0; x < C; ++x) zl[x][y - C] = U[x] * is[x];
+      }
+      __syncthreads();
+      double* ext = na.buf_out + la * na.out_stride + (int64_t)g.m * Emax * Emax;
+      for (int it = threadIdx.x; it < 256; it += blockDim.x) {
+        const int tx = it >> 4, ty = it & 15;
+        if (4 * tx >= E || 4 * ty >= E) continue;
+        double acc[4][4];
+#pragma unroll
+        for (int a = 0; a < 4; ++a)
+#pragma unroll
+          for (int b = 0; b < 4; ++b) acc[a][b] = 0.0;
+#pragma unroll 2
+        for (int k = 0; k < C; ++k) {
+          double xa[4], yb[4];
+#pragma unroll
+          for (int a = 0; a < 4; ++a) xa[a] = zl[k][4 * tx + a];
+#pragma unroll
+          for (int b = 0; b < 4; ++b) yb[b] = zl[k][4 * ty + b];
+#pragma unroll
+          for (int a = 0; a < 4; ++a)
+#pragma unroll
+            for (int b = 0; b < 4; ++b) acc[a][b] = fma(xa[a], yb[b], acc[a][b]);
+        }
+#pragma unroll
+        for (int a = 0; a < 4; ++a) {
+          const int x = 4 * tx + a;
+          if (x >= E) continue;
+          const int pa0 = invt[0][C + x], pa1 = invt[1][C + x];
+#pragma unroll
+          for (int b = 0; b < 4; ++b) {
+            const int yy = 4 * ty + b;
+            if (yy >= E) continue;
+            const int pb0 = invt[0][C + yy], pb1 = invt[1][C + yy];
+            const double v0 = Y0[max(pa0, 0) * g.Ein + max(pb0, 0)];
+            const double v1 = Y1[max(pa1, 0) * g.Ein + max(pb1, 0)];
+            const double v = ((pa0 >= 0 && pb0 >= 0) ? v0 : 0.0) +
+                             ((pa1 >= 0 && pb1 >= 0) ? v1 : 0.0);
+            ext[x * Emax + yy] = v - acc[a][b];
+          }
+        }
+      }
+      return;
+    }
+  }
+  if (!FINAL) {
+    // Z[x][y - C] = U[x][y] / sqrt(D_x) for the external columns
+    if (y >= C && y < ncol) {
+      double* zc = z + (unsigned)(y - C);
+#pragma unroll
+      for (int x = 0; x < C; ++x) {
+        zc[(unsigned)(x * Emax)] = U[x] * is[x];
+        if ((x & 15) == 15) __builtin_amdgcn_sched_barrier(0);
       }
     }
     return;
   }
   // G'[j][k] = sum_x Z[x][sink j] Z[x][source k]
   const int M = na.ms.M, N = na.ms.N;
-  if (lane < C) {
+  if (y >= C && y < C + M && y - C < 64) {
 #pragma unroll
-    for (int j = 0; j < CPT; ++j) {
-      const int y = wv + NW * j;
-      if (y >= C && y < C + M && y - C < 64) zq[lane][y - C] = U[j] * isq;
-      if (y >= C + M && y < ncol && y - C - M < 64) zs[lane][y - C - M] = U[j] * isq;
-    }
+    for (int x = 0; x < C; ++x) zq[x][y - C] = U[x] * is[x];
+  } else if (y >= C + M && y < ncol && y - C - M < 64) {
+#pragma unroll
+    for (int x = 0; x < C; ++x) zs[x][y - C - M] = U[x] * is[x];
   }
   __syncthreads();
   const int64_t arr = na.arr0 + la;
   float* out = na.gpt + arr * (int64_t)na.ms.Np * na.ms.Mp;
   const int Np = na.ms.Np, Mp = na.ms.Mp;
-  if (threadIdx.x < 256) {
-    const int tx = threadIdx.x >> 4, ty = threadIdx.x & 15;
+  for (int it = threadIdx.x; it < 256; it += blockDim.x) {
+    const int tx = it >> 4, ty = it & 15;
     double acc[4][4];
 #pragma unroll
     for (int a = 0; a < 4; ++a)
@@ -734,7 +844,7 @@ __global__ __launch_bounds__(64 * NW) void k_nd_cut(NdArgs na) {
   }
 }
 
-// ext = V - Zt Zt^T on one 64 x 64 tile of one merge (V: the children's
+// ext = V - Z^T Z on one 64 x 64 tile of one merge (V: the children's
 // external-external entries).
 __global__ __launch_bounds__(256) void k_nd_schur(NdArgs na) {
   constexpr int KC = 16;
@@ -753,8 +863,26 @@ __global__ __launch_bounds__(256) void k_nd_schur(NdArgs na) {
   const int nrx = min(64, E - x0), nry = min(64, E - y0);
   if (nrx <= 0 || nry <= 0) return;
   inverse_tables(na, g, invt, 256);
-  const double* zt = na.scratch + g.la * na.scr_stride + (int64_t)g.m * Emax * c;
+  const double* z = na.scratch + g.la * na.scr_stride + (int64_t)g.m * Emax * c;
   const int tx = tid >> 4, ty = tid & 15;
+  // the children's external entries of this thread's 4 x 4 outputs, loaded
+  // first so that they are in flight during the product
+  const double* Y0 = na.buf_in + g.la * na.in_stride + (int64_t)g.cm0 * g.Ein * g.Ein;
+  const double* Y1 = na.buf_in + g.la * na.in_stride + (int64_t)g.cm1 * g.Ein * g.Ein;
+  double vv[4][4];
+#pragma unroll
+  for (int a = 0; a < 4; ++a) {
+    const int x = min(x0 + 4 * tx + a, E - 1);
+    const int pa0 = invt[0][c + x], pa1 = invt[1][c + x];
+#pragma unroll
+    for (int b = 0; b < 4; ++b) {
+      const int yy = min(y0 + 4 * ty + b, E - 1);
+      const int pb0 = invt[0][c + yy], pb1 = invt[1][c + yy];
+      const double v0 = Y0[max(pa0, 0) * g.Ein + max(pb0, 0)];
+      const double v1 = Y1[max(pa1, 0) * g.Ein + max(pb1, 0)];
+      vv[a][b] = ((pa0 >= 0 && pb0 >= 0) ? v0 : 0.0) + ((pa1 >= 0 && pb1 >= 0) ? v1 : 0.0);
+    }
+  }
   double acc[4][4];
 #pragma unroll
   for (int a = 0; a < 4; ++a)
@@ -763,10 +891,10 @@ __global__ __launch_bounds__(256) void k_nd_schur(NdArgs na) {
   for (int k0 = 0; k0 < c; k0 += KC) {
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      const int e = tid + 256 * r, xx = e / KC, kk = e % KC;
+      const int e = tid + 256 * r, xx = e & 63, kk = e >> 6;
       const int k = k0 + kk;
-      za[kk][xx] = (xx < nrx && k < c) ? zt[(int64_t)(x0 + xx) * c + k] : 0.0;
-      zb[kk][xx] = (xx < nry && k < c) ? zt[(int64_t)(y0 + xx) * c + k] : 0.0;
+      za[kk][xx] = (xx < nrx && k < c) ? z[(int64_t)k * Emax + x0 + xx] : 0.0;
+      zb[kk][xx] = (xx < nry && k < c) ? z[(int64_t)k * Emax + y0 + xx] : 0.0;
     }
     __syncthreads();
 #pragma unroll 4
@@ -783,23 +911,15 @@ __global__ __launch_bounds__(256) void k_nd_schur(NdArgs na) {
     }
     __syncthreads();
   }
-  const double* Y0 = na.buf_in + g.la * na.in_stride + (int64_t)g.cm0 * g.Ein * g.Ein;
-  const double* Y1 = na.buf_in + g.la * na.in_stride + (int64_t)g.cm1 * g.Ein * g.Ein;
   double* ext = na.buf_out + g.la * na.out_stride + (int64_t)g.m * Emax * Emax;
 #pragma unroll
   for (int a = 0; a < 4; ++a) {
     const int x = x0 + 4 * tx + a;
     if (x >= E) continue;
-    const int pa0 = invt[0][c + x], pa1 = invt[1][c + x];
 #pragma unroll
     for (int b = 0; b < 4; ++b) {
       const int y = y0 + 4 * ty + b;
-      if (y >= E) continue;
-      const int pb0 = invt[0][c + y], pb1 = invt[1][c + y];
-      double v = 0.0;
-      if (pa0 >= 0 && pb0 >= 0) v += Y0[pa0 * g.Ein + pb0];
-      if (pa1 >= 0 && pb1 >= 0) v += Y1[pa1 * g.Ein + pb1];
-      ext[x * Emax + y] = v - acc[a][b];
+      if (y < E) ext[x * Emax + y] = vv[a][b] - acc[a][b];
     }
   }
 }
@@ -844,32 +964,25 @@ int nd_side(int M, int N) {
   return T;
 }
 
-// Register elimination (one cut row per lane): the cut sizes and column
-// counts that have an instantiation.  Cut sizes are powers of two.
+// Register elimination: cut sizes with an instantiation (powers of two up to
+// 64) and at most 8 waves of columns.
 static bool cut_in_registers(int c, int ncol) {
-  return (c == 8 && ncol <= 64) || (c == 16 && ncol <= 128) || (c == 32 && ncol <= 256) ||
-         (c == 64 && ncol <= 448);
+  return (c == 8 || c == 16 || c == 32 || c == 64) && ncol <= 512;
 }
 
 template <bool FINAL>
 static void launch_cut(const NdArgs& na, dim3 grid, int c, int ncol, hipStream_t s) {
-#define RXNN_CUT(Cv, NWv, CPTv) \
-  hipLaunchKernelGGL((k_nd_cut<Cv, NWv, CPTv, FINAL>), grid, dim3(64 * NWv), 0, s, na)
-  if constexpr (FINAL) {   // c = T, ncol = 2 T + M <= 3 T
-    if (c == 16) RXNN_CUT(16, 16, 8);
-    else if (c == 32) RXNN_CUT(32, 16, 8);
-    else RXNN_CUT(64, 16, 12);
+  const dim3 blk((unsigned)((ncol + 63) / 64 * 64));
+  if constexpr (FINAL) {
+    if (c == 16) hipLaunchKernelGGL((k_nd_cut<16, true>), grid, blk, 0, s, na);
+    else if (c == 32) hipLaunchKernelGGL((k_nd_cut<32, true>), grid, blk, 0, s, na);
+    else hipLaunchKernelGGL((k_nd_cut<64, true>), grid, blk, 0, s, na);
   } else {
-    if (c == 8) RXNN_CUT(8, 4, 16);
-    else if (c == 16) RXNN_CUT(16, 16, 8);
-    else if (c == 32 && ncol <= 128) RXNN_CUT(32, 16, 8);
-    else if (c == 32 && ncol <= 192) RXNN_CUT(32, 16, 12);
-    else if (c == 32) RXNN_CUT(32, 16, 16);
-    else if (ncol <= 192) RXNN_CUT(64, 16, 12);
-    else if (ncol <= 320) RXNN_CUT(64, 16, 20);
-    else RXNN_CUT(64, 16, 28);
+    if (c == 8) hipLaunchKernelGGL((k_nd_cut<8, false>), grid, blk, 0, s, na);
+    else if (c == 16) hipLaunchKernelGGL((k_nd_cut<16, false>), grid, blk, 0, s, na);
+    else if (c == 32) hipLaunchKernelGGL((k_nd_cut<32, false>), grid, blk, 0, s, na);
+    else hipLaunchKernelGGL((k_nd_cut<64, false>), grid, blk, 0, s, na);
   }
-#undef RXNN_CUT
 }
 
 // Builds G' of arrays [arr0, arr0 + n) with the workspace ws (ping-pong
@@ -933,9 +1046,12 @@ hipError_t launch_nd_build(const MapScalars& ms, const float* W, float* gpt, int
       ProfScope prof("nd_merge", s);
       if (cut_in_registers(c, c + e_layout)) {
         launch_cut<false>(na, grid, c, c + e_layout, s);
-        const int nt = (2 * (nh + nw) + 63) / 64;
-        hipLaunchKernelGGL(k_nd_schur, dim3((unsigned)(n * nmerge * nt * nt)), dim3(256), 0, s,
-                           na);
+        const int emax = 2 * (nh + nw);
+        if (!(c <= 16 && emax <= 64)) {   // else the Schur update ran in k_nd_cut
+          const int nt = (emax + 63) / 64;
+          hipLaunchKernelGGL(k_nd_schur, dim3((unsigned)(n * nmerge * nt * nt)), dim3(256), 0,
+                             s, na);
+        }
       } else {
         hipLaunchKernelGGL(k_nd_merge, grid, dim3(NTH),
                            (unsigned)((KB * KB + 2 * KB * 64) * sizeof(double)), s, na);
