@@ -35,6 +35,8 @@
 // digits, leaving G' accurate to ~1e-12.  Every wire, driver and sense
 // resistance must be positive (zero resistances take the row sweep instead).
 
+#include <algorithm>
+
 #include "common.h"
 
 namespace rxnn {
@@ -650,16 +652,16 @@ __global__ __launch_bounds__(512) void k_nd_cut(NdArgs na) {
     ncol = C + E;
     const int Ein = 4 * T, M = na.ms.M;
     const double* Y = na.buf_in + la * na.in_stride;
-    // column of this lane in the last level's matrix (clamped: always valid)
-    const int yc = y < C ? y : (y >= C + M && y < ncol ? T + (y - C - M) : 0);
+    // column of this lane in the last level's matrix (clamped: always valid);
+    // branch-free, so that the loads of a chunk stay in flight together
+    const bool useY = y < C || (y >= C + M && y < ncol);
+    const int yc = y < C ? y : (useY ? T + (y - C - M) : 0);
+    const int srow = (y >= C && y < C + M) ? na.row_off + (y - C) : -1;   // driver of row
     const __amdgpu_buffer_rsrc_t ry = nd_rsrc(Y, (unsigned)(C * Ein * 8));
 #pragma unroll
     for (int x = 0; x < C; ++x) {
       const double yv = nd_load(ry, 8u * (unsigned)yc, 8u * (unsigned)(x * Ein));
-      double v = 0.0;
-      if (y < C) v = yv + (x == y ? na.g_d : 0.0);
-      else if (y < C + M) v = (x == na.row_off + (y - C)) ? -na.g_d : 0.0;
-      else if (y < ncol) v = yv;
+      const double v = (useY ? yv : 0.0) + (x == y ? na.g_d : 0.0) - (x == srow ? na.g_d : 0.0);
       U[x] = v;
       if ((x & 31) == 31) {   // 32 loads in flight per round trip
         pin8(U, x - 31);
@@ -814,6 +816,7 @@ __global__ __launch_bounds__(512) void k_nd_cut(NdArgs na) {
   const int Np = na.ms.Np, Mp = na.ms.Mp;
   for (int it = threadIdx.x; it < 256; it += blockDim.x) {
     const int tx = it >> 4, ty = it & 15;
+    if (4 * tx >= Np || 4 * ty >= Mp) continue;
     double acc[4][4];
 #pragma unroll
     for (int a = 0; a < 4; ++a)
@@ -972,7 +975,8 @@ static bool cut_in_registers(int c, int ncol) {
 
 template <bool FINAL>
 static void launch_cut(const NdArgs& na, dim3 grid, int c, int ncol, hipStream_t s) {
-  const dim3 blk((unsigned)((ncol + 63) / 64 * 64));
+  // the final step's G' product has 256 work items: at least 256 threads
+  const dim3 blk((unsigned)std::max((ncol + 63) / 64 * 64, FINAL ? 256 : 64));
   if constexpr (FINAL) {
     if (c == 16) hipLaunchKernelGGL((k_nd_cut<16, true>), grid, blk, 0, s, na);
     else if (c == 32) hipLaunchKernelGGL((k_nd_cut<32, true>), grid, blk, 0, s, na);
