@@ -741,16 +741,31 @@ __global__ __launch_bounds__(512) void k_nd_cut(NdArgs na) {
   __syncthreads();
   const lds_f64* is = opaque_lds<lds_f64>(&isq[0]);
   if constexpr (kFuse) {
-    if (Emax <= 64) {
+    if (Emax <= 64) {   // schur_fused(C, Emax): launched with at least 256 threads
       if (y >= C && y < ncol) {
 #pragma unroll
         for (int x = 0; x < C; ++x) zl[x][y - C] = U[x] * is[x];
       }
       __syncthreads();
       double* ext = na.buf_out + la * na.out_stride + (int64_t)g.m * Emax * Emax;
-      for (int it = threadIdx.x; it < 256; it += blockDim.x) {
-        const int tx = it >> 4, ty = it & 15;
-        if (4 * tx >= E || 4 * ty >= E) continue;
+      // 256 threads (at least): one 4 x 4 block of outputs each
+      if (threadIdx.x < 256) {
+        const int tx = threadIdx.x >> 4, ty = threadIdx.x & 15;
+        // the children's entries first, so that their loads overlap the product
+        double vv[4][4];
+#pragma unroll
+        for (int a = 0; a < 4; ++a) {
+          const int x = min(4 * tx + a, E - 1);
+          const int pa0 = invt[0][C + x], pa1 = invt[1][C + x];
+#pragma unroll
+          for (int b = 0; b < 4; ++b) {
+            const int yy = min(4 * ty + b, E - 1);
+            const int pb0 = invt[0][C + yy], pb1 = invt[1][C + yy];
+            const double v0 = Y0[max(pa0, 0) * g.Ein + max(pb0, 0)];
+            const double v1 = Y1[max(pa1, 0) * g.Ein + max(pb1, 0)];
+            vv[a][b] = ((pa0 >= 0 && pb0 >= 0) ? v0 : 0.0) + ((pa1 >= 0 && pb1 >= 0) ? v1 : 0.0);
+          }
+        }
         double acc[4][4];
 #pragma unroll
         for (int a = 0; a < 4; ++a)
@@ -772,17 +787,10 @@ __global__ __launch_bounds__(512) void k_nd_cut(NdArgs na) {
         for (int a = 0; a < 4; ++a) {
           const int x = 4 * tx + a;
           if (x >= E) continue;
-          const int pa0 = invt[0][C + x], pa1 = invt[1][C + x];
 #pragma unroll
           for (int b = 0; b < 4; ++b) {
             const int yy = 4 * ty + b;
-            if (yy >= E) continue;
-            const int pb0 = invt[0][C + yy], pb1 = invt[1][C + yy];
-            const double v0 = Y0[max(pa0, 0) * g.Ein + max(pb0, 0)];
-            const double v1 = Y1[max(pa1, 0) * g.Ein + max(pb1, 0)];
-            const double v = ((pa0 >= 0 && pb0 >= 0) ? v0 : 0.0) +
-                             ((pa1 >= 0 && pb1 >= 0) ? v1 : 0.0);
-            ext[x * Emax + yy] = v - acc[a][b];
+            if (yy < E) ext[x * Emax + yy] = vv[a][b] - acc[a][b];
           }
         }
       }
@@ -872,6 +880,8 @@ __global__ __launch_bounds__(256) void k_nd_schur(NdArgs na) {
   // first so that they are in flight during the product
   const double* Y0 = na.buf_in + g.la * na.in_stride + (int64_t)g.cm0 * g.Ein * g.Ein;
   const double* Y1 = na.buf_in + g.la * na.in_stride + (int64_t)g.cm1 * g.Ein * g.Ein;
+  const unsigned cb = (unsigned)(g.Ein * g.Ein * 8);
+  const __amdgpu_buffer_rsrc_t r0 = nd_rsrc(Y0, cb), r1 = nd_rsrc(Y1, cb);
   double vv[4][4];
 #pragma unroll
   for (int a = 0; a < 4; ++a) {
@@ -881,8 +891,8 @@ __global__ __launch_bounds__(256) void k_nd_schur(NdArgs na) {
     for (int b = 0; b < 4; ++b) {
       const int yy = min(y0 + 4 * ty + b, E - 1);
       const int pb0 = invt[0][c + yy], pb1 = invt[1][c + yy];
-      const double v0 = Y0[max(pa0, 0) * g.Ein + max(pb0, 0)];
-      const double v1 = Y1[max(pa1, 0) * g.Ein + max(pb1, 0)];
+      const double v0 = nd_load(r0, 8u * (unsigned)(max(pa0, 0) * g.Ein + max(pb0, 0)), 0);
+      const double v1 = nd_load(r1, 8u * (unsigned)(max(pa1, 0) * g.Ein + max(pb1, 0)), 0);
       vv[a][b] = ((pa0 >= 0 && pb0 >= 0) ? v0 : 0.0) + ((pa1 >= 0 && pb1 >= 0) ? v1 : 0.0);
     }
   }
@@ -891,16 +901,37 @@ __global__ __launch_bounds__(256) void k_nd_schur(NdArgs na) {
   for (int a = 0; a < 4; ++a)
 #pragma unroll
     for (int b = 0; b < 4; ++b) acc[a][b] = 0.0;
-  for (int k0 = 0; k0 < c; k0 += KC) {
+  // every chunk of Z (c <= 64: at most 4) is loaded into registers first, so
+  // that the loads share one round trip
+  constexpr int NCH = 64 / KC;
+  double pza[NCH][4], pzb[NCH][4];
+  const __amdgpu_buffer_rsrc_t rz = nd_rsrc(z, (unsigned)(c * Emax * 8));
+  const unsigned ox = 8u * (unsigned)(x0 + min(tid & 63, nrx - 1));
+  const unsigned oy = 8u * (unsigned)(y0 + min(tid & 63, nry - 1));
+#pragma unroll
+  for (int q = 0; q < NCH; ++q)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int e = tid + 256 * r, xx = e & 63, kk = e >> 6;   // kk: uniform per wave
+      const int k = min(q * KC + kk, c - 1);
+      const unsigned ko = (unsigned)__builtin_amdgcn_readfirstlane(k * Emax * 8);
+      const double a = nd_load(rz, ox, ko);
+      const double b = nd_load(rz, oy, ko);
+      const bool ok = q * KC < c && q * KC + kk < c;
+      pza[q][r] = (ok && xx < nrx) ? a : 0.0;
+      pzb[q][r] = (ok && xx < nry) ? b : 0.0;
+    }
+#pragma unroll
+  for (int q = 0; q < NCH; ++q) {
+    if (q * KC >= c) break;
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const int e = tid + 256 * r, xx = e & 63, kk = e >> 6;
-      const int k = k0 + kk;
-      za[kk][xx] = (xx < nrx && k < c) ? z[(int64_t)k * Emax + x0 + xx] : 0.0;
-      zb[kk][xx] = (xx < nry && k < c) ? z[(int64_t)k * Emax + y0 + xx] : 0.0;
+      za[kk][xx] = pza[q][r];
+      zb[kk][xx] = pzb[q][r];
     }
     __syncthreads();
-#pragma unroll 4
+#pragma unroll 2
     for (int kk = 0; kk < KC; ++kk) {
       double xa[4], yb[4];
 #pragma unroll
@@ -973,10 +1004,14 @@ static bool cut_in_registers(int c, int ncol) {
   return (c == 8 || c == 16 || c == 32 || c == 64) && ncol <= 512;
 }
 
+// Merges whose Schur update runs inside k_nd_cut (its kFuse path).
+static bool schur_fused(int c, int emax) { return c <= 16 && emax <= 64; }
+
 template <bool FINAL>
-static void launch_cut(const NdArgs& na, dim3 grid, int c, int ncol, hipStream_t s) {
-  // the final step's G' product has 256 work items: at least 256 threads
-  const dim3 blk((unsigned)std::max((ncol + 63) / 64 * 64, FINAL ? 256 : 64));
+static void launch_cut(const NdArgs& na, dim3 grid, int c, int ncol, bool fused, hipStream_t s) {
+  // the final step's G' product and a fused Schur update have 256 work
+  // items, one per thread: at least 256 threads then
+  const dim3 blk((unsigned)std::max((ncol + 63) / 64 * 64, (FINAL || fused) ? 256 : 64));
   if constexpr (FINAL) {
     if (c == 16) hipLaunchKernelGGL((k_nd_cut<16, true>), grid, blk, 0, s, na);
     else if (c == 32) hipLaunchKernelGGL((k_nd_cut<32, true>), grid, blk, 0, s, na);
@@ -1049,9 +1084,10 @@ hipError_t launch_nd_build(const MapScalars& ms, const float* W, float* gpt, int
     {
       ProfScope prof("nd_merge", s);
       if (cut_in_registers(c, c + e_layout)) {
-        launch_cut<false>(na, grid, c, c + e_layout, s);
         const int emax = 2 * (nh + nw);
-        if (!(c <= 16 && emax <= 64)) {   // else the Schur update ran in k_nd_cut
+        const bool fused = schur_fused(c, emax);
+        launch_cut<false>(na, grid, c, c + e_layout, fused, s);
+        if (!fused) {
           const int nt = (emax + 63) / 64;
           hipLaunchKernelGGL(k_nd_schur, dim3((unsigned)(n * nmerge * nt * nt)), dim3(256), 0,
                              s, na);
@@ -1074,7 +1110,7 @@ hipError_t launch_nd_build(const MapScalars& ms, const float* W, float* gpt, int
   {
     ProfScope prof("nd_final", s);
     if (na.T <= 64 && cut_in_registers(na.T, 2 * na.T + ms.M)) {
-      launch_cut<true>(na, dim3((unsigned)n), na.T, 2 * na.T + ms.M, s);
+      launch_cut<true>(na, dim3((unsigned)n), na.T, 2 * na.T + ms.M, false, s);
     } else
       hipLaunchKernelGGL(k_nd_final, dim3((unsigned)n), dim3(NTH),
                          (unsigned)((KB * KB + 2 * KB * 64) * sizeof(double)), s, na);
