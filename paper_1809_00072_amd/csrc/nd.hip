@@ -46,6 +46,7 @@ struct NdArgs {
   const float* W;
   float* gpt;
   int64_t arr0;          // first array of this chunk
+  int64_t n_arrays;      // arrays in this chunk
   int T, row_off;        // grid side, first grid row of the tile (T - M)
   double g_r, g_c, g_s, g_d;
   double* buf_in;        // level buffers and scratch (per array strides below)
@@ -59,12 +60,9 @@ struct NdArgs {
 namespace {
 
 constexpr int NTH = 256;        // threads of the kernels on the blocked global path
-constexpr int NTB = 1024;       // threads of the 16 x 16 block kernel
-// doubles per LDS level buffer of a bs x bs block reduction
-__host__ __device__ constexpr int lbuf(int bs) { return bs == 16 ? 6400 : 1600; }
 constexpr int KB = 16;          // pivots per elimination block
 
-__device__ __forceinline__ void ports(int i0, int j0, int h, int w, int T, int& nL, int& nR,
+__host__ __device__ constexpr void ports(int i0, int j0, int h, int w, int T, int& nL, int& nR,
                                       int& nT, int& nB) {
   nL = h;
   nR = (j0 + w < T) ? h : 0;
@@ -75,14 +73,14 @@ __device__ __forceinline__ void ports(int i0, int j0, int h, int w, int T, int& 
 // Where port p of child `ch` (0: top/left, 1: bottom/right) of a merge of two
 // h x w blocks at (i0, j0) goes: >= 0 an external port of the merged block,
 // < 0 the shared (cut) node -1 - k.
-__device__ __forceinline__ int merge_dest(int ch, int p, int i0, int j0, int h, int w, bool vert,
+__host__ __device__ constexpr int merge_dest(int ch, int p, int i0, int j0, int h, int w, bool vert,
                                           int T) {
   const int nh = vert ? 2 * h : h, nw = vert ? w : 2 * w;
   const bool Rn = j0 + nw < T, Tn = i0 > 0;
   const int oR = nh, oT = nh + (Rn ? nh : 0), oB = oT + (Tn ? nw : 0);
   const int ci = (vert && ch) ? i0 + h : i0, cj = (!vert && ch) ? j0 + w : j0;
   const bool Rc = cj + w < T, Tc = ci > 0;
-  int seg, idx = p;  // 0 L, 1 R, 2 T, 3 B
+  int seg = 0, idx = p;  // 0 L, 1 R, 2 T, 3 B
   if (idx < h) seg = 0;
   else {
     idx -= h;
@@ -134,8 +132,8 @@ __device__ __forceinline__ double recip(double a) {
   return r;
 }
 
-__device__ __forceinline__ int nports(int i0, int j0, int h, int w, int T) {
-  int a, b, c, d;
+__host__ __device__ constexpr int nports(int i0, int j0, int h, int w, int T) {
+  int a = 0, b = 0, c = 0, d = 0;
   ports(i0, j0, h, w, T, a, b, c, d);
   return a + b + c + d;
 }
@@ -170,138 +168,193 @@ __device__ __forceinline__ double cell_conductance(const MapScalars& ms, const f
 }
 
 // ---------------------------------------------------------------------------
-// Levels 1 x 1 .. SB x SB of one SB x SB block, in LDS.
+// Levels 1 x 1 .. 8 x 8 of one 8 x 8 block per wave.  A level's merges are
+// packed into groups of GS lanes (GS: the power of two >= the merge's
+// combined size LD = c + E): lane y of a group holds column y of its merge's
+// combined matrix [c cut nodes | E external ports], every row in registers.
+// Eliminating the c cut pivots updates every later row, so the external
+// rows and columns end as the merged block's admittance matrix.  The
+// multiplier of row x at pivot k is that row's entry in column k, fetched
+// from the group's lane k (ds_bpermute; a lane read for a whole wave).  No
+// workgroup barrier: each wave's levels use its own LDS buffers.
 // ---------------------------------------------------------------------------
-template <int SB, int NB>
-__global__ __launch_bounds__(NB) void k_nd_block(NdArgs na) {
-  __shared__ double bufA[lbuf(SB)];
-  __shared__ double bufB[lbuf(SB)];
-  __shared__ short tab[1024];
-  const int tid = threadIdx.x;
+constexpr int BS = 8;                 // side of the blocks of this kernel
+constexpr int BWAVES = 4;             // blocks (waves) per workgroup
+constexpr int BLEVELS = 6;            // 1x1 -> 2x1 -> 2x2 -> 4x2 -> 4x4 -> 8x4 -> 8x8
+constexpr int BUFA = 1024, BUFB = 1152;   // doubles per wave: leaves / even / odd levels
+
+// Child port landing on each combined slot (cut nodes 0 .. c-1, then the
+// externals), per level and per boundary variant (bit 1: the merged block
+// has ports on its right, bit 0: on its top) - the only geometry on which
+// the port maps of a merge depend.
+struct BlkTab {
+  short s[BLEVELS][4][2][64];
+};
+
+constexpr BlkTab make_blk_tab() {
+  BlkTab t{};
+  for (int l = 0; l < BLEVELS; ++l)
+    for (int v = 0; v < 4; ++v)
+      for (int ch = 0; ch < 2; ++ch)
+        for (int k = 0; k < 64; ++k) t.s[l][v][ch][k] = -1;
+  const int hs[BLEVELS] = {1, 2, 2, 4, 4, 8}, ws[BLEVELS] = {1, 1, 2, 2, 4, 4};
+  const int Tr = 1024;   // any grid larger than the merged block
+  for (int l = 0; l < BLEVELS; ++l) {
+    const bool vert = (l % 2) == 0;
+    const int h = hs[l], w = ws[l];
+    const int nh = vert ? 2 * h : h, nw = vert ? w : 2 * w;
+    const int c = vert ? w : h;
+    for (int v = 0; v < 4; ++v) {
+      const int i0 = (v & 1) ? nh : 0, j0 = (v & 2) ? 0 : Tr - nw;
+      for (int ch = 0; ch < 2; ++ch) {
+        const int ci = (vert && ch) ? i0 + h : i0, cj = (!vert && ch) ? j0 + w : j0;
+        const int np = nports(ci, cj, h, w, Tr);
+        for (int p = 0; p < np; ++p) {
+          const int d = merge_dest(ch, p, i0, j0, h, w, vert, Tr);
+          t.s[l][v][ch][d >= 0 ? c + d : -1 - d] = (short)p;
+        }
+      }
+    }
+  }
+  return t;
+}
+
+__constant__ BlkTab kBlkTab = make_blk_tab();
+
+__device__ __forceinline__ double bperm_d(double v, int src_lane) {
+  const unsigned long long b = __builtin_bit_cast(unsigned long long, v);
+  const unsigned lo = (unsigned)__builtin_amdgcn_ds_bpermute(src_lane << 2, (int)(unsigned)b);
+  const unsigned hi = (unsigned)__builtin_amdgcn_ds_bpermute(src_lane << 2, (int)(unsigned)(b >> 32));
+  return __builtin_bit_cast(double, ((unsigned long long)hi << 32) | lo);
+}
+
+__device__ __forceinline__ double readlane_d(double v, int l) {
+  const unsigned long long b = __builtin_bit_cast(unsigned long long, v);
+  const unsigned lo = (unsigned)__builtin_amdgcn_readlane((int)(unsigned)b, l);
+  const unsigned hi = (unsigned)__builtin_amdgcn_readlane((int)(unsigned)(b >> 32), l);
+  return __builtin_bit_cast(double, ((unsigned long long)hi << 32) | lo);
+}
+
+// LDS written by some lanes of a wave, then read by others of the same wave.
+__device__ __forceinline__ void wave_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// One level of merges of the block at (I0, J0): children h x w (in: EIN x
+// EIN per child), merged blocks written with stride EM (out).
+template <int L, int H, int W, bool VERT>
+__device__ __forceinline__ void block_level(int T, int I0, int J0, const short* tab,
+                                            const double* in, double* out, int lane) {
+  constexpr int NH = VERT ? 2 * H : H, NW = VERT ? W : 2 * W;
+  constexpr int C = VERT ? W : H;
+  constexpr int EM = 2 * (NH + NW), EIN = 2 * (H + W);
+  constexpr int LD = C + EM;
+  constexpr int GS = LD <= 8 ? 8 : (LD <= 16 ? 16 : (LD <= 32 ? 32 : 64));
+  constexpr int GPW = 64 / GS;                 // merges per pass
+  constexpr int MC = BS / NW, CC = BS / W;     // merges / children per block row
+  constexpr int NM = (BS / NH) * MC;
+  static_assert(NM % GPW == 0, "whole passes");
+  const int g = lane / GS, yl = lane % GS, gb = lane - yl;
+#pragma unroll 1
+  for (int pass = 0; pass < NM / GPW; ++pass) {
+    const int m = pass * GPW + g;
+    const int mi = m / MC, mj = m % MC;
+    const int i0 = I0 + mi * NH, j0 = J0 + mj * NW;
+    const bool rn = j0 + NW < T, tn = i0 > 0;
+    const int ld = C + NH + (rn ? NH : 0) + (tn ? NW : 0) + NW;
+    const int cm0 = VERT ? (mi * 2) * CC + mj : mi * CC + mj * 2;
+    const int cm1 = VERT ? (mi * 2 + 1) * CC + mj : mi * CC + mj * 2 + 1;
+    const short* t0 = tab + (((L * 4) + (rn ? 2 : 0) + (tn ? 1 : 0)) * 2) * 64;
+    const short* t1 = t0 + 64;
+    const double* c0 = in + cm0 * EIN * EIN;
+    const double* c1 = in + cm1 * EIN * EIN;
+    const int s0 = t0[yl], s1 = t1[yl];
+    double U[LD];
+#pragma unroll
+    for (int x = 0; x < LD; ++x) {
+      const int r0 = t0[x], r1 = t1[x];
+      const double a = c0[max(r0, 0) * EIN + max(s0, 0)];
+      const double b = c1[max(r1, 0) * EIN + max(s1, 0)];
+      U[x] = ((r0 >= 0 && s0 >= 0) ? a : 0.0) + ((r1 >= 0 && s1 >= 0) ? b : 0.0);
+    }
+#pragma unroll
+    for (int k = 0; k < C; ++k) {
+      const double piv = GS == 64 ? readlane_d(U[k], k) : bperm_d(U[k], gb + k);
+      const double t = U[k] * recip(piv);
+#pragma unroll
+      for (int x = k + 1; x < LD; ++x) {
+        const double mx = GS == 64 ? readlane_d(U[x], k) : bperm_d(U[x], gb + k);
+        U[x] = fma(-mx, t, U[x]);
+      }
+    }
+    if (yl >= C && yl < ld) {
+#pragma unroll
+      for (int x = C; x < LD; ++x)
+        if (x < ld) out[m * EM * EM + (x - C) * EM + (yl - C)] = U[x];
+    }
+  }
+  wave_sync();
+}
+
+__global__ __launch_bounds__(64 * BWAVES) void k_nd_block(NdArgs na) {
+  __shared__ short tab[BLEVELS * 4 * 2 * 64];
+  __shared__ double bufA[BWAVES][BUFA];
+  __shared__ double bufB[BWAVES][BUFB];
+  const short* ct = &kBlkTab.s[0][0][0][0];
+  for (int e = threadIdx.x; e < BLEVELS * 4 * 2 * 64; e += 64 * BWAVES) tab[e] = ct[e];
+  __syncthreads();
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
   const int T = na.T;
-  const int nsb = T / SB;
-  const int64_t la = blockIdx.x / (nsb * nsb);
-  const int sb = (int)(blockIdx.x % (nsb * nsb));
-  const int I0 = (sb / nsb) * SB, J0 = (sb % nsb) * SB;
+  const int nsb = T / BS;
+  const int64_t blk = (int64_t)blockIdx.x * BWAVES + wv;
+  const int64_t nblk = na.n_arrays * nsb * nsb;
+  if (blk >= nblk) return;
+  const int64_t la = blk / (nsb * nsb);
+  const int sb = (int)(blk % (nsb * nsb));
+  const int I0 = (sb / nsb) * BS, J0 = (sb % nsb) * BS;
   const int64_t arr = na.arr0 + la;
   const MapScalars& ms = na.ms;
   const double wmax = ms.wmax_fixed > 0.0f ? (double)ms.wmax_fixed : (double)*ms.d_wmax;
-
-  // leaves: one cell per thread, 4 x 4 slots
-  if (tid < SB * SB) {
-    const int li = tid / SB, lj = tid % SB;
+  double* A = bufA[wv];
+  double* B = bufB[wv];
+  // leaves: one cell per lane, ports [L | R (not at the right edge) | T (not
+  // at the top) | B] in a 4 x 4 slot
+  {
+    const int li = lane / BS, lj = lane % BS;
     const int gi = I0 + li, gj = J0 + lj;
     const double G = cell_conductance(ms, na.W, wmax, arr, gi, gj, na.row_off);
     const bool hasR = gj + 1 < T, hasT = gi > 0;
     const double gv = (gi + 1 < T) ? na.g_c : na.g_s;
-    double* Y = bufA + tid * 16;
+    double* Y = A + lane * 16;   // this lane's slot (LDS: the indices below vary)
 #pragma unroll
     for (int e = 0; e < 16; ++e) Y[e] = 0.0;
-    const int L = 0, R = 1, Tp = hasR ? 2 : 1, B = (hasR ? 2 : 1) + (hasT ? 1 : 0);
-    auto st = [&](int p, int q, double g) {
-      Y[p * 4 + p] += g;
-      Y[q * 4 + q] += g;
-      Y[p * 4 + q] -= g;
-      Y[q * 4 + p] -= g;
+    const int Lp = 0, Rp = 1, Tp = hasR ? 2 : 1, Bp = (hasR ? 2 : 1) + (hasT ? 1 : 0);
+    auto st = [&](int p, int q, double gg) {
+      Y[p * 4 + p] += gg;
+      Y[q * 4 + q] += gg;
+      Y[p * 4 + q] -= gg;
+      Y[q * 4 + p] -= gg;
     };
-    if (hasR) st(L, R, na.g_r);
+    if (hasR) st(Lp, Rp, na.g_r);
     if (hasT) {
-      st(L, Tp, G);
-      st(Tp, B, gv);
+      st(Lp, Tp, G);
+      st(Tp, Bp, gv);
     } else {
       const double ge = G > 0.0 ? (G * gv) / (G + gv) : 0.0;
-      st(L, B, ge);
+      st(Lp, Bp, ge);
     }
   }
-  __syncthreads();
-
-  double* in = bufA;
-  double* out = bufB;
-  int h = 1, w = 1, ld_in = 4;
-  bool vert = true;
-  while (h < SB || w < SB) {
-    const int nh = vert ? 2 * h : h, nw = vert ? w : 2 * w;
-    const int E = 2 * (nh + nw), c = vert ? w : h, ld = E + c, slot = ld * ld;
-    const int cols = SB / nw;                    // merged blocks per row of the block
-    const int nmerge = (SB / nh) * cols;
-    const int ccols = SB / w;                    // child blocks per row
-    const int npc = ld_in;                       // child slot side
-    // destination of every child port in its merge's combined matrix
-    for (int t = tid; t < nmerge * 2 * npc; t += NB) {
-      const int m = t / (2 * npc), r2 = t - m * 2 * npc, ch = r2 >= npc ? 1 : 0;
-      const int p = r2 - ch * npc;
-      const int mi = m / cols, mj = m - mi * cols;
-      const int i0 = I0 + mi * nh, j0 = J0 + mj * nw;
-      const int np = nports((vert && ch) ? i0 + h : i0, (!vert && ch) ? j0 + w : j0, h, w, T);
-      int d = -1;
-      if (p < np) {
-        d = merge_dest(ch, p, i0, j0, h, w, vert, T);
-        d = d >= 0 ? d : E + (-1 - d);
-      }
-      tab[t] = (short)d;
-    }
-    for (int e = tid; e < nmerge * slot; e += NB) out[e] = 0.0;
-    __syncthreads();
-    // child entries: consecutive threads take consecutive columns q; task
-    // spaces are padded to powers of two so that indices come from shifts
-    const int lgq = lg2ceil(npc), lgc = lg2ceil(cols), lgcc = lg2ceil(ccols);
-    for (int ch = 0; ch < 2; ++ch) {
-      for (int t = tid; t < nmerge << (2 * lgq); t += NB) {
-        const int q = t & ((1 << lgq) - 1), p = (t >> lgq) & ((1 << lgq) - 1);
-        const int m = t >> (2 * lgq);
-        if (p >= npc || q >= npc) continue;
-        const short* dt = tab + (m * 2 + ch) * npc;
-        const int dp = dt[p], dq = dt[q];
-        if (dp < 0 || dq < 0) continue;
-        const int mi = m >> lgc, mj = m & (cols - 1);
-        const int cm = vert ? (((mi * 2 + ch) << lgcc) + mj) : ((mi << lgcc) + mj * 2 + ch);
-        out[m * slot + dp * ld + dq] += in[cm * npc * npc + p * npc + q];
-      }
-      __syncthreads();
-    }
-    // eliminate the c shared nodes (pivot rows / columns E .. E + c - 1):
-    // a task is one column y of one merge over a chunk of 8 rows
-    const int lgy = lg2ceil(ld), lgx = lg2ceil((ld + 7) / 8);
-    for (int k = 0; k < c; ++k) {
-      const int pv = E + k;
-      for (int t = tid; t < nmerge << (lgy + lgx); t += NB) {
-        const int y = t & ((1 << lgy) - 1);
-        const int x0 = ((t >> lgy) & ((1 << lgx) - 1)) * 8;
-        const int m = t >> (lgy + lgx);
-        if (y >= ld || y == pv || x0 >= ld) continue;
-        double* A = out + m * slot;
-        const double g = A[pv * ld + y] * recip(A[pv * ld + pv]);
-        if (g == 0.0) continue;
-        double axp[8], axy[8];
-#pragma unroll
-        for (int xx = 0; xx < 8; ++xx) {
-          const int x = min(x0 + xx, ld - 1);
-          axp[xx] = A[x * ld + pv];
-          axy[xx] = A[x * ld + y];
-        }
-#pragma unroll
-        for (int xx = 0; xx < 8; ++xx) {
-          const int x = x0 + xx;
-          if (x < ld && x != pv) A[x * ld + y] = axy[xx] - axp[xx] * g;
-        }
-      }
-      __syncthreads();
-    }
-    double* t = in;
-    in = out;
-    out = t;
-    ld_in = ld;
-    h = nh;
-    w = nw;
-    vert = !vert;
-  }
-  // the 16 x 16 block's matrix -> global (ld 64)
-  constexpr int EO = 4 * SB;   // ports of an interior SB x SB block
+  wave_sync();
+  block_level<0, 1, 1, true>(T, I0, J0, tab, A, B, lane);
+  block_level<1, 2, 1, false>(T, I0, J0, tab, B, A, lane);
+  block_level<2, 2, 2, true>(T, I0, J0, tab, A, B, lane);
+  block_level<3, 4, 2, false>(T, I0, J0, tab, B, A, lane);
+  block_level<4, 4, 4, true>(T, I0, J0, tab, A, B, lane);
+  constexpr int EO = 4 * BS;   // ports of an interior 8 x 8 block
   double* dst = na.buf_out + la * na.out_stride + (int64_t)sb * EO * EO;
-  for (int e = tid; e < EO * EO; e += NB) {
-    const int p = e / EO, q = e % EO;
-    dst[e] = (p < ld_in && q < ld_in) ? in[p * ld_in + q] : 0.0;
-  }
+  block_level<5, 8, 4, false>(T, I0, J0, tab, B, dst, lane);
 }
 
 // ---------------------------------------------------------------------------
@@ -960,11 +1013,11 @@ __global__ __launch_bounds__(256) void k_nd_schur(NdArgs na) {
 
 }  // namespace
 
-// Side of the blocks reduced in LDS: 8 x 8 blocks give more, smaller
-// workgroups (several per CU) when the arrays of a chunk alone would not fill
-// the device; 16 x 16 blocks need fewer merge passes.
+// Side of the blocks the first kernel reduces (one wave per block).
 int nd_block_side(int T, int64_t n_arrays) {
-  return (n_arrays * (T / 16) * (T / 16) < 1024) ? 8 : 16;
+  (void)T;
+  (void)n_arrays;
+  return BS;
 }
 
 // Doubles of workspace one array needs (level buffers in, out, scratch).
@@ -1033,6 +1086,7 @@ hipError_t launch_nd_build(const MapScalars& ms, const float* W, float* gpt, int
   na.W = W;
   na.gpt = gpt;
   na.arr0 = arr0;
+  na.n_arrays = n;
   na.T = nd_side(ms.M, ms.N);
   na.row_off = na.T - ms.M;
   na.g_r = 1.0 / ms.r_row;
@@ -1052,11 +1106,8 @@ hipError_t launch_nd_build(const MapScalars& ms, const float* W, float* gpt, int
   na.buf_out = bufA;
   {
     ProfScope prof("nd_block", s);
-    const dim3 grid((unsigned)(n * nsb * nsb));
-    if (bs == 8)
-      hipLaunchKernelGGL((k_nd_block<8, NTH>), grid, dim3(NTH), 0, s, na);
-    else
-      hipLaunchKernelGGL((k_nd_block<16, NTB>), grid, dim3(NTB), 0, s, na);
+    const dim3 grid((unsigned)((n * nsb * nsb + BWAVES - 1) / BWAVES));
+    hipLaunchKernelGGL(k_nd_block, grid, dim3(64 * BWAVES), 0, s, na);
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
