@@ -26,14 +26,18 @@
 // Attaching the drivers and eliminating the row-input nodes leaves the
 // transfer admittance from the row sources to the sinks, i.e. G'.
 //
-// Levels up to 16 x 16 cells run in LDS, one workgroup per 16 x 16 block;
-// every later merge and the final step is one workgroup that eliminates the
-// shared nodes in blocks of 16 (Cholesky of the 16 x 16 pivot block,
-// triangular solve of its rows, rank-16 update of the rest).  All arithmetic
-// is fp64; wire conductances exceed device conductances by about four orders
-// of magnitude, and the elimination of series wires loses about that many
-// digits, leaving G' accurate to ~1e-12.  Every wire, driver and sense
-// resistance must be positive (zero resistances take the row sweep instead).
+// Levels up to 8 x 8 cells: one wave per 8 x 8 block (k_nd_block).  Merges
+// with at most 64 shared nodes: one workgroup per merge eliminates them with
+// the shared rows in registers (k_nd_cut), and k_nd_schur applies the
+// resulting update to the external block on 64 x 64 tiles; the final step
+// with at most 64 row inputs likewise.  Larger merges and final steps run on
+// one workgroup with the shared rows in global memory, eliminated in blocks
+// of 16 (Cholesky of the 16 x 16 pivot block, triangular solve of its rows,
+// rank-16 update of the rest).  All arithmetic is fp64; wire conductances
+// exceed device conductances by about four orders of magnitude, and the
+// elimination of series wires loses about that many digits, leaving G'
+// accurate to ~1e-12.  Every wire, driver and sense resistance must be
+// positive (zero resistances take the row sweep instead).
 
 #include <algorithm>
 
