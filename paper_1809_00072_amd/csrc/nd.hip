@@ -664,11 +664,11 @@ __device__ __forceinline__ MergeGeom merge_geom(const NdArgs& na, int64_t blk) {
 
 // invt[ch][slot]: the port of child ch that lands on merged slot `slot`
 // (cut node k -> slot k, external port d -> slot c + d), or -1.
-__device__ void inverse_tables(const NdArgs& na, const MergeGeom& g, short (*invt)[MAXSLOT],
-                               int NT) {
+template <int NS>
+__device__ void inverse_tables(const NdArgs& na, const MergeGeom& g, short (*invt)[NS], int NT) {
   const int tid = threadIdx.x;
   const bool vert = na.vert != 0;
-  for (int t = tid; t < 2 * MAXSLOT; t += NT) invt[t / MAXSLOT][t % MAXSLOT] = -1;
+  for (int t = tid; t < 2 * NS; t += NT) invt[t / NS][t % NS] = -1;
   __syncthreads();
   for (int t = tid; t < 2 * g.Ein; t += NT) {
     const int ch = t / g.Ein, p = t - ch * g.Ein;
@@ -729,7 +729,7 @@ __global__ __launch_bounds__(512) void k_nd_cut(NdArgs na) {
     }
   } else {
     g = merge_geom(na, blockIdx.x);
-    inverse_tables(na, g, invt, blockDim.x);
+    inverse_tables<MAXSLOT>(na, g, invt, blockDim.x);
     la = g.la;
     E = g.E;
     Emax = g.Emax;
@@ -912,11 +912,205 @@ __global__ __launch_bounds__(512) void k_nd_cut(NdArgs na) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// Merges and the final step with 128 cut nodes: two row groups of 64 (lane y
+// of row group rg holds rows 64 rg .. 64 rg + 63 of column y in registers),
+// columns = the 128 cut columns plus a panel of up to 256 external columns
+// per workgroup (the cut block is eliminated again in every panel's
+// workgroup, so the panels need no exchange).  Pivot k: the row group
+// holding row k publishes it in LDS with the entries at and left of the
+// pivot column set to zero, so that every lane applies the pivot to all its
+// rows with one FMA each and no row test (a zero multiplier leaves a row
+// unchanged); chunks of 8 rows wholly at or above the pivot are skipped.  The
+// pivot loop runs over blocks of 8 pivots unrolled, which keeps the code
+// small.  Z (the eliminated rows scaled by D^-1/2, over this panel's
+// externals) goes to scratch for k_nd_schur or, for the final step, for
+// k_nd_gprod.
+// ---------------------------------------------------------------------------
+constexpr int C2 = 128;              // cut nodes
+constexpr int P2 = 256;              // external columns per panel
+constexpr int CP2 = C2 + P2;         // columns per workgroup
+constexpr int MAXSLOT2 = 1024;       // slots of a merge with 128 cut nodes (<= 7 c)
+
+template <bool FINAL>
+__global__ __launch_bounds__(2 * CP2) void k_nd_cut2(NdArgs na) {
+  __shared__ short invt[2][FINAL ? 1 : MAXSLOT2];
+  __shared__ double rowb[2][CP2];
+  __shared__ double pivs[2];
+  __shared__ double dg[C2];
+  const int yl = threadIdx.x % CP2, rg = threadIdx.x / CP2;   // rg: uniform per wave
+  const int T = na.T;
+  int64_t la;
+  int E, zld, pn;
+  double* z;
+  double U[64];
+  if constexpr (FINAL) {
+    la = blockIdx.x;
+    pn = 0;
+    E = na.ms.M + T;
+    zld = E;
+    z = na.scratch + la * na.scr_stride;
+    const int Ein = 4 * T, M = na.ms.M;
+    const double* Y = na.buf_in + la * na.in_stride;
+    const int e = yl - C2;
+    const bool useY = yl < C2 || (e >= M && e < E);
+    const int yc = yl < C2 ? yl : (useY ? T + (e - M) : 0);
+    const int srow = (e >= 0 && e < M) ? na.row_off + e : -1;
+    const __amdgpu_buffer_rsrc_t ry = nd_rsrc(Y, (unsigned)(C2 * Ein * 8));
+#pragma unroll
+    for (int i = 0; i < 64; ++i) {
+      const int x = 64 * rg + i;
+      const double yv = nd_load(ry, 8u * (unsigned)yc, 8u * (unsigned)(x * Ein));
+      U[i] = (useY ? yv : 0.0) + (x == yl ? na.g_d : 0.0) - (x == srow ? na.g_d : 0.0);
+      if ((i & 7) == 7) pin8(U, i - 7);
+    }
+  } else {
+    const int nh = na.vert ? 2 * na.h : na.h, nw = na.vert ? na.w : 2 * na.w;
+    const int npan = (2 * (nh + nw) + P2 - 1) / P2;
+    pn = (int)(blockIdx.x % npan);
+    const MergeGeom g = merge_geom(na, blockIdx.x / npan);
+    inverse_tables<MAXSLOT2>(na, g, invt, 2 * CP2);
+    la = g.la;
+    E = g.E;
+    zld = g.Emax;
+    z = na.scratch + la * na.scr_stride + (int64_t)g.m * g.Emax * C2;
+    const double* Y0 = na.buf_in + la * na.in_stride + (int64_t)g.cm0 * g.Ein * g.Ein;
+    const double* Y1 = na.buf_in + la * na.in_stride + (int64_t)g.cm1 * g.Ein * g.Ein;
+    const int e = pn * P2 + (yl - C2);
+    const int slot = yl < C2 ? yl : (e < E ? C2 + e : -1);
+    const int pb0 = slot >= 0 ? invt[0][slot] : -1, pb1 = slot >= 0 ? invt[1][slot] : -1;
+    const unsigned cb = (unsigned)(g.Ein * g.Ein * 8);
+    const __amdgpu_buffer_rsrc_t r0 = nd_rsrc(Y0, cb), r1 = nd_rsrc(Y1, cb);
+    const unsigned q0 = 8u * (unsigned)max(pb0, 0), q1 = 8u * (unsigned)max(pb1, 0);
+#pragma unroll
+    for (int i = 0; i < 64; ++i) {
+      const int x = 64 * rg + i;
+      const int pa0 = __builtin_amdgcn_readfirstlane(invt[0][x]);
+      const int pa1 = __builtin_amdgcn_readfirstlane(invt[1][x]);
+      const double v0 = nd_load(r0, q0, 8u * (unsigned)(max(pa0, 0) * g.Ein));
+      const double v1 = nd_load(r1, q1, 8u * (unsigned)(max(pa1, 0) * g.Ein));
+      U[i] = ((pa0 >= 0 && pb0 >= 0) ? v0 : 0.0) + ((pa1 >= 0 && pb1 >= 0) ? v1 : 0.0);
+      if ((i & 7) == 7) pin8(U, i - 7);
+    }
+  }
+  // row 0 (row group 0), zero at and left of the pivot
+  if (rg == 0) rowb[0][yl] = yl > 0 ? U[0] : 0.0;
+  if (rg == 0 && yl == 0) pivs[0] = U[0];
+  const lds_f64* rbase = opaque_lds<lds_f64>(&rowb[0][0]);
+#pragma unroll 1
+  for (int q = 0; q < C2 / 8; ++q) {
+#pragma clang loop unroll(full)
+    for (int r = 0; r < 8; ++r) {
+      const int k = 8 * q + r;
+      __syncthreads();
+      const lds_f64* rb = rbase + (k & 1) * CP2;
+      const double piv = pivs[k & 1];
+      if (threadIdx.x == 0) dg[k] = piv;
+      const double t = rb[yl] * recip(piv);
+#pragma clang loop unroll(full)
+      for (int j = 0; j < 8; ++j) {
+        const int xb = 64 * rg + 8 * j;
+        if (xb + 7 > k) {
+          double rr[8];
+#pragma clang loop unroll(full)
+          for (int i = 0; i < 8; ++i) rr[i] = rb[xb + i];
+#pragma clang loop unroll(full)
+          for (int i = 0; i < 8; ++i) U[8 * j + i] = fma(-rr[i], t, U[8 * j + i]);
+          pin8(U, 8 * j);
+        }
+      }
+      // publish row k + 1 from its row group
+      const int k1 = k + 1;
+      if (k1 < C2 && rg == (k1 >> 6)) {
+        const int jj = (k1 & 63) >> 3;
+        double v = 0.0;
+#pragma clang loop unroll(full)
+        for (int j = 0; j < 8; ++j)
+          if (j == jj) v = U[8 * j + ((r + 1) & 7)];
+        rowb[k1 & 1][yl] = yl > k1 ? v : 0.0;
+        if (yl == k1) pivs[k1 & 1] = v;
+      }
+    }
+  }
+  __syncthreads();
+  if (threadIdx.x < C2) dg[threadIdx.x] = 1.0 / sqrt(dg[threadIdx.x]);
+  __syncthreads();
+  // Z[x][e] = U[x][e] / sqrt(D_x) for this panel's externals
+  const int e = pn * P2 + (yl - C2);
+  if (yl >= C2 && e < E) {
+    const lds_f64* is = opaque_lds<lds_f64>(&dg[0]);
+    double* zc = z + (unsigned)e;
+#pragma unroll
+    for (int i = 0; i < 64; ++i) {
+      zc[(unsigned)((64 * rg + i) * zld)] = U[i] * is[64 * rg + i];
+      if ((i & 15) == 15) __builtin_amdgcn_sched_barrier(0);
+    }
+  }
+}
+
+// G' of the final step with more than 64 row inputs: G'[j][k] = sum_x
+// Z[x][M + j] Z[x][k] (Z: T x (M + T) in scratch) on 64 x 64 tiles.
+__global__ __launch_bounds__(256) void k_nd_gprod(NdArgs na) {
+  constexpr int KC = 16;
+  __shared__ double za[KC][64 + 2];
+  __shared__ double zb[KC][64 + 2];
+  const int tid = threadIdx.x;
+  const int M = na.ms.M, N = na.ms.N, T = na.T, Np = na.ms.Np, Mp = na.ms.Mp;
+  const int ntx = (Np + 63) / 64, nty = (Mp + 63) / 64;
+  const int64_t la = blockIdx.x / (ntx * nty);
+  const int tt = (int)(blockIdx.x % (ntx * nty));
+  const int j0 = (tt / nty) * 64, k0 = (tt % nty) * 64;
+  const int zld = M + T;
+  const double* z = na.scratch + la * na.scr_stride;
+  const int tx = tid >> 4, ty = tid & 15;
+  double acc[4][4];
+#pragma unroll
+  for (int a = 0; a < 4; ++a)
+#pragma unroll
+    for (int b = 0; b < 4; ++b) acc[a][b] = 0.0;
+  for (int x0 = 0; x0 < T; x0 += KC) {
+#pragma unroll
+    for (int rr = 0; rr < 4; ++rr) {
+      const int e = tid + 256 * rr, xx = e & 63, kk = e >> 6;
+      const int x = x0 + kk;
+      const int j = j0 + xx, k = k0 + xx;
+      za[kk][xx] = (x < T && j < N) ? z[(int64_t)x * zld + M + j] : 0.0;
+      zb[kk][xx] = (x < T && k < M) ? z[(int64_t)x * zld + k] : 0.0;
+    }
+    __syncthreads();
+#pragma unroll 2
+    for (int kk = 0; kk < KC; ++kk) {
+      double sa[4], qb[4];
+#pragma unroll
+      for (int a = 0; a < 4; ++a) sa[a] = za[kk][4 * tx + a];
+#pragma unroll
+      for (int b = 0; b < 4; ++b) qb[b] = zb[kk][4 * ty + b];
+#pragma unroll
+      for (int a = 0; a < 4; ++a)
+#pragma unroll
+        for (int b = 0; b < 4; ++b) acc[a][b] = fma(sa[a], qb[b], acc[a][b]);
+    }
+    __syncthreads();
+  }
+  const int64_t arr = na.arr0 + la;
+  float* out = na.gpt + arr * (int64_t)Np * Mp;
+#pragma unroll
+  for (int a = 0; a < 4; ++a) {
+    const int j = j0 + 4 * tx + a;
+    if (j >= Np) continue;
+#pragma unroll
+    for (int b = 0; b < 4; ++b) {
+      const int k = k0 + 4 * ty + b;
+      if (k < Mp) out[j * Mp + k] = (j < N && k < M) ? (float)acc[a][b] : 0.0f;
+    }
+  }
+}
+
 // ext = V - Z^T Z on one 64 x 64 tile of one merge (V: the children's
 // external-external entries).
 __global__ __launch_bounds__(256) void k_nd_schur(NdArgs na) {
   constexpr int KC = 16;
-  __shared__ short invt[2][MAXSLOT];
+  __shared__ short invt[2][MAXSLOT2];
   __shared__ double za[KC][64 + 2];
   __shared__ double zb[KC][64 + 2];
   const int tid = threadIdx.x;
@@ -930,7 +1124,7 @@ __global__ __launch_bounds__(256) void k_nd_schur(NdArgs na) {
   const int x0 = (tt / nt) * 64, y0 = (tt % nt) * 64;
   const int nrx = min(64, E - x0), nry = min(64, E - y0);
   if (nrx <= 0 || nry <= 0) return;
-  inverse_tables(na, g, invt, 256);
+  inverse_tables<MAXSLOT2>(na, g, invt, 256);
   const double* z = na.scratch + g.la * na.scr_stride + (int64_t)g.m * Emax * c;
   const int tx = tid >> 4, ty = tid & 15;
   // the children's external entries of this thread's 4 x 4 outputs, loaded
@@ -958,49 +1152,52 @@ __global__ __launch_bounds__(256) void k_nd_schur(NdArgs na) {
   for (int a = 0; a < 4; ++a)
 #pragma unroll
     for (int b = 0; b < 4; ++b) acc[a][b] = 0.0;
-  // every chunk of Z (c <= 64: at most 4) is loaded into registers first, so
-  // that the loads share one round trip
+  // Z in rounds of 64 rows (c <= 64: one round): a round's chunks are loaded
+  // into registers first, so that their loads share one round trip
   constexpr int NCH = 64 / KC;
-  double pza[NCH][4], pzb[NCH][4];
   const __amdgpu_buffer_rsrc_t rz = nd_rsrc(z, (unsigned)(c * Emax * 8));
   const unsigned ox = 8u * (unsigned)(x0 + min(tid & 63, nrx - 1));
   const unsigned oy = 8u * (unsigned)(y0 + min(tid & 63, nry - 1));
+#pragma unroll 1
+  for (int kb = 0; kb < c; kb += 64) {
+    double pza[NCH][4], pzb[NCH][4];
 #pragma unroll
-  for (int q = 0; q < NCH; ++q)
+    for (int q = 0; q < NCH; ++q)
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int e = tid + 256 * r, xx = e & 63, kk = e >> 6;   // kk: uniform per wave
-      const int k = min(q * KC + kk, c - 1);
-      const unsigned ko = (unsigned)__builtin_amdgcn_readfirstlane(k * Emax * 8);
-      const double a = nd_load(rz, ox, ko);
-      const double b = nd_load(rz, oy, ko);
-      const bool ok = q * KC < c && q * KC + kk < c;
-      pza[q][r] = (ok && xx < nrx) ? a : 0.0;
-      pzb[q][r] = (ok && xx < nry) ? b : 0.0;
-    }
+      for (int r = 0; r < 4; ++r) {
+        const int e = tid + 256 * r, xx = e & 63, kk = e >> 6;   // kk: uniform per wave
+        const int k = min(kb + q * KC + kk, c - 1);
+        const unsigned ko = (unsigned)__builtin_amdgcn_readfirstlane(k * Emax * 8);
+        const double a = nd_load(rz, ox, ko);
+        const double b = nd_load(rz, oy, ko);
+        const bool ok = kb + q * KC + kk < c;
+        pza[q][r] = (ok && xx < nrx) ? a : 0.0;
+        pzb[q][r] = (ok && xx < nry) ? b : 0.0;
+      }
 #pragma unroll
-  for (int q = 0; q < NCH; ++q) {
-    if (q * KC >= c) break;
+    for (int q = 0; q < NCH; ++q) {
+      if (kb + q * KC >= c) break;
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int e = tid + 256 * r, xx = e & 63, kk = e >> 6;
-      za[kk][xx] = pza[q][r];
-      zb[kk][xx] = pzb[q][r];
-    }
-    __syncthreads();
+      for (int r = 0; r < 4; ++r) {
+        const int e = tid + 256 * r, xx = e & 63, kk = e >> 6;
+        za[kk][xx] = pza[q][r];
+        zb[kk][xx] = pzb[q][r];
+      }
+      __syncthreads();
 #pragma unroll 2
-    for (int kk = 0; kk < KC; ++kk) {
-      double xa[4], yb[4];
+      for (int kk = 0; kk < KC; ++kk) {
+        double xa[4], yb[4];
 #pragma unroll
-      for (int a = 0; a < 4; ++a) xa[a] = za[kk][4 * tx + a];
+        for (int a = 0; a < 4; ++a) xa[a] = za[kk][4 * tx + a];
 #pragma unroll
-      for (int b = 0; b < 4; ++b) yb[b] = zb[kk][4 * ty + b];
+        for (int b = 0; b < 4; ++b) yb[b] = zb[kk][4 * ty + b];
 #pragma unroll
-      for (int a = 0; a < 4; ++a)
+        for (int a = 0; a < 4; ++a)
 #pragma unroll
-        for (int b = 0; b < 4; ++b) acc[a][b] = fma(xa[a], yb[b], acc[a][b]);
+          for (int b = 0; b < 4; ++b) acc[a][b] = fma(xa[a], yb[b], acc[a][b]);
+      }
+      __syncthreads();
     }
-    __syncthreads();
   }
   double* ext = na.buf_out + g.la * na.out_stride + (int64_t)g.m * Emax * Emax;
 #pragma unroll
@@ -1147,6 +1344,14 @@ hipError_t launch_nd_build(const MapScalars& ms, const float* W, float* gpt, int
           hipLaunchKernelGGL(k_nd_schur, dim3((unsigned)(n * nmerge * nt * nt)), dim3(256), 0,
                              s, na);
         }
+      } else if (c == C2) {
+        const int emax = 2 * (nh + nw);
+        const unsigned npan = (unsigned)((emax + P2 - 1) / P2);
+        hipLaunchKernelGGL((k_nd_cut2<false>), dim3((unsigned)(n * nmerge) * npan), dim3(2 * CP2),
+                           0, s, na);
+        const int nt = (emax + 63) / 64;
+        hipLaunchKernelGGL(k_nd_schur, dim3((unsigned)(n * nmerge * nt * nt)), dim3(256), 0, s,
+                           na);
       } else {
         hipLaunchKernelGGL(k_nd_merge, grid, dim3(NTH),
                            (unsigned)((KB * KB + 2 * KB * 64) * sizeof(double)), s, na);
@@ -1166,6 +1371,10 @@ hipError_t launch_nd_build(const MapScalars& ms, const float* W, float* gpt, int
     ProfScope prof("nd_final", s);
     if (na.T <= 64 && cut_in_registers(na.T, 2 * na.T + ms.M)) {
       launch_cut<true>(na, dim3((unsigned)n), na.T, 2 * na.T + ms.M, false, s);
+    } else if (na.T == C2) {
+      hipLaunchKernelGGL((k_nd_cut2<true>), dim3((unsigned)n), dim3(2 * CP2), 0, s, na);
+      const unsigned nt = (unsigned)(((ms.Np + 63) / 64) * ((ms.Mp + 63) / 64));
+      hipLaunchKernelGGL(k_nd_gprod, dim3((unsigned)n * nt), dim3(256), 0, s, na);
     } else
       hipLaunchKernelGGL(k_nd_final, dim3((unsigned)n), dim3(NTH),
                          (unsigned)((KB * KB + 2 * KB * 64) * sizeof(double)), s, na);
