@@ -59,6 +59,11 @@ struct NdArgs {
   int64_t in_stride, out_stride, scr_stride;  // doubles per array
   int h, w, vert;        // children size and merge direction (merge kernel)
   int e_layout;          // largest external port count of a merge at this level
+  // staged elimination of a dense combined matrix (more than 128 cut nodes)
+  const double* dA;      // stage input, dn x dn (row stride dld) per array (stride in_stride)
+  double* dB;            // stage output (row stride dldo) per array
+  int dn, dld, dldo;
+  int dpanel;            // external columns per workgroup of the cut kernel
 };
 
 namespace {
@@ -681,9 +686,13 @@ __device__ void inverse_tables(const NdArgs& na, const MergeGeom& g, short (*inv
   __syncthreads();
 }
 
-template <int C, bool FINAL>
+// MODE 0: a merge (children through the port tables); 1: the final step;
+// 2: a stage of a dense combined matrix (its first C rows are the pivots,
+// the rest of its columns are handled in panels of na.dpanel).
+template <int C, int MODE>
 __global__ __launch_bounds__(512) void k_nd_cut(NdArgs na) {
   static_assert(C <= 64, "at most 64 cut rows");
+  constexpr bool FINAL = MODE == 1;
   __shared__ short invt[2][MAXSLOT];
   __shared__ double rowb[2][64];
   __shared__ double isq[64];
@@ -692,18 +701,40 @@ __global__ __launch_bounds__(512) void k_nd_cut(NdArgs na) {
   __shared__ double zq[FINAL ? C : 1][FINAL ? 64 + 2 : 1];
   // small merges (C <= 16, at most 64 ports): Z and the Schur update stay
   // in this workgroup
-  constexpr bool kFuse = !FINAL && C <= 16;
+  constexpr bool kFuse = MODE == 0 && C <= 16;
   __shared__ double zl[kFuse ? C : 1][kFuse ? 64 + 2 : 1];
   const int y = threadIdx.x;
   const int T = na.T;
   int E, ncol, Emax = 0;
+  int zld = 0, ebase = 0;   // Z row stride, first external column of this workgroup
   int64_t la;
   double* z = nullptr;
   double U[C];
   MergeGeom g{};
   const double* Y0 = nullptr;
   const double* Y1 = nullptr;
-  if (FINAL) {
+  if constexpr (MODE == 2) {
+    const int npan = (na.dn - C + na.dpanel - 1) / na.dpanel;
+    la = blockIdx.x / npan;
+    const int pn = (int)(blockIdx.x % npan);
+    E = na.dn - C;
+    zld = E;
+    ebase = pn * na.dpanel;
+    ncol = C + min(na.dpanel, E - ebase);
+    z = na.scratch + la * na.scr_stride;
+    const double* A = na.dA + la * na.in_stride;
+    const int col = y < C ? y : (y < ncol ? C + ebase + (y - C) : 0);
+    const __amdgpu_buffer_rsrc_t ra = nd_rsrc(A, (unsigned)(C * na.dld * 8));
+#pragma unroll
+    for (int x = 0; x < C; ++x) {
+      const double v = nd_load(ra, 8u * (unsigned)col, 8u * (unsigned)(x * na.dld));
+      U[x] = y < ncol ? v : 0.0;
+      if ((x & 15) == 15) {
+        pin8(U, x - 15);
+        pin8(U, x - 7);
+      }
+    }
+  } else if constexpr (FINAL) {
     la = blockIdx.x;
     E = na.ms.M + T;
     ncol = C + E;
@@ -733,6 +764,7 @@ __global__ __launch_bounds__(512) void k_nd_cut(NdArgs na) {
     la = g.la;
     E = g.E;
     Emax = g.Emax;
+    zld = Emax;
     ncol = C + E;
     z = na.scratch + la * na.scr_stride + (int64_t)g.m * g.Emax * C;
     Y0 = na.buf_in + la * na.in_stride + (int64_t)g.cm0 * g.Ein * g.Ein;
@@ -855,12 +887,12 @@ __global__ __launch_bounds__(512) void k_nd_cut(NdArgs na) {
     }
   }
   if (!FINAL) {
-    // Z[x][y - C] = U[x][y] / sqrt(D_x) for the external columns
+    // Z[x][ebase + y - C] = U[x][y] / sqrt(D_x) for the external columns
     if (y >= C && y < ncol) {
-      double* zc = z + (unsigned)(y - C);
+      double* zc = z + (unsigned)(ebase + y - C);
 #pragma unroll
       for (int x = 0; x < C; ++x) {
-        zc[(unsigned)(x * Emax)] = U[x] * is[x];
+        zc[(unsigned)(x * zld)] = U[x] * is[x];
         if ((x & 15) == 15) __builtin_amdgcn_sched_barrier(0);
       }
     }
@@ -1106,6 +1138,139 @@ __global__ __launch_bounds__(256) void k_nd_gprod(NdArgs na) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// More than 128 cut nodes (the top merge and the final step of 256 x 256
+// grids): the combined matrix [cut | externals] is written out dense
+// (k_nd_dense0) and eliminated in stages of 64 pivots, each a k_nd_cut<64>
+// (mode 2) over column panels followed by the Schur update of the rest
+// (k_nd_dschur).  The last stage writes the merged block (or G').
+// ---------------------------------------------------------------------------
+// Dense combined matrix of one merge (rows in blocks of 16 per workgroup) or
+// of the final step: [row inputs (T) | sources (M) | sinks (T)].
+template <bool FINAL>
+__global__ __launch_bounds__(256) void k_nd_dense0(NdArgs na) {
+  __shared__ short invt[2][MAXSLOT2];
+  const int n = na.dn, ld = na.dldo;
+  const int nrb = (n + 15) / 16;
+  const int64_t la = blockIdx.x / nrb;
+  const int x0 = (int)(blockIdx.x % nrb) * 16;
+  double* B = na.dB + la * na.out_stride;
+  if constexpr (FINAL) {
+    const int T = na.T, M = na.ms.M, Ein = 4 * T;
+    const double* Y = na.buf_in + la * na.in_stride;
+    // index -> port of the last level (-1: a source terminal)
+    auto port = [&](int i) { return i < T ? i : (i < T + M ? -1 : T + (i - T - M)); };
+    for (int e = threadIdx.x; e < 16 * n; e += 256) {
+      const int x = x0 + e / n, y = e % n;
+      if (x >= n) continue;
+      const int px = port(x), py = port(y);
+      double v = (px >= 0 && py >= 0) ? Y[(int64_t)px * Ein + py] : 0.0;
+      if (x == y && (x < T || px < 0)) v += na.g_d;   // driver at the row input / source
+      if (x < T && py < 0 && x == na.row_off + (y - T)) v -= na.g_d;
+      if (y < T && px < 0 && y == na.row_off + (x - T)) v -= na.g_d;
+      B[(int64_t)x * ld + y] = v;
+    }
+  } else {
+    const MergeGeom g = merge_geom(na, la);   // one merge per array at this level
+    inverse_tables<MAXSLOT2>(na, g, invt, 256);
+    const double* Y0 = na.buf_in + la * na.in_stride + (int64_t)g.cm0 * g.Ein * g.Ein;
+    const double* Y1 = na.buf_in + la * na.in_stride + (int64_t)g.cm1 * g.Ein * g.Ein;
+    for (int e = threadIdx.x; e < 16 * n; e += 256) {
+      const int x = x0 + e / n, y = e % n;
+      if (x >= n) continue;
+      const int pa0 = invt[0][x], pa1 = invt[1][x], pb0 = invt[0][y], pb1 = invt[1][y];
+      double v = 0.0;
+      if (pa0 >= 0 && pb0 >= 0) v += Y0[pa0 * g.Ein + pb0];
+      if (pa1 >= 0 && pb1 >= 0) v += Y1[pa1 * g.Ein + pb1];
+      B[(int64_t)x * ld + y] = v;
+    }
+  }
+}
+
+// One stage's Schur update on a 64 x 64 tile: with Z (64 x E, E = dn - 64)
+// of the stage's pivots, OUT 0 writes A[64 + x][64 + y] - (Z^T Z)[x][y] for
+// x, y < E to dB (row stride dldo); OUT 1 writes G' = (Z^T Z - A) over the
+// sink x source block (A: [sources (M) | sinks (T)] after the pivots).
+template <int OUT>
+__global__ __launch_bounds__(256) void k_nd_dschur(NdArgs na) {
+  constexpr int KC = 16;
+  __shared__ double za[KC][64 + 2];
+  __shared__ double zb[KC][64 + 2];
+  const int tid = threadIdx.x;
+  const int E = na.dn - 64;
+  const int M = na.ms.M;
+  const int nrx = OUT == 0 ? E : na.ms.Np, nry = OUT == 0 ? E : na.ms.Mp;
+  const int ntx = (nrx + 63) / 64, nty = (nry + 63) / 64;
+  const int64_t la = blockIdx.x / (ntx * nty);
+  const int tt = (int)(blockIdx.x % (ntx * nty));
+  const int x0 = (tt / nty) * 64, y0 = (tt % nty) * 64;
+  // rows of Z and of A behind this tile's x and y
+  const int zx0 = OUT == 0 ? x0 : M + x0, zy0 = y0;
+  const int lx = OUT == 0 ? E : min(na.ms.N, na.T), ly = OUT == 0 ? E : M;   // valid x, y
+  const double* z = na.scratch + la * na.scr_stride;
+  const double* A = na.dA + la * na.in_stride;
+  const int tx = tid >> 4, ty = tid & 15;
+  double acc[4][4];
+#pragma unroll
+  for (int a = 0; a < 4; ++a)
+#pragma unroll
+    for (int b = 0; b < 4; ++b) acc[a][b] = 0.0;
+  for (int k0 = 0; k0 < 64; k0 += KC) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int e = tid + 256 * r, xx = e & 63, kk = e >> 6;
+      const int k = k0 + kk;
+      za[kk][xx] = (x0 + xx < lx) ? z[(int64_t)k * E + zx0 + xx] : 0.0;
+      zb[kk][xx] = (y0 + xx < ly) ? z[(int64_t)k * E + zy0 + xx] : 0.0;
+    }
+    __syncthreads();
+#pragma unroll 2
+    for (int kk = 0; kk < KC; ++kk) {
+      double xa[4], yb[4];
+#pragma unroll
+      for (int a = 0; a < 4; ++a) xa[a] = za[kk][4 * tx + a];
+#pragma unroll
+      for (int b = 0; b < 4; ++b) yb[b] = zb[kk][4 * ty + b];
+#pragma unroll
+      for (int a = 0; a < 4; ++a)
+#pragma unroll
+        for (int b = 0; b < 4; ++b) acc[a][b] = fma(xa[a], yb[b], acc[a][b]);
+    }
+    __syncthreads();
+  }
+  if constexpr (OUT == 0) {
+    double* B = na.dB + la * na.out_stride;
+#pragma unroll
+    for (int a = 0; a < 4; ++a) {
+      const int x = x0 + 4 * tx + a;
+      if (x >= E) continue;
+#pragma unroll
+      for (int b = 0; b < 4; ++b) {
+        const int y = y0 + 4 * ty + b;
+        if (y < E) B[(int64_t)x * na.dldo + y] = A[(int64_t)(64 + x) * na.dld + 64 + y] - acc[a][b];
+      }
+    }
+  } else {
+    const int64_t arr = na.arr0 + la;
+    const int Np = na.ms.Np, Mp = na.ms.Mp, N = na.ms.N;
+    float* out = na.gpt + arr * (int64_t)Np * Mp;
+#pragma unroll
+    for (int a = 0; a < 4; ++a) {
+      const int j = x0 + 4 * tx + a;
+      if (j >= Np) continue;
+#pragma unroll
+      for (int b = 0; b < 4; ++b) {
+        const int k = y0 + 4 * ty + b;
+        if (k >= Mp) continue;
+        float v = 0.0f;
+        if (j < N && k < M)
+          v = (float)(acc[a][b] - A[(int64_t)(64 + M + j) * na.dld + 64 + k]);
+        out[j * Mp + k] = v;
+      }
+    }
+  }
+}
+
 // ext = V - Z^T Z on one 64 x 64 tile of one merge (V: the children's
 // external-external entries).
 __global__ __launch_bounds__(256) void k_nd_schur(NdArgs na) {
@@ -1267,14 +1432,51 @@ static void launch_cut(const NdArgs& na, dim3 grid, int c, int ncol, bool fused,
   // items, one per thread: at least 256 threads then
   const dim3 blk((unsigned)std::max((ncol + 63) / 64 * 64, (FINAL || fused) ? 256 : 64));
   if constexpr (FINAL) {
-    if (c == 16) hipLaunchKernelGGL((k_nd_cut<16, true>), grid, blk, 0, s, na);
-    else if (c == 32) hipLaunchKernelGGL((k_nd_cut<32, true>), grid, blk, 0, s, na);
-    else hipLaunchKernelGGL((k_nd_cut<64, true>), grid, blk, 0, s, na);
+    if (c == 16) hipLaunchKernelGGL((k_nd_cut<16, 1>), grid, blk, 0, s, na);
+    else if (c == 32) hipLaunchKernelGGL((k_nd_cut<32, 1>), grid, blk, 0, s, na);
+    else hipLaunchKernelGGL((k_nd_cut<64, 1>), grid, blk, 0, s, na);
   } else {
-    if (c == 8) hipLaunchKernelGGL((k_nd_cut<8, false>), grid, blk, 0, s, na);
-    else if (c == 16) hipLaunchKernelGGL((k_nd_cut<16, false>), grid, blk, 0, s, na);
-    else if (c == 32) hipLaunchKernelGGL((k_nd_cut<32, false>), grid, blk, 0, s, na);
-    else hipLaunchKernelGGL((k_nd_cut<64, false>), grid, blk, 0, s, na);
+    if (c == 8) hipLaunchKernelGGL((k_nd_cut<8, 0>), grid, blk, 0, s, na);
+    else if (c == 16) hipLaunchKernelGGL((k_nd_cut<16, 0>), grid, blk, 0, s, na);
+    else if (c == 32) hipLaunchKernelGGL((k_nd_cut<32, 0>), grid, blk, 0, s, na);
+    else hipLaunchKernelGGL((k_nd_cut<64, 0>), grid, blk, 0, s, na);
+  }
+}
+
+// Staged elimination of a dense combined matrix of side n0 whose first c
+// rows are the pivots (c / 64 stages, an even count): the matrix is built in
+// `a`, the stages alternate between `a` and `b`, and the last stage writes
+// the merged block to `a` with row stride ldo (FINAL: G' instead).  Both
+// buffers hold in_stride (= out_stride) doubles per array.
+template <bool FINAL>
+static void launch_staged(NdArgs na, int64_t n, int c, int n0, double* a, double* b, int ldo,
+                          hipStream_t s) {
+  constexpr int PANEL = 448;   // external columns per cut workgroup (with 64 pivots: 512 lanes)
+  na.dB = a;
+  na.dn = n0;
+  na.dldo = n0;
+  hipLaunchKernelGGL((k_nd_dense0<FINAL>), dim3((unsigned)(n * ((n0 + 15) / 16))), dim3(256), 0,
+                     s, na);
+  const int stages = c / 64;
+  for (int st = 0; st < stages; ++st) {
+    const bool last = st == stages - 1;
+    na.dA = (st & 1) ? b : a;
+    na.dB = (st & 1) ? a : b;
+    na.dn = n0 - 64 * st;
+    na.dld = n0;
+    na.dldo = last ? ldo : n0;
+    na.dpanel = PANEL;
+    const int ext = na.dn - 64;
+    const unsigned npan = (unsigned)((ext + PANEL - 1) / PANEL);
+    const unsigned nthr = (unsigned)((64 + std::min(PANEL, ext) + 63) / 64 * 64);
+    hipLaunchKernelGGL((k_nd_cut<64, 2>), dim3((unsigned)n * npan), dim3(nthr), 0, s, na);
+    if (FINAL && last) {
+      const unsigned nt = (unsigned)(((na.ms.Np + 63) / 64) * ((na.ms.Mp + 63) / 64));
+      hipLaunchKernelGGL(k_nd_dschur<1>, dim3((unsigned)n * nt), dim3(256), 0, s, na);
+    } else {
+      const unsigned nt = (unsigned)((ext + 63) / 64);
+      hipLaunchKernelGGL(k_nd_dschur<0>, dim3((unsigned)n * nt * nt), dim3(256), 0, s, na);
+    }
   }
 }
 
@@ -1352,6 +1554,11 @@ hipError_t launch_nd_build(const MapScalars& ms, const float* W, float* gpt, int
         const int nt = (emax + 63) / 64;
         hipLaunchKernelGGL(k_nd_schur, dim3((unsigned)(n * nmerge * nt * nt)), dim3(256), 0, s,
                            na);
+      } else if (nmerge == 1 && c % 128 == 0 && (int64_t)(c + e_layout) * (c + e_layout) <= si &&
+                 c + e_layout <= MAXSLOT2) {
+        // the combined matrix in nxt, the stages in nxt / cur (the children
+        // are dead once it is built), the merged block back in nxt
+        launch_staged<false>(na, n, c, c + e_layout, nxt, cur, 2 * (nh + nw), s);
       } else {
         hipLaunchKernelGGL(k_nd_merge, grid, dim3(NTH),
                            (unsigned)((KB * KB + 2 * KB * 64) * sizeof(double)), s, na);
@@ -1375,9 +1582,13 @@ hipError_t launch_nd_build(const MapScalars& ms, const float* W, float* gpt, int
       hipLaunchKernelGGL((k_nd_cut2<true>), dim3((unsigned)n), dim3(2 * CP2), 0, s, na);
       const unsigned nt = (unsigned)(((ms.Np + 63) / 64) * ((ms.Mp + 63) / 64));
       hipLaunchKernelGGL(k_nd_gprod, dim3((unsigned)n * nt), dim3(256), 0, s, na);
-    } else
+    } else if (na.T % 128 == 0 && (int64_t)(2 * na.T + ms.M) * (2 * na.T + ms.M) <= si) {
+      // the combined matrix in the free buffer, the stages in it and cur
+      launch_staged<true>(na, n, na.T, 2 * na.T + ms.M, nxt, cur, 0, s);
+    } else {
       hipLaunchKernelGGL(k_nd_final, dim3((unsigned)n), dim3(NTH),
                          (unsigned)((KB * KB + 2 * KB * 64) * sizeof(double)), s, na);
+    }
   }
   return hipGetLastError();
 }
