@@ -25,6 +25,14 @@ Step 2 (W -> G), for a linear device between ``g_min`` and ``g_max``:
   crossbar with its own ADCs; the arrays are combined digitally with weight
   ``(+1 | -1) * 2^(s_b s)``.
 
+Device characteristic and variation (optional, ``oracle/variation.py``): with a
+table ``g_lut`` the normalised conductance of a level u is ``f(u)`` instead of
+u, the level being ``min(max(+-w, 0) / w_max, 1)`` (continuous) or
+``d_s / (2^s_b - 1)`` (a slice digit): ``G = g_min + (g_max - g_min) f(u)``.
+Every conductance is then multiplied by its device's variation factor: the
+caller's ``variation`` array ([C, R, A, M, N]) or, for ``variation_sigma > 0``,
+the factors drawn from ``variation_seed``.
+
 Step 3 (G -> G'): ``network.gprime_nodal`` per array, or for arrays above
 32 x 32 with positive wire and sense resistances ``network.gprime_rowsweep``
 (the same equations, eliminated row by row; the two agree to ~1e-12).
@@ -41,9 +49,11 @@ import math
 import numpy as np
 
 from .network import gprime_nodal, gprime_rowsweep
+from .variation import characteristic, device_indices, generated_factors
 
 PARAM_KEYS = ("rows", "cols", "g_min", "g_max", "r_driver", "r_sense", "r_row",
-              "r_col", "weight_bits", "bits_per_slice", "w_max")
+              "r_col", "weight_bits", "bits_per_slice", "w_max", "variation",
+              "variation_sigma", "variation_seed", "g_lut")
 
 
 def tile_grid(P, Q, M, N):
@@ -102,28 +112,53 @@ def tile_weights(W, params, r, c):
     return frag
 
 
-def array_conductances(frag, params, w_max):
-    """Step 2 for one tile fragment: conductances of every array, [A, M, N] fp64."""
+def array_conductances(frag, params, w_max, vf=None):
+    """Step 2 for one tile fragment: conductances of every array, [A, M, N]
+    fp64; ``vf`` ([A, M, N]) the devices' variation factors, or None."""
     g_min, g_max = float(params["g_min"]), float(params["g_max"])
+    lut = params.get("g_lut")
     w = frag.astype(np.float64)
     ns, sb = slicing(params)
     A = 2 * ns
     out = np.empty((A,) + frag.shape, dtype=np.float64)
     if sb == 0:
-        s_w = (g_max - g_min) / w_max
-        out[0] = g_min + s_w * np.maximum(w, 0.0)
-        out[1] = g_min + s_w * np.maximum(-w, 0.0)
-        return out
-    wb = int(params["weight_bits"])
-    qmax = (1 << wb) - 1
-    q = np.minimum(float(qmax), np.rint(np.abs(w) * (qmax / w_max))).astype(np.int64)
-    dG = (g_max - g_min) / ((1 << sb) - 1)
-    for s in range(ns):
-        d = (q >> (sb * s)) & ((1 << sb) - 1)
-        on = g_min + d.astype(np.float64) * dG
-        out[2 * s] = np.where(w > 0, on, g_min)
-        out[2 * s + 1] = np.where(w < 0, on, g_min)
+        if lut is None:
+            s_w = (g_max - g_min) / w_max
+            out[0] = g_min + s_w * np.maximum(w, 0.0)
+            out[1] = g_min + s_w * np.maximum(-w, 0.0)
+        else:
+            for side, mag in ((0, np.maximum(w, 0.0)), (1, np.maximum(-w, 0.0))):
+                u = np.minimum(mag / w_max, 1.0)
+                out[side] = g_min + (g_max - g_min) * characteristic(u, lut)
+    else:
+        wb = int(params["weight_bits"])
+        qmax = (1 << wb) - 1
+        q = np.minimum(float(qmax), np.rint(np.abs(w) * (qmax / w_max))).astype(np.int64)
+        levels = (1 << sb) - 1
+        dG = (g_max - g_min) / levels
+        for s in range(ns):
+            d = (q >> (sb * s)) & levels
+            if lut is None:
+                on = g_min + d.astype(np.float64) * dG
+            else:
+                on = g_min + (g_max - g_min) * characteristic(d / levels, lut)
+            out[2 * s] = np.where(w > 0, on, g_min)
+            out[2 * s + 1] = np.where(w < 0, on, g_min)
+    if vf is not None:
+        out = out * np.asarray(vf, dtype=np.float64)
     return out
+
+
+def variation_factors(params, r, c, R, A, M, N):
+    """[A, M, N] variation factors of tile (r, c), or None."""
+    var = params.get("variation")
+    if var is not None:
+        return np.asarray(var, dtype=np.float64)[c, r]
+    sigma = float(params.get("variation_sigma", 0.0) or 0.0)
+    if sigma > 0.0:
+        d = device_indices((c * R + r) * A, A, M, N)
+        return generated_factors(d, int(params.get("variation_seed", 0)), sigma)
+    return None
 
 
 def array_gprime(G, params):
@@ -150,9 +185,11 @@ def map_layer(W, params, col_tiles=None, row_tiles=None):
     cols = range(C) if col_tiles is None else col_tiles
     rows = range(R) if row_tiles is None else row_tiles
     gp = {}
+    A = arrays_per_position(params)
     for c in cols:
         for r in rows:
-            G = array_conductances(tile_weights(W, params, r, c), params, w_max)
+            vf = variation_factors(params, r, c, R, A, M, N)
+            G = array_conductances(tile_weights(W, params, r, c), params, w_max, vf)
             gp[(r, c)] = np.stack([array_gprime(G[a], params) for a in range(G.shape[0])])
     return {"gp": gp, "P": P, "Q": Q, "M": M, "N": N, "R": R, "C": C,
             "A": arrays_per_position(params), "w_max": w_max,
