@@ -73,7 +73,24 @@ typedef struct rxnn_layer rxnn_layer;
  *                  each on its own differential pair (shift-and-add).
  * w_max            |w| that maps to g_max; <= 0 means max|W| of the layer,
  *                  computed on the device at mapping time.
- * variation        reserved for per-device variation factors; must be NULL.
+ * variation        device, fp32, one variation factor per device in the
+ *                  layout [C][R][A][M][N] (tile column, tile row, array,
+ *                  device row, device column; padded positions included), or
+ *                  NULL.  Copied on `stream` at mapping time and kept by the
+ *                  layer (a remap reuses it): every device's conductance is
+ *                  multiplied by its factor (Sec. V-A generator step 2).
+ * variation_sigma  with variation NULL: > 0 draws each device's factor as
+ *                  max(0, 1 + variation_sigma z), z standard normal from
+ *                  Philox-4x64-10 (counter (d, 0, 0, 0), key (variation_seed,
+ *                  0), d = ((c R + r) A + a) M N + i N + j) and Box-Muller on
+ *                  its first two words: u1 = ((x0 >> 11) + 1) 2^-53,
+ *                  u2 = (x1 >> 11) 2^-53, z = sqrt(-2 ln u1) cos(2 pi u2).
+ *                  0: no variation.  Sec. IV-B studies sigma / mu = 0.1.
+ * variation_seed   key of the generated factors.
+ * g_lut, g_lut_n   host, the device characteristic: g_lut_n (2..4096) samples
+ *                  in [0, 1] of the normalised conductance (G - g_min) /
+ *                  (g_max - g_min) at levels k / (g_lut_n - 1), linear in
+ *                  between (copied).  NULL (g_lut_n 0): the linear device.
  *
  * Mapping of one weight w (fp64):
  *   continuous: G+ = g_min + s_w max(w,0), G- = g_min + s_w max(-w,0),
@@ -82,6 +99,10 @@ typedef struct rxnn_layer rxnn_layer;
  *               slice s digit d_s = (q >> (b_s s)) & (2^b_s - 1); the side of
  *               sign(w) gets g_min + d_s dG, the other side g_min,
  *               dG = (g_max - g_min) / (2^b_s - 1).
+ *   with g_lut: the level u = min(max(+-w, 0) / w_max, 1) (continuous) or
+ *               d_s / (2^b_s - 1) (quantised) gives G = g_min + (g_max -
+ *               g_min) f(u); the output scale keeps the linear device's s_w'.
+ *   then every G is multiplied by its device's variation factor.
  * Arrays at one tile position are ordered a = 2 s + side (side 0 = positive,
  * slice 0 least significant); array a carries the digital weight
  * (side ? -1 : +1) * 2^(b_s s).  Zero-padded positions hold weight 0, i.e.
@@ -95,6 +116,10 @@ typedef struct {
   int32_t bits_per_slice;
   double w_max;
   const float* variation;
+  double variation_sigma;
+  uint64_t variation_seed;
+  const double* g_lut;
+  int32_t g_lut_n;
 } rxnn_xbar_params;
 
 /*

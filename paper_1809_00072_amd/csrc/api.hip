@@ -72,6 +72,7 @@ bool nd_ok(const rxnn_xbar_params* p) {
 }
 
 constexpr size_t kNdBudget = (size_t)1 << 30;  // bytes of build workspace per layer
+constexpr int kMaxLut = 4096;                  // samples of a device characteristic table
 
 rxnn_status check_xbar(const rxnn_xbar_params* p) {
   if (!p) return fail(RXNN_EINVAL, "params is NULL");
@@ -95,8 +96,19 @@ rxnn_status check_xbar(const rxnn_xbar_params* p) {
                 p->weight_bits, p->bits_per_slice);
   if (!isfinite(p->w_max)) return fail(RXNN_EINVAL, "w_max must be finite");
   if (p->w_max > 3.0e38) return fail(RXNN_EINVAL, "w_max exceeds the fp32 range");
-  if (p->variation)
-    return fail(RXNN_EUNSUPPORTED, "per-device variation is not supported by this build");
+  if (!(isfinite(p->variation_sigma) && p->variation_sigma >= 0.0))
+    return fail(RXNN_EINVAL, "variation_sigma must be finite and >= 0");
+  if (p->variation && p->variation_sigma > 0.0)
+    return fail(RXNN_EINVAL, "give either variation factors or variation_sigma, not both");
+  if (p->g_lut) {
+    if (p->g_lut_n < 2 || p->g_lut_n > kMaxLut)
+      return fail(RXNN_EINVAL, "g_lut_n %d not in 2..%d", p->g_lut_n, kMaxLut);
+    for (int k = 0; k < p->g_lut_n; ++k)
+      if (!(isfinite(p->g_lut[k]) && p->g_lut[k] >= 0.0 && p->g_lut[k] <= 1.0))
+        return fail(RXNN_EINVAL, "g_lut[%d] = %g is not in [0, 1]", k, p->g_lut[k]);
+  } else if (p->g_lut_n != 0) {
+    return fail(RXNN_EINVAL, "g_lut_n must be 0 without g_lut");
+  }
   if (!nd_ok(p) && (p->rows > kMaxSweep || p->cols > kMaxSweep))
     return fail(RXNN_EUNSUPPORTED,
                 "crossbars above %dx%d need positive wire, driver and sense resistances",
@@ -156,6 +168,15 @@ struct Pending {
 int g_prof = 0;   // 0 off, 1 every kernel, 2 the evaluation kernel only
 std::vector<Pending> g_pending;
 std::map<std::string, std::pair<double, int64_t>> g_prof_tot;
+
+// Frees every device buffer of a layer and the handle itself.
+void release_buffers(rxnn_layer* L) {
+  void* bufs[] = {L->gpt, L->d_wmax, L->ws, L->nd_ws, L->ktab, L->vbuf, L->d_vf, L->d_lut};
+  for (void* b : bufs)
+    if (b) (void)hipFree(b);
+  L->magic = 0;
+  delete L;
+}
 
 rxnn_status grow_ws(rxnn_layer* L, size_t bytes) {
   if (L->ws_bytes >= bytes) return RXNN_OK;
@@ -403,16 +424,50 @@ rxnn_status rxnn_map_layer(const rxnn_xbar_params* params, const float* W, int64
   memset(L, 0, sizeof *L);
   L->device = dev;
   L->params = *params;
+  L->params.variation = nullptr;   // the layer keeps its own copies
+  L->params.g_lut = nullptr;
   if (hipMalloc((void**)&L->gpt, gbytes) != hipSuccess) {
     (void)hipGetLastError();
-    delete L;
+    release_buffers(L);
     return fail(RXNN_ENOMEM, "cannot allocate %zu bytes for G'", gbytes);
   }
   if (hipMalloc((void**)&L->d_wmax, 256) != hipSuccess) {
     (void)hipGetLastError();
-    (void)hipFree(L->gpt);
-    delete L;
+    release_buffers(L);
     return fail(RXNN_ENOMEM, "cannot allocate w_max");
+  }
+  if (params->variation) {
+    // one factor per device: [C][R][A][M][N]
+    const size_t vbytes = (size_t)ms.C * ms.R * ms.A * ms.M * ms.N * sizeof(float);
+    if (hipMalloc((void**)&L->d_vf, vbytes) != hipSuccess) {
+      (void)hipGetLastError();
+      release_buffers(L);
+      return fail(RXNN_ENOMEM, "cannot allocate %zu bytes of variation factors", vbytes);
+    }
+    if (hipMemcpyAsync(L->d_vf, params->variation, vbytes, hipMemcpyDeviceToDevice,
+                       (hipStream_t)stream) != hipSuccess) {
+      (void)hipGetLastError();
+      release_buffers(L);
+      return fail(RXNN_EHIP, "cannot copy the variation factors");
+    }
+    ms.vf = L->d_vf;
+  }
+  ms.vf_sigma = params->variation_sigma;
+  ms.vf_seed = params->variation_seed;
+  if (params->g_lut) {
+    const size_t lbytes = (size_t)params->g_lut_n * sizeof(double);
+    if (hipMalloc((void**)&L->d_lut, lbytes) != hipSuccess) {
+      (void)hipGetLastError();
+      release_buffers(L);
+      return fail(RXNN_ENOMEM, "cannot allocate the characteristic table");
+    }
+    if (hipMemcpy(L->d_lut, params->g_lut, lbytes, hipMemcpyHostToDevice) != hipSuccess) {
+      (void)hipGetLastError();
+      release_buffers(L);
+      return fail(RXNN_EHIP, "cannot copy the characteristic table");
+    }
+    ms.lut = L->d_lut;
+    ms.lut_n = params->g_lut_n;
   }
   if (nd_ok(params)) {
     int64_t si, so, sc;
@@ -426,9 +481,7 @@ rxnn_status rxnn_map_layer(const rxnn_xbar_params* params, const float* W, int64
     if (chunk > n_arrays) chunk = n_arrays;
     if (hipMalloc((void**)&L->nd_ws, per * chunk) != hipSuccess) {
       (void)hipGetLastError();
-      (void)hipFree(L->gpt);
-      (void)hipFree(L->d_wmax);
-      delete L;
+      release_buffers(L);
       return fail(RXNN_ENOMEM, "cannot allocate %zu bytes of build workspace", per * chunk);
     }
     L->nd_chunk = chunk;
@@ -438,10 +491,7 @@ rxnn_status rxnn_map_layer(const rxnn_xbar_params* params, const float* W, int64
   L->magic = kLayerMagic;
   hipError_t e = build_gprime(L, W, (hipStream_t)stream);
   if (e != hipSuccess) {
-    (void)hipFree(L->gpt);
-    (void)hipFree(L->d_wmax);
-    if (L->nd_ws) (void)hipFree(L->nd_ws);
-    delete L;
+    release_buffers(L);
     return fail(RXNN_EHIP, "mapping launch failed: %s", hipGetErrorString(e));
   }
   {
@@ -612,14 +662,7 @@ void rxnn_free_layer(rxnn_layer* layer) {
   }
   DeviceGuard dg(layer->device);
   (void)hipDeviceSynchronize();
-  (void)hipFree(layer->gpt);
-  (void)hipFree(layer->d_wmax);
-  if (layer->ws) (void)hipFree(layer->ws);
-  if (layer->nd_ws) (void)hipFree(layer->nd_ws);
-  if (layer->ktab) (void)hipFree(layer->ktab);
-  if (layer->vbuf) (void)hipFree(layer->vbuf);
-  layer->magic = 0;
-  delete layer;
+  release_buffers(layer);
 }
 
 rxnn_status rxnn_profile_enable(int32_t on) {

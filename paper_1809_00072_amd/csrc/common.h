@@ -25,6 +25,11 @@ struct MapScalars {
   float wmax_fixed;
   const float* d_wmax;
   double sw_num;               // s_w' = sw_num / w_max (siemens per unit weight)
+  const float* vf;             // per-device variation factors [C][R][A][M][N] (or null)
+  double vf_sigma;             // > 0 (vf null): generated factors N(1, vf_sigma^2)
+  uint64_t vf_seed;
+  const double* lut;           // device characteristic samples (or null: linear)
+  int lut_n;
 };
 
 // Peripheral constants prepared on the host from rxnn_periph_params; the
@@ -63,6 +68,8 @@ struct rxnn_layer {
   int ktab_key[6];     // c_in, h, w, kh, kw, pad the table was built for
   float* vbuf;         // DAC output of the current call (padded for a convolution)
   size_t vbuf_bytes;
+  float* d_vf;         // the layer's copy of the variation factors (or null)
+  double* d_lut;       // the layer's copy of the characteristic table (or null)
 };
 
 namespace rxnn {

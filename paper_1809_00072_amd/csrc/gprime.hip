@@ -32,6 +32,7 @@
 // suffices.  One workgroup builds one array; arrays are independent.
 
 #include "common.h"
+#include "device_map.h"
 
 namespace rxnn {
 namespace {
@@ -41,25 +42,7 @@ constexpr int TG = 16;  // thread grid side
 __device__ __forceinline__ double device_conductance(const MapScalars& ms, const float* W,
                                                      double wmax, int r, int c, int a,
                                                      int i, int j) {
-  // Tiling with zero padding (generator step 1) and W -> G (step 2).
-  const int64_t p = (int64_t)r * ms.M + i, q = (int64_t)c * ms.N + j;
-  const float wf = (p < ms.P && q < ms.Q) ? W[p * ms.Q + q] : 0.0f;
-  const double w = (double)wf;
-  const int side = a & 1, s = a >> 1;
-  if (ms.slice_bits == 0) {
-    if (!(wmax > 0.0)) return ms.g_min;
-    const double s_w = (ms.g_max - ms.g_min) / wmax;
-    const double mag = side ? fmax(-w, 0.0) : fmax(w, 0.0);
-    return ms.g_min + s_w * mag;
-  }
-  const double lw = (double)((1 << ms.weight_bits) - 1);
-  double qv = 0.0;
-  if (wmax > 0.0) qv = fmin(lw, rint(fabs(w) * (lw / wmax)));
-  const int64_t qi = (int64_t)qv;
-  const int64_t d = (qi >> (ms.slice_bits * s)) & ((1 << ms.slice_bits) - 1);
-  const double dG = (ms.g_max - ms.g_min) / (double)((1 << ms.slice_bits) - 1);
-  const bool on = side ? (wf < 0.0f) : (wf > 0.0f);
-  return on ? ms.g_min + (double)d * dG : ms.g_min;
+  return device_g(ms, W, wmax, ((int64_t)c * ms.R + r) * ms.A + a, i, j);
 }
 
 // Gauss-Jordan solve A Y = B in place on X = [A | B], A PS x PS SPD,

@@ -42,6 +42,7 @@
 #include <algorithm>
 
 #include "common.h"
+#include "device_map.h"
 
 namespace rxnn {
 
@@ -153,27 +154,7 @@ __device__ __forceinline__ double cell_conductance(const MapScalars& ms, const f
                                                    int row_off) {
   const int i = gi - row_off, j = gj;
   if (i < 0 || j >= ms.N) return 0.0;
-  const int a = (int)(arr % ms.A);
-  const int64_t rc = arr / ms.A;
-  const int r = (int)(rc % ms.R), c = (int)(rc / ms.R);
-  const int64_t p = (int64_t)r * ms.M + i, q = (int64_t)c * ms.N + j;
-  const float wf = (p < ms.P && q < ms.Q) ? W[p * ms.Q + q] : 0.0f;
-  const double wv = (double)wf;
-  const int side = a & 1, s = a >> 1;
-  if (ms.slice_bits == 0) {
-    if (!(wmax > 0.0)) return ms.g_min;
-    const double s_w = (ms.g_max - ms.g_min) / wmax;
-    const double mag = side ? fmax(-wv, 0.0) : fmax(wv, 0.0);
-    return ms.g_min + s_w * mag;
-  }
-  const double lw = (double)((1 << ms.weight_bits) - 1);
-  double qv = 0.0;
-  if (wmax > 0.0) qv = fmin(lw, rint(fabs(wv) * (lw / wmax)));
-  const int64_t qi = (int64_t)qv;
-  const int64_t d = (qi >> (ms.slice_bits * s)) & ((1 << ms.slice_bits) - 1);
-  const double dG = (ms.g_max - ms.g_min) / (double)((1 << ms.slice_bits) - 1);
-  const bool on = side ? (wf < 0.0f) : (wf > 0.0f);
-  return on ? ms.g_min + (double)d * dG : ms.g_min;
+  return device_g(ms, W, wmax, arr, i, j);
 }
 
 // ---------------------------------------------------------------------------

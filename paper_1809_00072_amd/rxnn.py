@@ -34,6 +34,10 @@ class XbarParams(ctypes.Structure):
         ("weight_bits", ctypes.c_int32), ("bits_per_slice", ctypes.c_int32),
         ("w_max", ctypes.c_double),
         ("variation", ctypes.c_void_p),
+        ("variation_sigma", ctypes.c_double),
+        ("variation_seed", ctypes.c_uint64),
+        ("g_lut", ctypes.c_void_p),
+        ("g_lut_n", ctypes.c_int32),
     ]
 
 
@@ -121,11 +125,18 @@ def _ptr(t, dtype=None, what="tensor"):
     return ctypes.c_void_p(t.data_ptr())
 
 
-def xbar_params(d) -> XbarParams:
+def xbar_params(d, variation=None, lut=None) -> XbarParams:
+    """The C struct of a parameter dict.  ``variation``: device address of the
+    factor array (or None); ``lut``: a ctypes double array the caller keeps
+    alive during the call (or None)."""
     return XbarParams(int(d["rows"]), int(d["cols"]), float(d["g_min"]), float(d["g_max"]),
                       float(d["r_driver"]), float(d["r_sense"]), float(d["r_row"]),
                       float(d["r_col"]), int(d.get("weight_bits", 0)),
-                      int(d.get("bits_per_slice", 0)), float(d.get("w_max", 0.0)), None)
+                      int(d.get("bits_per_slice", 0)), float(d.get("w_max", 0.0)), variation,
+                      float(d.get("variation_sigma", 0.0) or 0.0),
+                      int(d.get("variation_seed", 0) or 0),
+                      ctypes.cast(lut, ctypes.c_void_p) if lut is not None else None,
+                      len(lut) if lut is not None else 0)
 
 
 def periph_params(d) -> PeriphParams:
@@ -183,7 +194,20 @@ def map_layer(W, params, stream=None) -> Layer:
         raise ValueError("W must be 2-D (P x Q)")
     P, Q = W.shape
     h = ctypes.c_void_p()
-    p = xbar_params(params)
+    var = params.get("variation")
+    vptr = None
+    if var is not None:
+        # one factor per device, [C][R][A][M][N], on W's device
+        if not (isinstance(var, torch.Tensor) and var.dtype == torch.float32 and var.is_contiguous()
+                and var.device == W.device):
+            raise ValueError("variation must be a contiguous fp32 tensor on W's device")
+        vptr = var.data_ptr()
+    lut = params.get("g_lut")
+    lut_arr = None
+    if lut is not None:
+        vals = [float(v) for v in lut]
+        lut_arr = (ctypes.c_double * len(vals))(*vals)
+    p = xbar_params(params, vptr, lut_arr)
     _check(lib.rxnn_map_layer(ctypes.byref(p), _ptr(W, torch.float32, "W"), P, Q,
                               _stream(stream), ctypes.byref(h)))
     info = (ctypes.c_int64 * 7)()

@@ -84,12 +84,36 @@ def test_map_rejects_null_and_sizes(lib):
     assert lib.rxnn_map_layer(ctypes.byref(p), FAKE, 10, 10, None, None) == rxnn.RXNN_EINVAL
 
 
-def test_variation_is_reserved(lib):
+@pytest.mark.parametrize("setup,msg", [
+    (lambda p: (setattr(p, "variation", 0x2000), setattr(p, "variation_sigma", 0.1)), "not both"),
+    (lambda p: setattr(p, "variation_sigma", -0.1), "variation_sigma"),
+    (lambda p: setattr(p, "variation_sigma", float("nan")), "variation_sigma"),
+    (lambda p: setattr(p, "g_lut_n", 3), "without g_lut"),
+])
+def test_map_rejects_bad_variation(lib, setup, msg):
     p = good_params()
-    p.variation = ctypes.c_void_p(0x2000)
+    setup(p)
     h = ctypes.c_void_p()
     assert lib.rxnn_map_layer(ctypes.byref(p), FAKE, 10, 10, None, ctypes.byref(h)) == \
-        rxnn.RXNN_EUNSUPPORTED
+        rxnn.RXNN_EINVAL
+    assert msg in lib.rxnn_last_error().decode()
+
+
+@pytest.mark.parametrize("vals,msg", [
+    ([0.5], "g_lut_n"),
+    ([0.0, 1.5], "not in [0, 1]"),
+    ([0.0, float("nan"), 1.0], "not in [0, 1]"),
+    ([-0.1, 1.0], "not in [0, 1]"),
+])
+def test_map_rejects_bad_characteristic(lib, vals, msg):
+    arr = (ctypes.c_double * len(vals))(*vals)
+    p = good_params()
+    p.g_lut = ctypes.cast(arr, ctypes.c_void_p)
+    p.g_lut_n = len(vals)
+    h = ctypes.c_void_p()
+    assert lib.rxnn_map_layer(ctypes.byref(p), FAKE, 10, 10, None, ctypes.byref(h)) == \
+        rxnn.RXNN_EINVAL
+    assert msg in lib.rxnn_last_error().decode()
 
 
 def test_calls_reject_unknown_handles(lib):

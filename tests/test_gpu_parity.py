@@ -120,6 +120,103 @@ def test_gprime_parity(P, Q, M, N, wire, wb, sb):
     say("gprime worst rel err %.3g" % worst)
 
 
+# ---------------------------------------------------------------------------
+# Device variation and characteristic table (generator step 2)
+# ---------------------------------------------------------------------------
+
+LUT_SQRTISH = [(k / 16.0) ** 0.6 for k in range(17)]   # a saturating device
+
+
+@pytest.mark.parametrize("mode,P,Q,M,N,wire,wb,sb", [
+    ("supplied", 70, 50, 32, 16, 2.5, 0, 0),
+    ("generated", 70, 50, 32, 16, 2.5, 0, 0),
+    ("generated", 40, 20, 16, 16, 1.0, 8, 2),     # sliced: every device its own factor
+    ("lut", 70, 50, 32, 16, 2.5, 0, 0),
+    ("lut", 40, 20, 16, 16, 1.0, 8, 2),
+    ("lut+generated", 100, 90, 64, 64, 2.5, 4, 0),
+    ("supplied", 40, 30, 16, 16, 0.0, 0, 0),      # zero wire resistance: the row sweep
+    ("generated", 40, 30, 16, 16, 0.0, 8, 4),
+    ("generated", 140, 130, 128, 128, 2.5, 0, 0),  # 128 x 128: the register build
+])
+def test_gprime_variation_parity(mode, P, Q, M, N, wire, wb, sb):
+    say("gprime variation", mode, P, Q, M, N, wire, wb, sb)
+    rng = np.random.default_rng(P * 11 + Q + wb)
+    W = rng.normal(0, 0.05, size=(P, Q)).astype(np.float32)
+    xb = wl.xbar(M, N, wire, weight_bits=wb, bits_per_slice=sb)
+    xo, xg = dict(xb), dict(xb)
+    R, C = -(-P // M), -(-Q // N)
+    A = 2 * (wb // (sb or wb) if wb else 1)
+    if "supplied" in mode:
+        vf = rng.uniform(0.7, 1.3, size=(C, R, A, M, N)).astype(np.float32)
+        xo["variation"] = vf
+        xg["variation"] = dev(vf)
+    if "generated" in mode:
+        for d in (xo, xg):
+            d["variation_sigma"] = 0.1
+            d["variation_seed"] = 20240611
+    if "lut" in mode:
+        xo["g_lut"] = xg["g_lut"] = LUT_SQRTISH
+    L = rxnn.map_layer(dev(W), xg)
+    cols = None if C <= 3 else [0, C - 1]
+    lay = omap.map_layer(W, xo, col_tiles=cols)
+    base = omap.map_layer(W, xb, col_tiles=cols)
+    worst = 0.0
+    for (r, c), g in lay["gp"].items():
+        assert not np.allclose(g, base["gp"][(r, c)], rtol=1e-3)   # the option changes G'
+        for a in range(lay["A"]):
+            worst = max(worst, check_gprime(L.gprime(r, c, a), g[a]))
+    say("gprime variation worst rel err %.3g" % worst)
+    L.free()
+
+
+def test_variation_unit_factors_reproduce_base():
+    """Unit factors (supplied) and sigma 0 give the unvaried G' bit for bit."""
+    rng = np.random.default_rng(9)
+    W = rng.normal(0, 0.05, size=(70, 50)).astype(np.float32)
+    xb = wl.xbar(32, 16, 2.5)
+    say("variation unit factors")
+    L0 = rxnn.map_layer(dev(W), xb)
+    ones = torch.ones((4, 3, 2, 32, 16), dtype=torch.float32, device="cuda")
+    L1 = rxnn.map_layer(dev(W), dict(xb, variation=ones))
+    L2 = rxnn.map_layer(dev(W), dict(xb, variation_sigma=0.0, variation_seed=5))
+    for r in range(3):
+        for c in range(4):
+            for a in range(2):
+                g0 = L0.gprime(r, c, a)
+                np.testing.assert_array_equal(L1.gprime(r, c, a), g0)
+                np.testing.assert_array_equal(L2.gprime(r, c, a), g0)
+    for L in (L0, L1, L2):
+        L.free()
+
+
+def test_fc_with_variation_and_lut():
+    """The evaluation path on a varied, non-linear layer: currents, codes and
+    outputs against the oracle under the parity rules."""
+    W, X, xb, pp = fc_case(130, 70, 32, 32, 24, dac=6, adc=8, seed=21)
+    xb = dict(xb, variation_sigma=0.1, variation_seed=77, g_lut=LUT_SQRTISH)
+    compare_fc_debug(W, X, xb, pp, "fc varied+lut")
+
+
+def test_remap_keeps_variation():
+    """A remap rebuilds G' with the layer's own factors (supplied ones were
+    copied at mapping time)."""
+    rng = np.random.default_rng(12)
+    W = rng.normal(0, 0.05, size=(40, 30)).astype(np.float32)
+    W1 = rng.normal(0, 0.05, size=(40, 30)).astype(np.float32)
+    xb = wl.xbar(16, 16, 2.5)
+    vf = rng.uniform(0.8, 1.2, size=(2, 3, 2, 16, 16)).astype(np.float32)
+    say("remap with variation")
+    vt = dev(vf)
+    L = rxnn.map_layer(dev(W), dict(xb, variation=vt))
+    vt.fill_(0.0)   # the caller's array is no longer read after mapping
+    rxnn.remap_layer(L, dev(W1))
+    lay = omap.map_layer(W1, dict(xb, variation=vf))
+    for (r, c), g in lay["gp"].items():
+        for a in range(2):
+            check_gprime(L.gprime(r, c, a), g[a])
+    L.free()
+
+
 @pytest.mark.parametrize("P,Q,M,N,wire,arrays", [
     (128, 128, 128, 128, 1.0, 2),      # 128 x 128 crossbars
     (100, 200, 100, 200, 2.5, 1),      # rectangular, embedded in a 256 grid
