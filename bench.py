@@ -112,6 +112,31 @@ def read_kernels(rxnn, steps):
     return kern
 
 
+# A saturating device characteristic (normalised conductance at 17 levels).
+DEVICE_LUT = [(k / 16.0) ** 0.6 for k in range(17)]
+
+
+def device_options(xb, args, seed=5000):
+    """Per-device variation (generated, sigma = --variation) and the
+    non-linear characteristic (--lut) on a crossbar parameter dict."""
+    xb = dict(xb)
+    if args.variation > 0.0:
+        xb["variation_sigma"] = args.variation
+        xb["variation_seed"] = seed
+    if args.lut:
+        xb["g_lut"] = DEVICE_LUT
+    return xb
+
+
+def device_note(args):
+    note = ""
+    if args.variation > 0.0:
+        note += "; per-device variation sigma %g" % args.variation
+    if args.lut:
+        note += "; non-linear device table"
+    return note
+
+
 def copy_probe(torch, dev):
     """A plain elementwise copy of known size, for scaling HBM byte counters.
     The 2 GiB source is written first and then a 1 GiB buffer, so that
@@ -181,6 +206,8 @@ def bench_stack(args):
     for l in range(n_layers):
         w = wl.stack_layer(cfg, l, crossbar=args.crossbar if rebuild else None,
                            wire=args.wire if rebuild else None)
+        if rebuild:
+            w["xbar"] = device_options(w["xbar"], args, seed=5000 + l)
         Wd = torch.from_numpy(w["W"]).to(dev)
         Xd = torch.from_numpy(w["X"]).to(dev)
         L = rxnn.map_layer(Wd, w["xbar"])
@@ -277,7 +304,8 @@ def bench_stack(args):
                        "evaluation of the three layers",
             "resnet50": "ResNet-50 shaped stack (54 layers), batch 128, %dx%d crossbars, wire "
                         "%g ohm, 8-bit DAC/ADC; step = weight update + G' rebuild + evaluation "
-                        "of every layer" % (args.crossbar, args.crossbar, args.wire)}[cfg]
+                        "of every layer" % (args.crossbar, args.crossbar, args.wire)
+                        + device_note(args)}[cfg]
     value_ms = step_ms
     out = {
         "metric": "non-ideal crossbar MACs/sec per layer",
@@ -311,6 +339,10 @@ def main():
                     choices=["conv3x3", "fc256", "resnet18", "vgg16fc", "resnet50"])
     ap.add_argument("--crossbar", type=int, default=256, help="resnet50: crossbar side")
     ap.add_argument("--wire", type=float, default=2.5, help="resnet50: wire resistance (Ohm)")
+    ap.add_argument("--variation", type=float, default=0.0,
+                    help="conv3x3 / resnet50: generated per-device variation, sigma (e.g. 0.1)")
+    ap.add_argument("--lut", action="store_true",
+                    help="conv3x3 / resnet50: a non-linear device characteristic table")
     ap.add_argument("--breakdown", action="store_true",
                     help="stacks without rebuild: also time every launch in a second pass")
     args = ap.parse_args()
@@ -331,6 +363,7 @@ def main():
     assert torch.cuda.is_available(), "bench.py needs the HIP device"
     work = wl.conv3x3_64_56()
     cv, xb, pp = work["conv"], work["xbar"], work["periph"]
+    xb = device_options(xb, args)
     dev = torch.device("cuda:0")
     Wd = torch.from_numpy(work["W"]).to(dev)
     Xd = torch.from_numpy(work["X"]).to(dev)
@@ -420,7 +453,8 @@ def main():
         "data": "synthetic",
         "config": {
             "workload": "conv3x3 s1 p1 64->64, 56x56, batch 32, 64x64 crossbars, "
-                        "6-bit DAC / 8-bit ADC, 1k/1k/2.5 ohm; step = G' rebuild + evaluation",
+                        "6-bit DAC / 8-bit ADC, 1k/1k/2.5 ohm; step = G' rebuild + evaluation"
+                        + device_note(args),
             "alg_macs_per_step": macs,
             "arrays": n_arrays,
         },
@@ -433,7 +467,7 @@ def main():
     }
     if not args.no_cpu_baseline:
         print("[bench] oracle on the host", file=sys.stderr, flush=True)
-        out["cpu_baseline"] = cpu_baseline(work)
+        out["cpu_baseline"] = cpu_baseline(dict(work, xbar=xb))
     L.free()
     print(json.dumps(out), flush=True)
 
