@@ -1273,8 +1273,57 @@ __global__ __launch_bounds__(256) void k_nd_schur(NdArgs na) {
   inverse_tables<MAXSLOT2>(na, g, invt, 256);
   const double* z = na.scratch + g.la * na.scr_stride + (int64_t)g.m * Emax * c;
   const int tx = tid >> 4, ty = tid & 15;
-  // the children's external entries of this thread's 4 x 4 outputs, loaded
-  // first so that they are in flight during the product
+  double acc[4][4];
+#pragma unroll
+  for (int a = 0; a < 4; ++a)
+#pragma unroll
+    for (int b = 0; b < 4; ++b) acc[a][b] = 0.0;
+  // Z chunk by chunk (KC rows), software pipelined: the next chunk's loads
+  // are in flight while this chunk is multiplied
+  const __amdgpu_buffer_rsrc_t rz = nd_rsrc(z, (unsigned)(c * Emax * 8));
+  const unsigned ox = 8u * (unsigned)(x0 + min(tid & 63, nrx - 1));
+  const unsigned oy = 8u * (unsigned)(y0 + min(tid & 63, nry - 1));
+  auto load_chunk = [&](int k0, double (&pa)[4], double (&pb)[4]) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int e = tid + 256 * r, xx = e & 63, kk = e >> 6;   // kk: uniform per wave
+      const int k = min(k0 + kk, c - 1);
+      const unsigned ko = (unsigned)__builtin_amdgcn_readfirstlane(k * Emax * 8);
+      const double a = nd_load(rz, ox, ko);
+      const double b = nd_load(rz, oy, ko);
+      const bool ok = k0 + kk < c;
+      pa[r] = (ok && xx < nrx) ? a : 0.0;
+      pb[r] = (ok && xx < nry) ? b : 0.0;
+    }
+  };
+  double pza[4], pzb[4];
+  load_chunk(0, pza, pzb);
+#pragma unroll 1
+  for (int k0 = 0; k0 < c; k0 += KC) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int e = tid + 256 * r, xx = e & 63, kk = e >> 6;
+      za[kk][xx] = pza[r];
+      zb[kk][xx] = pzb[r];
+    }
+    __syncthreads();
+    if (k0 + KC < c) load_chunk(k0 + KC, pza, pzb);
+#pragma unroll 2
+    for (int kk = 0; kk < KC; ++kk) {
+      double xa[4], yb[4];
+#pragma unroll
+      for (int a = 0; a < 4; ++a) xa[a] = za[kk][4 * tx + a];
+#pragma unroll
+      for (int b = 0; b < 4; ++b) yb[b] = zb[kk][4 * ty + b];
+#pragma unroll
+      for (int a = 0; a < 4; ++a)
+#pragma unroll
+        for (int b = 0; b < 4; ++b) acc[a][b] = fma(xa[a], yb[b], acc[a][b]);
+    }
+    __syncthreads();
+  }
+  // the children's external entries of this thread's 4 x 4 outputs (all
+  // loads issued together)
   const double* Y0 = na.buf_in + g.la * na.in_stride + (int64_t)g.cm0 * g.Ein * g.Ein;
   const double* Y1 = na.buf_in + g.la * na.in_stride + (int64_t)g.cm1 * g.Ein * g.Ein;
   const unsigned cb = (unsigned)(g.Ein * g.Ein * 8);
@@ -1291,58 +1340,6 @@ __global__ __launch_bounds__(256) void k_nd_schur(NdArgs na) {
       const double v0 = nd_load(r0, 8u * (unsigned)(max(pa0, 0) * g.Ein + max(pb0, 0)), 0);
       const double v1 = nd_load(r1, 8u * (unsigned)(max(pa1, 0) * g.Ein + max(pb1, 0)), 0);
       vv[a][b] = ((pa0 >= 0 && pb0 >= 0) ? v0 : 0.0) + ((pa1 >= 0 && pb1 >= 0) ? v1 : 0.0);
-    }
-  }
-  double acc[4][4];
-#pragma unroll
-  for (int a = 0; a < 4; ++a)
-#pragma unroll
-    for (int b = 0; b < 4; ++b) acc[a][b] = 0.0;
-  // Z in rounds of 64 rows (c <= 64: one round): a round's chunks are loaded
-  // into registers first, so that their loads share one round trip
-  constexpr int NCH = 64 / KC;
-  const __amdgpu_buffer_rsrc_t rz = nd_rsrc(z, (unsigned)(c * Emax * 8));
-  const unsigned ox = 8u * (unsigned)(x0 + min(tid & 63, nrx - 1));
-  const unsigned oy = 8u * (unsigned)(y0 + min(tid & 63, nry - 1));
-#pragma unroll 1
-  for (int kb = 0; kb < c; kb += 64) {
-    double pza[NCH][4], pzb[NCH][4];
-#pragma unroll
-    for (int q = 0; q < NCH; ++q)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int e = tid + 256 * r, xx = e & 63, kk = e >> 6;   // kk: uniform per wave
-        const int k = min(kb + q * KC + kk, c - 1);
-        const unsigned ko = (unsigned)__builtin_amdgcn_readfirstlane(k * Emax * 8);
-        const double a = nd_load(rz, ox, ko);
-        const double b = nd_load(rz, oy, ko);
-        const bool ok = kb + q * KC + kk < c;
-        pza[q][r] = (ok && xx < nrx) ? a : 0.0;
-        pzb[q][r] = (ok && xx < nry) ? b : 0.0;
-      }
-#pragma unroll
-    for (int q = 0; q < NCH; ++q) {
-      if (kb + q * KC >= c) break;
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int e = tid + 256 * r, xx = e & 63, kk = e >> 6;
-        za[kk][xx] = pza[q][r];
-        zb[kk][xx] = pzb[q][r];
-      }
-      __syncthreads();
-#pragma unroll 2
-      for (int kk = 0; kk < KC; ++kk) {
-        double xa[4], yb[4];
-#pragma unroll
-        for (int a = 0; a < 4; ++a) xa[a] = za[kk][4 * tx + a];
-#pragma unroll
-        for (int b = 0; b < 4; ++b) yb[b] = zb[kk][4 * ty + b];
-#pragma unroll
-        for (int a = 0; a < 4; ++a)
-#pragma unroll
-          for (int b = 0; b < 4; ++b) acc[a][b] = fma(xa[a], yb[b], acc[a][b]);
-      }
-      __syncthreads();
     }
   }
   double* ext = na.buf_out + g.la * na.out_stride + (int64_t)g.m * Emax * Emax;
