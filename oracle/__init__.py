@@ -20,6 +20,10 @@ periph    DAC and ADC transfer models (Sec. IV-A, V-A; the curves themselves are
           a documented reading because the paper's figure is not available).
 fcm       The evaluation phase: DAC, V.G' per tile (Eq. 14), ADC, digital
           accumulation across tiles, and conv-as-GEMM (Sec. VI).
+variation Per-device variation factors (Philox-4x64-10 + Box-Muller) and the
+          device characteristic table of generator step 2 (Sec. V-A).
+backward  The floating-point backward pass of model-in-the-loop re-training
+          (Sec. VII), fully connected and convolution layers.
 
 Parity status per function is stated in each module header.
 """
