@@ -23,6 +23,11 @@ line; the default is the convolution above):
              side --crossbar (32 / 64 / 128 / 256), wire --wire; a step
              perturbs every layer's weights, rebuilds G' and evaluates it
              (reported: the whole step and the evaluation alone).
+
+--retrain adds, for the convolution, a leg timed after the others: one
+model-in-the-loop re-training step = G' rebuild + crossbar forward pass +
+floating-point backward pass (dX and dW through the ideal weights), with the
+backward GEMMs' fp32 roofline.
 """
 
 from __future__ import annotations
@@ -99,7 +104,7 @@ def cpu_baseline(work):
 
 
 KERNEL_NAMES = ("wmax", "nd_block", "nd_merge", "nd_final", "gprime_sweep", "dac", "ktab",
-                "fill", "xbar_vmm", "finish")
+                "fill", "xbar_vmm", "finish", "bw_gemm", "bw_aux")
 
 
 def read_kernels(rxnn, steps):
@@ -327,6 +332,49 @@ def bench_stack(args):
     print(json.dumps(out), flush=True)
 
 
+def retrain_leg(args, torch, rxnn, wl, L, pp, cv, Wd, Xd, Yd, stream):
+    """K re-training steps of the convolution: rebuild G' from the weights,
+    the crossbar forward pass, and the backward pass (dX, dW) of a seeded
+    output gradient.  The weight update itself (W -= lr dW) belongs to the
+    caller's optimizer and is not part of the step."""
+    dY = torch.from_numpy(wl.normal(3003, tuple(Yd.shape), 1.0)).to(Xd.device)
+    dX, dW = torch.empty_like(Xd), torch.empty_like(Wd)
+
+    def step():
+        rxnn.remap_layer(L, Wd, stream)
+        rxnn.conv_layer(L, pp, cv, Xd, Yd, stream)
+        rxnn.conv_backward(L, pp, cv, Wd, Xd, dY, dX=dX, dW=dW, stream=stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ev0.record(stream)
+    for _ in range(args.steps):
+        step()
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    ms = ev0.elapsed_time(ev1) / args.steps
+    rxnn.profile_reset()
+    rxnn.profile_enable(1)
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    rxnn.profile_enable(False)
+    kern = read_kernels(rxnn, args.steps)
+    ho, wo = rxnn.conv_out_hw(cv)
+    bv = cv["n"] * ho * wo
+    gemm_flops = 2 * 2.0 * bv * L.P * L.Q           # dW = cols^T dY and dcols = dY W^T
+    g_us = kern["bw_gemm"]["us_per_step"]
+    ach = gemm_flops / (g_us * 1e-6) / 1e12
+    print("[bench] retrain: %.3f ms/step" % ms, file=sys.stderr, flush=True)
+    return {"ms_per_step": ms, "backward_gemm": {
+        "us_per_step": g_us, "bound": "mfma", "achieved": ach, "peak": FP32_MFMA_PEAK_TFLOPS,
+        "unit": "TFLOP/s", "frac": ach / FP32_MFMA_PEAK_TFLOPS, "flops": gemm_flops},
+        "backward_aux_us_per_step": kern.get("bw_aux", {}).get("us_per_step", 0.0),
+        "kernels": kern}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -343,6 +391,8 @@ def main():
                     help="conv3x3 / resnet50: generated per-device variation, sigma (e.g. 0.1)")
     ap.add_argument("--lut", action="store_true",
                     help="conv3x3 / resnet50: a non-linear device characteristic table")
+    ap.add_argument("--retrain", action="store_true",
+                    help="conv3x3: also time re-training steps (rebuild + forward + backward)")
     ap.add_argument("--breakdown", action="store_true",
                     help="stacks without rebuild: also time every launch in a second pass")
     args = ap.parse_args()
@@ -437,6 +487,8 @@ def main():
 
     if args.copy_probe:
         copy_probe(torch, dev)
+    retrain = retrain_leg(args, torch, rxnn, wl, L, pp, cv, Wd, Xd, Yd, stream) \
+        if args.retrain else None
 
     out = {
         "metric": "non-ideal crossbar MACs/sec per layer",
@@ -465,6 +517,8 @@ def main():
         "kernels_pass": "a second pass of the same steps with every launch timed",
         "wall_s_timed": wall,
     }
+    if retrain is not None:
+        out["retrain"] = retrain
     if not args.no_cpu_baseline:
         print("[bench] oracle on the host", file=sys.stderr, flush=True)
         out["cpu_baseline"] = cpu_baseline(dict(work, xbar=xb))

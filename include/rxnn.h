@@ -209,6 +209,42 @@ rxnn_status rxnn_conv_layer(const rxnn_layer* layer, const rxnn_periph_params* p
                             void* stream);
 
 /*
+ * Backward pass of model-in-the-loop re-training (Sec. VI, re-training with
+ * RxNN: crossbar forward pass, floating-point backward pass, data kept within
+ * the range constraints).  The gradients flow through the layer's ideal fp32
+ * weights with straight-through DAC and ADC; inputs the DAC clips and weights
+ * beyond the layer's w_max get no gradient:
+ *   dX = (dY W^T) * [0 <= x <= x_max]
+ *   dW = clip(X, 0, x_max)^T dY * [|w| <= w_max]
+ * where x_max is the periph's x_max for a quantising DAC and +inf for the
+ * ideal one (which only drops negative inputs), and w_max is the one the
+ * layer was mapped with.
+ *   W   device fp32 P x Q row-major: the ideal weights the layer was mapped
+ *       from (the same layout as for rxnn_map_layer).
+ *   X   device fp32 forward input (FC: B x P row-major; conv: NCHW).
+ *   dY  device fp32 gradient of the forward output (FC: B x Q; conv: NCHW
+ *       n x c_out x H_out x W_out).
+ *   dX  device fp32, the layout of X, overwritten; dW device fp32 P x Q,
+ *       overwritten.  Either may be NULL to skip it.
+ * All buffers are read and written on `stream`.  The contractions are fp32
+ * GEMMs (rocBLAS, on `stream`); the convolution's unrolled patches, its
+ * gradient rows and the partial products of dW's contraction (split into at
+ * most 64 chunks of output pixels, at most 2^24 floats in all) live in a
+ * layer-owned scratch buffer (conv: Bv (P + Q) floats plus the partials,
+ * Bv = n H_out W_out; FC: B P floats for dW) that grows on demand
+ * (RXNN_ENOMEM when it cannot).  x_max enters the kernels rounded to fp32.  Calls on one layer that overlap on
+ * different streams race on that buffer.  RXNN_EINVAL for bad arguments or a
+ * convolution that does not match the layer; B = 0 or Bv = 0, or dX and dW
+ * both NULL, is a no-op.
+ */
+rxnn_status rxnn_fc_backward(const rxnn_layer* layer, const rxnn_periph_params* periph,
+                             const float* W, const float* X, const float* dY, int64_t B,
+                             float* dX, float* dW, void* stream);
+rxnn_status rxnn_conv_backward(const rxnn_layer* layer, const rxnn_periph_params* periph,
+                               const rxnn_conv_desc* conv, const float* W, const float* X,
+                               const float* dY, float* dX, float* dW, void* stream);
+
+/*
  * Parity/debug exports.
  * rxnn_get_gprime copies the M x N fp32 G' of array `array` at tile
  *   (row_tile, col_tile) to host memory `host_out` (row-major, G'[i][j] = the
@@ -246,8 +282,9 @@ void rxnn_free_layer(rxnn_layer* layer);
  * "nd_merge", "nd_final" (G' build by nested dissection), "gprime_sweep" (G'
  * build by the row sweep), "dac" (DAC of the inputs), "ktab" (patch-column
  * table), "xbar_vmm" (evaluation), "fill" (clearing of a new evaluation
- * workspace) and "finish" (workspace of the shared tiles to Y, which also
- * leaves the workspace zeroed).  rxnn_profile_read synchronises, folds pending events
+ * workspace), "finish" (workspace of the shared tiles to Y, which also
+ * leaves the workspace zeroed), "bw_gemm" (the backward pass's GEMMs) and
+ * "bw_aux" (its masks, unrolling and gathers).  rxnn_profile_read synchronises, folds pending events
  * into the totals and returns total milliseconds and launch count.
  */
 rxnn_status rxnn_profile_enable(int32_t on);

@@ -23,7 +23,8 @@ fcm       The evaluation phase: DAC, V.G' per tile (Eq. 14), ADC, digital
 variation Per-device variation factors (Philox-4x64-10 + Box-Muller) and the
           device characteristic table of generator step 2 (Sec. V-A).
 backward  The floating-point backward pass of model-in-the-loop re-training
-          (Sec. VII), fully connected and convolution layers.
+          (Sec. VI, its re-training paragraph), fully connected and convolution
+          layers.
 
 Parity status per function is stated in each module header.
 """

@@ -1,5 +1,6 @@
-"""Oracle: the backward pass of model-in-the-loop re-training (Sec. VII,
-"Re-training"; Sec. VI).
+"""Oracle: the backward pass of model-in-the-loop re-training (Sec. VI, the
+RxNN framework: its re-training paragraph, and the mapping of layers onto
+matrix products).
 
 TEST INFRASTRUCTURE ONLY (see ``oracle/__init__.py``).
 
@@ -12,6 +13,9 @@ inputs, outputs and weights stay within their range constraints.  Readings
   straight-through DAC and ADC: the quantisers pass gradients unchanged, but
   the DAC's range [0, x_max] clips its input, so an input outside it gets no
   gradient, and the forward input seen by the weights is clip(x, 0, x_max).
+* With the ideal DAC (no quantisation) the range is [0, inf): the DAC only
+  drops negative inputs (V = max(x, 0) v_read / x_max), so callers pass
+  x_max = inf for it.
 * The mapping's range [-w_max, w_max] clips the weights (the quantised
   mapping saturates at L_w), so a weight outside it gets no gradient.
 * Fully connected layer, Y = X W (B x P times P x Q):

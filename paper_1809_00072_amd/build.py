@@ -29,6 +29,10 @@ HIPCC_FLAGS = [
 ]
 
 
+# rocBLAS serves the fp32 GEMMs of the re-training backward pass
+LIBS = ["-L/opt/rocm/lib", "-lrocblas"]
+
+
 def sources():
     return sorted(glob.glob(os.path.join(HERE, "csrc", "*.hip")))
 
@@ -36,7 +40,7 @@ def sources():
 def build(verbose: bool = False) -> str:
     hipcc = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
     tmp = LIB + ".tmp"
-    cmd = [hipcc, *HIPCC_FLAGS, "-o", tmp, *sources()]
+    cmd = [hipcc, *HIPCC_FLAGS, "-o", tmp, *sources(), *LIBS]
     if verbose:
         print(" ".join(cmd), flush=True)
     res = subprocess.run(cmd, capture_output=True, text=True)

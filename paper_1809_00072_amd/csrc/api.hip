@@ -116,6 +116,21 @@ rxnn_status check_xbar(const rxnn_xbar_params* p) {
   return RXNN_OK;
 }
 
+// A convolution's shape, and that it matches the layer (P = c_in kh kw, Q = c_out).
+rxnn_status check_conv(const MapScalars& ms, const rxnn_conv_desc* conv) {
+  if (!conv) return fail(RXNN_EINVAL, "conv is NULL");
+  const rxnn_conv_desc cd = *conv;
+  if (cd.n < 0 || cd.c_in < 1 || cd.h < 1 || cd.w < 1 || cd.c_out < 1 || cd.kh < 1 ||
+      cd.kw < 1 || cd.stride < 1 || cd.pad < 0)
+    return fail(RXNN_EINVAL, "invalid convolution shape");
+  if (cd.h + 2 * cd.pad < cd.kh || cd.w + 2 * cd.pad < cd.kw)
+    return fail(RXNN_EINVAL, "kernel larger than the padded input");
+  if (ms.P != (int64_t)cd.c_in * cd.kh * cd.kw || ms.Q != cd.c_out)
+    return fail(RXNN_EINVAL, "layer is %lldx%lld but the convolution needs %lldx%d",
+                (long long)ms.P, (long long)ms.Q, (long long)cd.c_in * cd.kh * cd.kw, cd.c_out);
+  return RXNN_OK;
+}
+
 rxnn_status make_periph(const rxnn_periph_params* pp, const MapScalars& ms, PeriphScalars* out) {
   if (!pp) return fail(RXNN_EINVAL, "periph is NULL");
   if (pp->dac_bits < 0 || pp->dac_bits > kMaxBits)
@@ -171,7 +186,8 @@ std::map<std::string, std::pair<double, int64_t>> g_prof_tot;
 
 // Frees every device buffer of a layer and the handle itself.
 void release_buffers(rxnn_layer* L) {
-  void* bufs[] = {L->gpt, L->d_wmax, L->ws, L->nd_ws, L->ktab, L->vbuf, L->d_vf, L->d_lut};
+  void* bufs[] = {L->gpt,  L->d_wmax, L->ws,   L->nd_ws, L->ktab,
+                  L->vbuf, L->d_vf,   L->d_lut, L->bw_ws};
   for (void* b : bufs)
     if (b) (void)hipFree(b);
   L->magic = 0;
@@ -527,19 +543,11 @@ rxnn_status rxnn_conv_layer(const rxnn_layer* layer, const rxnn_periph_params* p
                             const rxnn_conv_desc* conv, const float* X, float* Y,
                             void* stream) {
   if (!live(layer)) return fail(RXNN_EINVAL, "invalid or released layer handle");
-  if (!conv) return fail(RXNN_EINVAL, "conv is NULL");
-  const rxnn_conv_desc cd = *conv;
-  if (cd.n < 0 || cd.c_in < 1 || cd.h < 1 || cd.w < 1 || cd.c_out < 1 || cd.kh < 1 ||
-      cd.kw < 1 || cd.stride < 1 || cd.pad < 0)
-    return fail(RXNN_EINVAL, "invalid convolution shape");
-  if (cd.h + 2 * cd.pad < cd.kh || cd.w + 2 * cd.pad < cd.kw)
-    return fail(RXNN_EINVAL, "kernel larger than the padded input");
-
   rxnn_layer* L = const_cast<rxnn_layer*>(layer);
   const MapScalars& ms = L->ms;
-  if (ms.P != (int64_t)cd.c_in * cd.kh * cd.kw || ms.Q != cd.c_out)
-    return fail(RXNN_EINVAL, "layer is %lldx%lld but the convolution needs %lldx%d",
-                (long long)ms.P, (long long)ms.Q, (long long)cd.c_in * cd.kh * cd.kw, cd.c_out);
+  rxnn_status cst = check_conv(ms, conv);
+  if (cst) return cst;
+  const rxnn_conv_desc cd = *conv;
   if (ms.P >= (int64_t)1 << 22)
     return fail(RXNN_EUNSUPPORTED, "P must be below 2^22 for the evaluation kernel");
   PeriphScalars ps;
@@ -664,6 +672,156 @@ void rxnn_free_layer(rxnn_layer* layer) {
   (void)hipDeviceSynchronize();
   release_buffers(layer);
 }
+
+// ---- backward pass of re-training -------------------------------------------
+namespace {
+
+rxnn_status grow_bw(rxnn_layer* L, size_t bytes) {
+  if (L->bw_bytes >= bytes) return RXNN_OK;
+  if (L->bw_ws) HIP_TRY(hipFree(L->bw_ws));
+  L->bw_ws = nullptr;
+  L->bw_bytes = 0;
+  if (hipMalloc((void**)&L->bw_ws, bytes) != hipSuccess) {
+    (void)hipGetLastError();
+    L->bw_ws = nullptr;
+    return fail(RXNN_ENOMEM, "cannot allocate %zu bytes of backward scratch", bytes);
+  }
+  L->bw_bytes = bytes;
+  return RXNN_OK;
+}
+
+// The DAC's input range: [0, x_max] for a quantising DAC, [0, inf) for the
+// ideal one.
+float dac_range(const rxnn_periph_params* pp) {
+  return pp->dac_bits ? (float)pp->x_max : __builtin_huge_valf();
+}
+
+}  // namespace
+
+extern "C" {
+
+rxnn_status rxnn_fc_backward(const rxnn_layer* layer, const rxnn_periph_params* periph,
+                             const float* W, const float* X, const float* dY, int64_t B,
+                             float* dX, float* dW, void* stream) {
+  if (!live(layer)) return fail(RXNN_EINVAL, "invalid or released layer handle");
+  rxnn_layer* L = const_cast<rxnn_layer*>(layer);
+  PeriphScalars ps;
+  rxnn_status st = make_periph(periph, L->ms, &ps);
+  if (st) return st;
+  if (B < 0) return fail(RXNN_EINVAL, "B must be >= 0");
+  if (!W || !X || !dY) return fail(RXNN_EINVAL, "W, X and dY must not be NULL");
+  const int64_t P = L->ms.P, Q = L->ms.Q;
+  if (B > INT32_MAX || P * B > ((int64_t)1 << 40))
+    return fail(RXNN_EUNSUPPORTED, "B too large for the backward pass");
+  if (B == 0 || (!dX && !dW)) return RXNN_OK;
+  DeviceGuard dg(L->device);
+  if (!dg.ok) return fail(RXNN_EHIP, "cannot select the layer's device");
+  hipStream_t s = (hipStream_t)stream;
+  const float xr = dac_range(periph);
+  if (dX) {
+    ProfScope t("bw_gemm", s);
+    HIP_TRY(bw_gemm(L->device, s, false, true, (int)B, (int)P, (int)Q, dY, (int)Q, W, (int)Q, dX,
+                    (int)P));
+  }
+  if (dX) {
+    ProfScope t("bw_aux", s);
+    HIP_TRY(launch_bw_mask_x(dX, X, B * P, xr, s));
+  }
+  if (dW) {
+    if ((st = grow_bw(L, (size_t)B * P * sizeof(float)))) return st;
+    {
+      ProfScope t("bw_aux", s);
+      HIP_TRY(launch_bw_clip(X, B * P, xr, L->bw_ws, s));
+    }
+    {
+      ProfScope t("bw_gemm", s);
+      HIP_TRY(bw_gemm(L->device, s, true, false, (int)P, (int)Q, (int)B, L->bw_ws, (int)P, dY,
+                      (int)Q, dW, (int)Q));
+    }
+    ProfScope t("bw_aux", s);
+    HIP_TRY(launch_bw_mask_w(dW, W, P * Q, L->ms, s));
+  }
+  return RXNN_OK;
+}
+
+rxnn_status rxnn_conv_backward(const rxnn_layer* layer, const rxnn_periph_params* periph,
+                               const rxnn_conv_desc* conv, const float* W, const float* X,
+                               const float* dY, float* dX, float* dW, void* stream) {
+  if (!live(layer)) return fail(RXNN_EINVAL, "invalid or released layer handle");
+  rxnn_layer* L = const_cast<rxnn_layer*>(layer);
+  PeriphScalars ps;
+  rxnn_status st = make_periph(periph, L->ms, &ps);
+  if (st) return st;
+  if ((st = check_conv(L->ms, conv))) return st;
+  if (!W || !X || !dY) return fail(RXNN_EINVAL, "W, X and dY must not be NULL");
+  const rxnn_conv_desc cd = *conv;
+  const int ho = (cd.h + 2 * cd.pad - cd.kh) / cd.stride + 1;
+  const int wo = (cd.w + 2 * cd.pad - cd.kw) / cd.stride + 1;
+  const int64_t Bv = (int64_t)cd.n * ho * wo, P = L->ms.P, Q = L->ms.Q;
+  // the unrolling and gather kernels index output pixels and image planes with
+  // 32-bit integers and put patch columns and images on grid dimensions y, z
+  if (Bv > INT32_MAX || (int64_t)cd.h * cd.w > INT32_MAX || P > 65535 || cd.n > 65535)
+    return fail(RXNN_EUNSUPPORTED, "convolution too large for the backward pass");
+  if (Bv == 0 || (!dX && !dW)) return RXNN_OK;
+  DeviceGuard dg(L->device);
+  if (!dg.ok) return fail(RXNN_EHIP, "cannot select the layer's device");
+  hipStream_t s = (hipStream_t)stream;
+  const float xr = dac_range(periph);
+  // scratch: the patches k-major (P x Bv: the clipped patches, then their
+  // gradients), the output gradient as rows (Bv x Q) and, for a long
+  // contraction over the output pixels, dW's split-K partial products
+  const int64_t PQ = P * Q;
+  int64_t S = 1;
+  if (dW) S = std::max<int64_t>(1, std::min<int64_t>({64, Bv / 1024, ((int64_t)16 << 20) / PQ}));
+  const int64_t Kc = Bv / S, tail = Bv - S * Kc;
+  const int64_t nparts = S > 1 ? S + (tail ? 1 : 0) : 0;
+  if ((st = grow_bw(L, (size_t)(Bv * (P + Q) + nparts * PQ) * sizeof(float)))) return st;
+  float* colsT = L->bw_ws;
+  float* rows = colsT + Bv * P;
+  float* part = rows + Bv * Q;
+  {
+    ProfScope t("bw_aux", s);
+    HIP_TRY(launch_bw_rows(dY, Bv, (int)Q, ho * wo, rows, s));
+  }
+  if (dW) {
+    {
+      ProfScope t("bw_aux", s);
+      HIP_TRY(launch_bw_im2col(X, cd, ho, wo, xr, colsT, s));
+    }
+    if (S == 1) {
+      {
+        ProfScope t("bw_gemm", s);
+        HIP_TRY(bw_gemm(L->device, s, false, false, (int)P, (int)Q, (int)Bv, colsT, (int)Bv, rows,
+                        (int)Q, dW, (int)Q));
+      }
+      ProfScope t("bw_aux", s);
+      HIP_TRY(launch_bw_mask_w(dW, W, PQ, L->ms, s));
+    } else {
+      {
+        ProfScope t("bw_gemm", s);
+        HIP_TRY(bw_gemm_batched(L->device, s, false, false, (int)P, (int)Q, (int)Kc, colsT,
+                                (int)Bv, Kc, rows, (int)Q, Kc * Q, part, (int)Q, PQ, (int)S));
+        if (tail)
+          HIP_TRY(bw_gemm(L->device, s, false, false, (int)P, (int)Q, (int)tail, colsT + S * Kc,
+                          (int)Bv, rows + S * Kc * Q, (int)Q, part + S * PQ, (int)Q));
+      }
+      ProfScope t("bw_aux", s);
+      HIP_TRY(launch_bw_reduce_w(part, (int)nparts, W, PQ, L->ms, dW, s));
+    }
+  }
+  if (dX) {
+    {
+      ProfScope t("bw_gemm", s);
+      HIP_TRY(bw_gemm(L->device, s, false, true, (int)P, (int)Bv, (int)Q, W, (int)Q, rows,
+                      (int)Q, colsT, (int)Bv));
+    }
+    ProfScope t("bw_aux", s);
+    HIP_TRY(launch_bw_col2im(colsT, X, cd, ho, wo, xr, dX, s));
+  }
+  return RXNN_OK;
+}
+
+}  // extern "C"
 
 rxnn_status rxnn_profile_enable(int32_t on) {
   if (on < 0 || on > 2) return fail(RXNN_EINVAL, "profile level must be 0, 1 or 2");

@@ -70,6 +70,8 @@ struct rxnn_layer {
   size_t vbuf_bytes;
   float* d_vf;         // the layer's copy of the variation factors (or null)
   double* d_lut;       // the layer's copy of the characteristic table (or null)
+  float* bw_ws;        // backward-pass scratch (clipped inputs, patches, gradient rows)
+  size_t bw_bytes;
 };
 
 namespace rxnn {
@@ -123,6 +125,24 @@ hipError_t launch_dac(const MapScalars& ms, const PeriphScalars& ps,
 hipError_t launch_finish(const MapScalars& ms, const PeriphScalars& ps, int32_t* iacc,
                          int64_t row0, int64_t Bv, float* Y, int64_t hw_out, hipStream_t s);
 VmmPlan vmm_plan(const MapScalars& ms, const PeriphScalars& ps, int64_t Bv, bool conv);
+
+// backward pass of re-training (backward.hip)
+hipError_t bw_gemm(int device, hipStream_t s, bool ta, bool tb, int m, int n, int k,
+                   const float* A, int lda, const float* B, int ldb, float* C, int ldc);
+hipError_t bw_gemm_batched(int device, hipStream_t s, bool ta, bool tb, int m, int n, int k,
+                           const float* A, int lda, int64_t sA, const float* B, int ldb,
+                           int64_t sB, float* C, int ldc, int64_t sC, int batch);
+hipError_t launch_bw_reduce_w(const float* part, int nparts, const float* W, int64_t n,
+                              const MapScalars& ms, float* dW, hipStream_t s);
+hipError_t launch_bw_clip(const float* X, int64_t n, float x_max, float* out, hipStream_t s);
+hipError_t launch_bw_mask_x(float* dX, const float* X, int64_t n, float x_max, hipStream_t s);
+hipError_t launch_bw_mask_w(float* dW, const float* W, int64_t n, const MapScalars& ms,
+                            hipStream_t s);
+hipError_t launch_bw_im2col(const float* X, const rxnn_conv_desc& cd, int ho, int wo,
+                            float x_max, float* cols, hipStream_t s);
+hipError_t launch_bw_rows(const float* dY, int64_t Bv, int Q, int hw, float* rows, hipStream_t s);
+hipError_t launch_bw_col2im(const float* dcols, const float* X, const rxnn_conv_desc& cd, int ho,
+                            int wo, float x_max, float* dX, hipStream_t s);
 
 // ---- kernel timing (api.hip) ------------------------------------------------
 struct ProfScope {

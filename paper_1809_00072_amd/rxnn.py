@@ -21,7 +21,7 @@ EXPORTS = (
     "rxnn_map_layer", "rxnn_remap_layer", "rxnn_crossbar_vmm", "rxnn_conv_layer", "rxnn_get_gprime",
     "rxnn_set_gprime", "rxnn_vmm_debug", "rxnn_layer_info", "rxnn_layer_wmax",
     "rxnn_free_layer", "rxnn_profile_enable", "rxnn_profile_reset", "rxnn_profile_read",
-    "rxnn_status_string", "rxnn_last_error",
+    "rxnn_status_string", "rxnn_last_error", "rxnn_fc_backward", "rxnn_conv_backward",
 )
 
 
@@ -87,6 +87,9 @@ def load(path: str = LIB_PATH):
         "rxnn_profile_enable": ([i32], i32),
         "rxnn_profile_reset": ([], i32),
         "rxnn_profile_read": ([ctypes.c_char_p, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(i64)], i32),
+        "rxnn_fc_backward": ([vp, ctypes.POINTER(PeriphParams), vp, vp, vp, i64, vp, vp, vp], i32),
+        "rxnn_conv_backward": ([vp, ctypes.POINTER(PeriphParams), ctypes.POINTER(ConvDesc), vp, vp,
+                                vp, vp, vp, vp], i32),
         "rxnn_status_string": ([i32], ctypes.c_char_p),
         "rxnn_last_error": ([], ctypes.c_char_p),
     }
@@ -271,6 +274,60 @@ def conv_layer(layer: Layer, periph, conv, X, Y=None, stream=None):
                                   _ptr(X, torch.float32, "X"), _ptr(Y, torch.float32, "Y"),
                                   _stream(stream)))
     return Y
+
+
+def _grad_out(buf, like, want, what):
+    import torch
+    if buf is not None:
+        if tuple(buf.shape) != tuple(like.shape):
+            raise ValueError(f"{what} must have shape {tuple(like.shape)}")
+        return buf
+    return torch.empty_like(like) if want else None
+
+
+def fc_backward(layer: Layer, periph, W, X, dY, want_dx=True, want_dw=True, dX=None, dW=None,
+                stream=None):
+    """rxnn_fc_backward: (dX B x P or None, dW P x Q or None), device fp32,
+    written into the given buffers or new ones."""
+    import torch
+    B = X.shape[0]
+    if tuple(W.shape) != (layer.P, layer.Q):
+        raise ValueError(f"W must be {layer.P} x {layer.Q}")
+    if X.dim() != 2 or X.shape[1] != layer.P:
+        raise ValueError(f"X must be B x {layer.P}")
+    if tuple(dY.shape) != (B, layer.Q):
+        raise ValueError(f"dY must be {B} x {layer.Q}")
+    dX = _grad_out(dX, X, want_dx, "dX")
+    dW = _grad_out(dW, W, want_dw, "dW")
+    pp = periph_params(periph)
+    _check(load().rxnn_fc_backward(layer.handle, ctypes.byref(pp), _ptr(W, torch.float32, "W"),
+                                   _ptr(X, torch.float32, "X"), _ptr(dY, torch.float32, "dY"), B,
+                                   _ptr(dX), _ptr(dW), _stream(stream)))
+    return dX, dW
+
+
+def conv_backward(layer: Layer, periph, conv, W, X, dY, want_dx=True, want_dw=True, dX=None,
+                  dW=None, stream=None):
+    """rxnn_conv_backward: (dX NCHW or None, dW P x Q or None), device fp32,
+    written into the given buffers or new ones."""
+    import torch
+    cd = ConvDesc(*[int(conv[k]) for k in ("n", "c_in", "h", "w", "c_out", "kh", "kw",
+                                           "stride", "pad")])
+    if tuple(W.shape) != (layer.P, layer.Q):
+        raise ValueError(f"W must be {layer.P} x {layer.Q}")
+    if tuple(X.shape) != (conv["n"], conv["c_in"], conv["h"], conv["w"]):
+        raise ValueError("X shape does not match the convolution")
+    ho, wo = conv_out_hw(conv)
+    if tuple(dY.shape) != (conv["n"], conv["c_out"], ho, wo):
+        raise ValueError("dY shape does not match the convolution")
+    dX = _grad_out(dX, X, want_dx, "dX")
+    dW = _grad_out(dW, W, want_dw, "dW")
+    pp = periph_params(periph)
+    _check(load().rxnn_conv_backward(layer.handle, ctypes.byref(pp), ctypes.byref(cd),
+                                     _ptr(W, torch.float32, "W"), _ptr(X, torch.float32, "X"),
+                                     _ptr(dY, torch.float32, "dY"), _ptr(dX), _ptr(dW),
+                                     _stream(stream)))
+    return dX, dW
 
 
 def profile_enable(on=True):

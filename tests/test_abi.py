@@ -125,6 +125,11 @@ def test_calls_reject_unknown_handles(lib):
     cd = rxnn.ConvDesc(1, 1, 4, 4, 1, 3, 3, 1, 1)
     assert lib.rxnn_conv_layer(bogus, ctypes.byref(pp), ctypes.byref(cd), FAKE, FAKE, None) == \
         rxnn.RXNN_EINVAL
+    assert lib.rxnn_fc_backward(bogus, ctypes.byref(pp), FAKE, FAKE, FAKE, 4, FAKE, FAKE,
+                                None) == rxnn.RXNN_EINVAL
+    assert lib.rxnn_conv_backward(bogus, ctypes.byref(pp), ctypes.byref(cd), FAKE, FAKE, FAKE,
+                                  FAKE, FAKE, None) == rxnn.RXNN_EINVAL
+    assert "handle" in lib.rxnn_last_error().decode()
     buf = (ctypes.c_float * 16)()
     assert lib.rxnn_get_gprime(bogus, 0, 0, 0, buf) == rxnn.RXNN_EINVAL
     assert lib.rxnn_set_gprime(bogus, 0, 0, 0, buf) == rxnn.RXNN_EINVAL
