@@ -6,7 +6,11 @@ TEST INFRASTRUCTURE ONLY (see ``oracle/__init__.py``).
 For every tile (r, c) and array a of the layer:
 
 1. DAC: the layer inputs of row tile r become row voltages
-   (``periph.dac_voltages``); padded rows carry 0 V.
+   (``periph.dac_voltages``); padded rows carry 0 V.  With the load-dependent
+   divider DAC the inputs become codes, and every array turns them into its
+   own row voltages from its rows' loads, the row sums of its G'
+   (``periph.divider_voltages``); the layer must then be mapped without a
+   driver resistance.
 2. Crossbar: ``I = V_r . G'[r, c, a]`` (Eq. 14), fp64, one matrix product.
 3. ADC: ``code = periph.adc_codes(I)``.
 4. Digital accumulation across tiles (the tiles are merged back into one layer,
@@ -53,8 +57,13 @@ def crossbar_vmm(X, layer, params, periph, rows=None, col_tiles=None, debug=Fals
     B, P = X.shape
     M, N, R, C, A, Q = (layer[k] for k in ("M", "N", "R", "C", "A", "Q"))
     assert P == layer["P"]
+    divider = pp.divider_dac(periph)
     V = np.zeros((B, R * M), dtype=np.float64)
-    V[:, :P] = pp.dac_voltages(X, periph).astype(np.float64)
+    if divider:
+        assert float(params["r_driver"]) == 0.0, "the divider DAC replaces the driver resistance"
+        V[:, :P] = pp.dac_codes(X, int(periph["dac_bits"]), periph["x_max"])
+    else:
+        V[:, :P] = pp.dac_voltages(X, periph).astype(np.float64)
     quant = int(periph["adc_bits"]) > 0
     if quant:
         i_fs = pp.adc_full_scale(periph, M, params["g_max"])
@@ -74,7 +83,12 @@ def crossbar_vmm(X, layer, params, periph, rows=None, col_tiles=None, debug=Fals
         for r in (range(R) if row_tiles is None else sorted(row_tiles)):
             Vr = V[:, r * M:(r + 1) * M]
             for a in range(A):
-                I = Vr @ layer["gp"][(r, c)][a]
+                Gp = layer["gp"][(r, c)][a]
+                if divider:
+                    # Vr holds codes; this array's rows see their own loads
+                    I = pp.divider_voltages(Vr, Gp.sum(axis=1), periph) @ Gp
+                else:
+                    I = Vr @ Gp
                 w = array_weight(params, a)
                 if quant:
                     code = pp.adc_codes(I, thr)

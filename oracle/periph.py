@@ -26,17 +26,34 @@ implemented here:
   the precision the accelerator computes currents in.  ``adc_bits == 0`` is the
   ideal ADC (the current passes through).
 
+* Load-dependent DAC (the divider form of Sec. IV-A and Sec. V-A, selected
+  by ``dac_g_pd > 0``): the DAC is a divider between the supply V_DD and
+  ground, an input-dependent conductance g(c) to the supply and a fixed
+  pull-down g_PD to ground, whose output node drives the row into the load
+  G_Load.  Readings: the input-dependent branch is binary weighted,
+  ``g(c) = (c / L) g_on``; V_DD is set so that the unloaded DAC reaches v_read
+  at full scale, ``V_DD = v_read (g_on + g_PD) / g_on``; and the load of row i
+  of an array is that array's row sum of G', ``G_Load,i = sum_j G'_ij``, with
+  G' built without a driver resistance (the divider stands in for the
+  driver).  Then ``V_i = V_DD g(c_i) / (g(c_i) + g_PD + G_Load,i)`` in fp64,
+  per array (each array's rows see their own load).  The code c is the
+  quantiser's above; the static bend does not apply.
+
 Parity status: the curve shapes and the constants (v_read, beta, gamma) are
 readings, "parity unpinned" against the paper; the functions are pinned to
 their textbook special cases (beta = 0 is a uniform DAC, gamma = 0 a uniform
 round-half-up quantiser) and to their breakpoints in ``tests/test_oracle_periph.py``.
+The divider is pinned against the exact network (a one-row array driven by
+the divider's Thevenin equivalent, where the row sum of G' is the exact load)
+and its limits in ``tests/test_oracle_divider.py``.
 """
 
 from __future__ import annotations
 
 import numpy as np
 
-PERIPH_KEYS = ("dac_bits", "x_max", "v_read", "dac_bend", "adc_bits", "adc_bend")
+PERIPH_KEYS = ("dac_bits", "x_max", "v_read", "dac_bend", "adc_bits", "adc_bend", "dac_g_on",
+               "dac_g_pd")
 
 
 def _phi(u, bend):
@@ -69,6 +86,25 @@ def dac_voltages(X, periph):
         return np.maximum(X, np.float32(0.0)) * s_v
     lut = dac_lut(b, periph["v_read"], periph["dac_bend"])
     return lut[dac_codes(X, b, periph["x_max"])]
+
+
+def divider_dac(periph):
+    """True when the periph selects the load-dependent divider DAC."""
+    return float(periph.get("dac_g_pd", 0.0) or 0.0) > 0.0
+
+
+def divider_vdd(periph):
+    g_on, g_pd = float(periph["dac_g_on"]), float(periph["dac_g_pd"])
+    return float(periph["v_read"]) * (g_on + g_pd) / g_on
+
+
+def divider_voltages(codes, g_load, periph):
+    """Row voltages (fp64) of the divider DAC for integer codes [..., M] and
+    the rows' loads g_load [M] (siemens)."""
+    L = (1 << int(periph["dac_bits"])) - 1
+    g = np.asarray(codes, dtype=np.float64) / L * float(periph["dac_g_on"])
+    return divider_vdd(periph) * g / (g + float(periph["dac_g_pd"]) +
+                                      np.asarray(g_load, dtype=np.float64))
 
 
 def adc_full_scale(periph, M, g_max):
