@@ -104,7 +104,7 @@ def cpu_baseline(work):
 
 
 KERNEL_NAMES = ("wmax", "nd_block", "nd_merge", "nd_final", "gprime_sweep", "dac", "ktab",
-                "fill", "xbar_vmm", "finish", "bw_gemm", "bw_aux")
+                "fill", "xbar_vmm", "finish", "bw_gemm", "bw_aux", "gload")
 
 
 def read_kernels(rxnn, steps):
@@ -133,8 +133,14 @@ def device_options(xb, args, seed=5000):
     return xb
 
 
+# The load-dependent divider DAC: full-scale branch 200 ohm, pull-down 2 kOhm.
+DIVIDER_G_ON, DIVIDER_G_PD = 5e-3, 5e-4
+
+
 def device_note(args):
     note = ""
+    if getattr(args, "divider", False):
+        note += "; load-dependent divider DAC (g_on 5 mS, g_pd 0.5 mS, no driver resistance)"
     if args.variation > 0.0:
         note += "; per-device variation sigma %g" % args.variation
     if args.lut:
@@ -391,6 +397,9 @@ def main():
                     help="conv3x3 / resnet50: generated per-device variation, sigma (e.g. 0.1)")
     ap.add_argument("--lut", action="store_true",
                     help="conv3x3 / resnet50: a non-linear device characteristic table")
+    ap.add_argument("--divider", action="store_true",
+                    help="conv3x3: the load-dependent divider DAC (layer mapped without "
+                         "driver resistance)")
     ap.add_argument("--retrain", action="store_true",
                     help="conv3x3: also time re-training steps (rebuild + forward + backward)")
     ap.add_argument("--breakdown", action="store_true",
@@ -414,6 +423,9 @@ def main():
     work = wl.conv3x3_64_56()
     cv, xb, pp = work["conv"], work["xbar"], work["periph"]
     xb = device_options(xb, args)
+    if args.divider:
+        xb = dict(xb, r_driver=0.0)
+        pp = dict(pp, dac_bend=0.0, dac_g_on=DIVIDER_G_ON, dac_g_pd=DIVIDER_G_PD)
     dev = torch.device("cuda:0")
     Wd = torch.from_numpy(work["W"]).to(dev)
     Xd = torch.from_numpy(work["X"]).to(dev)
@@ -521,7 +533,7 @@ def main():
         out["retrain"] = retrain
     if not args.no_cpu_baseline:
         print("[bench] oracle on the host", file=sys.stderr, flush=True)
-        out["cpu_baseline"] = cpu_baseline(dict(work, xbar=xb))
+        out["cpu_baseline"] = cpu_baseline(dict(work, xbar=xb, periph=pp))
     L.free()
     print(json.dumps(out), flush=True)
 

@@ -137,6 +137,22 @@ typedef struct {
  *   itself is accumulated).
  * x_max > 0, v_read > 0, 0 <= dac_bend < 1, |adc_bend| <= 0.5.
  *
+ * Load-dependent DAC (the resistive divider of Sec. IV-A and Sec. V-A),
+ * selected by dac_g_pd > 0: the DAC output node sits between the supply V_DD
+ * through an input-dependent conductance g(c) = (c / L) dac_g_on and ground
+ * through the pull-down dac_g_pd, and drives the row into the load G_Load,i =
+ * sum_j G'_ij of the array it feeds (each array's rows see their own load):
+ *   V_i = V_DD g(c_i) / (g(c_i) + dac_g_pd + G_Load,i),
+ *   V_DD = v_read (dac_g_on + dac_g_pd) / dac_g_on (the unloaded DAC reaches
+ *   v_read at full scale).
+ * The divider stands in for the driver: the layer must have been mapped with
+ * r_driver = 0 (RXNN_EINVAL otherwise).  Requires dac_bits > 0, dac_g_on > 0
+ * and dac_bend = 0; the code c is the quantiser's above.  The evaluation
+ * kernel converts codes to voltages per array in fp32 (one reciprocal per
+ * element); the layer keeps the rows' loads (n_arrays x M floats, from the
+ * stored G', recomputed after a remap).  dac_g_pd = 0 selects the static DAC
+ * above and ignores dac_g_on.  Siemens; finite and >= 0.
+ *
  * Output scale: with the quantising ADC, Y = fp32(acc) * fp32(LSB / (s_v s_w'))
  * where acc = sum over row tiles and arrays of weight(a) * code, LSB = I_FS / L,
  * s_v = v_read / x_max and s_w' = s_w (continuous) or dG L_w / w_max
@@ -147,6 +163,7 @@ typedef struct {
   double x_max, v_read, dac_bend;
   int32_t adc_bits;
   double adc_bend;
+  double dac_g_on, dac_g_pd;
 } rxnn_periph_params;
 
 /* Convolution shape: input NCHW n x c_in x h x w, weight c_out x c_in x kh x kw,

@@ -38,20 +38,42 @@ def sources():
 
 
 def build(verbose: bool = False) -> str:
+    """Compiles every source to an object in parallel, then links the library."""
     hipcc = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
+    objdir = os.path.join(HERE, "_build")
+    os.makedirs(objdir, exist_ok=True)
+    compile_flags = [f for f in HIPCC_FLAGS if f != "-shared"]
+    jobs = []
+    for src in sources():
+        obj = os.path.join(objdir, os.path.basename(src) + ".o")
+        cmd = [hipcc, *compile_flags, "-c", "-o", obj, src]
+        if verbose:
+            print(" ".join(cmd), flush=True)
+        jobs.append((obj, subprocess.Popen(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT,
+                                           text=True)))
+    failed = False
+    noise = "packed-fp32-ops"
+    objs = []
+    for obj, proc in jobs:
+        out, _ = proc.communicate()
+        objs.append(obj)
+        if proc.returncode != 0:
+            failed = True
+            sys.stderr.write(out)
+        elif verbose and out:
+            for line in out.splitlines():
+                if noise not in line:
+                    print(line)
+    if failed:
+        raise RuntimeError("hipcc failed to build librxnn.so")
     tmp = LIB + ".tmp"
-    cmd = [hipcc, *HIPCC_FLAGS, "-o", tmp, *sources(), *LIBS]
+    cmd = [hipcc, "--offload-arch=gfx950", "-shared", "-fPIC", "-o", tmp, *objs, *LIBS]
     if verbose:
         print(" ".join(cmd), flush=True)
     res = subprocess.run(cmd, capture_output=True, text=True)
     if res.returncode != 0:
         sys.stderr.write(res.stdout + res.stderr)
-        raise RuntimeError("hipcc failed to build librxnn.so")
-    if verbose and (res.stdout or res.stderr):
-        noise = "packed-fp32-ops"
-        for line in (res.stdout + res.stderr).splitlines():
-            if noise not in line:
-                print(line)
+        raise RuntimeError("hipcc failed to link librxnn.so")
     os.replace(tmp, LIB)
     return LIB
 

@@ -145,6 +145,14 @@ rxnn_status make_periph(const rxnn_periph_params* pp, const MapScalars& ms, Peri
     return fail(RXNN_EINVAL, "dac_bend must be in [0, 1)");
   if (!(isfinite(pp->adc_bend) && fabs(pp->adc_bend) <= 0.5))
     return fail(RXNN_EINVAL, "|adc_bend| must be <= 0.5");
+  if (!(isfinite(pp->dac_g_on) && pp->dac_g_on >= 0.0 && isfinite(pp->dac_g_pd) &&
+        pp->dac_g_pd >= 0.0))
+    return fail(RXNN_EINVAL, "dac_g_on and dac_g_pd must be finite and >= 0");
+  if (pp->dac_g_pd > 0.0) {
+    if (!(pp->dac_g_on > 0.0)) return fail(RXNN_EINVAL, "the divider DAC needs dac_g_on > 0");
+    if (pp->dac_bits == 0) return fail(RXNN_EINVAL, "the divider DAC needs dac_bits > 0");
+    if (pp->dac_bend != 0.0) return fail(RXNN_EINVAL, "the divider DAC needs dac_bend = 0");
+  }
   PeriphScalars ps;
   memset(&ps, 0, sizeof ps);
   ps.dac_bits = pp->dac_bits;
@@ -157,6 +165,13 @@ rxnn_status make_periph(const rxnn_periph_params* pp, const MapScalars& ms, Peri
   ps.dac_s_in = pp->dac_bits ? (float)((double)ps.dac_levels / pp->x_max) : 0.0f;
   ps.s_v_ideal = (float)(pp->v_read / pp->x_max);
   ps.s_v = pp->v_read / pp->x_max;
+  if (pp->dac_g_pd > 0.0) {
+    const double vdd = pp->v_read * (pp->dac_g_on + pp->dac_g_pd) / pp->dac_g_on;
+    ps.ldac = 1;
+    ps.dac_inv_vdd = (float)(1.0 / vdd);
+    ps.dac_hs = (float)((double)ps.dac_levels / (pp->dac_g_on * vdd));
+    ps.dac_gpd = (float)pp->dac_g_pd;
+  }
   ps.i_fs = pp->v_read * (double)ms.M * ms.g_max;
   if (pp->adc_bits) {
     ps.lsb = ps.i_fs / (double)ps.adc_levels;
@@ -186,8 +201,8 @@ std::map<std::string, std::pair<double, int64_t>> g_prof_tot;
 
 // Frees every device buffer of a layer and the handle itself.
 void release_buffers(rxnn_layer* L) {
-  void* bufs[] = {L->gpt,  L->d_wmax, L->ws,   L->nd_ws, L->ktab,
-                  L->vbuf, L->d_vf,   L->d_lut, L->bw_ws};
+  void* bufs[] = {L->gpt,  L->d_wmax, L->ws,    L->nd_ws, L->ktab,
+                  L->vbuf, L->d_vf,   L->d_lut, L->bw_ws, L->gload};
   for (void* b : bufs)
     if (b) (void)hipFree(b);
   L->magic = 0;
@@ -226,6 +241,26 @@ rxnn_status run_vmm(const rxnn_layer* L, const PeriphScalars& ps, const float* X
                     int64_t hw_out, float* dbgI, int32_t* dbgC, hipStream_t s,
                     const int* ktab = nullptr) {
   const MapScalars& ms = L->ms;
+  if (ps.ldac) {
+    // the divider stands in for the driver; the rows' loads follow G'
+    if (ms.r_driver != 0.0)
+      return fail(RXNN_EINVAL, "the divider DAC needs a layer mapped with r_driver = 0");
+    rxnn_layer* Lm = const_cast<rxnn_layer*>(L);
+    if (!Lm->gload) {
+      void* p = nullptr;
+      const size_t bytes = (size_t)ms.R * ms.C * ms.A * ms.Mp * sizeof(float);
+      if (hipMalloc(&p, bytes) != hipSuccess) {
+        (void)hipGetLastError();
+        return fail(RXNN_ENOMEM, "cannot allocate %zu bytes for the row loads", bytes);
+      }
+      Lm->gload = (float*)p;
+    }
+    if (!Lm->gload_valid) {
+      ProfScope t("gload", s);
+      HIP_TRY(launch_gload(ms, L->gpt, Lm->gload, s));
+      Lm->gload_valid = true;
+    }
+  }
   VmmPlan plan{0, 0, 0};
   if (!(dbgI || dbgC)) plan = vmm_plan(ms, ps, Bv, conv != nullptr);
   const int workers = plan.workers;
@@ -267,6 +302,7 @@ rxnn_status run_vmm(const rxnn_layer* L, const PeriphScalars& ps, const float* X
   vl.dbg_I = dbgI;
   vl.dbg_code = dbgC;
   vl.ktab = ktab;
+  vl.gload = L->gload;
   // The shared-tile units add into a zeroed workspace.  The finish kernel
   // zeroes again every word it reads, and no other word is ever written, so
   // the workspace is cleared only when new or after a call that did not end.
@@ -315,6 +351,7 @@ rxnn_status vmm_common(const rxnn_layer* layer, const rxnn_periph_params* periph
 
 // w_max (fixed or reduced from W) followed by the G' build of every array.
 hipError_t build_gprime(rxnn_layer* L, const float* W, hipStream_t s) {
+  L->gload_valid = false;   // the row loads follow G'
   const MapScalars& ms = L->ms;
   hipError_t e = hipSuccess;
   {
@@ -635,6 +672,7 @@ rxnn_status rxnn_set_gprime(rxnn_layer* layer, int64_t row_tile, int64_t col_til
   for (int i = 0; i < ms.M; ++i)
     for (int j = 0; j < ms.N; ++j) t[(size_t)j * ms.Mp + i] = host_in[(size_t)i * ms.N + j];
   const int64_t arr = (col_tile * ms.R + row_tile) * ms.A + array;
+  layer->gload_valid = false;
   HIP_TRY(hipDeviceSynchronize());
   HIP_TRY(hipMemcpy(layer->gpt + arr * ms.Np * ms.Mp, t.data(), t.size() * sizeof(float),
                     hipMemcpyHostToDevice));

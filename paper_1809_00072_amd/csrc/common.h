@@ -46,6 +46,11 @@ struct PeriphScalars {
   int n_buckets;               // ADC bucket table size
   float bucket_inv_w;          // fp32(n_buckets / i_fs)
   double bucket_w;             // i_fs / n_buckets
+  // load-dependent divider DAC: V = c / (c / V_DD + (g_pd + G_Load) L / (g_on V_DD))
+  int ldac;                    // 1: the DAC pass writes codes, the evaluation converts
+  float dac_inv_vdd;           // fp32(1 / V_DD)
+  float dac_hs;                // fp32(L / (g_on V_DD))
+  float dac_gpd;               // fp32(g_pd)
 };
 
 }  // namespace rxnn
@@ -72,6 +77,8 @@ struct rxnn_layer {
   double* d_lut;       // the layer's copy of the characteristic table (or null)
   float* bw_ws;        // backward-pass scratch (clipped inputs, patches, gradient rows)
   size_t bw_bytes;
+  float* gload;        // row loads sum_j G'_ij per array, [C][R][A][Mp] (divider DAC), or null
+  bool gload_valid;    // gload matches the stored G'
 };
 
 namespace rxnn {
@@ -100,6 +107,7 @@ struct VmmLaunch {
   float* dbg_I;         // [R][C][A][Bv][N] or null
   int32_t* dbg_code;    // [R][C][A][Bv][N] or null
   const int* ktab;      // conv: patch-column table
+  const float* gload;   // divider DAC: row loads [C][R][A][Mp]
 };
 // Schedule of the evaluation kernel.  workers = 0: one workgroup per tile.
 // workers > 0: persistent workgroups; tiles [0, dp_tiles) are whole-tile work,
@@ -125,6 +133,8 @@ hipError_t launch_dac(const MapScalars& ms, const PeriphScalars& ps,
 hipError_t launch_finish(const MapScalars& ms, const PeriphScalars& ps, int32_t* iacc,
                          int64_t row0, int64_t Bv, float* Y, int64_t hw_out, hipStream_t s);
 VmmPlan vmm_plan(const MapScalars& ms, const PeriphScalars& ps, int64_t Bv, bool conv);
+// row loads of every array: gload[arr][m] = sum over columns of G'[arr][m][.]
+hipError_t launch_gload(const MapScalars& ms, const float* gpt, float* gload, hipStream_t s);
 
 // backward pass of re-training (backward.hip)
 hipError_t bw_gemm(int device, hipStream_t s, bool ta, bool tb, int m, int n, int k,

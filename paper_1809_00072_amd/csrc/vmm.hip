@@ -77,6 +77,7 @@ struct VmmArgs {
   float* dbg_I;
   int32_t* dbg_code;
   const int* ktab;      // conv: per (row tile, input) byte offset inside the window
+  const float* gload;   // divider DAC: row loads [C][R][A][Mp]
   int n_cb;             // column blocks (tiles along y)
   int workers;          // 0: one workgroup per tile; > 0: persistent workgroups
   int64_t dp_tiles;     // persistent: tiles [0, dp_tiles) are whole-tile work (direct
@@ -114,10 +115,12 @@ __global__ __launch_bounds__(256) void k_dac(PeriphScalars ps, ConvGeom cg, cons
       lut[k] = (float)(ps.v_read * bend((double)k / (double)L, ps.dac_bend));
   }
   __syncthreads();
+  // the divider DAC's voltage depends on the array a row feeds: the pass then
+  // writes the code, which the evaluation kernel converts per array
   auto dac = [&](float x) -> float {
     if (ps.dac_bits > 0) {
-      const float t = rintf(x * ps.dac_s_in);
-      return lut[(int)fminf(fmaxf(t, 0.0f), (float)ps.dac_levels)];
+      const float c = fminf(fmaxf(rintf(x * ps.dac_s_in), 0.0f), (float)ps.dac_levels);
+      return ps.ldac ? c : lut[(int)c];
     }
     return fmaxf(x, 0.0f) * ps.s_v_ideal;
   };
@@ -144,13 +147,18 @@ __global__ __launch_bounds__(256) void k_dac(PeriphScalars ps, ConvGeom cg, cons
   }
 }
 
-template <int BN, bool CONV, bool QADC, bool DEBUG>
+// LDAC (the load-dependent divider DAC): V holds codes c, and every array p of
+// the pair converts them with its rows' loads, staged per chunk as
+// h_p[k] = (g_pd + G_Load,p,k) L / (g_on V_DD):
+//   V = c / (c / V_DD + h_p[k]) = V_DD g(c) / (g(c) + g_pd + G_Load).
+template <int BN, bool CONV, bool QADC, bool DEBUG, bool LDAC>
 __global__ __launch_bounds__(NTHR, 2) void k_xbar_vmm(VmmArgs va) {
   constexpr int NT = BN / 16;   // column fragments per wave
   constexpr int MT = 2;         // row fragments per wave (32 rows)
   constexpr int GV4 = BN / 8;   // float4 of G' staged per thread
   __shared__ __attribute__((aligned(16))) float Vs[BM * LDK];
   __shared__ __attribute__((aligned(16))) float Gs[2 * BN * LDK];
+  __shared__ __attribute__((aligned(16))) float Hs[LDAC ? 2 * KC : 4];
   extern __shared__ float2 adct[];   // ADC table, n_buckets + 2 entries
 
   const MapScalars& ms = va.ms;
@@ -263,6 +271,7 @@ __global__ __launch_bounds__(NTHR, 2) void k_xbar_vmm(VmmArgs va) {
 
   float xr[XPT];
   f32x4 gr[GV4];
+  float hr = 0.0f;   // LDAC: the load of row kc0 + (tid % KC) of array tid / KC of the pair
 
   auto load_stage = [&](int s) {
     int r, ap, kci, nk;
@@ -312,6 +321,10 @@ __global__ __launch_bounds__(NTHR, 2) void k_xbar_vmm(VmmArgs va) {
       const int off = kidx < ms.Mp ? (p * tile_elems + (n0 + n) * ms.Mp + kidx) * 4 : kOob;
       gr[it] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(gsrc, off, 0, 0));
     }
+    if (LDAC && tid < 2 * KC) {
+      const int kidx = kc0 + (tid & (KC - 1));
+      hr = kidx < ms.Mp ? va.gload[(arr0 + (tid >> 6)) * ms.Mp + kidx] : 0.0f;
+    }
   };
 
   auto store_stage = [&](int s) {
@@ -349,6 +362,7 @@ __global__ __launch_bounds__(NTHR, 2) void k_xbar_vmm(VmmArgs va) {
       const int n = rm / (KC / 4), k4 = rm % (KC / 4);
       *(f32x4*)&Gs[(p * BN + n) * LDK + 4 * k4] = gr[it];
     }
+    if (LDAC && tid < 2 * KC) Hs[tid] = (ps.dac_gpd + hr) * ps.dac_hs;
   };
 
   // ---- accumulators -----------------------------------------------------
@@ -390,6 +404,19 @@ __global__ __launch_bounds__(NTHR, 2) void k_xbar_vmm(VmmArgs va) {
 #pragma unroll
         for (int nt = 0; nt < NT; ++nt)
           bf[nt] = *(const f32x4*)&Gs[(p * BN + nt * 16 + li) * LDK + kb + 4 * g];
+        f32x4 vf[MT];
+        if (LDAC) {
+          const f32x4 hv = *(const f32x4*)&Hs[p * KC + kb + 4 * g];
+#pragma unroll
+          for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+              vf[mt][j] = af[mt][j] *
+                          __builtin_amdgcn_rcpf(__builtin_fmaf(af[mt][j], ps.dac_inv_vdd, hv[j]));
+        } else {
+#pragma unroll
+          for (int mt = 0; mt < MT; ++mt) vf[mt] = af[mt];
+        }
 #pragma unroll
         for (int ss = 0; ss < 4; ++ss)
 #pragma unroll
@@ -397,7 +424,7 @@ __global__ __launch_bounds__(NTHR, 2) void k_xbar_vmm(VmmArgs va) {
 #pragma unroll
             for (int nt = 0; nt < NT; ++nt)
               acc[p][mt][nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(
-                  af[mt][ss], bf[nt][ss], acc[p][mt][nt], 0, 0, 0);
+                  vf[mt][ss], bf[nt][ss], acc[p][mt][nt], 0, 0, 0);
       }
     };
     const int kb_end = min(KC, ms.Mp - kc0);
@@ -613,9 +640,9 @@ hipError_t allow_adc_table(K kernel) {
                              (kMaxBuckets + 2) * (int)sizeof(float2));
 }
 
-template <int BN, bool CONV, bool QADC, bool DEBUG>
+template <int BN, bool CONV, bool QADC, bool DEBUG, bool LDAC>
 hipError_t launch_one(const VmmArgs& va, dim3 grid, hipStream_t s) {
-  auto kern = k_xbar_vmm<BN, CONV, QADC, DEBUG>;
+  auto kern = k_xbar_vmm<BN, CONV, QADC, DEBUG, LDAC>;
   static const hipError_t attr = allow_adc_table(kern);
   if (attr != hipSuccess) return attr;
   const size_t shm = QADC ? (size_t)(va.ps.n_buckets + 2) * sizeof(float2) : 0;
@@ -625,8 +652,11 @@ hipError_t launch_one(const VmmArgs& va, dim3 grid, hipStream_t s) {
 
 template <int BN, bool CONV, bool QADC>
 hipError_t launch_t(const VmmArgs& va, dim3 grid, hipStream_t s, bool debug) {
-  return debug ? launch_one<BN, CONV, QADC, true>(va, grid, s)
-               : launch_one<BN, CONV, QADC, false>(va, grid, s);
+  if (va.ps.ldac)
+    return debug ? launch_one<BN, CONV, QADC, true, true>(va, grid, s)
+                 : launch_one<BN, CONV, QADC, false, true>(va, grid, s);
+  return debug ? launch_one<BN, CONV, QADC, true, false>(va, grid, s)
+               : launch_one<BN, CONV, QADC, false, false>(va, grid, s);
 }
 
 template <int BN>
@@ -656,13 +686,13 @@ int col_blocks(const MapScalars& ms, int bn, bool debug) {
 }
 
 // Workgroups of the quantising evaluation kernel resident on the device at once.
-template <int BN, bool CONV>
+template <int BN, bool CONV, bool LDAC>
 int64_t slots_t(const PeriphScalars& ps) {
   int dev = 0, cus = 0, per_cu = 0;
   if (hipGetDevice(&dev) != hipSuccess) return 0;
   if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
     return 0;
-  auto kern = k_xbar_vmm<BN, CONV, true, false>;
+  auto kern = k_xbar_vmm<BN, CONV, true, false, LDAC>;
   if (allow_adc_table(kern) != hipSuccess) return 0;
   const size_t shm = (size_t)(ps.n_buckets + 2) * sizeof(float2);
   if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void*>(kern),
@@ -671,10 +701,38 @@ int64_t slots_t(const PeriphScalars& ps) {
   return (int64_t)cus * per_cu;
 }
 
+template <bool LDAC>
+int64_t slots_l(int bn, bool conv, const PeriphScalars& ps) {
+  if (bn == 64) return conv ? slots_t<64, true, LDAC>(ps) : slots_t<64, false, LDAC>(ps);
+  if (bn == 32) return conv ? slots_t<32, true, LDAC>(ps) : slots_t<32, false, LDAC>(ps);
+  return conv ? slots_t<16, true, LDAC>(ps) : slots_t<16, false, LDAC>(ps);
+}
+
 int64_t slots_for(int bn, bool conv, const PeriphScalars& ps) {
-  if (bn == 64) return conv ? slots_t<64, true>(ps) : slots_t<64, false>(ps);
-  if (bn == 32) return conv ? slots_t<32, true>(ps) : slots_t<32, false>(ps);
-  return conv ? slots_t<16, true>(ps) : slots_t<16, false>(ps);
+  return ps.ldac ? slots_l<true>(bn, conv, ps) : slots_l<false>(bn, conv, ps);
+}
+
+// Row loads of the arrays, fp64 sums over each array's stored columns (the
+// padded storage columns are zero).  Workgroup (x, y): array x, rows
+// 64 y .. 64 y + 63; its four waves take every fourth column and combine
+// their partial sums in LDS.
+__global__ __launch_bounds__(256) void k_gload(const float* __restrict__ gpt, int Np, int Mp,
+                                               float* __restrict__ gload) {
+  __shared__ double part[4][64];
+  const int64_t arr = blockIdx.x;
+  const int m = blockIdx.y * 64 + (threadIdx.x & 63), jq = threadIdx.x >> 6;
+  double acc = 0.0;
+  if (m < Mp) {
+    const float* g = gpt + arr * ((int64_t)Np * Mp) + m;
+#pragma unroll 4
+    for (int j = jq; j < Np; j += 4) acc += (double)g[(int64_t)j * Mp];
+  }
+  part[jq][threadIdx.x & 63] = acc;
+  __syncthreads();
+  if (jq == 0 && m < Mp) {
+    const int t = threadIdx.x;
+    gload[arr * Mp + m] = (float)(((part[0][t] + part[1][t]) + part[2][t]) + part[3][t]);
+  }
 }
 
 ConvGeom conv_geom(const rxnn_conv_desc& cd) {
@@ -762,6 +820,7 @@ hipError_t launch_xbar_vmm(const MapScalars& ms, const PeriphScalars& ps, const 
   va.dbg_I = vl.dbg_I;
   va.dbg_code = vl.dbg_code;
   va.ktab = vl.ktab;
+  va.gload = vl.gload;
   const int bn = pick_bn(ms.Np);
   const bool debug = vl.dbg_I != nullptr || vl.dbg_code != nullptr;
   va.n_cb = col_blocks(ms, bn, debug);
@@ -774,6 +833,13 @@ hipError_t launch_xbar_vmm(const MapScalars& ms, const PeriphScalars& ps, const 
   if (bn == 64) return launch_bn<64>(va, grid, s, conv, qadc, debug);
   if (bn == 32) return launch_bn<32>(va, grid, s, conv, qadc, debug);
   return launch_bn<16>(va, grid, s, conv, qadc, debug);
+}
+
+hipError_t launch_gload(const MapScalars& ms, const float* gpt, float* gload, hipStream_t s) {
+  const int64_t n_arrays = (int64_t)ms.R * ms.C * ms.A;
+  const dim3 grid((unsigned)n_arrays, (unsigned)((ms.Mp + 63) / 64));
+  hipLaunchKernelGGL(k_gload, grid, dim3(256), 0, s, gpt, ms.Np, ms.Mp, gload);
+  return hipGetLastError();
 }
 
 int ktab_entries(const MapScalars& ms) { return ms.R * (((ms.Mp + KC - 1) / KC) * KC); }

@@ -47,6 +47,7 @@ class PeriphParams(ctypes.Structure):
         ("x_max", ctypes.c_double), ("v_read", ctypes.c_double), ("dac_bend", ctypes.c_double),
         ("adc_bits", ctypes.c_int32),
         ("adc_bend", ctypes.c_double),
+        ("dac_g_on", ctypes.c_double), ("dac_g_pd", ctypes.c_double),
     ]
 
 
@@ -144,7 +145,9 @@ def xbar_params(d, variation=None, lut=None) -> XbarParams:
 
 def periph_params(d) -> PeriphParams:
     return PeriphParams(int(d["dac_bits"]), float(d["x_max"]), float(d["v_read"]),
-                        float(d["dac_bend"]), int(d["adc_bits"]), float(d["adc_bend"]))
+                        float(d["dac_bend"]), int(d["adc_bits"]), float(d["adc_bend"]),
+                        float(d.get("dac_g_on", 0.0) or 0.0),
+                        float(d.get("dac_g_pd", 0.0) or 0.0))
 
 
 @dataclass
