@@ -594,6 +594,8 @@ rxnn_status rxnn_conv_layer(const rxnn_layer* layer, const rxnn_periph_params* p
   const int64_t ho = (cd.h + 2 * cd.pad - cd.kh) / cd.stride + 1;
   const int64_t wo = (cd.w + 2 * cd.pad - cd.kw) / cd.stride + 1;
   const int64_t Bv = (int64_t)cd.n * ho * wo;
+  if (Bv > INT32_MAX)
+    return fail(RXNN_EUNSUPPORTED, "more than 2^31 - 1 output pixels per call");
   {
     // the images one 128-pixel block of the evaluation kernel reads are
     // addressed with 32-bit byte offsets

@@ -78,6 +78,7 @@ struct VmmArgs {
   int32_t* dbg_code;
   const int* ktab;      // conv: per (row tile, input) byte offset inside the window
   const float* gload;   // divider DAC: row loads [C][R][A][Mp]
+  FastDiv fd_hw, fd_wo; // conv: division by H_out W_out and by W_out (product rows < 2^31)
   int n_cb;             // column blocks (tiles along y)
   int workers;          // 0: one workgroup per tile; > 0: persistent workgroups
   int64_t dp_tiles;     // persistent: tiles [0, dp_tiles) are whole-tile work (direct
@@ -233,15 +234,15 @@ __global__ __launch_bounds__(NTHR, 2) void k_xbar_vmm(VmmArgs va) {
   if (CONV) {
     const int hw = va.cg.ho * va.cg.wo;
     const int64_t chw = (int64_t)va.cg.c_in * va.cg.hp * va.cg.wp;
-    const int64_t img_first = b0 / hw;
-    const int64_t img_last = (b0 + n_rows - 1) / hw;
+    const int img_first = (int)div_by((uint32_t)b0, va.fd_hw);
+    const int img_last = (int)div_by((uint32_t)(b0 + n_rows - 1), va.fd_hw);
     xsrc = uniform_rsrc(va.V + img_first * chw, (img_last - img_first + 1) * chw * 4);
     // rows past the batch read the last real row (their outputs are dropped)
-    const int64_t bv = b0 + min(row_cv, n_rows - 1);
-    const int64_t img = bv / hw;
-    const int pix = (int)(bv - img * hw);
-    const int oy = pix / va.cg.wo, ox = pix - oy * va.cg.wo;
-    xbase = (int)(((img - img_first) * chw + (int64_t)oy * va.cg.stride * va.cg.wp +
+    const int bv = (int)b0 + min(row_cv, n_rows - 1);
+    const int img = (int)div_by((uint32_t)bv, va.fd_hw);
+    const int pix = bv - img * hw;
+    const int oy = (int)div_by((uint32_t)pix, va.fd_wo), ox = pix - oy * va.cg.wo;
+    xbase = (int)(((int64_t)(img - img_first) * chw + (int64_t)oy * va.cg.stride * va.cg.wp +
                    (int64_t)ox * va.cg.stride) * 4);
   } else {
     xsrc = uniform_rsrc(va.V + b0 * va.ldx, (int64_t)n_rows * va.ldx * 4);
@@ -259,23 +260,37 @@ __global__ __launch_bounds__(NTHR, 2) void k_xbar_vmm(VmmArgs va) {
   const int n_stages = r_end == ms.R ? (r_end - 1 - r_begin) * per_r + n_pairs * nkc_last
                                      : (r_end - r_begin) * per_r;
   const int tile_elems = ms.Np * ms.Mp;
-  // stage s -> row tile r, pair ap, chunk kci of the nk chunks of r
-  auto decode = [&](int s, int& r, int& ap, int& kci, int& nk) {
-    const int rr = s / per_r;
-    const int rem = s - rr * per_r;
-    r = r_begin + rr;
-    nk = r == ms.R - 1 ? nkc_last : nkc;
-    ap = rem / nk;
-    kci = rem - ap * nk;
+  // Stages in order: row tile r, then pair ap, then chunk kci of the nk
+  // chunks of r (all workgroup-uniform).
+  struct Stage {
+    int r, ap, kci, nk;
   };
+  auto first_stage = [&]() {
+    return Stage{r_begin, 0, 0, r_begin == ms.R - 1 ? nkc_last : nkc};
+  };
+  auto next_stage = [&](Stage t) {
+    if (++t.kci == t.nk) {
+      t.kci = 0;
+      if (++t.ap == n_pairs) {
+        t.ap = 0;
+        ++t.r;
+        t.nk = t.r == ms.R - 1 ? nkc_last : nkc;
+      }
+    }
+    return t;
+  };
+  (void)per_r;
+  // G' staging: thread tid loads inputs 4 (tid % 16) .. + 3 of column
+  // tid / 16 + 16 j of array p of the pair, j + p BN / 16 = it; only the
+  // column and array move with it, so they go into the uniform offset
+  const int goff_v = ((tid >> 4) * ms.Mp + 4 * (tid & 15)) * 4;
 
   float xr[XPT];
   f32x4 gr[GV4];
   float hr = 0.0f;   // LDAC: the load of row kc0 + (tid % KC) of array tid / KC of the pair
 
-  auto load_stage = [&](int s) {
-    int r, ap, kci, nk;
-    decode(s, r, ap, kci, nk);
+  auto load_stage = [&](Stage st) {
+    const int r = st.r, ap = st.ap, kci = st.kci, nk = st.nk;
     const int kc0 = kci * KC;
     if (ap == 0 || nk > 1) {
       if (CONV) {
@@ -311,15 +326,27 @@ __global__ __launch_bounds__(NTHR, 2) void k_xbar_vmm(VmmArgs va) {
     }
     const int64_t arr0 = ((int64_t)c * ms.R + r) * ms.A + 2 * ap;
     __amdgpu_buffer_rsrc_t gsrc = uniform_rsrc(va.gpt + arr0 * tile_elems, (int64_t)2 * tile_elems * 4);
+    if (kc0 + KC <= ms.Mp) {
+      // a full chunk: every load is inside the pair's G'
 #pragma unroll
-    for (int it = 0; it < GV4; ++it) {
-      const int e4 = tid + NTHR * it;
-      const int p = e4 / (BN * (KC / 4));
-      const int rm = e4 % (BN * (KC / 4));
-      const int n = rm / (KC / 4), k4 = rm % (KC / 4);
-      const int kidx = kc0 + 4 * k4;
-      const int off = kidx < ms.Mp ? (p * tile_elems + (n0 + n) * ms.Mp + kidx) * 4 : kOob;
-      gr[it] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(gsrc, off, 0, 0));
+      for (int it = 0; it < GV4; ++it) {
+        const int p = it / (BN / 16), nb = 16 * (it % (BN / 16));
+        const int soff =
+            __builtin_amdgcn_readfirstlane((p * tile_elems + (n0 + nb) * ms.Mp + kc0) * 4);
+        gr[it] = __builtin_bit_cast(f32x4,
+                                    __builtin_amdgcn_raw_buffer_load_b128(gsrc, goff_v, soff, 0));
+      }
+    } else {
+#pragma unroll
+      for (int it = 0; it < GV4; ++it) {
+        const int e4 = tid + NTHR * it;
+        const int p = e4 / (BN * (KC / 4));
+        const int rm = e4 % (BN * (KC / 4));
+        const int n = rm / (KC / 4), k4 = rm % (KC / 4);
+        const int kidx = kc0 + 4 * k4;
+        const int off = kidx < ms.Mp ? (p * tile_elems + (n0 + n) * ms.Mp + kidx) * 4 : kOob;
+        gr[it] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(gsrc, off, 0, 0));
+      }
     }
     if (LDAC && tid < 2 * KC) {
       const int kidx = kc0 + (tid & (KC - 1));
@@ -327,9 +354,8 @@ __global__ __launch_bounds__(NTHR, 2) void k_xbar_vmm(VmmArgs va) {
     }
   };
 
-  auto store_stage = [&](int s) {
-    int r, ap, kci, nk;
-    decode(s, r, ap, kci, nk);
+  auto store_stage = [&](Stage st) {
+    const int r = st.r, ap = st.ap, kci = st.kci, nk = st.nk;
     if (ap == 0 || nk > 1) {
       if (CONV) {
         // inputs past the tile's or the layer's end are 0 (only in a chunk
@@ -376,15 +402,17 @@ __global__ __launch_bounds__(NTHR, 2) void k_xbar_vmm(VmmArgs va) {
       for (int v = 0; v < 4; ++v) { iacc[mt][nt][v] = 0; facc[mt][nt][v] = 0.0f; }
   f32x4 acc[2][MT][NT];
 
-  if (n_stages > 0) load_stage(0);
+  Stage cur = first_stage();
+  if (n_stages > 0) load_stage(cur);
   for (int s = 0; s < n_stages; ++s) {
-    int r, ap, kci, nk;
-    decode(s, r, ap, kci, nk);
+    const int r = cur.r, ap = cur.ap, kci = cur.kci, nk = cur.nk;
+    const Stage nxt = next_stage(cur);
     const int kc0 = kci * KC;
     __syncthreads();
-    store_stage(s);
+    store_stage(cur);
     __syncthreads();
-    if (s + 1 < n_stages) load_stage(s + 1);
+    if (s + 1 < n_stages) load_stage(nxt);
+    cur = nxt;
     if (kci == 0) {
 #pragma unroll
       for (int p = 0; p < 2; ++p)
@@ -486,8 +514,8 @@ __global__ __launch_bounds__(NTHR, 2) void k_xbar_vmm(VmmArgs va) {
       if (bv >= va.Bv) continue;
       int64_t row_base;
       if (va.hw_out > 0) {
-        const int64_t img = bv / va.hw_out;
-        row_base = img * ms.Q * va.hw_out + (bv - img * va.hw_out);
+        const int img = (int)div_by((uint32_t)bv, va.fd_hw);   // hw_out = H_out W_out
+        row_base = (int64_t)img * ms.Q * va.hw_out + (bv - (int64_t)img * va.hw_out);
       } else {
         row_base = bv * ms.Q;
       }
@@ -821,6 +849,8 @@ hipError_t launch_xbar_vmm(const MapScalars& ms, const PeriphScalars& ps, const 
   va.dbg_code = vl.dbg_code;
   va.ktab = vl.ktab;
   va.gload = vl.gload;
+  va.fd_hw = fast_div((uint32_t)(va.cg.ho * va.cg.wo));
+  va.fd_wo = fast_div((uint32_t)va.cg.wo);
   const int bn = pick_bn(ms.Np);
   const bool debug = vl.dbg_I != nullptr || vl.dbg_code != nullptr;
   va.n_cb = col_blocks(ms, bn, debug);
