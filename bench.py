@@ -47,7 +47,7 @@ FP32_MFMA_PEAK_TFLOPS = 157.3   # MI355X dense fp32 matrix
 # FETCH_SIZE / WRITE_SIZE counters of this kernel version, each scaled by what
 # the counter reads for a plain 2 GiB copy (fetch x 2.000, write x 1.000);
 # the summary and its commands are in the repository's profiles folder
-VMM_TRAFFIC_BYTES = 2.0 * 29888 * 1024 + 48362 * 1024
+VMM_TRAFFIC_BYTES = 2.0 * 29835 * 1024 + 42727 * 1024
 FP64_PEAK_TFLOPS = 78.6         # MI355X fp64 (vector and matrix)
 HBM_PEAK_GBS = 8000.0
 
@@ -338,6 +338,47 @@ def bench_stack(args):
     print(json.dumps(out), flush=True)
 
 
+def ideal_fp32_leg(torch, cv, Wd, Xd, vmm_us, eval_ms, steps):
+    """Context, not the product path: the same contraction done ideally by the
+    vendor libraries in fp32 (no TF32), timed with events on torch's stream.
+    A convolution with Q A output channels (the differential pair as one
+    layer, MIOpen) and the unrolled-patch GEMM [Bv x P] . [P x Q A]
+    (hipBLASLt).  The paper sets the slowdown of its non-ideal inference
+    against the ideal framework the same way (Sec. VIII, application-level
+    evaluation: 2.5x)."""
+    F = torch.nn.functional
+    torch.backends.cuda.matmul.allow_tf32 = False
+    torch.backends.cudnn.allow_tf32 = False
+    q = Wd.shape[1]
+    w_pair = torch.cat([Wd.clamp(min=0.0), (-Wd).clamp(min=0.0)], dim=1)   # P x 2Q
+    wconv = w_pair.t().contiguous().view(2 * q, cv["c_in"], cv["kh"], cv["kw"])
+    cols = F.unfold(Xd, (cv["kh"], cv["kw"]), padding=cv["pad"], stride=cv["stride"])
+    cols = cols.transpose(1, 2).reshape(-1, cols.shape[1]).contiguous()       # Bv x P
+    out = torch.empty((cols.shape[0], 2 * q), dtype=torch.float32, device=Xd.device)
+    flops = 2.0 * cols.shape[0] * cols.shape[1] * 2 * q
+
+    def timed(fn):
+        for _ in range(3):
+            fn()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record()
+        for _ in range(steps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return 1e3 * e0.elapsed_time(e1) / steps
+
+    conv_us = timed(lambda: F.conv2d(Xd, wconv, stride=cv["stride"], padding=cv["pad"]))
+    gemm_us = timed(lambda: torch.matmul(cols, w_pair, out=out))
+    return {"what": "ideal fp32 layer of the same MACs by the vendor libraries (context)",
+            "conv2d_us": conv_us, "conv2d_tflops": flops / conv_us * 1e-6,
+            "gemm_us": gemm_us, "gemm_tflops": flops / gemm_us * 1e-6,
+            "xbar_vmm_over_gemm": vmm_us / gemm_us,
+            "eval_over_conv2d": 1e3 * eval_ms / conv_us}
+
+
 def retrain_leg(args, torch, rxnn, wl, L, pp, cv, Wd, Xd, Yd, stream):
     """K re-training steps of the convolution: rebuild G' from the weights,
     the crossbar forward pass, and the backward pass (dX, dW) of a seeded
@@ -497,6 +538,7 @@ def main():
     build = {"us_per_step": build_us, "bound": "alu", "achieved": b_ach,
              "peak": FP64_PEAK_TFLOPS, "unit": "TFLOP/s", "frac": b_ach / FP64_PEAK_TFLOPS}
 
+    ideal = ideal_fp32_leg(torch, cv, Wd, Xd, vmm_us, eval_ms, args.steps)
     if args.copy_probe:
         copy_probe(torch, dev)
     retrain = retrain_leg(args, torch, rxnn, wl, L, pp, cv, Wd, Xd, Yd, stream) \
@@ -525,6 +567,7 @@ def main():
         "roofline": roof,
         "build": build,
         "eval_only": {"ms": eval_ms, "value": macs / (eval_ms * 1e-3), "unit": "MAC/s"},
+        "ideal_fp32": ideal,
         "kernels": kern,
         "kernels_pass": "a second pass of the same steps with every launch timed",
         "wall_s_timed": wall,
