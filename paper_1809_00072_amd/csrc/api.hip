@@ -359,8 +359,7 @@ hipError_t build_gprime(rxnn_layer* L, const float* W, hipStream_t s) {
     if (ms.wmax_fixed > 0.0f) {
       e = launch_fill_u32((unsigned*)L->d_wmax, 1, __builtin_bit_cast(unsigned, ms.wmax_fixed), s);
     } else {
-      e = launch_fill_u32((unsigned*)L->d_wmax, 1, 0u, s);
-      if (e == hipSuccess) e = launch_absmax(W, ms.P * ms.Q, (unsigned*)L->d_wmax, s);
+      e = launch_absmax(W, ms.P * ms.Q, (unsigned*)L->d_wmax, s);
     }
   }
   if (e == hipSuccess) {
@@ -542,7 +541,10 @@ rxnn_status rxnn_map_layer(const rxnn_xbar_params* params, const float* W, int64
   ms.d_wmax = L->d_wmax;
   L->ms = ms;
   L->magic = kLayerMagic;
-  hipError_t e = build_gprime(L, W, (hipStream_t)stream);
+  // the w_max reduction's accumulator and ticket counter start at zero (it
+  // leaves them so after every call)
+  hipError_t e = launch_fill_u32((unsigned*)L->d_wmax, 4, 0u, (hipStream_t)stream);
+  if (e == hipSuccess) e = build_gprime(L, W, (hipStream_t)stream);
   if (e != hipSuccess) {
     release_buffers(L);
     return fail(RXNN_EHIP, "mapping launch failed: %s", hipGetErrorString(e));

@@ -80,7 +80,7 @@ struct rxnn_layer {
   rxnn_xbar_params params;
   rxnn::MapScalars ms;
   float* gpt;          // G' of every array, [C][R][A][Np][Mp] fp32, transposed per array
-  float* d_wmax;       // one float
+  float* d_wmax;       // [0] w_max; [1], [2] accumulator and ticket counter of its reduction
   void* ws;            // scratch of the evaluation calls
   size_t ws_bytes;
   bool ws_dirty;       // ws may hold non-zero words (new, or a call did not finish)

@@ -224,6 +224,12 @@ __global__ __launch_bounds__(TG* TG) void k_gprime_build(MapScalars ms, const fl
 
 // max |W| as the bit pattern of a non-negative float (ordered like the
 // value): wave then workgroup reduction, one atomic per workgroup
+// out[0] = max |W| as fp32 bits (non-negative floats order like their bits),
+// in one launch: every workgroup folds its maximum into out[1] and takes a
+// ticket from out[2]; the workgroup with the last ticket moves the maximum to
+// out[0].  Both words are left at zero for the next call (atomicInc wraps the
+// ticket counter at the grid size; the last workgroup swaps the maximum out),
+// so they only need clearing once, when the buffer is allocated.
 __global__ __launch_bounds__(256) void k_absmax(const float* __restrict__ W, int64_t n,
                                                 unsigned* out) {
   __shared__ unsigned wm[4];
@@ -234,7 +240,14 @@ __global__ __launch_bounds__(256) void k_absmax(const float* __restrict__ W, int
   for (int off = 32; off > 0; off >>= 1) m = max(m, (unsigned)__shfl_xor((int)m, off, 64));
   if ((threadIdx.x & 63) == 0) wm[threadIdx.x >> 6] = m;
   __syncthreads();
-  if (threadIdx.x == 0) atomicMax(out, max(max(wm[0], wm[1]), max(wm[2], wm[3])));
+  if (threadIdx.x == 0) {
+    atomicMax(&out[1], max(max(wm[0], wm[1]), max(wm[2], wm[3])));
+    __threadfence();
+    if (atomicInc(&out[2], gridDim.x - 1) == gridDim.x - 1) {
+      __threadfence();
+      out[0] = atomicExch(&out[1], 0u);
+    }
+  }
 }
 
 __global__ void k_fill_u32(unsigned* p, int64_t n, unsigned v) {

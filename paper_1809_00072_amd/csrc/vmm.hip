@@ -107,8 +107,9 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t uniform_rsrc(const void* p, in
 // n_out: rows Bv (FC; cg.c_in = P, cg.wp = row stride of V) or planes n c_in
 // (convolution)
 template <bool CONV>
-__global__ __launch_bounds__(256) void k_dac(PeriphScalars ps, ConvGeom cg, const float* X,
-                                             float* V, int64_t n_out) {
+__global__ __launch_bounds__(256) void k_dac(PeriphScalars ps, ConvGeom cg,
+                                             const float* __restrict__ X, float* __restrict__ V,
+                                             int64_t n_out) {
   __shared__ float lut[256];
   if (ps.dac_bits > 0) {
     const int L = ps.dac_levels;
@@ -126,17 +127,30 @@ __global__ __launch_bounds__(256) void k_dac(PeriphScalars ps, ConvGeom cg, cons
     return fmaxf(x, 0.0f) * ps.s_v_ideal;
   };
   if (CONV) {
-    // planes (img, ci) over the blocks; threads stride over the padded plane
+    // planes (img, ci) over the blocks; the waves take the padded rows in
+    // turn, their lanes run along the row (coalesced, no index division)
     const int plane_p = cg.hp * cg.wp;
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, nwaves = blockDim.x >> 6;
     for (int64_t plane = blockIdx.x; plane < n_out; plane += gridDim.x) {
       const float* Xp = X + plane * cg.h * cg.w;
       float* Vp = V + plane * plane_p;
-      for (int e = threadIdx.x; e < plane_p; e += blockDim.x) {
-        const int yp = e / cg.wp, xp = e - yp * cg.wp;
-        const int iy = yp - cg.pad, ix = xp - cg.pad;
-        float x = 0.0f;
-        if (iy >= 0 && iy < cg.h && ix >= 0 && ix < cg.w) x = Xp[iy * cg.w + ix];
-        Vp[e] = dac(x);
+      // eight rows at a time: their loads are in flight together
+      for (int y0 = wave; y0 < cg.hp; y0 += 8 * nwaves) {
+        for (int xp = lane; xp < cg.wp; xp += 64) {
+          const int ix = xp - cg.pad;
+          const bool col_in = ix >= 0 && ix < cg.w;
+          float x[8];
+#pragma unroll
+          for (int j = 0; j < 8; ++j) {
+            const int iy = y0 + j * nwaves - cg.pad;
+            x[j] = (col_in && iy >= 0 && iy < cg.h) ? Xp[iy * cg.w + ix] : 0.0f;
+          }
+#pragma unroll
+          for (int j = 0; j < 8; ++j) {
+            const int yp = y0 + j * nwaves;
+            if (yp < cg.hp) Vp[yp * cg.wp + xp] = dac(x[j]);
+          }
+        }
       }
     }
   } else {

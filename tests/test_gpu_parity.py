@@ -268,6 +268,25 @@ def test_gprime_fixed_wmax():
         check_gprime(L.gprime(r, c, 1), g[1])
 
 
+@pytest.mark.parametrize("P,Q", [(30, 30), (2048, 1536)])   # one workgroup; 512 workgroups
+def test_wmax_over_remaps(P, Q):
+    """w_max = max |W| on every remap, growing and shrinking: the single-launch
+    reduction leaves its accumulator and ticket counter cleared after each call."""
+    say("w_max over remaps", P, Q)
+    rng = np.random.default_rng(P)
+    W = rng.normal(0, 0.05, size=(P, Q)).astype(np.float32)
+    W[P // 2, Q // 3] = 0.9
+    L = rxnn.map_layer(dev(W), wl.xbar(64, 64, 2.5))
+    assert L.w_max() == np.float32(0.9)
+    for scale in (0.25, 2.0, 0.5, 1.0):
+        Ws = (W * np.float32(scale)).astype(np.float32)
+        rxnn.remap_layer(L, dev(Ws))
+        assert L.w_max() == np.max(np.abs(Ws)), scale
+    rxnn.remap_layer(L, dev(-W))
+    assert L.w_max() == np.float32(0.9)
+    L.free()
+
+
 # ---------------------------------------------------------------------------
 # FC evaluation
 # ---------------------------------------------------------------------------
