@@ -261,8 +261,9 @@ rxnn_status run_vmm(const rxnn_layer* L, const PeriphScalars& ps, const float* X
       Lm->gload_valid = true;
     }
   }
+  const bool grp = use_groups(ms, ps, dbgI || dbgC);
   VmmPlan plan{0, 0, 0};
-  if (!(dbgI || dbgC)) plan = vmm_plan(ms, ps, Bv, conv != nullptr);
+  if (!(dbgI || dbgC)) plan = vmm_plan(ms, ps, Bv, conv != nullptr, grp);
   const int workers = plan.workers;
   int32_t* iacc_ws = nullptr;
   if (workers > 0) {
@@ -303,6 +304,7 @@ rxnn_status run_vmm(const rxnn_layer* L, const PeriphScalars& ps, const float* X
   vl.dbg_code = dbgC;
   vl.ktab = ktab;
   vl.gload = L->gload;
+  vl.grp = grp;
   // The shared-tile units add into a zeroed workspace.  The finish kernel
   // zeroes again every word it reads, and no other word is ever written, so
   // the workspace is cleared only when new or after a call that did not end.
@@ -614,8 +616,9 @@ rxnn_status rxnn_conv_layer(const rxnn_layer* layer, const rxnn_periph_params* p
   // patch-column table (per row tile and input: byte offset in the window of
   // the padded input), rebuilt when the geometry changes
   {
-    const int key[6] = {cd.c_in, cd.h, cd.w, cd.kh, cd.kw, cd.pad};
-    const int64_t n = ktab_entries(ms);
+    const bool grp = use_groups(ms, ps, false);
+    const int key[7] = {cd.c_in, cd.h, cd.w, cd.kh, cd.kw, cd.pad, grp ? 1 : 0};
+    const int64_t n = ktab_entries(ms, grp);
     if (!L->ktab || memcmp(key, L->ktab_key, sizeof key) != 0) {
       if (L->ktab_cap < n) {
         if (L->ktab) HIP_TRY(hipFree(L->ktab));
@@ -631,7 +634,7 @@ rxnn_status rxnn_conv_layer(const rxnn_layer* layer, const rxnn_periph_params* p
       }
       {
         ProfScope t("ktab", s);
-        HIP_TRY(launch_conv_ktab(ms, cd, L->ktab, s));
+        HIP_TRY(launch_conv_ktab(ms, cd, grp, L->ktab, s));
       }
       memcpy(L->ktab_key, key, sizeof key);
     }

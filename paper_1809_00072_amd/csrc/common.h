@@ -89,7 +89,7 @@ struct rxnn_layer {
   int nd_bs;           // side of the blocks reduced in LDS
   int* ktab;           // patch-column table of the last convolution geometry (or null)
   int64_t ktab_cap;    // entries allocated
-  int ktab_key[6];     // c_in, h, w, kh, kw, pad the table was built for
+  int ktab_key[7];     // c_in, h, w, kh, kw, pad, grouped walk the table was built for
   float* vbuf;         // DAC output of the current call (padded for a convolution)
   size_t vbuf_bytes;
   float* d_vf;         // the layer's copy of the variation factors (or null)
@@ -127,6 +127,7 @@ struct VmmLaunch {
   int32_t* dbg_code;    // [R][C][A][Bv][N] or null
   const int* ktab;      // conv: patch-column table
   const float* gload;   // divider DAC: row loads [C][R][A][Mp]
+  bool grp;             // grouped mode (use_groups)
 };
 // Schedule of the evaluation kernel.  workers = 0: one workgroup per tile.
 // workers > 0: persistent workgroups; tiles [0, dp_tiles) are whole-tile work,
@@ -139,8 +140,11 @@ struct VmmPlan {
 };
 hipError_t launch_xbar_vmm(const MapScalars& ms, const PeriphScalars& ps, const float* gpt,
                            const VmmLaunch& vl, const VmmPlan& plan, hipStream_t s);
-int ktab_entries(const MapScalars& ms);
-hipError_t launch_conv_ktab(const MapScalars& ms, const rxnn_conv_desc& cd, int* tab,
+// grouped evaluation: 2 x 2 arrays of 32 x 32 crossbars walked as one 64 x 64
+// tile (the patch-column table follows the walk)
+bool use_groups(const MapScalars& ms, const PeriphScalars& ps, bool debug);
+int ktab_entries(const MapScalars& ms, bool grp);
+hipError_t launch_conv_ktab(const MapScalars& ms, const rxnn_conv_desc& cd, bool grp, int* tab,
                             hipStream_t s);
 // DAC output: FC rows of fc_ldv(ms) floats (zero past P); conv the input with
 // pad pixels on every side
@@ -151,7 +155,8 @@ hipError_t launch_dac(const MapScalars& ms, const PeriphScalars& ps,
                       hipStream_t s);
 hipError_t launch_finish(const MapScalars& ms, const PeriphScalars& ps, int32_t* iacc,
                          int64_t row0, int64_t Bv, float* Y, int64_t hw_out, hipStream_t s);
-VmmPlan vmm_plan(const MapScalars& ms, const PeriphScalars& ps, int64_t Bv, bool conv);
+VmmPlan vmm_plan(const MapScalars& ms, const PeriphScalars& ps, int64_t Bv, bool conv,
+                 bool grp);
 // row loads of every array: gload[arr][m] = sum over columns of G'[arr][m][.]
 hipError_t launch_gload(const MapScalars& ms, const float* gpt, float* gload, hipStream_t s);
 

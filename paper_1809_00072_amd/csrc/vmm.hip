@@ -64,8 +64,16 @@ struct ConvGeom {
   int c_in, h, w, kh, kw, stride, pad, ho, wo, hp, wp;   // hp, wp: padded input sides
 };
 
+// Tiles as the evaluation kernel walks them: the layer's own (R, C, M, N,
+// Mp, Np), or, for 32 x 32 crossbars, groups of 2 x 2 arrays seen as one
+// 64 x 64 tile (grouped mode).
+struct TileGeo {
+  int R, C, M, N, Mp, Np;
+};
+
 struct VmmArgs {
   MapScalars ms;
+  TileGeo tg;
   PeriphScalars ps;
   ConvGeom cg;
   const float* gpt;
@@ -166,7 +174,11 @@ __global__ __launch_bounds__(256) void k_dac(PeriphScalars ps, ConvGeom cg,
 // the pair converts them with its rows' loads, staged per chunk as
 // h_p[k] = (g_pd + G_Load,p,k) L / (g_on V_DD):
 //   V = c / (c / V_DD + h_p[k]) = V_DD g(c) / (g(c) + g_pd + G_Load).
-template <int BN, bool CONV, bool QADC, bool DEBUG, bool LDAC>
+// GRP (grouped mode, 32 x 32 crossbars): a tile of the walk is 64 x 64 and
+// holds the arrays of row tiles 2 r, 2 r + 1 and column tiles 2 c, 2 c + 1;
+// a stage stages all four arrays of each side of the pair, and the ADC runs
+// after each physical row tile's 32 inputs.
+template <int BN, bool CONV, bool QADC, bool DEBUG, bool LDAC, bool GRP>
 __global__ __launch_bounds__(NTHR, 2) void k_xbar_vmm(VmmArgs va) {
   constexpr int NT = BN / 16;   // column fragments per wave
   constexpr int MT = 2;         // row fragments per wave (32 rows)
@@ -176,12 +188,14 @@ __global__ __launch_bounds__(NTHR, 2) void k_xbar_vmm(VmmArgs va) {
   __shared__ __attribute__((aligned(16))) float Hs[LDAC ? 2 * KC : 4];
   extern __shared__ float2 adct[];   // ADC table, n_buckets + 2 entries
 
+  static_assert(!GRP || (BN == 64 && !DEBUG && !LDAC), "grouped mode: 64-wide blocks only");
   const MapScalars& ms = va.ms;
+  const TileGeo& tg = va.tg;
   const PeriphScalars& ps = va.ps;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int g = lane >> 4, li = lane & 15;
-  const int nblk_per_tile = ms.Np / BN;
+  const int nblk_per_tile = tg.Np / BN;
 
   // ---- ADC table ------------------------------------------------------------
   // Thresholds t_1 .. t_L = fp32(I_FS phi((k - 1/2) / L)) (fp64 formula), held
@@ -268,10 +282,10 @@ __global__ __launch_bounds__(NTHR, 2) void k_xbar_vmm(VmmArgs va) {
   const int n_pairs = ms.A / 2;
   // Stages run over (row tile, pair, chunk).  Chunks that hold only padded
   // inputs (V = 0) are skipped: only the last row tile has them.
-  const int nkc = (ms.Mp + KC - 1) / KC;
-  const int nkc_last = min(nkc, (int)((ms.P - (int64_t)(ms.R - 1) * ms.M + KC - 1) / KC));
+  const int nkc = (tg.Mp + KC - 1) / KC;
+  const int nkc_last = min(nkc, (int)((ms.P - (int64_t)(tg.R - 1) * tg.M + KC - 1) / KC));
   const int per_r = n_pairs * nkc;
-  const int n_stages = r_end == ms.R ? (r_end - 1 - r_begin) * per_r + n_pairs * nkc_last
+  const int n_stages = r_end == tg.R ? (r_end - 1 - r_begin) * per_r + n_pairs * nkc_last
                                      : (r_end - r_begin) * per_r;
   const int tile_elems = ms.Np * ms.Mp;
   // Stages in order: row tile r, then pair ap, then chunk kci of the nk
@@ -280,7 +294,7 @@ __global__ __launch_bounds__(NTHR, 2) void k_xbar_vmm(VmmArgs va) {
     int r, ap, kci, nk;
   };
   auto first_stage = [&]() {
-    return Stage{r_begin, 0, 0, r_begin == ms.R - 1 ? nkc_last : nkc};
+    return Stage{r_begin, 0, 0, r_begin == tg.R - 1 ? nkc_last : nkc};
   };
   auto next_stage = [&](Stage t) {
     if (++t.kci == t.nk) {
@@ -288,7 +302,7 @@ __global__ __launch_bounds__(NTHR, 2) void k_xbar_vmm(VmmArgs va) {
       if (++t.ap == n_pairs) {
         t.ap = 0;
         ++t.r;
-        t.nk = t.r == ms.R - 1 ? nkc_last : nkc;
+        t.nk = t.r == tg.R - 1 ? nkc_last : nkc;
       }
     }
     return t;
@@ -298,6 +312,11 @@ __global__ __launch_bounds__(NTHR, 2) void k_xbar_vmm(VmmArgs va) {
   // tid / 16 + 16 j of array p of the pair, j + p BN / 16 = it; only the
   // column and array move with it, so they go into the uniform offset
   const int goff_v = ((tid >> 4) * ms.Mp + 4 * (tid & 15)) * 4;
+  // grouped mode (32 x 32 arrays of 1024 elements): input 4 (tid % 16) of the
+  // group is in row tile 2 r + (tid % 16) / 8; that array sits A arrays after
+  // the first row tile's
+  const int goff_g = ((((tid & 15) >> 3) * ms.A * tile_elems) + (tid >> 4) * 32 +
+                      4 * (tid & 7)) * 4;
 
   float xr[XPT];
   f32x4 gr[GV4];
@@ -326,7 +345,7 @@ __global__ __launch_bounds__(NTHR, 2) void k_xbar_vmm(VmmArgs va) {
         // 16 bytes per lane; V is zero past P, inputs past the tile's M meet
         // zero G' rows or G' loads past the tile; rows past the batch are
         // beyond the descriptor and read 0
-        const int soff = __builtin_amdgcn_readfirstlane((r * ms.M + kc0) * 4);
+        const int soff = __builtin_amdgcn_readfirstlane((r * tg.M + kc0) * 4);
 #pragma unroll
         for (int it = 0; it < XPT / 4; ++it) {
           const f32x4 x4 = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(
@@ -337,6 +356,24 @@ __global__ __launch_bounds__(NTHR, 2) void k_xbar_vmm(VmmArgs va) {
           xr[4 * it + 3] = x4[3];
         }
       }
+    }
+    if (GRP) {
+      // the pair's arrays of row tiles 2 r, 2 r + 1 and column tiles 2 c,
+      // 2 c + 1; a missing row or column tile (odd R or C) reads either zero
+      // (past the end of G') or a real array whose inputs are zero
+      const int64_t a0 = ((int64_t)(2 * c) * ms.R + 2 * r) * ms.A + 2 * ap;
+      const int64_t left = ((int64_t)ms.C * ms.R * ms.A - a0) * tile_elems * 4;
+      const __amdgpu_buffer_rsrc_t gq =
+          uniform_rsrc(va.gpt + a0 * tile_elems, min(left, (int64_t)0x7fffffff));
+#pragma unroll
+      for (int it = 0; it < GV4; ++it) {
+        const int p = it / 4, dc = (it % 4) >> 1, nb = 16 * (it & 1);
+        const int soff = __builtin_amdgcn_readfirstlane(
+            (((dc * ms.R * ms.A) + p) * tile_elems + nb * 32) * 4);
+        gr[it] = __builtin_bit_cast(f32x4,
+                                    __builtin_amdgcn_raw_buffer_load_b128(gq, goff_g, soff, 0));
+      }
+      return;
     }
     const int64_t arr0 = ((int64_t)c * ms.R + r) * ms.A + 2 * ap;
     __amdgpu_buffer_rsrc_t gsrc = uniform_rsrc(va.gpt + arr0 * tile_elems, (int64_t)2 * tile_elems * 4);
@@ -375,7 +412,7 @@ __global__ __launch_bounds__(NTHR, 2) void k_xbar_vmm(VmmArgs va) {
         // inputs past the tile's or the layer's end are 0 (only in a chunk
         // that is not full, a uniform condition)
         const int kc0 = kci * KC;
-        const int nvalid = min(ms.M - kc0, (int)(ms.P - (int64_t)r * ms.M) - kc0);
+        const int nvalid = min(tg.M - kc0, (int)(ms.P - (int64_t)r * tg.M) - kc0);
         if (nvalid < KC) {
 #pragma unroll
           for (int q = 0; q < XPT / 4; ++q)
@@ -427,14 +464,15 @@ __global__ __launch_bounds__(NTHR, 2) void k_xbar_vmm(VmmArgs va) {
     __syncthreads();
     if (s + 1 < n_stages) load_stage(nxt);
     cur = nxt;
-    if (kci == 0) {
+    auto zero_acc = [&]() __attribute__((always_inline)) {
 #pragma unroll
       for (int p = 0; p < 2; ++p)
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
           for (int nt = 0; nt < NT; ++nt) acc[p][mt][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
-    }
+    };
+    if (kci == 0) zero_acc();
     auto block = [&](int kb) {
       f32x4 af[MT];
 #pragma unroll
@@ -469,45 +507,60 @@ __global__ __launch_bounds__(NTHR, 2) void k_xbar_vmm(VmmArgs va) {
                   vf[mt][ss], bf[nt][ss], acc[p][mt][nt], 0, 0, 0);
       }
     };
-    const int kb_end = min(KC, ms.Mp - kc0);
-    for (int kb = 0; kb < kb_end; kb += 16) block(kb);
-    if (kci != nk - 1) continue;
-
-    // ---- ADC and digital accumulation -------------------------------------
-    const int sh = ms.slice_bits * ap;   // the pair's weight is +-2^sh
+    // ---- ADC and digital accumulation (physical row tile rp) ----------------
+    auto convert = [&](int rp) __attribute__((always_inline)) {
+      const int sh = ms.slice_bits * ap;   // the pair's weight is +-2^sh
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
+      for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-      for (int nt = 0; nt < NT; ++nt)
+        for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
-        for (int v = 0; v < 4; ++v) {
-          const float Ip = acc[0][mt][nt][v], In = acc[1][mt][nt][v];
-          int cp = 0, cn = 0;
-          if (QADC) {
-            cp = adc(Ip);
-            cn = adc(In);
-            iacc[mt][nt][v] += (cp - cn) << sh;
-          } else {
-            facc[mt][nt][v] += (float)(1 << sh) * Ip;
-            facc[mt][nt][v] += -(float)(1 << sh) * In;
-          }
-          if (DEBUG) {
-            const int64_t bv = b0 + wave * 32 + mt * 16 + 4 * g + v;
-            const int n = n0 + nt * 16 + li;
-            if (bv < va.Bv && n < ms.N) {
-              const int64_t slot = (((int64_t)r * ms.C + c) * ms.A + 2 * ap) * va.Bv + bv;
-              if (va.dbg_I) {
-                va.dbg_I[slot * ms.N + n] = Ip;
-                va.dbg_I[(slot + va.Bv) * ms.N + n] = In;
-              }
-              if (va.dbg_code) {
-                va.dbg_code[slot * ms.N + n] = cp;
-                va.dbg_code[(slot + va.Bv) * ms.N + n] = cn;
+          for (int v = 0; v < 4; ++v) {
+            const float Ip = acc[0][mt][nt][v], In = acc[1][mt][nt][v];
+            int cp = 0, cn = 0;
+            if (QADC) {
+              cp = adc(Ip);
+              cn = adc(In);
+              iacc[mt][nt][v] += (cp - cn) << sh;
+            } else {
+              facc[mt][nt][v] += (float)(1 << sh) * Ip;
+              facc[mt][nt][v] += -(float)(1 << sh) * In;
+            }
+            if (DEBUG) {
+              const int64_t bv = b0 + wave * 32 + mt * 16 + 4 * g + v;
+              const int n = n0 + nt * 16 + li;
+              if (bv < va.Bv && n < ms.N) {
+                const int64_t slot = (((int64_t)rp * ms.C + c) * ms.A + 2 * ap) * va.Bv + bv;
+                if (va.dbg_I) {
+                  va.dbg_I[slot * ms.N + n] = Ip;
+                  va.dbg_I[(slot + va.Bv) * ms.N + n] = In;
+                }
+                if (va.dbg_code) {
+                  va.dbg_code[slot * ms.N + n] = cp;
+                  va.dbg_code[(slot + va.Bv) * ms.N + n] = cn;
+                }
               }
             }
           }
-        }
-  }
+    };
+    if (GRP) {
+      // inputs 0 .. 31 belong to row tile 2 r, 32 .. 63 to row tile 2 r + 1
+      // (absent when R is odd and r is the last)
+      const int nh = 2 * r + 1 < ms.R ? 2 : 1;
+#pragma unroll 1
+      for (int h = 0; h < nh; ++h) {
+        if (h) zero_acc();
+        block(32 * h);
+        block(32 * h + 16);
+        convert(2 * r + h);
+      }
+      continue;
+    }
+    const int kb_end = min(KC, tg.Mp - kc0);
+    for (int kb = 0; kb < kb_end; kb += 16) block(kb);
+    if (kci != nk - 1) continue;
+    convert(r);
+}
 
   // ---- output ---------------------------------------------------------------
   const double wmax = ms.wmax_fixed > 0.0f ? (double)ms.wmax_fixed : (double)*ms.d_wmax;
@@ -536,8 +589,8 @@ __global__ __launch_bounds__(NTHR, 2) void k_xbar_vmm(VmmArgs va) {
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt) {
         const int n = n0 + nt * 16 + li;
-        const int64_t q = (int64_t)c * ms.N + n;
-        if (n >= ms.N || q >= ms.Q) continue;
+        const int64_t q = (int64_t)c * tg.N + n;
+        if (n >= tg.N || q >= ms.Q) continue;
         const int64_t e = row_base + q * qstride;
         if (atomic) {
           atomicAdd(&va.iacc[bv * ms.Q + q], iacc[mt][nt][v]);
@@ -552,7 +605,7 @@ __global__ __launch_bounds__(NTHR, 2) void k_xbar_vmm(VmmArgs va) {
                      __attribute__((always_inline)) {
     // column blocks: every block of a full column tile, and of the last tile
     // only those that hold real output columns (padded columns are discarded)
-    const int c = min(cb / nblk_per_tile, ms.C - 1);
+    const int c = min(cb / nblk_per_tile, tg.C - 1);
     run_tile((int64_t)bx * BM, c, (cb - c * nblk_per_tile) * BN, r_begin, r_end, atomic);
   };
   // One workgroup per tile, or persistent workers: worker w first takes the
@@ -562,14 +615,14 @@ __global__ __launch_bounds__(NTHR, 2) void k_xbar_vmm(VmmArgs va) {
   int64_t u, u1, t_dp, dp_end;
   bool shared_units = false;
   if (va.workers == 0) {
-    u = ((int64_t)blockIdx.x * va.n_cb + blockIdx.y) * ms.R;
-    u1 = u + ms.R;
+    u = ((int64_t)blockIdx.x * va.n_cb + blockIdx.y) * tg.R;
+    u1 = u + tg.R;
     t_dp = dp_end = 0;
   } else {
     const int64_t n_tiles = (int64_t)((va.Bv + BM - 1) / BM) * va.n_cb;
-    const int64_t U = (n_tiles - va.dp_tiles) * ms.R;
-    u = va.dp_tiles * ms.R + U * blockIdx.x / va.workers;
-    u1 = va.dp_tiles * ms.R + U * (blockIdx.x + 1) / va.workers;
+    const int64_t U = (n_tiles - va.dp_tiles) * tg.R;
+    u = va.dp_tiles * tg.R + U * blockIdx.x / va.workers;
+    u1 = va.dp_tiles * tg.R + U * (blockIdx.x + 1) / va.workers;
     t_dp = blockIdx.x;
     dp_end = va.dp_tiles;
     shared_units = true;
@@ -581,13 +634,13 @@ __global__ __launch_bounds__(NTHR, 2) void k_xbar_vmm(VmmArgs va) {
     if (t_dp < dp_end) {
       t = t_dp;
       r0 = 0;
-      r1 = ms.R;
+      r1 = tg.R;
       atomic = false;
       t_dp += va.workers;
     } else if (u < u1) {
-      t = u / ms.R;
-      r0 = (int)(u - t * ms.R);
-      r1 = (int)min((int64_t)ms.R, r0 + (u1 - u));
+      t = u / tg.R;
+      r0 = (int)(u - t * tg.R);
+      r1 = (int)min((int64_t)tg.R, r0 + (u1 - u));
       atomic = shared_units;
       u += r1 - r0;
     } else {
@@ -652,19 +705,20 @@ __global__ __launch_bounds__(256) void k_finish_nchw(MapScalars ms, PeriphScalar
     if (q0 + i < ms.Q) Y[(img * ms.Q + q0 + i) * hw + pix] = (float)tile[t][i] * scale;
 }
 
-// Table of the patch columns of a convolution, per row tile r and tile input
-// kk < nkc KC: byte offset of input p = r M + kk inside an output pixel's
-// window of the padded input; an input past the tile or the layer gets 0 (it
-// is zeroed when staged).
-__global__ void k_conv_ktab(MapScalars ms, ConvGeom cg, int kcp, int* tab) {
-  const int64_t n = (int64_t)ms.R * kcp;
+// Table of the patch columns of a convolution, per row tile r of the walk
+// (tg: a grouped tile spans two row tiles) and tile input kk < nkc KC: byte
+// offset of input p = r M + kk inside an output pixel's window of the padded
+// input; an input past the tile or the layer gets 0 (it is zeroed when
+// staged).
+__global__ void k_conv_ktab(MapScalars ms, TileGeo tg, ConvGeom cg, int kcp, int* tab) {
+  const int64_t n = (int64_t)tg.R * kcp;
   const int khw = cg.kh * cg.kw;
   for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < n;
        e += (int64_t)gridDim.x * blockDim.x) {
     const int r = (int)(e / kcp), kk = (int)(e - (int64_t)r * kcp);
-    const int64_t p = (int64_t)r * ms.M + kk;
+    const int64_t p = (int64_t)r * tg.M + kk;
     int v = 0;
-    if (kk < ms.M && p < ms.P) {
+    if (kk < tg.M && p < ms.P) {
       const int ci = (int)(p / khw), tap = (int)(p - (int64_t)ci * khw);
       const int ky = tap / cg.kw, kx = tap - ky * cg.kw;
       v = ((ci * cg.hp + ky) * cg.wp + kx) * 4;
@@ -682,9 +736,9 @@ hipError_t allow_adc_table(K kernel) {
                              (kMaxBuckets + 2) * (int)sizeof(float2));
 }
 
-template <int BN, bool CONV, bool QADC, bool DEBUG, bool LDAC>
+template <int BN, bool CONV, bool QADC, bool DEBUG, bool LDAC, bool GRP = false>
 hipError_t launch_one(const VmmArgs& va, dim3 grid, hipStream_t s) {
-  auto kern = k_xbar_vmm<BN, CONV, QADC, DEBUG, LDAC>;
+  auto kern = k_xbar_vmm<BN, CONV, QADC, DEBUG, LDAC, GRP>;
   static const hipError_t attr = allow_adc_table(kern);
   if (attr != hipSuccess) return attr;
   const size_t shm = QADC ? (size_t)(va.ps.n_buckets + 2) * sizeof(float2) : 0;
@@ -703,7 +757,16 @@ hipError_t launch_t(const VmmArgs& va, dim3 grid, hipStream_t s, bool debug) {
 
 template <int BN>
 hipError_t launch_bn(const VmmArgs& va, dim3 grid, hipStream_t s, bool conv, bool qadc,
-                     bool debug) {
+                     bool debug, bool grp) {
+  if constexpr (BN == 64) {
+    if (grp) {
+      if (conv)
+        return qadc ? launch_one<64, true, true, false, false, true>(va, grid, s)
+                    : launch_one<64, true, false, false, false, true>(va, grid, s);
+      return qadc ? launch_one<64, false, true, false, false, true>(va, grid, s)
+                  : launch_one<64, false, false, false, false, true>(va, grid, s);
+    }
+  }
   if (conv) {
     return qadc ? launch_t<BN, true, true>(va, grid, s, debug)
                 : launch_t<BN, true, false>(va, grid, s, debug);
@@ -721,20 +784,25 @@ int pick_bn(int Np) {
 // Column blocks of the grid: every block of a full column tile, and of the
 // last tile only those holding real outputs (all of them for the debug entry,
 // which reports the padded columns' currents too).
-int col_blocks(const MapScalars& ms, int bn, bool debug) {
-  const int64_t q_last = ms.Q - (int64_t)(ms.C - 1) * ms.N;
-  const int blk_last = debug ? ms.Np / bn : (int)((q_last + bn - 1) / bn);
-  return (ms.C - 1) * (ms.Np / bn) + blk_last;
+int col_blocks(const MapScalars& ms, const TileGeo& tg, int bn, bool debug) {
+  const int64_t q_last = ms.Q - (int64_t)(tg.C - 1) * tg.N;
+  const int blk_last = debug ? tg.Np / bn : (int)((q_last + bn - 1) / bn);
+  return (tg.C - 1) * (tg.Np / bn) + blk_last;
+}
+
+TileGeo tile_geo(const MapScalars& ms, bool grp) {
+  if (grp) return TileGeo{(ms.R + 1) / 2, (ms.C + 1) / 2, 64, 64, 64, 64};
+  return TileGeo{ms.R, ms.C, ms.M, ms.N, ms.Mp, ms.Np};
 }
 
 // Workgroups of the quantising evaluation kernel resident on the device at once.
-template <int BN, bool CONV, bool LDAC>
+template <int BN, bool CONV, bool LDAC, bool GRP = false>
 int64_t slots_t(const PeriphScalars& ps) {
   int dev = 0, cus = 0, per_cu = 0;
   if (hipGetDevice(&dev) != hipSuccess) return 0;
   if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
     return 0;
-  auto kern = k_xbar_vmm<BN, CONV, true, false, LDAC>;
+  auto kern = k_xbar_vmm<BN, CONV, true, false, LDAC, GRP>;
   if (allow_adc_table(kern) != hipSuccess) return 0;
   const size_t shm = (size_t)(ps.n_buckets + 2) * sizeof(float2);
   if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void*>(kern),
@@ -750,7 +818,8 @@ int64_t slots_l(int bn, bool conv, const PeriphScalars& ps) {
   return conv ? slots_t<16, true, LDAC>(ps) : slots_t<16, false, LDAC>(ps);
 }
 
-int64_t slots_for(int bn, bool conv, const PeriphScalars& ps) {
+int64_t slots_for(int bn, bool conv, bool grp, const PeriphScalars& ps) {
+  if (grp) return conv ? slots_t<64, true, false, true>(ps) : slots_t<64, false, false, true>(ps);
   return ps.ldac ? slots_l<true>(bn, conv, ps) : slots_l<false>(bn, conv, ps);
 }
 
@@ -795,14 +864,22 @@ ConvGeom conv_geom(const rxnn_conv_desc& cd) {
 
 }  // namespace
 
-VmmPlan vmm_plan(const MapScalars& ms, const PeriphScalars& ps, int64_t Bv, bool conv) {
+// Grouped mode for 32 x 32 crossbars (not for the debug entry, whose
+// per-array outputs follow the layer's own tiles, nor for the divider DAC).
+bool use_groups(const MapScalars& ms, const PeriphScalars& ps, bool debug) {
+  return ms.M == 32 && ms.N == 32 && ms.Mp == 32 && ms.Np == 32 && !ps.ldac && !debug;
+}
+
+VmmPlan vmm_plan(const MapScalars& ms, const PeriphScalars& ps, int64_t Bv, bool conv,
+                 bool grp) {
   VmmPlan pl{0, 0, 0};
+  const TileGeo tg = tile_geo(ms, grp);
   // fp32 accumulation (ideal ADC) keeps one workgroup per tile: a fixed order
-  if (ps.adc_bits == 0 || ms.R < 2 || Bv <= 0) return pl;
-  const int bn = pick_bn(ms.Np);
-  const int n_cb = col_blocks(ms, bn, false);
+  if (ps.adc_bits == 0 || tg.R < 2 || Bv <= 0) return pl;
+  const int bn = pick_bn(tg.Np);
+  const int n_cb = col_blocks(ms, tg, bn, false);
   const int64_t tiles = ((Bv + BM - 1) / BM) * n_cb;
-  const int64_t slots = slots_for(bn, conv, ps);
+  const int64_t slots = slots_for(bn, conv, grp, ps);
   if (slots <= 0) return pl;
   // one workgroup per tile fills the last round of the GPU only partly; when
   // that wastes more than 10 %, the full rounds stay whole-tile work and the
@@ -810,7 +887,7 @@ VmmPlan vmm_plan(const MapScalars& ms, const PeriphScalars& ps, int64_t Bv, bool
   const int64_t rounds = (tiles + slots - 1) / slots;
   if ((double)tiles >= 0.9 * (double)(rounds * slots)) return pl;
   const int64_t dp = ((tiles / slots) * slots / n_cb) * n_cb;   // whole row blocks
-  const int64_t units = (tiles - dp) * ms.R;
+  const int64_t units = (tiles - dp) * tg.R;
   pl.workers = (int)(units + dp < slots ? units + dp : slots);
   pl.dp_tiles = dp;
   pl.row0 = (dp / n_cb) * BM;
@@ -865,18 +942,19 @@ hipError_t launch_xbar_vmm(const MapScalars& ms, const PeriphScalars& ps, const 
   va.gload = vl.gload;
   va.fd_hw = fast_div((uint32_t)(va.cg.ho * va.cg.wo));
   va.fd_wo = fast_div((uint32_t)va.cg.wo);
-  const int bn = pick_bn(ms.Np);
   const bool debug = vl.dbg_I != nullptr || vl.dbg_code != nullptr;
-  va.n_cb = col_blocks(ms, bn, debug);
+  va.tg = tile_geo(ms, vl.grp);
+  const int bn = pick_bn(va.tg.Np);
+  va.n_cb = col_blocks(ms, va.tg, bn, debug);
   va.workers = workers;
   va.dp_tiles = plan.dp_tiles;
   const dim3 grid = workers > 0 ? dim3((unsigned)workers)
                                 : dim3((unsigned)((vl.Bv + BM - 1) / BM), (unsigned)va.n_cb);
   const bool qadc = ps.adc_bits > 0;
   const bool conv = vl.conv != nullptr;
-  if (bn == 64) return launch_bn<64>(va, grid, s, conv, qadc, debug);
-  if (bn == 32) return launch_bn<32>(va, grid, s, conv, qadc, debug);
-  return launch_bn<16>(va, grid, s, conv, qadc, debug);
+  if (bn == 64) return launch_bn<64>(va, grid, s, conv, qadc, debug, vl.grp);
+  if (bn == 32) return launch_bn<32>(va, grid, s, conv, qadc, debug, false);
+  return launch_bn<16>(va, grid, s, conv, qadc, debug, false);
 }
 
 hipError_t launch_gload(const MapScalars& ms, const float* gpt, float* gload, hipStream_t s) {
@@ -886,15 +964,19 @@ hipError_t launch_gload(const MapScalars& ms, const float* gpt, float* gload, hi
   return hipGetLastError();
 }
 
-int ktab_entries(const MapScalars& ms) { return ms.R * (((ms.Mp + KC - 1) / KC) * KC); }
+int ktab_entries(const MapScalars& ms, bool grp) {
+  const TileGeo tg = tile_geo(ms, grp);
+  return tg.R * (((tg.Mp + KC - 1) / KC) * KC);
+}
 
-hipError_t launch_conv_ktab(const MapScalars& ms, const rxnn_conv_desc& cd, int* tab,
+hipError_t launch_conv_ktab(const MapScalars& ms, const rxnn_conv_desc& cd, bool grp, int* tab,
                             hipStream_t s) {
-  const int kcp = ((ms.Mp + KC - 1) / KC) * KC;
-  const int64_t n = (int64_t)ms.R * kcp;
+  const TileGeo tg = tile_geo(ms, grp);
+  const int kcp = ((tg.Mp + KC - 1) / KC) * KC;
+  const int64_t n = (int64_t)tg.R * kcp;
   int64_t blocks = (n + 255) / 256;
   if (blocks > 1024) blocks = 1024;
-  hipLaunchKernelGGL(k_conv_ktab, dim3((unsigned)blocks), dim3(256), 0, s, ms, conv_geom(cd),
+  hipLaunchKernelGGL(k_conv_ktab, dim3((unsigned)blocks), dim3(256), 0, s, ms, tg, conv_geom(cd),
                      kcp, tab);
   return hipGetLastError();
 }

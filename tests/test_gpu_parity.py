@@ -75,6 +75,9 @@ def compare_fc_debug(W, X, xb, pp, label):
             wsum[:, c * N:(c + 1) * N] += np.abs(Io)
         tol = 1e-4 * wsum[:, :W.shape[1]] * scale + 1e-6
         assert np.all(np.abs(Y - Yo) <= tol)
+        say(label, "crossbar_vmm")
+        Yp = rxnn.crossbar_vmm(L, pp, dev(X)).cpu().numpy()
+        assert np.all(np.abs(Yp - Yo) <= tol)
         return L, Y, Yo
     # outputs: the GPU's own codes, accumulated exactly, reproduce Y bit for bit
     aw = array_weights(A, omap.slicing(xb)[1])
@@ -299,7 +302,8 @@ def test_fc_256x128_parity():
 @pytest.mark.parametrize("P,Q,M,N,B,dac,adc", [
     (200, 70, 64, 64, 130, 4, 8),     # ragged tiles, two batch blocks + tail
     (50, 40, 16, 16, 1, 8, 8),        # one row
-    (90, 33, 32, 32, 257, 6, 6),      # N = 32 path, three batch blocks
+    (90, 33, 32, 32, 257, 6, 6),      # 32 x 32: grouped walk, odd R, three batch blocks
+    (90, 70, 32, 32, 200, 8, 8),      # 32 x 32: odd R and odd C (absent tiles of a group)
     (60, 20, 13, 10, 37, 3, 5),       # N = 10 -> 16-wide path
     (100, 70, 256, 256, 33, 8, 8),    # one 256 x 256 tile: padded chunks and column blocks
     (300, 130, 128, 128, 20, 8, 8),   # last row tile 44 inputs, last column tile 2 outputs
