@@ -203,7 +203,10 @@ rxnn_status rxnn_remap_layer(rxnn_layer* layer, const float* W, void* stream);
  *   B >= 0 (B = 0 is a no-op).
  * The layer keeps a DAC output buffer (B x (R M + 64) floats) and, when the
  * evaluation is shared across persistent workgroups, an int32 B x Q
- * workspace; both grow on demand (RXNN_ENOMEM when they cannot).
+ * workspace; both grow on demand (RXNN_ENOMEM when they cannot).  It also
+ * keeps the quantising ADC's bucket table (16 KiB, rebuilt on `stream` when
+ * the peripheral parameters change).  Calls on one layer that overlap on
+ * different streams race on these buffers.
  * RXNN_EUNSUPPORTED when P >= 2^22 (32-bit buffer offsets).
  */
 rxnn_status rxnn_crossbar_vmm(const rxnn_layer* layer, const rxnn_periph_params* periph,

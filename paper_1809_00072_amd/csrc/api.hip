@@ -202,7 +202,7 @@ std::map<std::string, std::pair<double, int64_t>> g_prof_tot;
 // Frees every device buffer of a layer and the handle itself.
 void release_buffers(rxnn_layer* L) {
   void* bufs[] = {L->gpt,  L->d_wmax, L->ws,    L->nd_ws, L->ktab,
-                  L->vbuf, L->d_vf,   L->d_lut, L->bw_ws, L->gload};
+                  L->vbuf, L->d_vf,   L->d_lut, L->bw_ws, L->gload, L->adct};
   for (void* b : bufs)
     if (b) (void)hipFree(b);
   L->magic = 0;
@@ -261,6 +261,28 @@ rxnn_status run_vmm(const rxnn_layer* L, const PeriphScalars& ps, const float* X
       Lm->gload_valid = true;
     }
   }
+  if (ps.adc_bits > 0) {
+    // the ADC's bucket table, rebuilt when the converter changes
+    rxnn_layer* Lm = const_cast<rxnn_layer*>(L);
+    const double key[5] = {(double)ps.adc_levels, (double)ps.n_buckets, ps.i_fs, ps.adc_bend,
+                           ps.bucket_w};
+    const bool current = Lm->adct && memcmp(key, Lm->adct_key, sizeof key) == 0;
+    if (!Lm->adct) {
+      void* p = nullptr;
+      if (hipMalloc(&p, (size_t)(kMaxBuckets + 2) * sizeof(float2)) != hipSuccess) {
+        (void)hipGetLastError();
+        return fail(RXNN_ENOMEM, "cannot allocate the ADC table");
+      }
+      Lm->adct = (float2*)p;
+    }
+    if (!current) {
+      {
+        ProfScope t("adc_table", s);
+        HIP_TRY(launch_adc_table(ps, Lm->adct, s));
+      }
+      memcpy(Lm->adct_key, key, sizeof key);
+    }
+  }
   const bool grp = use_groups(ms, ps, dbgI || dbgC);
   VmmPlan plan{0, 0, 0};
   if (!(dbgI || dbgC)) plan = vmm_plan(ms, ps, Bv, conv != nullptr, grp);
@@ -305,6 +327,7 @@ rxnn_status run_vmm(const rxnn_layer* L, const PeriphScalars& ps, const float* X
   vl.ktab = ktab;
   vl.gload = L->gload;
   vl.grp = grp;
+  vl.adc_tab = L->adct;
   // The shared-tile units add into a zeroed workspace.  The finish kernel
   // zeroes again every word it reads, and no other word is ever written, so
   // the workspace is cleared only when new or after a call that did not end.

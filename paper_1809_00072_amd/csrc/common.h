@@ -98,6 +98,8 @@ struct rxnn_layer {
   size_t bw_bytes;
   float* gload;        // row loads sum_j G'_ij per array, [C][R][A][Mp] (divider DAC), or null
   bool gload_valid;    // gload matches the stored G'
+  float2* adct;        // ADC bucket table of the quantising evaluation (or null)
+  double adct_key[5];  // adc_levels, n_buckets, i_fs, adc_bend, bucket_w it was built for
 };
 
 namespace rxnn {
@@ -128,6 +130,7 @@ struct VmmLaunch {
   const int* ktab;      // conv: patch-column table
   const float* gload;   // divider DAC: row loads [C][R][A][Mp]
   bool grp;             // grouped mode (use_groups)
+  const float2* adc_tab;  // quantising ADC: the bucket table of launch_adc_table
 };
 // Schedule of the evaluation kernel.  workers = 0: one workgroup per tile.
 // workers > 0: persistent workgroups; tiles [0, dp_tiles) are whole-tile work,
@@ -149,6 +152,8 @@ hipError_t launch_conv_ktab(const MapScalars& ms, const rxnn_conv_desc& cd, bool
 // DAC output: FC rows of fc_ldv(ms) floats (zero past P); conv the input with
 // pad pixels on every side
 int64_t fc_ldv(const MapScalars& ms);
+// ADC bucket table of the quantising evaluation (n_buckets + 2 float2 entries)
+hipError_t launch_adc_table(const PeriphScalars& ps, float2* tab, hipStream_t s);
 int64_t dac_elems(const MapScalars& ms, const rxnn_conv_desc* conv, int64_t Bv);
 hipError_t launch_dac(const MapScalars& ms, const PeriphScalars& ps,
                       const rxnn_conv_desc* conv, const float* X, int64_t Bv, float* V,

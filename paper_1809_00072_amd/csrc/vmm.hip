@@ -85,6 +85,7 @@ struct VmmArgs {
   float* dbg_I;
   int32_t* dbg_code;
   const int* ktab;      // conv: per (row tile, input) byte offset inside the window
+  const float2* adc_tab;  // ADC bucket table, n_buckets + 2 entries (k_adc_table)
   const float* gload;   // divider DAC: row loads [C][R][A][Mp]
   FastDiv fd_hw, fd_wo; // conv: division by H_out W_out and by W_out (product rows < 2^31)
   int n_cb;             // column blocks (tiles along y)
@@ -115,7 +116,7 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t uniform_rsrc(const void* p, in
 // n_out: rows Bv (FC; cg.c_in = P, cg.wp = row stride of V) or planes n c_in
 // (convolution)
 template <bool CONV>
-__global__ __launch_bounds__(256) void k_dac(PeriphScalars ps, ConvGeom cg,
+__global__ __launch_bounds__(256) void k_dac(PeriphScalars ps, ConvGeom cg, FastDiv fd_wp,
                                              const float* __restrict__ X, float* __restrict__ V,
                                              int64_t n_out) {
   __shared__ float lut[256];
@@ -135,30 +136,27 @@ __global__ __launch_bounds__(256) void k_dac(PeriphScalars ps, ConvGeom cg,
     return fmaxf(x, 0.0f) * ps.s_v_ideal;
   };
   if (CONV) {
-    // planes (img, ci) over the blocks; the waves take the padded rows in
-    // turn, their lanes run along the row (coalesced, no index division)
+    // planes (img, ci) over the blocks; the threads stride over the padded
+    // plane eight elements at a time, so that their loads are in flight
+    // together (row = e / wp by an invariant-divisor multiply)
     const int plane_p = cg.hp * cg.wp;
-    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, nwaves = blockDim.x >> 6;
+    const int nt = blockDim.x;
     for (int64_t plane = blockIdx.x; plane < n_out; plane += gridDim.x) {
       const float* Xp = X + plane * cg.h * cg.w;
       float* Vp = V + plane * plane_p;
-      // eight rows at a time: their loads are in flight together
-      for (int y0 = wave; y0 < cg.hp; y0 += 8 * nwaves) {
-        for (int xp = lane; xp < cg.wp; xp += 64) {
-          const int ix = xp - cg.pad;
-          const bool col_in = ix >= 0 && ix < cg.w;
-          float x[8];
+      for (int e0 = threadIdx.x; e0 < plane_p; e0 += 8 * nt) {
+        float x[8];
 #pragma unroll
-          for (int j = 0; j < 8; ++j) {
-            const int iy = y0 + j * nwaves - cg.pad;
-            x[j] = (col_in && iy >= 0 && iy < cg.h) ? Xp[iy * cg.w + ix] : 0.0f;
-          }
-#pragma unroll
-          for (int j = 0; j < 8; ++j) {
-            const int yp = y0 + j * nwaves;
-            if (yp < cg.hp) Vp[yp * cg.wp + xp] = dac(x[j]);
-          }
+        for (int j = 0; j < 8; ++j) {
+          const int e = e0 + j * nt;
+          const int yp = (int)div_by((uint32_t)e, fd_wp), xp = e - yp * cg.wp;
+          const int iy = yp - cg.pad, ix = xp - cg.pad;
+          x[j] = (e < plane_p && iy >= 0 && iy < cg.h && ix >= 0 && ix < cg.w)
+                     ? Xp[iy * cg.w + ix] : 0.0f;
         }
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+          if (e0 + j * nt < plane_p) Vp[e0 + j * nt] = dac(x[j]);
       }
     }
   } else {
@@ -167,6 +165,36 @@ __global__ __launch_bounds__(256) void k_dac(PeriphScalars ps, ConvGeom cg,
     for (int64_t b = blockIdx.x; b < n_out; b += gridDim.x)
       for (int p = threadIdx.x; p < ldv; p += blockDim.x)
         V[b * ldv + p] = p < P ? dac(X[b * P + p]) : 0.0f;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// ADC bucket table (Sec. IV-A 'Non-ideal ADC'; one workgroup).  Thresholds
+// t_1 .. t_L = fp32(I_FS phi((k - 1/2) / L)) from the fp64 formula.  Entry b:
+// c = #{k : t_k <= (b - 1) w} and t_{c+1}.  The bucket width w is at most
+// 1 / 3.25 of the smallest threshold spacing: I / w rounded in fp32 lands in
+// bucket floor(I / w) or a neighbour, which leaves at most one threshold
+// between the entry's edge and I, so code(I) = c + (I >= t_{c+1}).
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void k_adc_table(PeriphScalars ps, float2* __restrict__ tab) {
+  __shared__ float thr[257];
+  const int L = ps.adc_levels;
+  for (int k = threadIdx.x; k <= L + 1; k += blockDim.x) {
+    float t;
+    if (k == 0) t = -__builtin_inff();
+    else if (k == L + 1) t = __builtin_inff();
+    else t = (float)(ps.i_fs * bend(((double)k - 0.5) / (double)L, ps.adc_bend));
+    thr[k] = t;
+  }
+  __syncthreads();
+  for (int b = threadIdx.x; b < ps.n_buckets + 2; b += blockDim.x) {
+    const double edge = (double)(b - 1) * ps.bucket_w;
+    int lo = 0, hi = L;
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if ((double)thr[mid] <= edge) lo = mid; else hi = mid - 1;
+    }
+    tab[b] = make_float2(__int_as_float(lo), thr[lo + 1]);
   }
 }
 
@@ -197,33 +225,9 @@ __global__ __launch_bounds__(NTHR, 2) void k_xbar_vmm(VmmArgs va) {
   const int g = lane >> 4, li = lane & 15;
   const int nblk_per_tile = tg.Np / BN;
 
-  // ---- ADC table ------------------------------------------------------------
-  // Thresholds t_1 .. t_L = fp32(I_FS phi((k - 1/2) / L)) (fp64 formula), held
-  // in the G' space until staging starts.  Entry b: c = #{k : t_k <= (b - 1) w}
-  // and t_{c+1}.  The bucket width w is at most 1 / 3.25 of the smallest
-  // threshold spacing: I / w rounded in fp32 lands in bucket floor(I / w) or a
-  // neighbour, which leaves at most one threshold between the entry's edge
-  // and I, so code(I) = c + (I >= t_{c+1}).
+  // ---- ADC table (built by k_adc_table) -------------------------------------
   if (QADC) {
-    float* thr = Gs;
-    const int L = ps.adc_levels;
-    for (int k = tid; k <= L + 1; k += NTHR) {
-      float t;
-      if (k == 0) t = -__builtin_inff();
-      else if (k == L + 1) t = __builtin_inff();
-      else t = (float)(ps.i_fs * bend(((double)k - 0.5) / (double)L, ps.adc_bend));
-      thr[k] = t;
-    }
-    __syncthreads();
-    for (int b = tid; b < ps.n_buckets + 2; b += NTHR) {
-      const double edge = (double)(b - 1) * ps.bucket_w;
-      int lo = 0, hi = L;
-      while (lo < hi) {
-        const int mid = (lo + hi + 1) >> 1;
-        if ((double)thr[mid] <= edge) lo = mid; else hi = mid - 1;
-      }
-      adct[b] = make_float2(__int_as_float(lo), thr[lo + 1]);
-    }
+    for (int b = tid; b < ps.n_buckets + 2; b += NTHR) adct[b] = va.adc_tab[b];
   }
 
   const unsigned b_max = (unsigned)ps.n_buckets;
@@ -232,7 +236,7 @@ __global__ __launch_bounds__(NTHR, 2) void k_xbar_vmm(VmmArgs va) {
     const float2 e = adct[b];
     return __float_as_int(e.x) + (I >= e.y ? 1 : 0);
   };
-  __syncthreads();   // the ADC table build used the G' space
+  __syncthreads();
 
   // One tile: product rows [b0, b0 + BM) x columns [n0, n0 + BN) of column
   // tile c, row tiles [r_begin, r_end).
@@ -911,14 +915,19 @@ hipError_t launch_dac(const MapScalars& ms, const PeriphScalars& ps,
     const ConvGeom cg = conv_geom(*conv);
     const int64_t planes = (int64_t)conv->n * conv->c_in;
     hipLaunchKernelGGL(k_dac<true>, dim3((unsigned)(planes < 8192 ? planes : 8192)), dim3(256),
-                       0, s, ps, cg, X, V, planes);
+                       0, s, ps, cg, fast_div((uint32_t)cg.wp), X, V, planes);
   } else {
     ConvGeom cg{};
     cg.c_in = (int)ms.P;
     cg.wp = (int)fc_ldv(ms);
     hipLaunchKernelGGL(k_dac<false>, dim3((unsigned)(Bv < 8192 ? Bv : 8192)), dim3(256), 0, s,
-                       ps, cg, X, V, Bv);
+                       ps, cg, FastDiv{1, 0, 0}, X, V, Bv);
   }
+  return hipGetLastError();
+}
+
+hipError_t launch_adc_table(const PeriphScalars& ps, float2* tab, hipStream_t s) {
+  hipLaunchKernelGGL(k_adc_table, dim3(1), dim3(256), 0, s, ps, tab);
   return hipGetLastError();
 }
 
@@ -939,6 +948,7 @@ hipError_t launch_xbar_vmm(const MapScalars& ms, const PeriphScalars& ps, const 
   va.dbg_I = vl.dbg_I;
   va.dbg_code = vl.dbg_code;
   va.ktab = vl.ktab;
+  va.adc_tab = vl.adc_tab;
   va.gload = vl.gload;
   va.fd_hw = fast_div((uint32_t)(va.cg.ho * va.cg.wo));
   va.fd_wo = fast_div((uint32_t)va.cg.wo);

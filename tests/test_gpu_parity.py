@@ -368,6 +368,26 @@ def test_fc_workspace_reuse():
     L.free()
 
 
+def test_adc_table_follows_periph():
+    """The layer caches the ADC's bucket table: alternating converters on one
+    layer (bits, bend, full-scale through v_read) give what a fresh layer gives."""
+    W, X, xb, pp = fc_case(300, 70, 64, 64, 30, dac=6, adc=8, seed=13)
+    variants = [pp, wl.periph(6, 6, 1.0), wl.periph(6, 8, 1.0, adc_bend=0.2),
+                wl.periph(6, 8, 1.0, v_read=0.1), pp]
+    L = rxnn.map_layer(dev(W), xb)
+    for i, p in enumerate(variants):
+        say("adc table variant %d" % i)
+        Yp = rxnn.crossbar_vmm(L, p, dev(X)).cpu().numpy()
+        Lf = rxnn.map_layer(dev(W), xb)
+        Yf = rxnn.crossbar_vmm(Lf, p, dev(X)).cpu().numpy()
+        Lf.free()
+        np.testing.assert_array_equal(Yp, Yf)
+        if i == 0:
+            Y0 = Yp
+    np.testing.assert_array_equal(Yp, Y0)
+    L.free()
+
+
 def test_fc_batch_zero():
     W, X, xb, pp = fc_case(40, 20, 16, 16, 4)
     say("fc B=0")
