@@ -48,7 +48,7 @@ typedef enum {
   RXNN_EINVAL = -1,       /* an argument is out of range or inconsistent      */
   RXNN_ENOMEM = -2,       /* a device allocation failed                       */
   RXNN_EHIP = -3,         /* a HIP runtime call failed                        */
-  RXNN_EUNSUPPORTED = -4  /* valid, but not supported by this build           */
+  RXNN_EUNSUPPORTED = -4  /* valid, but not supported by this library         */
 } rxnn_status;
 
 /* Opaque handle of one mapped layer: owns the tiled G' buffer on the device. */
@@ -182,7 +182,7 @@ typedef struct {
  *           transposed.
  *   out     receives the new handle; free it with rxnn_free_layer.
  * G' is built in fp64 and stored as fp32.  Returns RXNN_EINVAL for a bad
- * argument, RXNN_EUNSUPPORTED for sizes beyond this build, RXNN_ENOMEM.
+ * argument, RXNN_EUNSUPPORTED for sizes beyond the library's limits, RXNN_ENOMEM.
  */
 rxnn_status rxnn_map_layer(const rxnn_xbar_params* params, const float* W,
                            int64_t P, int64_t Q, void* stream, rxnn_layer** out);

@@ -442,7 +442,7 @@ const char* rxnn_status_string(rxnn_status st) {
     case RXNN_EINVAL: return "invalid argument";
     case RXNN_ENOMEM: return "out of device memory";
     case RXNN_EHIP: return "HIP runtime error";
-    case RXNN_EUNSUPPORTED: return "unsupported by this build";
+    case RXNN_EUNSUPPORTED: return "unsupported by this library";
   }
   return "unknown status";
 }

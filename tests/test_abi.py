@@ -37,7 +37,7 @@ def test_every_declared_symbol_is_exported(lib):
 
 def test_status_strings(lib):
     for st, text in ((0, b"ok"), (-1, b"invalid argument"), (-2, b"out of device memory"),
-                     (-3, b"HIP runtime error"), (-4, b"unsupported by this build")):
+                     (-3, b"HIP runtime error"), (-4, b"unsupported by this library")):
         assert lib.rxnn_status_string(st) == text
 
 
