@@ -97,6 +97,15 @@ struct VmmArgs {
 
 __device__ __forceinline__ double bend(double u, double b) { return u - (b * u) * (1.0 - u); }
 
+// Workgroups are dispatched to the 8 XCDs in turn (workgroup i of a grid of n
+// to XCD i mod 8), and every XCD has its own L2.  This renumbering gives XCD x
+// the contiguous range of n / 8 (+1) logical numbers that starts at
+// x (n / 8) + min(x, n mod 8); it is a bijection of [0, n).
+__device__ __forceinline__ int64_t xcd_local(int64_t i, int64_t n) {
+  const int64_t q = n >> 3, r = n & 7, x = i & 7, j = i >> 3;
+  return x * q + min(x, r) + j;
+}
+
 // Buffer descriptor of a workgroup-uniform range; readfirstlane keeps it in
 // scalar registers (a descriptor the compiler cannot prove uniform costs a
 // loop over the distinct values at every load).
@@ -616,18 +625,23 @@ __global__ __launch_bounds__(NTHR, 2) void k_xbar_vmm(VmmArgs va) {
   // whole tiles w, w + W, ... below dp_tiles (the full rounds of the GPU), then
   // the units (tile, row tile) of the remaining tiles in the range
   // [U w / W, U (w + 1) / W) (tile-major), which may cover parts of tiles.
+  // Tile and worker numbers are XCD-local (xcd_local): neighbouring tiles,
+  // which share the halo rows of a convolution's input and, in a layer with
+  // several column blocks, the same input rows, run on one XCD and its L2.
   int64_t u, u1, t_dp, dp_end;
   bool shared_units = false;
   if (va.workers == 0) {
-    u = ((int64_t)blockIdx.x * va.n_cb + blockIdx.y) * tg.R;
+    const int64_t lin = blockIdx.x + (int64_t)blockIdx.y * gridDim.x;
+    u = xcd_local(lin, (int64_t)gridDim.x * gridDim.y) * tg.R;
     u1 = u + tg.R;
     t_dp = dp_end = 0;
   } else {
+    const int64_t w = xcd_local(blockIdx.x, va.workers);
     const int64_t n_tiles = (int64_t)((va.Bv + BM - 1) / BM) * va.n_cb;
     const int64_t U = (n_tiles - va.dp_tiles) * tg.R;
-    u = va.dp_tiles * tg.R + U * blockIdx.x / va.workers;
-    u1 = va.dp_tiles * tg.R + U * (blockIdx.x + 1) / va.workers;
-    t_dp = blockIdx.x;
+    u = va.dp_tiles * tg.R + U * w / va.workers;
+    u1 = va.dp_tiles * tg.R + U * (w + 1) / va.workers;
+    t_dp = w;
     dp_end = va.dp_tiles;
     shared_units = true;
   }
