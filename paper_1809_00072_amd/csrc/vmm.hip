@@ -702,7 +702,7 @@ __global__ __launch_bounds__(256) void k_finish(MapScalars ms, PeriphScalars ps,
 __global__ __launch_bounds__(256) void k_finish_nchw(MapScalars ms, PeriphScalars ps,
                                                      int32_t* __restrict__ iacc,
                                                      float* __restrict__ Y, int64_t row0,
-                                                     int64_t Bv, int64_t hw) {
+                                                     int64_t Bv, int64_t hw, FastDiv fd_hw) {
   __shared__ int32_t tile[64][65];
   const double wmax = ms.wmax_fixed > 0.0f ? (double)ms.wmax_fixed : (double)*ms.d_wmax;
   float scale = 0.0f;
@@ -710,17 +710,28 @@ __global__ __launch_bounds__(256) void k_finish_nchw(MapScalars ms, PeriphScalar
   const int64_t bv0 = row0 + (int64_t)blockIdx.x * 64;
   const int64_t q0 = (int64_t)blockIdx.y * 64;
   const int t = threadIdx.x & 63, u = threadIdx.x >> 6;
-  for (int i = u; i < 64; i += 4)
-    if (bv0 + i < Bv && q0 + t < ms.Q) {
-      tile[i][t] = iacc[(bv0 + i) * ms.Q + q0 + t];
-      iacc[(bv0 + i) * ms.Q + q0 + t] = 0;   // left zeroed for the next call
-    }
+  // all sixteen reads first (in flight together), then the zeroing writes
+  int32_t v[16];
+#pragma unroll
+  for (int j = 0; j < 16; ++j) {
+    const int i = u + 4 * j;
+    v[j] = (bv0 + i < Bv && q0 + t < ms.Q) ? iacc[(bv0 + i) * ms.Q + q0 + t] : 0;
+  }
+#pragma unroll
+  for (int j = 0; j < 16; ++j) {
+    const int i = u + 4 * j;
+    tile[i][t] = v[j];
+    if (bv0 + i < Bv && q0 + t < ms.Q) iacc[(bv0 + i) * ms.Q + q0 + t] = 0;   // left zeroed
+  }
   __syncthreads();
   const int64_t bv = bv0 + t;
   if (bv >= Bv) return;
-  const int64_t img = bv / hw, pix = bv - img * hw;
-  for (int i = u; i < 64; i += 4)
+  const int64_t img = div_by((uint32_t)bv, fd_hw), pix = bv - img * hw;   // Bv < 2^31
+#pragma unroll
+  for (int j = 0; j < 16; ++j) {
+    const int i = u + 4 * j;
     if (q0 + i < ms.Q) Y[(img * ms.Q + q0 + i) * hw + pix] = (float)tile[t][i] * scale;
+  }
 }
 
 // Table of the patch columns of a convolution, per row tile r of the walk
@@ -1010,7 +1021,8 @@ hipError_t launch_finish(const MapScalars& ms, const PeriphScalars& ps, int32_t*
   if (Bv <= row0) return hipSuccess;
   if (hw_out > 0) {
     const dim3 grid((unsigned)((Bv - row0 + 63) / 64), (unsigned)((ms.Q + 63) / 64));
-    hipLaunchKernelGGL(k_finish_nchw, grid, dim3(256), 0, s, ms, ps, iacc, Y, row0, Bv, hw_out);
+    hipLaunchKernelGGL(k_finish_nchw, grid, dim3(256), 0, s, ms, ps, iacc, Y, row0, Bv, hw_out,
+                       fast_div((uint32_t)hw_out));
     return hipGetLastError();
   }
   iacc += row0 * ms.Q;
