@@ -234,9 +234,18 @@ __global__ __launch_bounds__(256) void k_absmax(const float* __restrict__ W, int
                                                 unsigned* out) {
   __shared__ unsigned wm[4];
   unsigned m = 0;
-  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
-       i += (int64_t)gridDim.x * blockDim.x)
-    m = max(m, __float_as_uint(fabsf(W[i])));
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  // eight loads in flight per thread
+  for (int64_t i0 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i0 < n; i0 += 8 * stride) {
+    unsigned v[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int64_t i = i0 + j * stride;
+      v[j] = i < n ? __float_as_uint(fabsf(W[i])) : 0u;
+    }
+#pragma unroll
+    for (int j = 0; j < 8; ++j) m = max(m, v[j]);
+  }
   for (int off = 32; off > 0; off >>= 1) m = max(m, (unsigned)__shfl_xor((int)m, off, 64));
   if ((threadIdx.x & 63) == 0) wm[threadIdx.x >> 6] = m;
   __syncthreads();
@@ -259,8 +268,8 @@ __global__ void k_fill_u32(unsigned* p, int64_t n, unsigned v) {
 }  // namespace
 
 hipError_t launch_absmax(const float* W, int64_t n, unsigned* out, hipStream_t s) {
-  int64_t blocks = (n + 4095) / 4096;   // at least 16 elements per thread
-  if (blocks > 512) blocks = 512;
+  int64_t blocks = (n + 2047) / 2048;   // at least 8 elements per thread
+  if (blocks > 1024) blocks = 1024;
   if (blocks < 1) blocks = 1;
   hipLaunchKernelGGL(k_absmax, dim3((unsigned)blocks), dim3(256), 0, s, W, n, out);
   return hipGetLastError();
