@@ -317,6 +317,20 @@ def bench_stack(args):
     rxnn.profile_enable(False)
     eval_ms = ev0.elapsed_time(ev1) / args.steps
     kern_eval = read_kernels(rxnn, args.steps)
+    # model generation (the paper's phase 1): one G' build of every array of
+    # every layer, on one stream (the mapped-once stacks time it here; for the
+    # rebuilt stack it is part of every step)
+    gen = None
+    if not rebuild:
+        torch.cuda.synchronize()
+        ev0.record(stream)
+        for e in layers:
+            rxnn.remap_layer(e["L"], e["W"], stream)
+        ev1.record(stream)
+        torch.cuda.synchronize()
+        gen = generation_info(ev0.elapsed_time(ev1),
+                              int(sum(e["L"].R * e["L"].C * e["L"].A for e in layers)),
+                              layers[0]["L"].M, layers[0]["L"].N)
     macs = wl.stack_alg_macs(cfg)
     vmm_us = kern_eval["xbar_vmm"]["us_per_step"]
     ach = 2.0 * macs / (vmm_us * 1e-6) / 1e12
@@ -345,9 +359,24 @@ def bench_stack(args):
                       "kernels": kern_eval},
         "kernels": kern,
     }
+    if gen is not None:
+        out["generation"] = gen
     for e in layers:
         e["L"].free()
     print(json.dumps(out), flush=True)
+
+
+# The paper's FCM model generation time for one crossbar (Sec. VIII-A; its
+# hardware is not named): context for the G' build, not a target.
+PAPER_GEN_S = {16: 0.038, 32: 1.2, 64: 61.0}
+
+
+def generation_info(ms, arrays, M, N):
+    out = {"what": "G' build of every array once (model generation)", "ms": ms,
+           "arrays": arrays, "us_per_array": 1e3 * ms / arrays, "crossbar": [M, N]}
+    if M == N and M in PAPER_GEN_S:
+        out["paper_s_per_crossbar"] = PAPER_GEN_S[M]
+    return out
 
 
 def ideal_fp32_leg(torch, cv, Wd, Xd, vmm_us, eval_ms, steps):
@@ -548,7 +577,8 @@ def main():
                                                      "gprime_sweep") if k in kern)
     b_ach = n_arrays * build_flops(L.M, L.N) / (build_us * 1e-6) / 1e12
     build = {"us_per_step": build_us, "bound": "alu", "achieved": b_ach,
-             "peak": FP64_PEAK_TFLOPS, "unit": "TFLOP/s", "frac": b_ach / FP64_PEAK_TFLOPS}
+             "peak": FP64_PEAK_TFLOPS, "unit": "TFLOP/s", "frac": b_ach / FP64_PEAK_TFLOPS,
+             "generation": generation_info(1e-3 * build_us, n_arrays, L.M, L.N)}
 
     ideal = ideal_fp32_leg(torch, cv, Wd, Xd, vmm_us, eval_ms, args.steps)
     if args.copy_probe:
