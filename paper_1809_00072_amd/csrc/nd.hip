@@ -26,7 +26,8 @@
 // Attaching the drivers and eliminating the row-input nodes leaves the
 // transfer admittance from the row sources to the sinks, i.e. G'.
 //
-// Levels up to 8 x 8 cells: one wave per 8 x 8 block (k_nd_block).  Merges
+// Levels up to 8 x 8 cells: one workgroup per 8 x 8 block, its waves sharing
+// each level's merges (k_nd_block).  Merges
 // with at most 64 shared nodes: one workgroup per merge eliminates them with
 // the shared rows in registers (k_nd_cut), and k_nd_schur applies the
 // resulting update to the external block on 64 x 64 tiles; the final step
@@ -169,7 +170,8 @@ __device__ __forceinline__ double cell_conductance(const MapScalars& ms, const f
 // workgroup barrier: each wave's levels use its own LDS buffers.
 // ---------------------------------------------------------------------------
 constexpr int BS = 8;                 // side of the blocks of this kernel
-constexpr int BWAVES = 4;             // blocks (waves) per workgroup
+constexpr int BWAVES = 4;             // waves per workgroup of the block kernel
+constexpr int64_t kSplitBlocks = 2048; // at most this many blocks: one workgroup per block
 constexpr int BLEVELS = 6;            // 1x1 -> 2x1 -> 2x2 -> 4x2 -> 4x4 -> 8x4 -> 8x8
 constexpr int BUFA = 1024, BUFB = 1152;   // doubles per wave: leaves / even / odd levels
 
@@ -233,10 +235,12 @@ __device__ __forceinline__ void wave_sync() {
 }
 
 // One level of merges of the block at (I0, J0): children h x w (in: EIN x
-// EIN per child), merged blocks written with stride EM (out).
-template <int L, int H, int W, bool VERT>
+// EIN per child), merged blocks written with stride EM (out).  SPLIT: the
+// level's passes (GPW merges each) are shared by the workgroup's waves, which
+// all work on this block; otherwise the wave does them all.
+template <int L, int H, int W, bool VERT, bool SPLIT>
 __device__ __forceinline__ void block_level(int T, int I0, int J0, const short* tab,
-                                            const double* in, double* out, int lane) {
+                                            const double* in, double* out, int lane, int wv) {
   constexpr int NH = VERT ? 2 * H : H, NW = VERT ? W : 2 * W;
   constexpr int C = VERT ? W : H;
   constexpr int EM = 2 * (NH + NW), EIN = 2 * (H + W);
@@ -248,7 +252,7 @@ __device__ __forceinline__ void block_level(int T, int I0, int J0, const short* 
   static_assert(NM % GPW == 0, "whole passes");
   const int g = lane / GS, yl = lane % GS, gb = lane - yl;
 #pragma unroll 1
-  for (int pass = 0; pass < NM / GPW; ++pass) {
+  for (int pass = SPLIT ? wv : 0; pass < NM / GPW; pass += SPLIT ? BWAVES : 1) {
     const int m = pass * GPW + g;
     const int mi = m / MC, mj = m % MC;
     const int i0 = I0 + mi * NH, j0 = J0 + mj * NW;
@@ -285,20 +289,26 @@ __device__ __forceinline__ void block_level(int T, int I0, int J0, const short* 
         if (x < ld) out[m * EM * EM + (x - C) * EM + (yl - C)] = U[x];
     }
   }
-  wave_sync();
+  if (SPLIT) __syncthreads();
+  else wave_sync();
 }
 
+// SPLIT (few blocks, a latency-bound build): one 8 x 8 block per workgroup,
+// its waves sharing each level; otherwise one block per wave (BWAVES blocks
+// per workgroup), no workgroup barriers.
+template <bool SPLIT>
 __global__ __launch_bounds__(64 * BWAVES) void k_nd_block(NdArgs na) {
   __shared__ short tab[BLEVELS * 4 * 2 * 64];
-  __shared__ double bufA[BWAVES][BUFA];
-  __shared__ double bufB[BWAVES][BUFB];
+  constexpr int NB = SPLIT ? 1 : BWAVES;   // blocks per workgroup
+  __shared__ double bufA[NB][BUFA];
+  __shared__ double bufB[NB][BUFB];
   const short* ct = &kBlkTab.s[0][0][0][0];
   for (int e = threadIdx.x; e < BLEVELS * 4 * 2 * 64; e += 64 * BWAVES) tab[e] = ct[e];
   __syncthreads();
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
   const int T = na.T;
   const int nsb = T / BS;
-  const int64_t blk = (int64_t)blockIdx.x * BWAVES + wv;
+  const int64_t blk = SPLIT ? (int64_t)blockIdx.x : (int64_t)blockIdx.x * BWAVES + wv;
   const int64_t nblk = na.n_arrays * nsb * nsb;
   if (blk >= nblk) return;
   const int64_t la = blk / (nsb * nsb);
@@ -307,11 +317,11 @@ __global__ __launch_bounds__(64 * BWAVES) void k_nd_block(NdArgs na) {
   const int64_t arr = na.arr0 + la;
   const MapScalars& ms = na.ms;
   const double wmax = ms.wmax_fixed > 0.0f ? (double)ms.wmax_fixed : (double)*ms.d_wmax;
-  double* A = bufA[wv];
-  double* B = bufB[wv];
-  // leaves: one cell per lane, ports [L | R (not at the right edge) | T (not
-  // at the top) | B] in a 4 x 4 slot
-  {
+  double* A = bufA[SPLIT ? 0 : wv];
+  double* B = bufB[SPLIT ? 0 : wv];
+  // leaves (the first wave): one cell per lane, ports [L | R (not at the
+  // right edge) | T (not at the top) | B] in a 4 x 4 slot
+  if (!SPLIT || wv == 0) {
     const int li = lane / BS, lj = lane % BS;
     const int gi = I0 + li, gj = J0 + lj;
     const double G = cell_conductance(ms, na.W, wmax, arr, gi, gj, na.row_off);
@@ -336,15 +346,16 @@ __global__ __launch_bounds__(64 * BWAVES) void k_nd_block(NdArgs na) {
       st(Lp, Bp, ge);
     }
   }
-  wave_sync();
-  block_level<0, 1, 1, true>(T, I0, J0, tab, A, B, lane);
-  block_level<1, 2, 1, false>(T, I0, J0, tab, B, A, lane);
-  block_level<2, 2, 2, true>(T, I0, J0, tab, A, B, lane);
-  block_level<3, 4, 2, false>(T, I0, J0, tab, B, A, lane);
-  block_level<4, 4, 4, true>(T, I0, J0, tab, A, B, lane);
+  if (SPLIT) __syncthreads();
+  else wave_sync();
+  block_level<0, 1, 1, true, SPLIT>(T, I0, J0, tab, A, B, lane, wv);
+  block_level<1, 2, 1, false, SPLIT>(T, I0, J0, tab, B, A, lane, wv);
+  block_level<2, 2, 2, true, SPLIT>(T, I0, J0, tab, A, B, lane, wv);
+  block_level<3, 4, 2, false, SPLIT>(T, I0, J0, tab, B, A, lane, wv);
+  block_level<4, 4, 4, true, SPLIT>(T, I0, J0, tab, A, B, lane, wv);
   constexpr int EO = 4 * BS;   // ports of an interior 8 x 8 block
   double* dst = na.buf_out + la * na.out_stride + (int64_t)sb * EO * EO;
-  block_level<5, 8, 4, false>(T, I0, J0, tab, B, dst, lane);
+  block_level<5, 8, 4, false, SPLIT>(T, I0, J0, tab, B, dst, lane, wv);
 }
 
 // ---------------------------------------------------------------------------
@@ -1487,8 +1498,15 @@ hipError_t launch_nd_build(const MapScalars& ms, const float* W, float* gpt, int
   na.buf_out = bufA;
   {
     ProfScope prof("nd_block", s);
-    const dim3 grid((unsigned)((n * nsb * nsb + BWAVES - 1) / BWAVES));
-    hipLaunchKernelGGL(k_nd_block, grid, dim3(64 * BWAVES), 0, s, na);
+    // few blocks: one per workgroup, its waves sharing each level (shorter
+    // latency); many: one per wave (more blocks in flight per CU)
+    const int64_t nblk = n * nsb * nsb;
+    if (nblk <= kSplitBlocks) {
+      hipLaunchKernelGGL(k_nd_block<true>, dim3((unsigned)nblk), dim3(64 * BWAVES), 0, s, na);
+    } else {
+      const dim3 grid((unsigned)((nblk + BWAVES - 1) / BWAVES));
+      hipLaunchKernelGGL(k_nd_block<false>, grid, dim3(64 * BWAVES), 0, s, na);
+    }
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
