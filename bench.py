@@ -47,7 +47,7 @@ FP32_MFMA_PEAK_TFLOPS = 157.3   # MI355X dense fp32 matrix
 # FETCH_SIZE / WRITE_SIZE counters of this kernel version, each scaled by what
 # the counter reads for a plain 2 GiB copy (fetch x 2.000, write x 1.000);
 # the summary and its commands are in the repository's profiles folder
-VMM_TRAFFIC_BYTES = 2.0 * 15399 * 1024 + 40245 * 1024
+VMM_TRAFFIC_BYTES = 2.0 * 15384 * 1024 + 40314 * 1024
 FP64_PEAK_TFLOPS = 78.6         # MI355X fp64 (vector and matrix)
 HBM_PEAK_GBS = 8000.0
 
