@@ -201,13 +201,20 @@ def bench_fc256(args):
     rxnn.profile_enable(False)
     ms = ev0.elapsed_time(ev1) / args.steps
     macs = wl.alg_macs(w)
+    kern = read_kernels(rxnn, args.steps)
+    vmm_us = kern["xbar_vmm"]["avg_us"]
+    ach = 2.0 * macs / (vmm_us * 1e-6) / 1e12
     out = {"metric": "non-ideal crossbar MACs/sec per layer", "value": macs / (ms * 1e-3),
            "unit": "MAC/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
            "ms_per_step": ms, "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
            "dtype": "f32", "data": "synthetic",
            "config": {"workload": "fc256->128, batch 16, 64x64 crossbars, 4-bit DAC / 8-bit ADC; "
                                   "step = evaluation (launch bound)", "alg_macs_per_step": macs},
-           "kernels": read_kernels(rxnn, args.steps)}
+           "roofline": {"kernel": "k_xbar_vmm", "bound": "mfma", "achieved": ach,
+                        "peak": FP32_MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
+                        "frac": ach / FP32_MFMA_PEAK_TFLOPS, "traffic": None,
+                        "note": "16 arrays of 64 x 64: launch and latency bound"},
+           "kernels": kern}
     L.free()
     print(json.dumps(out), flush=True)
 
