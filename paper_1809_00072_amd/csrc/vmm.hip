@@ -39,6 +39,9 @@
 // Integer accumulation makes the result independent of the order of row
 // tiles and arrays, so splitting the row tiles over workgroups and combining
 // with int32 atomics gives bit-identical results.
+// Tiles are numbered XCD-locally (consecutive tiles on one XCD and its L2),
+// and 32 x 32 crossbars are walked in groups of 2 x 2 arrays, one 64 x 64
+// tile with the ADC after each row tile's 32 inputs.
 //
 // K-order inside a 16-deep MFMA block: lane l in sub-step s multiplies the
 // elements k = 4 (l / 16) + s of its row and column, so each lane fetches
