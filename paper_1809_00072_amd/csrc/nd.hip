@@ -295,9 +295,11 @@ __device__ __forceinline__ void block_level(int T, int I0, int J0, const short* 
 
 // SPLIT (few blocks, a latency-bound build): one 8 x 8 block per workgroup,
 // its waves sharing each level; otherwise one block per wave (BWAVES blocks
-// per workgroup), no workgroup barriers.
+// per workgroup), no workgroup barriers.  At most 96 VGPRs (5 waves per
+// SIMD): five split workgroups per CU, so 1,280 blocks run in one round
+// (LDS bounds the unsplit form at two workgroups per CU either way).
 template <bool SPLIT>
-__global__ __launch_bounds__(64 * BWAVES) void k_nd_block(NdArgs na) {
+__global__ __launch_bounds__(64 * BWAVES) __attribute__((amdgpu_waves_per_eu(5))) void k_nd_block(NdArgs na) {
   __shared__ short tab[BLEVELS * 4 * 2 * 64];
   constexpr int NB = SPLIT ? 1 : BWAVES;   // blocks per workgroup
   __shared__ double bufA[NB][BUFA];
