@@ -295,11 +295,9 @@ __device__ __forceinline__ void block_level(int T, int I0, int J0, const short* 
 
 // SPLIT (few blocks, a latency-bound build): one 8 x 8 block per workgroup,
 // its waves sharing each level; otherwise one block per wave (BWAVES blocks
-// per workgroup), no workgroup barriers.  At most 96 VGPRs (5 waves per
-// SIMD): five split workgroups per CU, so 1,280 blocks run in one round
-// (LDS bounds the unsplit form at two workgroups per CU either way).
+// per workgroup), no workgroup barriers.
 template <bool SPLIT>
-__global__ __launch_bounds__(64 * BWAVES) __attribute__((amdgpu_waves_per_eu(5))) void k_nd_block(NdArgs na) {
+__device__ __forceinline__ void nd_block(const NdArgs& na) {
   __shared__ short tab[BLEVELS * 4 * 2 * 64];
   constexpr int NB = SPLIT ? 1 : BWAVES;   // blocks per workgroup
   __shared__ double bufA[NB][BUFA];
@@ -358,6 +356,18 @@ __global__ __launch_bounds__(64 * BWAVES) __attribute__((amdgpu_waves_per_eu(5))
   constexpr int EO = 4 * BS;   // ports of an interior 8 x 8 block
   double* dst = na.buf_out + la * na.out_stride + (int64_t)sb * EO * EO;
   block_level<5, 8, 4, false, SPLIT>(T, I0, J0, tab, B, dst, lane, wv);
+}
+
+// The split form is held to 96 VGPRs (5 waves per SIMD): five workgroups per
+// CU, so 1,280 blocks run in one round.  LDS bounds the other form at two
+// workgroups per CU either way.
+__global__ __launch_bounds__(64 * BWAVES) __attribute__((amdgpu_waves_per_eu(5)))
+void k_nd_block_split(NdArgs na) {
+  nd_block<true>(na);
+}
+
+__global__ __launch_bounds__(64 * BWAVES) void k_nd_block(NdArgs na) {
+  nd_block<false>(na);
 }
 
 // ---------------------------------------------------------------------------
@@ -1504,10 +1514,10 @@ hipError_t launch_nd_build(const MapScalars& ms, const float* W, float* gpt, int
     // latency); many: one per wave (more blocks in flight per CU)
     const int64_t nblk = n * nsb * nsb;
     if (nblk <= kSplitBlocks) {
-      hipLaunchKernelGGL(k_nd_block<true>, dim3((unsigned)nblk), dim3(64 * BWAVES), 0, s, na);
+      hipLaunchKernelGGL(k_nd_block_split, dim3((unsigned)nblk), dim3(64 * BWAVES), 0, s, na);
     } else {
       const dim3 grid((unsigned)((nblk + BWAVES - 1) / BWAVES));
-      hipLaunchKernelGGL(k_nd_block<false>, grid, dim3(64 * BWAVES), 0, s, na);
+      hipLaunchKernelGGL(k_nd_block, grid, dim3(64 * BWAVES), 0, s, na);
     }
   }
   hipError_t e = hipGetLastError();
