@@ -1,17 +1,27 @@
 """Benchmark of the FCM crossbar path on one MI355X.
 
 One step = one pass of the whole path over one batch: rebuild every array's
-G' from the layer weights (w_max reduction + fp64 build), unroll the input
-patches through the DAC, and evaluate DAC -> V.G' -> ADC -> accumulate for
-every row tile and array.  The workload is the 3x3 64->64 convolution on a
-batch of 32 56 x 56 inputs mapped onto 64 x 64 crossbars (6-bit DAC, 8-bit
-ADC, 1 kOhm driver and sense, 2.5 Ohm wire segments).
+G' from the step's layer weights (w_max reduction + fp64 build; the model is
+regenerated every step, as in model-in-the-loop re-training), and evaluate
+DAC -> V.G' -> ADC -> accumulate for every row tile and array of every
+layer.  The default workload is the ResNet-50 shaped stack (53 convolutions
+and the classifier), batch 128, on 256 x 256 crossbars with 2.5 Ohm wire
+segments, 8-bit DAC / ADC, 1 kOhm driver and sense resistances.
 
-Prints one JSON line.  Kernel durations come from HIP events that the
-library records around each of its launches on the launch stream.
+Prints one JSON line: `value` is the whole step (map + VMM); `eval_only` the
+evaluation alone (VMM only, G' kept), `map_only` the rebuild alone.  The
+`roofline` is the evaluation kernel's, summed over the layers of an
+evaluation-only pass; `hbm` gives the DAC pass's and the finish kernel's
+achieved bandwidth; `cpu_baseline` the oracle on a seeded sample, on the
+host's cores, extrapolated to the whole step, and `sample_parity` the GPU's
+outputs on that sample under the parity tests' rule.  Kernel durations come
+from HIP events that the library records around its launches on the launch
+stream.
 
---workload selects one of the other workloads instead (each prints its own
-line; the default is the convolution above):
+--workload selects one of the other workloads instead:
+  conv3x3    3x3 s1 p1 64 -> 64 convolution on 32 x 64 x 56 x 56, 64 x 64
+             crossbars, 6-bit DAC / 8-bit ADC; a step rebuilds G' (18 arrays)
+             and evaluates; the oracle runs the whole workload;
   fc256      FC 256 -> 128, batch 16, 64 x 64 crossbars (launch bound);
   resnet18   the 21 layers of a ResNet-18 shaped stack, 128 x 128 crossbars,
              wire 1 Ohm, batch 64, each layer on its own seeded input; a step
@@ -19,10 +29,7 @@ line; the default is the convolution above):
   vgg16fc    the VGG-16 shaped FC head 25088 -> 4096 -> 4096 -> 1000, batch
              256, 8-bit weights in four 2-bit slices; a step evaluates the
              three layers;
-  resnet50   the 54 layers of a ResNet-50 shaped stack, batch 128, crossbar
-             side --crossbar (32 / 64 / 128 / 256), wire --wire; a step
-             perturbs every layer's weights, rebuilds G' and evaluates it
-             (reported: the whole step and the evaluation alone).
+  resnet50   the default, with --crossbar (32 / 64 / 128 / 256) and --wire.
 
 --retrain adds, for the convolution, a leg timed after the others: one
 model-in-the-loop re-training step = G' rebuild + crossbar forward pass +
@@ -48,6 +55,10 @@ FP32_MFMA_PEAK_TFLOPS = 157.3   # MI355X dense fp32 matrix
 # the counter reads for a plain 2 GiB copy (fetch x 2.000, write x 1.000);
 # the summary and its commands are in the repository's profiles folder
 VMM_TRAFFIC_BYTES = 2.0 * 15384 * 1024 + 40314 * 1024
+# HBM bytes of k_xbar_vmm per evaluation-only pass of a stacked workload
+# (summed over its layers), from the same counters and calibration, keyed by
+# (workload, crossbar side, wire); None where they have not been taken
+STACK_VMM_TRAFFIC = {}
 FP64_PEAK_TFLOPS = 78.6         # MI355X fp64 (vector and matrix)
 HBM_PEAK_GBS = 8000.0
 
@@ -80,38 +91,347 @@ def build_flops(M, N):
     return flops
 
 
-def cpu_baseline(work):
-    """The oracle on the full workload (map every array, evaluate all images)."""
-    import numpy as np
-    from oracle import fcm as ofcm, mapping as omap
-    from paper_1809_00072_amd import workloads as wl
+def host_info():
+    """CPU model and the number of cores this process may run on."""
+    model = "unknown"
     try:
-        from threadpoolctl import threadpool_info
-        threads = max([d.get("num_threads", 1) for d in threadpool_info()] or [1])
-    except Exception:
-        threads = 1
-    t0 = time.perf_counter()
-    lay = omap.map_layer(work["W"], work["xbar"])
-    t1 = time.perf_counter()
-    Y = ofcm.conv_layer(work["X"], lay, work["xbar"], work["periph"], work["conv"])
-    t2 = time.perf_counter()
-    assert np.isfinite(Y).all()
-    macs = wl.alg_macs(work)
-    out = {"value": macs / (t2 - t0), "unit": "MAC/s", "cores": threads, "kind": "oracle",
-           "sample": "full workload once: G' of all %d arrays by sparse nodal LU (%.2f s) + "
-                     "evaluation of all %d images (%.2f s), fp64 numpy/scipy"
-                     % (lay["R"] * lay["C"] * lay["A"], t1 - t0, work["conv"]["n"], t2 - t1)}
-    # the same on one core (BLAS limited to one thread)
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    try:
+        n = len(os.sched_getaffinity(0))
+    except AttributeError:
+        n = os.cpu_count() or 1
+    return model, n
+
+
+def oracle_workers():
+    # the GPU box gives one GPU's job a share of 16 host cores
+    return max(1, min(16, host_info()[1]))
+
+
+def _one_thread_blas():
+    # every worker runs its own share: one BLAS thread each, no oversubscription
     try:
         from threadpoolctl import threadpool_limits
-        with threadpool_limits(limits=1):
-            t0 = time.perf_counter()
-            lay = omap.map_layer(work["W"], work["xbar"])
-            ofcm.conv_layer(work["X"], lay, work["xbar"], work["periph"], work["conv"])
-            t2 = time.perf_counter()
-        out["one_core"] = {"value": macs / (t2 - t0), "unit": "MAC/s", "seconds": t2 - t0}
+        threadpool_limits(limits=1)
     except ImportError:
         pass
+
+
+# Inputs of the oracle's sample, set before the worker pool forks (the workers
+# inherit them): key -> dict of numpy arrays and parameters.
+_SAMPLE = {}
+
+
+def _oracle_tile(task):
+    """Worker: G' of every array of tile (r, c) of sampled layer `key`
+    (generator steps 1-3 of the oracle)."""
+    import numpy as np
+    from oracle import mapping as omap
+    key, r, c = task
+    s = _SAMPLE[key]
+    xb = s["xbar"]
+    t0 = time.perf_counter()
+    vf = omap.variation_factors(xb, r, c, s["R"], s["A"], s["M"], s["N"])
+    G = omap.array_conductances(omap.tile_weights(s["W"], xb, r, c), xb, s["w_max"], vf)
+    gp = np.stack([omap.array_gprime(G[a], xb) for a in range(G.shape[0])])
+    return key, r, c, gp, time.perf_counter() - t0
+
+
+def _oracle_eval(task):
+    """Worker: product rows [lo, hi) of the sample of layer `key` through the
+    oracle's evaluation (DAC, V.G', ADC, integer accumulation) over its column
+    tiles, with the G' the sample holds (built before the workers forked).
+    Returns those columns of Y; with `debug` also the per-array currents and
+    codes (for the parity check; not timed: moving them between processes
+    costs more than computing them)."""
+    from oracle import fcm as ofcm
+    key, lo, hi, debug = task
+    s = _SAMPLE[key]
+    lay = dict(s["lay"], gp=s["gp"])
+    t0 = time.perf_counter()
+    res = ofcm.crossbar_vmm(s["Xs"][lo:hi], lay, s["xbar"], s["periph"], col_tiles=s["cols"],
+                            debug=debug)
+    dt = time.perf_counter() - t0
+    Y, dbg = res if debug else (res, None)
+    q0 = min(s["cols"]) * s["N"]
+    q1 = min(s["Q"], (max(s["cols"]) + 1) * s["N"])
+    return key, Y[:, q0:q1], dbg, dt
+
+
+def _ready(_):
+    return os.getpid()
+
+
+def _layer_scalars(W, xb):
+    from oracle import mapping as omap
+    P, Q = W.shape
+    M, N = int(xb["rows"]), int(xb["cols"])
+    R, C = omap.tile_grid(P, Q, M, N)
+    w_max = omap.layer_w_max(W, xb)
+    return {"P": P, "Q": Q, "M": M, "N": N, "R": R, "C": C,
+            "A": omap.arrays_per_position(xb), "w_max": w_max,
+            "s_w_eff": omap.effective_weight_scale(xb, w_max)}
+
+
+def conv_patch_sample(conv, per_image, seed):
+    """Seeded product rows of a convolution: per_image output pixels of the
+    first and of the last image, always including each image's first and
+    last pixel, interleaved (first image, last image, first, ...).  Returns
+    (images, pixels, H_out, W_out)."""
+    import numpy as np
+    ho = (conv["h"] + 2 * conv["pad"] - conv["kh"]) // conv["stride"] + 1
+    wo = (conv["w"] + 2 * conv["pad"] - conv["kw"]) // conv["stride"] + 1
+    rng = np.random.default_rng(seed)
+    per = []
+    for img in sorted({0, conv["n"] - 1}):
+        k = min(per_image, ho * wo)
+        pix = [0, ho * wo - 1] + [int(v) for v in rng.permutation(ho * wo)]
+        pix = list(dict.fromkeys(pix))[:k]
+        per.append([(img, p) for p in pix])
+    rows = [r for grp in zip(*per) for r in grp] if len(per) > 1 else per[0]
+    return (np.array([r[0] for r in rows]), np.array([r[1] for r in rows]), ho, wo)
+
+
+def sample_rows(work, n_rows, seed):
+    """The layer's sampled product rows: (X rows for the oracle [S x P],
+    a selector that takes the same rows out of the GPU's output)."""
+    import numpy as np
+    from oracle import fcm as ofcm
+    if work["kind"] == "conv":
+        cv = work["conv"]
+        img, pix, ho, wo = conv_patch_sample(cv, n_rows // 2, seed)
+        imgs = sorted(set(int(i) for i in img))
+        patches = ofcm.im2col(work["X"], cv, imgs)
+        local = np.searchsorted(imgs, img) * (ho * wo) + pix
+        return patches[local], ("conv", img, pix, wo)
+    B = work["X"].shape[0]
+    rows = np.sort(np.random.default_rng(seed).permutation(B)[:min(n_rows, B)])
+    return work["X"][rows], ("fc", rows)
+
+
+def select_rows(Y, sel):
+    """The sampled rows of a GPU output (numpy), as [S x Q]."""
+    if sel[0] == "conv":
+        _, img, pix, wo = sel
+        return Y[img, :, pix // wo, pix % wo]
+    return Y[sel[1]]
+
+
+# Sampled rows per layer whose outputs are compared with the GPU's.
+PARITY_ROWS = 128
+# Arrays of the oracle's build sample per crossbar side: about 10-20 s on 16
+# host cores with the oracle's per-array cost at that side.
+SAMPLE_ARRAYS = {16: 4096, 32: 2048, 64: 768, 128: 256, 256: 96}
+
+
+def oracle_sample(works, total_arrays, total_macs, seed=4242, n_rows=1024):
+    """The oracle timed on a seeded sample of a stacked workload, on the host's
+    cores, and extrapolated to the whole workload.
+
+    Sample: layers in a seeded order until about SAMPLE_ARRAYS[side] arrays;
+    for each, the last column tile (possibly padded) with every row tile's G'
+    (one process per tile), and n_rows product rows (FC: batch rows; conv:
+    output pixels of the first and last image) evaluated over it (one process
+    per block of 128 rows).  Full time = build time per array x arrays + evaluation time
+    per MAC x MACs, both measured here, on all workers and on one core."""
+    import multiprocessing as mp
+    import numpy as np
+    M = int(works[0]["xbar"]["rows"])
+    target = SAMPLE_ARRAYS.get(M, 256)
+    order = np.random.default_rng(seed).permutation(len(works))
+    keys, n_arrays = [], 0
+    for l in order:
+        w = works[int(l)]
+        sc = _layer_scalars(w["W"], w["xbar"])
+        if keys and n_arrays + sc["R"] * sc["A"] > 1.5 * target:
+            continue
+        c = sc["C"] - 1
+        Xs, sel = sample_rows(w, n_rows, seed + int(l))
+        _SAMPLE[int(l)] = {"W": w["W"], "xbar": w["xbar"], "periph": w["periph"], "Xs": Xs,
+                           "sel": sel, "cols": [c], **sc, "lay": sc}
+        keys.append(int(l))
+        n_arrays += sc["R"] * sc["A"]
+        if n_arrays >= target:
+            break
+    tasks = [(k, r, _SAMPLE[k]["cols"][0]) for k in keys for r in range(_SAMPLE[k]["R"])]
+    workers = oracle_workers()
+    ctx = mp.get_context("fork")
+    print("[bench] oracle sample: %d layers, %d arrays, %d workers"
+          % (len(keys), n_arrays, workers), file=sys.stderr, flush=True)
+    with ctx.Pool(workers, initializer=_one_thread_blas) as pool:
+        pool.map(_ready, range(workers))   # the workers are up before the clock starts
+        t0 = time.perf_counter()
+        built = pool.map(_oracle_tile, tasks, chunksize=1)
+        t_build = time.perf_counter() - t0
+    for k in keys:
+        _SAMPLE[k]["gp"] = {}
+    for k, r, c, gp, _ in built:
+        _SAMPLE[k]["gp"][(r, c)] = gp
+    # the evaluation: row blocks over a second pool, forked after the build so
+    # that its workers hold every G'; one untimed pass first (the workers'
+    # first allocations), then the timed one
+    blocks = [(k, lo, min(lo + 128, _SAMPLE[k]["Xs"].shape[0]), False) for k in keys
+              for lo in range(0, _SAMPLE[k]["Xs"].shape[0], 128)]
+    with ctx.Pool(workers, initializer=_one_thread_blas) as pool:
+        pool.map(_oracle_eval, blocks, chunksize=1)
+        t0 = time.perf_counter()
+        pool.map(_oracle_eval, blocks, chunksize=1)
+        t_eval = time.perf_counter() - t0
+        # for the parity check (not timed): the first PARITY_ROWS rows
+        evals = pool.map(_oracle_eval, [(k, 0, min(PARITY_ROWS, _SAMPLE[k]["Xs"].shape[0]), True)
+                                        for k in keys], chunksize=1)
+
+    def sample_macs(s):
+        c = s["cols"][0]
+        return s["Xs"].shape[0] * s["P"] * (min(s["Q"], (c + 1) * s["N"]) - c * s["N"]) * s["A"]
+
+    macs_all = sum(sample_macs(_SAMPLE[k]) for k in keys)
+    # one core: one tile's build and the whole evaluation sample, here
+    try:
+        from threadpoolctl import threadpool_limits
+        limit = threadpool_limits(limits=1)
+    except ImportError:
+        limit = None
+    _, _, _, _, t1_tile = _oracle_tile(tasks[0])
+    t0 = time.perf_counter()
+    for k in keys:
+        _oracle_eval((k, 0, _SAMPLE[k]["Xs"].shape[0], False))
+    t1_eval = time.perf_counter() - t0
+    if limit is not None:
+        limit.unregister()
+    macs1 = macs_all
+    a0 = _SAMPLE[tasks[0][0]]["A"]
+    t_full = t_build / n_arrays * total_arrays + t_eval / macs_all * total_macs
+    t_one = t1_tile / a0 * total_arrays + t1_eval / macs1 * total_macs
+    model, ncores = host_info()
+    out = {"value": total_macs / t_full, "unit": "MAC/s", "cores": workers, "kind": "oracle",
+           "extrapolated": True,
+           "sample": "seeded: %d of %d layers, each its last column tile with every row "
+                     "tile's G' (%d arrays of %dx%d: oracle row sweep / nodal LU, fp64) and %d "
+                     "product rows evaluated over it (%.3g MACs); full step extrapolated as "
+                     "build s/array x %d arrays + evaluation s/MAC x %.4g MACs"
+                     % (len(keys), len(works), n_arrays, M, M, n_rows, macs_all,
+                        total_arrays, total_macs),
+           "seconds": {"sample_build": t_build, "sample_eval": t_eval,
+                       "extrapolated_step": t_full,
+                       "extrapolated_build": t_build / n_arrays * total_arrays,
+                       "extrapolated_eval": t_eval / macs_all * total_macs},
+           "host": {"cpu": model, "cores_available": ncores, "workers": workers},
+           "one_core": {"value": total_macs / t_one, "unit": "MAC/s", "extrapolated_step_s": t_one,
+                        "sample": "one tile's build (%d arrays, %.2f s) and the evaluation "
+                                  "sample (%.3g MACs, %.2f s) on one core"
+                                  % (a0, t1_tile, macs1, t1_eval)}}
+    out["all_over_one_core"] = out["value"] / out["one_core"]["value"]
+    results = {k: (Y, dbg) for k, Y, dbg, _ in evals}
+    return out, results
+
+
+def sample_parity(works, layers, results, rxnn, torch, stream):
+    """GPU outputs of the sampled rows against the oracle's codes on the base
+    weights (the rule of the parity tests: fp32(integer) * scale, the integer
+    off the oracle's only by codes whose current sits on a threshold)."""
+    import numpy as np
+    tests_dir = os.path.join(ROOT, "tests")
+    if tests_dir not in sys.path:
+        sys.path.insert(0, tests_dir)
+    from parity import array_weights, check_outputs_by_codes
+    from oracle import mapping as omap, periph as oper
+    n_out = n_diff = n_codes = 0
+    for k, (Yo, dbg) in results.items():
+        s, e = _SAMPLE[k], layers[k]
+        rxnn.remap_layer(e["L"], e["W"], stream)
+        w = works[k]
+        if w["kind"] == "conv":
+            rxnn.conv_layer(e["L"], w["periph"], w["conv"], e["X"], e["Y"], stream)
+        else:
+            rxnn.crossbar_vmm(e["L"], w["periph"], e["X"], e["Y"], stream)
+        torch.cuda.synchronize()
+        n_par = next(iter(dbg.values()))[0].shape[0]
+        Yg = select_rows(e["Y"].cpu().numpy(), s["sel"])[:n_par]
+        pp, xb = s["periph"], s["xbar"]
+        thr = oper.adc_thresholds(int(pp["adc_bits"]), oper.adc_full_scale(pp, s["M"], xb["g_max"]),
+                                  pp["adc_bend"])
+        scale = oper.output_scale(pp, s["M"], xb["g_max"], s["s_w_eff"])
+        weights = array_weights(s["A"], omap.slicing(xb)[1])
+        c = s["cols"][0]
+        q0, q1 = c * s["N"], min(s["Q"], (c + 1) * s["N"])
+        part = {(r, a): (I[:, :q1 - q0], code[:, :q1 - q0])
+                for (r, cc, a), (I, code) in dbg.items() if cc == c}
+        nd, nc = check_outputs_by_codes(Yg[:, q0:q1], part, weights, thr, scale)
+        n_out += Yg[:, q0:q1].size
+        n_diff += nd
+        n_codes += nc
+    return {"outputs_compared": n_out, "outputs_off_by_threshold_flips": n_diff,
+            "codes_behind_them": n_codes, "rule": "fp32(integer) x scale; integer off the "
+            "oracle's only by codes within 1e-4 of a threshold, <= 0.1 % of the codes"}
+
+
+def cpu_baseline_conv(work):
+    """The oracle on the whole convolution workload: every array's G' (one
+    process per tile) and the evaluation of every image (one process per
+    image), on the host's cores; then one tile and one image on one core."""
+    import multiprocessing as mp
+    import numpy as np
+    from paper_1809_00072_amd import workloads as wl
+    from oracle import fcm as ofcm
+    cv = work["conv"]
+    sc = _layer_scalars(work["W"], work["xbar"])
+    n = cv["n"]
+    ho, wo = ofcm.conv_out_hw(cv)
+    for img in range(n):
+        _SAMPLE[("img", img)] = {"W": work["W"], "xbar": work["xbar"], "periph": work["periph"],
+                                 "Xs": ofcm.im2col(work["X"], cv, [img]),
+                                 "cols": list(range(sc["C"])), **sc, "lay": sc}
+    _SAMPLE["conv"] = _SAMPLE[("img", 0)]
+    tasks = [("conv", r, c) for c in range(sc["C"]) for r in range(sc["R"])]
+    workers = oracle_workers()
+    ctx = mp.get_context("fork")
+    with ctx.Pool(workers, initializer=_one_thread_blas) as pool:
+        pool.map(_ready, range(workers))   # the workers are up before the clock starts
+        t0 = time.perf_counter()
+        built = pool.map(_oracle_tile, tasks, chunksize=1)
+        t1 = time.perf_counter()
+    gp = {(r, c): g for _, r, c, g, _ in built}
+    for img in range(n):
+        _SAMPLE[("img", img)]["gp"] = gp
+    # the evaluation: one process per image, forked after the build (the
+    # workers hold G'); one untimed pass first, then the timed one
+    img_tasks = [(("img", i), 0, ho * wo, False) for i in range(n)]
+    with ctx.Pool(workers, initializer=_one_thread_blas) as pool:
+        pool.map(_oracle_eval, img_tasks[:workers], chunksize=1)
+        t1b = time.perf_counter()
+        evals = pool.map(_oracle_eval, img_tasks, chunksize=1)
+        t2 = time.perf_counter()
+    t2 -= t1b - t1
+    for _, Y, _, _ in evals:
+        assert np.isfinite(Y).all()
+    macs = wl.alg_macs(work)
+    try:
+        from threadpoolctl import threadpool_limits
+        limit = threadpool_limits(limits=1)
+    except ImportError:
+        limit = None
+    _, _, _, _, t_tile = _oracle_tile(tasks[0])
+    _, _, _, t_img = _oracle_eval((("img", 0), 0, ho * wo, False))
+    if limit is not None:
+        limit.unregister()
+    t_one = t_tile * len(tasks) + t_img * n
+    model, ncores = host_info()
+    out = {"value": macs / (t2 - t0), "unit": "MAC/s", "cores": workers, "kind": "oracle",
+           "sample": "full workload once: G' of all %d arrays (%.2f s) + evaluation of all %d "
+                     "images (%.2f s), fp64 numpy/scipy, one process per tile / image"
+                     % (sc["R"] * sc["C"] * sc["A"], t1 - t0, n, t2 - t1),
+           "host": {"cpu": model, "cores_available": ncores, "workers": workers},
+           "one_core": {"value": macs / t_one, "unit": "MAC/s", "seconds": t_one,
+                        "sample": "one tile's build and one image's evaluation on one core, "
+                                  "scaled to the whole workload"}}
+    out["all_over_one_core"] = out["value"] / out["one_core"]["value"]
     return out
 
 
@@ -219,25 +539,61 @@ def bench_fc256(args):
     print(json.dumps(out), flush=True)
 
 
+STACK_DESC = {
+    "resnet18": "ResNet-18 shaped stack (21 layers), batch 64, 128x128 crossbars, wire 1 ohm, "
+                "8-bit DAC/ADC; step = evaluation of every layer (G' mapped once)",
+    "vgg16fc": "VGG-16 shaped FC head 25088->4096->4096->1000, batch 256, 64x64 crossbars, "
+               "8-bit weights in 4x2-bit slices, 8-bit DAC/ADC; step = evaluation of the three "
+               "layers (G' mapped once)",
+    "resnet50": "ResNet-50 shaped stack (54 layers), batch 128, %dx%d crossbars, wire %g ohm, "
+                "8-bit DAC/ADC; step = G' rebuild of all %d arrays from the step's weights + "
+                "evaluation of every layer (each step's weights W + 1e-3 sigma eps_t are drawn "
+                "before the timed region)",
+}
+
+
 def bench_stack(args):
-    """Every layer of a stacked workload, standalone on its seeded input."""
+    """Every layer of a stacked workload, standalone on its seeded input.
+
+    resnet50 (the default workload): a step rebuilds every array's G' from
+    that step's weights (model-in-the-loop re-training, G' regenerated every
+    step) and evaluates every layer; the line also gives the evaluation alone
+    (VMM only) and the rebuild alone (map only)."""
     import numpy as np
-    import torch
-    from paper_1809_00072_amd import rxnn, workloads as wl
-    rxnn.load()
-    assert torch.cuda.is_available(), "bench.py needs the HIP device"
-    dev = torch.device("cuda:0")
+    from paper_1809_00072_amd import workloads as wl
     cfg = args.workload
-    n_layers = {"resnet18": len(wl.resnet18_layers()), "vgg16fc": len(wl.vgg16_fc_layers()),
-                "resnet50": len(wl.resnet50_layers())}[cfg]
+    specs = {"resnet18": wl.resnet18_layers, "vgg16fc": wl.vgg16_fc_layers,
+             "resnet50": wl.resnet50_layers}[cfg]()
     rebuild = cfg == "resnet50"
-    layers = []
-    print("[bench] %s: generating %d layers" % (cfg, n_layers), file=sys.stderr, flush=True)
-    for l in range(n_layers):
+    print("[bench] %s: generating %d layers" % (cfg, len(specs)), file=sys.stderr, flush=True)
+    works = []
+    for l in range(len(specs)):
         w = wl.stack_layer(cfg, l, crossbar=args.crossbar if rebuild else None,
                            wire=args.wire if rebuild else None)
         if rebuild:
             w["xbar"] = device_options(w["xbar"], args, seed=5000 + l)
+        works.append(w)
+    macs = wl.stack_alg_macs(cfg)
+    total_arrays = 0
+    for w in works:
+        sc = _layer_scalars(w["W"], w["xbar"])
+        total_arrays += sc["R"] * sc["C"] * sc["A"]
+    # the oracle's sample runs first, before the GPU is touched (its worker
+    # processes fork from this one)
+    cpu = results = None
+    if not args.no_cpu_baseline:
+        cpu, results = oracle_sample(works, total_arrays, macs)
+        print("[bench] oracle: %.3g MAC/s extrapolated on %d workers (%.3g on one core)"
+              % (cpu["value"], cpu["cores"], cpu["one_core"]["value"]), file=sys.stderr,
+              flush=True)
+
+    import torch
+    from paper_1809_00072_amd import rxnn
+    rxnn.load()
+    assert torch.cuda.is_available(), "bench.py needs the HIP device"
+    dev = torch.device("cuda:0")
+    layers = []
+    for l, w in enumerate(works):
         Wd = torch.from_numpy(w["W"]).to(dev)
         Xd = torch.from_numpy(w["X"]).to(dev)
         L = rxnn.map_layer(Wd, w["xbar"])
@@ -245,7 +601,7 @@ def bench_stack(args):
             Y = rxnn.conv_layer(L, w["periph"], w["conv"], Xd)
         else:
             Y = rxnn.crossbar_vmm(L, w["periph"], Xd)
-        ent = {"w": w, "L": L, "X": Xd, "Y": Y, "W": Wd, "Wt": []}
+        ent = {"L": L, "X": Xd, "Y": Y, "W": Wd, "Wt": []}
         if rebuild:
             # model-in-the-loop update of every step: W + 1e-3 sigma eps_t
             sigma = float(np.sqrt(2.0 / w["W"].shape[0]))
@@ -253,13 +609,13 @@ def bench_stack(args):
                 g = torch.Generator(device=dev).manual_seed(3000 + t)
                 eps = torch.randn(Wd.shape, generator=g, device=dev)
                 ent["Wt"].append(Wd + 1e-3 * sigma * eps)
-        del w["X"]
+        w["X"] = None
         layers.append(ent)
     torch.cuda.synchronize()
     stream = torch.cuda.current_stream()
 
-    def evaluate(e):
-        w = e["w"]
+    def evaluate(l):
+        e, w = layers[l], works[l]
         if w["kind"] == "conv":
             rxnn.conv_layer(e["L"], w["periph"], w["conv"], e["X"], e["Y"], stream)
         else:
@@ -270,104 +626,144 @@ def bench_stack(args):
     # and every evaluation waits for its layer's rebuild.
     build_streams = [torch.cuda.Stream(device=dev) for _ in range(8)] if rebuild else []
 
+    def rebuild_all(t):
+        done = []
+        for i, e in enumerate(layers):
+            bs = build_streams[i % len(build_streams)]
+            bs.wait_stream(stream)
+            rxnn.remap_layer(e["L"], e["Wt"][t], bs)
+            ev = torch.cuda.Event()
+            ev.record(bs)
+            done.append(ev)
+        return done
+
     def step(t):
         if rebuild:
-            done = []
-            for i, e in enumerate(layers):
-                bs = build_streams[i % len(build_streams)]
-                bs.wait_stream(stream)
-                rxnn.remap_layer(e["L"], e["Wt"][t], bs)
-                ev = torch.cuda.Event()
-                ev.record(bs)
-                done.append(ev)
-            for e, ev in zip(layers, done):
+            for l, ev in enumerate(rebuild_all(t)):
                 stream.wait_event(ev)
-                evaluate(e)
+                evaluate(l)
         else:
-            for e in layers:
-                evaluate(e)
+            for l in range(len(layers)):
+                evaluate(l)
+
+    def timed(fn, n, level):
+        rxnn.profile_reset()
+        rxnn.profile_enable(level)
+        ev0 = torch.cuda.Event(enable_timing=True)
+        ev1 = torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        ev0.record(stream)
+        for i in range(n):
+            fn(i)
+        ev1.record(stream)
+        torch.cuda.synchronize()
+        rxnn.profile_enable(0)
+        return ev0.elapsed_time(ev1) / n
 
     for t in range(args.warmup):
         step(t)
     torch.cuda.synchronize()
     # timed steps: only the evaluation kernel carries timing events (an event
     # pair around every launch would leave the GPU idle between kernels)
-    rxnn.profile_reset()
-    rxnn.profile_enable(2)
-    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    ev0.record(stream)
-    for t in range(args.steps):
-        step(args.warmup + t)
-    ev1.record(stream)
-    torch.cuda.synchronize()
-    rxnn.profile_enable(False)
-    step_ms = ev0.elapsed_time(ev1) / args.steps
-    # per-kernel breakdown: the same steps again (same weights), every launch timed
+    w0 = time.perf_counter()
+    step_ms = timed(lambda i: step(args.warmup + i), args.steps, 2)
+    wall = time.perf_counter() - w0
+    print("[bench] timed %d steps: %.3f ms/step" % (args.steps, step_ms), file=sys.stderr,
+          flush=True)
+    # per-kernel breakdown: the same steps again, every launch timed
+    kern = None
     if rebuild or args.breakdown:
-        rxnn.profile_reset()
-        rxnn.profile_enable(1)
-        for t in range(args.steps):
-            step(args.warmup + t)
-        torch.cuda.synchronize()
-        rxnn.profile_enable(False)
-    kern = read_kernels(rxnn, args.steps)
-    # evaluation alone (G' kept); the evaluation kernel's roofline is taken
-    # here, where no rebuild of another layer shares the GPU with it
-    rxnn.profile_reset()
-    rxnn.profile_enable(2)
-    ev0.record(stream)
-    for _ in range(args.steps):
-        for e in layers:
-            evaluate(e)
-    ev1.record(stream)
-    torch.cuda.synchronize()
-    rxnn.profile_enable(False)
-    eval_ms = ev0.elapsed_time(ev1) / args.steps
+        timed(lambda i: step(args.warmup + i), args.steps, 1)
+        kern = read_kernels(rxnn, args.steps)
+    # the rebuild alone (map only), on the same streams
+    map_ms = None
+    if rebuild:
+        def map_only(i):
+            for ev in rebuild_all(args.warmup + i):
+                stream.wait_event(ev)
+        map_ms = timed(map_only, args.steps, 0)
+    # the evaluation alone (VMM only, G' kept): the evaluation kernel's
+    # roofline is taken here, where no rebuild shares the GPU with it
+    def eval_all(i):
+        for l in range(len(layers)):
+            evaluate(l)
+    eval_ms = timed(eval_all, args.steps, 2)
     kern_eval = read_kernels(rxnn, args.steps)
-    # model generation (the paper's phase 1): one G' build of every array of
-    # every layer, on one stream (the mapped-once stacks time it here; for the
-    # rebuilt stack it is part of every step)
+    # and once more with every launch timed: the DAC pass and the finish
+    # kernel's achieved HBM bandwidth (their algorithmic bytes per launch are
+    # counted by the library)
+    timed(eval_all, args.steps, 1)
+    kern_eval_all = read_kernels(rxnn, args.steps)
+    hbm = {}
+    for name, what in (("dac", "k_dac: DAC of every input into the (padded) V buffer; "
+                                "4 B read per input + 4 B written per V element"),
+                       ("finish", "k_finish / k_finish_nchw: shared tiles' int32 workspace -> "
+                                  "Y; 12 B per output (read, zeroing write, fp32 write)")):
+        tot_ms, cnt = rxnn.profile_read(name)
+        if cnt:
+            gbs = rxnn.profile_bytes(name) / (tot_ms * 1e-3) / 1e9
+            hbm[name] = {"what": what, "us_per_step": 1e3 * tot_ms / args.steps,
+                         "bytes_per_step": rxnn.profile_bytes(name) / args.steps,
+                         "achieved": gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                         "frac": gbs / HBM_PEAK_GBS}
     gen = None
     if not rebuild:
-        torch.cuda.synchronize()
-        ev0.record(stream)
-        for e in layers:
-            rxnn.remap_layer(e["L"], e["W"], stream)
-        ev1.record(stream)
-        torch.cuda.synchronize()
-        gen = generation_info(ev0.elapsed_time(ev1),
-                              int(sum(e["L"].R * e["L"].C * e["L"].A for e in layers)),
-                              layers[0]["L"].M, layers[0]["L"].N)
-    macs = wl.stack_alg_macs(cfg)
+        # model generation (the paper's phase 1): one G' build of every array
+        # of every layer, on one stream
+        def gen_all(i):
+            for e in layers:
+                rxnn.remap_layer(e["L"], e["W"], stream)
+        gen = generation_info(timed(gen_all, 1, 0), total_arrays, layers[0]["L"].M,
+                              layers[0]["L"].N)
+    parity = None
+    if results is not None:
+        try:
+            parity = sample_parity(works, layers, results, rxnn, torch, stream)
+        except AssertionError as exc:
+            parity = {"FAILED": str(exc)}
+        print("[bench] sample parity: %s" % parity, file=sys.stderr, flush=True)
     vmm_us = kern_eval["xbar_vmm"]["us_per_step"]
     ach = 2.0 * macs / (vmm_us * 1e-6) / 1e12
-    desc = {"resnet18": "ResNet-18 shaped stack (21 layers), batch 64, 128x128 crossbars, "
-                        "wire 1 ohm, 8-bit DAC/ADC; step = evaluation of every layer",
-            "vgg16fc": "VGG-16 shaped FC head 25088->4096->4096->1000, batch 256, 64x64 "
-                       "crossbars, 8-bit weights in 4x2-bit slices, 8-bit DAC/ADC; step = "
-                       "evaluation of the three layers",
-            "resnet50": "ResNet-50 shaped stack (54 layers), batch 128, %dx%d crossbars, wire "
-                        "%g ohm, 8-bit DAC/ADC; step = weight update + G' rebuild + evaluation "
-                        "of every layer" % (args.crossbar, args.crossbar, args.wire)
-                        + device_note(args)}[cfg]
-    value_ms = step_ms
+    M, N = layers[0]["L"].M, layers[0]["L"].N
+    desc = STACK_DESC[cfg]
+    if rebuild:
+        desc = desc % (M, N, args.wire, total_arrays) + device_note(args)
+    traffic = STACK_VMM_TRAFFIC.get((cfg, M, args.wire if rebuild else None))
     out = {
         "metric": "non-ideal crossbar MACs/sec per layer",
-        "value": macs / (value_ms * 1e-3),
+        "value": macs / (step_ms * 1e-3),
         "unit": "MAC/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
-        "ms_per_step": value_ms, "higher_is_better": True, "scaling": "weak",
+        "ms_per_step": step_ms, "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "f32", "data": "synthetic",
-        "config": {"workload": desc, "alg_macs_per_step": macs,
-                   "arrays": int(sum(e["L"].R * e["L"].C * e["L"].A for e in layers))},
-        "roofline": {"kernel": "k_xbar_vmm (all layers)", "bound": "mfma", "achieved": ach,
-                     "peak": FP32_MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
-                     "frac": ach / FP32_MFMA_PEAK_TFLOPS, "traffic": None},
-        "eval_only": {"ms": eval_ms, "value": macs / (eval_ms * 1e-3), "unit": "MAC/s",
+        "config": {"workload": desc, "alg_macs_per_step": macs, "arrays": total_arrays},
+        "roofline": {"kernel": "k_xbar_vmm, summed over the layers of an evaluation-only pass",
+                     "bound": "mfma", "achieved": ach, "peak": FP32_MFMA_PEAK_TFLOPS,
+                     "unit": "TFLOP/s", "frac": ach / FP32_MFMA_PEAK_TFLOPS,
+                     "traffic": traffic, "us_per_pass": vmm_us,
+                     "flops_per_pass": 2.0 * macs},
+        "eval_only": {"what": "VMM only: DAC, V.G', ADC, accumulation of every layer, G' kept",
+                      "ms": eval_ms, "value": macs / (eval_ms * 1e-3), "unit": "MAC/s",
                       "kernels": kern_eval},
-        "kernels": kern,
+        "hbm": hbm,
+        "wall_s_timed": wall,
     }
+    if kern is not None:
+        out["kernels"] = kern
+    if rebuild:
+        b_flops = sum(e["L"].R * e["L"].C * e["L"].A for e in layers) * build_flops(M, N)
+        b_ach = b_flops / (map_ms * 1e-3) / 1e12
+        out["map_only"] = {"what": "G' rebuild of every array (w_max + fp64 build), 8 streams",
+                           "ms": map_ms, "fp64_flops": b_flops, "achieved": b_ach,
+                           "peak": FP64_PEAK_TFLOPS, "unit": "TFLOP/s",
+                           "frac": b_ach / FP64_PEAK_TFLOPS,
+                           "generation": generation_info(map_ms, total_arrays, M, N)}
     if gen is not None:
         out["generation"] = gen
+    if cpu is not None:
+        cpu["speedup_gpu_over_oracle"] = out["value"] / cpu["value"]
+        out["cpu_baseline"] = cpu
+    if parity is not None:
+        out["sample_parity"] = parity
     for e in layers:
         e["L"].free()
     print(json.dumps(out), flush=True)
@@ -478,7 +874,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-probe", action="store_true",
                     help="also run a plain 2 GiB copy kernel (counter calibration)")
-    ap.add_argument("--workload", default="conv3x3",
+    ap.add_argument("--workload", default="resnet50",
                     choices=["conv3x3", "fc256", "resnet18", "vgg16fc", "resnet50"])
     ap.add_argument("--crossbar", type=int, default=256, help="resnet50: crossbar side")
     ap.add_argument("--wire", type=float, default=2.5, help="resnet50: wire resistance (Ohm)")
@@ -503,18 +899,25 @@ def main():
     if args.workload == "fc256":
         return bench_fc256(args)
 
-    import numpy as np
-    import torch
-    from paper_1809_00072_amd import rxnn, workloads as wl
+    from paper_1809_00072_amd import workloads as wl
 
-    rxnn.load()
-    assert torch.cuda.is_available(), "bench.py needs the HIP device"
     work = wl.conv3x3_64_56()
     cv, xb, pp = work["conv"], work["xbar"], work["periph"]
     xb = device_options(xb, args)
     if args.divider:
         xb = dict(xb, r_driver=0.0)
         pp = dict(pp, dac_bend=0.0, dac_g_on=DIVIDER_G_ON, dac_g_pd=DIVIDER_G_PD)
+    # the oracle first, before the GPU is touched (its worker processes fork
+    # from this one)
+    cpu = None
+    if not args.no_cpu_baseline:
+        print("[bench] oracle on the host", file=sys.stderr, flush=True)
+        cpu = cpu_baseline_conv(dict(work, xbar=xb, periph=pp))
+
+    import torch
+    from paper_1809_00072_amd import rxnn
+    rxnn.load()
+    assert torch.cuda.is_available(), "bench.py needs the HIP device"
     dev = torch.device("cuda:0")
     Wd = torch.from_numpy(work["W"]).to(dev)
     Xd = torch.from_numpy(work["X"]).to(dev)
@@ -573,6 +976,15 @@ def main():
     ev1.record(stream)
     torch.cuda.synchronize()
     eval_ms = ev0.elapsed_time(ev1) / args.steps
+    hbm = {}
+    for name in ("dac", "finish"):
+        tot_ms, cnt = rxnn.profile_read(name)
+        if cnt:
+            gbs = rxnn.profile_bytes(name) / (tot_ms * 1e-3) / 1e9
+            hbm[name] = {"us_per_step": 1e3 * tot_ms / args.steps,
+                         "bytes_per_step": rxnn.profile_bytes(name) / args.steps,
+                         "achieved": gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                         "frac": gbs / HBM_PEAK_GBS}
 
     # the dominant single kernel is the evaluation kernel (timed in the timed region)
     vmm_us = vmm_timed["avg_us"]
@@ -616,6 +1028,7 @@ def main():
         "roofline": roof,
         "build": build,
         "eval_only": {"ms": eval_ms, "value": macs / (eval_ms * 1e-3), "unit": "MAC/s"},
+        "hbm": hbm,
         "ideal_fp32": ideal,
         "kernels": kern,
         "kernels_pass": "a second pass of the same steps with every launch timed",
@@ -623,9 +1036,9 @@ def main():
     }
     if retrain is not None:
         out["retrain"] = retrain
-    if not args.no_cpu_baseline:
-        print("[bench] oracle on the host", file=sys.stderr, flush=True)
-        out["cpu_baseline"] = cpu_baseline(dict(work, xbar=xb, periph=pp))
+    if cpu is not None:
+        cpu["speedup_gpu_over_oracle"] = out["value"] / cpu["value"]
+        out["cpu_baseline"] = cpu
     L.free()
     print(json.dumps(out), flush=True)
 

@@ -306,10 +306,18 @@ void rxnn_free_layer(rxnn_layer* layer);
  * leaves the workspace zeroed), "bw_gemm" (the backward pass's GEMMs) and
  * "bw_aux" (its masks, unrolling and gathers).  rxnn_profile_read synchronises, folds pending events
  * into the totals and returns total milliseconds and launch count.
+ * rxnn_profile_bytes returns, for the same timed launches, the sum of their
+ * algorithmic HBM bytes where the library counts them ("dac": 4 bytes per
+ * input read plus 4 per DAC output written; "finish": 12 bytes per output it
+ * converts, the int32 read, its zeroing and the fp32 write), else 0; divided
+ * by rxnn_profile_read's time it is the kernel's achieved bandwidth.  Both
+ * take a NUL-terminated kernel name and host output pointers (RXNN_EINVAL
+ * when NULL).
  */
 rxnn_status rxnn_profile_enable(int32_t on);
 rxnn_status rxnn_profile_reset(void);
 rxnn_status rxnn_profile_read(const char* kernel, double* total_ms, int64_t* count);
+rxnn_status rxnn_profile_bytes(const char* kernel, double* bytes);
 
 const char* rxnn_status_string(rxnn_status status);
 const char* rxnn_last_error(void);

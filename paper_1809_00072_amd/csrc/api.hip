@@ -194,10 +194,16 @@ rxnn_status make_periph(const rxnn_periph_params* pp, const MapScalars& ms, Peri
 struct Pending {
   std::string name;
   hipEvent_t a, b;
+  double bytes;
+};
+struct ProfTotal {
+  double ms = 0.0;
+  int64_t count = 0;
+  double bytes = 0.0;
 };
 int g_prof = 0;   // 0 off, 1 every kernel, 2 the evaluation kernel only
 std::vector<Pending> g_pending;
-std::map<std::string, std::pair<double, int64_t>> g_prof_tot;
+std::map<std::string, ProfTotal> g_prof_tot;
 
 // Frees every device buffer of a layer and the handle itself.
 void release_buffers(rxnn_layer* L) {
@@ -310,7 +316,9 @@ rxnn_status run_vmm(const rxnn_layer* L, const PeriphScalars& ps, const float* X
     Lm->vbuf_bytes = (size_t)n_v * sizeof(float);
   }
   {
-    ProfScope t("dac", s);
+    // algorithmic bytes: every input read once, every V element written once
+    const double n_in = conv ? (double)conv->n * conv->c_in * conv->h * conv->w : (double)Bv * ms.P;
+    ProfScope t("dac", s, 4.0 * (n_in + (double)n_v));
     HIP_TRY(launch_dac(ms, ps, conv, X, Bv, L->vbuf, s));
   }
   VmmLaunch vl;
@@ -346,7 +354,8 @@ rxnn_status run_vmm(const rxnn_layer* L, const PeriphScalars& ps, const float* X
     HIP_TRY(launch_xbar_vmm(ms, ps, L->gpt, vl, plan, s));
   }
   if (workers > 0) {
-    ProfScope t("finish", s);
+    // per output of a shared tile: the int32 read, its zeroing write, the fp32 write
+    ProfScope t("finish", s, 12.0 * (double)(Bv - plan.row0) * (double)ms.Q);
     HIP_TRY(launch_finish(ms, ps, iacc_ws, plan.row0, Bv, Y, hw_out, s));
     Lw->ws_dirty = false;
   }
@@ -405,7 +414,8 @@ hipError_t build_gprime(rxnn_layer* L, const float* W, hipStream_t s) {
 
 namespace rxnn {
 
-ProfScope::ProfScope(const char* name, hipStream_t s) : name_(name), s_(s), on_(false) {
+ProfScope::ProfScope(const char* name, hipStream_t s, double bytes)
+    : name_(name), s_(s), bytes_(bytes), on_(false) {
   if (!g_prof || (g_prof == 2 && strcmp(name, "xbar_vmm") != 0)) return;
   // no system-scope fence: a timing event then costs no cache flush on the GPU
   if (hipEventCreateWithFlags(&a_, hipEventDisableSystemFence) != hipSuccess) return;
@@ -429,7 +439,7 @@ ProfScope::~ProfScope() {
     return;
   }
   std::lock_guard<std::mutex> g(g_mu);
-  g_pending.push_back(Pending{name_, a_, b_});
+  g_pending.push_back(Pending{name_, a_, b_, bytes_});
 }
 
 }  // namespace rxnn
@@ -913,8 +923,8 @@ rxnn_status rxnn_profile_reset(void) {
   return RXNN_OK;
 }
 
-rxnn_status rxnn_profile_read(const char* kernel, double* total_ms, int64_t* count) {
-  if (!kernel || !total_ms || !count) return fail(RXNN_EINVAL, "NULL argument");
+// Folds the pending event pairs into the per-kernel totals.
+static rxnn_status fold_pending() {
   std::vector<Pending> p;
   {
     std::lock_guard<std::mutex> g(g_mu);
@@ -928,14 +938,33 @@ rxnn_status rxnn_profile_read(const char* kernel, double* total_ms, int64_t* cou
     (void)hipEventDestroy(e.b);
     std::lock_guard<std::mutex> g(g_mu);
     auto& t = g_prof_tot[e.name];
-    t.first += ms;
-    t.second += 1;
+    t.ms += ms;
+    t.count += 1;
+    t.bytes += e.bytes;
   }
-  std::lock_guard<std::mutex> g(g_mu);
-  auto it = g_prof_tot.find(kernel);
-  *total_ms = it == g_prof_tot.end() ? 0.0 : it->second.first;
-  *count = it == g_prof_tot.end() ? 0 : it->second.second;
   return RXNN_OK;
 }
+
+rxnn_status rxnn_profile_read(const char* kernel, double* total_ms, int64_t* count) {
+  if (!kernel || !total_ms || !count) return fail(RXNN_EINVAL, "NULL argument");
+  rxnn_status st = fold_pending();
+  if (st) return st;
+  std::lock_guard<std::mutex> g(g_mu);
+  auto it = g_prof_tot.find(kernel);
+  *total_ms = it == g_prof_tot.end() ? 0.0 : it->second.ms;
+  *count = it == g_prof_tot.end() ? 0 : it->second.count;
+  return RXNN_OK;
+}
+
+rxnn_status rxnn_profile_bytes(const char* kernel, double* bytes) {
+  if (!kernel || !bytes) return fail(RXNN_EINVAL, "NULL argument");
+  rxnn_status st = fold_pending();
+  if (st) return st;
+  std::lock_guard<std::mutex> g(g_mu);
+  auto it = g_prof_tot.find(kernel);
+  *bytes = it == g_prof_tot.end() ? 0.0 : it->second.bytes;
+  return RXNN_OK;
+}
+
 
 }  // extern "C"

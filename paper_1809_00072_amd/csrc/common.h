@@ -184,11 +184,14 @@ hipError_t launch_bw_col2im(const float* dcols, const float* X, const rxnn_conv_
                             int wo, float x_max, float* dX, hipStream_t s);
 
 // ---- kernel timing (api.hip) ------------------------------------------------
+// `bytes`: the launch's algorithmic HBM bytes, summed per kernel name for the
+// achieved bandwidth of memory-bound kernels (0 where it is not counted).
 struct ProfScope {
-  ProfScope(const char* name, hipStream_t s);
+  ProfScope(const char* name, hipStream_t s, double bytes = 0.0);
   ~ProfScope();
   const char* name_;
   hipStream_t s_;
+  double bytes_;
   hipEvent_t a_, b_;
   bool on_;
 };

@@ -22,6 +22,7 @@ EXPORTS = (
     "rxnn_set_gprime", "rxnn_vmm_debug", "rxnn_layer_info", "rxnn_layer_wmax",
     "rxnn_free_layer", "rxnn_profile_enable", "rxnn_profile_reset", "rxnn_profile_read",
     "rxnn_status_string", "rxnn_last_error", "rxnn_fc_backward", "rxnn_conv_backward",
+    "rxnn_profile_bytes",
 )
 
 
@@ -88,6 +89,7 @@ def load(path: str = LIB_PATH):
         "rxnn_profile_enable": ([i32], i32),
         "rxnn_profile_reset": ([], i32),
         "rxnn_profile_read": ([ctypes.c_char_p, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(i64)], i32),
+        "rxnn_profile_bytes": ([ctypes.c_char_p, ctypes.POINTER(ctypes.c_double)], i32),
         "rxnn_fc_backward": ([vp, ctypes.POINTER(PeriphParams), vp, vp, vp, i64, vp, vp, vp], i32),
         "rxnn_conv_backward": ([vp, ctypes.POINTER(PeriphParams), ctypes.POINTER(ConvDesc), vp, vp,
                                 vp, vp, vp, vp], i32),
@@ -348,3 +350,11 @@ def profile_read(kernel):
     n = ctypes.c_int64()
     _check(load().rxnn_profile_read(kernel.encode(), ctypes.byref(t), ctypes.byref(n)))
     return t.value, n.value
+
+
+def profile_bytes(kernel):
+    """Algorithmic HBM bytes of the timed launches of one kernel name since the
+    last reset (0 where the library does not count them)."""
+    b = ctypes.c_double()
+    _check(load().rxnn_profile_bytes(kernel.encode(), ctypes.byref(b)))
+    return b.value

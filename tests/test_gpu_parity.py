@@ -13,7 +13,8 @@ from oracle import mapping as omap
 from oracle import periph as oper
 from oracle.network import gprime_nodal
 
-from parity import (array_weights, check_codes, check_currents, check_gprime, FLIP_FRAC)
+from parity import (array_weights, check_codes, check_currents, check_gprime,
+                    check_outputs_by_codes)
 
 torch = pytest.importorskip("torch")
 pytestmark = pytest.mark.gpu
@@ -440,30 +441,47 @@ def test_adc_codes_exact_at_thresholds():
 # ---------------------------------------------------------------------------
 
 def conv_compare(cv, W, X, xb, pp, images=None, label="conv"):
+    """Map + convolution on the GPU (production launch) against the oracle on
+    the images ``images`` (default: all).
+
+    Quantising ADC: ``parity.check_outputs_by_codes`` per column tile, with
+    the oracle's per-array currents and codes over those images' patch rows:
+    every output is fp32(integer) * scale, and its integer may differ from the
+    oracle's only by codes whose current lies on a threshold (within 1e-4),
+    for at most 0.1 % of the codes behind the sample.  Ideal ADC: the
+    accumulated currents within 1e-4 of the summed magnitudes."""
     say(label, "map")
     L = rxnn.map_layer(dev(W), xb)
     say(label, "conv_layer")
     Y = rxnn.conv_layer(L, pp, cv, dev(X)).cpu().numpy()
     lay = omap.map_layer(W, xb)
     imgs = list(range(cv["n"])) if images is None else images
-    Yo = ofcm.conv_layer(X, lay, xb, pp, cv, images=imgs)
     Yg = Y[imgs]
     if pp["adc_bits"] == 0:
+        Yo = ofcm.conv_layer(X, lay, xb, pp, cv, images=imgs)
         cols = ofcm.im2col(X, cv, imgs)
         bound = np.abs(cols).astype(np.float64) @ np.abs(W).astype(np.float64)
         ho, wo = ofcm.conv_out_hw(cv)
         bound = bound.reshape(len(imgs), ho, wo, -1).transpose(0, 3, 1, 2)
         assert np.all(np.abs(Yg - Yo) <= 1e-4 * bound * 2 + 1e-6)
+        L.free()
         return
+    _, dbg = ofcm.conv_layer(X, lay, xb, pp, cv, images=imgs, debug=True)
+    Q, N = W.shape[1], lay["N"]
+    rows = Yg.transpose(0, 2, 3, 1).reshape(-1, Q)        # patch rows x Q
+    thr = oracle_thresholds(pp, lay["M"], xb["g_max"])
     scale = oper.output_scale(pp, lay["M"], xb["g_max"], lay["s_w_eff"])
-    d = np.rint((Yg.astype(np.float64) - Yo.astype(np.float64)) / float(scale))
-    assert np.allclose(Yg, Yo + d * scale, rtol=1e-6, atol=0)
-    # each ADC flip moves an output by one code step; allow the flip budget
-    n_conv = lay["R"] * lay["A"]
-    assert np.abs(d).max() <= n_conv
-    frac = np.count_nonzero(d) / d.size
-    assert frac <= n_conv * FLIP_FRAC, f"{frac:.3g} of outputs differ"
-    say(label, "outputs differing by a flip: %.3g" % frac)
+    weights = array_weights(lay["A"], omap.slicing(xb)[1])
+    n_diff = n_codes = 0
+    for c in range(lay["C"]):
+        q0, q1 = c * N, min(Q, (c + 1) * N)
+        part = {(r, a): (I[:, :q1 - q0], code[:, :q1 - q0])
+                for (r, cc, a), (I, code) in dbg.items() if cc == c}
+        nd, nc = check_outputs_by_codes(rows[:, q0:q1], part, weights, thr, scale)
+        n_diff += nd
+        n_codes += nc
+    say(label, "outputs differing by a threshold flip: %d (of %d codes)" % (n_diff, n_codes))
+    L.free()
 
 
 @pytest.mark.parametrize("n,c_in,hw,c_out,k,s,p,M,N,dac", [

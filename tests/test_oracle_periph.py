@@ -30,23 +30,21 @@ def test_dac_lut_shape(bits):
 
 
 def test_dac_codes_rounding_and_clamp():
-    bits, x_max = 4, 1.0
-    s = pp.dac_scale_in(bits, x_max)          # fp32(15)
-    assert s == np.float32(15.0)
-    # exact ties of x * 15 round to even
-    x = np.array([0.5 / 15, 1.5 / 15, 2.5 / 15], dtype=np.float64)
-    x32 = x.astype(np.float32)
-    prod = x32 * s
-    ties = prod == np.rint(prod * 2) / 2
+    # x_max = 15/16 makes s_in = fp32(15 / x_max) = 16 exactly, so x = (k + 1/2) / 16
+    # (exact in fp32) gives products that are exact ties
+    bits, x_max = 4, 15.0 / 16.0
+    s = pp.dac_scale_in(bits, x_max)
+    assert s == np.float32(16.0)
+    ties = (np.arange(8) + 0.5) / 16.0
+    x32 = ties.astype(np.float32)
+    assert np.all(x32 * s == np.arange(8) + 0.5)                  # every product is a tie
     codes = pp.dac_codes(x32, bits, x_max)
-    for p, c in zip(prod, codes):
-        if p == np.floor(p) + 0.5:
-            assert c % 2 == 0
-        else:
-            assert c == int(np.floor(p + 0.5))
-    assert ties.any() or True
+    assert codes.tolist() == [0, 2, 2, 4, 4, 6, 6, 8]             # ties go to even
+    # off-tie products round to nearest
+    off = np.array([0.49, 0.51, 1.49, 1.51, 7.2, 7.8], dtype=np.float64) / 16.0
+    assert pp.dac_codes(off.astype(np.float32), bits, x_max).tolist() == [0, 1, 1, 2, 7, 8]
     # unipolar clamp
-    assert list(pp.dac_codes(np.array([-1.0, 0.0, 1.0, 7.5], np.float32), bits, x_max)) == [0, 0, 15, 15]
+    assert list(pp.dac_codes(np.array([-1.0, 0.0, 1.0, 7.5], np.float32), bits, 1.0)) == [0, 0, 15, 15]
 
 
 def test_dac_codes_vs_integer_reference():
@@ -112,7 +110,19 @@ def test_adc_bend_shape():
 
 
 def test_output_scale():
-    per = dict(dac_bits=4, x_max=1.0, v_read=0.2, dac_bend=0.1, adc_bits=8, adc_bend=0.05)
-    s = pp.output_scale(per, 64, 5e-5, 2.0e-4)
-    lsb = 0.2 * 64 * 5e-5 / 255
-    assert s == np.float32(lsb / (0.2 * 2.0e-4))
+    """The output scale turns a code count back into units of w x, fixed by the
+    physics of one differential pair: a weight w_max on a one-row array with
+    ideal input x_max drives v_read (g_max - g_min) more current into the
+    positive array than into the negative one.  With g_min = g_max (1 - k / L)
+    that difference is exactly k LSBs of the ADC (I_FS = v_read g_max for
+    M = 1), so k codes must read back as w_max x_max."""
+    L = 255
+    for k, w_max, x_max in ((51, 0.3, 2.0), (17, 1.0, 1.0), (200, 0.05, 4.0)):
+        g_max = 5e-5
+        g_min = g_max * (1.0 - k / L)
+        per = dict(dac_bits=8, x_max=x_max, v_read=0.2, dac_bend=0.0, adc_bits=8, adc_bend=0.0)
+        s_w = (g_max - g_min) / w_max                    # conductance per unit weight
+        lsb = pp.adc_full_scale(per, 1, g_max) / L
+        assert abs(0.2 * (g_max - g_min) / lsb - k) < 1e-9 * k
+        y = float(np.float32(k) * pp.output_scale(per, 1, g_max, s_w))
+        assert abs(y - w_max * x_max) <= 2e-7 * w_max * x_max
