@@ -375,19 +375,22 @@ __global__ __launch_bounds__(NTHR, 2) void k_xbar_vmm(VmmArgs va) {
     }
     if (GRP) {
       // the pair's arrays of row tiles 2 r, 2 r + 1 and column tiles 2 c,
-      // 2 c + 1; a missing row or column tile (odd R or C) reads either zero
-      // (past the end of G') or a real array whose inputs are zero
+      // 2 c + 1; a missing row or column tile (odd R or C) is read as zeros:
+      // its lanes take the out-of-range offset in their own (VGPR) offset,
+      // which the buffer's range check always covers
       const int64_t a0 = ((int64_t)(2 * c) * ms.R + 2 * r) * ms.A + 2 * ap;
       const int64_t left = ((int64_t)ms.C * ms.R * ms.A - a0) * tile_elems * 4;
       const __amdgpu_buffer_rsrc_t gq =
           uniform_rsrc(va.gpt + a0 * tile_elems, min(left, (int64_t)0x7fffffff));
+      const bool row_absent = 2 * r + ((tid & 15) >> 3) >= ms.R;
 #pragma unroll
       for (int it = 0; it < GV4; ++it) {
         const int p = it / 4, dc = (it % 4) >> 1, nb = 16 * (it & 1);
-        const int soff = __builtin_amdgcn_readfirstlane(
+        const bool absent = row_absent || 2 * c + dc >= ms.C;
+        const int soff = absent ? 0 : __builtin_amdgcn_readfirstlane(
             (((dc * ms.R * ms.A) + p) * tile_elems + nb * 32) * 4);
-        gr[it] = __builtin_bit_cast(f32x4,
-                                    __builtin_amdgcn_raw_buffer_load_b128(gq, goff_g, soff, 0));
+        gr[it] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(
+            gq, absent ? kOob : goff_g, soff, 0));
       }
       return;
     }
