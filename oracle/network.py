@@ -88,8 +88,8 @@ def _solve_nodal(G, Vin_cols, r_driver, r_sense, r_row, r_col):
     """
     G = np.asarray(G, dtype=np.float64)
     M, N = G.shape
-    if np.any(G <= 0):
-        raise ValueError("device conductances must be positive")
+    if not np.all(np.isfinite(G)) or np.any(G < 0):
+        raise ValueError("device conductances must be finite and >= 0 (0: an open device)")
     for r in (r_driver, r_sense, r_row, r_col):
         if r < 0:
             raise ValueError("resistances must be non-negative")
@@ -270,8 +270,8 @@ def gprime_rowsweep(G, r_driver, r_sense, r_row, r_col):
     """
     G = np.asarray(G, dtype=np.float64)
     M, N = G.shape
-    if np.any(G <= 0):
-        raise ValueError("device conductances must be positive")
+    if not np.all(np.isfinite(G)) or np.any(G < 0):
+        raise ValueError("device conductances must be finite and >= 0 (0: an open device)")
     if not (r_row > 0 and r_col > 0 and r_sense > 0 and r_driver >= 0):
         raise ValueError("the row sweep needs positive wire and sense resistances")
     g_in, g_r, g_c, g_s = 1.0 / (r_driver + r_row), 1.0 / r_row, 1.0 / r_col, 1.0 / r_sense

@@ -38,6 +38,9 @@ namespace rxnn {
 namespace {
 
 constexpr int TG = 16;  // thread grid side
+// Impedance of an open device: its admittance 1e-30 S is 25 orders of
+// magnitude below g_min's, far below what an fp64 sum can see.
+constexpr double kOpenOhm = 1e30;
 
 __device__ __forceinline__ double device_conductance(const MapScalars& ms, const float* W,
                                                      double wmax, int r, int c, int a,
@@ -172,7 +175,12 @@ __global__ __launch_bounds__(TG* TG) void k_gprime_build(MapScalars ms, const fl
         double z;
         if (row < N && col < N) {
           z = ms.r_driver + ms.r_row * (double)(min(row, col) + 1);
-          if (row == col) z += 1.0 / device_conductance(ms, W, wmax, r, c, a, i, row);
+          if (row == col) {
+            // a device of zero conductance (a variation factor of 0) is an
+            // open circuit: kOpenOhm stands for its infinite impedance
+            const double g = device_conductance(ms, W, wmax, r, c, a, i, row);
+            z += g > 0.0 ? 1.0 / g : kOpenOhm;
+          }
         } else {
           z = (row == col) ? 1.0 : 0.0;
         }

@@ -141,6 +141,8 @@ LUT_SQRTISH = [(k / 16.0) ** 0.6 for k in range(17)]   # a saturating device
     ("supplied", 40, 30, 16, 16, 0.0, 0, 0),      # zero wire resistance: the row sweep
     ("generated", 40, 30, 16, 16, 0.0, 8, 4),
     ("generated", 140, 130, 128, 128, 2.5, 0, 0),  # 128 x 128: the register build
+    ("supplied zeros", 40, 30, 16, 16, 0.0, 0, 0),    # open devices on the row sweep
+    ("supplied zeros", 70, 50, 32, 16, 2.5, 0, 0),    # open devices, nested dissection
 ])
 def test_gprime_variation_parity(mode, P, Q, M, N, wire, wb, sb):
     say("gprime variation", mode, P, Q, M, N, wire, wb, sb)
@@ -152,6 +154,8 @@ def test_gprime_variation_parity(mode, P, Q, M, N, wire, wb, sb):
     A = 2 * (wb // (sb or wb) if wb else 1)
     if "supplied" in mode:
         vf = rng.uniform(0.7, 1.3, size=(C, R, A, M, N)).astype(np.float32)
+        if "zeros" in mode:
+            vf[rng.random(vf.shape) < 0.05] = 0.0      # open devices
         xo["variation"] = vf
         xg["variation"] = dev(vf)
     if "generated" in mode:

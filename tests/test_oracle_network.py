@@ -128,6 +128,50 @@ def test_exact_rational_with_zero_elements(res):
         assert np.max(np.abs(got - ref) / ref) < 1e-12, fn.__name__
 
 
+@pytest.mark.parametrize("M,N", [(2, 2), (3, 3), (4, 4)])
+def test_exact_rational_open_devices(M, N):
+    """Devices of zero conductance (a variation factor of 0 makes them) are
+    open circuits; both exact formulations and every oracle solver agree on
+    arrays that hold some, and a column whose devices are all open carries
+    no current."""
+    rng = np.random.default_rng(300 + 10 * M + N)
+    Gq = _rand_exact(rng, M, N)
+    Gq[0][0] = Fr(0)
+    Gq[M - 1][N - 2] = Fr(0)
+    for i in range(M):
+        Gq[i][N - 1] = Fr(0)                      # the last column is open throughout
+    e1 = exact_gprime_device_voltages(Gq, *RES_EXACT)
+    e2 = exact_gprime_nodal(Gq, *RES_EXACT)
+    assert e1 == e2
+    assert all(e1[i][N - 1] == 0 for i in range(M))
+    ref = np.array([[float(v) for v in row] for row in e1])
+    G = np.array([[float(v) for v in row] for row in Gq])
+    res = tuple(float(r) for r in RES_EXACT)
+    scale = np.abs(ref).max()
+    for fn in (gprime_nodal, gprime_paper, gprime_rowsweep):
+        got = fn(G, *res)
+        assert np.all(np.abs(got - ref) <= 1e-12 * np.maximum(np.abs(ref), 1e-10 * scale)), \
+            fn.__name__
+
+
+def test_open_device_is_the_limit_of_small_conductance():
+    """G = 0 is the continuous limit G -> 0+ (40 x 40, nodal and row sweep)."""
+    rng = np.random.default_rng(5)
+    G = rng.uniform(5e-6, 50e-6, size=(40, 40))
+    G[rng.random(G.shape) < 0.05] = 0.0
+    Gs = np.where(G == 0.0, 1e-24, G)
+    res = (1000.0, 1000.0, 2.5, 2.5)
+    a = gprime_nodal(G, *res)
+    b = gprime_nodal(Gs, *res)
+    c = gprime_rowsweep(G, *res)
+    assert np.all(np.isfinite(a)) and np.all(a >= -1e-20)
+    assert np.max(np.abs(a - b)) <= 1e-12 * np.max(np.abs(b))
+    assert np.max(np.abs(a - c)) <= 1e-11 * np.max(np.abs(a))
+    for fn in (gprime_nodal, gprime_rowsweep):
+        with pytest.raises(ValueError):
+            fn(-G, *res)
+
+
 # ---------------------------------------------------------------------------
 # closed forms and textbook ladders
 # ---------------------------------------------------------------------------
