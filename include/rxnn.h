@@ -213,6 +213,25 @@ rxnn_status rxnn_crossbar_vmm(const rxnn_layer* layer, const rxnn_periph_params*
                               const float* X, int64_t B, float* Y, void* stream);
 
 /*
+ * rxnn_crossbar_vmm without any allocation, for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops, harnesses
+ * that forbid hipMalloc).  Same arguments, kernels and results as
+ * rxnn_crossbar_vmm (bit for bit).  Every evaluation buffer of the call (the
+ * ADC bucket table, the divider DAC's row loads, the shared-tile int32
+ * workspace and the DAC output) lives in one fixed device array of 64 MiB
+ * that the library holds on each device it runs on until the process ends;
+ * the call needs about 4 (B (R M + 64) + B Q) bytes plus the tables
+ * (16 KiB; divider DAC: 4 R C A M bytes) and returns RXNN_EINVAL, launching
+ * nothing, when that exceeds 64 MiB.  The tables are rebuilt and the
+ * workspace cleared by kernels in every call (no memset nodes).  All calls on
+ * one device share the array, which keeps the last call's contents: calls
+ * that overlap on one device (different streams, threads or layers) race,
+ * and must be ordered by the caller.
+ */
+rxnn_status rxnn_crossbar_vmm_noalloc(const rxnn_layer* layer, const rxnn_periph_params* periph,
+                                      const float* X, int64_t B, float* Y, void* stream);
+
+/*
  * Phase 2 for a convolution evaluated as a matrix product over unrolled
  * patches (Sec. VI): patch column k = (ci kh + ky) kw + kx, patch row
  * bv = (n H_out + oy) W_out + ox, padded pixels are 0.  The layer must have

@@ -18,6 +18,15 @@
 
 using namespace rxnn;
 
+// Fixed scratch of rxnn_crossbar_vmm_noalloc: every evaluation buffer of a
+// call (ADC table, row loads, shared-tile workspace, DAC output) is carved
+// out of this array, so the entry point allocates nothing.  Each device the
+// library runs on holds its own copy until the process ends.  Host code must
+// not pass the array's name to a kernel: its device address comes from
+// hipGetSymbolAddress, once per device.
+constexpr size_t kScratchBytes = (size_t)64 << 20;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
 namespace {
 
 thread_local std::string g_err;
@@ -242,16 +251,25 @@ rxnn_status check_acc_range(const MapScalars& ms, const PeriphScalars& ps) {
   return RXNN_OK;
 }
 
-rxnn_status run_vmm(const rxnn_layer* L, const PeriphScalars& ps, const float* X,
-                    const rxnn_conv_desc* conv, int64_t ldx, int64_t Bv, float* Y,
-                    int64_t hw_out, float* dbgI, int32_t* dbgC, hipStream_t s,
-                    const int* ktab = nullptr) {
+// Device buffers of one evaluation call: the layer's own (grown on demand,
+// cached across calls) or carved out of the fixed scratch array.
+struct EvalBufs {
+  float2* adct = nullptr;     // ADC bucket table
+  bool adct_build = false;    // (re)build it in this call
+  float* gload = nullptr;     // divider DAC: row loads of every array
+  bool gload_build = false;
+  int32_t* iacc = nullptr;    // shared-tile int32 workspace (null: no split)
+  int64_t iacc_clear = 0;     // words of it to clear before the evaluation kernel
+  float* vbuf = nullptr;      // DAC output
+};
+
+// The layer-owned buffers for a call with `workers` shared-tile workers and
+// n_v DAC outputs (allocates what is missing or too small).
+rxnn_status layer_bufs(const rxnn_layer* L, const PeriphScalars& ps, int workers, int64_t Bv,
+                       int64_t n_v, EvalBufs* b) {
   const MapScalars& ms = L->ms;
+  rxnn_layer* Lm = const_cast<rxnn_layer*>(L);
   if (ps.ldac) {
-    // the divider stands in for the driver; the rows' loads follow G'
-    if (ms.r_driver != 0.0)
-      return fail(RXNN_EINVAL, "the divider DAC needs a layer mapped with r_driver = 0");
-    rxnn_layer* Lm = const_cast<rxnn_layer*>(L);
     if (!Lm->gload) {
       void* p = nullptr;
       const size_t bytes = (size_t)ms.R * ms.C * ms.A * ms.Mp * sizeof(float);
@@ -261,15 +279,11 @@ rxnn_status run_vmm(const rxnn_layer* L, const PeriphScalars& ps, const float* X
       }
       Lm->gload = (float*)p;
     }
-    if (!Lm->gload_valid) {
-      ProfScope t("gload", s);
-      HIP_TRY(launch_gload(ms, L->gpt, Lm->gload, s));
-      Lm->gload_valid = true;
-    }
+    b->gload = Lm->gload;
+    b->gload_build = !Lm->gload_valid;
   }
   if (ps.adc_bits > 0) {
     // the ADC's bucket table, rebuilt when the converter changes
-    rxnn_layer* Lm = const_cast<rxnn_layer*>(L);
     const double key[5] = {(double)ps.adc_levels, (double)ps.n_buckets, ps.i_fs, ps.adc_bend,
                            ps.bucket_w};
     const bool current = Lm->adct && memcmp(key, Lm->adct_key, sizeof key) == 0;
@@ -281,28 +295,19 @@ rxnn_status run_vmm(const rxnn_layer* L, const PeriphScalars& ps, const float* X
       }
       Lm->adct = (float2*)p;
     }
-    if (!current) {
-      {
-        ProfScope t("adc_table", s);
-        HIP_TRY(launch_adc_table(ps, Lm->adct, s));
-      }
-      memcpy(Lm->adct_key, key, sizeof key);
-    }
+    b->adct = Lm->adct;
+    b->adct_build = !current;
   }
-  const bool grp = use_groups(ms, ps, dbgI || dbgC);
-  VmmPlan plan{0, 0, 0};
-  if (!(dbgI || dbgC)) plan = vmm_plan(ms, ps, Bv, conv != nullptr, grp);
-  const int workers = plan.workers;
-  int32_t* iacc_ws = nullptr;
   if (workers > 0) {
-    rxnn_status st = grow_ws(const_cast<rxnn_layer*>(L), (size_t)Bv * ms.Q * sizeof(int32_t));
+    rxnn_status st = grow_ws(Lm, (size_t)Bv * ms.Q * sizeof(int32_t));
     if (st) return st;
-    iacc_ws = (int32_t*)L->ws;
+    b->iacc = (int32_t*)Lm->ws;
+    // the finish kernel zeroes again every word it reads and no other word is
+    // ever written, so the workspace is cleared only when new or after a call
+    // that did not end
+    b->iacc_clear = Lm->ws_dirty ? (int64_t)(Lm->ws_bytes / sizeof(int32_t)) : 0;
   }
-  // DAC of every input into the layer's V buffer (padded for a convolution)
-  const int64_t n_v = dac_elems(ms, conv, Bv);
   if ((size_t)n_v * sizeof(float) > L->vbuf_bytes) {
-    rxnn_layer* Lm = const_cast<rxnn_layer*>(L);
     if (Lm->vbuf) HIP_TRY(hipFree(Lm->vbuf));
     Lm->vbuf = nullptr;
     Lm->vbuf_bytes = 0;
@@ -315,39 +320,126 @@ rxnn_status run_vmm(const rxnn_layer* L, const PeriphScalars& ps, const float* X
     Lm->vbuf = (float*)p;
     Lm->vbuf_bytes = (size_t)n_v * sizeof(float);
   }
+  b->vbuf = L->vbuf;
+  return RXNN_OK;
+}
+
+// The same buffers carved out of `base` (kScratchBytes, 256-byte aligned):
+// every table is rebuilt and the workspace cleared in every call, since
+// calls on other layers share the scratch.  RXNN_EINVAL when they do not fit.
+rxnn_status scratch_bufs(const rxnn_layer* L, const PeriphScalars& ps, int workers, int64_t Bv,
+                         int64_t n_v, unsigned char* base, EvalBufs* b) {
+  const MapScalars& ms = L->ms;
+  auto up = [](size_t v) { return (v + 255) / 256 * 256; };
+  size_t off = 0;
+  if (ps.adc_bits > 0) {
+    b->adct = (float2*)(base + off);
+    b->adct_build = true;
+    off += up((size_t)(kMaxBuckets + 2) * sizeof(float2));
+  }
+  if (ps.ldac) {
+    b->gload = (float*)(base + off);
+    b->gload_build = true;
+    off += up((size_t)ms.R * ms.C * ms.A * ms.Mp * sizeof(float));
+  }
+  if (workers > 0) {
+    b->iacc = (int32_t*)(base + off);
+    b->iacc_clear = Bv * ms.Q;
+    off += up((size_t)Bv * ms.Q * sizeof(int32_t));
+  }
+  b->vbuf = (float*)(base + off);
+  off += up((size_t)n_v * sizeof(float));
+  if (off > kScratchBytes)
+    return fail(RXNN_EINVAL,
+                "the call needs %zu bytes of scratch, more than the fixed %zu (B x (R M + 64) "
+                "DAC outputs, B x Q workspace words and the tables); use rxnn_crossbar_vmm or a "
+                "smaller batch",
+                off, kScratchBytes);
+  return RXNN_OK;
+}
+
+// Device address of the scratch array on device `dev` (current), looked up
+// once per device.
+constexpr int kMaxDevices = 64;
+unsigned char* g_scratch_ptr[kMaxDevices];
+
+rxnn_status scratch_address(int dev, unsigned char** out) {
+  if (dev < 0 || dev >= kMaxDevices) return fail(RXNN_EUNSUPPORTED, "device %d out of range", dev);
+  std::lock_guard<std::mutex> g(g_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p)
+      return fail(RXNN_EHIP, "hipGetSymbolAddress of the scratch array failed: %s",
+                  hipGetErrorString(e));
+    g_scratch_ptr[dev] = (unsigned char*)p;
+  }
+  *out = g_scratch_ptr[dev];
+  return RXNN_OK;
+}
+
+rxnn_status run_vmm(const rxnn_layer* L, const PeriphScalars& ps, const float* X,
+                    const rxnn_conv_desc* conv, int64_t Bv, float* Y, int64_t hw_out,
+                    float* dbgI, int32_t* dbgC, hipStream_t s, const int* ktab = nullptr,
+                    unsigned char* scratch_base = nullptr) {
+  const MapScalars& ms = L->ms;
+  // the divider stands in for the driver; the rows' loads follow G'
+  if (ps.ldac && ms.r_driver != 0.0)
+    return fail(RXNN_EINVAL, "the divider DAC needs a layer mapped with r_driver = 0");
+  const bool grp = use_groups(ms, ps, dbgI || dbgC);
+  VmmPlan plan{0, 0, 0};
+  if (!(dbgI || dbgC)) plan = vmm_plan(ms, ps, Bv, conv != nullptr, grp);
+  const int workers = plan.workers;
+  const int64_t n_v = dac_elems(ms, conv, Bv);
+  EvalBufs b;
+  rxnn_status st = scratch_base ? scratch_bufs(L, ps, workers, Bv, n_v, scratch_base, &b)
+                                : layer_bufs(L, ps, workers, Bv, n_v, &b);
+  if (st) return st;
+  rxnn_layer* Lw = const_cast<rxnn_layer*>(L);
+  if (b.gload_build) {
+    {
+      ProfScope t("gload", s);
+      HIP_TRY(launch_gload(ms, L->gpt, b.gload, s));
+    }
+    if (!scratch_base) Lw->gload_valid = true;
+  }
+  if (b.adct_build) {
+    {
+      ProfScope t("adc_table", s);
+      HIP_TRY(launch_adc_table(ps, b.adct, s));
+    }
+    if (!scratch_base) {
+      const double key[5] = {(double)ps.adc_levels, (double)ps.n_buckets, ps.i_fs, ps.adc_bend,
+                             ps.bucket_w};
+      memcpy(Lw->adct_key, key, sizeof key);
+    }
+  }
   {
     // algorithmic bytes: every input read once, every V element written once
     const double n_in = conv ? (double)conv->n * conv->c_in * conv->h * conv->w : (double)Bv * ms.P;
     ProfScope t("dac", s, 4.0 * (n_in + (double)n_v));
-    HIP_TRY(launch_dac(ms, ps, conv, X, Bv, L->vbuf, s));
+    HIP_TRY(launch_dac(ms, ps, conv, X, Bv, b.vbuf, s));
   }
   VmmLaunch vl;
-  vl.V = L->vbuf;
+  vl.V = b.vbuf;
   vl.conv = conv;
   vl.ldx = conv ? 0 : fc_ldv(ms);
-  (void)ldx;
   vl.Bv = Bv;
   vl.Y = Y;
   vl.hw_out = hw_out;
-  vl.iacc = nullptr;
+  vl.iacc = b.iacc;
   vl.dbg_I = dbgI;
   vl.dbg_code = dbgC;
   vl.ktab = ktab;
-  vl.gload = L->gload;
+  vl.gload = b.gload;
   vl.grp = grp;
-  vl.adc_tab = L->adct;
-  // The shared-tile units add into a zeroed workspace.  The finish kernel
-  // zeroes again every word it reads, and no other word is ever written, so
-  // the workspace is cleared only when new or after a call that did not end.
-  rxnn_layer* Lw = const_cast<rxnn_layer*>(L);
+  vl.adc_tab = b.adct;
   if (workers > 0) {
-    vl.iacc = iacc_ws;
-    if (Lw->ws_dirty) {
+    if (b.iacc_clear > 0) {
       ProfScope z("fill", s);
-      HIP_TRY(launch_fill_u32((unsigned*)Lw->ws, (int64_t)(Lw->ws_bytes / sizeof(unsigned)), 0u,
-                              s));
+      HIP_TRY(launch_fill_u32((unsigned*)b.iacc, b.iacc_clear, 0u, s));
     }
-    Lw->ws_dirty = true;   // until the finish kernel has been launched
+    if (!scratch_base) Lw->ws_dirty = true;   // until the finish kernel has been launched
   }
   {
     ProfScope t("xbar_vmm", s);
@@ -356,8 +448,8 @@ rxnn_status run_vmm(const rxnn_layer* L, const PeriphScalars& ps, const float* X
   if (workers > 0) {
     // per output of a shared tile: the int32 read, its zeroing write, the fp32 write
     ProfScope t("finish", s, 12.0 * (double)(Bv - plan.row0) * (double)ms.Q);
-    HIP_TRY(launch_finish(ms, ps, iacc_ws, plan.row0, Bv, Y, hw_out, s));
-    Lw->ws_dirty = false;
+    HIP_TRY(launch_finish(ms, ps, b.iacc, plan.row0, Bv, Y, hw_out, s));
+    if (!scratch_base) Lw->ws_dirty = false;
   }
   return RXNN_OK;
 }
@@ -380,7 +472,7 @@ rxnn_status vmm_common(const rxnn_layer* layer, const rxnn_periph_params* periph
   DeviceGuard dg(L->device);
   if (!dg.ok) return fail(RXNN_EHIP, "cannot select the layer's device");
   hipStream_t s = (hipStream_t)stream;
-  return run_vmm(L, ps, X, nullptr, L->ms.P, B, Y, 0, dbgI, dbgC, s);
+  return run_vmm(L, ps, X, nullptr, B, Y, 0, dbgI, dbgC, s);
 }
 
 // w_max (fixed or reduced from W) followed by the G' build of every array.
@@ -607,6 +699,27 @@ rxnn_status rxnn_crossbar_vmm(const rxnn_layer* layer, const rxnn_periph_params*
   return vmm_common(layer, periph, X, B, Y, nullptr, nullptr, stream);
 }
 
+rxnn_status rxnn_crossbar_vmm_noalloc(const rxnn_layer* layer, const rxnn_periph_params* periph,
+                                      const float* X, int64_t B, float* Y, void* stream) {
+  if (!live(layer)) return fail(RXNN_EINVAL, "invalid or released layer handle");
+  if (B < 0) return fail(RXNN_EINVAL, "B must be >= 0");
+  if (B > 0 && (!X || !Y)) return fail(RXNN_EINVAL, "X and Y must not be NULL");
+  const rxnn_layer* L = layer;
+  PeriphScalars ps;
+  rxnn_status st = make_periph(periph, L->ms, &ps);
+  if (st) return st;
+  if ((st = check_acc_range(L->ms, ps))) return st;
+  if (L->ms.P >= (int64_t)1 << 22)
+    return fail(RXNN_EUNSUPPORTED, "P must be below 2^22 for the evaluation kernel");
+  if (B == 0) return RXNN_OK;
+  DeviceGuard dg(L->device);
+  if (!dg.ok) return fail(RXNN_EHIP, "cannot select the layer's device");
+  unsigned char* base = nullptr;
+  if ((st = scratch_address(L->device, &base))) return st;
+  return run_vmm(L, ps, X, nullptr, B, Y, 0, nullptr, nullptr, (hipStream_t)stream, nullptr,
+                 base);
+}
+
 rxnn_status rxnn_vmm_debug(const rxnn_layer* layer, const rxnn_periph_params* periph,
                            const float* X, int64_t B, float* Y, float* I_preadc, int32_t* codes,
                            void* stream) {
@@ -673,7 +786,7 @@ rxnn_status rxnn_conv_layer(const rxnn_layer* layer, const rxnn_periph_params* p
     }
   }
   const int* ktab = L->ktab;
-  return run_vmm(L, ps, X, &cd, 0, Bv, Y, ho * wo, nullptr, nullptr, s, ktab);
+  return run_vmm(L, ps, X, &cd, Bv, Y, ho * wo, nullptr, nullptr, s, ktab);
 }
 
 rxnn_status rxnn_get_gprime(const rxnn_layer* layer, int64_t row_tile, int64_t col_tile,
@@ -965,6 +1078,5 @@ rxnn_status rxnn_profile_bytes(const char* kernel, double* bytes) {
   *bytes = it == g_prof_tot.end() ? 0.0 : it->second.bytes;
   return RXNN_OK;
 }
-
 
 }  // extern "C"

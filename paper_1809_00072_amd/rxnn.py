@@ -22,7 +22,7 @@ EXPORTS = (
     "rxnn_set_gprime", "rxnn_vmm_debug", "rxnn_layer_info", "rxnn_layer_wmax",
     "rxnn_free_layer", "rxnn_profile_enable", "rxnn_profile_reset", "rxnn_profile_read",
     "rxnn_status_string", "rxnn_last_error", "rxnn_fc_backward", "rxnn_conv_backward",
-    "rxnn_profile_bytes",
+    "rxnn_profile_bytes", "rxnn_crossbar_vmm_noalloc",
 )
 
 
@@ -79,6 +79,7 @@ def load(path: str = LIB_PATH):
         "rxnn_map_layer": ([ctypes.POINTER(XbarParams), vp, i64, i64, vp, ctypes.POINTER(vp)], i32),
         "rxnn_remap_layer": ([vp, vp, vp], i32),
         "rxnn_crossbar_vmm": ([vp, ctypes.POINTER(PeriphParams), vp, i64, vp, vp], i32),
+        "rxnn_crossbar_vmm_noalloc": ([vp, ctypes.POINTER(PeriphParams), vp, i64, vp, vp], i32),
         "rxnn_conv_layer": ([vp, ctypes.POINTER(PeriphParams), ctypes.POINTER(ConvDesc), vp, vp, vp], i32),
         "rxnn_get_gprime": ([vp, i64, i64, i64, vp], i32),
         "rxnn_set_gprime": ([vp, i64, i64, i64, vp], i32),
@@ -242,6 +243,22 @@ def crossbar_vmm(layer: Layer, periph, X, Y=None, stream=None):
     pp = periph_params(periph)
     _check(load().rxnn_crossbar_vmm(layer.handle, ctypes.byref(pp), _ptr(X, torch.float32, "X"),
                                     B, _ptr(Y, torch.float32, "Y"), _stream(stream)))
+    return Y
+
+
+def crossbar_vmm_noalloc(layer: Layer, periph, X, Y, stream=None):
+    """rxnn_crossbar_vmm_noalloc: like crossbar_vmm, into the caller's Y
+    (device fp32 B x Q); the library allocates nothing."""
+    import torch
+    B = X.shape[0]
+    if X.dim() != 2 or X.shape[1] != layer.P:
+        raise ValueError(f"X must be B x {layer.P}")
+    if tuple(Y.shape) != (B, layer.Q):
+        raise ValueError(f"Y must be {B} x {layer.Q}")
+    pp = periph_params(periph)
+    _check(load().rxnn_crossbar_vmm_noalloc(layer.handle, ctypes.byref(pp),
+                                            _ptr(X, torch.float32, "X"), B,
+                                            _ptr(Y, torch.float32, "Y"), _stream(stream)))
     return Y
 
 
