@@ -546,7 +546,8 @@ STACK_DESC = {
                "8-bit weights in 4x2-bit slices, 8-bit DAC/ADC; step = evaluation of the three "
                "layers (G' mapped once)",
     "resnet50": "ResNet-50 shaped stack (54 layers), batch 128, %dx%d crossbars, wire %g ohm, "
-                "8-bit DAC/ADC; step = G' rebuild of all %d arrays from the step's weights + "
+                "8-bit DAC/ADC; step = G' rebuild of all %d arrays from the step's weights "
+                "(%s) + "
                 "evaluation of every layer (each step's weights W + 1e-3 sigma eps_t are drawn "
                 "before the timed region)",
 }
@@ -621,12 +622,15 @@ def bench_stack(args):
         else:
             rxnn.crossbar_vmm(e["L"], w["periph"], e["X"], e["Y"], stream)
 
-    # The layers' G' rebuilds are independent: they are spread over a few
-    # streams (default priority) so that the small layers' builds overlap,
-    # and every evaluation waits for its layer's rebuild.
+    # Per-layer rebuilds (for comparison) are spread over a few streams
+    # (default priority) so that the small layers' builds overlap.
     build_streams = [torch.cuda.Stream(device=dev) for _ in range(8)] if rebuild else []
+    if rebuild and not args.per_layer_rebuild:
+        # the batched rebuild's tables and workspace are set up here, outside
+        # the timed region
+        rxnn.remap_layers([e["L"] for e in layers], [e["W"] for e in layers], stream)
 
-    def rebuild_all(t):
+    def rebuild_per_layer(t):
         done = []
         for i, e in enumerate(layers):
             bs = build_streams[i % len(build_streams)]
@@ -635,16 +639,22 @@ def bench_stack(args):
             ev = torch.cuda.Event()
             ev.record(bs)
             done.append(ev)
-        return done
+        for ev in done:
+            stream.wait_event(ev)
+
+    def rebuild_all(t):
+        # every layer's G' in one launch sequence (the layers share the
+        # crossbar size and resistances)
+        if args.per_layer_rebuild:
+            rebuild_per_layer(t)
+        else:
+            rxnn.remap_layers([e["L"] for e in layers], [e["Wt"][t] for e in layers], stream)
 
     def step(t):
         if rebuild:
-            for l, ev in enumerate(rebuild_all(t)):
-                stream.wait_event(ev)
-                evaluate(l)
-        else:
-            for l in range(len(layers)):
-                evaluate(l)
+            rebuild_all(t)
+        for l in range(len(layers)):
+            evaluate(l)
 
     def timed(fn, n, level):
         rxnn.profile_reset()
@@ -676,12 +686,11 @@ def bench_stack(args):
         timed(lambda i: step(args.warmup + i), args.steps, 1)
         kern = read_kernels(rxnn, args.steps)
     # the rebuild alone (map only), on the same streams
-    map_ms = None
+    map_ms = map_pl_ms = None
     if rebuild:
-        def map_only(i):
-            for ev in rebuild_all(args.warmup + i):
-                stream.wait_event(ev)
-        map_ms = timed(map_only, args.steps, 0)
+        map_ms = timed(lambda i: rebuild_all(args.warmup + i), args.steps, 0)
+        # for comparison: one rxnn_remap_layer per layer, spread over 8 streams
+        map_pl_ms = timed(lambda i: rebuild_per_layer(args.warmup + i), args.steps, 0)
     # the evaluation alone (VMM only, G' kept): the evaluation kernel's
     # roofline is taken here, where no rebuild shares the GPU with it
     def eval_all(i):
@@ -727,7 +736,9 @@ def bench_stack(args):
     M, N = layers[0]["L"].M, layers[0]["L"].N
     desc = STACK_DESC[cfg]
     if rebuild:
-        desc = desc % (M, N, args.wire, total_arrays) + device_note(args)
+        desc = desc % (M, N, args.wire, total_arrays,
+                       "one rxnn_remap_layer per layer on 8 streams" if args.per_layer_rebuild
+                       else "one rxnn_remap_layers call") + device_note(args)
     traffic = STACK_VMM_TRAFFIC.get((cfg, M, args.wire if rebuild else None))
     out = {
         "metric": "non-ideal crossbar MACs/sec per layer",
@@ -752,8 +763,11 @@ def bench_stack(args):
     if rebuild:
         b_flops = sum(e["L"].R * e["L"].C * e["L"].A for e in layers) * build_flops(M, N)
         b_ach = b_flops / (map_ms * 1e-3) / 1e12
-        out["map_only"] = {"what": "G' rebuild of every array (w_max + fp64 build), 8 streams",
-                           "ms": map_ms, "fp64_flops": b_flops, "achieved": b_ach,
+        out["map_only"] = {"what": "G' rebuild of every array (w_max + fp64 build)"
+                                   + (", one rxnn_remap_layer per layer on 8 streams"
+                                      if args.per_layer_rebuild else
+                                      ", all layers in one rxnn_remap_layers call"),
+                           "ms": map_ms, "per_layer_8_streams_ms": map_pl_ms, "fp64_flops": b_flops, "achieved": b_ach,
                            "peak": FP64_PEAK_TFLOPS, "unit": "TFLOP/s",
                            "frac": b_ach / FP64_PEAK_TFLOPS,
                            "generation": generation_info(map_ms, total_arrays, M, N)}
@@ -887,6 +901,9 @@ def main():
                          "driver resistance)")
     ap.add_argument("--retrain", action="store_true",
                     help="conv3x3: also time re-training steps (rebuild + forward + backward)")
+    ap.add_argument("--per-layer-rebuild", action="store_true",
+                    help="resnet50: rebuild G' with one rxnn_remap_layer per layer on 8 streams "
+                         "instead of one rxnn_remap_layers call")
     ap.add_argument("--breakdown", action="store_true",
                     help="stacks without rebuild: also time every launch in a second pass")
     args = ap.parse_args()

@@ -197,6 +197,28 @@ rxnn_status rxnn_map_layer(const rxnn_xbar_params* params, const float* W,
 rxnn_status rxnn_remap_layer(rxnn_layer* layer, const float* W, void* stream);
 
 /*
+ * Phase 1 for several layers at once: rxnn_remap_layer of every layers[i]
+ * from W[i] (device fp32, P_i x Q_i row-major, as for rxnn_map_layer), as one
+ * launch sequence over the arrays of all of them, so that each level of the
+ * G' build runs as one large grid (the per-level grids of one small layer
+ * leave most of the GPU idle).  Same results as rxnn_remap_layer, bit for bit.
+ *   layers  host array of n (>= 1) distinct live handles on one device, all
+ *           mapped with the same crossbar size (rows, cols) and the same
+ *           r_driver, r_sense, r_row and r_col, each of them > 0 for r_row,
+ *           r_col and r_sense (the nested-dissection build); weights, sizes,
+ *           w_max, slicing, device table and variation may differ.
+ *   W       host array of n device pointers.
+ * The library keeps, per device, the batch's layer and array tables (copied
+ * from host memory on `stream`) and one build workspace of at most 16 GiB,
+ * grown on demand and held until the process ends; batches whose workspace
+ * would exceed it are built in chunks.  Calls that overlap on one device
+ * (different streams) race on these.  RXNN_EINVAL for a bad argument or a
+ * mismatch, RXNN_ENOMEM when the tables or workspace cannot grow.
+ */
+rxnn_status rxnn_remap_layers(rxnn_layer* const* layers, const float* const* W, int32_t n,
+                              void* stream);
+
+/*
  * Phase 2 for a fully connected layer: DAC -> V . G' (Eq. 14) -> ADC ->
  * accumulation over row tiles and arrays -> scale.
  *   X  device fp32 B x P row-major; Y  device fp32 B x Q row-major.

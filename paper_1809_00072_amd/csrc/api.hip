@@ -476,18 +476,19 @@ rxnn_status vmm_common(const rxnn_layer* layer, const rxnn_periph_params* periph
 }
 
 // w_max (fixed or reduced from W) followed by the G' build of every array.
+// w_max of a layer: the fixed one, or max |W| reduced on the device.
+hipError_t launch_wmax(rxnn_layer* L, const float* W, hipStream_t s) {
+  const MapScalars& ms = L->ms;
+  ProfScope t("wmax", s);
+  if (ms.wmax_fixed > 0.0f)
+    return launch_fill_u32((unsigned*)L->d_wmax, 1, __builtin_bit_cast(unsigned, ms.wmax_fixed), s);
+  return launch_absmax(W, ms.P * ms.Q, (unsigned*)L->d_wmax, s);
+}
+
 hipError_t build_gprime(rxnn_layer* L, const float* W, hipStream_t s) {
   L->gload_valid = false;   // the row loads follow G'
   const MapScalars& ms = L->ms;
-  hipError_t e = hipSuccess;
-  {
-    ProfScope t("wmax", s);
-    if (ms.wmax_fixed > 0.0f) {
-      e = launch_fill_u32((unsigned*)L->d_wmax, 1, __builtin_bit_cast(unsigned, ms.wmax_fixed), s);
-    } else {
-      e = launch_absmax(W, ms.P * ms.Q, (unsigned*)L->d_wmax, s);
-    }
-  }
+  hipError_t e = launch_wmax(L, W, s);
   if (e == hipSuccess) {
     if (!L->nd_ws) {
       ProfScope t("gprime_sweep", s);
@@ -681,6 +682,118 @@ rxnn_status rxnn_map_layer(const rxnn_xbar_params* params, const float* W, int64
     g_live.insert(L);
   }
   *out = L;
+  return RXNN_OK;
+}
+
+}  // extern "C"
+
+namespace {
+
+// Batched rebuilds: per device, the layer and array tables of the last batch
+// and one build workspace, grown on demand and kept until the process ends
+// (at most kBatchBudget bytes: larger batches are built in chunks).
+struct BatchState {
+  NdBatchLayer* d_layers = nullptr;
+  int64_t layers_cap = 0;
+  int2* d_ent = nullptr;
+  int64_t ent_cap = 0;
+  double* ws = nullptr;
+  int64_t ws_cap = 0;          // doubles
+  std::vector<NdBatchLayer> h_layers;
+  std::vector<int2> h_ent;
+};
+constexpr size_t kBatchBudget = (size_t)16 << 30;
+BatchState g_batch[kMaxDevices];
+std::mutex g_batch_mu;
+
+template <typename T>
+rxnn_status grow_dev(T** p, int64_t* cap, int64_t need, const char* what) {
+  if (*cap >= need) return RXNN_OK;
+  if (*p) HIP_TRY(hipFree(*p));
+  *p = nullptr;
+  *cap = 0;
+  if (hipMalloc((void**)p, (size_t)need * sizeof(T)) != hipSuccess) {
+    (void)hipGetLastError();
+    *p = nullptr;
+    return fail(RXNN_ENOMEM, "cannot allocate %zu bytes for the %s",
+                (size_t)need * sizeof(T), what);
+  }
+  *cap = need;
+  return RXNN_OK;
+}
+
+bool same_network(const rxnn_layer* a, const rxnn_layer* b) {
+  return a->device == b->device && a->ms.M == b->ms.M && a->ms.N == b->ms.N &&
+         a->ms.r_driver == b->ms.r_driver && a->ms.r_sense == b->ms.r_sense &&
+         a->ms.r_row == b->ms.r_row && a->ms.r_col == b->ms.r_col;
+}
+
+}  // namespace
+
+extern "C" {
+
+rxnn_status rxnn_remap_layers(rxnn_layer* const* layers, const float* const* W, int32_t n,
+                              void* stream) {
+  if (n < 1) return fail(RXNN_EINVAL, "n must be >= 1");
+  if (!layers || !W) return fail(RXNN_EINVAL, "layers and W must not be NULL");
+  for (int32_t i = 0; i < n; ++i) {
+    if (!live(layers[i])) return fail(RXNN_EINVAL, "layer %d is invalid or released", i);
+    if (!W[i]) return fail(RXNN_EINVAL, "W[%d] is NULL", i);
+    if (!layers[i]->nd_ws)
+      return fail(RXNN_EINVAL, "layer %d uses the row-sweep build (a zero wire or sense "
+                  "resistance); rebuild it with rxnn_remap_layer", i);
+    if (!same_network(layers[i], layers[0]))
+      return fail(RXNN_EINVAL, "layer %d differs from layer 0 in device, crossbar size or "
+                  "resistances", i);
+    for (int32_t j = 0; j < i; ++j)
+      if (layers[j] == layers[i]) return fail(RXNN_EINVAL, "layer %d appears twice", i);
+  }
+  const int dev = layers[0]->device;
+  if (dev < 0 || dev >= kMaxDevices) return fail(RXNN_EUNSUPPORTED, "device %d out of range", dev);
+  DeviceGuard dg(dev);
+  if (!dg.ok) return fail(RXNN_EHIP, "cannot select the layers' device");
+  hipStream_t s = (hipStream_t)stream;
+  std::lock_guard<std::mutex> g(g_batch_mu);
+  BatchState& bs = g_batch[dev];
+  bs.h_layers.resize((size_t)n);
+  bs.h_ent.clear();
+  for (int32_t i = 0; i < n; ++i) {
+    rxnn_layer* L = layers[i];
+    bs.h_layers[(size_t)i] = NdBatchLayer{L->ms, W[i], L->gpt};
+    const int64_t na = (int64_t)L->ms.R * L->ms.C * L->ms.A;
+    for (int64_t a = 0; a < na; ++a) bs.h_ent.push_back(make_int2(i, (int)a));
+  }
+  const int64_t total = (int64_t)bs.h_ent.size();
+  const MapScalars& ms0 = layers[0]->ms;
+  int64_t si, so, sc;
+  const int T = nd_side(ms0.M, ms0.N);
+  const int nbs = nd_block_side(T, total);
+  nd_sizes(T, ms0.M, nbs, &si, &so, &sc);
+  const int64_t per = si + so + sc;   // doubles of workspace per array
+  int64_t chunk = (int64_t)(kBatchBudget / sizeof(double)) / per;
+  if (chunk < 1) chunk = 1;
+  if (chunk > total) chunk = total;
+  rxnn_status st;
+  if ((st = grow_dev(&bs.d_layers, &bs.layers_cap, n, "batch layer table"))) return st;
+  if ((st = grow_dev(&bs.d_ent, &bs.ent_cap, total, "batch array table"))) return st;
+  if ((st = grow_dev(&bs.ws, &bs.ws_cap, chunk * per, "batch build workspace"))) return st;
+  // the tables go over on the stream (from pageable memory: staged before return)
+  HIP_TRY(hipMemcpyAsync(bs.d_layers, bs.h_layers.data(), (size_t)n * sizeof(NdBatchLayer),
+                         hipMemcpyHostToDevice, s));
+  HIP_TRY(hipMemcpyAsync(bs.d_ent, bs.h_ent.data(), (size_t)total * sizeof(int2),
+                         hipMemcpyHostToDevice, s));
+  for (int32_t i = 0; i < n; ++i) {
+    layers[i]->gload_valid = false;   // the row loads follow G'
+    hipError_t e = launch_wmax(layers[i], W[i], s);
+    if (e != hipSuccess) return fail(RXNN_EHIP, "w_max launch failed: %s", hipGetErrorString(e));
+  }
+  const NdBatch batch{bs.d_layers, bs.d_ent};
+  for (int64_t a0 = 0; a0 < total; a0 += chunk) {
+    const int64_t m = total - a0 < chunk ? total - a0 : chunk;
+    hipError_t e = launch_nd_build(ms0, nullptr, nullptr, a0, m, nbs, bs.ws, s, &batch);
+    if (e != hipSuccess)
+      return fail(RXNN_EHIP, "mapping launch failed: %s", hipGetErrorString(e));
+  }
   return RXNN_OK;
 }
 

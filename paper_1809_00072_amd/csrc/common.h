@@ -114,8 +114,21 @@ int nd_side(int M, int N);
 int nd_block_side(int T, int64_t n_arrays);
 void nd_sizes(int T, int M, int bs, int64_t* in_stride, int64_t* out_stride,
               int64_t* scr_stride);
+// A build over the arrays of several layers that share the crossbar size and
+// its resistances (one launch sequence for all of them): per layer its
+// scalars, weights and G' buffer; per array of the batch, (layer, array).
+struct NdBatchLayer {
+  MapScalars ms;
+  const float* W;
+  float* gpt;
+};
+struct NdBatch {
+  const NdBatchLayer* layers;   // device
+  const int2* ent;              // device: batch array -> (layer slot, array of that layer)
+};
 hipError_t launch_nd_build(const MapScalars& ms, const float* W, float* gpt, int64_t arr0,
-                           int64_t n, int bs, double* ws, hipStream_t s);
+                           int64_t n, int bs, double* ws, hipStream_t s,
+                           const NdBatch* batch = nullptr);
 
 struct VmmLaunch {
   const float* V;       // DAC output: FC Bv x ldx rows (ldx = fc_ldv); conv the padded NCHW tensor

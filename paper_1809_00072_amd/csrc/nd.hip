@@ -66,6 +66,8 @@ struct NdArgs {
   double* dB;            // stage output (row stride dldo) per array
   int dn, dld, dldo;
   int dpanel;            // external columns per workgroup of the cut kernel
+  // several layers at once (null tables: the one layer of ms / W / gpt)
+  NdBatch batch;
 };
 
 namespace {
@@ -156,6 +158,27 @@ __device__ __forceinline__ double cell_conductance(const MapScalars& ms, const f
   const int i = gi - row_off, j = gj;
   if (i < 0 || j >= ms.N) return 0.0;
   return device_g(ms, W, wmax, arr, i, j);
+}
+
+// Array `la` of the launch: its layer's scalars and weights, its index in
+// that layer, and where its G' goes.  Every layer of a batch shares M, N (so
+// Mp, Np) with na.ms.
+struct ArrRef {
+  const MapScalars* ms;
+  const float* W;
+  int64_t arr;
+  float* out;
+};
+
+__device__ __forceinline__ ArrRef nd_ref(const NdArgs& na, int64_t la) {
+  const int64_t tile = (int64_t)na.ms.Np * na.ms.Mp;
+  if (na.batch.ent) {
+    const int2 e = na.batch.ent[na.arr0 + la];
+    const NdBatchLayer* bl = na.batch.layers + e.x;
+    return ArrRef{&bl->ms, bl->W, (int64_t)e.y, bl->gpt + (int64_t)e.y * tile};
+  }
+  const int64_t arr = na.arr0 + la;
+  return ArrRef{&na.ms, na.W, arr, na.gpt + arr * tile};
 }
 
 // ---------------------------------------------------------------------------
@@ -314,8 +337,9 @@ __device__ __forceinline__ void nd_block(const NdArgs& na) {
   const int64_t la = blk / (nsb * nsb);
   const int sb = (int)(blk % (nsb * nsb));
   const int I0 = (sb / nsb) * BS, J0 = (sb % nsb) * BS;
-  const int64_t arr = na.arr0 + la;
-  const MapScalars& ms = na.ms;
+  const ArrRef ref = nd_ref(na, la);
+  const MapScalars& ms = *ref.ms;
+  const int64_t arr = ref.arr;
   const double wmax = ms.wmax_fixed > 0.0f ? (double)ms.wmax_fixed : (double)*ms.d_wmax;
   double* A = bufA[SPLIT ? 0 : wv];
   double* B = bufB[SPLIT ? 0 : wv];
@@ -324,7 +348,7 @@ __device__ __forceinline__ void nd_block(const NdArgs& na) {
   if (!SPLIT || wv == 0) {
     const int li = lane / BS, lj = lane % BS;
     const int gi = I0 + li, gj = J0 + lj;
-    const double G = cell_conductance(ms, na.W, wmax, arr, gi, gj, na.row_off);
+    const double G = cell_conductance(ms, ref.W, wmax, arr, gi, gj, na.row_off);
     const bool hasR = gj + 1 < T, hasT = gi > 0;
     const double gv = (gi + 1 < T) ? na.g_c : na.g_s;
     double* Y = A + lane * 16;   // this lane's slot (LDS: the indices below vary)
@@ -577,8 +601,7 @@ __global__ __launch_bounds__(NTH) void k_nd_final(NdArgs na) {
     cut[i * ldc + y] = v;
   }
   __syncthreads();
-  const int64_t arr = na.arr0 + la;
-  float* out = na.gpt + arr * (int64_t)na.ms.Np * na.ms.Mp;
+  float* out = nd_ref(na, la).out;
   eliminate(cut, c, E, ldc, ext, E, lds);
   for (int e = tid; e < na.ms.Np * na.ms.Mp; e += NT) {
     const int j = e / na.ms.Mp, k = e % na.ms.Mp;
@@ -912,8 +935,7 @@ __global__ __launch_bounds__(512) void k_nd_cut(NdArgs na) {
     for (int x = 0; x < C; ++x) zs[x][y - C - M] = U[x] * is[x];
   }
   __syncthreads();
-  const int64_t arr = na.arr0 + la;
-  float* out = na.gpt + arr * (int64_t)na.ms.Np * na.ms.Mp;
+  float* out = nd_ref(na, la).out;
   const int Np = na.ms.Np, Mp = na.ms.Mp;
   for (int it = threadIdx.x; it < 256; it += blockDim.x) {
     const int tx = it >> 4, ty = it & 15;
@@ -1128,8 +1150,7 @@ __global__ __launch_bounds__(256) void k_nd_gprod(NdArgs na) {
     }
     __syncthreads();
   }
-  const int64_t arr = na.arr0 + la;
-  float* out = na.gpt + arr * (int64_t)Np * Mp;
+  float* out = nd_ref(na, la).out;
 #pragma unroll
   for (int a = 0; a < 4; ++a) {
     const int j = j0 + 4 * tx + a;
@@ -1255,9 +1276,8 @@ __global__ __launch_bounds__(256) void k_nd_dschur(NdArgs na) {
       }
     }
   } else {
-    const int64_t arr = na.arr0 + la;
     const int Np = na.ms.Np, Mp = na.ms.Mp, N = na.ms.N;
-    float* out = na.gpt + arr * (int64_t)Np * Mp;
+    float* out = nd_ref(na, la).out;
 #pragma unroll
     for (int a = 0; a < 4; ++a) {
       const int j = x0 + 4 * tx + a;
@@ -1484,11 +1504,12 @@ static void launch_staged(NdArgs na, int64_t n, int c, int n0, double* a, double
 // Builds G' of arrays [arr0, arr0 + n) with the workspace ws (ping-pong
 // level buffers and scratch, sized by nd_sizes for one array, times n).
 hipError_t launch_nd_build(const MapScalars& ms, const float* W, float* gpt, int64_t arr0,
-                           int64_t n, int bs, double* ws, hipStream_t s) {
+                           int64_t n, int bs, double* ws, hipStream_t s, const NdBatch* batch) {
   NdArgs na;
   na.ms = ms;
   na.W = W;
   na.gpt = gpt;
+  na.batch = batch ? *batch : NdBatch{nullptr, nullptr};
   na.arr0 = arr0;
   na.n_arrays = n;
   na.T = nd_side(ms.M, ms.N);

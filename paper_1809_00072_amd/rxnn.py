@@ -22,7 +22,7 @@ EXPORTS = (
     "rxnn_set_gprime", "rxnn_vmm_debug", "rxnn_layer_info", "rxnn_layer_wmax",
     "rxnn_free_layer", "rxnn_profile_enable", "rxnn_profile_reset", "rxnn_profile_read",
     "rxnn_status_string", "rxnn_last_error", "rxnn_fc_backward", "rxnn_conv_backward",
-    "rxnn_profile_bytes", "rxnn_crossbar_vmm_noalloc",
+    "rxnn_profile_bytes", "rxnn_crossbar_vmm_noalloc", "rxnn_remap_layers",
 )
 
 
@@ -78,6 +78,7 @@ def load(path: str = LIB_PATH):
     sig = {
         "rxnn_map_layer": ([ctypes.POINTER(XbarParams), vp, i64, i64, vp, ctypes.POINTER(vp)], i32),
         "rxnn_remap_layer": ([vp, vp, vp], i32),
+        "rxnn_remap_layers": ([ctypes.POINTER(vp), ctypes.POINTER(vp), i32, vp], i32),
         "rxnn_crossbar_vmm": ([vp, ctypes.POINTER(PeriphParams), vp, i64, vp, vp], i32),
         "rxnn_crossbar_vmm_noalloc": ([vp, ctypes.POINTER(PeriphParams), vp, i64, vp, vp], i32),
         "rxnn_conv_layer": ([vp, ctypes.POINTER(PeriphParams), ctypes.POINTER(ConvDesc), vp, vp, vp], i32),
@@ -230,6 +231,22 @@ def remap_layer(layer: Layer, W, stream=None):
     if tuple(W.shape) != (layer.P, layer.Q):
         raise ValueError(f"W must be {layer.P} x {layer.Q}")
     _check(load().rxnn_remap_layer(layer.handle, _ptr(W, torch.float32, "W"), _stream(stream)))
+
+
+def remap_layers(layers, Ws, stream=None):
+    """rxnn_remap_layers: rebuild the G' of every layer from its new weights
+    in one launch sequence (layers of one crossbar size and resistances)."""
+    import torch
+    if len(layers) != len(Ws) or not layers:
+        raise ValueError("one weight tensor per layer, at least one layer")
+    for L, W in zip(layers, Ws):
+        if tuple(W.shape) != (L.P, L.Q):
+            raise ValueError(f"W must be {L.P} x {L.Q}")
+    n = len(layers)
+    hs = (ctypes.c_void_p * n)(*[L.handle.value if isinstance(L.handle, ctypes.c_void_p)
+                                  else L.handle for L in layers])
+    ws = (ctypes.c_void_p * n)(*[_ptr(W, torch.float32, "W").value for W in Ws])
+    _check(load().rxnn_remap_layers(hs, ws, n, _stream(stream)))
 
 
 def crossbar_vmm(layer: Layer, periph, X, Y=None, stream=None):
