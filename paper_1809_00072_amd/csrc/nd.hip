@@ -196,7 +196,13 @@ constexpr int BS = 8;                 // side of the blocks of this kernel
 constexpr int BWAVES = 4;             // waves per workgroup of the block kernel
 constexpr int64_t kSplitBlocks = 2048; // at most this many blocks: one workgroup per block
 constexpr int BLEVELS = 6;            // 1x1 -> 2x1 -> 2x2 -> 4x2 -> 4x4 -> 8x4 -> 8x8
-constexpr int BUFA = 1024, BUFB = 1152;   // doubles per wave: leaves / even / odd levels
+// In LDS every cell's or merged block's matrix takes its side squared plus one
+// double: consecutive matrices then start in different banks, so the lanes of
+// different merge groups (and the leaf lanes) do not collide.
+__host__ __device__ constexpr int lds_mat(int side) { return side * side + 1; }
+// doubles per wave: the leaves and odd levels (64 x 17, 16 x 65, 4 x 257) and
+// the even levels (32 x 37, 8 x 145, 2 x 577)
+constexpr int BUFA = 64 * 17, BUFB = 32 * 37;
 
 // Child port landing on each combined slot (cut nodes 0 .. c-1, then the
 // externals), per level and per boundary variant (bit 1: the merged block
@@ -236,6 +242,19 @@ constexpr BlkTab make_blk_tab() {
 
 __constant__ BlkTab kBlkTab = make_blk_tab();
 
+typedef __attribute__((address_space(3))) double lds_f64;
+typedef __attribute__((address_space(3))) short lds_i16;
+
+// An LDS pointer the compiler cannot see through: element reads at fixed
+// indices then use the instruction's offset field instead of a register
+// holding each address.
+template <typename P>
+__device__ __forceinline__ P* opaque_lds(const void* p) {
+  unsigned a = (unsigned)(uintptr_t)(const __attribute__((address_space(3))) char*)p;
+  asm volatile("" : "+v"(a));
+  return (P*)(uintptr_t)a;
+}
+
 __device__ __forceinline__ double bperm_d(double v, int src_lane) {
   const unsigned long long b = __builtin_bit_cast(unsigned long long, v);
   const unsigned lo = (unsigned)__builtin_amdgcn_ds_bpermute(src_lane << 2, (int)(unsigned)b);
@@ -261,19 +280,29 @@ __device__ __forceinline__ void wave_sync() {
 // EIN per child), merged blocks written with stride EM (out).  SPLIT: the
 // level's passes (GPW merges each) are shared by the workgroup's waves, which
 // all work on this block; otherwise the wave does them all.
+// The combined matrix is symmetric, and so is what remains of it after each
+// pivot, so the multiplier of row x at pivot k (its entry in column k) equals
+// the pivot row's entry in column x: at every pivot each lane publishes its
+// entry of the pivot row in LDS (`pr`, GS + 1 doubles per group) and every
+// lane of the group reads the multipliers back as broadcasts.  The SPLIT form
+// (capped at 96 VGPRs) reads them from the pivot lane's registers instead.
 template <int L, int H, int W, bool VERT, bool SPLIT>
 __device__ __forceinline__ void block_level(int T, int I0, int J0, const short* tab,
-                                            const double* in, double* out, int lane, int wv) {
+                                            const double* in, double* out, double* pr, int lane,
+                                            int wv) {
   constexpr int NH = VERT ? 2 * H : H, NW = VERT ? W : 2 * W;
   constexpr int C = VERT ? W : H;
   constexpr int EM = 2 * (NH + NW), EIN = 2 * (H + W);
   constexpr int LD = C + EM;
   constexpr int GS = LD <= 8 ? 8 : (LD <= 16 ? 16 : (LD <= 32 ? 32 : 64));
   constexpr int GPW = 64 / GS;                 // merges per pass
+  // merged blocks: padded in LDS, dense in the global level buffer (last level)
+  constexpr int OSTRIDE = L == BLEVELS - 1 ? EM * EM : lds_mat(EM);
   constexpr int MC = BS / NW, CC = BS / W;     // merges / children per block row
   constexpr int NM = (BS / NH) * MC;
   static_assert(NM % GPW == 0, "whole passes");
   const int g = lane / GS, yl = lane % GS, gb = lane - yl;
+  lds_f64* gr = opaque_lds<lds_f64>(pr + g * (GS + 1));   // this group's pivot row
 #pragma unroll 1
   for (int pass = SPLIT ? wv : 0; pass < NM / GPW; pass += SPLIT ? BWAVES : 1) {
     const int m = pass * GPW + g;
@@ -285,8 +314,8 @@ __device__ __forceinline__ void block_level(int T, int I0, int J0, const short* 
     const int cm1 = VERT ? (mi * 2 + 1) * CC + mj : mi * CC + mj * 2 + 1;
     const short* t0 = tab + (((L * 4) + (rn ? 2 : 0) + (tn ? 1 : 0)) * 2) * 64;
     const short* t1 = t0 + 64;
-    const double* c0 = in + cm0 * EIN * EIN;
-    const double* c1 = in + cm1 * EIN * EIN;
+    const double* c0 = in + cm0 * lds_mat(EIN);
+    const double* c1 = in + cm1 * lds_mat(EIN);
     const int s0 = t0[yl], s1 = t1[yl];
     double U[LD];
 #pragma unroll
@@ -296,20 +325,39 @@ __device__ __forceinline__ void block_level(int T, int I0, int J0, const short* 
       const double b = c1[max(r1, 0) * EIN + max(s1, 0)];
       U[x] = ((r0 >= 0 && s0 >= 0) ? a : 0.0) + ((r1 >= 0 && s1 >= 0) ? b : 0.0);
     }
+    if constexpr (SPLIT) {
+      // few blocks (a latency-bound build at 96 VGPRs): the multiplier of
+      // row x comes from lane k's register by a lane read
+#pragma unroll
+      for (int k = 0; k < C; ++k) {
+        const double piv = GS == 64 ? readlane_d(U[k], k) : bperm_d(U[k], gb + k);
+        const double t = U[k] * recip(piv);
+#pragma unroll
+        for (int x = k + 1; x < LD; ++x) {
+          const double mx = GS == 64 ? readlane_d(U[x], k) : bperm_d(U[x], gb + k);
+          U[x] = fma(-mx, t, U[x]);
+        }
+      }
+    } else {
 #pragma unroll
     for (int k = 0; k < C; ++k) {
-      const double piv = GS == 64 ? readlane_d(U[k], k) : bperm_d(U[k], gb + k);
-      const double t = U[k] * recip(piv);
+      gr[yl] = U[k];
+      wave_sync();
+      const double t = U[k] * recip(gr[k]);
 #pragma unroll
       for (int x = k + 1; x < LD; ++x) {
-        const double mx = GS == 64 ? readlane_d(U[x], k) : bperm_d(U[x], gb + k);
-        U[x] = fma(-mx, t, U[x]);
+        U[x] = fma(-gr[x], t, U[x]);
+        // the update is done here: deferring it past the next pivots would
+        // hold every pivot row's values live
+        asm volatile("" : "+v"(U[x]));
       }
+      wave_sync();   // every read of this pivot row precedes the next one's writes
+    }
     }
     if (yl >= C && yl < ld) {
 #pragma unroll
       for (int x = C; x < LD; ++x)
-        if (x < ld) out[m * EM * EM + (x - C) * EM + (yl - C)] = U[x];
+        if (x < ld) out[m * OSTRIDE + (x - C) * EM + (yl - C)] = U[x];
     }
   }
   if (SPLIT) __syncthreads();
@@ -325,6 +373,7 @@ __device__ __forceinline__ void nd_block(const NdArgs& na) {
   constexpr int NB = SPLIT ? 1 : BWAVES;   // blocks per workgroup
   __shared__ double bufA[NB][BUFA];
   __shared__ double bufB[NB][BUFB];
+  __shared__ double prow[BWAVES][72];   // pivot rows of each wave's merge groups
   const short* ct = &kBlkTab.s[0][0][0][0];
   for (int e = threadIdx.x; e < BLEVELS * 4 * 2 * 64; e += 64 * BWAVES) tab[e] = ct[e];
   __syncthreads();
@@ -351,7 +400,7 @@ __device__ __forceinline__ void nd_block(const NdArgs& na) {
     const double G = cell_conductance(ms, ref.W, wmax, arr, gi, gj, na.row_off);
     const bool hasR = gj + 1 < T, hasT = gi > 0;
     const double gv = (gi + 1 < T) ? na.g_c : na.g_s;
-    double* Y = A + lane * 16;   // this lane's slot (LDS: the indices below vary)
+    double* Y = A + lane * lds_mat(4);   // this lane's slot (LDS: the indices below vary)
 #pragma unroll
     for (int e = 0; e < 16; ++e) Y[e] = 0.0;
     const int Lp = 0, Rp = 1, Tp = hasR ? 2 : 1, Bp = (hasR ? 2 : 1) + (hasT ? 1 : 0);
@@ -372,14 +421,14 @@ __device__ __forceinline__ void nd_block(const NdArgs& na) {
   }
   if (SPLIT) __syncthreads();
   else wave_sync();
-  block_level<0, 1, 1, true, SPLIT>(T, I0, J0, tab, A, B, lane, wv);
-  block_level<1, 2, 1, false, SPLIT>(T, I0, J0, tab, B, A, lane, wv);
-  block_level<2, 2, 2, true, SPLIT>(T, I0, J0, tab, A, B, lane, wv);
-  block_level<3, 4, 2, false, SPLIT>(T, I0, J0, tab, B, A, lane, wv);
-  block_level<4, 4, 4, true, SPLIT>(T, I0, J0, tab, A, B, lane, wv);
+  block_level<0, 1, 1, true, SPLIT>(T, I0, J0, tab, A, B, prow[wv], lane, wv);
+  block_level<1, 2, 1, false, SPLIT>(T, I0, J0, tab, B, A, prow[wv], lane, wv);
+  block_level<2, 2, 2, true, SPLIT>(T, I0, J0, tab, A, B, prow[wv], lane, wv);
+  block_level<3, 4, 2, false, SPLIT>(T, I0, J0, tab, B, A, prow[wv], lane, wv);
+  block_level<4, 4, 4, true, SPLIT>(T, I0, J0, tab, A, B, prow[wv], lane, wv);
   constexpr int EO = 4 * BS;   // ports of an interior 8 x 8 block
   double* dst = na.buf_out + la * na.out_stride + (int64_t)sb * EO * EO;
-  block_level<5, 8, 4, false, SPLIT>(T, I0, J0, tab, B, dst, lane, wv);
+  block_level<5, 8, 4, false, SPLIT>(T, I0, J0, tab, B, dst, prow[wv], lane, wv);
 }
 
 // The split form is held to 96 VGPRs (5 waves per SIMD): five workgroups per
@@ -623,8 +672,6 @@ __global__ __launch_bounds__(NTH) void k_nd_final(NdArgs na) {
 // ---------------------------------------------------------------------------
 constexpr int MAXSLOT = 512;    // cut + external slots of a merge with c <= 64
 
-typedef __attribute__((address_space(3))) double lds_f64;
-typedef __attribute__((address_space(3))) short lds_i16;
 
 // Empty asm that takes rows x0 .. x0 + 7 of U (those below N) as operands:
 // their updates must be complete here and cannot be deferred past it.
@@ -656,15 +703,6 @@ __device__ __forceinline__ double nd_load(__amdgpu_buffer_rsrc_t r, unsigned vof
   return __builtin_bit_cast(double, __builtin_amdgcn_raw_buffer_load_b64(r, voff, soff, 0));
 }
 
-// An LDS pointer the compiler cannot see through: element reads at fixed
-// indices then use the instruction's offset field instead of a register
-// holding each address.
-template <typename P>
-__device__ __forceinline__ P* opaque_lds(const void* p) {
-  unsigned a = (unsigned)(uintptr_t)(const __attribute__((address_space(3))) char*)p;
-  asm volatile("" : "+v"(a));
-  return (P*)(uintptr_t)a;
-}
 
 // Geometry of merge `m` of the level described by na (children h x w).
 struct MergeGeom {
@@ -1106,12 +1144,60 @@ __global__ __launch_bounds__(2 * CP2) void k_nd_cut2(NdArgs na) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// 64 x 64 tiles of acc[x][y] = sum_k Za[k][x] Zb[k][y] on the fp64 matrix
+// cores (v_mfma_f64_16x16x4f64).  The workgroup's 4 waves each own a 32 x 32
+// quarter (wave w: rows 32 (w / 2), columns 32 (w % 2)) as 2 x 2 blocks of
+// 16 x 16.  Operands: lane l supplies A[l % 16][l / 16] and B[l / 16][l % 16]
+// of a 16 x 4 by 4 x 16 step; the result block holds D[l / 16 + 4 v][l % 16]
+// in element v of lane l.  The k-chunks pass through LDS rows of KLD doubles:
+// 16 lanes read 128 contiguous bytes, and the 640-byte row stride puts the
+// four row groups of a read in different bank halves.
+// ---------------------------------------------------------------------------
+typedef double f64x4 __attribute__((ext_vector_type(4)));
+constexpr int KC64 = 16;      // k per LDS chunk
+constexpr int KLD = 80;       // LDS row stride (doubles)
+
+struct MfmaTile {
+  f64x4 acc[2][2];
+  int wr, wc, lr, lc;         // wave quarter, lane row group, lane column
+  __device__ __forceinline__ void init(int tid) {
+    const int wv = tid >> 6, lane = tid & 63;
+    wr = wv >> 1;
+    wc = wv & 1;
+    lr = lane >> 4;
+    lc = lane & 15;
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j) acc[i][j] = f64x4{0.0, 0.0, 0.0, 0.0};
+  }
+  // one chunk of KC64 k from LDS (za, zb: [KC64][KLD], k-major)
+  __device__ __forceinline__ void step(const double* za, const double* zb) {
+#pragma unroll
+    for (int k4 = 0; k4 < KC64; k4 += 4) {
+      double a[2], b[2];
+#pragma unroll
+      for (int i = 0; i < 2; ++i) a[i] = za[(k4 + lr) * KLD + wr * 32 + i * 16 + lc];
+#pragma unroll
+      for (int j = 0; j < 2; ++j) b[j] = zb[(k4 + lr) * KLD + wc * 32 + j * 16 + lc];
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f64_16x16x4f64(a[i], b[j], acc[i][j], 0, 0, 0);
+    }
+  }
+  // tile-local coordinates of this lane's element v of block (i, j)
+  __device__ __forceinline__ int row(int i, int v) const { return wr * 32 + i * 16 + lr + 4 * v; }
+  __device__ __forceinline__ int col(int j) const { return wc * 32 + j * 16 + lc; }
+};
+
 // G' of the final step with more than 64 row inputs: G'[j][k] = sum_x
 // Z[x][M + j] Z[x][k] (Z: T x (M + T) in scratch) on 64 x 64 tiles.
 __global__ __launch_bounds__(256) void k_nd_gprod(NdArgs na) {
-  constexpr int KC = 16;
-  __shared__ double za[KC][64 + 2];
-  __shared__ double zb[KC][64 + 2];
+  __shared__ __attribute__((aligned(16))) double za[KC64 * KLD];
+  __shared__ __attribute__((aligned(16))) double zb[KC64 * KLD];
   const int tid = threadIdx.x;
   const int M = na.ms.M, N = na.ms.N, T = na.T, Np = na.ms.Np, Mp = na.ms.Mp;
   const int ntx = (Np + 63) / 64, nty = (Mp + 63) / 64;
@@ -1120,47 +1206,31 @@ __global__ __launch_bounds__(256) void k_nd_gprod(NdArgs na) {
   const int j0 = (tt / nty) * 64, k0 = (tt % nty) * 64;
   const int zld = M + T;
   const double* z = na.scratch + la * na.scr_stride;
-  const int tx = tid >> 4, ty = tid & 15;
-  double acc[4][4];
-#pragma unroll
-  for (int a = 0; a < 4; ++a)
-#pragma unroll
-    for (int b = 0; b < 4; ++b) acc[a][b] = 0.0;
-  for (int x0 = 0; x0 < T; x0 += KC) {
+  MfmaTile mt;
+  mt.init(tid);
+  for (int x0 = 0; x0 < T; x0 += KC64) {
 #pragma unroll
     for (int rr = 0; rr < 4; ++rr) {
       const int e = tid + 256 * rr, xx = e & 63, kk = e >> 6;
       const int x = x0 + kk;
       const int j = j0 + xx, k = k0 + xx;
-      za[kk][xx] = (x < T && j < N) ? z[(int64_t)x * zld + M + j] : 0.0;
-      zb[kk][xx] = (x < T && k < M) ? z[(int64_t)x * zld + k] : 0.0;
+      za[kk * KLD + xx] = (x < T && j < N) ? z[(int64_t)x * zld + M + j] : 0.0;
+      zb[kk * KLD + xx] = (x < T && k < M) ? z[(int64_t)x * zld + k] : 0.0;
     }
     __syncthreads();
-#pragma unroll 2
-    for (int kk = 0; kk < KC; ++kk) {
-      double sa[4], qb[4];
-#pragma unroll
-      for (int a = 0; a < 4; ++a) sa[a] = za[kk][4 * tx + a];
-#pragma unroll
-      for (int b = 0; b < 4; ++b) qb[b] = zb[kk][4 * ty + b];
-#pragma unroll
-      for (int a = 0; a < 4; ++a)
-#pragma unroll
-        for (int b = 0; b < 4; ++b) acc[a][b] = fma(sa[a], qb[b], acc[a][b]);
-    }
+    mt.step(za, zb);
     __syncthreads();
   }
   float* out = nd_ref(na, la).out;
 #pragma unroll
-  for (int a = 0; a < 4; ++a) {
-    const int j = j0 + 4 * tx + a;
-    if (j >= Np) continue;
+  for (int i = 0; i < 2; ++i)
 #pragma unroll
-    for (int b = 0; b < 4; ++b) {
-      const int k = k0 + 4 * ty + b;
-      if (k < Mp) out[j * Mp + k] = (j < N && k < M) ? (float)acc[a][b] : 0.0f;
-    }
-  }
+    for (int jb = 0; jb < 2; ++jb)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int j = j0 + mt.row(i, v), k = k0 + mt.col(jb);
+        if (j < Np && k < Mp) out[j * Mp + k] = (j < N && k < M) ? (float)mt.acc[i][jb][v] : 0.0f;
+      }
 }
 
 // ---------------------------------------------------------------------------
@@ -1218,9 +1288,8 @@ __global__ __launch_bounds__(256) void k_nd_dense0(NdArgs na) {
 // sink x source block (A: [sources (M) | sinks (T)] after the pivots).
 template <int OUT>
 __global__ __launch_bounds__(256) void k_nd_dschur(NdArgs na) {
-  constexpr int KC = 16;
-  __shared__ double za[KC][64 + 2];
-  __shared__ double zb[KC][64 + 2];
+  __shared__ __attribute__((aligned(16))) double za[KC64 * KLD];
+  __shared__ __attribute__((aligned(16))) double zb[KC64 * KLD];
   const int tid = threadIdx.x;
   const int E = na.dn - 64;
   const int M = na.ms.M;
@@ -1234,74 +1303,58 @@ __global__ __launch_bounds__(256) void k_nd_dschur(NdArgs na) {
   const int lx = OUT == 0 ? E : min(na.ms.N, na.T), ly = OUT == 0 ? E : M;   // valid x, y
   const double* z = na.scratch + la * na.scr_stride;
   const double* A = na.dA + la * na.in_stride;
-  const int tx = tid >> 4, ty = tid & 15;
-  double acc[4][4];
-#pragma unroll
-  for (int a = 0; a < 4; ++a)
-#pragma unroll
-    for (int b = 0; b < 4; ++b) acc[a][b] = 0.0;
-  for (int k0 = 0; k0 < 64; k0 += KC) {
+  MfmaTile mt;
+  mt.init(tid);
+  for (int k0 = 0; k0 < 64; k0 += KC64) {
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const int e = tid + 256 * r, xx = e & 63, kk = e >> 6;
       const int k = k0 + kk;
-      za[kk][xx] = (x0 + xx < lx) ? z[(int64_t)k * E + zx0 + xx] : 0.0;
-      zb[kk][xx] = (y0 + xx < ly) ? z[(int64_t)k * E + zy0 + xx] : 0.0;
+      za[kk * KLD + xx] = (x0 + xx < lx) ? z[(int64_t)k * E + zx0 + xx] : 0.0;
+      zb[kk * KLD + xx] = (y0 + xx < ly) ? z[(int64_t)k * E + zy0 + xx] : 0.0;
     }
     __syncthreads();
-#pragma unroll 2
-    for (int kk = 0; kk < KC; ++kk) {
-      double xa[4], yb[4];
-#pragma unroll
-      for (int a = 0; a < 4; ++a) xa[a] = za[kk][4 * tx + a];
-#pragma unroll
-      for (int b = 0; b < 4; ++b) yb[b] = zb[kk][4 * ty + b];
-#pragma unroll
-      for (int a = 0; a < 4; ++a)
-#pragma unroll
-        for (int b = 0; b < 4; ++b) acc[a][b] = fma(xa[a], yb[b], acc[a][b]);
-    }
+    mt.step(za, zb);
     __syncthreads();
   }
   if constexpr (OUT == 0) {
     double* B = na.dB + la * na.out_stride;
 #pragma unroll
-    for (int a = 0; a < 4; ++a) {
-      const int x = x0 + 4 * tx + a;
-      if (x >= E) continue;
+    for (int i = 0; i < 2; ++i)
 #pragma unroll
-      for (int b = 0; b < 4; ++b) {
-        const int y = y0 + 4 * ty + b;
-        if (y < E) B[(int64_t)x * na.dldo + y] = A[(int64_t)(64 + x) * na.dld + 64 + y] - acc[a][b];
-      }
-    }
+      for (int j = 0; j < 2; ++j)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          const int x = x0 + mt.row(i, v), y = y0 + mt.col(j);
+          if (x < E && y < E)
+            B[(int64_t)x * na.dldo + y] = A[(int64_t)(64 + x) * na.dld + 64 + y] - mt.acc[i][j][v];
+        }
   } else {
     const int Np = na.ms.Np, Mp = na.ms.Mp, N = na.ms.N;
     float* out = nd_ref(na, la).out;
 #pragma unroll
-    for (int a = 0; a < 4; ++a) {
-      const int j = x0 + 4 * tx + a;
-      if (j >= Np) continue;
+    for (int i = 0; i < 2; ++i)
 #pragma unroll
-      for (int b = 0; b < 4; ++b) {
-        const int k = y0 + 4 * ty + b;
-        if (k >= Mp) continue;
-        float v = 0.0f;
-        if (j < N && k < M)
-          v = (float)(acc[a][b] - A[(int64_t)(64 + M + j) * na.dld + 64 + k]);
-        out[j * Mp + k] = v;
-      }
-    }
+      for (int jb = 0; jb < 2; ++jb)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          const int j = x0 + mt.row(i, v), k = y0 + mt.col(jb);
+          if (j >= Np || k >= Mp) continue;
+          float val = 0.0f;
+          if (j < N && k < M)
+            val = (float)(mt.acc[i][jb][v] - A[(int64_t)(64 + M + j) * na.dld + 64 + k]);
+          out[j * Mp + k] = val;
+        }
   }
 }
 
 // ext = V - Z^T Z on one 64 x 64 tile of one merge (V: the children's
 // external-external entries).
-__global__ __launch_bounds__(256) void k_nd_schur(NdArgs na) {
-  constexpr int KC = 16;
+// Five waves per SIMD (96 VGPRs): its gathers need many waves in flight.
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(5))) void k_nd_schur(NdArgs na) {
   __shared__ short invt[2][MAXSLOT2];
-  __shared__ double za[KC][64 + 2];
-  __shared__ double zb[KC][64 + 2];
+  __shared__ __attribute__((aligned(16))) double za[KC64 * KLD];
+  __shared__ __attribute__((aligned(16))) double zb[KC64 * KLD];
   const int tid = threadIdx.x;
   const int nh = na.vert ? 2 * na.h : na.h, nw = na.vert ? na.w : 2 * na.w;
   const int Emax = 2 * (nh + nw);
@@ -1315,13 +1368,9 @@ __global__ __launch_bounds__(256) void k_nd_schur(NdArgs na) {
   if (nrx <= 0 || nry <= 0) return;
   inverse_tables<MAXSLOT2>(na, g, invt, 256);
   const double* z = na.scratch + g.la * na.scr_stride + (int64_t)g.m * Emax * c;
-  const int tx = tid >> 4, ty = tid & 15;
-  double acc[4][4];
-#pragma unroll
-  for (int a = 0; a < 4; ++a)
-#pragma unroll
-    for (int b = 0; b < 4; ++b) acc[a][b] = 0.0;
-  // Z chunk by chunk (KC rows), software pipelined: the next chunk's loads
+  MfmaTile mt;
+  mt.init(tid);
+  // Z chunk by chunk (KC64 rows), software pipelined: the next chunk's loads
   // are in flight while this chunk is multiplied
   const __amdgpu_buffer_rsrc_t rz = nd_rsrc(z, (unsigned)(c * Emax * 8));
   const unsigned ox = 8u * (unsigned)(x0 + min(tid & 63, nrx - 1));
@@ -1342,59 +1391,48 @@ __global__ __launch_bounds__(256) void k_nd_schur(NdArgs na) {
   double pza[4], pzb[4];
   load_chunk(0, pza, pzb);
 #pragma unroll 1
-  for (int k0 = 0; k0 < c; k0 += KC) {
+  for (int k0 = 0; k0 < c; k0 += KC64) {
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const int e = tid + 256 * r, xx = e & 63, kk = e >> 6;
-      za[kk][xx] = pza[r];
-      zb[kk][xx] = pzb[r];
+      za[kk * KLD + xx] = pza[r];
+      zb[kk * KLD + xx] = pzb[r];
     }
     __syncthreads();
-    if (k0 + KC < c) load_chunk(k0 + KC, pza, pzb);
-#pragma unroll 2
-    for (int kk = 0; kk < KC; ++kk) {
-      double xa[4], yb[4];
-#pragma unroll
-      for (int a = 0; a < 4; ++a) xa[a] = za[kk][4 * tx + a];
-#pragma unroll
-      for (int b = 0; b < 4; ++b) yb[b] = zb[kk][4 * ty + b];
-#pragma unroll
-      for (int a = 0; a < 4; ++a)
-#pragma unroll
-        for (int b = 0; b < 4; ++b) acc[a][b] = fma(xa[a], yb[b], acc[a][b]);
-    }
+    if (k0 + KC64 < c) load_chunk(k0 + KC64, pza, pzb);
+    mt.step(za, zb);
     __syncthreads();
   }
-  // the children's external entries of this thread's 4 x 4 outputs (all
-  // loads issued together)
+  // ext = V - Z^T Z, V the children's external entries: per block column,
+  // this lane's 8 entries are loaded together, then written
   const double* Y0 = na.buf_in + g.la * na.in_stride + (int64_t)g.cm0 * g.Ein * g.Ein;
   const double* Y1 = na.buf_in + g.la * na.in_stride + (int64_t)g.cm1 * g.Ein * g.Ein;
   const unsigned cb = (unsigned)(g.Ein * g.Ein * 8);
   const __amdgpu_buffer_rsrc_t r0 = nd_rsrc(Y0, cb), r1 = nd_rsrc(Y1, cb);
-  double vv[4][4];
-#pragma unroll
-  for (int a = 0; a < 4; ++a) {
-    const int x = min(x0 + 4 * tx + a, E - 1);
-    const int pa0 = invt[0][c + x], pa1 = invt[1][c + x];
-#pragma unroll
-    for (int b = 0; b < 4; ++b) {
-      const int yy = min(y0 + 4 * ty + b, E - 1);
-      const int pb0 = invt[0][c + yy], pb1 = invt[1][c + yy];
-      const double v0 = nd_load(r0, 8u * (unsigned)(max(pa0, 0) * g.Ein + max(pb0, 0)), 0);
-      const double v1 = nd_load(r1, 8u * (unsigned)(max(pa1, 0) * g.Ein + max(pb1, 0)), 0);
-      vv[a][b] = ((pa0 >= 0 && pb0 >= 0) ? v0 : 0.0) + ((pa1 >= 0 && pb1 >= 0) ? v1 : 0.0);
-    }
-  }
   double* ext = na.buf_out + g.la * na.out_stride + (int64_t)g.m * Emax * Emax;
 #pragma unroll
-  for (int a = 0; a < 4; ++a) {
-    const int x = x0 + 4 * tx + a;
-    if (x >= E) continue;
+  for (int j = 0; j < 2; ++j) {
+    const int y = y0 + mt.col(j);
+    const int yy = min(y, E - 1);
+    const int pb0 = invt[0][c + yy], pb1 = invt[1][c + yy];
+    double vv[2][4];
 #pragma unroll
-    for (int b = 0; b < 4; ++b) {
-      const int y = y0 + 4 * ty + b;
-      if (y < E) ext[x * Emax + y] = vv[a][b] - acc[a][b];
-    }
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int x = min(x0 + mt.row(i, v), E - 1);
+        const int pa0 = invt[0][c + x], pa1 = invt[1][c + x];
+        const double v0 = nd_load(r0, 8u * (unsigned)(max(pa0, 0) * g.Ein + max(pb0, 0)), 0);
+        const double v1 = nd_load(r1, 8u * (unsigned)(max(pa1, 0) * g.Ein + max(pb1, 0)), 0);
+        vv[i][v] = ((pa0 >= 0 && pb0 >= 0) ? v0 : 0.0) + ((pa1 >= 0 && pb1 >= 0) ? v1 : 0.0);
+      }
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int x = x0 + mt.row(i, v);
+        if (x < E && y < E) ext[x * Emax + y] = vv[i][v] - mt.acc[i][j][v];
+      }
   }
 }
 
