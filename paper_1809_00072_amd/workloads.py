@@ -132,6 +132,23 @@ def resnet18_layers():
     return L
 
 
+def resnet18_blocks():
+    """How the layers of ``resnet18_layers`` connect (the digital glue between
+    crossbar layers is not part of the crossbar path; this only names it):
+    the stem (conv1, ReLU, 3x3 stride-2 max pool), eight basic blocks
+    ``(conv1, conv2, downsample or None)`` as layer indices, each computing
+    ReLU(conv2(ReLU(conv1(x))) + shortcut(x)), then a global average pool and
+    the classifier."""
+    layers = resnet18_layers()
+    idx = {spec["name"]: l for l, spec in enumerate(layers)}
+    blocks = []
+    for stage in range(4):
+        for block in range(2):
+            pre = "layer%d.%d" % (stage + 1, block)
+            blocks.append((idx[pre + ".conv1"], idx[pre + ".conv2"], idx.get(pre + ".downsample")))
+    return {"stem": idx["conv1"], "blocks": blocks, "fc": idx["fc"]}
+
+
 def resnet50_layers():
     """The 53 convolutions and the classifier of ResNet-50 (bottleneck blocks,
     stride on the 3x3 convolution)."""
