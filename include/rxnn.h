@@ -262,8 +262,9 @@ rxnn_status rxnn_crossbar_vmm_noalloc(const rxnn_layer* layer, const rxnn_periph
  * The patch matrix is never written: the layer keeps a DAC output buffer
  * (the input with pad zero pixels on every side), a table of patch-column
  * offsets (rebuilt when the geometry changes) and, as for the FC entry, an
- * int32 workspace when needed.  RXNN_EUNSUPPORTED when P >= 2^22 or when
- * the padded images one 128-pixel block touches exceed 2 GiB.
+ * int32 workspace when needed.  RXNN_EUNSUPPORTED when P >= 2^22, when
+ * the padded images one 128-pixel block touches exceed 2 GiB, or when the
+ * zero-bordered input holds 2^32 - 2^23 elements or more.
  */
 rxnn_status rxnn_conv_layer(const rxnn_layer* layer, const rxnn_periph_params* periph,
                             const rxnn_conv_desc* conv, const float* X, float* Y,

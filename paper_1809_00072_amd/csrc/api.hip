@@ -867,6 +867,10 @@ rxnn_status rxnn_conv_layer(const rxnn_layer* layer, const rxnn_periph_params* p
         (int64_t)1 << 31)
       return fail(RXNN_EUNSUPPORTED, "input images too large for the evaluation kernel");
   }
+  if ((int64_t)cd.n * cd.c_in * (cd.h + 2 * (int64_t)cd.pad) * (cd.w + 2 * (int64_t)cd.pad) >=
+      ((int64_t)1 << 32) - ((int64_t)1 << 23))
+    return fail(RXNN_EUNSUPPORTED, "the zero-bordered input must hold fewer than 2^32 - 2^23 "
+                "elements (32-bit indexing of the DAC pass)");
   if (Bv == 0) return RXNN_OK;
   if (!X || !Y) return fail(RXNN_EINVAL, "X and Y must not be NULL");
   DeviceGuard dg(L->device);

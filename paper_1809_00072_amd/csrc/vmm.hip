@@ -47,6 +47,8 @@
 // elements k = 4 (l / 16) + s of its row and column, so each lane fetches
 // four consecutive k with one 16-byte LDS read for both operands.
 
+#include <algorithm>
+
 #include "common.h"
 
 namespace rxnn {
@@ -129,8 +131,8 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t uniform_rsrc(const void* p, in
 // (convolution)
 template <bool CONV>
 __global__ __launch_bounds__(256) void k_dac(PeriphScalars ps, ConvGeom cg, FastDiv fd_wp,
-                                             const float* __restrict__ X, float* __restrict__ V,
-                                             int64_t n_out) {
+                                             FastDiv fd_pp, const float* __restrict__ X,
+                                             float* __restrict__ V, int64_t n_out) {
   __shared__ float lut[256];
   if (ps.dac_bits > 0) {
     const int L = ps.dac_levels;
@@ -148,28 +150,28 @@ __global__ __launch_bounds__(256) void k_dac(PeriphScalars ps, ConvGeom cg, Fast
     return fmaxf(x, 0.0f) * ps.s_v_ideal;
   };
   if (CONV) {
-    // planes (img, ci) over the blocks; the threads stride over the padded
-    // plane eight elements at a time, so that their loads are in flight
-    // together (row = e / wp by an invariant-divisor multiply)
-    const int plane_p = cg.hp * cg.wp;
-    const int nt = blockDim.x;
-    for (int64_t plane = blockIdx.x; plane < n_out; plane += gridDim.x) {
-      const float* Xp = X + plane * cg.h * cg.w;
-      float* Vp = V + plane * plane_p;
-      for (int e0 = threadIdx.x; e0 < plane_p; e0 += 8 * nt) {
-        float x[8];
+    // the threads stride over the whole padded tensor (every plane of every
+    // image) eight elements at a time, so that their loads are in flight
+    // together; plane, row and column by invariant-divisor multiplies
+    // (the tensor holds fewer than 2^32 elements)
+    const uint32_t plane_p = (uint32_t)(cg.hp * cg.wp);
+    const uint32_t total = (uint32_t)(n_out * plane_p);
+    const uint32_t stride = gridDim.x * blockDim.x;
+    for (uint32_t e0 = blockIdx.x * blockDim.x + threadIdx.x; e0 < total; e0 += 8 * stride) {
+      float x[8];
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
-          const int e = e0 + j * nt;
-          const int yp = (int)div_by((uint32_t)e, fd_wp), xp = e - yp * cg.wp;
-          const int iy = yp - cg.pad, ix = xp - cg.pad;
-          x[j] = (e < plane_p && iy >= 0 && iy < cg.h && ix >= 0 && ix < cg.w)
-                     ? Xp[iy * cg.w + ix] : 0.0f;
-        }
-#pragma unroll
-        for (int j = 0; j < 8; ++j)
-          if (e0 + j * nt < plane_p) Vp[e0 + j * nt] = dac(x[j]);
+      for (int j = 0; j < 8; ++j) {
+        const uint32_t e = e0 + j * stride;
+        const uint32_t plane = div_by(e, fd_pp);
+        const uint32_t rem = e - plane * plane_p;
+        const int yp = (int)div_by(rem, fd_wp), xp = (int)rem - yp * cg.wp;
+        const int iy = yp - cg.pad, ix = xp - cg.pad;
+        x[j] = (e < total && iy >= 0 && iy < cg.h && ix >= 0 && ix < cg.w)
+                   ? X[(size_t)plane * cg.h * cg.w + iy * cg.w + ix] : 0.0f;
       }
+#pragma unroll
+      for (int j = 0; j < 8; ++j)
+        if (e0 + j * stride < total) V[e0 + j * stride] = dac(x[j]);
     }
   } else {
     // rows b over blockIdx.y: V[b][p] = DAC(X[b][p]) for p < P, 0 up to ldv
@@ -592,6 +594,43 @@ __global__ __launch_bounds__(NTHR, 2) void k_xbar_vmm(VmmArgs va) {
   // is row_base(bv) + q times the column stride.  The int32 workspace is
   // Bv x Q (lanes along q: coalesced atomics).
   const int64_t qstride = va.hw_out > 0 ? va.hw_out : 1;
+  if (CONV && !DEBUG && !atomic) {
+    // NCHW output: a lane's results are 4 rows of one output channel, so a
+    // direct store would scatter each instruction over 16 channels.  Each
+    // wave passes its 32 x BN block through LDS (the V staging buffer, free
+    // once every wave is past its last stage) and then writes 32
+    // consecutive pixels of each channel per instruction.
+    constexpr int TS = 33;   // LDS column stride of the transposed block
+    static_assert(4 * BN * TS <= BM * LDK, "the transposed blocks fit the V buffer");
+    __syncthreads();
+    float* tb = Vs + wave * (BN * TS);
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+        for (int v = 0; v < 4; ++v)
+          tb[(nt * 16 + li) * TS + mt * 16 + 4 * g + v] =
+              QADC ? (float)iacc[mt][nt][v] * scale : facc[mt][nt][v] * scale;
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    const int row = lane & 31;
+    const int64_t bv = b0 + wave * 32 + row;
+    int64_t row_base = 0;
+    if (bv < va.Bv) {
+      const int img = (int)div_by((uint32_t)bv, va.fd_hw);   // hw_out = H_out W_out
+      row_base = (int64_t)img * ms.Q * va.hw_out + (bv - (int64_t)img * va.hw_out);
+    }
+#pragma unroll 4
+    for (int j = 0; j < BN / 2; ++j) {
+      const int col = 2 * j + (lane >> 5);
+      const int n = n0 + col;
+      const int64_t q = (int64_t)c * tg.N + n;
+      if (bv < va.Bv && n < tg.N && q < ms.Q) va.Y[row_base + q * qstride] = tb[col * TS + row];
+    }
+    return;
+  }
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
@@ -945,14 +984,18 @@ hipError_t launch_dac(const MapScalars& ms, const PeriphScalars& ps,
   if (conv) {
     const ConvGeom cg = conv_geom(*conv);
     const int64_t planes = (int64_t)conv->n * conv->c_in;
-    hipLaunchKernelGGL(k_dac<true>, dim3((unsigned)(planes < 8192 ? planes : 8192)), dim3(256),
-                       0, s, ps, cg, fast_div((uint32_t)cg.wp), X, V, planes);
+    const int64_t total = planes * cg.hp * cg.wp;
+    if (total >= ((int64_t)1 << 32) - 8 * 256 * 2048) return hipErrorInvalidValue;
+    const int64_t blocks = std::min<int64_t>(2048, (total + 8 * 256 - 1) / (8 * 256));
+    hipLaunchKernelGGL(k_dac<true>, dim3((unsigned)std::max<int64_t>(1, blocks)), dim3(256), 0,
+                       s, ps, cg, fast_div((uint32_t)cg.wp),
+                       fast_div((uint32_t)(cg.hp * cg.wp)), X, V, planes);
   } else {
     ConvGeom cg{};
     cg.c_in = (int)ms.P;
     cg.wp = (int)fc_ldv(ms);
     hipLaunchKernelGGL(k_dac<false>, dim3((unsigned)(Bv < 8192 ? Bv : 8192)), dim3(256), 0, s,
-                       ps, cg, FastDiv{1, 0, 0}, X, V, Bv);
+                       ps, cg, FastDiv{1, 0, 0}, FastDiv{1, 0, 0}, X, V, Bv);
   }
   return hipGetLastError();
 }
