@@ -699,6 +699,10 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t nd_rsrc(const void* p, unsigne
                                            __builtin_amdgcn_readfirstlane((int)bytes), 0x00020000);
 }
 
+// A per-lane buffer offset beyond every level buffer's range: the load returns
+// 0 and touches no memory (the range check covers the VGPR offset).
+constexpr unsigned kNdOob = 0x80000000u;
+
 __device__ __forceinline__ double nd_load(__amdgpu_buffer_rsrc_t r, unsigned voff, unsigned soff) {
   return __builtin_bit_cast(double, __builtin_amdgcn_raw_buffer_load_b64(r, voff, soff, 0));
 }
@@ -751,6 +755,78 @@ __device__ void inverse_tables(const NdArgs& na, const MergeGeom& g, short (*inv
   __syncthreads();
 }
 
+// ---------------------------------------------------------------------------
+// 64 x 64 tiles of acc[x][y] = sum_k Za[k][x] Zb[k][y] on the fp64 matrix
+// cores (v_mfma_f64_16x16x4f64).  The workgroup's 4 waves each own a 32 x 32
+// quarter (wave w: rows 32 (w / 2), columns 32 (w % 2)) as 2 x 2 blocks of
+// 16 x 16.  Operands: lane l supplies A[l % 16][l / 16] and B[l / 16][l % 16]
+// of a 16 x 4 by 4 x 16 step; the result block holds D[l / 16 + 4 v][l % 16]
+// in element v of lane l.  The k-chunks pass through LDS rows of KLD doubles:
+// 16 lanes read 128 contiguous bytes, and the 640-byte row stride puts the
+// four row groups of a read in different bank halves.
+// ---------------------------------------------------------------------------
+typedef double f64x4 __attribute__((ext_vector_type(4)));
+constexpr int KC64 = 16;      // k per LDS chunk
+constexpr int KLD = 80;       // LDS row stride (doubles)
+
+struct MfmaTile {
+  f64x4 acc[2][2];
+  int wr, wc, lr, lc;         // wave quarter, lane row group, lane column
+  __device__ __forceinline__ void init(int tid) {
+    const int wv = tid >> 6, lane = tid & 63;
+    wr = wv >> 1;
+    wc = wv & 1;
+    lr = lane >> 4;
+    lc = lane & 15;
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j) acc[i][j] = f64x4{0.0, 0.0, 0.0, 0.0};
+  }
+  // one chunk of KC64 k from LDS (za, zb: [KC64][KLD], k-major)
+  __device__ __forceinline__ void step(const double* za, const double* zb) {
+#pragma unroll
+    for (int k4 = 0; k4 < KC64; k4 += 4) {
+      double a[2], b[2];
+#pragma unroll
+      for (int i = 0; i < 2; ++i) a[i] = za[(k4 + lr) * KLD + wr * 32 + i * 16 + lc];
+#pragma unroll
+      for (int j = 0; j < 2; ++j) b[j] = zb[(k4 + lr) * KLD + wc * 32 + j * 16 + lc];
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f64_16x16x4f64(a[i], b[j], acc[i][j], 0, 0, 0);
+    }
+  }
+  // kn k (a multiple of 4) from k-major LDS rows of ld doubles; columns at or
+  // beyond `lim` of either operand read as 0
+  __device__ __forceinline__ void step_ld(const double* za, const double* zb, int ld, int kn,
+                                          int xlim, int ylim) {
+    for (int k4 = 0; k4 < kn; k4 += 4) {
+      double a[2], b[2];
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        const int x = wr * 32 + i * 16 + lc;
+        a[i] = x < xlim ? za[(k4 + lr) * ld + x] : 0.0;
+      }
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        const int y = wc * 32 + j * 16 + lc;
+        b[j] = y < ylim ? zb[(k4 + lr) * ld + y] : 0.0;
+      }
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f64_16x16x4f64(a[i], b[j], acc[i][j], 0, 0, 0);
+    }
+  }
+  // tile-local coordinates of this lane's element v of block (i, j)
+  __device__ __forceinline__ int row(int i, int v) const { return wr * 32 + i * 16 + lr + 4 * v; }
+  __device__ __forceinline__ int col(int j) const { return wc * 32 + j * 16 + lc; }
+};
+
 // MODE 0: a merge (children through the port tables); 1: the final step;
 // 2: a stage of a dense combined matrix (its first C rows are the pivots,
 // the rest of its columns are handled in panels of na.dpanel).
@@ -764,10 +840,11 @@ __global__ __launch_bounds__(512) void k_nd_cut(NdArgs na) {
   // final step: the eliminated rows' sink and source columns for G'
   __shared__ double zs[FINAL ? C : 1][FINAL ? 64 + 2 : 1];
   __shared__ double zq[FINAL ? C : 1][FINAL ? 64 + 2 : 1];
-  // small merges (C <= 16, at most 64 ports): Z and the Schur update stay
-  // in this workgroup
-  constexpr bool kFuse = MODE == 0 && C <= 16;
-  __shared__ double zl[kFuse ? C : 1][kFuse ? 64 + 2 : 1];
+  // small merges (C <= 32 cut nodes, at most 192 ports): Z stays in LDS and
+  // this workgroup also computes the Schur update on fp64 MFMA tiles
+  constexpr bool kFuse = MODE == 0 && C <= 32;
+  constexpr int ZLD = C <= 8 ? 52 : (C <= 16 ? 100 : 196);   // Z row stride in LDS
+  __shared__ __attribute__((aligned(16))) double zl[kFuse ? C * ZLD : 1];
   const int y = threadIdx.x;
   const int T = na.T;
   int E, ncol, Emax = 0;
@@ -837,18 +914,20 @@ __global__ __launch_bounds__(512) void k_nd_cut(NdArgs na) {
     const int pb0 = y < ncol ? invt[0][y] : -1, pb1 = y < ncol ? invt[1][y] : -1;
     const unsigned cb = (unsigned)(g.Ein * g.Ein * 8);
     const __amdgpu_buffer_rsrc_t r0 = nd_rsrc(Y0, cb), r1 = nd_rsrc(Y1, cb);
-    const unsigned q0 = 8u * (unsigned)max(pb0, 0), q1 = 8u * (unsigned)max(pb1, 0);
+    const unsigned q0 = pb0 >= 0 ? 8u * (unsigned)pb0 : kNdOob;
+    const unsigned q1 = pb1 >= 0 ? 8u * (unsigned)pb1 : kNdOob;
     const lds_i16* iv = opaque_lds<lds_i16>(&invt[0][0]);
     // the row's port is uniform (a scalar offset), the column's fixed per
-    // lane; clamped ports keep every offset valid, so that all loads of a
-    // chunk are in flight together, and entries without a port are masked
+    // lane; an entry without a port takes the out-of-range lane offset, so it
+    // reads 0 without a memory access, and every load of a chunk stays in
+    // flight together
 #pragma unroll
     for (int x = 0; x < C; ++x) {
       const int pa0 = __builtin_amdgcn_readfirstlane(iv[x]);
       const int pa1 = __builtin_amdgcn_readfirstlane(iv[MAXSLOT + x]);
-      const double v0 = nd_load(r0, q0, 8u * (unsigned)(max(pa0, 0) * g.Ein));
-      const double v1 = nd_load(r1, q1, 8u * (unsigned)(max(pa1, 0) * g.Ein));
-      U[x] = ((pa0 >= 0 && pb0 >= 0) ? v0 : 0.0) + ((pa1 >= 0 && pb1 >= 0) ? v1 : 0.0);
+      const double v0 = nd_load(r0, pa0 >= 0 ? q0 : kNdOob, 8u * (unsigned)(max(pa0, 0) * g.Ein));
+      const double v1 = nd_load(r1, pa1 >= 0 ? q1 : kNdOob, 8u * (unsigned)(max(pa1, 0) * g.Ein));
+      U[x] = v0 + v1;
       // 16 rows (32 loads) in flight per round trip
       if ((x & 15) == 15) {
         pin8(U, x - 15);
@@ -895,58 +974,51 @@ __global__ __launch_bounds__(512) void k_nd_cut(NdArgs na) {
   __syncthreads();
   const lds_f64* is = opaque_lds<lds_f64>(&isq[0]);
   if constexpr (kFuse) {
-    if (Emax <= 64) {   // schur_fused(C, Emax): launched with at least 256 threads
+    if (Emax <= ZLD - 4) {   // schur_fused(C, Emax): launched with exactly 256 threads
       if (y >= C && y < ncol) {
 #pragma unroll
-        for (int x = 0; x < C; ++x) zl[x][y - C] = U[x] * is[x];
+        for (int x = 0; x < C; ++x) zl[x * ZLD + (y - C)] = U[x] * is[x];
       }
       __syncthreads();
       double* ext = na.buf_out + la * na.out_stride + (int64_t)g.m * Emax * Emax;
-      // 256 threads (at least): one 4 x 4 block of outputs each
-      if (threadIdx.x < 256) {
-        const int tx = threadIdx.x >> 4, ty = threadIdx.x & 15;
-        // the children's entries first, so that their loads overlap the product
-        double vv[4][4];
+      const unsigned cbf = (unsigned)(g.Ein * g.Ein * 8);
+      const __amdgpu_buffer_rsrc_t r0f = nd_rsrc(Y0, cbf), r1f = nd_rsrc(Y1, cbf);
+      const int nt = (E + 63) / 64;
+      // ext = V - Z^T Z on 64 x 64 tiles: the children's entries of a tile
+      // are loaded before its product, so that they arrive during it
+#pragma unroll 1
+      for (int tt = 0; tt < nt * nt; ++tt) {
+        const int x0 = (tt / nt) * 64, y0 = (tt % nt) * 64;
+        MfmaTile mt;
+        mt.init(threadIdx.x);
+        double vv[2][2][4];
 #pragma unroll
-        for (int a = 0; a < 4; ++a) {
-          const int x = min(4 * tx + a, E - 1);
-          const int pa0 = invt[0][C + x], pa1 = invt[1][C + x];
+        for (int j = 0; j < 2; ++j) {
+          const int yy = min(y0 + mt.col(j), E - 1);
+          const int pb0 = invt[0][C + yy], pb1 = invt[1][C + yy];
 #pragma unroll
-          for (int b = 0; b < 4; ++b) {
-            const int yy = min(4 * ty + b, E - 1);
-            const int pb0 = invt[0][C + yy], pb1 = invt[1][C + yy];
-            const double v0 = Y0[max(pa0, 0) * g.Ein + max(pb0, 0)];
-            const double v1 = Y1[max(pa1, 0) * g.Ein + max(pb1, 0)];
-            vv[a][b] = ((pa0 >= 0 && pb0 >= 0) ? v0 : 0.0) + ((pa1 >= 0 && pb1 >= 0) ? v1 : 0.0);
-          }
+          for (int i = 0; i < 2; ++i)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+              const int x = min(x0 + mt.row(i, v), E - 1);
+              const int pa0 = invt[0][C + x], pa1 = invt[1][C + x];
+              const double v0 = nd_load(r0f, (pa0 >= 0 && pb0 >= 0)
+                                                 ? 8u * (unsigned)(pa0 * g.Ein + pb0) : kNdOob, 0);
+              const double v1 = nd_load(r1f, (pa1 >= 0 && pb1 >= 0)
+                                                 ? 8u * (unsigned)(pa1 * g.Ein + pb1) : kNdOob, 0);
+              vv[i][j][v] = v0 + v1;
+            }
         }
-        double acc[4][4];
+        mt.step_ld(zl + x0, zl + y0, ZLD, C, E - x0, E - y0);
 #pragma unroll
-        for (int a = 0; a < 4; ++a)
+        for (int i = 0; i < 2; ++i)
 #pragma unroll
-          for (int b = 0; b < 4; ++b) acc[a][b] = 0.0;
-#pragma unroll 2
-        for (int k = 0; k < C; ++k) {
-          double xa[4], yb[4];
+          for (int j = 0; j < 2; ++j)
 #pragma unroll
-          for (int a = 0; a < 4; ++a) xa[a] = zl[k][4 * tx + a];
-#pragma unroll
-          for (int b = 0; b < 4; ++b) yb[b] = zl[k][4 * ty + b];
-#pragma unroll
-          for (int a = 0; a < 4; ++a)
-#pragma unroll
-            for (int b = 0; b < 4; ++b) acc[a][b] = fma(xa[a], yb[b], acc[a][b]);
-        }
-#pragma unroll
-        for (int a = 0; a < 4; ++a) {
-          const int x = 4 * tx + a;
-          if (x >= E) continue;
-#pragma unroll
-          for (int b = 0; b < 4; ++b) {
-            const int yy = 4 * ty + b;
-            if (yy < E) ext[x * Emax + yy] = vv[a][b] - acc[a][b];
-          }
-        }
+            for (int v = 0; v < 4; ++v) {
+              const int x = x0 + mt.row(i, v), yy = y0 + mt.col(j);
+              if (x < E && yy < E) ext[x * Emax + yy] = vv[i][j][v] - mt.acc[i][j][v];
+            }
       }
       return;
     }
@@ -1077,15 +1149,16 @@ __global__ __launch_bounds__(2 * CP2) void k_nd_cut2(NdArgs na) {
     const int pb0 = slot >= 0 ? invt[0][slot] : -1, pb1 = slot >= 0 ? invt[1][slot] : -1;
     const unsigned cb = (unsigned)(g.Ein * g.Ein * 8);
     const __amdgpu_buffer_rsrc_t r0 = nd_rsrc(Y0, cb), r1 = nd_rsrc(Y1, cb);
-    const unsigned q0 = 8u * (unsigned)max(pb0, 0), q1 = 8u * (unsigned)max(pb1, 0);
+    const unsigned q0 = pb0 >= 0 ? 8u * (unsigned)pb0 : kNdOob;
+    const unsigned q1 = pb1 >= 0 ? 8u * (unsigned)pb1 : kNdOob;
 #pragma unroll
     for (int i = 0; i < 64; ++i) {
       const int x = 64 * rg + i;
       const int pa0 = __builtin_amdgcn_readfirstlane(invt[0][x]);
       const int pa1 = __builtin_amdgcn_readfirstlane(invt[1][x]);
-      const double v0 = nd_load(r0, q0, 8u * (unsigned)(max(pa0, 0) * g.Ein));
-      const double v1 = nd_load(r1, q1, 8u * (unsigned)(max(pa1, 0) * g.Ein));
-      U[i] = ((pa0 >= 0 && pb0 >= 0) ? v0 : 0.0) + ((pa1 >= 0 && pb1 >= 0) ? v1 : 0.0);
+      const double v0 = nd_load(r0, pa0 >= 0 ? q0 : kNdOob, 8u * (unsigned)(max(pa0, 0) * g.Ein));
+      const double v1 = nd_load(r1, pa1 >= 0 ? q1 : kNdOob, 8u * (unsigned)(max(pa1, 0) * g.Ein));
+      U[i] = v0 + v1;
       if ((i & 7) == 7) pin8(U, i - 7);
     }
   }
@@ -1143,55 +1216,6 @@ __global__ __launch_bounds__(2 * CP2) void k_nd_cut2(NdArgs na) {
     }
   }
 }
-
-// ---------------------------------------------------------------------------
-// 64 x 64 tiles of acc[x][y] = sum_k Za[k][x] Zb[k][y] on the fp64 matrix
-// cores (v_mfma_f64_16x16x4f64).  The workgroup's 4 waves each own a 32 x 32
-// quarter (wave w: rows 32 (w / 2), columns 32 (w % 2)) as 2 x 2 blocks of
-// 16 x 16.  Operands: lane l supplies A[l % 16][l / 16] and B[l / 16][l % 16]
-// of a 16 x 4 by 4 x 16 step; the result block holds D[l / 16 + 4 v][l % 16]
-// in element v of lane l.  The k-chunks pass through LDS rows of KLD doubles:
-// 16 lanes read 128 contiguous bytes, and the 640-byte row stride puts the
-// four row groups of a read in different bank halves.
-// ---------------------------------------------------------------------------
-typedef double f64x4 __attribute__((ext_vector_type(4)));
-constexpr int KC64 = 16;      // k per LDS chunk
-constexpr int KLD = 80;       // LDS row stride (doubles)
-
-struct MfmaTile {
-  f64x4 acc[2][2];
-  int wr, wc, lr, lc;         // wave quarter, lane row group, lane column
-  __device__ __forceinline__ void init(int tid) {
-    const int wv = tid >> 6, lane = tid & 63;
-    wr = wv >> 1;
-    wc = wv & 1;
-    lr = lane >> 4;
-    lc = lane & 15;
-#pragma unroll
-    for (int i = 0; i < 2; ++i)
-#pragma unroll
-      for (int j = 0; j < 2; ++j) acc[i][j] = f64x4{0.0, 0.0, 0.0, 0.0};
-  }
-  // one chunk of KC64 k from LDS (za, zb: [KC64][KLD], k-major)
-  __device__ __forceinline__ void step(const double* za, const double* zb) {
-#pragma unroll
-    for (int k4 = 0; k4 < KC64; k4 += 4) {
-      double a[2], b[2];
-#pragma unroll
-      for (int i = 0; i < 2; ++i) a[i] = za[(k4 + lr) * KLD + wr * 32 + i * 16 + lc];
-#pragma unroll
-      for (int j = 0; j < 2; ++j) b[j] = zb[(k4 + lr) * KLD + wc * 32 + j * 16 + lc];
-#pragma unroll
-      for (int i = 0; i < 2; ++i)
-#pragma unroll
-        for (int j = 0; j < 2; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f64_16x16x4f64(a[i], b[j], acc[i][j], 0, 0, 0);
-    }
-  }
-  // tile-local coordinates of this lane's element v of block (i, j)
-  __device__ __forceinline__ int row(int i, int v) const { return wr * 32 + i * 16 + lr + 4 * v; }
-  __device__ __forceinline__ int col(int j) const { return wc * 32 + j * 16 + lc; }
-};
 
 // G' of the final step with more than 64 row inputs: G'[j][k] = sum_x
 // Z[x][M + j] Z[x][k] (Z: T x (M + T) in scratch) on 64 x 64 tiles.
@@ -1422,9 +1446,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(5))) void k
       for (int v = 0; v < 4; ++v) {
         const int x = min(x0 + mt.row(i, v), E - 1);
         const int pa0 = invt[0][c + x], pa1 = invt[1][c + x];
-        const double v0 = nd_load(r0, 8u * (unsigned)(max(pa0, 0) * g.Ein + max(pb0, 0)), 0);
-        const double v1 = nd_load(r1, 8u * (unsigned)(max(pa1, 0) * g.Ein + max(pb1, 0)), 0);
-        vv[i][v] = ((pa0 >= 0 && pb0 >= 0) ? v0 : 0.0) + ((pa1 >= 0 && pb1 >= 0) ? v1 : 0.0);
+        // an entry that a child does not hold reads 0 without a memory access
+        const double v0 = nd_load(r0, (pa0 >= 0 && pb0 >= 0) ? 8u * (unsigned)(pa0 * g.Ein + pb0)
+                                                             : kNdOob, 0);
+        const double v1 = nd_load(r1, (pa1 >= 0 && pb1 >= 0) ? 8u * (unsigned)(pa1 * g.Ein + pb1)
+                                                             : kNdOob, 0);
+        vv[i][v] = v0 + v1;
       }
 #pragma unroll
     for (int i = 0; i < 2; ++i)
@@ -1483,7 +1510,9 @@ static bool cut_in_registers(int c, int ncol) {
 }
 
 // Merges whose Schur update runs inside k_nd_cut (its kFuse path).
-static bool schur_fused(int c, int emax) { return c <= 16 && emax <= 64; }
+static bool schur_fused(int c, int emax) {
+  return (c == 8 && emax <= 48) || (c == 16 && emax <= 96) || (c == 32 && emax <= 192);
+}
 
 template <bool FINAL>
 static void launch_cut(const NdArgs& na, dim3 grid, int c, int ncol, bool fused, hipStream_t s) {
