@@ -56,9 +56,15 @@ FP32_MFMA_PEAK_TFLOPS = 157.3   # MI355X dense fp32 matrix
 # the summary and its commands are in the repository's profiles folder
 VMM_TRAFFIC_BYTES = 2.0 * 15384 * 1024 + 40314 * 1024
 # HBM bytes of k_xbar_vmm per evaluation-only pass of a stacked workload
-# (summed over its layers), from the same counters and calibration, keyed by
-# (workload, crossbar side, wire); None where they have not been taken
-STACK_VMM_TRAFFIC = {}
+# (summed over its layers), from the same counters and the same calibration
+# (fetch x 2.000, write x 1.000 from a plain 2 GiB copy in the same run), keyed
+# by (workload, crossbar side, wire); the summary and its commands are in the
+# repository's profiles folder.  Absent where they have not been taken.
+STACK_VMM_TRAFFIC = {
+    # ResNet-50 stack, 256 x 256, 2.5 ohm: 7,188,444 KiB fetched x 2.000 +
+    # 5,896,956 KiB written per pass (54 dispatches)
+    ("resnet50", 256, 2.5): 2.0 * 7188443.9 * 1024 + 5896956.4 * 1024,
+}
 FP64_PEAK_TFLOPS = 78.6         # MI355X fp64 (vector and matrix)
 HBM_PEAK_GBS = 8000.0
 
@@ -724,6 +730,8 @@ def bench_stack(args):
                 rxnn.remap_layer(e["L"], e["W"], stream)
         gen = generation_info(timed(gen_all, 1, 0), total_arrays, layers[0]["L"].M,
                               layers[0]["L"].N)
+    if args.copy_probe:
+        copy_probe(torch, dev)
     parity = None
     if results is not None:
         try:
