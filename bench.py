@@ -34,7 +34,7 @@ stream.
 --retrain adds, for the convolution, a leg timed after the others: one
 model-in-the-loop re-training step = G' rebuild + crossbar forward pass +
 floating-point backward pass (dX and dW through the ideal weights), with the
-backward GEMMs' fp32 roofline.
+backward contractions' fp32 roofline.
 """
 
 from __future__ import annotations
@@ -442,7 +442,7 @@ def cpu_baseline_conv(work):
 
 
 KERNEL_NAMES = ("wmax", "nd_block", "nd_merge", "nd_final", "gprime_sweep", "dac", "ktab",
-                "fill", "xbar_vmm", "finish", "bw_gemm", "bw_aux", "gload")
+                "fill", "xbar_vmm", "finish", "bw_dw", "bw_dx", "bw_reduce", "gload")
 
 
 def read_kernels(rxnn, steps):
@@ -877,14 +877,23 @@ def retrain_leg(args, torch, rxnn, wl, L, pp, cv, Wd, Xd, Yd, stream):
     kern = read_kernels(rxnn, args.steps)
     ho, wo = rxnn.conv_out_hw(cv)
     bv = cv["n"] * ho * wo
-    gemm_flops = 2 * 2.0 * bv * L.P * L.Q           # dW = cols^T dY and dcols = dY W^T
-    g_us = kern["bw_gemm"]["us_per_step"]
-    ach = gemm_flops / (g_us * 1e-6) / 1e12
+    # dW = clip(patches)^T dY and dX = dY W^T over the patch columns: 2 Bv P Q
+    # multiply-adds each
+    leg = {}
+    for name in ("bw_dw", "bw_dx"):
+        us = kern[name]["us_per_step"]
+        ach = 2.0 * bv * L.P * L.Q / (us * 1e-6) / 1e12
+        leg[name] = {"us_per_step": us, "bound": "mfma", "achieved": ach,
+                     "peak": FP32_MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
+                     "frac": ach / FP32_MFMA_PEAK_TFLOPS, "flops": 2.0 * bv * L.P * L.Q}
+    g_us = leg["bw_dw"]["us_per_step"] + leg["bw_dx"]["us_per_step"]
+    ach = 4.0 * bv * L.P * L.Q / (g_us * 1e-6) / 1e12
     print("[bench] retrain: %.3f ms/step" % ms, file=sys.stderr, flush=True)
-    return {"ms_per_step": ms, "backward_gemm": {
+    return {"ms_per_step": ms, "backward": {
         "us_per_step": g_us, "bound": "mfma", "achieved": ach, "peak": FP32_MFMA_PEAK_TFLOPS,
-        "unit": "TFLOP/s", "frac": ach / FP32_MFMA_PEAK_TFLOPS, "flops": gemm_flops},
-        "backward_aux_us_per_step": kern.get("bw_aux", {}).get("us_per_step", 0.0),
+        "unit": "TFLOP/s", "frac": ach / FP32_MFMA_PEAK_TFLOPS, "flops": 4.0 * bv * L.P * L.Q},
+        **leg,
+        "backward_reduce_us_per_step": kern.get("bw_reduce", {}).get("us_per_step", 0.0),
         "kernels": kern}
 
 

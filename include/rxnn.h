@@ -288,14 +288,20 @@ rxnn_status rxnn_conv_layer(const rxnn_layer* layer, const rxnn_periph_params* p
  *       n x c_out x H_out x W_out).
  *   dX  device fp32, the layout of X, overwritten; dW device fp32 P x Q,
  *       overwritten.  Either may be NULL to skip it.
- * All buffers are read and written on `stream`.  The contractions are fp32
- * GEMMs (rocBLAS, on `stream`); the convolution's unrolled patches, its
- * gradient rows and the partial products of dW's contraction (split into at
- * most 64 chunks of output pixels, at most 2^24 floats in all) live in a
- * layer-owned scratch buffer (conv: Bv (P + Q) floats plus the partials,
- * Bv = n H_out W_out; FC: B P floats for dW) that grows on demand
- * (RXNN_ENOMEM when it cannot).  x_max enters the kernels rounded to fp32.  Calls on one layer that overlap on
- * different streams race on that buffer.  RXNN_EINVAL for bad arguments or a
+ * All buffers are read and written on `stream`.  The two contractions run as
+ * implicit GEMMs on the fp32 matrix cores: dW's gathers the clipped input
+ * patches and the output gradient tile by tile, dX's gathers the output
+ * gradient per kernel tap, so no unrolled patch matrix is formed.  An FC layer
+ * runs as the 1 x 1 convolution of B images of 1 x 1 pixels.  When dW's
+ * contraction over the Bv = n H_out W_out output pixels is split across
+ * workgroups (at most 64 ranges, at most 2^24 floats of partial products), the
+ * partials live in a layer-owned scratch buffer that grows on demand
+ * (RXNN_ENOMEM when it cannot); calls on one layer that overlap on different
+ * streams race on it.  Both sums are taken in fp32 in an order that differs
+ * from a sequential one.  x_max enters the kernels rounded to fp32.
+ * RXNN_EUNSUPPORTED when a pixel count, P, kh kw Q or an image's c_in H W
+ * reaches 2^31 - 64, or a gradient has 2^24 tiles of 64 x 64 or more.
+ * RXNN_EINVAL for bad arguments or a
  * convolution that does not match the layer; B = 0 or Bv = 0, or dX and dW
  * both NULL, is a no-op.
  */
@@ -345,8 +351,9 @@ void rxnn_free_layer(rxnn_layer* layer);
  * build by the row sweep), "dac" (DAC of the inputs), "ktab" (patch-column
  * table), "xbar_vmm" (evaluation), "fill" (clearing of a new evaluation
  * workspace), "finish" (workspace of the shared tiles to Y, which also
- * leaves the workspace zeroed), "bw_gemm" (the backward pass's GEMMs) and
- * "bw_aux" (its masks, unrolling and gathers).  rxnn_profile_read synchronises, folds pending events
+ * leaves the workspace zeroed), "bw_dw", "bw_dx" (the backward pass's
+ * contractions) and "bw_reduce" (the sum of dW's split partial products,
+ * which counts 4 bytes per partial read, W read and dW written).  rxnn_profile_read synchronises, folds pending events
  * into the totals and returns total milliseconds and launch count.
  * rxnn_profile_bytes returns, for the same timed launches, the sum of their
  * algorithmic HBM bytes where the library counts them ("dac": 4 bytes per

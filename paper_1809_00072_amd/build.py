@@ -29,8 +29,8 @@ HIPCC_FLAGS = [
 ]
 
 
-# rocBLAS serves the fp32 GEMMs of the re-training backward pass
-LIBS = ["-L/opt/rocm/lib", "-lrocblas"]
+# the library links the HIP runtime only
+LIBS = []
 
 
 def sources():

@@ -1004,6 +1004,52 @@ float dac_range(const rxnn_periph_params* pp) {
   return pp->dac_bits ? (float)pp->x_max : __builtin_huge_valf();
 }
 
+// dX and dW of a convolution whose shape has been checked against the layer.
+rxnn_status bw_run(rxnn_layer* L, const rxnn_periph_params* periph, const rxnn_conv_desc& cd,
+                   const float* W, const float* X, const float* dY, float* dX, float* dW,
+                   hipStream_t s) {
+  const int64_t ho = (cd.h + 2 * cd.pad - cd.kh) / cd.stride + 1;
+  const int64_t wo = (cd.w + 2 * cd.pad - cd.kw) / cd.stride + 1;
+  const int64_t Bv = (int64_t)cd.n * ho * wo, npix = (int64_t)cd.n * cd.h * cd.w;
+  const int64_t P = L->ms.P, Q = L->ms.Q, khw = (int64_t)cd.kh * cd.kw;
+  // the kernels index pixels, patch columns, the (tap, output) reduction and
+  // an image's input planes with 32-bit integers, and launch one workgroup of
+  // 256 threads per 64 x 64 tile
+  const int64_t kLim = INT32_MAX - 64;
+  const int64_t dx_tiles = ((npix + 63) / 64) * ((cd.c_in + 63) / 64);
+  const int64_t dw_tiles = ((P + 63) / 64) * ((Q + 63) / 64);
+  if (Bv > kLim || npix > kLim || P > kLim || khw * Q > kLim ||
+      (int64_t)cd.c_in * cd.h * cd.w > kLim || dx_tiles >= ((int64_t)1 << 24) ||
+      dw_tiles >= ((int64_t)1 << 24))
+    return fail(RXNN_EUNSUPPORTED, "layer too large for the backward pass");
+  if (Bv == 0 || (!dX && !dW)) return RXNN_OK;
+  DeviceGuard dg(L->device);
+  if (!dg.ok) return fail(RXNN_EHIP, "cannot select the layer's device");
+  const float xr = dac_range(periph);
+  if (dW) {
+    const bool vec_ok = ((uintptr_t)X | (uintptr_t)dY | (uintptr_t)W) % 16 == 0;
+    const BwPlan plan = bw_plan(cd, (int)P, (int)Q, vec_ok);
+    if (plan.nsplit == 1) {
+      ProfScope t("bw_dw", s);
+      HIP_TRY(launch_bw_dw(cd, (int)P, (int)Q, xr, X, dY, W, L->ms, plan, dW, s));
+    } else {
+      rxnn_status st = grow_bw(L, (size_t)plan.nsplit * P * Q * sizeof(float));
+      if (st) return st;
+      {
+        ProfScope t("bw_dw", s);
+        HIP_TRY(launch_bw_dw(cd, (int)P, (int)Q, xr, X, dY, W, L->ms, plan, L->bw_ws, s));
+      }
+      ProfScope t("bw_reduce", s, (double)(plan.nsplit + 2) * P * Q * sizeof(float));
+      HIP_TRY(launch_bw_reduce_w(L->bw_ws, plan.nsplit, W, P * Q, L->ms, dW, s));
+    }
+  }
+  if (dX) {
+    ProfScope t("bw_dx", s);
+    HIP_TRY(launch_bw_dx(cd, (int)P, (int)Q, xr, X, dY, W, dX, s));
+  }
+  return RXNN_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -1018,38 +1064,18 @@ rxnn_status rxnn_fc_backward(const rxnn_layer* layer, const rxnn_periph_params* 
   if (st) return st;
   if (B < 0) return fail(RXNN_EINVAL, "B must be >= 0");
   if (!W || !X || !dY) return fail(RXNN_EINVAL, "W, X and dY must not be NULL");
-  const int64_t P = L->ms.P, Q = L->ms.Q;
-  if (B > INT32_MAX || P * B > ((int64_t)1 << 40))
+  if (B > INT32_MAX || L->ms.P > INT32_MAX || L->ms.Q > INT32_MAX)
     return fail(RXNN_EUNSUPPORTED, "B too large for the backward pass");
-  if (B == 0 || (!dX && !dW)) return RXNN_OK;
-  DeviceGuard dg(L->device);
-  if (!dg.ok) return fail(RXNN_EHIP, "cannot select the layer's device");
-  hipStream_t s = (hipStream_t)stream;
-  const float xr = dac_range(periph);
-  if (dX) {
-    ProfScope t("bw_gemm", s);
-    HIP_TRY(bw_gemm(L->device, s, false, true, (int)B, (int)P, (int)Q, dY, (int)Q, W, (int)Q, dX,
-                    (int)P));
-  }
-  if (dX) {
-    ProfScope t("bw_aux", s);
-    HIP_TRY(launch_bw_mask_x(dX, X, B * P, xr, s));
-  }
-  if (dW) {
-    if ((st = grow_bw(L, (size_t)B * P * sizeof(float)))) return st;
-    {
-      ProfScope t("bw_aux", s);
-      HIP_TRY(launch_bw_clip(X, B * P, xr, L->bw_ws, s));
-    }
-    {
-      ProfScope t("bw_gemm", s);
-      HIP_TRY(bw_gemm(L->device, s, true, false, (int)P, (int)Q, (int)B, L->bw_ws, (int)P, dY,
-                      (int)Q, dW, (int)Q));
-    }
-    ProfScope t("bw_aux", s);
-    HIP_TRY(launch_bw_mask_w(dW, W, P * Q, L->ms, s));
-  }
-  return RXNN_OK;
+  // the layer as the 1 x 1 convolution of B images of 1 x 1 pixels
+  rxnn_conv_desc cd;
+  cd.n = (int32_t)B;
+  cd.c_in = (int32_t)L->ms.P;
+  cd.h = cd.w = 1;
+  cd.c_out = (int32_t)L->ms.Q;
+  cd.kh = cd.kw = 1;
+  cd.stride = 1;
+  cd.pad = 0;
+  return bw_run(L, periph, cd, W, X, dY, dX, dW, (hipStream_t)stream);
 }
 
 rxnn_status rxnn_conv_backward(const rxnn_layer* layer, const rxnn_periph_params* periph,
@@ -1062,71 +1088,7 @@ rxnn_status rxnn_conv_backward(const rxnn_layer* layer, const rxnn_periph_params
   if (st) return st;
   if ((st = check_conv(L->ms, conv))) return st;
   if (!W || !X || !dY) return fail(RXNN_EINVAL, "W, X and dY must not be NULL");
-  const rxnn_conv_desc cd = *conv;
-  const int ho = (cd.h + 2 * cd.pad - cd.kh) / cd.stride + 1;
-  const int wo = (cd.w + 2 * cd.pad - cd.kw) / cd.stride + 1;
-  const int64_t Bv = (int64_t)cd.n * ho * wo, P = L->ms.P, Q = L->ms.Q;
-  // the unrolling and gather kernels index output pixels and image planes with
-  // 32-bit integers and put patch columns and images on grid dimensions y, z
-  if (Bv > INT32_MAX || (int64_t)cd.h * cd.w > INT32_MAX || P > 65535 || cd.n > 65535)
-    return fail(RXNN_EUNSUPPORTED, "convolution too large for the backward pass");
-  if (Bv == 0 || (!dX && !dW)) return RXNN_OK;
-  DeviceGuard dg(L->device);
-  if (!dg.ok) return fail(RXNN_EHIP, "cannot select the layer's device");
-  hipStream_t s = (hipStream_t)stream;
-  const float xr = dac_range(periph);
-  // scratch: the patches k-major (P x Bv: the clipped patches, then their
-  // gradients), the output gradient as rows (Bv x Q) and, for a long
-  // contraction over the output pixels, dW's split-K partial products
-  const int64_t PQ = P * Q;
-  int64_t S = 1;
-  if (dW) S = std::max<int64_t>(1, std::min<int64_t>({64, Bv / 1024, ((int64_t)16 << 20) / PQ}));
-  const int64_t Kc = Bv / S, tail = Bv - S * Kc;
-  const int64_t nparts = S > 1 ? S + (tail ? 1 : 0) : 0;
-  if ((st = grow_bw(L, (size_t)(Bv * (P + Q) + nparts * PQ) * sizeof(float)))) return st;
-  float* colsT = L->bw_ws;
-  float* rows = colsT + Bv * P;
-  float* part = rows + Bv * Q;
-  {
-    ProfScope t("bw_aux", s);
-    HIP_TRY(launch_bw_rows(dY, Bv, (int)Q, ho * wo, rows, s));
-  }
-  if (dW) {
-    {
-      ProfScope t("bw_aux", s);
-      HIP_TRY(launch_bw_im2col(X, cd, ho, wo, xr, colsT, s));
-    }
-    if (S == 1) {
-      {
-        ProfScope t("bw_gemm", s);
-        HIP_TRY(bw_gemm(L->device, s, false, false, (int)P, (int)Q, (int)Bv, colsT, (int)Bv, rows,
-                        (int)Q, dW, (int)Q));
-      }
-      ProfScope t("bw_aux", s);
-      HIP_TRY(launch_bw_mask_w(dW, W, PQ, L->ms, s));
-    } else {
-      {
-        ProfScope t("bw_gemm", s);
-        HIP_TRY(bw_gemm_batched(L->device, s, false, false, (int)P, (int)Q, (int)Kc, colsT,
-                                (int)Bv, Kc, rows, (int)Q, Kc * Q, part, (int)Q, PQ, (int)S));
-        if (tail)
-          HIP_TRY(bw_gemm(L->device, s, false, false, (int)P, (int)Q, (int)tail, colsT + S * Kc,
-                          (int)Bv, rows + S * Kc * Q, (int)Q, part + S * PQ, (int)Q));
-      }
-      ProfScope t("bw_aux", s);
-      HIP_TRY(launch_bw_reduce_w(part, (int)nparts, W, PQ, L->ms, dW, s));
-    }
-  }
-  if (dX) {
-    {
-      ProfScope t("bw_gemm", s);
-      HIP_TRY(bw_gemm(L->device, s, false, true, (int)P, (int)Bv, (int)Q, W, (int)Q, rows,
-                      (int)Q, colsT, (int)Bv));
-    }
-    ProfScope t("bw_aux", s);
-    HIP_TRY(launch_bw_col2im(colsT, X, cd, ho, wo, xr, dX, s));
-  }
-  return RXNN_OK;
+  return bw_run(L, periph, *conv, W, X, dY, dX, dW, (hipStream_t)stream);
 }
 
 }  // extern "C"

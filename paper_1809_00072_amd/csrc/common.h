@@ -178,23 +178,24 @@ VmmPlan vmm_plan(const MapScalars& ms, const PeriphScalars& ps, int64_t Bv, bool
 // row loads of every array: gload[arr][m] = sum over columns of G'[arr][m][.]
 hipError_t launch_gload(const MapScalars& ms, const float* gpt, float* gload, hipStream_t s);
 
-// backward pass of re-training (backward.hip)
-hipError_t bw_gemm(int device, hipStream_t s, bool ta, bool tb, int m, int n, int k,
-                   const float* A, int lda, const float* B, int ldb, float* C, int ldc);
-hipError_t bw_gemm_batched(int device, hipStream_t s, bool ta, bool tb, int m, int n, int k,
-                           const float* A, int lda, int64_t sA, const float* B, int ldb,
-                           int64_t sB, float* C, int ldc, int64_t sC, int batch);
+// backward pass of re-training (backward.hip): implicit-GEMM kernels on the
+// fp32 matrix cores; a fully connected layer is the 1 x 1 convolution of
+// B images of 1 x 1 pixels.  dW's contraction over the output pixels is split
+// into `nsplit` ranges (of `kc` pixels for the generic kernel; kc = 0 selects
+// the 3 x 3 kernel, which splits whole 64-pixel chunks); with nsplit > 1 the
+// partial products (nsplit P Q floats) are summed and masked by
+// launch_bw_reduce_w.  vec_ok: X, dY and W are 16-byte aligned.
+struct BwPlan {
+  int nsplit, kc;
+};
+BwPlan bw_plan(const rxnn_conv_desc& cd, int P, int Q, bool vec_ok);
+hipError_t launch_bw_dw(const rxnn_conv_desc& cd, int P, int Q, float x_max, const float* X,
+                        const float* dY, const float* W, const MapScalars& ms, const BwPlan& plan,
+                        float* out, hipStream_t s);
+hipError_t launch_bw_dx(const rxnn_conv_desc& cd, int P, int Q, float x_max, const float* X,
+                        const float* dY, const float* W, float* dX, hipStream_t s);
 hipError_t launch_bw_reduce_w(const float* part, int nparts, const float* W, int64_t n,
                               const MapScalars& ms, float* dW, hipStream_t s);
-hipError_t launch_bw_clip(const float* X, int64_t n, float x_max, float* out, hipStream_t s);
-hipError_t launch_bw_mask_x(float* dX, const float* X, int64_t n, float x_max, hipStream_t s);
-hipError_t launch_bw_mask_w(float* dW, const float* W, int64_t n, const MapScalars& ms,
-                            hipStream_t s);
-hipError_t launch_bw_im2col(const float* X, const rxnn_conv_desc& cd, int ho, int wo,
-                            float x_max, float* cols, hipStream_t s);
-hipError_t launch_bw_rows(const float* dY, int64_t Bv, int Q, int hw, float* rows, hipStream_t s);
-hipError_t launch_bw_col2im(const float* dcols, const float* X, const rxnn_conv_desc& cd, int ho,
-                            int wo, float x_max, float* dX, hipStream_t s);
 
 // ---- kernel timing (api.hip) ------------------------------------------------
 // `bytes`: the launch's algorithmic HBM bytes, summed per kernel name for the

@@ -161,6 +161,12 @@ def conv_dict(n, c_in, hw, c_out, k, s, p, w=None):
     (conv_dict(3, 5, 10, 7, 3, 2, 0, w=13), 4, 0.0),    # non-square, no padding
     (conv_dict(4, 64, 28, 64, 3, 1, 1), 6, 0.1),        # several tiles, weight mask
     (conv_dict(2, 128, 14, 256, 3, 2, 1), 8, 0.0),
+    (conv_dict(2, 20, 15, 70, 3, 1, 2), 4, 0.0),        # 3x3, odd widths: generic kernels
+    (conv_dict(1, 4, 5, 3, 3, 1, 0, w=80), 0, 0.0),     # 3x3 rows wider than a chunk
+    (conv_dict(3, 17, 7, 33, 3, 2, 1), 6, 0.0),         # 3x3 / 2 on 7 x 7 images
+    (conv_dict(2, 20, 12, 68, 3, 1, 1), 4, 0.0),        # 3x3 halo kernels: ragged c_in, Q
+    (conv_dict(2, 17, 16, 33, 3, 2, 1), 6, 0.1),        # 3x3 / 2 halo dW, weight mask
+    (conv_dict(1, 8, 8, 12, 3, 1, 1, w=60), 0, 0.0),    # 3x3 halo, ideal DAC, 60-wide rows
 ])
 def test_conv_backward_parity(conv, dac, w_max):
     label = "conv_backward %s dac=%d w_max=%g" % (conv, dac, w_max)
