@@ -357,10 +357,11 @@ struct Halo {
 };
 
 constexpr int YS = 68;       // dW: LDS row of the output gradient (64 pixels + 4)
-constexpr int DW_X4 = 10;    // dW: X halo vectors per thread (n4 <= 2560)
+constexpr int DW_X4 = 6;     // dW: X halo vectors per thread (n4 <= 1536)
 constexpr int QC = 8;        // dX: outputs per staged chunk
 constexpr int WSTR = 12;     // dX: LDS row of W (QC + 4)
 constexpr int WTAP = 64 * WSTR;
+constexpr int DX_PIX = 128;  // dX: input pixels per workgroup
 constexpr int DX_Y4 = 4;     // dX: dY halo vectors per thread (n4 <= 1024)
 constexpr int DX_W4 = 9 * 64 * QC / 4 / NTH + 1;   // W vectors per thread (1152 in all)
 
@@ -509,11 +510,12 @@ __global__ __launch_bounds__(NTH) void k_bw_dw3(BwGeom gm, Halo hl, const float*
   }
 }
 
-// dX tile of a stride-1 3 x 3 convolution: 64 input pixels of one image x 64
+// dX tile of a stride-1 3 x 3 convolution: 128 input pixels of one image x 64
 // channels, reduction over (tap, output q) with the output gradient staged QC
-// outputs at a time.  Wave v takes pixels 16 v .. 16 v + 15; lane (c, j)
-// supplies pixel 16 v + c and output 4 s + j of step s, and channel
-// 16 b + c of block b.  Needs w, W_out and Q divisible by 4.
+// outputs at a time.  Wave v takes pixels 32 v .. 32 v + 31 in two blocks of
+// 16; lane (c, j) supplies pixel 32 v + 16 a + c of block a and output 4 s + j
+// of step s, and channel 16 b + c of block b.  Needs w, W_out and Q divisible
+// by 4.
 __global__ __launch_bounds__(NTH) void k_bw_dx3(BwGeom gm, Halo hl, const float* __restrict__ X,
                                                 const float* __restrict__ dY,
                                                 const float* __restrict__ W,
@@ -527,17 +529,21 @@ __global__ __launch_bounds__(NTH) void k_bw_dx3(BwGeom gm, Halo hl, const float*
   const int lin = xcd_tile((int)blockIdx.x, (int)gridDim.x);
   const int unit = lin / hl.ncb, ci0 = (lin - unit * hl.ncb) * 64;
   const int img = (int)div_by((uint32_t)unit, hl.fd_upi);
-  const int p0 = (unit - img * hl.upi) * 64;
-  const int len = min(64, gm.hw_in - p0);
+  const int p0 = (unit - img * hl.upi) * DX_PIX;
+  const int len = min(DX_PIX, gm.hw_in - p0);
   const int y_first = (int)div_by((uint32_t)p0, gm.fd_w);
   const int HS = hl.HS;
   const int oy0 = y_first + gm.pad - 2;
   const int wo4 = gm.wo >> 2;
   for (int e = tid; e < QC * hl.CS; e += NTH) Ys[e] = 0.0f;   // border columns
-  // this lane's pixel (clamped into the chunk; rows past it are not stored)
-  const int pp = p0 + min(16 * wave + c, len - 1);
-  const int py = (int)div_by((uint32_t)pp, gm.fd_w);
-  const int abase = j * hl.CS + (py - y_first) * HS + (pp - py * gm.w) + gm.pad + 4;
+  // this lane's two pixels (clamped into the chunk; rows past it are not stored)
+  int abase[2];
+#pragma unroll
+  for (int a = 0; a < 2; ++a) {
+    const int pp = p0 + min(32 * wave + 16 * a + c, len - 1);
+    const int py = (int)div_by((uint32_t)pp, gm.fd_w);
+    abase[a] = j * hl.CS + (py - y_first) * HS + (pp - py * gm.w) + gm.pad + 4;
+  }
   const float* ysrc = dY + (int64_t)img * gm.Q * gm.hw_out;
   // W rows (channel, tap) r = f / 2 of the block's 9 x 64, outputs 4 (f % 2) ..
   const int wrows = 9 * min(64, gm.c_in - ci0);
@@ -582,9 +588,11 @@ __global__ __launch_bounds__(NTH) void k_bw_dx3(BwGeom gm, Halo hl, const float*
       }
     }
   };
-  f32x4 acc[4];
+  f32x4 acc[2][4];
 #pragma unroll
-  for (int b = 0; b < 4; ++b) acc[b] = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int a = 0; a < 2; ++a)
+#pragma unroll
+    for (int b = 0; b < 4; ++b) acc[a][b] = f32x4{0.f, 0.f, 0.f, 0.f};
   fetch(0);
 #pragma unroll 1
   for (int qc0 = 0; qc0 < gm.Q; qc0 += QC) {
@@ -596,40 +604,49 @@ __global__ __launch_bounds__(NTH) void k_bw_dx3(BwGeom gm, Halo hl, const float*
     for (int ky = 0; ky < 3; ++ky)
 #pragma unroll
       for (int kx = 0; kx < 3; ++kx) {
-        const int ar = abase + (2 - ky) * HS - kx;
+        const int toff = (2 - ky) * HS - kx;
         const float* wt = Ws + (ky * 3 + kx) * WTAP + c * WSTR + j;
 #pragma unroll
         for (int k4 = 0; k4 < QC / 4; ++k4) {
-          const float a = Ys[ar + 4 * k4 * hl.CS];
+          float av[2], bv[4];
 #pragma unroll
-          for (int b = 0; b < 4; ++b)
-            acc[b] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, wt[16 * b * WSTR + 4 * k4], acc[b],
-                                                          0, 0, 0);
+          for (int a = 0; a < 2; ++a) av[a] = Ys[abase[a] + toff + 4 * k4 * hl.CS];
+#pragma unroll
+          for (int b = 0; b < 4; ++b) bv[b] = wt[16 * b * WSTR + 4 * k4];
+#pragma unroll
+          for (int a = 0; a < 2; ++a)
+#pragma unroll
+            for (int b = 0; b < 4; ++b)
+              acc[a][b] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[a], bv[b], acc[a][b], 0, 0, 0);
         }
       }
   }
-  // element v of lane (c, j) in block b: pixel 16 wave + 4 j + v, channel 16 b + c
-  const int pl = 16 * wave + 4 * j;
-  if (pl >= len) return;
+  // element v of lane (c, j) in blocks (a, b): pixel 32 wave + 16 a + 4 j + v,
+  // channel 16 b + c
 #pragma unroll
-  for (int b = 0; b < 4; ++b) {
-    const int ci = ci0 + 16 * b + c;
-    if (ci >= gm.c_in) continue;
-    const int64_t e = ((int64_t)img * gm.c_in + ci) * gm.hw_in + p0 + pl;
-    const float4 xv = *reinterpret_cast<const float4*>(X + e);
-    float4 o;
-    o.x = (xv.x >= 0.0f && xv.x <= gm.x_max) ? acc[b][0] : 0.0f;
-    o.y = (xv.y >= 0.0f && xv.y <= gm.x_max) ? acc[b][1] : 0.0f;
-    o.z = (xv.z >= 0.0f && xv.z <= gm.x_max) ? acc[b][2] : 0.0f;
-    o.w = (xv.w >= 0.0f && xv.w <= gm.x_max) ? acc[b][3] : 0.0f;
-    *reinterpret_cast<float4*>(dX + e) = o;
+  for (int a = 0; a < 2; ++a) {
+    const int pl = 32 * wave + 16 * a + 4 * j;
+    if (pl >= len) continue;
+#pragma unroll
+    for (int b = 0; b < 4; ++b) {
+      const int ci = ci0 + 16 * b + c;
+      if (ci >= gm.c_in) continue;
+      const int64_t e = ((int64_t)img * gm.c_in + ci) * gm.hw_in + p0 + pl;
+      const float4 xv = *reinterpret_cast<const float4*>(X + e);
+      float4 o;
+      o.x = (xv.x >= 0.0f && xv.x <= gm.x_max) ? acc[a][b][0] : 0.0f;
+      o.y = (xv.y >= 0.0f && xv.y <= gm.x_max) ? acc[a][b][1] : 0.0f;
+      o.z = (xv.z >= 0.0f && xv.z <= gm.x_max) ? acc[a][b][2] : 0.0f;
+      o.w = (xv.w >= 0.0f && xv.w <= gm.x_max) ? acc[a][b][3] : 0.0f;
+      *reinterpret_cast<float4*>(dX + e) = o;
+    }
   }
 }
 
 // 3 x 3 plans.  dW: a chunk of 64 output pixels spans `span` output rows and
 // (span - 1) stride + 3 input rows; the channel stride is 4 mod 8 words so
 // that the 16 channels of a read fall in distinct LDS banks.  dX (stride 1):
-// 64 input pixels read span + 2 output-gradient rows; the per-output stride
+// 128 input pixels read span + 2 output-gradient rows; the per-output stride
 // is 16 mod 64 words so that the 4 outputs of a read fall 16 banks apart.
 // Rows move as 16-byte vectors: the widths (and dX's Q) must be multiples of
 // 4.  lds = 0: the shape is served by the generic kernels.
@@ -680,7 +697,7 @@ HaloPlan dx3_plan(const rxnn_conv_desc& cd, int P, int Q) {
   if (cd.kh != 3 || cd.kw != 3 || cd.stride != 1) return r;
   const BwGeom g = bw_geom(cd, P, Q, 0.0f);
   if (g.w % 4 || g.wo % 4 || Q % 4) return r;
-  const int span = std::min(g.h, (63 + g.w - 1) / g.w + 1);
+  const int span = std::min(g.h, (DX_PIX - 1 + g.w - 1) / g.w + 1);
   r.h.HS = round4(std::max(g.w + g.pad + 4, g.wo + 4));
   r.h.HR = span + 2;
   int cs = r.h.HR * r.h.HS;
@@ -689,7 +706,7 @@ HaloPlan dx3_plan(const rxnn_conv_desc& cd, int P, int Q) {
   r.h.n4 = QC * r.h.HR * (g.wo / 4);
   if (r.h.n4 > DX_Y4 * NTH) return r;
   const size_t lds = ((size_t)QC * cs + 9 * WTAP) * sizeof(float);
-  r.h.upi = (g.hw_in + 63) / 64;
+  r.h.upi = (g.hw_in + DX_PIX - 1) / DX_PIX;
   const int64_t units = (int64_t)g.n * r.h.upi;
   r.h.ncb = (g.c_in + 63) / 64;
   if (lds > kHaloLds || units * r.h.ncb >= ((int64_t)1 << 24)) return r;
