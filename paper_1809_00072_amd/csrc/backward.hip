@@ -427,7 +427,9 @@ __global__ __launch_bounds__(NTH) void k_bw_dw3(BwGeom gm, Halo hl, const float*
       const int img = (int)div_by((uint32_t)u, hl.fd_upi);
       const int p0 = (u - img * hl.upi) * 64;
       const int len = min(64, gm.hw_out - p0);
-      int po = 0;
+      // pixels past the chunk read LDS columns 0 .. 2, which are never written
+      // (image columns start at 4) and stay zero: their steps add exactly 0
+      int po = gm.pad - 4;
       if (tid < len) {
         const int oy_first = (int)div_by((uint32_t)p0, gm.fd_wo);
         const int pix = p0 + tid;
@@ -478,18 +480,14 @@ __global__ __launch_bounds__(NTH) void k_bw_dw3(BwGeom gm, Halo hl, const float*
               __builtin_amdgcn_mfma_f32_16x16x4f32(Xs[ar + kx], b, acc[ky * 3 + kx], 0, 0, 0);
       }
     };
-    // len is a multiple of 4: every step is whole
+    // groups of four steps; pixels past the chunk contribute zeros
 #pragma unroll 1
     for (int g = 0; g < len; g += 16) {
-      if (g + 16 <= len) {
-        int po[4];
+      int po[4];
 #pragma unroll
-        for (int k = 0; k < 4; ++k) po[k] = pofs[g + 4 * k + j];
+      for (int k = 0; k < 4; ++k) po[k] = pofs[g + 4 * k + j];
 #pragma unroll
-        for (int k = 0; k < 4; ++k) step((g >> 2) + k, po[k]);
-      } else {
-        for (int k4 = g >> 2; 4 * k4 < len; ++k4) step(k4, pofs[4 * k4 + j]);
-      }
+      for (int k = 0; k < 4; ++k) step((g >> 2) + k, po[k]);
     }
   }
   float wmax = 0.0f;
