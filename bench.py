@@ -54,7 +54,7 @@ FP32_MFMA_PEAK_TFLOPS = 157.3   # MI355X dense fp32 matrix
 # FETCH_SIZE / WRITE_SIZE counters of this kernel version, each scaled by what
 # the counter reads for a plain 2 GiB copy (fetch x 2.000, write x 1.000);
 # the summary and its commands are in the repository's profiles folder
-VMM_TRAFFIC_BYTES = 2.0 * 15384 * 1024 + 40314 * 1024
+VMM_TRAFFIC_BYTES = 2.0 * 15182.7 * 1024 + 39424 * 1024
 # HBM bytes of k_xbar_vmm per evaluation-only pass of a stacked workload
 # (summed over its layers), from the same counters and the same calibration
 # (fetch x 2.000, write x 1.000 from a plain 2 GiB copy in the same run), keyed
