@@ -825,7 +825,46 @@ struct MfmaTile {
   // tile-local coordinates of this lane's element v of block (i, j)
   __device__ __forceinline__ int row(int i, int v) const { return wr * 32 + i * 16 + lr + 4 * v; }
   __device__ __forceinline__ int col(int j) const { return wc * 32 + j * 16 + lc; }
+  // Writes the transpose of the tile's values val (this lane's 16) to
+  // out[(y0 + y) * ld + x0 + x] for x0 + x < xlim, y0 + y < ylim, through
+  // `t` (at least 32 x TT doubles of LDS, free on entry; every thread of
+  // the workgroup calls this), half the rows per pass so that each store
+  // writes 32 consecutive doubles of a row.
+  __device__ __forceinline__ void store_transposed(const double (&val)[2][2][4], double* t,
+                                                   double* out, int64_t ld, int x0, int y0,
+                                                   int xlim, int ylim, int tid) const {
+    constexpr int TT = 65;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      __syncthreads();
+      if (wr == h) {
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+          for (int j = 0; j < 2; ++j)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) t[(i * 16 + lr + 4 * v) * TT + col(j)] = val[i][j][v];
+      }
+      __syncthreads();
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        const int e = tid + 256 * k, y = e >> 5, xl = e & 31;
+        const int x = x0 + 32 * h + xl;
+        if (x < xlim && y0 + y < ylim) out[(int64_t)(y0 + y) * ld + x] = t[xl * TT + y];
+      }
+    }
+  }
 };
+
+// Tile (tx, ty), tx >= ty, of the lower triangle of an nt x nt tile grid from
+// its index tt in row-major order of that triangle.
+__device__ __forceinline__ void tri_tile(int tt, int* tx, int* ty) {
+  int x = (int)((sqrtf(8.0f * (float)tt + 1.0f) - 1.0f) * 0.5f);
+  while ((x + 1) * (x + 2) / 2 <= tt) ++x;
+  while (x * (x + 1) / 2 > tt) --x;
+  *tx = x;
+  *ty = tt - x * (x + 1) / 2;
+}
 
 // MODE 0: a merge (children through the port tables); 1: the final step;
 // 2: a stage of a dense combined matrix (its first C rows are the pivots,
@@ -1310,18 +1349,29 @@ __global__ __launch_bounds__(256) void k_nd_dense0(NdArgs na) {
 // of the stage's pivots, OUT 0 writes A[64 + x][64 + y] - (Z^T Z)[x][y] for
 // x, y < E to dB (row stride dldo); OUT 1 writes G' = (Z^T Z - A) over the
 // sink x source block (A: [sources (M) | sinks (T)] after the pivots).
+// OUT 0 is symmetric: a workgroup computes one tile of the lower triangle
+// (tx >= ty) and writes it and its mirror image.
 template <int OUT>
 __global__ __launch_bounds__(256) void k_nd_dschur(NdArgs na) {
-  __shared__ __attribute__((aligned(16))) double za[KC64 * KLD];
-  __shared__ __attribute__((aligned(16))) double zb[KC64 * KLD];
+  __shared__ __attribute__((aligned(16))) double zab[2 * KC64 * KLD];
+  double* za = zab;
+  double* zb = zab + KC64 * KLD;
   const int tid = threadIdx.x;
   const int E = na.dn - 64;
   const int M = na.ms.M;
   const int nrx = OUT == 0 ? E : na.ms.Np, nry = OUT == 0 ? E : na.ms.Mp;
   const int ntx = (nrx + 63) / 64, nty = (nry + 63) / 64;
-  const int64_t la = blockIdx.x / (ntx * nty);
-  const int tt = (int)(blockIdx.x % (ntx * nty));
-  const int x0 = (tt / nty) * 64, y0 = (tt % nty) * 64;
+  const int ntiles = OUT == 0 ? ntx * (ntx + 1) / 2 : ntx * nty;
+  const int64_t la = blockIdx.x / ntiles;
+  const int tt = (int)(blockIdx.x % ntiles);
+  int tx, ty;
+  if (OUT == 0) {
+    tri_tile(tt, &tx, &ty);
+  } else {
+    tx = tt / nty;
+    ty = tt % nty;
+  }
+  const int x0 = tx * 64, y0 = ty * 64;
   // rows of Z and of A behind this tile's x and y
   const int zx0 = OUT == 0 ? x0 : M + x0, zy0 = y0;
   const int lx = OUT == 0 ? E : min(na.ms.N, na.T), ly = OUT == 0 ? E : M;   // valid x, y
@@ -1343,6 +1393,7 @@ __global__ __launch_bounds__(256) void k_nd_dschur(NdArgs na) {
   }
   if constexpr (OUT == 0) {
     double* B = na.dB + la * na.out_stride;
+    double val[2][2][4];
 #pragma unroll
     for (int i = 0; i < 2; ++i)
 #pragma unroll
@@ -1350,9 +1401,11 @@ __global__ __launch_bounds__(256) void k_nd_dschur(NdArgs na) {
 #pragma unroll
         for (int v = 0; v < 4; ++v) {
           const int x = x0 + mt.row(i, v), y = y0 + mt.col(j);
-          if (x < E && y < E)
-            B[(int64_t)x * na.dldo + y] = A[(int64_t)(64 + x) * na.dld + 64 + y] - mt.acc[i][j][v];
+          const bool in = x < E && y < E;
+          val[i][j][v] = in ? A[(int64_t)(64 + x) * na.dld + 64 + y] - mt.acc[i][j][v] : 0.0;
+          if (in) B[(int64_t)x * na.dldo + y] = val[i][j][v];
         }
+    if (tx != ty) mt.store_transposed(val, zab, B, na.dldo, x0, y0, E, E, tid);
   } else {
     const int Np = na.ms.Np, Mp = na.ms.Mp, N = na.ms.N;
     float* out = nd_ref(na, la).out;
@@ -1372,22 +1425,26 @@ __global__ __launch_bounds__(256) void k_nd_dschur(NdArgs na) {
   }
 }
 
-// ext = V - Z^T Z on one 64 x 64 tile of one merge (V: the children's
-// external-external entries).
+// ext = V - Z^T Z of one merge (V: the children's external-external
+// entries).  ext is symmetric, so a workgroup computes one 64 x 64 tile of
+// the lower triangle (tx >= ty) and writes it and its mirror image.
 // Five waves per SIMD (96 VGPRs): its gathers need many waves in flight.
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(5))) void k_nd_schur(NdArgs na) {
   __shared__ short invt[2][MAXSLOT2];
-  __shared__ __attribute__((aligned(16))) double za[KC64 * KLD];
-  __shared__ __attribute__((aligned(16))) double zb[KC64 * KLD];
+  __shared__ __attribute__((aligned(16))) double zab[2 * KC64 * KLD];
+  double* za = zab;
+  double* zb = zab + KC64 * KLD;
   const int tid = threadIdx.x;
   const int nh = na.vert ? 2 * na.h : na.h, nw = na.vert ? na.w : 2 * na.w;
   const int Emax = 2 * (nh + nw);
   const int nt = (Emax + 63) / 64;
-  const int64_t blk = blockIdx.x / (nt * nt);
+  const int ntri = nt * (nt + 1) / 2;
+  const int64_t blk = blockIdx.x / ntri;
   const MergeGeom g = merge_geom(na, blk);
   const int c = g.c, E = g.E;
-  const int tt = (int)(blockIdx.x % (nt * nt));
-  const int x0 = (tt / nt) * 64, y0 = (tt % nt) * 64;
+  int tx, ty;
+  tri_tile((int)(blockIdx.x % ntri), &tx, &ty);
+  const int x0 = tx * 64, y0 = ty * 64;
   const int nrx = min(64, E - x0), nry = min(64, E - y0);
   if (nrx <= 0 || nry <= 0) return;
   inverse_tables<MAXSLOT2>(na, g, invt, 256);
@@ -1434,6 +1491,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(5))) void k
   const unsigned cb = (unsigned)(g.Ein * g.Ein * 8);
   const __amdgpu_buffer_rsrc_t r0 = nd_rsrc(Y0, cb), r1 = nd_rsrc(Y1, cb);
   double* ext = na.buf_out + g.la * na.out_stride + (int64_t)g.m * Emax * Emax;
+  double val[2][2][4];
 #pragma unroll
   for (int j = 0; j < 2; ++j) {
     const int y = y0 + mt.col(j);
@@ -1458,9 +1516,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(5))) void k
 #pragma unroll
       for (int v = 0; v < 4; ++v) {
         const int x = x0 + mt.row(i, v);
-        if (x < E && y < E) ext[x * Emax + y] = vv[i][v] - mt.acc[i][j][v];
+        val[i][j][v] = vv[i][v] - mt.acc[i][j][v];
+        if (x < E && y < E) ext[x * Emax + y] = val[i][j][v];
       }
   }
+  if (tx != ty) mt.store_transposed(val, zab, ext, Emax, x0, y0, E, E, tid);
 }
 
 }  // namespace
@@ -1563,7 +1623,8 @@ static void launch_staged(NdArgs na, int64_t n, int c, int n0, double* a, double
       hipLaunchKernelGGL(k_nd_dschur<1>, dim3((unsigned)n * nt), dim3(256), 0, s, na);
     } else {
       const unsigned nt = (unsigned)((ext + 63) / 64);
-      hipLaunchKernelGGL(k_nd_dschur<0>, dim3((unsigned)n * nt * nt), dim3(256), 0, s, na);
+      hipLaunchKernelGGL(k_nd_dschur<0>, dim3((unsigned)n * (nt * (nt + 1) / 2)), dim3(256), 0, s,
+                         na);
     }
   }
 }
@@ -1639,8 +1700,8 @@ hipError_t launch_nd_build(const MapScalars& ms, const float* W, float* gpt, int
         launch_cut<false>(na, grid, c, c + e_layout, fused, s);
         if (!fused) {
           const int nt = (emax + 63) / 64;
-          hipLaunchKernelGGL(k_nd_schur, dim3((unsigned)(n * nmerge * nt * nt)), dim3(256), 0,
-                             s, na);
+          hipLaunchKernelGGL(k_nd_schur, dim3((unsigned)(n * nmerge * (nt * (nt + 1) / 2))),
+                             dim3(256), 0, s, na);
         }
       } else if (c == C2) {
         const int emax = 2 * (nh + nw);
@@ -1648,8 +1709,8 @@ hipError_t launch_nd_build(const MapScalars& ms, const float* W, float* gpt, int
         hipLaunchKernelGGL((k_nd_cut2<false>), dim3((unsigned)(n * nmerge) * npan), dim3(2 * CP2),
                            0, s, na);
         const int nt = (emax + 63) / 64;
-        hipLaunchKernelGGL(k_nd_schur, dim3((unsigned)(n * nmerge * nt * nt)), dim3(256), 0, s,
-                           na);
+        hipLaunchKernelGGL(k_nd_schur, dim3((unsigned)(n * nmerge * (nt * (nt + 1) / 2))),
+                           dim3(256), 0, s, na);
       } else if (nmerge == 1 && c % 128 == 0 && (int64_t)(c + e_layout) * (c + e_layout) <= si &&
                  c + e_layout <= MAXSLOT2) {
         // the combined matrix in nxt, the stages in nxt / cur (the children
