@@ -1023,11 +1023,15 @@ __global__ __launch_bounds__(512) void k_nd_cut(NdArgs na) {
       const unsigned cbf = (unsigned)(g.Ein * g.Ein * 8);
       const __amdgpu_buffer_rsrc_t r0f = nd_rsrc(Y0, cbf), r1f = nd_rsrc(Y1, cbf);
       const int nt = (E + 63) / 64;
-      // ext = V - Z^T Z on 64 x 64 tiles: the children's entries of a tile
-      // are loaded before its product, so that they arrive during it
+      // ext = V - Z^T Z on the 64 x 64 tiles of its lower triangle (ext is
+      // symmetric: each tile also writes its mirror image); the children's
+      // entries of a tile are loaded before its product, so that they arrive
+      // during it
 #pragma unroll 1
-      for (int tt = 0; tt < nt * nt; ++tt) {
-        const int x0 = (tt / nt) * 64, y0 = (tt % nt) * 64;
+      for (int tt = 0; tt < nt * (nt + 1) / 2; ++tt) {
+        int tx, ty;
+        tri_tile(tt, &tx, &ty);
+        const int x0 = tx * 64, y0 = ty * 64;
         MfmaTile mt;
         mt.init(threadIdx.x);
         double vv[2][2][4];
@@ -1056,7 +1060,12 @@ __global__ __launch_bounds__(512) void k_nd_cut(NdArgs na) {
 #pragma unroll
             for (int v = 0; v < 4; ++v) {
               const int x = x0 + mt.row(i, v), yy = y0 + mt.col(j);
-              if (x < E && yy < E) ext[x * Emax + yy] = vv[i][j][v] - mt.acc[i][j][v];
+              if (x < E && yy < E) {
+                const double e = vv[i][j][v] - mt.acc[i][j][v];
+                ext[x * Emax + yy] = e;
+                // the mirror: lanes lr = 0 .. 3 hold consecutive x
+                if (tx != ty) ext[yy * Emax + x] = e;
+              }
             }
       }
       return;
