@@ -66,6 +66,8 @@ struct NdArgs {
   double* dB;            // stage output (row stride dldo) per array
   int dn, dld, dldo;
   int dpanel;            // external columns per workgroup of the cut kernel
+  int dfull;             // the stage writes both triangles (else only the
+                         // lower tiles, which is all the next stage reads)
   // several layers at once (null tables: the one layer of ms / W / gpt)
   NdBatch batch;
 };
@@ -856,6 +858,14 @@ struct MfmaTile {
   }
 };
 
+// Workgroups are dispatched to the 8 XCDs in turn, each with its own L2: this
+// renumbering gives every XCD a contiguous range of logical workgroups, so the
+// tiles of one merge (which all read its Z) share one L2.
+__device__ __forceinline__ int64_t nd_xcd(int64_t i, int64_t n) {
+  const int64_t q = n >> 3, r = n & 7, x = i & 7, j = i >> 3;
+  return x * q + (x < r ? x : r) + j;
+}
+
 // Tile (tx, ty), tx >= ty, of the lower triangle of an nt x nt tile grid from
 // its index tt in row-major order of that triangle.
 __device__ __forceinline__ void tri_tile(int tt, int* tx, int* ty) {
@@ -905,10 +915,12 @@ __global__ __launch_bounds__(512) void k_nd_cut(NdArgs na) {
     z = na.scratch + la * na.scr_stride;
     const double* A = na.dA + la * na.in_stride;
     const int col = y < C ? y : (y < ncol ? C + ebase + (y - C) : 0);
-    const __amdgpu_buffer_rsrc_t ra = nd_rsrc(A, (unsigned)(C * na.dld * 8));
+    // the pivot rows' entries A[x][col] are read as A[col][x] (A is
+    // symmetric, and a stage writes only its lower tiles)
+    const __amdgpu_buffer_rsrc_t ra = nd_rsrc(A, (unsigned)(na.dn * na.dld * 8));
 #pragma unroll
     for (int x = 0; x < C; ++x) {
-      const double v = nd_load(ra, 8u * (unsigned)col, 8u * (unsigned)(x * na.dld));
+      const double v = nd_load(ra, 8u * (unsigned)(col * na.dld), 8u * (unsigned)x);
       U[x] = y < ncol ? v : 0.0;
       if ((x & 15) == 15) {
         pin8(U, x - 15);
@@ -1273,8 +1285,9 @@ __global__ __launch_bounds__(256) void k_nd_gprod(NdArgs na) {
   const int tid = threadIdx.x;
   const int M = na.ms.M, N = na.ms.N, T = na.T, Np = na.ms.Np, Mp = na.ms.Mp;
   const int ntx = (Np + 63) / 64, nty = (Mp + 63) / 64;
-  const int64_t la = blockIdx.x / (ntx * nty);
-  const int tt = (int)(blockIdx.x % (ntx * nty));
+  const int64_t lin = nd_xcd(blockIdx.x, gridDim.x);   // an array's tiles share one L2
+  const int64_t la = lin / (ntx * nty);
+  const int tt = (int)(lin % (ntx * nty));
   const int j0 = (tt / nty) * 64, k0 = (tt % nty) * 64;
   const int zld = M + T;
   const double* z = na.scratch + la * na.scr_stride;
@@ -1359,7 +1372,8 @@ __global__ __launch_bounds__(256) void k_nd_dense0(NdArgs na) {
 // x, y < E to dB (row stride dldo); OUT 1 writes G' = (Z^T Z - A) over the
 // sink x source block (A: [sources (M) | sinks (T)] after the pivots).
 // OUT 0 is symmetric: a workgroup computes one tile of the lower triangle
-// (tx >= ty) and writes it and its mirror image.
+// (tx >= ty) and writes it and, when the stage's output is the merged block
+// (dfull), its mirror image.
 template <int OUT>
 __global__ __launch_bounds__(256) void k_nd_dschur(NdArgs na) {
   __shared__ __attribute__((aligned(16))) double zab[2 * KC64 * KLD];
@@ -1371,8 +1385,9 @@ __global__ __launch_bounds__(256) void k_nd_dschur(NdArgs na) {
   const int nrx = OUT == 0 ? E : na.ms.Np, nry = OUT == 0 ? E : na.ms.Mp;
   const int ntx = (nrx + 63) / 64, nty = (nry + 63) / 64;
   const int ntiles = OUT == 0 ? ntx * (ntx + 1) / 2 : ntx * nty;
-  const int64_t la = blockIdx.x / ntiles;
-  const int tt = (int)(blockIdx.x % ntiles);
+  const int64_t lin = nd_xcd(blockIdx.x, gridDim.x);   // an array's tiles share one L2
+  const int64_t la = lin / ntiles;
+  const int tt = (int)(lin % ntiles);
   int tx, ty;
   if (OUT == 0) {
     tri_tile(tt, &tx, &ty);
@@ -1414,7 +1429,7 @@ __global__ __launch_bounds__(256) void k_nd_dschur(NdArgs na) {
           val[i][j][v] = in ? A[(int64_t)(64 + x) * na.dld + 64 + y] - mt.acc[i][j][v] : 0.0;
           if (in) B[(int64_t)x * na.dldo + y] = val[i][j][v];
         }
-    if (tx != ty) mt.store_transposed(val, zab, B, na.dldo, x0, y0, E, E, tid);
+    if (tx != ty && na.dfull) mt.store_transposed(val, zab, B, na.dldo, x0, y0, E, E, tid);
   } else {
     const int Np = na.ms.Np, Mp = na.ms.Mp, N = na.ms.N;
     float* out = nd_ref(na, la).out;
@@ -1448,11 +1463,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(5))) void k
   const int Emax = 2 * (nh + nw);
   const int nt = (Emax + 63) / 64;
   const int ntri = nt * (nt + 1) / 2;
-  const int64_t blk = blockIdx.x / ntri;
+  const int64_t lin = nd_xcd(blockIdx.x, gridDim.x);
+  const int64_t blk = lin / ntri;
   const MergeGeom g = merge_geom(na, blk);
   const int c = g.c, E = g.E;
   int tx, ty;
-  tri_tile((int)(blockIdx.x % ntri), &tx, &ty);
+  tri_tile((int)(lin % ntri), &tx, &ty);
   const int x0 = tx * 64, y0 = ty * 64;
   const int nrx = min(64, E - x0), nry = min(64, E - y0);
   if (nrx <= 0 || nry <= 0) return;
@@ -1623,6 +1639,7 @@ static void launch_staged(NdArgs na, int64_t n, int c, int n0, double* a, double
     na.dld = n0;
     na.dldo = last ? ldo : n0;
     na.dpanel = PANEL;
+    na.dfull = last ? 1 : 0;
     const int ext = na.dn - 64;
     const unsigned npan = (unsigned)((ext + PANEL - 1) / PANEL);
     const unsigned nthr = (unsigned)((64 + std::min(PANEL, ext) + 63) / 64 * 64);
