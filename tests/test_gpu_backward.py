@@ -76,6 +76,7 @@ def fc_oracle(W, X, dY, x_max, w_max):
     (37, 300, 70, 64, 64, 0, 0.0),        # ideal DAC: only negative inputs clipped
     (64, 513, 129, 128, 128, 6, 0.08),    # fixed w_max below max|W|: weight mask
     (256, 1024, 512, 64, 64, 8, 0.0),
+    (2048, 64, 32, 64, 64, 4, 0.0),       # dW split over 8 row ranges, then summed
 ])
 def test_fc_backward_parity(B, P, Q, M, N, dac, w_max):
     label = f"fc_backward B={B} P={P} Q={Q} dac={dac} w_max={w_max}"
@@ -167,6 +168,8 @@ def conv_dict(n, c_in, hw, c_out, k, s, p, w=None):
     (conv_dict(2, 20, 12, 68, 3, 1, 1), 4, 0.0),        # 3x3 halo kernels: ragged c_in, Q
     (conv_dict(2, 17, 16, 33, 3, 2, 1), 6, 0.1),        # 3x3 / 2 halo dW, weight mask
     (conv_dict(1, 8, 8, 12, 3, 1, 1, w=60), 0, 0.0),    # 3x3 halo, ideal DAC, 60-wide rows
+    (conv_dict(1, 17, 8, 70, 3, 1, 1), 4, 0.1),         # 3x3 halo dW in one chunk: direct write
+    (conv_dict(4, 16, 32, 8, 1, 1, 0), 6, 0.0),         # generic dW split over 16 pixel ranges
 ])
 def test_conv_backward_parity(conv, dac, w_max):
     label = "conv_backward %s dac=%d w_max=%g" % (conv, dac, w_max)
