@@ -17,7 +17,11 @@
 //                when both divisions are exact and in range
 //                (M = the n H W input pixels, N = c_in, K = kh kw Q).
 // A fully connected layer is the 1 x 1 convolution of 1 x 1 images
-// (n = B, c_in = P, c_out = Q).
+// (n = B, c_in = P, c_out = Q).  The generic kernels (k_bw_dw, k_bw_dx) gather
+// every operand element by element; 3 x 3 convolutions whose widths are
+// multiples of 4 use k_bw_dw3 / k_bw_dx3, which stage whole input or
+// output-gradient rows of a pixel chunk in LDS once and read the nine taps
+// from them.
 
 #include <algorithm>
 
