@@ -68,6 +68,8 @@ struct NdArgs {
   int dpanel;            // external columns per workgroup of the cut kernel
   int dfull;             // the stage writes both triangles (else only the
                          // lower tiles, which is all the next stage reads)
+  int fuse;              // k_nd_cut finishes the Schur update itself (its kFuse
+                         // path; the host's schur_fused decides)
   // several layers at once (null tables: the one layer of ms / W / gpt)
   NdBatch batch;
 };
@@ -1025,7 +1027,7 @@ __global__ __launch_bounds__(512) void k_nd_cut(NdArgs na) {
   __syncthreads();
   const lds_f64* is = opaque_lds<lds_f64>(&isq[0]);
   if constexpr (kFuse) {
-    if (Emax <= ZLD - 4) {   // schur_fused(C, Emax): launched with exactly 256 threads
+    if (na.fuse && Emax <= ZLD - 4) {   // schur_fused(C, Emax): launched with 256 threads
       if (y >= C && y < ncol) {
 #pragma unroll
         for (int x = 0; x < C; ++x) zl[x * ZLD + (y - C)] = U[x] * is[x];
@@ -1659,7 +1661,7 @@ static void launch_staged(NdArgs na, int64_t n, int c, int n0, double* a, double
 // level buffers and scratch, sized by nd_sizes for one array, times n).
 hipError_t launch_nd_build(const MapScalars& ms, const float* W, float* gpt, int64_t arr0,
                            int64_t n, int bs, double* ws, hipStream_t s, const NdBatch* batch) {
-  NdArgs na;
+  NdArgs na{};
   na.ms = ms;
   na.W = W;
   na.gpt = gpt;
@@ -1722,7 +1724,11 @@ hipError_t launch_nd_build(const MapScalars& ms, const float* W, float* gpt, int
       ProfScope prof("nd_merge", s);
       if (cut_in_registers(c, c + e_layout)) {
         const int emax = 2 * (nh + nw);
-        const bool fused = schur_fused(c, emax);
+        // a fused Schur update runs in the merge's own workgroup; with fewer
+        // merges than half the CUs its tiles are spread over k_nd_schur's
+        // workgroups instead (the 64 x 64 conv layer: 229 -> 217 us)
+        const bool fused = schur_fused(c, emax) && (int64_t)n * nmerge >= 128;
+        na.fuse = fused ? 1 : 0;
         launch_cut<false>(na, grid, c, c + e_layout, fused, s);
         if (!fused) {
           const int nt = (emax + 63) / 64;
