@@ -273,6 +273,37 @@ __device__ __forceinline__ double readlane_d(double v, int l) {
   return __builtin_bit_cast(double, ((unsigned long long)hi << 32) | lo);
 }
 
+// Lane k of every row of 16 lanes, to the whole row (DPP row broadcast).
+template <int K>
+__device__ __forceinline__ double rowbcast_d(double v) {
+  const unsigned long long b = __builtin_bit_cast(unsigned long long, v);
+  const unsigned lo = (unsigned)__builtin_amdgcn_update_dpp(0, (int)(unsigned)b, 0x150 + K, 0xf, 0xf, false);
+  const unsigned hi =
+      (unsigned)__builtin_amdgcn_update_dpp(0, (int)(unsigned)(b >> 32), 0x150 + K, 0xf, 0xf, false);
+  return __builtin_bit_cast(double, ((unsigned long long)hi << 32) | lo);
+}
+
+__device__ __forceinline__ double rowbcast_d(double v, int k) {
+  switch (k & 15) {
+    case 0: return rowbcast_d<0>(v);
+    case 1: return rowbcast_d<1>(v);
+    case 2: return rowbcast_d<2>(v);
+    case 3: return rowbcast_d<3>(v);
+    case 4: return rowbcast_d<4>(v);
+    case 5: return rowbcast_d<5>(v);
+    case 6: return rowbcast_d<6>(v);
+    case 7: return rowbcast_d<7>(v);
+    case 8: return rowbcast_d<8>(v);
+    case 9: return rowbcast_d<9>(v);
+    case 10: return rowbcast_d<10>(v);
+    case 11: return rowbcast_d<11>(v);
+    case 12: return rowbcast_d<12>(v);
+    case 13: return rowbcast_d<13>(v);
+    case 14: return rowbcast_d<14>(v);
+    default: return rowbcast_d<15>(v);
+  }
+}
+
 // LDS written by some lanes of a wave, then read by others of the same wave.
 __device__ __forceinline__ void wave_sync() {
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
@@ -329,16 +360,19 @@ __device__ __forceinline__ void block_level(int T, int I0, int J0, const short* 
       const double b = c1[max(r1, 0) * EIN + max(s1, 0)];
       U[x] = ((r0 >= 0 && s0 >= 0) ? a : 0.0) + ((r1 >= 0 && s1 >= 0) ? b : 0.0);
     }
-    if constexpr (SPLIT) {
-      // few blocks (a latency-bound build at 96 VGPRs): the multiplier of
-      // row x comes from lane k's register by a lane read
+    if constexpr (SPLIT || GS == 64 || GS == 16) {
+      // the multiplier of row x comes from the group's lane k: a lane read
+      // (one group per wave) or a row broadcast (groups of 16 lanes), no LDS;
+      // the split form (few blocks, 96 VGPRs) takes a lane permute otherwise
 #pragma unroll
       for (int k = 0; k < C; ++k) {
-        const double piv = GS == 64 ? readlane_d(U[k], k) : bperm_d(U[k], gb + k);
+        const double piv = GS == 64 ? readlane_d(U[k], k)
+                                    : (GS == 16 ? rowbcast_d(U[k], k) : bperm_d(U[k], gb + k));
         const double t = U[k] * recip(piv);
 #pragma unroll
         for (int x = k + 1; x < LD; ++x) {
-          const double mx = GS == 64 ? readlane_d(U[x], k) : bperm_d(U[x], gb + k);
+          const double mx = GS == 64 ? readlane_d(U[x], k)
+                                     : (GS == 16 ? rowbcast_d(U[x], k) : bperm_d(U[x], gb + k));
           U[x] = fma(-mx, t, U[x]);
         }
       }
