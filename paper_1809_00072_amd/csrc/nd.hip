@@ -192,8 +192,8 @@ __device__ __forceinline__ ArrRef nd_ref(const NdArgs& na, int64_t la) {
 // combined matrix [c cut nodes | E external ports], every row in registers.
 // Eliminating the c cut pivots updates every later row, so the external
 // rows and columns end as the merged block's admittance matrix.  The
-// multiplier of row x at pivot k is that row's entry in column k, fetched
-// from the group's lane k (ds_bpermute; a lane read for a whole wave).  No
+// multiplier of row x at pivot k is that row's entry in column k, held by
+// the group's lane k (see block_level for how it reaches the others).  No
 // workgroup barrier: each wave's levels use its own LDS buffers.
 // ---------------------------------------------------------------------------
 constexpr int BS = 8;                 // side of the blocks of this kernel
@@ -317,10 +317,12 @@ __device__ __forceinline__ void wave_sync() {
 // all work on this block; otherwise the wave does them all.
 // The combined matrix is symmetric, and so is what remains of it after each
 // pivot, so the multiplier of row x at pivot k (its entry in column k) equals
-// the pivot row's entry in column x: at every pivot each lane publishes its
-// entry of the pivot row in LDS (`pr`, GS + 1 doubles per group) and every
-// lane of the group reads the multipliers back as broadcasts.  The SPLIT form
-// (capped at 96 VGPRs) reads them from the pivot lane's registers instead.
+// the pivot row's entry in column x, i.e. lane k's register x.  Groups of 64
+// lanes read it with a lane read and groups of 16 with a DPP row broadcast,
+// neither touching LDS (which bounds this kernel); groups of 8 and 32 lanes
+// publish the pivot row in LDS (`pr`, GS + 1 doubles per group) and read it
+// back as broadcasts, or, in the SPLIT form (capped at 96 VGPRs), take it by
+// a lane permute.
 template <int L, int H, int W, bool VERT, bool SPLIT>
 __device__ __forceinline__ void block_level(int T, int I0, int J0, const short* tab,
                                             const double* in, double* out, double* pr, int lane,
