@@ -404,6 +404,83 @@ __device__ __forceinline__ void block_level(int T, int I0, int J0, const short* 
   else wave_sync();
 }
 
+// Conductance g between nodes p and q of a small symmetric matrix held in
+// registers (lower triangle used).
+template <int N>
+__device__ __forceinline__ void stamp(double (&X)[N][N], int p, int q, double g) {
+  X[p][p] += g;
+  X[q][q] += g;
+  if (p > q) X[p][q] -= g;
+  else X[q][p] -= g;
+}
+
+// Eliminates nodes 0 .. NC - 1 of the symmetric N x N matrix X (lower
+// triangle): X[i][j] -= X[i][k] X[j][k] / X[k][k] for i >= j > k.
+template <int N, int NC>
+__device__ __forceinline__ void eliminate_lead(double (&X)[N][N]) {
+#pragma unroll
+  for (int k = 0; k < NC; ++k) {
+    const double r = recip(X[k][k]);
+#pragma unroll
+    for (int i = k + 1; i < N; ++i) {
+      const double f = X[i][k] * r;
+#pragma unroll
+      for (int j = k + 1; j <= i; ++j) X[i][j] = fma(-f, X[j][k], X[i][j]);
+    }
+  }
+}
+
+// Levels 1 x 1 and 2 x 1 -> 2 x 2 of the 2 x 2 block whose top-left cell is
+// (gi0, gj0), in one lane's registers: each cell's ports in the padded order
+// [L | R | T | B] (an absent R or T port is a zero row: no row-wire edge at
+// the right edge of the grid; at the top the cell's b-node is eliminated in
+// series), the cells of each column merged (their shared b-node eliminated),
+// then the two 2 x 1 halves (their two shared a-nodes).  Returns the 8 x 8
+// matrix over [L0 L1 | R0 R1 | T0 T1 | B0 B1] in rows 2 .. 9 of X.
+__device__ __forceinline__ void block2x2(const MapScalars& ms, const float* W, double wmax,
+                                         int64_t arr, int gi0, int gj0, int T, int row_off,
+                                         double g_r, double g_c, double g_s, double (&X)[10][10]) {
+#pragma unroll
+  for (int i = 0; i < 10; ++i)
+#pragma unroll
+    for (int j = 0; j <= i; ++j) X[i][j] = 0.0;
+#pragma unroll
+  for (int c = 0; c < 2; ++c) {
+    // the column's two cells over [s | L0 L1 | R0 R1 | T | B], s the b-node
+    // between them
+    double Y[7][7];
+#pragma unroll
+    for (int i = 0; i < 7; ++i)
+#pragma unroll
+      for (int j = 0; j <= i; ++j) Y[i][j] = 0.0;
+#pragma unroll
+    for (int r = 0; r < 2; ++r) {
+      const int gi = gi0 + r, gj = gj0 + c;
+      const double G = cell_conductance(ms, W, wmax, arr, gi, gj, row_off);
+      const bool hasT = gi > 0;
+      const double gv = (gi + 1 < T) ? g_c : g_s;
+      const int iL = 1 + r, iR = 3 + r, iT = r == 0 ? 5 : 0, iB = r == 0 ? 0 : 6;
+      stamp(Y, iL, iR, gj + 1 < T ? g_r : 0.0);
+      stamp(Y, iL, iT, hasT ? G : 0.0);
+      stamp(Y, iT, iB, hasT ? gv : 0.0);
+      stamp(Y, iL, iB, (!hasT && G > 0.0) ? (G * gv) / (G + gv) : 0.0);
+    }
+    eliminate_lead<7, 1>(Y);
+    // the half's ports [L0 L1 R0 R1 T B] in the 2 x 2 merge's order
+    // [s0 s1 | L0 L1 | R0 R1 | T0 T1 | B0 B1] (s: the shared a-nodes)
+    constexpr int kMap[2][6] = {{2, 3, 0, 1, 6, 8}, {0, 1, 4, 5, 7, 9}};
+#pragma unroll
+    for (int p = 0; p < 6; ++p)
+#pragma unroll
+      for (int q = 0; q <= p; ++q) {
+        const int a = kMap[c][p], b = kMap[c][q];
+        if (a >= b) X[a][b] += Y[1 + p][1 + q];
+        else X[b][a] += Y[1 + p][1 + q];
+      }
+  }
+  eliminate_lead<10, 2>(X);
+}
+
 // SPLIT (few blocks, a latency-bound build): one 8 x 8 block per workgroup,
 // its waves sharing each level; otherwise one block per wave (BWAVES blocks
 // per workgroup), no workgroup barriers.
@@ -432,6 +509,38 @@ __device__ __forceinline__ void nd_block(const NdArgs& na) {
   const double wmax = ms.wmax_fixed > 0.0f ? (double)ms.wmax_fixed : (double)*ms.d_wmax;
   double* A = bufA[SPLIT ? 0 : wv];
   double* B = bufB[SPLIT ? 0 : wv];
+  if constexpr (!SPLIT) {
+    // levels 1 x 1 .. 2 x 2 in registers, lane q < 16 taking 2 x 2 block q,
+    // written to the level buffer as block_level<1> would (ports [L | R (not
+    // at the right edge) | T (not at the top) | B], row stride 8)
+    if (lane < 16) {
+      const int qi = lane >> 2, qj = lane & 3;
+      const int gi0 = I0 + 2 * qi, gj0 = J0 + 2 * qj;
+      double X[10][10];
+      block2x2(ms, ref.W, wmax, arr, gi0, gj0, T, na.row_off, na.g_r, na.g_c, na.g_s, X);
+      const bool rn = gj0 + 2 < T, tn = gi0 > 0;
+      const int oT = rn ? 4 : 2, oB = oT + (tn ? 2 : 0);
+      // padded port -> stored port (-1: absent)
+      int pos[8];
+      pos[0] = 0;
+      pos[1] = 1;
+      pos[2] = rn ? 2 : -1;
+      pos[3] = rn ? 3 : -1;
+      pos[4] = tn ? oT : -1;
+      pos[5] = tn ? oT + 1 : -1;
+      pos[6] = oB;
+      pos[7] = oB + 1;
+      double* o = A + lane * lds_mat(8);
+#pragma unroll
+      for (int p = 0; p < 8; ++p)
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+          const double v = p >= q ? X[2 + p][2 + q] : X[2 + q][2 + p];
+          if (pos[p] >= 0 && pos[q] >= 0) o[pos[p] * 8 + pos[q]] = v;
+        }
+    }
+    wave_sync();
+  } else {
   // leaves (the first wave): one cell per lane, ports [L | R (not at the
   // right edge) | T (not at the top) | B] in a 4 x 4 slot
   if (!SPLIT || wv == 0) {
@@ -463,6 +572,7 @@ __device__ __forceinline__ void nd_block(const NdArgs& na) {
   else wave_sync();
   block_level<0, 1, 1, true, SPLIT>(T, I0, J0, tab, A, B, prow[wv], lane, wv);
   block_level<1, 2, 1, false, SPLIT>(T, I0, J0, tab, B, A, prow[wv], lane, wv);
+  }
   block_level<2, 2, 2, true, SPLIT>(T, I0, J0, tab, A, B, prow[wv], lane, wv);
   block_level<3, 4, 2, false, SPLIT>(T, I0, J0, tab, B, A, prow[wv], lane, wv);
   block_level<4, 4, 4, true, SPLIT>(T, I0, J0, tab, A, B, prow[wv], lane, wv);
