@@ -199,14 +199,16 @@ __device__ __forceinline__ ArrRef nd_ref(const NdArgs& na, int64_t la) {
 constexpr int BS = 8;                 // side of the blocks of this kernel
 constexpr int BWAVES = 4;             // waves per workgroup of the block kernel
 constexpr int64_t kSplitBlocks = 2048; // at most this many blocks: one workgroup per block
-constexpr int BLEVELS = 6;            // 1x1 -> 2x1 -> 2x2 -> 4x2 -> 4x4 -> 8x4 -> 8x8
+constexpr int BLEVELS = 7;  // 1x1 -> 2x1 -> 2x2 -> 4x2 -> 4x4 -> 8x4 -> 8x8 -> 16x8
 // In LDS every cell's or merged block's matrix takes its side squared plus one
 // double: consecutive matrices then start in different banks, so the lanes of
 // different merge groups (and the leaf lanes) do not collide.
 __host__ __device__ constexpr int lds_mat(int side) { return side * side + 1; }
 // doubles per wave: the leaves and odd levels (64 x 17, 16 x 65, 4 x 257) and
-// the even levels (32 x 37, 8 x 145, 2 x 577)
+// the even levels (32 x 37, 8 x 145, 2 x 577); without the leaves and the
+// first level (the 2 x 2 blocks formed in registers) 16 x 65 and 8 x 145
 constexpr int BUFA = 64 * 17, BUFB = 32 * 37;
+constexpr int BUFA2 = 16 * 65, BUFB2 = 8 * 145;
 
 // Child port landing on each combined slot (cut nodes 0 .. c-1, then the
 // externals), per level and per boundary variant (bit 1: the merged block
@@ -222,7 +224,7 @@ constexpr BlkTab make_blk_tab() {
     for (int v = 0; v < 4; ++v)
       for (int ch = 0; ch < 2; ++ch)
         for (int k = 0; k < 64; ++k) t.s[l][v][ch][k] = -1;
-  const int hs[BLEVELS] = {1, 2, 2, 4, 4, 8}, ws[BLEVELS] = {1, 1, 2, 2, 4, 4};
+  const int hs[BLEVELS] = {1, 2, 2, 4, 4, 8, 8}, ws[BLEVELS] = {1, 1, 2, 2, 4, 4, 8};
   const int Tr = 1024;   // any grid larger than the merged block
   for (int l = 0; l < BLEVELS; ++l) {
     const bool vert = (l % 2) == 0;
@@ -323,7 +325,13 @@ __device__ __forceinline__ void wave_sync() {
 // publish the pivot row in LDS (`pr`, GS + 1 doubles per group) and read it
 // back as broadcasts, or, in the SPLIT form (capped at 96 VGPRs), take it by
 // a lane permute.
-template <int L, int H, int W, bool VERT, bool SPLIT>
+// DENSE: merged blocks go to a global level buffer (dense, EM x EM each),
+// else to LDS (lds_mat(EM) apart).  RS: side of the region whose merges the
+// call makes (the children h x w tiling it); CSTR: doubles between children
+// in `in` (0: lds_mat(EIN)); DIST: the passes are shared by the workgroup's
+// waves (then a workgroup barrier ends the level).
+template <int L, int H, int W, bool VERT, bool SPLIT, bool DENSE, int RS = BS, int CSTR = 0,
+          bool DIST = SPLIT>
 __device__ __forceinline__ void block_level(int T, int I0, int J0, const short* tab,
                                             const double* in, double* out, double* pr, int lane,
                                             int wv) {
@@ -333,15 +341,15 @@ __device__ __forceinline__ void block_level(int T, int I0, int J0, const short* 
   constexpr int LD = C + EM;
   constexpr int GS = LD <= 8 ? 8 : (LD <= 16 ? 16 : (LD <= 32 ? 32 : 64));
   constexpr int GPW = 64 / GS;                 // merges per pass
-  // merged blocks: padded in LDS, dense in the global level buffer (last level)
-  constexpr int OSTRIDE = L == BLEVELS - 1 ? EM * EM : lds_mat(EM);
-  constexpr int MC = BS / NW, CC = BS / W;     // merges / children per block row
-  constexpr int NM = (BS / NH) * MC;
+  constexpr int OSTRIDE = DENSE ? EM * EM : lds_mat(EM);
+  constexpr int CS = CSTR > 0 ? CSTR : lds_mat(EIN);
+  constexpr int MC = RS / NW, CC = RS / W;     // merges / children per region row
+  constexpr int NM = (RS / NH) * MC;
   static_assert(NM % GPW == 0, "whole passes");
   const int g = lane / GS, yl = lane % GS, gb = lane - yl;
   lds_f64* gr = opaque_lds<lds_f64>(pr + g * (GS + 1));   // this group's pivot row
 #pragma unroll 1
-  for (int pass = SPLIT ? wv : 0; pass < NM / GPW; pass += SPLIT ? BWAVES : 1) {
+  for (int pass = DIST ? wv : 0; pass < NM / GPW; pass += DIST ? BWAVES : 1) {
     const int m = pass * GPW + g;
     const int mi = m / MC, mj = m % MC;
     const int i0 = I0 + mi * NH, j0 = J0 + mj * NW;
@@ -351,8 +359,8 @@ __device__ __forceinline__ void block_level(int T, int I0, int J0, const short* 
     const int cm1 = VERT ? (mi * 2 + 1) * CC + mj : mi * CC + mj * 2 + 1;
     const short* t0 = tab + (((L * 4) + (rn ? 2 : 0) + (tn ? 1 : 0)) * 2) * 64;
     const short* t1 = t0 + 64;
-    const double* c0 = in + cm0 * lds_mat(EIN);
-    const double* c1 = in + cm1 * lds_mat(EIN);
+    const double* c0 = in + cm0 * CS;
+    const double* c1 = in + cm1 * CS;
     const int s0 = t0[yl], s1 = t1[yl];
     double U[LD];
 #pragma unroll
@@ -400,7 +408,7 @@ __device__ __forceinline__ void block_level(int T, int I0, int J0, const short* 
         if (x < ld) out[m * OSTRIDE + (x - C) * EM + (yl - C)] = U[x];
     }
   }
-  if (SPLIT) __syncthreads();
+  if (DIST) __syncthreads();
   else wave_sync();
 }
 
@@ -482,14 +490,18 @@ __device__ __forceinline__ void block2x2(const MapScalars& ms, const float* W, d
 }
 
 // SPLIT (few blocks, a latency-bound build): one 8 x 8 block per workgroup,
-// its waves sharing each level; otherwise one block per wave (BWAVES blocks
-// per workgroup), no workgroup barriers.
+// its waves sharing each level, the 8 x 8 block to the level buffer.
+// Otherwise one 16 x 16 region per workgroup: wave w builds its 8 x 8 block
+// (row w / 2, column w % 2 of the region) alone, without workgroup barriers,
+// into its LDS buffer A; then waves 0 and 1 merge the two columns' pairs into
+// 16 x 8 blocks, which go to the level buffer.
 template <bool SPLIT>
 __device__ __forceinline__ void nd_block(const NdArgs& na) {
   __shared__ short tab[BLEVELS * 4 * 2 * 64];
   constexpr int NB = SPLIT ? 1 : BWAVES;   // blocks per workgroup
-  __shared__ double bufA[NB][BUFA];
-  __shared__ double bufB[NB][BUFB];
+  constexpr int BA = SPLIT ? BUFA : BUFA2, BB = SPLIT ? BUFB : BUFB2;
+  __shared__ double bufA[NB][BA];
+  __shared__ double bufB[NB][BB];
   __shared__ double prow[BWAVES][72];   // pivot rows of each wave's merge groups
   const short* ct = &kBlkTab.s[0][0][0][0];
   for (int e = threadIdx.x; e < BLEVELS * 4 * 2 * 64; e += 64 * BWAVES) tab[e] = ct[e];
@@ -497,12 +509,24 @@ __device__ __forceinline__ void nd_block(const NdArgs& na) {
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
   const int T = na.T;
   const int nsb = T / BS;
-  const int64_t blk = SPLIT ? (int64_t)blockIdx.x : (int64_t)blockIdx.x * BWAVES + wv;
-  const int64_t nblk = na.n_arrays * nsb * nsb;
-  if (blk >= nblk) return;
-  const int64_t la = blk / (nsb * nsb);
-  const int sb = (int)(blk % (nsb * nsb));
-  const int I0 = (sb / nsb) * BS, J0 = (sb % nsb) * BS;
+  int64_t la;
+  int sb, I0, J0;
+  if constexpr (SPLIT) {
+    const int64_t blk = blockIdx.x;
+    if (blk >= na.n_arrays * nsb * nsb) return;
+    la = blk / (nsb * nsb);
+    sb = (int)(blk % (nsb * nsb));
+    I0 = (sb / nsb) * BS;
+    J0 = (sb % nsb) * BS;
+  } else {
+    const int nr = nsb / 2;   // regions per side
+    const int64_t rg = blockIdx.x;
+    if (rg >= na.n_arrays * nr * nr) return;   // whole workgroups
+    la = rg / (nr * nr);
+    sb = (int)(rg % (nr * nr));   // region
+    I0 = (sb / nr) * 2 * BS + (wv >> 1) * BS;
+    J0 = (sb % nr) * 2 * BS + (wv & 1) * BS;
+  }
   const ArrRef ref = nd_ref(na, la);
   const MapScalars& ms = *ref.ms;
   const int64_t arr = ref.arr;
@@ -570,15 +594,29 @@ __device__ __forceinline__ void nd_block(const NdArgs& na) {
   }
   if (SPLIT) __syncthreads();
   else wave_sync();
-  block_level<0, 1, 1, true, SPLIT>(T, I0, J0, tab, A, B, prow[wv], lane, wv);
-  block_level<1, 2, 1, false, SPLIT>(T, I0, J0, tab, B, A, prow[wv], lane, wv);
+  block_level<0, 1, 1, true, SPLIT, false>(T, I0, J0, tab, A, B, prow[wv], lane, wv);
+  block_level<1, 2, 1, false, SPLIT, false>(T, I0, J0, tab, B, A, prow[wv], lane, wv);
   }
-  block_level<2, 2, 2, true, SPLIT>(T, I0, J0, tab, A, B, prow[wv], lane, wv);
-  block_level<3, 4, 2, false, SPLIT>(T, I0, J0, tab, B, A, prow[wv], lane, wv);
-  block_level<4, 4, 4, true, SPLIT>(T, I0, J0, tab, A, B, prow[wv], lane, wv);
-  constexpr int EO = 4 * BS;   // ports of an interior 8 x 8 block
-  double* dst = na.buf_out + la * na.out_stride + (int64_t)sb * EO * EO;
-  block_level<5, 8, 4, false, SPLIT>(T, I0, J0, tab, B, dst, prow[wv], lane, wv);
+  block_level<2, 2, 2, true, SPLIT, false>(T, I0, J0, tab, A, B, prow[wv], lane, wv);
+  block_level<3, 4, 2, false, SPLIT, false>(T, I0, J0, tab, B, A, prow[wv], lane, wv);
+  block_level<4, 4, 4, true, SPLIT, false>(T, I0, J0, tab, A, B, prow[wv], lane, wv);
+  if constexpr (SPLIT) {
+    constexpr int EO = 4 * BS;   // ports of an interior 8 x 8 block
+    double* dst = na.buf_out + la * na.out_stride + (int64_t)sb * EO * EO;
+    block_level<5, 8, 4, false, true, true>(T, I0, J0, tab, B, dst, prow[wv], lane, wv);
+  } else {
+    // the 8 x 8 block to A (row stride 32), then the region's two 16 x 8
+    // merges (children BA apart: the waves' A buffers), to merged blocks
+    // (region row, 2 region column + 0 / 1) of the 16 x 8 level
+    block_level<5, 8, 4, false, false, false>(T, I0, J0, tab, B, A, prow[wv], lane, wv);
+    __syncthreads();
+    constexpr int E16 = 2 * (2 * BS + BS);   // ports of an interior 16 x 8 block
+    const int RI = I0 - (wv >> 1) * BS, RJ = J0 - (wv & 1) * BS;
+    double* dst = na.buf_out + la * na.out_stride +
+                  ((int64_t)(RI / (2 * BS)) * (T / BS) + RJ / BS) * E16 * E16;
+    block_level<6, 8, 8, true, false, true, 2 * BS, BA, true>(T, RI, RJ, tab, &bufA[0][0], dst,
+                                                             prow[wv], lane, wv);
+  }
 }
 
 // The split form is held to 96 VGPRs (5 waves per SIMD): five workgroups per
@@ -1839,8 +1877,8 @@ hipError_t launch_nd_build(const MapScalars& ms, const float* W, float* gpt, int
     if (nblk <= kSplitBlocks) {
       hipLaunchKernelGGL(k_nd_block_split, dim3((unsigned)nblk), dim3(64 * BWAVES), 0, s, na);
     } else {
-      const dim3 grid((unsigned)((nblk + BWAVES - 1) / BWAVES));
-      hipLaunchKernelGGL(k_nd_block, grid, dim3(64 * BWAVES), 0, s, na);
+      // 16 x 16 regions; the kernel also makes the 16 x 8 level
+      hipLaunchKernelGGL(k_nd_block, dim3((unsigned)(nblk / 4)), dim3(64 * BWAVES), 0, s, na);
     }
   }
   hipError_t e = hipGetLastError();
@@ -1849,6 +1887,10 @@ hipError_t launch_nd_build(const MapScalars& ms, const float* W, float* gpt, int
   double* nxt = bufB;
   int h = bs, w = bs;
   bool vert = true;
+  if (n * nsb * nsb > kSplitBlocks) {   // the block kernel made the 16 x 8 level
+    h = 2 * bs;
+    vert = false;
+  }
   while (h < na.T || w < na.T) {
     const int nh = vert ? 2 * h : h, nw = vert ? w : 2 * w;
     const int64_t nmerge = (int64_t)(na.T / nh) * (na.T / nw);
