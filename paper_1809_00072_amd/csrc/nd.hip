@@ -489,12 +489,16 @@ __device__ __forceinline__ void block2x2(const MapScalars& ms, const float* W, d
   eliminate_lead<10, 2>(X);
 }
 
+__device__ void region_merge16(int T, int RI, int RJ, const double* ch, double* dst,
+                               double* scr);
+
 // SPLIT (few blocks, a latency-bound build): one 8 x 8 block per workgroup,
 // its waves sharing each level, the 8 x 8 block to the level buffer.
 // Otherwise one 16 x 16 region per workgroup: wave w builds its 8 x 8 block
 // (row w / 2, column w % 2 of the region) alone, without workgroup barriers,
-// into its LDS buffer A; then waves 0 and 1 merge the two columns' pairs into
-// 16 x 8 blocks, which go to the level buffer.
+// into its LDS buffer A; waves 0 and 1 merge the two columns' pairs into
+// 16 x 8 blocks (in LDS), and the workgroup merges those into the region's
+// 16 x 16 block, which goes to the level buffer.
 template <bool SPLIT>
 __device__ __forceinline__ void nd_block(const NdArgs& na) {
   __shared__ short tab[BLEVELS * 4 * 2 * 64];
@@ -605,17 +609,19 @@ __device__ __forceinline__ void nd_block(const NdArgs& na) {
     double* dst = na.buf_out + la * na.out_stride + (int64_t)sb * EO * EO;
     block_level<5, 8, 4, false, true, true>(T, I0, J0, tab, B, dst, prow[wv], lane, wv);
   } else {
-    // the 8 x 8 block to A (row stride 32), then the region's two 16 x 8
-    // merges (children BA apart: the waves' A buffers), to merged blocks
-    // (region row, 2 region column + 0 / 1) of the 16 x 8 level
+    // the 8 x 8 block to A (row stride 32); the region's two 16 x 8 merges
+    // (children BA apart: the waves' A buffers) to the B buffers (row stride
+    // 48); their 16 x 16 merge (the A buffers as scratch) to merged block
+    // (region row, region column) of the 16 x 16 level
     block_level<5, 8, 4, false, false, false>(T, I0, J0, tab, B, A, prow[wv], lane, wv);
     __syncthreads();
-    constexpr int E16 = 2 * (2 * BS + BS);   // ports of an interior 16 x 8 block
     const int RI = I0 - (wv >> 1) * BS, RJ = J0 - (wv & 1) * BS;
+    block_level<6, 8, 8, true, false, false, 2 * BS, BA, true>(T, RI, RJ, tab, &bufA[0][0],
+                                                              &bufB[0][0], prow[wv], lane, wv);
+    constexpr int E16 = 8 * BS;   // ports of an interior 16 x 16 block
     double* dst = na.buf_out + la * na.out_stride +
-                  ((int64_t)(RI / (2 * BS)) * (T / BS) + RJ / BS) * E16 * E16;
-    block_level<6, 8, 8, true, false, true, 2 * BS, BA, true>(T, RI, RJ, tab, &bufA[0][0], dst,
-                                                             prow[wv], lane, wv);
+                  ((int64_t)(RI / (2 * BS)) * (T / (2 * BS)) + RJ / (2 * BS)) * E16 * E16;
+    region_merge16(T, RI, RJ, &bufB[0][0], dst, &bufA[0][0]);
   }
 }
 
@@ -1060,6 +1066,90 @@ __device__ __forceinline__ void tri_tile(int tt, int* tx, int* ty) {
   while (x * (x + 1) / 2 > tt) --x;
   *tx = x;
   *ty = tt - x * (x + 1) / 2;
+}
+
+// The 16 x 16 merge of a region's two 16 x 8 halves (left, right) at (RI, RJ):
+// ch holds them in LDS (row stride 48, lds_mat(48) apart), the merged block
+// (E <= 64 ports, row stride 64) goes to dst, scr is LDS scratch of at least
+// 1400 doubles.  Waves 0 and 1 each hold, lane by lane, columns of the
+// combined matrix's 16 cut rows (the shared a-nodes): lanes 0 .. 15 the cut
+// columns (both waves), the other lanes externals 0 .. 47 (wave 0) and
+// 48 .. 63 (wave 1).  Each wave eliminates the cut rows by itself, taking
+// pivot k's column from lane k by lane reads (no barriers); Z (the
+// eliminated rows scaled by D^-1/2) goes to LDS, and the external block
+// V - Z^T Z is one 64 x 64 tile on the fp64 matrix cores (all four waves).
+__device__ void region_merge16(int T, int RI, int RJ, const double* ch, double* dst,
+                               double* scr) {
+  constexpr int C = 16, EIN = 48, CH1 = EIN * EIN + 1, ZL = 68;
+  const int tid = threadIdx.x;
+  short* invt = reinterpret_cast<short*>(scr);   // [2][80]
+  double* zl = scr + 48;                         // [16][ZL]
+  const int E = nports(RI, RJ, C, C, T);
+  for (int t = tid; t < 160; t += 256) invt[t] = -1;
+  __syncthreads();
+  if (tid < 2 * EIN) {
+    const int c = tid / EIN, p = tid - c * EIN;
+    if (p < nports(RI, RJ + c * (C / 2), C, C / 2, T)) {
+      const int d = merge_dest(c, p, RI, RJ, C, C / 2, false, T);
+      invt[c * 80 + (d >= 0 ? C + d : -1 - d)] = (short)p;
+    }
+  }
+  __syncthreads();
+  const int wv = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
+  if (wv < 2) {
+    const int y = lane < C ? lane : C + 48 * wv + (lane - C);   // combined column
+    const int pb0 = y < C + E ? invt[y] : -1, pb1 = y < C + E ? invt[80 + y] : -1;
+    double U[C];
+#pragma unroll
+    for (int x = 0; x < C; ++x) {
+      const int pa0 = invt[x], pa1 = invt[80 + x];
+      const double a = ch[max(pa0, 0) * EIN + max(pb0, 0)];
+      const double b = ch[CH1 + max(pa1, 0) * EIN + max(pb1, 0)];
+      U[x] = ((pa0 >= 0 && pb0 >= 0) ? a : 0.0) + ((pa1 >= 0 && pb1 >= 0) ? b : 0.0);
+    }
+    double sq[C];
+#pragma unroll
+    for (int k = 0; k < C; ++k) {
+      const double piv = readlane_d(U[k], k);
+      sq[k] = 1.0 / sqrt(piv);
+      const double t = U[k] * recip(piv);
+#pragma unroll
+      for (int x = k + 1; x < C; ++x) U[x] = fma(-readlane_d(U[x], k), t, U[x]);
+    }
+    if (lane >= C && y < C + E) {
+#pragma unroll
+      for (int x = 0; x < C; ++x) zl[x * ZL + (y - C)] = U[x] * sq[x];
+    }
+  }
+  __syncthreads();
+  MfmaTile mt;
+  mt.init(tid);
+  double vv[2][2][4];
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    const int yy = min(mt.col(j), E - 1);
+    const int qb0 = invt[C + yy], qb1 = invt[80 + C + yy];
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int x = min(mt.row(i, v), E - 1);
+        const int qa0 = invt[C + x], qa1 = invt[80 + C + x];
+        const double a = ch[max(qa0, 0) * EIN + max(qb0, 0)];
+        const double b = ch[CH1 + max(qa1, 0) * EIN + max(qb1, 0)];
+        vv[i][j][v] = ((qa0 >= 0 && qb0 >= 0) ? a : 0.0) + ((qa1 >= 0 && qb1 >= 0) ? b : 0.0);
+      }
+  }
+  mt.step_ld(zl, zl, ZL, C, E, E);
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int x = mt.row(i, v), yy = mt.col(j);
+        if (x < E && yy < E) dst[x * 64 + yy] = vv[i][j][v] - mt.acc[i][j][v];
+      }
 }
 
 // MODE 0: a merge (children through the port tables); 1: the final step;
@@ -1877,7 +1967,7 @@ hipError_t launch_nd_build(const MapScalars& ms, const float* W, float* gpt, int
     if (nblk <= kSplitBlocks) {
       hipLaunchKernelGGL(k_nd_block_split, dim3((unsigned)nblk), dim3(64 * BWAVES), 0, s, na);
     } else {
-      // 16 x 16 regions; the kernel also makes the 16 x 8 level
+      // 16 x 16 regions; the kernel also makes the 16 x 8 and 16 x 16 levels
       hipLaunchKernelGGL(k_nd_block, dim3((unsigned)(nblk / 4)), dim3(64 * BWAVES), 0, s, na);
     }
   }
@@ -1887,9 +1977,9 @@ hipError_t launch_nd_build(const MapScalars& ms, const float* W, float* gpt, int
   double* nxt = bufB;
   int h = bs, w = bs;
   bool vert = true;
-  if (n * nsb * nsb > kSplitBlocks) {   // the block kernel made the 16 x 8 level
+  if (n * nsb * nsb > kSplitBlocks) {   // the block kernel made the 16 x 16 level
     h = 2 * bs;
-    vert = false;
+    w = 2 * bs;
   }
   while (h < na.T || w < na.T) {
     const int nh = vert ? 2 * h : h, nw = vert ? w : 2 * w;
