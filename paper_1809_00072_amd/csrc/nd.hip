@@ -26,13 +26,20 @@
 // Attaching the drivers and eliminating the row-input nodes leaves the
 // transfer admittance from the row sources to the sinks, i.e. G'.
 //
-// Levels up to 8 x 8 cells: one workgroup per 8 x 8 block, its waves sharing
-// each level's merges (k_nd_block).  Merges
-// with at most 64 shared nodes: one workgroup per merge eliminates them with
-// the shared rows in registers (k_nd_cut), and k_nd_schur applies the
-// resulting update to the external block on 64 x 64 tiles; the final step
-// with at most 64 row inputs likewise.  Larger merges and final steps run on
-// one workgroup with the shared rows in global memory, eliminated in blocks
+// Levels up to 16 x 16 cells: one workgroup per 16 x 16 region (k_nd_block):
+// each wave builds an 8 x 8 block (its 2 x 2 blocks in registers, the larger
+// merges in its own LDS), then the workgroup merges the four into the
+// region's block; small builds take one workgroup per 8 x 8 block instead
+// (k_nd_block_split).  Merges with 8 to 64 shared nodes: one workgroup per
+// merge eliminates them with the shared rows in registers (k_nd_cut), and
+// the Schur update of the external block runs on 64 x 64 fp64 MFMA tiles of
+// its lower triangle, in the same workgroup for small merges, else in
+// k_nd_schur; the final step with at most 64 row inputs likewise.  Merges
+// with 128 shared nodes: k_nd_cut2 (panels of 256 external columns), then
+// k_nd_schur.  The merge of the two halves of a large grid and its final
+// step: the combined matrix is built dense (k_nd_dense0) and eliminated in
+// stages of 64 pivots (k_nd_cut<64, 2>, k_nd_dschur).  Other sizes run on one
+// workgroup with the shared rows in global memory, eliminated in blocks
 // of 16 (Cholesky of the 16 x 16 pivot block, triangular solve of its rows,
 // rank-16 update of the rest).  All arithmetic is fp64; wire conductances
 // exceed device conductances by about four orders of magnitude, and the
@@ -198,7 +205,7 @@ __device__ __forceinline__ ArrRef nd_ref(const NdArgs& na, int64_t la) {
 // ---------------------------------------------------------------------------
 constexpr int BS = 8;                 // side of the blocks of this kernel
 constexpr int BWAVES = 4;             // waves per workgroup of the block kernel
-constexpr int64_t kSplitBlocks = 2048; // at most this many blocks: one workgroup per block
+constexpr int64_t kSplitBlocks = 256;  // at most this many blocks: one workgroup per block
 constexpr int BLEVELS = 7;  // 1x1 -> 2x1 -> 2x2 -> 4x2 -> 4x4 -> 8x4 -> 8x8 -> 16x8
 // In LDS every cell's or merged block's matrix takes its side squared plus one
 // double: consecutive matrices then start in different banks, so the lanes of
@@ -625,9 +632,9 @@ __device__ __forceinline__ void nd_block(const NdArgs& na) {
   }
 }
 
-// The split form is held to 96 VGPRs (5 waves per SIMD): five workgroups per
-// CU, so 1,280 blocks run in one round.  LDS bounds the other form at two
-// workgroups per CU either way.
+// The split form (small builds: at most kSplitBlocks blocks) is held to 96
+// VGPRs (5 waves per SIMD, five workgroups per CU).  LDS bounds the region
+// form at two workgroups per CU.
 __global__ __launch_bounds__(64 * BWAVES) __attribute__((amdgpu_waves_per_eu(5)))
 void k_nd_block_split(NdArgs na) {
   nd_block<true>(na);
