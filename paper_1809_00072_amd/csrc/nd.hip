@@ -1686,15 +1686,50 @@ __global__ __launch_bounds__(256) void k_nd_dschur(NdArgs na) {
   const double* A = na.dA + la * na.in_stride;
   MfmaTile mt;
   mt.init(tid);
+  // this lane's entries of A behind the tile, loaded first so that they
+  // arrive during the product (an entry outside the tile reads 0 without a
+  // memory access)
+  const __amdgpu_buffer_rsrc_t ra = nd_rsrc(A, (unsigned)(na.dn * na.dld * 8));
+  const int N = na.ms.N;
+  double av[2][2][4];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int x = x0 + mt.row(i, v), y = y0 + mt.col(j);
+        const bool in = OUT == 0 ? (x < E && y < E) : (x < N && y < M);
+        const int row = OUT == 0 ? 64 + x : 64 + M + x;
+        av[i][j][v] = nd_load(ra, in ? 8u * (unsigned)(row * na.dld + 64 + y) : kNdOob, 0);
+      }
+  // Z chunk by chunk (KC64 rows), software pipelined: the next chunk's loads
+  // are in flight while this chunk is multiplied
+  const __amdgpu_buffer_rsrc_t rz = nd_rsrc(z, (unsigned)(64 * E * 8));
+  const int xl = tid & 63;
+  const unsigned ox = x0 + xl < lx ? 8u * (unsigned)(zx0 + xl) : kNdOob;
+  const unsigned oy = y0 + xl < ly ? 8u * (unsigned)(zy0 + xl) : kNdOob;
+  auto load_chunk = [&](int k0, double (&pa)[4], double (&pb)[4]) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int kk = (tid >> 6) + 4 * r;   // uniform per wave
+      const unsigned ko = (unsigned)__builtin_amdgcn_readfirstlane((k0 + kk) * E * 8);
+      pa[r] = nd_load(rz, ox, ko);
+      pb[r] = nd_load(rz, oy, ko);
+    }
+  };
+  double pza[4], pzb[4];
+  load_chunk(0, pza, pzb);
+#pragma unroll 1
   for (int k0 = 0; k0 < 64; k0 += KC64) {
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      const int e = tid + 256 * r, xx = e & 63, kk = e >> 6;
-      const int k = k0 + kk;
-      za[kk * KLD + xx] = (x0 + xx < lx) ? z[(int64_t)k * E + zx0 + xx] : 0.0;
-      zb[kk * KLD + xx] = (y0 + xx < ly) ? z[(int64_t)k * E + zy0 + xx] : 0.0;
+      const int kk = (tid >> 6) + 4 * r;
+      za[kk * KLD + xl] = pza[r];
+      zb[kk * KLD + xl] = pzb[r];
     }
     __syncthreads();
+    if (k0 + KC64 < 64) load_chunk(k0 + KC64, pza, pzb);
     mt.step(za, zb);
     __syncthreads();
   }
@@ -1708,13 +1743,12 @@ __global__ __launch_bounds__(256) void k_nd_dschur(NdArgs na) {
 #pragma unroll
         for (int v = 0; v < 4; ++v) {
           const int x = x0 + mt.row(i, v), y = y0 + mt.col(j);
-          const bool in = x < E && y < E;
-          val[i][j][v] = in ? A[(int64_t)(64 + x) * na.dld + 64 + y] - mt.acc[i][j][v] : 0.0;
-          if (in) B[(int64_t)x * na.dldo + y] = val[i][j][v];
+          val[i][j][v] = av[i][j][v] - mt.acc[i][j][v];
+          if (x < E && y < E) B[(int64_t)x * na.dldo + y] = val[i][j][v];
         }
     if (tx != ty && na.dfull) mt.store_transposed(val, zab, B, na.dldo, x0, y0, E, E, tid);
   } else {
-    const int Np = na.ms.Np, Mp = na.ms.Mp, N = na.ms.N;
+    const int Np = na.ms.Np, Mp = na.ms.Mp;
     float* out = nd_ref(na, la).out;
 #pragma unroll
     for (int i = 0; i < 2; ++i)
@@ -1724,10 +1758,7 @@ __global__ __launch_bounds__(256) void k_nd_dschur(NdArgs na) {
         for (int v = 0; v < 4; ++v) {
           const int j = x0 + mt.row(i, v), k = y0 + mt.col(jb);
           if (j >= Np || k >= Mp) continue;
-          float val = 0.0f;
-          if (j < N && k < M)
-            val = (float)(mt.acc[i][jb][v] - A[(int64_t)(64 + M + j) * na.dld + 64 + k]);
-          out[j * Mp + k] = val;
+          out[j * Mp + k] = (j < N && k < M) ? (float)(mt.acc[i][jb][v] - av[i][jb][v]) : 0.0f;
         }
   }
 }
