@@ -1609,7 +1609,10 @@ __global__ __launch_bounds__(256) void k_nd_gprod(NdArgs na) {
 // (k_nd_dschur).  The last stage writes the merged block (or G').
 // ---------------------------------------------------------------------------
 // Dense combined matrix of one merge (rows in blocks of 16 per workgroup) or
-// of the final step: [row inputs (T) | sources (M) | sinks (T)].
+// of the final step: [row inputs (T) | sources (M) | sinks (T)].  Only the
+// 64 x 64 tiles on and below the diagonal are written: the stages read no
+// others (the cut kernel reads the pivot columns as rows, k_nd_dschur the
+// lower tiles).
 template <bool FINAL>
 __global__ __launch_bounds__(256) void k_nd_dense0(NdArgs na) {
   __shared__ short invt[2][MAXSLOT2];
@@ -1623,29 +1626,31 @@ __global__ __launch_bounds__(256) void k_nd_dense0(NdArgs na) {
     const double* Y = na.buf_in + la * na.in_stride;
     // index -> port of the last level (-1: a source terminal)
     auto port = [&](int i) { return i < T ? i : (i < T + M ? -1 : T + (i - T - M)); };
-    for (int e = threadIdx.x; e < 16 * n; e += 256) {
-      const int x = x0 + e / n, y = e % n;
-      if (x >= n) continue;
-      const int px = port(x), py = port(y);
-      double v = (px >= 0 && py >= 0) ? Y[(int64_t)px * Ein + py] : 0.0;
-      if (x == y && (x < T || px < 0)) v += na.g_d;   // driver at the row input / source
-      if (x < T && py < 0 && x == na.row_off + (y - T)) v -= na.g_d;
-      if (y < T && px < 0 && y == na.row_off + (x - T)) v -= na.g_d;
-      B[(int64_t)x * ld + y] = v;
+    for (int x = x0; x < min(x0 + 16, n); ++x) {
+      const int px = port(x);
+      for (int y = threadIdx.x; y < min(n, (x / 64 + 1) * 64); y += 256) {
+        const int py = port(y);
+        double v = (px >= 0 && py >= 0) ? Y[(int64_t)px * Ein + py] : 0.0;
+        if (x == y && (x < T || px < 0)) v += na.g_d;   // driver at the row input / source
+        if (x < T && py < 0 && x == na.row_off + (y - T)) v -= na.g_d;
+        if (y < T && px < 0 && y == na.row_off + (x - T)) v -= na.g_d;
+        B[(int64_t)x * ld + y] = v;
+      }
     }
   } else {
     const MergeGeom g = merge_geom(na, la);   // one merge per array at this level
     inverse_tables<MAXSLOT2>(na, g, invt, 256);
     const double* Y0 = na.buf_in + la * na.in_stride + (int64_t)g.cm0 * g.Ein * g.Ein;
     const double* Y1 = na.buf_in + la * na.in_stride + (int64_t)g.cm1 * g.Ein * g.Ein;
-    for (int e = threadIdx.x; e < 16 * n; e += 256) {
-      const int x = x0 + e / n, y = e % n;
-      if (x >= n) continue;
-      const int pa0 = invt[0][x], pa1 = invt[1][x], pb0 = invt[0][y], pb1 = invt[1][y];
-      double v = 0.0;
-      if (pa0 >= 0 && pb0 >= 0) v += Y0[pa0 * g.Ein + pb0];
-      if (pa1 >= 0 && pb1 >= 0) v += Y1[pa1 * g.Ein + pb1];
-      B[(int64_t)x * ld + y] = v;
+    for (int x = x0; x < min(x0 + 16, n); ++x) {
+      const int pa0 = invt[0][x], pa1 = invt[1][x];
+      for (int y = threadIdx.x; y < min(n, (x / 64 + 1) * 64); y += 256) {
+        const int pb0 = invt[0][y], pb1 = invt[1][y];
+        double v = 0.0;
+        if (pa0 >= 0 && pb0 >= 0) v += Y0[pa0 * g.Ein + pb0];
+        if (pa1 >= 0 && pb1 >= 0) v += Y1[pa1 * g.Ein + pb1];
+        B[(int64_t)x * ld + y] = v;
+      }
     }
   }
 }
