@@ -73,8 +73,6 @@ struct NdArgs {
   double* dB;            // stage output (row stride dldo) per array
   int dn, dld, dldo;
   int dpanel;            // external columns per workgroup of the cut kernel
-  int dfull;             // the stage writes both triangles (else only the
-                         // lower tiles, which is all the next stage reads)
   int fuse;              // k_nd_cut finishes the Schur update itself (its kFuse
                          // path; the host's schur_fused decides)
   // several layers at once (null tables: the one layer of ms / W / gpt)
@@ -154,6 +152,13 @@ __device__ __forceinline__ double recip(double a) {
   r = fma(r, fma(-a, r, 1.0), r);
   r = fma(r, fma(-a, r, 1.0), r);
   return r;
+}
+
+// A level's merged blocks are symmetric, and the Schur kernels store only
+// their 64 x 64 tiles on and below the diagonal: entry (r, c) of a block
+// with row stride ld is read from its mirror when it lies in a tile above.
+__host__ __device__ __forceinline__ int sym_at(int r, int c, int ld) {
+  return (r >> 6) >= (c >> 6) ? r * ld + c : c * ld + r;
 }
 
 __host__ __device__ constexpr int nports(int i0, int j0, int h, int w, int T) {
@@ -797,7 +802,7 @@ __global__ __launch_bounds__(NTH) void k_nd_merge(NdArgs na) {
       for (int u = 0; u < 8; ++u) {
         const int t = min(t0 + u * NT, (Ein << lgi) - 1);
         const int p = t >> lgi, q = min(t & ((1 << lgi) - 1), Ein - 1);
-        v[u] = Yc[p * Ein + q];
+        v[u] = Yc[sym_at(p, q, Ein)];
       }
 #pragma unroll
       for (int u = 0; u < 8; ++u) {
@@ -837,7 +842,7 @@ __global__ __launch_bounds__(NTH) void k_nd_final(NdArgs na) {
     const int x = e / E, y = e % E;
     double v = 0.0;
     if (x < M && y < M) v = (x == y) ? na.g_d : 0.0;
-    else if (x >= M && y >= M) v = Y[(T + x - M) * Ein + (T + y - M)];
+    else if (x >= M && y >= M) v = Y[sym_at(T + x - M, T + y - M, Ein)];
     ext[e] = v;
   }
   const int lgl = lg2ceil(ldc);
@@ -845,9 +850,9 @@ __global__ __launch_bounds__(NTH) void k_nd_final(NdArgs na) {
     const int i = e >> lgl, y = e & ((1 << lgl) - 1);
     if (y >= ldc) continue;
     double v;
-    if (y < c) v = Y[i * Ein + y] + (i == y ? na.g_d : 0.0);
+    if (y < c) v = Y[sym_at(i, y, Ein)] + (i == y ? na.g_d : 0.0);
     else if (y < c + M) v = (i == na.row_off + (y - c)) ? -na.g_d : 0.0;
-    else v = Y[i * Ein + T + (y - c - M)];
+    else v = Y[sym_at(i, T + (y - c - M), Ein)];
     cut[i * ldc + y] = v;
   }
   __syncthreads();
@@ -903,6 +908,7 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t nd_rsrc(const void* p, unsigne
 // A per-lane buffer offset beyond every level buffer's range: the load returns
 // 0 and touches no memory (the range check covers the VGPR offset).
 constexpr unsigned kNdOob = 0x80000000u;
+
 
 __device__ __forceinline__ double nd_load(__amdgpu_buffer_rsrc_t r, unsigned voff, unsigned soff) {
   return __builtin_bit_cast(double, __builtin_amdgcn_raw_buffer_load_b64(r, voff, soff, 0));
@@ -1026,35 +1032,6 @@ struct MfmaTile {
   // tile-local coordinates of this lane's element v of block (i, j)
   __device__ __forceinline__ int row(int i, int v) const { return wr * 32 + i * 16 + lr + 4 * v; }
   __device__ __forceinline__ int col(int j) const { return wc * 32 + j * 16 + lc; }
-  // Writes the transpose of the tile's values val (this lane's 16) to
-  // out[(y0 + y) * ld + x0 + x] for x0 + x < xlim, y0 + y < ylim, through
-  // `t` (at least 32 x TT doubles of LDS, free on entry; every thread of
-  // the workgroup calls this), half the rows per pass so that each store
-  // writes 32 consecutive doubles of a row.
-  __device__ __forceinline__ void store_transposed(const double (&val)[2][2][4], double* t,
-                                                   double* out, int64_t ld, int x0, int y0,
-                                                   int xlim, int ylim, int tid) const {
-    constexpr int TT = 65;
-#pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      __syncthreads();
-      if (wr == h) {
-#pragma unroll
-        for (int i = 0; i < 2; ++i)
-#pragma unroll
-          for (int j = 0; j < 2; ++j)
-#pragma unroll
-            for (int v = 0; v < 4; ++v) t[(i * 16 + lr + 4 * v) * TT + col(j)] = val[i][j][v];
-      }
-      __syncthreads();
-#pragma unroll
-      for (int k = 0; k < 8; ++k) {
-        const int e = tid + 256 * k, y = e >> 5, xl = e & 31;
-        const int x = x0 + 32 * h + xl;
-        if (x < xlim && y0 + y < ylim) out[(int64_t)(y0 + y) * ld + x] = t[xl * TT + y];
-      }
-    }
-  }
 };
 
 // Workgroups are dispatched to the 8 XCDs in turn, each with its own L2: this
@@ -1221,10 +1198,10 @@ __global__ __launch_bounds__(512) void k_nd_cut(NdArgs na) {
     const bool useY = y < C || (y >= C + M && y < ncol);
     const int yc = y < C ? y : (useY ? T + (y - C - M) : 0);
     const int srow = (y >= C && y < C + M) ? na.row_off + (y - C) : -1;   // driver of row
-    const __amdgpu_buffer_rsrc_t ry = nd_rsrc(Y, (unsigned)(C * Ein * 8));
+    const __amdgpu_buffer_rsrc_t ry = nd_rsrc(Y, (unsigned)(2 * T * Ein * 8));
 #pragma unroll
     for (int x = 0; x < C; ++x) {
-      const double yv = nd_load(ry, 8u * (unsigned)yc, 8u * (unsigned)(x * Ein));
+      const double yv = nd_load(ry, 8u * (unsigned)sym_at(x, yc, Ein), 0);
       const double v = (useY ? yv : 0.0) + (x == y ? na.g_d : 0.0) - (x == srow ? na.g_d : 0.0);
       U[x] = v;
       if ((x & 31) == 31) {   // 32 loads in flight per round trip
@@ -1248,19 +1225,18 @@ __global__ __launch_bounds__(512) void k_nd_cut(NdArgs na) {
     const int pb0 = y < ncol ? invt[0][y] : -1, pb1 = y < ncol ? invt[1][y] : -1;
     const unsigned cb = (unsigned)(g.Ein * g.Ein * 8);
     const __amdgpu_buffer_rsrc_t r0 = nd_rsrc(Y0, cb), r1 = nd_rsrc(Y1, cb);
-    const unsigned q0 = pb0 >= 0 ? 8u * (unsigned)pb0 : kNdOob;
-    const unsigned q1 = pb1 >= 0 ? 8u * (unsigned)pb1 : kNdOob;
     const lds_i16* iv = opaque_lds<lds_i16>(&invt[0][0]);
-    // the row's port is uniform (a scalar offset), the column's fixed per
-    // lane; an entry without a port takes the out-of-range lane offset, so it
-    // reads 0 without a memory access, and every load of a chunk stays in
-    // flight together
+    // the row's port is uniform, the column's fixed per lane; an entry
+    // without a port takes the out-of-range offset, so it reads 0 without a
+    // memory access, and every load of a chunk stays in flight together
 #pragma unroll
     for (int x = 0; x < C; ++x) {
       const int pa0 = __builtin_amdgcn_readfirstlane(iv[x]);
       const int pa1 = __builtin_amdgcn_readfirstlane(iv[MAXSLOT + x]);
-      const double v0 = nd_load(r0, pa0 >= 0 ? q0 : kNdOob, 8u * (unsigned)(max(pa0, 0) * g.Ein));
-      const double v1 = nd_load(r1, pa1 >= 0 ? q1 : kNdOob, 8u * (unsigned)(max(pa1, 0) * g.Ein));
+      const double v0 = nd_load(r0, (pa0 >= 0 && pb0 >= 0) ? 8u * (unsigned)sym_at(pa0, pb0, g.Ein)
+                                                           : kNdOob, 0);
+      const double v1 = nd_load(r1, (pa1 >= 0 && pb1 >= 0) ? 8u * (unsigned)sym_at(pa1, pb1, g.Ein)
+                                                           : kNdOob, 0);
       U[x] = v0 + v1;
       // 16 rows (32 loads) in flight per round trip
       if ((x & 15) == 15) {
@@ -1319,7 +1295,7 @@ __global__ __launch_bounds__(512) void k_nd_cut(NdArgs na) {
       const __amdgpu_buffer_rsrc_t r0f = nd_rsrc(Y0, cbf), r1f = nd_rsrc(Y1, cbf);
       const int nt = (E + 63) / 64;
       // ext = V - Z^T Z on the 64 x 64 tiles of its lower triangle (ext is
-      // symmetric: each tile also writes its mirror image); the children's
+      // symmetric; readers take the mirror of an entry above); the children's
       // entries of a tile are loaded before its product, so that they arrive
       // during it
 #pragma unroll 1
@@ -1341,9 +1317,9 @@ __global__ __launch_bounds__(512) void k_nd_cut(NdArgs na) {
               const int x = min(x0 + mt.row(i, v), E - 1);
               const int pa0 = invt[0][C + x], pa1 = invt[1][C + x];
               const double v0 = nd_load(r0f, (pa0 >= 0 && pb0 >= 0)
-                                                 ? 8u * (unsigned)(pa0 * g.Ein + pb0) : kNdOob, 0);
+                                                 ? 8u * (unsigned)sym_at(pa0, pb0, g.Ein) : kNdOob, 0);
               const double v1 = nd_load(r1f, (pa1 >= 0 && pb1 >= 0)
-                                                 ? 8u * (unsigned)(pa1 * g.Ein + pb1) : kNdOob, 0);
+                                                 ? 8u * (unsigned)sym_at(pa1, pb1, g.Ein) : kNdOob, 0);
               vv[i][j][v] = v0 + v1;
             }
         }
@@ -1356,10 +1332,7 @@ __global__ __launch_bounds__(512) void k_nd_cut(NdArgs na) {
             for (int v = 0; v < 4; ++v) {
               const int x = x0 + mt.row(i, v), yy = y0 + mt.col(j);
               if (x < E && yy < E) {
-                const double e = vv[i][j][v] - mt.acc[i][j][v];
-                ext[x * Emax + yy] = e;
-                // the mirror: lanes lr = 0 .. 3 hold consecutive x
-                if (tx != ty) ext[yy * Emax + x] = e;
+                ext[x * Emax + yy] = vv[i][j][v] - mt.acc[i][j][v];
               }
             }
       }
@@ -1467,11 +1440,11 @@ __global__ __launch_bounds__(2 * CP2) void k_nd_cut2(NdArgs na) {
     const bool useY = yl < C2 || (e >= M && e < E);
     const int yc = yl < C2 ? yl : (useY ? T + (e - M) : 0);
     const int srow = (e >= 0 && e < M) ? na.row_off + e : -1;
-    const __amdgpu_buffer_rsrc_t ry = nd_rsrc(Y, (unsigned)(C2 * Ein * 8));
+    const __amdgpu_buffer_rsrc_t ry = nd_rsrc(Y, (unsigned)(2 * T * Ein * 8));
 #pragma unroll
     for (int i = 0; i < 64; ++i) {
       const int x = 64 * rg + i;
-      const double yv = nd_load(ry, 8u * (unsigned)yc, 8u * (unsigned)(x * Ein));
+      const double yv = nd_load(ry, 8u * (unsigned)sym_at(x, yc, Ein), 0);
       U[i] = (useY ? yv : 0.0) + (x == yl ? na.g_d : 0.0) - (x == srow ? na.g_d : 0.0);
       if ((i & 7) == 7) pin8(U, i - 7);
     }
@@ -1492,15 +1465,15 @@ __global__ __launch_bounds__(2 * CP2) void k_nd_cut2(NdArgs na) {
     const int pb0 = slot >= 0 ? invt[0][slot] : -1, pb1 = slot >= 0 ? invt[1][slot] : -1;
     const unsigned cb = (unsigned)(g.Ein * g.Ein * 8);
     const __amdgpu_buffer_rsrc_t r0 = nd_rsrc(Y0, cb), r1 = nd_rsrc(Y1, cb);
-    const unsigned q0 = pb0 >= 0 ? 8u * (unsigned)pb0 : kNdOob;
-    const unsigned q1 = pb1 >= 0 ? 8u * (unsigned)pb1 : kNdOob;
 #pragma unroll
     for (int i = 0; i < 64; ++i) {
       const int x = 64 * rg + i;
       const int pa0 = __builtin_amdgcn_readfirstlane(invt[0][x]);
       const int pa1 = __builtin_amdgcn_readfirstlane(invt[1][x]);
-      const double v0 = nd_load(r0, pa0 >= 0 ? q0 : kNdOob, 8u * (unsigned)(max(pa0, 0) * g.Ein));
-      const double v1 = nd_load(r1, pa1 >= 0 ? q1 : kNdOob, 8u * (unsigned)(max(pa1, 0) * g.Ein));
+      const double v0 = nd_load(r0, (pa0 >= 0 && pb0 >= 0) ? 8u * (unsigned)sym_at(pa0, pb0, g.Ein)
+                                                           : kNdOob, 0);
+      const double v1 = nd_load(r1, (pa1 >= 0 && pb1 >= 0) ? 8u * (unsigned)sym_at(pa1, pb1, g.Ein)
+                                                           : kNdOob, 0);
       U[i] = v0 + v1;
       if ((i & 7) == 7) pin8(U, i - 7);
     }
@@ -1630,7 +1603,7 @@ __global__ __launch_bounds__(256) void k_nd_dense0(NdArgs na) {
       const int px = port(x);
       for (int y = threadIdx.x; y < min(n, (x / 64 + 1) * 64); y += 256) {
         const int py = port(y);
-        double v = (px >= 0 && py >= 0) ? Y[(int64_t)px * Ein + py] : 0.0;
+        double v = (px >= 0 && py >= 0) ? Y[sym_at(px, py, Ein)] : 0.0;
         if (x == y && (x < T || px < 0)) v += na.g_d;   // driver at the row input / source
         if (x < T && py < 0 && x == na.row_off + (y - T)) v -= na.g_d;
         if (y < T && px < 0 && y == na.row_off + (x - T)) v -= na.g_d;
@@ -1647,8 +1620,8 @@ __global__ __launch_bounds__(256) void k_nd_dense0(NdArgs na) {
       for (int y = threadIdx.x; y < min(n, (x / 64 + 1) * 64); y += 256) {
         const int pb0 = invt[0][y], pb1 = invt[1][y];
         double v = 0.0;
-        if (pa0 >= 0 && pb0 >= 0) v += Y0[pa0 * g.Ein + pb0];
-        if (pa1 >= 0 && pb1 >= 0) v += Y1[pa1 * g.Ein + pb1];
+        if (pa0 >= 0 && pb0 >= 0) v += Y0[sym_at(pa0, pb0, g.Ein)];
+        if (pa1 >= 0 && pb1 >= 0) v += Y1[sym_at(pa1, pb1, g.Ein)];
         B[(int64_t)x * ld + y] = v;
       }
     }
@@ -1659,9 +1632,8 @@ __global__ __launch_bounds__(256) void k_nd_dense0(NdArgs na) {
 // of the stage's pivots, OUT 0 writes A[64 + x][64 + y] - (Z^T Z)[x][y] for
 // x, y < E to dB (row stride dldo); OUT 1 writes G' = (Z^T Z - A) over the
 // sink x source block (A: [sources (M) | sinks (T)] after the pivots).
-// OUT 0 is symmetric: a workgroup computes one tile of the lower triangle
-// (tx >= ty) and writes it and, when the stage's output is the merged block
-// (dfull), its mirror image.
+// OUT 0 is symmetric: a workgroup computes and writes one tile of the lower
+// triangle (tx >= ty); the tiles above are never read.
 template <int OUT>
 __global__ __launch_bounds__(256) void k_nd_dschur(NdArgs na) {
   __shared__ __attribute__((aligned(16))) double zab[2 * KC64 * KLD];
@@ -1740,7 +1712,6 @@ __global__ __launch_bounds__(256) void k_nd_dschur(NdArgs na) {
   }
   if constexpr (OUT == 0) {
     double* B = na.dB + la * na.out_stride;
-    double val[2][2][4];
 #pragma unroll
     for (int i = 0; i < 2; ++i)
 #pragma unroll
@@ -1748,10 +1719,9 @@ __global__ __launch_bounds__(256) void k_nd_dschur(NdArgs na) {
 #pragma unroll
         for (int v = 0; v < 4; ++v) {
           const int x = x0 + mt.row(i, v), y = y0 + mt.col(j);
-          val[i][j][v] = av[i][j][v] - mt.acc[i][j][v];
-          if (x < E && y < E) B[(int64_t)x * na.dldo + y] = val[i][j][v];
+          if (x < E && y < E) B[(int64_t)x * na.dldo + y] = av[i][j][v] - mt.acc[i][j][v];
         }
-    if (tx != ty && na.dfull) mt.store_transposed(val, zab, B, na.dldo, x0, y0, E, E, tid);
+
   } else {
     const int Np = na.ms.Np, Mp = na.ms.Mp;
     float* out = nd_ref(na, la).out;
@@ -1769,8 +1739,9 @@ __global__ __launch_bounds__(256) void k_nd_dschur(NdArgs na) {
 }
 
 // ext = V - Z^T Z of one merge (V: the children's external-external
-// entries).  ext is symmetric, so a workgroup computes one 64 x 64 tile of
-// the lower triangle (tx >= ty) and writes it and its mirror image.
+// entries).  ext is symmetric, so a workgroup computes and writes one 64 x 64
+// tile of the lower triangle (tx >= ty); readers take the mirror of an entry
+// above.
 // Five waves per SIMD (96 VGPRs): its gathers need many waves in flight.
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(5))) void k_nd_schur(NdArgs na) {
   __shared__ short invt[2][MAXSLOT2];
@@ -1835,7 +1806,6 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(5))) void k
   const unsigned cb = (unsigned)(g.Ein * g.Ein * 8);
   const __amdgpu_buffer_rsrc_t r0 = nd_rsrc(Y0, cb), r1 = nd_rsrc(Y1, cb);
   double* ext = na.buf_out + g.la * na.out_stride + (int64_t)g.m * Emax * Emax;
-  double val[2][2][4];
 #pragma unroll
   for (int j = 0; j < 2; ++j) {
     const int y = y0 + mt.col(j);
@@ -1849,9 +1819,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(5))) void k
         const int x = min(x0 + mt.row(i, v), E - 1);
         const int pa0 = invt[0][c + x], pa1 = invt[1][c + x];
         // an entry that a child does not hold reads 0 without a memory access
-        const double v0 = nd_load(r0, (pa0 >= 0 && pb0 >= 0) ? 8u * (unsigned)(pa0 * g.Ein + pb0)
+        const double v0 = nd_load(r0, (pa0 >= 0 && pb0 >= 0) ? 8u * (unsigned)sym_at(pa0, pb0, g.Ein)
                                                              : kNdOob, 0);
-        const double v1 = nd_load(r1, (pa1 >= 0 && pb1 >= 0) ? 8u * (unsigned)(pa1 * g.Ein + pb1)
+        const double v1 = nd_load(r1, (pa1 >= 0 && pb1 >= 0) ? 8u * (unsigned)sym_at(pa1, pb1, g.Ein)
                                                              : kNdOob, 0);
         vv[i][v] = v0 + v1;
       }
@@ -1860,11 +1830,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(5))) void k
 #pragma unroll
       for (int v = 0; v < 4; ++v) {
         const int x = x0 + mt.row(i, v);
-        val[i][j][v] = vv[i][v] - mt.acc[i][j][v];
-        if (x < E && y < E) ext[x * Emax + y] = val[i][j][v];
+        if (x < E && y < E) ext[x * Emax + y] = vv[i][v] - mt.acc[i][j][v];
       }
   }
-  if (tx != ty) mt.store_transposed(val, zab, ext, Emax, x0, y0, E, E, tid);
 }
 
 }  // namespace
@@ -1958,7 +1926,6 @@ static void launch_staged(NdArgs na, int64_t n, int c, int n0, double* a, double
     na.dld = n0;
     na.dldo = last ? ldo : n0;
     na.dpanel = PANEL;
-    na.dfull = last ? 1 : 0;
     const int ext = na.dn - 64;
     const unsigned npan = (unsigned)((ext + PANEL - 1) / PANEL);
     const unsigned nthr = (unsigned)((64 + std::min(PANEL, ext) + 63) / 64 * 64);
