@@ -73,6 +73,8 @@ struct NdArgs {
   double* dB;            // stage output (row stride dldo) per array
   int dn, dld, dldo;
   int dpanel;            // external columns per workgroup of the cut kernel
+  int npan;              // workgroups (column panels of dpanel) per merge of the
+                         // cut kernel's merge mode (0 or 1: one, all columns)
   int fuse;              // k_nd_cut finishes the Schur update itself (its kFuse
                          // path; the host's schur_fused decides)
   // several layers at once (null tables: the one layer of ms / W / gpt)
@@ -1212,17 +1214,22 @@ __global__ __launch_bounds__(512) void k_nd_cut(NdArgs na) {
       }
     }
   } else {
-    g = merge_geom(na, blockIdx.x);
+    // with several panels per merge, workgroup pn takes the cut columns and
+    // externals [pn dpanel, (pn + 1) dpanel)
+    const int npan = max(na.npan, 1), pn = (int)(blockIdx.x % npan);
+    g = merge_geom(na, blockIdx.x / npan);
     inverse_tables<MAXSLOT>(na, g, invt, blockDim.x);
     la = g.la;
     E = g.E;
     Emax = g.Emax;
     zld = Emax;
-    ncol = C + E;
+    ebase = npan > 1 ? pn * na.dpanel : 0;
+    ncol = C + (npan > 1 ? max(0, min(na.dpanel, E - ebase)) : E);
     z = na.scratch + la * na.scr_stride + (int64_t)g.m * g.Emax * C;
     Y0 = na.buf_in + la * na.in_stride + (int64_t)g.cm0 * g.Ein * g.Ein;
     Y1 = na.buf_in + la * na.in_stride + (int64_t)g.cm1 * g.Ein * g.Ein;
-    const int pb0 = y < ncol ? invt[0][y] : -1, pb1 = y < ncol ? invt[1][y] : -1;
+    const int slot = y < C ? y : (y < ncol ? C + ebase + (y - C) : -1);
+    const int pb0 = slot >= 0 ? invt[0][slot] : -1, pb1 = slot >= 0 ? invt[1][slot] : -1;
     const unsigned cb = (unsigned)(g.Ein * g.Ein * 8);
     const __amdgpu_buffer_rsrc_t r0 = nd_rsrc(Y0, cb), r1 = nd_rsrc(Y1, cb);
     const lds_i16* iv = opaque_lds<lds_i16>(&invt[0][0]);
@@ -2015,9 +2022,17 @@ hipError_t launch_nd_build(const MapScalars& ms, const float* W, float* gpt, int
         // a fused Schur update runs in the merge's own workgroup; with fewer
         // merges than half the CUs its tiles are spread over k_nd_schur's
         // workgroups instead (the 64 x 64 conv layer: 229 -> 217 us)
-        const bool fused = schur_fused(c, emax) && (int64_t)n * nmerge >= 128;
+        const bool few = (int64_t)n * nmerge < 128;
+        const bool fused = schur_fused(c, emax) && !few;
         na.fuse = fused ? 1 : 0;
-        launch_cut<false>(na, grid, c, c + e_layout, fused, s);
+        // few merges: each one's columns in panels of 64 externals over
+        // several workgroups (the cut block eliminated in each)
+        constexpr int kPanel = 64;
+        na.npan = few ? (e_layout + kPanel - 1) / kPanel : 1;
+        na.dpanel = kPanel;
+        launch_cut<false>(na, dim3((unsigned)(n * nmerge * na.npan)), c,
+                          c + (few ? std::min(kPanel, e_layout) : e_layout), fused, s);
+        na.npan = 1;
         if (!fused) {
           const int nt = (emax + 63) / 64;
           hipLaunchKernelGGL(k_nd_schur, dim3((unsigned)(n * nmerge * (nt * (nt + 1) / 2))),
