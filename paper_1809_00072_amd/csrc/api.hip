@@ -702,7 +702,7 @@ struct BatchState {
   std::vector<NdBatchLayer> h_layers;
   std::vector<int2> h_ent;
 };
-constexpr size_t kBatchBudget = (size_t)16 << 30;
+constexpr size_t kBatchBudget = (size_t)24 << 30;
 BatchState g_batch[kMaxDevices];
 std::mutex g_batch_mu;
 
