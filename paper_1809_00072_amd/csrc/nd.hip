@@ -75,6 +75,10 @@ struct NdArgs {
   int dpanel;            // external columns per workgroup of the cut kernel
   int npan;              // workgroups (column panels of dpanel) per merge of the
                          // cut kernel's merge mode (0 or 1: one, all columns)
+  int dead[4];           // staged path: index ranges [dead[0], dead[1]) and
+                         // [dead[2], dead[3]) of the combined matrix whose
+                         // mutual entries nothing reads (sinks x sinks,
+                         // sources x sources): neither written nor updated
   int fuse;              // k_nd_cut finishes the Schur update itself (its kFuse
                          // path; the host's schur_fused decides)
   // several layers at once (null tables: the one layer of ms / W / gpt)
@@ -1588,6 +1592,18 @@ __global__ __launch_bounds__(256) void k_nd_gprod(NdArgs na) {
 // (mode 2) over column panels followed by the Schur update of the rest
 // (k_nd_dschur).  The last stage writes the merged block (or G').
 // ---------------------------------------------------------------------------
+// Entry (x, y) of a staged combined matrix lies in one of its dead ranges.
+__device__ __forceinline__ bool dead_pair(const NdArgs& na, int x, int y) {
+  return (x >= na.dead[0] && x < na.dead[1] && y >= na.dead[0] && y < na.dead[1]) ||
+         (x >= na.dead[2] && x < na.dead[3] && y >= na.dead[2] && y < na.dead[3]);
+}
+
+// The whole 64 x 64 tile at (x, y) lies in one dead range (the ranges need
+// not be tile-aligned: M is any row count).
+__device__ __forceinline__ bool dead_tile(const NdArgs& na, int x, int y) {
+  return dead_pair(na, x, y) && dead_pair(na, x + 63, y + 63) && dead_pair(na, x, y + 63);
+}
+
 // Dense combined matrix of one merge (rows in blocks of 16 per workgroup) or
 // of the final step: [row inputs (T) | sources (M) | sinks (T)].  Only the
 // 64 x 64 tiles on and below the diagonal are written: the stages read no
@@ -1609,6 +1625,7 @@ __global__ __launch_bounds__(256) void k_nd_dense0(NdArgs na) {
     for (int x = x0; x < min(x0 + 16, n); ++x) {
       const int px = port(x);
       for (int y = threadIdx.x; y < min(n, (x / 64 + 1) * 64); y += 256) {
+        if (dead_pair(na, x, y)) continue;
         const int py = port(y);
         double v = (px >= 0 && py >= 0) ? Y[sym_at(px, py, Ein)] : 0.0;
         if (x == y && (x < T || px < 0)) v += na.g_d;   // driver at the row input / source
@@ -1625,6 +1642,7 @@ __global__ __launch_bounds__(256) void k_nd_dense0(NdArgs na) {
     for (int x = x0; x < min(x0 + 16, n); ++x) {
       const int pa0 = invt[0][x], pa1 = invt[1][x];
       for (int y = threadIdx.x; y < min(n, (x / 64 + 1) * 64); y += 256) {
+        if (dead_pair(na, x, y)) continue;
         const int pb0 = invt[0][y], pb1 = invt[1][y];
         double v = 0.0;
         if (pa0 >= 0 && pb0 >= 0) v += Y0[sym_at(pa0, pb0, g.Ein)];
@@ -1663,6 +1681,9 @@ __global__ __launch_bounds__(256) void k_nd_dschur(NdArgs na) {
     ty = tt % nty;
   }
   const int x0 = tx * 64, y0 = ty * 64;
+  // a tile wholly in a dead range (combined index = stage index + dld - dn
+  // + 64) is neither read nor written
+  if (OUT == 0 && dead_tile(na, na.dld - na.dn + 64 + x0, na.dld - na.dn + 64 + y0)) return;
   // rows of Z and of A behind this tile's x and y
   const int zx0 = OUT == 0 ? x0 : M + x0, zy0 = y0;
   const int lx = OUT == 0 ? E : min(na.ms.N, na.T), ly = OUT == 0 ? E : M;   // valid x, y
@@ -1919,6 +1940,21 @@ template <bool FINAL>
 static void launch_staged(NdArgs na, int64_t n, int c, int n0, double* a, double* b, int ldo,
                           hipStream_t s) {
   constexpr int PANEL = 448;   // external columns per cut workgroup (with 64 pivots: 512 lanes)
+  // Entries between two sinks, or between two sources, are never read: G' is
+  // the sink x source block, and sinks and sources are never pivots.  The
+  // final step: [row inputs (T) | sources (M) | sinks (T)]; the merge of the
+  // whole grid: [cut (c) | L (T) | B (T)], B the sinks.
+  const int T = na.T;
+  if (FINAL) {
+    na.dead[0] = T;
+    na.dead[1] = T + na.ms.M;
+    na.dead[2] = T + na.ms.M;
+    na.dead[3] = 2 * T + na.ms.M;
+  } else {
+    na.dead[0] = c + T;
+    na.dead[1] = c + 2 * T;
+    na.dead[2] = na.dead[3] = 0;
+  }
   na.dB = a;
   na.dn = n0;
   na.dldo = n0;
