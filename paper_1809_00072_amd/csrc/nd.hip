@@ -509,6 +509,8 @@ __device__ __forceinline__ void block2x2(const MapScalars& ms, const float* W, d
 
 __device__ void region_merge16(int T, int RI, int RJ, const double* ch, double* dst,
                                double* scr);
+__device__ void block_l5_mfma(int T, int I0, int J0, const short* tab, const double* in,
+                              double* out, int lane);
 
 // SPLIT (few blocks, a latency-bound build): one 8 x 8 block per workgroup,
 // its waves sharing each level, the 8 x 8 block to the level buffer.
@@ -631,7 +633,7 @@ __device__ __forceinline__ void nd_block(const NdArgs& na) {
     // (children BA apart: the waves' A buffers) to the B buffers (row stride
     // 48); their 16 x 16 merge (the A buffers as scratch) to merged block
     // (region row, region column) of the 16 x 16 level
-    block_level<5, 8, 4, false, false, false>(T, I0, J0, tab, B, A, prow[wv], lane, wv);
+    block_l5_mfma(T, I0, J0, tab, B, A, lane);
     __syncthreads();
     const int RI = I0 - (wv >> 1) * BS, RJ = J0 - (wv & 1) * BS;
     block_level<6, 8, 8, true, false, false, 2 * BS, BA, true>(T, RI, RJ, tab, &bufA[0][0],
@@ -1056,6 +1058,96 @@ __device__ __forceinline__ void tri_tile(int tt, int* tx, int* ty) {
   while (x * (x + 1) / 2 > tt) --x;
   *tx = x;
   *ty = tt - x * (x + 1) / 2;
+}
+
+// Level 8 x 4 -> 8 x 8 of one wave's block (the region kernel) with its
+// Schur update on the fp64 matrix cores.  Lane y holds column y of the
+// merge's 8 cut rows only and eliminates them (pivot k's column by lane reads
+// from lane k); Z (the eliminated rows scaled by D^-1/2, 8 x 32, zero past
+// the block's ports) goes to `out` as scratch, and the merged block
+// V - Z^T Z is four 16 x 16 tiles (lane l: rows 16 bi + l / 16 + 4 v,
+// column 16 bj + l % 16), written to `out` (row stride 32) once Z is read.
+__device__ void block_l5_mfma(int T, int I0, int J0, const short* tab, const double* in,
+                              double* out, int lane) {
+  constexpr int L = 5, C = 8, EIN = 24, ZS = 36;
+  const bool rn = J0 + 8 < T, tn = I0 > 0;
+  const int E = 8 + (rn ? 8 : 0) + (tn ? 8 : 0) + 8;   // ports of the merged block
+  const short* t0 = tab + (((L * 4) + (rn ? 2 : 0) + (tn ? 1 : 0)) * 2) * 64;
+  const short* t1 = t0 + 64;
+  const double* c0 = in;                   // left child
+  const double* c1 = in + lds_mat(EIN);    // right child
+  const int s0 = t0[lane], s1 = t1[lane];
+  double U[C];
+#pragma unroll
+  for (int x = 0; x < C; ++x) {
+    const int r0 = t0[x], r1 = t1[x];
+    const double a = c0[max(r0, 0) * EIN + max(s0, 0)];
+    const double b = c1[max(r1, 0) * EIN + max(s1, 0)];
+    U[x] = ((r0 >= 0 && s0 >= 0) ? a : 0.0) + ((r1 >= 0 && s1 >= 0) ? b : 0.0);
+  }
+  double sq[C];
+#pragma unroll
+  for (int k = 0; k < C; ++k) {
+    const double piv = readlane_d(U[k], k);
+    sq[k] = 1.0 / sqrt(piv);
+    const double t = U[k] * recip(piv);
+#pragma unroll
+    for (int x = k + 1; x < C; ++x) U[x] = fma(-readlane_d(U[x], k), t, U[x]);
+  }
+  double* z = out;
+  if (lane >= C && lane < C + 32) {
+    const int e = lane - C;
+#pragma unroll
+    for (int k = 0; k < C; ++k) z[k * ZS + e] = e < E ? U[k] * sq[k] : 0.0;
+  }
+  wave_sync();
+  const int lr = lane >> 4, lc = lane & 15;
+  double vv[2][2][4];
+#pragma unroll
+  for (int bj = 0; bj < 2; ++bj) {
+    const int yy = 16 * bj + lc;
+    const int pb0 = t0[C + yy], pb1 = t1[C + yy];
+#pragma unroll
+    for (int bi = 0; bi < 2; ++bi)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int xx = 16 * bi + lr + 4 * v;
+        const int pa0 = t0[C + xx], pa1 = t1[C + xx];
+        const double a = c0[max(pa0, 0) * EIN + max(pb0, 0)];
+        const double b = c1[max(pa1, 0) * EIN + max(pb1, 0)];
+        vv[bi][bj][v] = ((pa0 >= 0 && pb0 >= 0) ? a : 0.0) + ((pa1 >= 0 && pb1 >= 0) ? b : 0.0);
+      }
+  }
+  f64x4 acc[2][2];
+#pragma unroll
+  for (int bi = 0; bi < 2; ++bi)
+#pragma unroll
+    for (int bj = 0; bj < 2; ++bj) acc[bi][bj] = f64x4{0.0, 0.0, 0.0, 0.0};
+#pragma unroll
+  for (int k4 = 0; k4 < C; k4 += 4) {
+    double a[2], b[2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      a[i] = z[(k4 + lr) * ZS + 16 * i + lc];
+      b[i] = a[i];
+    }
+#pragma unroll
+    for (int bi = 0; bi < 2; ++bi)
+#pragma unroll
+      for (int bj = 0; bj < 2; ++bj)
+        acc[bi][bj] = __builtin_amdgcn_mfma_f64_16x16x4f64(a[bi], b[bj], acc[bi][bj], 0, 0, 0);
+  }
+  wave_sync();   // Z read before the block overwrites it
+#pragma unroll
+  for (int bi = 0; bi < 2; ++bi)
+#pragma unroll
+    for (int bj = 0; bj < 2; ++bj)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int xx = 16 * bi + lr + 4 * v, yy = 16 * bj + lc;
+        if (xx < E && yy < E) out[xx * 32 + yy] = vv[bi][bj][v] - acc[bi][bj][v];
+      }
+  wave_sync();
 }
 
 // The 16 x 16 merge of a region's two 16 x 8 halves (left, right) at (RI, RJ):
