@@ -509,8 +509,10 @@ __device__ __forceinline__ void block2x2(const MapScalars& ms, const float* W, d
 
 __device__ void region_merge16(int T, int RI, int RJ, const double* ch, double* dst,
                                double* scr);
-__device__ void block_l5_mfma(int T, int I0, int J0, const short* tab, const double* in,
-                              double* out, int lane);
+template <int L, int H, int W, bool VERT, int NB>
+__device__ __forceinline__ void merge_mfma(int T, int i0, int j0, const short* tab,
+                                           const double* c0, const double* c1, double* out,
+                                           int lane);
 
 // SPLIT (few blocks, a latency-bound build): one 8 x 8 block per workgroup,
 // its waves sharing each level, the 8 x 8 block to the level buffer.
@@ -633,11 +635,15 @@ __device__ __forceinline__ void nd_block(const NdArgs& na) {
     // (children BA apart: the waves' A buffers) to the B buffers (row stride
     // 48); their 16 x 16 merge (the A buffers as scratch) to merged block
     // (region row, region column) of the 16 x 16 level
-    block_l5_mfma(T, I0, J0, tab, B, A, lane);
+    merge_mfma<5, 8, 4, false, 2>(T, I0, J0, tab, B, B + lds_mat(24), A, lane);
     __syncthreads();
     const int RI = I0 - (wv >> 1) * BS, RJ = J0 - (wv & 1) * BS;
-    block_level<6, 8, 8, true, false, false, 2 * BS, BA, true>(T, RI, RJ, tab, &bufA[0][0],
-                                                              &bufB[0][0], prow[wv], lane, wv);
+    if (wv < 2) {   // wave m: the pair of column m (children: the A buffers of waves m, 2 + m)
+      const double* ca = &bufA[0][0];
+      merge_mfma<6, 8, 8, true, 3>(T, RI, RJ + wv * BS, tab, ca + wv * BA, ca + (2 + wv) * BA,
+                                   &bufB[0][0] + wv * lds_mat(48), lane);
+    }
+    __syncthreads();
     constexpr int E16 = 8 * BS;   // ports of an interior 16 x 16 block
     double* dst = na.buf_out + la * na.out_stride +
                   ((int64_t)(RI / (2 * BS)) * (T / (2 * BS)) + RJ / (2 * BS)) * E16 * E16;
@@ -1060,22 +1066,29 @@ __device__ __forceinline__ void tri_tile(int tt, int* tx, int* ty) {
   *ty = tt - x * (x + 1) / 2;
 }
 
-// Level 8 x 4 -> 8 x 8 of one wave's block (the region kernel) with its
-// Schur update on the fp64 matrix cores.  Lane y holds column y of the
-// merge's 8 cut rows only and eliminates them (pivot k's column by lane reads
-// from lane k); Z (the eliminated rows scaled by D^-1/2, 8 x 32, zero past
-// the block's ports) goes to `out` as scratch, and the merged block
-// V - Z^T Z is four 16 x 16 tiles (lane l: rows 16 bi + l / 16 + 4 v,
-// column 16 bj + l % 16), written to `out` (row stride 32) once Z is read.
-__device__ void block_l5_mfma(int T, int I0, int J0, const short* tab, const double* in,
-                              double* out, int lane) {
-  constexpr int L = 5, C = 8, EIN = 24, ZS = 36;
-  const bool rn = J0 + 8 < T, tn = I0 > 0;
-  const int E = 8 + (rn ? 8 : 0) + (tn ? 8 : 0) + 8;   // ports of the merged block
+// One merge of the region kernel by one wave, with its Schur update on the
+// fp64 matrix cores: level L, children H x W (VERT: stacked), the merged
+// block at (i0, j0), children c0 and c1 (matrices of EIN ports, row stride
+// EIN), result to `out` (row stride EM = the merged block's largest port
+// count).  Lane y holds column y of the merge's C cut rows only and
+// eliminates them (pivot k's column by lane reads from lane k); Z (the
+// eliminated rows scaled by D^-1/2, zero past the block's ports) goes to the
+// last C rows of `out` as scratch, and the merged block V - Z^T Z is NB x NB
+// tiles of 16 x 16 (lane l: rows 16 bi + l / 16 + 4 v, column 16 bj +
+// l % 16), each written at once except the last tile row's, which covers Z.
+template <int L, int H, int W, bool VERT, int NB>
+__device__ __forceinline__ void merge_mfma(int T, int i0, int j0, const short* tab,
+                                           const double* c0, const double* c1, double* out,
+                                           int lane) {
+  constexpr int NH = VERT ? 2 * H : H, NW = VERT ? W : 2 * W;
+  constexpr int C = VERT ? W : H;
+  constexpr int EM = 2 * (NH + NW), EIN = 2 * (H + W), ZS = EM;
+  static_assert(C % 4 == 0 && C <= 16 && EM == 16 * NB && C + EM <= 64, "one wave per merge");
+  static_assert(EM - C >= 16 * (NB - 1), "Z only under the last tile row");
+  const bool rn = j0 + NW < T, tn = i0 > 0;
+  const int E = NH + (rn ? NH : 0) + (tn ? NW : 0) + NW;   // ports of the merged block
   const short* t0 = tab + (((L * 4) + (rn ? 2 : 0) + (tn ? 1 : 0)) * 2) * 64;
   const short* t1 = t0 + 64;
-  const double* c0 = in;                   // left child
-  const double* c1 = in + lds_mat(EIN);    // right child
   const int s0 = t0[lane], s1 = t1[lane];
   double U[C];
 #pragma unroll
@@ -1094,59 +1107,53 @@ __device__ void block_l5_mfma(int T, int I0, int J0, const short* tab, const dou
 #pragma unroll
     for (int x = k + 1; x < C; ++x) U[x] = fma(-readlane_d(U[x], k), t, U[x]);
   }
-  double* z = out;
-  if (lane >= C && lane < C + 32) {
+  double* z = out + (EM - C) * EM;
+  if (lane >= C && lane < C + 16 * NB) {
     const int e = lane - C;
 #pragma unroll
     for (int k = 0; k < C; ++k) z[k * ZS + e] = e < E ? U[k] * sq[k] : 0.0;
   }
   wave_sync();
   const int lr = lane >> 4, lc = lane & 15;
-  double vv[2][2][4];
+  // tile by tile (few registers live): its product and V entries; the
+  // last tile row waits in registers until every tile has read Z
+  double res[NB][4];
 #pragma unroll
-  for (int bj = 0; bj < 2; ++bj) {
-    const int yy = 16 * bj + lc;
-    const int pb0 = t0[C + yy], pb1 = t1[C + yy];
+  for (int bi = 0; bi < NB; ++bi)
 #pragma unroll
-    for (int bi = 0; bi < 2; ++bi)
+    for (int bj = 0; bj < NB; ++bj) {
+      const int yy = 16 * bj + lc;
+      const int pb0 = t0[C + yy], pb1 = t1[C + yy];
+      f64x4 acc = f64x4{0.0, 0.0, 0.0, 0.0};
+#pragma unroll
+      for (int k4 = 0; k4 < C; k4 += 4) {
+        const double a = z[(k4 + lr) * ZS + 16 * bi + lc];
+        const double b = z[(k4 + lr) * ZS + 16 * bj + lc];
+        acc = __builtin_amdgcn_mfma_f64_16x16x4f64(a, b, acc, 0, 0, 0);
+      }
 #pragma unroll
       for (int v = 0; v < 4; ++v) {
         const int xx = 16 * bi + lr + 4 * v;
         const int pa0 = t0[C + xx], pa1 = t1[C + xx];
         const double a = c0[max(pa0, 0) * EIN + max(pb0, 0)];
         const double b = c1[max(pa1, 0) * EIN + max(pb1, 0)];
-        vv[bi][bj][v] = ((pa0 >= 0 && pb0 >= 0) ? a : 0.0) + ((pa1 >= 0 && pb1 >= 0) ? b : 0.0);
+        const double r =
+            ((pa0 >= 0 && pb0 >= 0) ? a : 0.0) + ((pa1 >= 0 && pb1 >= 0) ? b : 0.0) - acc[v];
+        if (bi + 1 < NB) {
+          if (xx < E && yy < E) out[xx * EM + yy] = r;
+        } else {
+          res[bj][v] = r;
+        }
       }
-  }
-  f64x4 acc[2][2];
-#pragma unroll
-  for (int bi = 0; bi < 2; ++bi)
-#pragma unroll
-    for (int bj = 0; bj < 2; ++bj) acc[bi][bj] = f64x4{0.0, 0.0, 0.0, 0.0};
-#pragma unroll
-  for (int k4 = 0; k4 < C; k4 += 4) {
-    double a[2], b[2];
-#pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      a[i] = z[(k4 + lr) * ZS + 16 * i + lc];
-      b[i] = a[i];
     }
+  wave_sync();   // Z read before the last tile row overwrites it
 #pragma unroll
-    for (int bi = 0; bi < 2; ++bi)
+  for (int bj = 0; bj < NB; ++bj)
 #pragma unroll
-      for (int bj = 0; bj < 2; ++bj)
-        acc[bi][bj] = __builtin_amdgcn_mfma_f64_16x16x4f64(a[bi], b[bj], acc[bi][bj], 0, 0, 0);
-  }
-  wave_sync();   // Z read before the block overwrites it
-#pragma unroll
-  for (int bi = 0; bi < 2; ++bi)
-#pragma unroll
-    for (int bj = 0; bj < 2; ++bj)
-#pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        const int xx = 16 * bi + lr + 4 * v, yy = 16 * bj + lc;
-        if (xx < E && yy < E) out[xx * 32 + yy] = vv[bi][bj][v] - acc[bi][bj][v];
-      }
+    for (int v = 0; v < 4; ++v) {
+      const int xx = 16 * (NB - 1) + lr + 4 * v, yy = 16 * bj + lc;
+      if (xx < E && yy < E) out[xx * EM + yy] = res[bj][v];
+    }
   wave_sync();
 }
 
