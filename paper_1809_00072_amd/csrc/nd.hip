@@ -160,6 +160,17 @@ __device__ __forceinline__ double recip(double a) {
   return r;
 }
 
+// 1 / sqrt(a) for a > 0: the hardware estimate and three Newton steps
+// (r <- r + r (1 - a r^2) / 2), each squaring the relative error, to fp64
+// accuracy; a dozen instructions instead of a correctly rounded square root
+// and division.
+__device__ __forceinline__ double rsqrt_nr(double a) {
+  double r = __builtin_amdgcn_rsq(a);
+#pragma unroll
+  for (int i = 0; i < 3; ++i) r = fma(0.5 * r, fma(-a * r, r, 1.0), r);
+  return r;
+}
+
 // A level's merged blocks are symmetric, and the Schur kernels store only
 // their 64 x 64 tiles on and below the diagonal: entry (r, c) of a block
 // with row stride ld is read from its mirror when it lies in a tile above.
@@ -1102,7 +1113,7 @@ __device__ __forceinline__ void merge_mfma(int T, int i0, int j0, const short* t
 #pragma unroll
   for (int k = 0; k < C; ++k) {
     const double piv = readlane_d(U[k], k);
-    sq[k] = 1.0 / sqrt(piv);
+    sq[k] = rsqrt_nr(piv);
     const double t = U[k] * recip(piv);
 #pragma unroll
     for (int x = k + 1; x < C; ++x) U[x] = fma(-readlane_d(U[x], k), t, U[x]);
@@ -1200,7 +1211,7 @@ __device__ void region_merge16(int T, int RI, int RJ, const double* ch, double* 
 #pragma unroll
     for (int k = 0; k < C; ++k) {
       const double piv = readlane_d(U[k], k);
-      sq[k] = 1.0 / sqrt(piv);
+      sq[k] = rsqrt_nr(piv);
       const double t = U[k] * recip(piv);
 #pragma unroll
       for (int x = k + 1; x < C; ++x) U[x] = fma(-readlane_d(U[x], k), t, U[x]);
