@@ -635,7 +635,19 @@ __device__ __forceinline__ void nd_block(const NdArgs& na) {
   block_level<1, 2, 1, false, SPLIT, false>(T, I0, J0, tab, B, A, prow[wv], lane, wv);
   }
   block_level<2, 2, 2, true, SPLIT, false>(T, I0, J0, tab, A, B, prow[wv], lane, wv);
-  block_level<3, 4, 2, false, SPLIT, false>(T, I0, J0, tab, B, A, prow[wv], lane, wv);
+  if constexpr (SPLIT) {
+    block_level<3, 4, 2, false, SPLIT, false>(T, I0, J0, tab, B, A, prow[wv], lane, wv);
+  } else {
+    // the four 4 x 2 -> 4 x 4 merges one after another, each by the whole
+    // wave (children lds_mat(12) apart in B, results lds_mat(16) apart in A)
+#pragma unroll
+    for (int m = 0; m < 4; ++m) {
+      const int cm0 = (m >> 1) * 4 + (m & 1) * 2;
+      merge_mfma<3, 4, 2, false, 1>(T, I0 + (m >> 1) * 4, J0 + (m & 1) * 4, tab,
+                                    B + cm0 * lds_mat(12), B + (cm0 + 1) * lds_mat(12),
+                                    A + m * lds_mat(16), lane);
+    }
+  }
   block_level<4, 4, 4, true, SPLIT, false>(T, I0, J0, tab, A, B, prow[wv], lane, wv);
   if constexpr (SPLIT) {
     constexpr int EO = 4 * BS;   // ports of an interior 8 x 8 block
