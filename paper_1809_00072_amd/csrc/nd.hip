@@ -648,7 +648,16 @@ __device__ __forceinline__ void nd_block(const NdArgs& na) {
                                     A + m * lds_mat(16), lane);
     }
   }
-  block_level<4, 4, 4, true, SPLIT, false>(T, I0, J0, tab, A, B, prow[wv], lane, wv);
+  if constexpr (SPLIT) {
+    block_level<4, 4, 4, true, SPLIT, false>(T, I0, J0, tab, A, B, prow[wv], lane, wv);
+  } else {
+    // the two 4 x 4 -> 8 x 4 merges (children lds_mat(16) apart in A, results
+    // lds_mat(24) apart in B)
+#pragma unroll
+    for (int m = 0; m < 2; ++m)
+      merge_mfma<4, 4, 4, true, 2>(T, I0, J0 + m * 4, tab, A + m * lds_mat(16),
+                                   A + (2 + m) * lds_mat(16), B + m * lds_mat(24), lane);
+  }
   if constexpr (SPLIT) {
     constexpr int EO = 4 * BS;   // ports of an interior 8 x 8 block
     double* dst = na.buf_out + la * na.out_stride + (int64_t)sb * EO * EO;
@@ -1095,19 +1104,21 @@ __device__ __forceinline__ void tri_tile(int tt, int* tx, int* ty) {
 // EIN), result to `out` (row stride EM = the merged block's largest port
 // count).  Lane y holds column y of the merge's C cut rows only and
 // eliminates them (pivot k's column by lane reads from lane k); Z (the
-// eliminated rows scaled by D^-1/2, zero past the block's ports) goes to the
-// last C rows of `out` as scratch, and the merged block V - Z^T Z is NB x NB
-// tiles of 16 x 16 (lane l: rows 16 bi + l / 16 + 4 v, column 16 bj +
-// l % 16), each written at once except the last tile row's, which covers Z.
+// eliminated rows scaled by D^-1/2, zero past the block's ports and in the
+// rows that pad C to a multiple of 4) goes to `out` as scratch, under the
+// last tile row, and the merged block V - Z^T Z is NB x NB tiles of 16 x 16
+// (lane l: rows 16 bi + l / 16 + 4 v, column 16 bj + l % 16), each written
+// at once except the last tile row's, which waits until Z is read.
 template <int L, int H, int W, bool VERT, int NB>
 __device__ __forceinline__ void merge_mfma(int T, int i0, int j0, const short* tab,
                                            const double* c0, const double* c1, double* out,
                                            int lane) {
   constexpr int NH = VERT ? 2 * H : H, NW = VERT ? W : 2 * W;
   constexpr int C = VERT ? W : H;
-  constexpr int EM = 2 * (NH + NW), EIN = 2 * (H + W), ZS = EM;
-  static_assert(C % 4 == 0 && C <= 16 && EM == 16 * NB && C + EM <= 64, "one wave per merge");
-  static_assert(EM - C >= 16 * (NB - 1), "Z only under the last tile row");
+  constexpr int EM = 2 * (NH + NW), EIN = 2 * (H + W), ZS = 16 * NB, CK = (C + 3) & ~3;
+  static_assert(C <= 16 && EM <= 16 * NB && EM > 16 * (NB - 1) && C + 16 * NB <= 64,
+                "one wave per merge");
+  static_assert(CK * ZS <= (EM - 16 * (NB - 1)) * EM, "Z only under the last tile row");
   const bool rn = j0 + NW < T, tn = i0 > 0;
   const int E = NH + (rn ? NH : 0) + (tn ? NW : 0) + NW;   // ports of the merged block
   const short* t0 = tab + (((L * 4) + (rn ? 2 : 0) + (tn ? 1 : 0)) * 2) * 64;
@@ -1130,11 +1141,11 @@ __device__ __forceinline__ void merge_mfma(int T, int i0, int j0, const short* t
 #pragma unroll
     for (int x = k + 1; x < C; ++x) U[x] = fma(-readlane_d(U[x], k), t, U[x]);
   }
-  double* z = out + (EM - C) * EM;
+  double* z = out + 16 * (NB - 1) * EM;
   if (lane >= C && lane < C + 16 * NB) {
     const int e = lane - C;
 #pragma unroll
-    for (int k = 0; k < C; ++k) z[k * ZS + e] = e < E ? U[k] * sq[k] : 0.0;
+    for (int k = 0; k < CK; ++k) z[k * ZS + e] = (k < C && e < E) ? U[k] * sq[k] : 0.0;
   }
   wave_sync();
   const int lr = lane >> 4, lc = lane & 15;
@@ -1149,7 +1160,7 @@ __device__ __forceinline__ void merge_mfma(int T, int i0, int j0, const short* t
       const int pb0 = t0[C + yy], pb1 = t1[C + yy];
       f64x4 acc = f64x4{0.0, 0.0, 0.0, 0.0};
 #pragma unroll
-      for (int k4 = 0; k4 < C; k4 += 4) {
+      for (int k4 = 0; k4 < CK; k4 += 4) {
         const double a = z[(k4 + lr) * ZS + 16 * bi + lc];
         const double b = z[(k4 + lr) * ZS + 16 * bj + lc];
         acc = __builtin_amdgcn_mfma_f64_16x16x4f64(a, b, acc, 0, 0, 0);
