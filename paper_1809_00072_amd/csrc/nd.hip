@@ -27,10 +27,10 @@
 // transfer admittance from the row sources to the sinks, i.e. G'.
 //
 // Levels up to 16 x 16 cells: one workgroup per 16 x 16 region (k_nd_block):
-// each wave builds an 8 x 8 block (its 2 x 2 blocks in registers, the larger
-// merges in its own LDS), then the workgroup merges the four into the
-// region's block; small builds take one workgroup per 8 x 8 block instead
-// (k_nd_block_split).  Merges with 8 to 64 shared nodes: one workgroup per
+// each wave builds an 8 x 8 block (its 2 x 2 blocks in registers, each larger
+// merge by the whole wave: the cut rows eliminated by lane reads, the Schur
+// update on fp64 MFMA tiles), then the workgroup merges the four into the
+// region's block.  Merges with 8 to 64 shared nodes: one workgroup per
 // merge eliminates them with the shared rows in registers (k_nd_cut), and
 // the Schur update of the external block runs on 64 x 64 fp64 MFMA tiles of
 // its lower triangle, in the same workgroup for small merges, else in
@@ -215,29 +215,19 @@ __device__ __forceinline__ ArrRef nd_ref(const NdArgs& na, int64_t la) {
 }
 
 // ---------------------------------------------------------------------------
-// Levels 1 x 1 .. 8 x 8 of one 8 x 8 block per wave.  A level's merges are
-// packed into groups of GS lanes (GS: the power of two >= the merge's
-// combined size LD = c + E): lane y of a group holds column y of its merge's
-// combined matrix [c cut nodes | E external ports], every row in registers.
-// Eliminating the c cut pivots updates every later row, so the external
-// rows and columns end as the merged block's admittance matrix.  The
-// multiplier of row x at pivot k is that row's entry in column k, held by
-// the group's lane k (see block_level for how it reaches the others).  No
-// workgroup barrier: each wave's levels use its own LDS buffers.
+// Levels 1 x 1 .. 16 x 16: one workgroup per 16 x 16 region, wave w building
+// the 8 x 8 block (w / 2, w % 2) of it in its own LDS buffers (no workgroup
+// barrier), then the workgroup merging the four.
 // ---------------------------------------------------------------------------
-constexpr int BS = 8;                 // side of the blocks of this kernel
+constexpr int BS = 8;                 // side of the blocks one wave builds
 constexpr int BWAVES = 4;             // waves per workgroup of the block kernel
-constexpr int64_t kSplitBlocks = 256;  // at most this many blocks: one workgroup per block
 constexpr int BLEVELS = 7;  // 1x1 -> 2x1 -> 2x2 -> 4x2 -> 4x4 -> 8x4 -> 8x8 -> 16x8
-// In LDS every cell's or merged block's matrix takes its side squared plus one
-// double: consecutive matrices then start in different banks, so the lanes of
-// different merge groups (and the leaf lanes) do not collide.
+// In LDS every merged block's matrix takes its side squared plus one double:
+// consecutive matrices then start in different banks.
 __host__ __device__ constexpr int lds_mat(int side) { return side * side + 1; }
-// doubles per wave: the leaves and odd levels (64 x 17, 16 x 65, 4 x 257) and
-// the even levels (32 x 37, 8 x 145, 2 x 577); without the leaves and the
-// first level (the 2 x 2 blocks formed in registers) 16 x 65 and 8 x 145
-constexpr int BUFA = 64 * 17, BUFB = 32 * 37;
-constexpr int BUFA2 = 16 * 65, BUFB2 = 8 * 145;
+// doubles per wave: the odd levels' results (16 x 65 for the 2 x 2 blocks,
+// 4 x 257, then the 8 x 8 block) and the even levels' (8 x 145, 2 x 577)
+constexpr int BUFA = 16 * 65, BUFB = 8 * 145;
 
 // Child port landing on each combined slot (cut nodes 0 .. c-1, then the
 // externals), per level and per boundary variant (bit 1: the merged block
@@ -290,18 +280,18 @@ __device__ __forceinline__ P* opaque_lds(const void* p) {
   return (P*)(uintptr_t)a;
 }
 
-__device__ __forceinline__ double bperm_d(double v, int src_lane) {
-  const unsigned long long b = __builtin_bit_cast(unsigned long long, v);
-  const unsigned lo = (unsigned)__builtin_amdgcn_ds_bpermute(src_lane << 2, (int)(unsigned)b);
-  const unsigned hi = (unsigned)__builtin_amdgcn_ds_bpermute(src_lane << 2, (int)(unsigned)(b >> 32));
-  return __builtin_bit_cast(double, ((unsigned long long)hi << 32) | lo);
-}
-
 __device__ __forceinline__ double readlane_d(double v, int l) {
   const unsigned long long b = __builtin_bit_cast(unsigned long long, v);
   const unsigned lo = (unsigned)__builtin_amdgcn_readlane((int)(unsigned)b, l);
   const unsigned hi = (unsigned)__builtin_amdgcn_readlane((int)(unsigned)(b >> 32), l);
   return __builtin_bit_cast(double, ((unsigned long long)hi << 32) | lo);
+}
+
+// LDS written by some lanes of a wave, then read by others of the same wave.
+__device__ __forceinline__ void wave_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
 // Lane k of every row of 16 lanes, to the whole row (DPP row broadcast).
@@ -335,61 +325,29 @@ __device__ __forceinline__ double rowbcast_d(double v, int k) {
   }
 }
 
-// LDS written by some lanes of a wave, then read by others of the same wave.
-__device__ __forceinline__ void wave_sync() {
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-  __builtin_amdgcn_wave_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-}
-
-// One level of merges of the block at (I0, J0): children h x w (in: EIN x
-// EIN per child), merged blocks written with stride EM (out).  SPLIT: the
-// level's passes (GPW merges each) are shared by the workgroup's waves, which
-// all work on this block; otherwise the wave does them all.
-// The combined matrix is symmetric, and so is what remains of it after each
-// pivot, so the multiplier of row x at pivot k (its entry in column k) equals
-// the pivot row's entry in column x, i.e. lane k's register x.  Groups of 64
-// lanes read it with a lane read and groups of 16 with a DPP row broadcast,
-// neither touching LDS (which bounds this kernel); groups of 8 and 32 lanes
-// publish the pivot row in LDS (`pr`, GS + 1 doubles per group) and read it
-// back as broadcasts, or, in the SPLIT form (capped at 96 VGPRs), take it by
-// a lane permute.
-// DENSE: merged blocks go to a global level buffer (dense, EM x EM each),
-// else to LDS (lds_mat(EM) apart).  RS: side of the region whose merges the
-// call makes (the children h x w tiling it); CSTR: doubles between children
-// in `in` (0: lds_mat(EIN)); DIST: the passes are shared by the workgroup's
-// waves (then a workgroup barrier ends the level).
-template <int L, int H, int W, bool VERT, bool SPLIT, bool DENSE, int RS = BS, int CSTR = 0,
-          bool DIST = SPLIT>
-__device__ __forceinline__ void block_level(int T, int I0, int J0, const short* tab,
-                                            const double* in, double* out, double* pr, int lane,
-                                            int wv) {
-  constexpr int NH = VERT ? 2 * H : H, NW = VERT ? W : 2 * W;
-  constexpr int C = VERT ? W : H;
-  constexpr int EM = 2 * (NH + NW), EIN = 2 * (H + W);
-  constexpr int LD = C + EM;
-  constexpr int GS = LD <= 8 ? 8 : (LD <= 16 ? 16 : (LD <= 32 ? 32 : 64));
-  constexpr int GPW = 64 / GS;                 // merges per pass
-  constexpr int OSTRIDE = DENSE ? EM * EM : lds_mat(EM);
-  constexpr int CS = CSTR > 0 ? CSTR : lds_mat(EIN);
-  constexpr int MC = RS / NW, CC = RS / W;     // merges / children per region row
-  constexpr int NM = (RS / NH) * MC;
-  static_assert(NM % GPW == 0, "whole passes");
-  const int g = lane / GS, yl = lane % GS, gb = lane - yl;
-  lds_f64* gr = opaque_lds<lds_f64>(pr + g * (GS + 1));   // this group's pivot row
+// The eight 2 x 2 -> 4 x 2 merges of a wave's 8 x 8 block (children
+// lds_mat(8) apart in `in`, results lds_mat(12) apart in `out`), in two
+// passes of four, a group of 16 lanes per merge: lane y holds column y of
+// its merge's combined matrix [2 cut nodes | 12 external ports], every row
+// in registers, and the multiplier of row x at pivot k (lane k's register x,
+// the matrix being symmetric) comes by a DPP row broadcast; eliminating the
+// cut rows leaves the merged block in the external rows.
+__device__ __forceinline__ void level2_dpp(int T, int I0, int J0, const short* tab,
+                                           const double* in, double* out, int lane) {
+  constexpr int L = 2, NH = 4, NW = 2, C = 2, EM = 12, EIN = 8, LD = C + EM, GS = 16;
+  const int g = lane / GS, yl = lane % GS;
 #pragma unroll 1
-  for (int pass = DIST ? wv : 0; pass < NM / GPW; pass += DIST ? BWAVES : 1) {
-    const int m = pass * GPW + g;
-    const int mi = m / MC, mj = m % MC;
+  for (int pass = 0; pass < 2; ++pass) {
+    const int m = pass * (64 / GS) + g;
+    const int mi = m >> 2, mj = m & 3;
     const int i0 = I0 + mi * NH, j0 = J0 + mj * NW;
     const bool rn = j0 + NW < T, tn = i0 > 0;
     const int ld = C + NH + (rn ? NH : 0) + (tn ? NW : 0) + NW;
-    const int cm0 = VERT ? (mi * 2) * CC + mj : mi * CC + mj * 2;
-    const int cm1 = VERT ? (mi * 2 + 1) * CC + mj : mi * CC + mj * 2 + 1;
+    const int cm0 = mi * 8 + mj, cm1 = cm0 + 4;
     const short* t0 = tab + (((L * 4) + (rn ? 2 : 0) + (tn ? 1 : 0)) * 2) * 64;
     const short* t1 = t0 + 64;
-    const double* c0 = in + cm0 * CS;
-    const double* c1 = in + cm1 * CS;
+    const double* c0 = in + cm0 * lds_mat(EIN);
+    const double* c1 = in + cm1 * lds_mat(EIN);
     const int s0 = t0[yl], s1 = t1[yl];
     double U[LD];
 #pragma unroll
@@ -399,46 +357,19 @@ __device__ __forceinline__ void block_level(int T, int I0, int J0, const short* 
       const double b = c1[max(r1, 0) * EIN + max(s1, 0)];
       U[x] = ((r0 >= 0 && s0 >= 0) ? a : 0.0) + ((r1 >= 0 && s1 >= 0) ? b : 0.0);
     }
-    if constexpr (SPLIT || GS == 64 || GS == 16) {
-      // the multiplier of row x comes from the group's lane k: a lane read
-      // (one group per wave) or a row broadcast (groups of 16 lanes), no LDS;
-      // the split form (few blocks, 96 VGPRs) takes a lane permute otherwise
-#pragma unroll
-      for (int k = 0; k < C; ++k) {
-        const double piv = GS == 64 ? readlane_d(U[k], k)
-                                    : (GS == 16 ? rowbcast_d(U[k], k) : bperm_d(U[k], gb + k));
-        const double t = U[k] * recip(piv);
-#pragma unroll
-        for (int x = k + 1; x < LD; ++x) {
-          const double mx = GS == 64 ? readlane_d(U[x], k)
-                                     : (GS == 16 ? rowbcast_d(U[x], k) : bperm_d(U[x], gb + k));
-          U[x] = fma(-mx, t, U[x]);
-        }
-      }
-    } else {
 #pragma unroll
     for (int k = 0; k < C; ++k) {
-      gr[yl] = U[k];
-      wave_sync();
-      const double t = U[k] * recip(gr[k]);
+      const double t = U[k] * recip(rowbcast_d(U[k], k));
 #pragma unroll
-      for (int x = k + 1; x < LD; ++x) {
-        U[x] = fma(-gr[x], t, U[x]);
-        // the update is done here: deferring it past the next pivots would
-        // hold every pivot row's values live
-        asm volatile("" : "+v"(U[x]));
-      }
-      wave_sync();   // every read of this pivot row precedes the next one's writes
-    }
+      for (int x = k + 1; x < LD; ++x) U[x] = fma(-rowbcast_d(U[x], k), t, U[x]);
     }
     if (yl >= C && yl < ld) {
 #pragma unroll
       for (int x = C; x < LD; ++x)
-        if (x < ld) out[m * OSTRIDE + (x - C) * EM + (yl - C)] = U[x];
+        if (x < ld) out[m * lds_mat(EM) + (x - C) * EM + (yl - C)] = U[x];
     }
   }
-  if (DIST) __syncthreads();
-  else wave_sync();
+  wave_sync();
 }
 
 // Conductance g between nodes p and q of a small symmetric matrix held in
@@ -525,174 +456,100 @@ __device__ __forceinline__ void merge_mfma(int T, int i0, int j0, const short* t
                                            const double* c0, const double* c1, double* out,
                                            int lane);
 
-// SPLIT (few blocks, a latency-bound build): one 8 x 8 block per workgroup,
-// its waves sharing each level, the 8 x 8 block to the level buffer.
-// Otherwise one 16 x 16 region per workgroup: wave w builds its 8 x 8 block
-// (row w / 2, column w % 2 of the region) alone, without workgroup barriers,
-// into its LDS buffer A; waves 0 and 1 merge the two columns' pairs into
-// 16 x 8 blocks (in LDS), and the workgroup merges those into the region's
-// 16 x 16 block, which goes to the level buffer.
-template <bool SPLIT>
-__device__ __forceinline__ void nd_block(const NdArgs& na) {
+// One 16 x 16 region per workgroup (every build, whatever its size, so that
+// an array's arithmetic never depends on how many arrays are built with it):
+// wave w builds its 8 x 8 block (row w / 2, column w % 2 of the region)
+// alone, without workgroup barriers, in its LDS buffers A and B: the 2 x 2
+// blocks in registers, the merges 2 x 2 -> 4 x 2 in 16-lane groups
+// (level2_dpp), then 4 x 2 -> 4 x 4 -> 8 x 4 -> 8 x 8, each by the whole
+// wave (merge_mfma).  Waves 0 and 1 then merge the
+// two columns' pairs into 16 x 8 blocks (in LDS), and the workgroup merges
+// those into the region's 16 x 16 block, which goes to the level buffer.
+// LDS (78 KB) allows two workgroups per CU.
+__global__ __launch_bounds__(64 * BWAVES) void k_nd_block(NdArgs na) {
   __shared__ short tab[BLEVELS * 4 * 2 * 64];
-  constexpr int NB = SPLIT ? 1 : BWAVES;   // blocks per workgroup
-  constexpr int BA = SPLIT ? BUFA : BUFA2, BB = SPLIT ? BUFB : BUFB2;
-  __shared__ double bufA[NB][BA];
-  __shared__ double bufB[NB][BB];
-  __shared__ double prow[BWAVES][72];   // pivot rows of each wave's merge groups
+  __shared__ double bufA[BWAVES][BUFA];
+  __shared__ double bufB[BWAVES][BUFB];
   const short* ct = &kBlkTab.s[0][0][0][0];
   for (int e = threadIdx.x; e < BLEVELS * 4 * 2 * 64; e += 64 * BWAVES) tab[e] = ct[e];
   __syncthreads();
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
   const int T = na.T;
-  const int nsb = T / BS;
-  int64_t la;
-  int sb, I0, J0;
-  if constexpr (SPLIT) {
-    const int64_t blk = blockIdx.x;
-    if (blk >= na.n_arrays * nsb * nsb) return;
-    la = blk / (nsb * nsb);
-    sb = (int)(blk % (nsb * nsb));
-    I0 = (sb / nsb) * BS;
-    J0 = (sb % nsb) * BS;
-  } else {
-    const int nr = nsb / 2;   // regions per side
-    const int64_t rg = blockIdx.x;
-    if (rg >= na.n_arrays * nr * nr) return;   // whole workgroups
-    la = rg / (nr * nr);
-    sb = (int)(rg % (nr * nr));   // region
-    I0 = (sb / nr) * 2 * BS + (wv >> 1) * BS;
-    J0 = (sb % nr) * 2 * BS + (wv & 1) * BS;
-  }
+  const int nr = T / (2 * BS);   // regions per side
+  const int64_t rg = blockIdx.x;
+  if (rg >= na.n_arrays * nr * nr) return;   // whole workgroups
+  const int64_t la = rg / (nr * nr);
+  const int sr = (int)(rg % (nr * nr));      // region
+  const int RI = (sr / nr) * 2 * BS, RJ = (sr % nr) * 2 * BS;
+  const int I0 = RI + (wv >> 1) * BS, J0 = RJ + (wv & 1) * BS;
   const ArrRef ref = nd_ref(na, la);
   const MapScalars& ms = *ref.ms;
   const int64_t arr = ref.arr;
   const double wmax = ms.wmax_fixed > 0.0f ? (double)ms.wmax_fixed : (double)*ms.d_wmax;
-  double* A = bufA[SPLIT ? 0 : wv];
-  double* B = bufB[SPLIT ? 0 : wv];
-  if constexpr (!SPLIT) {
-    // levels 1 x 1 .. 2 x 2 in registers, lane q < 16 taking 2 x 2 block q,
-    // written to the level buffer as block_level<1> would (ports [L | R (not
-    // at the right edge) | T (not at the top) | B], row stride 8)
-    if (lane < 16) {
-      const int qi = lane >> 2, qj = lane & 3;
-      const int gi0 = I0 + 2 * qi, gj0 = J0 + 2 * qj;
-      double X[10][10];
-      block2x2(ms, ref.W, wmax, arr, gi0, gj0, T, na.row_off, na.g_r, na.g_c, na.g_s, X);
-      const bool rn = gj0 + 2 < T, tn = gi0 > 0;
-      const int oT = rn ? 4 : 2, oB = oT + (tn ? 2 : 0);
-      // padded port -> stored port (-1: absent)
-      int pos[8];
-      pos[0] = 0;
-      pos[1] = 1;
-      pos[2] = rn ? 2 : -1;
-      pos[3] = rn ? 3 : -1;
-      pos[4] = tn ? oT : -1;
-      pos[5] = tn ? oT + 1 : -1;
-      pos[6] = oB;
-      pos[7] = oB + 1;
-      double* o = A + lane * lds_mat(8);
+  double* A = bufA[wv];
+  double* B = bufB[wv];
+  // levels 1 x 1 .. 2 x 2 in registers, lane q < 16 taking 2 x 2 block q,
+  // written to A with ports [L | R (not at the right edge) | T (not at the
+  // top) | B], row stride 8, lds_mat(8) apart
+  if (lane < 16) {
+    const int qi = lane >> 2, qj = lane & 3;
+    const int gi0 = I0 + 2 * qi, gj0 = J0 + 2 * qj;
+    double X[10][10];
+    block2x2(ms, ref.W, wmax, arr, gi0, gj0, T, na.row_off, na.g_r, na.g_c, na.g_s, X);
+    const bool rn = gj0 + 2 < T, tn = gi0 > 0;
+    const int oT = rn ? 4 : 2, oB = oT + (tn ? 2 : 0);
+    // padded port -> stored port (-1: absent)
+    int pos[8];
+    pos[0] = 0;
+    pos[1] = 1;
+    pos[2] = rn ? 2 : -1;
+    pos[3] = rn ? 3 : -1;
+    pos[4] = tn ? oT : -1;
+    pos[5] = tn ? oT + 1 : -1;
+    pos[6] = oB;
+    pos[7] = oB + 1;
+    double* o = A + lane * lds_mat(8);
 #pragma unroll
-      for (int p = 0; p < 8; ++p)
+    for (int p = 0; p < 8; ++p)
 #pragma unroll
-        for (int q = 0; q < 8; ++q) {
-          const double v = p >= q ? X[2 + p][2 + q] : X[2 + q][2 + p];
-          if (pos[p] >= 0 && pos[q] >= 0) o[pos[p] * 8 + pos[q]] = v;
-        }
-    }
-    wave_sync();
-  } else {
-  // leaves (the first wave): one cell per lane, ports [L | R (not at the
-  // right edge) | T (not at the top) | B] in a 4 x 4 slot
-  if (!SPLIT || wv == 0) {
-    const int li = lane / BS, lj = lane % BS;
-    const int gi = I0 + li, gj = J0 + lj;
-    const double G = cell_conductance(ms, ref.W, wmax, arr, gi, gj, na.row_off);
-    const bool hasR = gj + 1 < T, hasT = gi > 0;
-    const double gv = (gi + 1 < T) ? na.g_c : na.g_s;
-    double* Y = A + lane * lds_mat(4);   // this lane's slot (LDS: the indices below vary)
+      for (int q = 0; q < 8; ++q) {
+        const double v = p >= q ? X[2 + p][2 + q] : X[2 + q][2 + p];
+        if (pos[p] >= 0 && pos[q] >= 0) o[pos[p] * 8 + pos[q]] = v;
+      }
+  }
+  wave_sync();
+  level2_dpp(T, I0, J0, tab, A, B, lane);
+  // the four 4 x 2 -> 4 x 4 merges (children lds_mat(12) apart in B,
+  // results lds_mat(16) apart in A)
 #pragma unroll
-    for (int e = 0; e < 16; ++e) Y[e] = 0.0;
-    const int Lp = 0, Rp = 1, Tp = hasR ? 2 : 1, Bp = (hasR ? 2 : 1) + (hasT ? 1 : 0);
-    auto st = [&](int p, int q, double gg) {
-      Y[p * 4 + p] += gg;
-      Y[q * 4 + q] += gg;
-      Y[p * 4 + q] -= gg;
-      Y[q * 4 + p] -= gg;
-    };
-    if (hasR) st(Lp, Rp, na.g_r);
-    if (hasT) {
-      st(Lp, Tp, G);
-      st(Tp, Bp, gv);
-    } else {
-      const double ge = G > 0.0 ? (G * gv) / (G + gv) : 0.0;
-      st(Lp, Bp, ge);
-    }
+  for (int m = 0; m < 4; ++m) {
+    const int cm0 = (m >> 1) * 4 + (m & 1) * 2;
+    merge_mfma<3, 4, 2, false, 1>(T, I0 + (m >> 1) * 4, J0 + (m & 1) * 4, tab,
+                                  B + cm0 * lds_mat(12), B + (cm0 + 1) * lds_mat(12),
+                                  A + m * lds_mat(16), lane);
   }
-  if (SPLIT) __syncthreads();
-  else wave_sync();
-  block_level<0, 1, 1, true, SPLIT, false>(T, I0, J0, tab, A, B, prow[wv], lane, wv);
-  block_level<1, 2, 1, false, SPLIT, false>(T, I0, J0, tab, B, A, prow[wv], lane, wv);
-  }
-  block_level<2, 2, 2, true, SPLIT, false>(T, I0, J0, tab, A, B, prow[wv], lane, wv);
-  if constexpr (SPLIT) {
-    block_level<3, 4, 2, false, SPLIT, false>(T, I0, J0, tab, B, A, prow[wv], lane, wv);
-  } else {
-    // the four 4 x 2 -> 4 x 4 merges one after another, each by the whole
-    // wave (children lds_mat(12) apart in B, results lds_mat(16) apart in A)
+  // the two 4 x 4 -> 8 x 4 merges (children lds_mat(16) apart in A, results
+  // lds_mat(24) apart in B)
 #pragma unroll
-    for (int m = 0; m < 4; ++m) {
-      const int cm0 = (m >> 1) * 4 + (m & 1) * 2;
-      merge_mfma<3, 4, 2, false, 1>(T, I0 + (m >> 1) * 4, J0 + (m & 1) * 4, tab,
-                                    B + cm0 * lds_mat(12), B + (cm0 + 1) * lds_mat(12),
-                                    A + m * lds_mat(16), lane);
-    }
+  for (int m = 0; m < 2; ++m)
+    merge_mfma<4, 4, 4, true, 2>(T, I0, J0 + m * 4, tab, A + m * lds_mat(16),
+                                 A + (2 + m) * lds_mat(16), B + m * lds_mat(24), lane);
+  // the 8 x 8 block to A (row stride 32); the region's two 16 x 8 merges
+  // (children BUFA apart: the waves' A buffers) to the B buffers (row stride
+  // 48); their 16 x 16 merge (the A buffers as scratch) to merged block
+  // (region row, region column) of the 16 x 16 level
+  merge_mfma<5, 8, 4, false, 2>(T, I0, J0, tab, B, B + lds_mat(24), A, lane);
+  __syncthreads();
+  if (wv < 2) {   // wave m: the pair of column m (children: the A buffers of waves m, 2 + m)
+    const double* ca = &bufA[0][0];
+    merge_mfma<6, 8, 8, true, 3>(T, RI, RJ + wv * BS, tab, ca + wv * BUFA, ca + (2 + wv) * BUFA,
+                                 &bufB[0][0] + wv * lds_mat(48), lane);
   }
-  if constexpr (SPLIT) {
-    block_level<4, 4, 4, true, SPLIT, false>(T, I0, J0, tab, A, B, prow[wv], lane, wv);
-  } else {
-    // the two 4 x 4 -> 8 x 4 merges (children lds_mat(16) apart in A, results
-    // lds_mat(24) apart in B)
-#pragma unroll
-    for (int m = 0; m < 2; ++m)
-      merge_mfma<4, 4, 4, true, 2>(T, I0, J0 + m * 4, tab, A + m * lds_mat(16),
-                                   A + (2 + m) * lds_mat(16), B + m * lds_mat(24), lane);
-  }
-  if constexpr (SPLIT) {
-    constexpr int EO = 4 * BS;   // ports of an interior 8 x 8 block
-    double* dst = na.buf_out + la * na.out_stride + (int64_t)sb * EO * EO;
-    block_level<5, 8, 4, false, true, true>(T, I0, J0, tab, B, dst, prow[wv], lane, wv);
-  } else {
-    // the 8 x 8 block to A (row stride 32); the region's two 16 x 8 merges
-    // (children BA apart: the waves' A buffers) to the B buffers (row stride
-    // 48); their 16 x 16 merge (the A buffers as scratch) to merged block
-    // (region row, region column) of the 16 x 16 level
-    merge_mfma<5, 8, 4, false, 2>(T, I0, J0, tab, B, B + lds_mat(24), A, lane);
-    __syncthreads();
-    const int RI = I0 - (wv >> 1) * BS, RJ = J0 - (wv & 1) * BS;
-    if (wv < 2) {   // wave m: the pair of column m (children: the A buffers of waves m, 2 + m)
-      const double* ca = &bufA[0][0];
-      merge_mfma<6, 8, 8, true, 3>(T, RI, RJ + wv * BS, tab, ca + wv * BA, ca + (2 + wv) * BA,
-                                   &bufB[0][0] + wv * lds_mat(48), lane);
-    }
-    __syncthreads();
-    constexpr int E16 = 8 * BS;   // ports of an interior 16 x 16 block
-    double* dst = na.buf_out + la * na.out_stride +
-                  ((int64_t)(RI / (2 * BS)) * (T / (2 * BS)) + RJ / (2 * BS)) * E16 * E16;
-    region_merge16(T, RI, RJ, &bufB[0][0], dst, &bufA[0][0]);
-  }
-}
-
-// The split form (small builds: at most kSplitBlocks blocks) is held to 96
-// VGPRs (5 waves per SIMD, five workgroups per CU).  LDS bounds the region
-// form at two workgroups per CU.
-__global__ __launch_bounds__(64 * BWAVES) __attribute__((amdgpu_waves_per_eu(5)))
-void k_nd_block_split(NdArgs na) {
-  nd_block<true>(na);
-}
-
-__global__ __launch_bounds__(64 * BWAVES) void k_nd_block(NdArgs na) {
-  nd_block<false>(na);
+  __syncthreads();
+  constexpr int E16 = 8 * BS;   // ports of an interior 16 x 16 block
+  double* dst = na.buf_out + la * na.out_stride +
+                ((int64_t)(RI / (2 * BS)) * (T / (2 * BS)) + RJ / (2 * BS)) * E16 * E16;
+  region_merge16(T, RI, RJ, &bufB[0][0], dst, &bufA[0][0]);
 }
 
 // ---------------------------------------------------------------------------
@@ -2147,26 +2004,17 @@ hipError_t launch_nd_build(const MapScalars& ms, const float* W, float* gpt, int
   na.buf_out = bufA;
   {
     ProfScope prof("nd_block", s);
-    // few blocks: one per workgroup, its waves sharing each level (shorter
-    // latency); many: one per wave (more blocks in flight per CU)
-    const int64_t nblk = n * nsb * nsb;
-    if (nblk <= kSplitBlocks) {
-      hipLaunchKernelGGL(k_nd_block_split, dim3((unsigned)nblk), dim3(64 * BWAVES), 0, s, na);
-    } else {
-      // 16 x 16 regions; the kernel also makes the 16 x 8 and 16 x 16 levels
-      hipLaunchKernelGGL(k_nd_block, dim3((unsigned)(nblk / 4)), dim3(64 * BWAVES), 0, s, na);
-    }
+    // 16 x 16 regions: the kernel makes the levels up to 16 x 16
+    hipLaunchKernelGGL(k_nd_block, dim3((unsigned)(n * nsb * nsb / 4)), dim3(64 * BWAVES), 0, s,
+                       na);
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   double* cur = bufA;
   double* nxt = bufB;
-  int h = bs, w = bs;
+  // the block kernel made the 16 x 16 level
+  int h = 2 * bs, w = 2 * bs;
   bool vert = true;
-  if (n * nsb * nsb > kSplitBlocks) {   // the block kernel made the 16 x 16 level
-    h = 2 * bs;
-    w = 2 * bs;
-  }
   while (h < na.T || w < na.T) {
     const int nh = vert ? 2 * h : h, nw = vert ? w : 2 * w;
     const int64_t nmerge = (int64_t)(na.T / nh) * (na.T / nw);
