@@ -1299,11 +1299,15 @@ __global__ __launch_bounds__(512) void k_nd_cut(NdArgs na) {
       // symmetric; readers take the mirror of an entry above); the children's
       // entries of a tile are loaded before its product, so that they arrive
       // during it
+      // at the bottom of the grid, tiles wholly among the B ports (sinks)
+      const int bsink = g.i0 + (na.vert ? 2 * na.h : na.h) == T ? E - (na.vert ? na.w : 2 * na.w)
+                                                              : E;
 #pragma unroll 1
       for (int tt = 0; tt < nt * (nt + 1) / 2; ++tt) {
         int tx, ty;
         tri_tile(tt, &tx, &ty);
         const int x0 = tx * 64, y0 = ty * 64;
+        if (x0 >= bsink && y0 >= bsink) continue;
         MfmaTile mt;
         mt.init(threadIdx.x);
         double vv[2][2][4];
@@ -1780,6 +1784,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(5))) void k
   const int x0 = tx * 64, y0 = ty * 64;
   const int nrx = min(64, E - x0), nry = min(64, E - y0);
   if (nrx <= 0 || nry <= 0) return;
+  // at the bottom of the grid the B ports (the last nw) are sinks: entries
+  // between two sinks are never read (sinks are never pivots, and G' is the
+  // sink x source block), so tiles wholly among them are skipped
+  if (g.i0 + nh == na.T && x0 >= E - nw && y0 >= E - nw) return;
   inverse_tables<MAXSLOT2>(na, g, invt, 256);
   const double* z = na.scratch + g.la * na.scr_stride + (int64_t)g.m * Emax * c;
   MfmaTile mt;
