@@ -31,8 +31,9 @@
 // merge by the whole wave: the cut rows eliminated by lane reads, the Schur
 // update on fp64 MFMA tiles), then the workgroup merges the four into the
 // region's block.  Merges with 8 to 64 shared nodes: one workgroup per
-// merge eliminates them with the shared rows in registers (k_nd_cut), and
-// the Schur update of the external block runs on 64 x 64 fp64 MFMA tiles of
+// merge eliminates them with the shared rows in registers (k_nd_cut; each
+// lane reads one multiplier per 16 rows from LDS, the FMAs take them by DPP
+// row broadcast), and the Schur update of the external block runs on 64 x 64 fp64 MFMA tiles of
 // its lower triangle, in the same workgroup for small merges, else in
 // k_nd_schur; the final step with at most 64 row inputs likewise.  Merges
 // with 128 shared nodes: k_nd_cut2 (panels of 256 external columns), then
@@ -48,6 +49,7 @@
 // positive (zero resistances take the row sweep instead).
 
 #include <algorithm>
+#include <utility>
 
 #include "common.h"
 #include "device_map.h"
@@ -297,11 +299,9 @@ __device__ __forceinline__ void wave_sync() {
 // Lane k of every row of 16 lanes, to the whole row (DPP row broadcast).
 template <int K>
 __device__ __forceinline__ double rowbcast_d(double v) {
-  const unsigned long long b = __builtin_bit_cast(unsigned long long, v);
-  const unsigned lo = (unsigned)__builtin_amdgcn_update_dpp(0, (int)(unsigned)b, 0x150 + K, 0xf, 0xf, false);
-  const unsigned hi =
-      (unsigned)__builtin_amdgcn_update_dpp(0, (int)(unsigned)(b >> 32), 0x150 + K, 0xf, 0xf, false);
-  return __builtin_bit_cast(double, ((unsigned long long)hi << 32) | lo);
+  // every source lane of a row broadcast exists: bound_ctrl only spares the
+  // move that would set the unused old value
+  return __builtin_amdgcn_update_dpp(0.0, v, 0x150 + K, 0xf, 0xf, true);
 }
 
 __device__ __forceinline__ double rowbcast_d(double v, int k) {
@@ -797,6 +797,49 @@ __device__ __forceinline__ void pin8(double (&U)[N], int x0) {
   }
 }
 
+// u += m(lane K of this row of 16 lanes) * tn: one FMA whose first operand
+// comes through a DPP row broadcast (64-bit DPP takes row_newbcast only).
+// The compiler does not look into inline assembly for DPP hazards: the
+// s_nop gives the two wait states a DPP instruction needs after a write of
+// any VGPR it reads, and the callers branch only on scalar conditions, so
+// that no VALU write of EXEC comes before it.
+template <int K>
+__device__ __forceinline__ void fmac_bcast(double& u, double m, double tn) {
+  asm("s_nop 1\n\tv_fmac_f64_dpp %0, %1, %2 row_newbcast:%3 row_mask:0xf bank_mask:0xf bound_ctrl:1"
+      : "+v"(u)
+      : "v"(m), "v"(tn), "i"(K));
+}
+
+// The same for eight rows u[i] with the multipliers of lanes B + i, after
+// one s_nop (the eight FMAs write no register that another of them reads).
+template <int B>
+__device__ __forceinline__ void fmac8_bcast(double* u, double m, double tn) {
+#define RXNN_FMAC_DPP(d, k) \
+  "v_fmac_f64_dpp %" #d ", %8, %9 row_newbcast:%" #k " row_mask:0xf bank_mask:0xf bound_ctrl:1\n\t"
+  asm("s_nop 1\n\t" RXNN_FMAC_DPP(0, 10) RXNN_FMAC_DPP(1, 11) RXNN_FMAC_DPP(2, 12)
+          RXNN_FMAC_DPP(3, 13) RXNN_FMAC_DPP(4, 14) RXNN_FMAC_DPP(5, 15) RXNN_FMAC_DPP(6, 16)
+              RXNN_FMAC_DPP(7, 17)
+      : "+v"(u[0]), "+v"(u[1]), "+v"(u[2]), "+v"(u[3]), "+v"(u[4]), "+v"(u[5]), "+v"(u[6]),
+        "+v"(u[7])
+      : "v"(m), "v"(tn), "i"(B), "i"(B + 1), "i"(B + 2), "i"(B + 3), "i"(B + 4), "i"(B + 5),
+        "i"(B + 6), "i"(B + 7));
+#undef RXNN_FMAC_DPP
+}
+
+// U[x0 + i] -= m(lane B + i of this row of 16 lanes) * t for the rows x0 + i
+// of a chunk of 8 with x0 + i >= lo, given tn = -t (the same rounded result
+// as negating the multiplier)
+template <int B, int N, int... I>
+__device__ __forceinline__ void fma8_bcast_seq(double (&U)[N], int x0, int lo, double m, double tn,
+                                               std::integer_sequence<int, I...>) {
+  ((x0 + I >= lo && x0 + I < N ? fmac_bcast<B + I>(U[x0 + I], m, tn) : (void)0), ...);
+}
+template <int B, int N>
+__device__ __forceinline__ void fma8_bcast(double (&U)[N], int x0, int lo, double m, double tn) {
+  if (x0 >= lo && x0 + 8 <= N) fmac8_bcast<B>(U + x0, m, tn);
+  else fma8_bcast_seq<B>(U, x0, lo, m, tn, std::make_integer_sequence<int, 8>{});
+}
+
 // Buffer descriptor over [p, p + bytes) with a wave-uniform base and size:
 // loads through it take a per-lane 32-bit offset and a scalar offset, so a
 // gather of many rows holds no 64-bit address per load.
@@ -1248,6 +1291,8 @@ __global__ __launch_bounds__(512) void k_nd_cut(NdArgs na) {
   }
   if (y < C) rowb[0][y] = U[0];
   const lds_f64* rbase = opaque_lds<lds_f64>(&rowb[0][0]);
+  constexpr int G = C < 16 ? C : 16;   // rows per multiplier read
+  const int lg = y & (G - 1);
 #pragma clang loop unroll(full)
   for (int k = 0; k < C; ++k) {
     __syncthreads();
@@ -1262,22 +1307,27 @@ __global__ __launch_bounds__(512) void k_nd_cut(NdArgs na) {
       U[k + 1] = fma(-rb[k + 1], t, U[k + 1]);
       if (y < C) rowb[(k + 1) & 1][y] = U[k + 1];
     }
-    // chunks of 8 rows, software pipelined: the next chunk's reads are
-    // issued before this chunk's FMAs, and a fence after the FMAs pins the
-    // updated rows here
-    double ra[8], rn[8];
+    // rows k + 2 .. in groups of G: lane l of every row of 16 lanes reads
+    // the multiplier of row g0 + l % G (one LDS read per group, where each
+    // lane reading every multiplier would make the loop bound by LDS
+    // bandwidth), and the FMA of row g0 + i takes it from lane i of its
+    // row of lanes (DPP row broadcast); t is negated instead of the
+    // multiplier, which gives the same rounded result
+    const double tn = -t;
+    double m[C / G];
 #pragma clang loop unroll(full)
-    for (int i = 0; i < 8; ++i) ra[i] = (k + 2 + i < C) ? rb[k + 2 + i] : 0.0;
+    for (int g0 = 0; g0 < C; g0 += G)
+      if (g0 + G > k + 2) m[g0 / G] = rb[g0 + lg];
 #pragma clang loop unroll(full)
-    for (int x0 = k + 2; x0 < C; x0 += 8) {
+    for (int g0 = 0; g0 < C; g0 += G) {
+      if (g0 + G <= k + 2) continue;
 #pragma clang loop unroll(full)
-      for (int i = 0; i < 8; ++i) rn[i] = (x0 + 8 + i < C) ? rb[x0 + 8 + i] : 0.0;
-#pragma clang loop unroll(full)
-      for (int i = 0; i < 8; ++i)
-        if (x0 + i < C) U[x0 + i] = fma(-ra[i], t, U[x0 + i]);
-      pin8(U, x0);
-#pragma clang loop unroll(full)
-      for (int i = 0; i < 8; ++i) ra[i] = rn[i];
+      for (int x0 = g0; x0 < g0 + G; x0 += 8) {
+        if (x0 + 8 <= k + 2) continue;
+        if (x0 % G == 0) fma8_bcast<0>(U, x0, k + 2, m[g0 / G], tn);
+        else fma8_bcast<8>(U, x0, k + 2, m[g0 / G], tn);
+        pin8(U, x0);
+      }
     }
   }
   __syncthreads();
@@ -1410,11 +1460,13 @@ __global__ __launch_bounds__(512) void k_nd_cut(NdArgs na) {
 // holding row k publishes it in LDS with the entries at and left of the
 // pivot column set to zero, so that every lane applies the pivot to all its
 // rows with one FMA each and no row test (a zero multiplier leaves a row
-// unchanged); chunks of 8 rows wholly at or above the pivot are skipped.  The
-// pivot loop runs over blocks of 8 pivots unrolled, which keeps the code
-// small.  Z (the eliminated rows scaled by D^-1/2, over this panel's
-// externals) goes to scratch for k_nd_schur or, for the final step, for
-// k_nd_gprod.
+// unchanged); chunks of 8 rows wholly at or above the pivot are skipped.
+// Every lane reads one multiplier per 16 rows from LDS and the FMAs take them
+// by DPP row broadcast (the LDS traffic of every lane reading every
+// multiplier would bound the loop).  The pivot loop runs over blocks of 8
+// pivots unrolled, which keeps the code small.  Z (the eliminated rows scaled
+// by D^-1/2, over this panel's externals) goes to scratch for k_nd_schur or,
+// for the final step, for k_nd_gprod.
 // ---------------------------------------------------------------------------
 constexpr int C2 = 128;              // cut nodes
 constexpr int P2 = 256;              // external columns per panel
@@ -1427,7 +1479,8 @@ __global__ __launch_bounds__(2 * CP2) void k_nd_cut2(NdArgs na) {
   __shared__ double rowb[2][CP2];
   __shared__ double pivs[2];
   __shared__ double dg[C2];
-  const int yl = threadIdx.x % CP2, rg = threadIdx.x / CP2;   // rg: uniform per wave
+  // rg: uniform per wave (CP2 is a multiple of 64), kept in a scalar register
+  const int yl = threadIdx.x % CP2, rg = __builtin_amdgcn_readfirstlane(threadIdx.x / CP2);
   const int T = na.T;
   int64_t la;
   int E, zld, pn;
@@ -1486,6 +1539,7 @@ __global__ __launch_bounds__(2 * CP2) void k_nd_cut2(NdArgs na) {
   // row 0 (row group 0), zero at and left of the pivot
   if (rg == 0) rowb[0][yl] = yl > 0 ? U[0] : 0.0;
   if (rg == 0 && yl == 0) pivs[0] = U[0];
+  const int l16 = threadIdx.x & 15;
   const lds_f64* rbase = opaque_lds<lds_f64>(&rowb[0][0]);
 #pragma unroll 1
   for (int q = 0; q < C2 / 8; ++q) {
@@ -1496,17 +1550,25 @@ __global__ __launch_bounds__(2 * CP2) void k_nd_cut2(NdArgs na) {
       const lds_f64* rb = rbase + (k & 1) * CP2;
       const double piv = pivs[k & 1];
       if (threadIdx.x == 0) dg[k] = piv;
-      const double t = rb[yl] * recip(piv);
+      // negated t: the same rounded result as negating the multiplier
+      const double tn = -(rb[yl] * recip(piv));
+      // lane l of every row of 16 lanes reads the multiplier of row
+      // xb + l % 16 (xb = 64 rg + 16 j); row xb + i takes it from lane i
+      // (DPP row broadcast)
+      double m[4];
 #pragma clang loop unroll(full)
-      for (int j = 0; j < 8; ++j) {
-        const int xb = 64 * rg + 8 * j;
-        if (xb + 7 > k) {
-          double rr[8];
+      for (int j = 0; j < 4; ++j)
+        if (64 * rg + 16 * j + 15 > k) m[j] = rb[64 * rg + 16 * j + l16];
 #pragma clang loop unroll(full)
-          for (int i = 0; i < 8; ++i) rr[i] = rb[xb + i];
+      for (int j = 0; j < 4; ++j) {
+        const int xb = 64 * rg + 16 * j;
 #pragma clang loop unroll(full)
-          for (int i = 0; i < 8; ++i) U[8 * j + i] = fma(-rr[i], t, U[8 * j + i]);
-          pin8(U, 8 * j);
+        for (int h = 0; h < 2; ++h) {
+          if (xb + 8 * h + 7 > k) {
+            if (h == 0) fma8_bcast<0>(U, 16 * j, 0, m[j], tn);
+            else fma8_bcast<8>(U, 16 * j + 8, 0, m[j], tn);
+            pin8(U, 16 * j + 8 * h);
+          }
         }
       }
       // publish row k + 1 from its row group
