@@ -1476,9 +1476,12 @@ constexpr int MAXSLOT2 = 1024;       // slots of a merge with 128 cut nodes (<= 
 template <bool FINAL>
 __global__ __launch_bounds__(2 * CP2) void k_nd_cut2(NdArgs na) {
   __shared__ short invt[2][FINAL ? 1 : MAXSLOT2];
-  __shared__ double rowb[2][CP2];
-  __shared__ double pivs[2];
+  __shared__ double rowb[2][2][CP2];   // [pair parity][row of the pair][column]
+  __shared__ double pivs[2][3];
   __shared__ double dg[C2];
+  // a wave's batch of 8 rows on its way to the lanes of their columns
+  constexpr int TBL = 65;
+  __shared__ double tb[FINAL ? 1 : 2 * CP2 / 64][FINAL ? 1 : 8 * TBL];
   // rg: uniform per wave (CP2 is a multiple of 64), kept in a scalar register
   const int yl = threadIdx.x % CP2, rg = __builtin_amdgcn_readfirstlane(threadIdx.x / CP2);
   const int T = na.T;
@@ -1518,69 +1521,133 @@ __global__ __launch_bounds__(2 * CP2) void k_nd_cut2(NdArgs na) {
     z = na.scratch + la * na.scr_stride + (int64_t)g.m * g.Emax * C2;
     const double* Y0 = na.buf_in + la * na.in_stride + (int64_t)g.cm0 * g.Ein * g.Ein;
     const double* Y1 = na.buf_in + la * na.in_stride + (int64_t)g.cm1 * g.Ein * g.Ein;
-    const int e = pn * P2 + (yl - C2);
-    const int slot = yl < C2 ? yl : (e < E ? C2 + e : -1);
-    const int pb0 = slot >= 0 ? invt[0][slot] : -1, pb1 = slot >= 0 ? invt[1][slot] : -1;
     const unsigned cb = (unsigned)(g.Ein * g.Ein * 8);
     const __amdgpu_buffer_rsrc_t r0 = nd_rsrc(Y0, cb), r1 = nd_rsrc(Y1, cb);
+    // batches of 8 rows: lane l loads the entry of row x0 + l % 8 and column
+    // c0 + 8 s + l / 8 (s = 0 .. 7), so that eight lanes read 64 contiguous
+    // bytes whichever mirror position of the entry the child stores (lower
+    // tiles only); the batch passes through LDS to the lanes of its columns
+    const int lane = threadIdx.x & 63, xq = lane & 7, yq = lane >> 3;
+    const int c0 = yl - lane;   // the wave's first column
+    double* tw = &tb[threadIdx.x >> 6][0];
+    int qb[8];   // the ports of column c0 + 8 s + l / 8 in the children, 16 bits each
 #pragma unroll
-    for (int i = 0; i < 64; ++i) {
-      const int x = 64 * rg + i;
-      const int pa0 = __builtin_amdgcn_readfirstlane(invt[0][x]);
-      const int pa1 = __builtin_amdgcn_readfirstlane(invt[1][x]);
-      const double v0 = nd_load(r0, (pa0 >= 0 && pb0 >= 0) ? 8u * (unsigned)sym_at(pa0, pb0, g.Ein)
-                                                           : kNdOob, 0);
-      const double v1 = nd_load(r1, (pa1 >= 0 && pb1 >= 0) ? 8u * (unsigned)sym_at(pa1, pb1, g.Ein)
-                                                           : kNdOob, 0);
-      U[i] = v0 + v1;
-      if ((i & 7) == 7) pin8(U, i - 7);
+    for (int s = 0; s < 8; ++s) {
+      const int ys = c0 + 8 * s + yq, es = pn * P2 + (ys - C2);
+      const int slot = ys < C2 ? ys : (es < E ? C2 + es : -1);
+      const int q0 = slot >= 0 ? invt[0][slot] : -1, q1 = slot >= 0 ? invt[1][slot] : -1;
+      qb[s] = (q0 & 0xffff) | (q1 << 16);
+    }
+#pragma unroll
+    for (int b = 0; b < 8; ++b) {
+      const int x = 64 * rg + 8 * b + xq;
+      const int pa0 = invt[0][x], pa1 = invt[1][x];
+      double v[8];
+#pragma unroll
+      for (int s = 0; s < 8; ++s) {
+        const int pb0 = (int)(short)(qb[s] & 0xffff), pb1 = qb[s] >> 16;
+        const double v0 = nd_load(r0, (pa0 >= 0 && pb0 >= 0) ? 8u * (unsigned)sym_at(pa0, pb0, g.Ein)
+                                                             : kNdOob, 0);
+        const double v1 = nd_load(r1, (pa1 >= 0 && pb1 >= 0) ? 8u * (unsigned)sym_at(pa1, pb1, g.Ein)
+                                                             : kNdOob, 0);
+        v[s] = v0 + v1;
+      }
+#pragma unroll
+      for (int s = 0; s < 8; ++s) tw[xq * TBL + 8 * s + yq] = v[s];
+      wave_sync();
+#pragma unroll
+      for (int i = 0; i < 8; ++i) U[8 * b + i] = tw[i * TBL + lane];
+      pin8(U, 8 * b);
+      wave_sync();   // read before the next batch is written
     }
   }
-  // row 0 (row group 0), zero at and left of the pivot
-  if (rg == 0) rowb[0][yl] = yl > 0 ? U[0] : 0.0;
-  if (rg == 0 && yl == 0) pivs[0] = U[0];
+  // pivots in pairs (k, k + 1), one barrier per pair: rows k and k + 1 as
+  // they stand before pivot k are published with the entries at and left of
+  // column k + 1 set to zero, with S[k][k], S[k][k + 1], S[k + 1][k + 1]
+  // apart; every lane derives row k + 1 after pivot k (in its own column and,
+  // for the multipliers, in the columns of its row of 16 lanes), which gives
+  // the same rounded values as eliminating one pivot per barrier
+  if (rg == 0) {
+    rowb[0][0][yl] = yl > 1 ? U[0] : 0.0;
+    rowb[0][1][yl] = yl > 1 ? U[1] : 0.0;
+    if (yl == 0) pivs[0][0] = U[0];
+    if (yl == 1) {
+      pivs[0][1] = U[0];
+      pivs[0][2] = U[1];
+    }
+  }
   const int l16 = threadIdx.x & 15;
-  const lds_f64* rbase = opaque_lds<lds_f64>(&rowb[0][0]);
+  const lds_f64* rbase = opaque_lds<lds_f64>(&rowb[0][0][0]);
 #pragma unroll 1
   for (int q = 0; q < C2 / 8; ++q) {
 #pragma clang loop unroll(full)
-    for (int r = 0; r < 8; ++r) {
-      const int k = 8 * q + r;
+    for (int p = 0; p < 4; ++p) {
+      const int k = 8 * q + 2 * p, par = p & 1;
       __syncthreads();
-      const lds_f64* rb = rbase + (k & 1) * CP2;
-      const double piv = pivs[k & 1];
-      if (threadIdx.x == 0) dg[k] = piv;
-      // negated t: the same rounded result as negating the multiplier
-      const double tn = -(rb[yl] * recip(piv));
-      // lane l of every row of 16 lanes reads the multiplier of row
-      // xb + l % 16 (xb = 64 rg + 16 j); row xb + i takes it from lane i
-      // (DPP row broadcast)
-      double m[4];
-#pragma clang loop unroll(full)
-      for (int j = 0; j < 4; ++j)
-        if (64 * rg + 16 * j + 15 > k) m[j] = rb[64 * rg + 16 * j + l16];
+      const lds_f64* r0 = rbase + 2 * par * CP2;
+      const lds_f64* r1 = r0 + CP2;
+      const double d0 = pivs[par][0], s01 = pivs[par][1], e11 = pivs[par][2];
+      const double rd0 = recip(d0);
+      // S[k + 1][k + 1] after pivot k
+      const double d1 = fma(s01, -(s01 * rd0), e11);
+      if (threadIdx.x == 0) {
+        dg[k] = d0;
+        dg[k + 1] = d1;
+      }
+      // negated t of both pivots for this lane's column (the same rounded
+      // result as negating the multipliers); row k + 1 after pivot k
+      const double t0n = -(r0[yl] * rd0);
+      const double t1n = -(fma(s01, t0n, r1[yl]) * recip(d1));
+      // lane l of every row of 16 lanes takes the multipliers of row
+      // xb + l % 16 (xb = 64 rg + 16 j) for both pivots; row xb + i takes
+      // them from lane i (DPP row broadcast)
 #pragma clang loop unroll(full)
       for (int j = 0; j < 4; ++j) {
         const int xb = 64 * rg + 16 * j;
+        if (xb + 15 > k + 1) {
+          const double m0 = r0[xb + l16];
+          const double m1 = fma(s01, -(m0 * rd0), r1[xb + l16]);
 #pragma clang loop unroll(full)
-        for (int h = 0; h < 2; ++h) {
-          if (xb + 8 * h + 7 > k) {
-            if (h == 0) fma8_bcast<0>(U, 16 * j, 0, m[j], tn);
-            else fma8_bcast<8>(U, 16 * j + 8, 0, m[j], tn);
-            pin8(U, 16 * j + 8 * h);
+          for (int h = 0; h < 2; ++h) {
+            if (xb + 8 * h + 7 > k + 1) {
+              if (h == 0) {
+                fma8_bcast<0>(U, 16 * j, 0, m0, t0n);
+                fma8_bcast<0>(U, 16 * j, 0, m1, t1n);
+              } else {
+                fma8_bcast<8>(U, 16 * j + 8, 0, m0, t0n);
+                fma8_bcast<8>(U, 16 * j + 8, 0, m1, t1n);
+              }
+              pin8(U, 16 * j + 8 * h);
+            }
           }
         }
       }
-      // publish row k + 1 from its row group
-      const int k1 = k + 1;
-      if (k1 < C2 && rg == (k1 >> 6)) {
-        const int jj = (k1 & 63) >> 3;
-        double v = 0.0;
+      // row k + 1 in its row group: its value after pivot k (its published
+      // entries at the pair's columns were zero, so the loop left it as is)
+      if (rg == (k >> 6)) {
+        const int jj = (k & 63) >> 3;
 #pragma clang loop unroll(full)
         for (int j = 0; j < 8; ++j)
-          if (j == jj) v = U[8 * j + ((r + 1) & 7)];
-        rowb[k1 & 1][yl] = yl > k1 ? v : 0.0;
-        if (yl == k1) pivs[k1 & 1] = v;
+          if (j == jj) U[8 * j + 2 * p + 1] = fma(s01, t0n, U[8 * j + 2 * p + 1]);
+      }
+      // publish rows k + 2 and k + 3 from their row group
+      const int k2 = k + 2;
+      if (k2 < C2 && rg == (k2 >> 6)) {
+        const int jj = (k2 & 63) >> 3, np = par ^ 1;
+        double v2 = 0.0, v3 = 0.0;
+#pragma clang loop unroll(full)
+        for (int j = 0; j < 8; ++j)
+          if (j == jj) {
+            v2 = U[8 * j + ((2 * p + 2) & 7)];
+            v3 = U[8 * j + ((2 * p + 3) & 7)];
+          }
+        rowb[np][0][yl] = yl > k2 + 1 ? v2 : 0.0;
+        rowb[np][1][yl] = yl > k2 + 1 ? v3 : 0.0;
+        if (yl == k2) pivs[np][0] = v2;
+        if (yl == k2 + 1) {
+          pivs[np][1] = v2;
+          pivs[np][2] = v3;
+        }
       }
     }
   }
