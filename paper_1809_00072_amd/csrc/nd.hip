@@ -1193,6 +1193,11 @@ __global__ __launch_bounds__(512) void k_nd_cut(NdArgs na) {
   constexpr bool kFuse = MODE == 0 && C <= 32;
   constexpr int ZLD = C <= 8 ? 52 : (C <= 16 ? 100 : 196);   // Z row stride in LDS
   __shared__ __attribute__((aligned(16))) double zl[kFuse ? C * ZLD : 1];
+  // merges with 64 cut rows: a wave's batch of 8 rows of the gather on its
+  // way to the lanes of their columns
+  constexpr bool kTGather = MODE == 0 && C == 64;
+  constexpr int TBL = 65;
+  __shared__ double tb[kTGather ? 8 : 1][kTGather ? 8 * TBL : 1];
   const int y = threadIdx.x;
   const int T = na.T;
   int E, ncol, Emax = 0;
@@ -1270,22 +1275,62 @@ __global__ __launch_bounds__(512) void k_nd_cut(NdArgs na) {
     const unsigned cb = (unsigned)(g.Ein * g.Ein * 8);
     const __amdgpu_buffer_rsrc_t r0 = nd_rsrc(Y0, cb), r1 = nd_rsrc(Y1, cb);
     const lds_i16* iv = opaque_lds<lds_i16>(&invt[0][0]);
-    // the row's port is uniform, the column's fixed per lane; an entry
-    // without a port takes the out-of-range offset, so it reads 0 without a
-    // memory access, and every load of a chunk stays in flight together
+    if constexpr (kTGather) {
+      // batches of 8 rows: lane l loads the entry of row x0 + l % 8 and
+      // column c0 + 8 s + l / 8 (s = 0 .. 7), so that eight lanes read 64
+      // contiguous bytes whichever mirror position of the entry the child
+      // stores (lower tiles only); the batch passes through LDS to the lanes
+      // of its columns
+      const int lane = y & 63, xq = lane & 7, yq = lane >> 3;
+      const int c0 = y - lane;   // the wave's first column
+      double* tw = &tb[y >> 6][0];
+      int qb[8];   // the ports of column c0 + 8 s + l / 8 in the children, 16 bits each
 #pragma unroll
-    for (int x = 0; x < C; ++x) {
-      const int pa0 = __builtin_amdgcn_readfirstlane(iv[x]);
-      const int pa1 = __builtin_amdgcn_readfirstlane(iv[MAXSLOT + x]);
-      const double v0 = nd_load(r0, (pa0 >= 0 && pb0 >= 0) ? 8u * (unsigned)sym_at(pa0, pb0, g.Ein)
-                                                           : kNdOob, 0);
-      const double v1 = nd_load(r1, (pa1 >= 0 && pb1 >= 0) ? 8u * (unsigned)sym_at(pa1, pb1, g.Ein)
-                                                           : kNdOob, 0);
-      U[x] = v0 + v1;
-      // 16 rows (32 loads) in flight per round trip
-      if ((x & 15) == 15) {
-        pin8(U, x - 15);
-        pin8(U, x - 7);
+      for (int s = 0; s < 8; ++s) {
+        const int ys = c0 + 8 * s + yq;
+        const int sl = ys < C ? ys : (ys < ncol ? C + ebase + (ys - C) : -1);
+        const int q0 = sl >= 0 ? invt[0][sl] : -1, q1 = sl >= 0 ? invt[1][sl] : -1;
+        qb[s] = (q0 & 0xffff) | (q1 << 16);
+      }
+#pragma unroll
+      for (int b = 0; b < C / 8; ++b) {
+        const int pa0 = iv[8 * b + xq], pa1 = iv[MAXSLOT + 8 * b + xq];
+        double v[8];
+#pragma unroll
+        for (int s = 0; s < 8; ++s) {
+          const int q0 = (int)(short)(qb[s] & 0xffff), q1 = qb[s] >> 16;
+          const double v0 = nd_load(r0, (pa0 >= 0 && q0 >= 0) ? 8u * (unsigned)sym_at(pa0, q0, g.Ein)
+                                                              : kNdOob, 0);
+          const double v1 = nd_load(r1, (pa1 >= 0 && q1 >= 0) ? 8u * (unsigned)sym_at(pa1, q1, g.Ein)
+                                                              : kNdOob, 0);
+          v[s] = v0 + v1;
+        }
+#pragma unroll
+        for (int s = 0; s < 8; ++s) tw[xq * TBL + 8 * s + yq] = v[s];
+        wave_sync();
+#pragma unroll
+        for (int i = 0; i < 8; ++i) U[8 * b + i] = tw[i * TBL + lane];
+        pin8(U, 8 * b);
+        wave_sync();   // read before the next batch is written
+      }
+    } else {
+      // the row's port is uniform, the column's fixed per lane; an entry
+      // without a port takes the out-of-range offset, so it reads 0 without a
+      // memory access, and every load of a chunk stays in flight together
+#pragma unroll
+      for (int x = 0; x < C; ++x) {
+        const int pa0 = __builtin_amdgcn_readfirstlane(iv[x]);
+        const int pa1 = __builtin_amdgcn_readfirstlane(iv[MAXSLOT + x]);
+        const double v0 = nd_load(r0, (pa0 >= 0 && pb0 >= 0) ? 8u * (unsigned)sym_at(pa0, pb0, g.Ein)
+                                                             : kNdOob, 0);
+        const double v1 = nd_load(r1, (pa1 >= 0 && pb1 >= 0) ? 8u * (unsigned)sym_at(pa1, pb1, g.Ein)
+                                                             : kNdOob, 0);
+        U[x] = v0 + v1;
+        // 16 rows (32 loads) in flight per round trip
+        if ((x & 15) == 15) {
+          pin8(U, x - 15);
+          pin8(U, x - 7);
+        }
       }
     }
   }
