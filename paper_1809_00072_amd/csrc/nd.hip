@@ -451,10 +451,10 @@ __device__ __forceinline__ void block2x2(const MapScalars& ms, const float* W, d
 
 __device__ void region_merge16(int T, int RI, int RJ, const double* ch, double* dst,
                                double* scr);
-template <int L, int H, int W, bool VERT, int NB>
+template <int L, int H, int W, bool VERT, int NB, bool SPLIT = false>
 __device__ __forceinline__ void merge_mfma(int T, int i0, int j0, const short* tab,
                                            const double* c0, const double* c1, double* out,
-                                           int lane);
+                                           int lane, int part = 0);
 
 // One 16 x 16 region per workgroup (every build, whatever its size, so that
 // an array's arithmetic never depends on how many arrays are built with it):
@@ -462,8 +462,8 @@ __device__ __forceinline__ void merge_mfma(int T, int i0, int j0, const short* t
 // alone, without workgroup barriers, in its LDS buffers A and B: the 2 x 2
 // blocks in registers, the merges 2 x 2 -> 4 x 2 in 16-lane groups
 // (level2_dpp), then 4 x 2 -> 4 x 4 -> 8 x 4 -> 8 x 8, each by the whole
-// wave (merge_mfma).  Waves 0 and 1 then merge the
-// two columns' pairs into 16 x 8 blocks (in LDS), and the workgroup merges
+// wave (merge_mfma).  Waves m and 2 + m then merge
+// column m's pair into a 16 x 8 block (in LDS), and the workgroup merges
 // those into the region's 16 x 16 block, which goes to the level buffer.
 // LDS (78 KB) allows two workgroups per CU.
 __global__ __launch_bounds__(64 * BWAVES) void k_nd_block(NdArgs na) {
@@ -540,10 +540,12 @@ __global__ __launch_bounds__(64 * BWAVES) void k_nd_block(NdArgs na) {
   // (region row, region column) of the 16 x 16 level
   merge_mfma<5, 8, 4, false, 2>(T, I0, J0, tab, B, B + lds_mat(24), A, lane);
   __syncthreads();
-  if (wv < 2) {   // wave m: the pair of column m (children: the A buffers of waves m, 2 + m)
+  {   // waves m and 2 + m: the pair of column m (children: the A buffers of
+      // waves m, 2 + m), each wave half of its tiles
     const double* ca = &bufA[0][0];
-    merge_mfma<6, 8, 8, true, 3>(T, RI, RJ + wv * BS, tab, ca + wv * BUFA, ca + (2 + wv) * BUFA,
-                                 &bufB[0][0] + wv * lds_mat(48), lane);
+    const int m = wv & 1;
+    merge_mfma<6, 8, 8, true, 3, true>(T, RI, RJ + m * BS, tab, ca + m * BUFA, ca + (2 + m) * BUFA,
+                                       &bufB[0][0] + m * lds_mat(48), lane, wv >> 1);
   }
   __syncthreads();
   constexpr int E16 = 8 * BS;   // ports of an interior 16 x 16 block
@@ -1008,11 +1010,14 @@ __device__ __forceinline__ void tri_tile(int tt, int* tx, int* ty) {
 // rows that pad C to a multiple of 4) goes to `out` as scratch, under the
 // last tile row, and the merged block V - Z^T Z is NB x NB tiles of 16 x 16
 // (lane l: rows 16 bi + l / 16 + 4 v, column 16 bj + l % 16), each written
-// at once except the last tile row's, which waits until Z is read.
-template <int L, int H, int W, bool VERT, int NB>
+// at once except the last tile row's, which waits until Z is read.  SPLIT:
+// two waves share the merge (every wave of the workgroup calls it, so the
+// waits are workgroup barriers): both eliminate, part 0 writes Z and takes
+// the first half of the tiles in row-major order, part 1 the rest.
+template <int L, int H, int W, bool VERT, int NB, bool SPLIT>
 __device__ __forceinline__ void merge_mfma(int T, int i0, int j0, const short* tab,
                                            const double* c0, const double* c1, double* out,
-                                           int lane) {
+                                           int lane, int part) {
   constexpr int NH = VERT ? 2 * H : H, NW = VERT ? W : 2 * W;
   constexpr int C = VERT ? W : H;
   constexpr int EM = 2 * (NH + NW), EIN = 2 * (H + W), ZS = 16 * NB, CK = (C + 3) & ~3;
@@ -1042,12 +1047,13 @@ __device__ __forceinline__ void merge_mfma(int T, int i0, int j0, const short* t
     for (int x = k + 1; x < C; ++x) U[x] = fma(-readlane_d(U[x], k), t, U[x]);
   }
   double* z = out + 16 * (NB - 1) * EM;
-  if (lane >= C && lane < C + 16 * NB) {
+  if (lane >= C && lane < C + 16 * NB && (!SPLIT || part == 0)) {
     const int e = lane - C;
 #pragma unroll
     for (int k = 0; k < CK; ++k) z[k * ZS + e] = (k < C && e < E) ? U[k] * sq[k] : 0.0;
   }
-  wave_sync();
+  if constexpr (SPLIT) __syncthreads();
+  else wave_sync();
   const int lr = lane >> 4, lc = lane & 15;
   // tile by tile (few registers live): its product and V entries; the
   // last tile row waits in registers until every tile has read Z
@@ -1056,6 +1062,7 @@ __device__ __forceinline__ void merge_mfma(int T, int i0, int j0, const short* t
   for (int bi = 0; bi < NB; ++bi)
 #pragma unroll
     for (int bj = 0; bj < NB; ++bj) {
+      if (SPLIT && (bi * NB + bj < (NB * NB + 1) / 2) != (part == 0)) continue;
       const int yy = 16 * bj + lc;
       const int pb0 = t0[C + yy], pb1 = t1[C + yy];
       f64x4 acc = f64x4{0.0, 0.0, 0.0, 0.0};
@@ -1080,14 +1087,18 @@ __device__ __forceinline__ void merge_mfma(int T, int i0, int j0, const short* t
         }
       }
     }
-  wave_sync();   // Z read before the last tile row overwrites it
+  // Z read before the last tile row overwrites it
+  if constexpr (SPLIT) __syncthreads();
+  else wave_sync();
 #pragma unroll
-  for (int bj = 0; bj < NB; ++bj)
+  for (int bj = 0; bj < NB; ++bj) {
+    if (SPLIT && ((NB - 1) * NB + bj < (NB * NB + 1) / 2) != (part == 0)) continue;
 #pragma unroll
     for (int v = 0; v < 4; ++v) {
       const int xx = 16 * (NB - 1) + lr + 4 * v, yy = 16 * bj + lc;
       if (xx < E && yy < E) out[xx * EM + yy] = res[bj][v];
     }
+  }
   wave_sync();
 }
 
