@@ -403,10 +403,10 @@ __device__ __forceinline__ void eliminate_lead(double (&X)[N][N]) {
 // [L | R | T | B] (an absent R or T port is a zero row: no row-wire edge at
 // the right edge of the grid; at the top the cell's b-node is eliminated in
 // series), the cells of each column merged (their shared b-node eliminated),
-// then the two 2 x 1 halves (their two shared a-nodes).  Returns the 8 x 8
-// matrix over [L0 L1 | R0 R1 | T0 T1 | B0 B1] in rows 2 .. 9 of X.
-__device__ __forceinline__ void block2x2(const MapScalars& ms, const float* W, double wmax,
-                                         int64_t arr, int gi0, int gj0, int T, int row_off,
+// then the two 2 x 1 halves (their two shared a-nodes); Gc[r][c] is the
+// conductance of cell (gi0 + r, gj0 + c).  Returns the 8 x 8 matrix over
+// [L0 L1 | R0 R1 | T0 T1 | B0 B1] in rows 2 .. 9 of X.
+__device__ __forceinline__ void block2x2(const double (&Gc)[2][2], int gi0, int gj0, int T,
                                          double g_r, double g_c, double g_s, double (&X)[10][10]) {
 #pragma unroll
   for (int i = 0; i < 10; ++i)
@@ -424,7 +424,7 @@ __device__ __forceinline__ void block2x2(const MapScalars& ms, const float* W, d
 #pragma unroll
     for (int r = 0; r < 2; ++r) {
       const int gi = gi0 + r, gj = gj0 + c;
-      const double G = cell_conductance(ms, W, wmax, arr, gi, gj, row_off);
+      const double G = Gc[r][c];
       const bool hasT = gi > 0;
       const double gv = (gi + 1 < T) ? g_c : g_s;
       const int iL = 1 + r, iR = 3 + r, iT = r == 0 ? 5 : 0, iB = r == 0 ? 0 : 6;
@@ -491,11 +491,24 @@ __global__ __launch_bounds__(64 * BWAVES) void k_nd_block(NdArgs na) {
   // levels 1 x 1 .. 2 x 2 in registers, lane q < 16 taking 2 x 2 block q,
   // written to A with ports [L | R (not at the right edge) | T (not at the
   // top) | B], row stride 8, lds_mat(8) apart
+  {
+    // the 64 cells' conductances, one per lane (lane q + 16 r + 32 c: row r,
+    // column c of 2 x 2 block q), through B to the lanes of their blocks
+    const int q = lane & 15, r = (lane >> 4) & 1, c = lane >> 5;
+    B[lane] = cell_conductance(ms, ref.W, wmax, arr, I0 + 2 * (q >> 2) + r, J0 + 2 * (q & 3) + c,
+                               na.row_off);
+  }
+  wave_sync();
   if (lane < 16) {
     const int qi = lane >> 2, qj = lane & 3;
     const int gi0 = I0 + 2 * qi, gj0 = J0 + 2 * qj;
+    double Gc[2][2];
+#pragma unroll
+    for (int r = 0; r < 2; ++r)
+#pragma unroll
+      for (int c = 0; c < 2; ++c) Gc[r][c] = B[lane + 16 * r + 32 * c];
     double X[10][10];
-    block2x2(ms, ref.W, wmax, arr, gi0, gj0, T, na.row_off, na.g_r, na.g_c, na.g_s, X);
+    block2x2(Gc, gi0, gj0, T, na.g_r, na.g_c, na.g_s, X);
     const bool rn = gj0 + 2 < T, tn = gi0 > 0;
     const int oT = rn ? 4 : 2, oB = oT + (tn ? 2 : 0);
     // padded port -> stored port (-1: absent)
