@@ -1217,9 +1217,9 @@ __global__ __launch_bounds__(512) void k_nd_cut(NdArgs na) {
   constexpr bool kFuse = MODE == 0 && C <= 32;
   constexpr int ZLD = C <= 8 ? 52 : (C <= 16 ? 100 : 196);   // Z row stride in LDS
   __shared__ __attribute__((aligned(16))) double zl[kFuse ? C * ZLD : 1];
-  // merges with 64 cut rows: a wave's batch of 8 rows of the gather on its
-  // way to the lanes of their columns
-  constexpr bool kTGather = MODE == 0 && C == 64;
+  // merges and dense stages with 64 cut rows: a wave's batch of 8 rows of
+  // the gather on its way to the lanes of their columns
+  constexpr bool kTGather = (MODE == 0 || MODE == 2) && C == 64;
   constexpr int TBL = 65;
   __shared__ double tb[kTGather ? 8 : 1][kTGather ? 8 * TBL : 1];
   const int y = threadIdx.x;
@@ -1246,13 +1246,43 @@ __global__ __launch_bounds__(512) void k_nd_cut(NdArgs na) {
     // the pivot rows' entries A[x][col] are read as A[col][x] (A is
     // symmetric, and a stage writes only its lower tiles)
     const __amdgpu_buffer_rsrc_t ra = nd_rsrc(A, (unsigned)(na.dn * na.dld * 8));
+    if constexpr (kTGather) {
+      // batches of 8 rows in 8 x 8 blocks through LDS, as for the merges:
+      // lane l loads entry x0 + l % 8 of column c0 + 8 s + l / 8, eight lanes
+      // 64 contiguous bytes of one row of A
+      const int lane = y & 63, xq = lane & 7, yq = lane >> 3;
+      const int c0 = y - lane;   // the wave's first column
+      double* tw = &tb[y >> 6][0];
+      unsigned ro[8];            // byte offsets of the columns' rows of A (out of range: none)
 #pragma unroll
-    for (int x = 0; x < C; ++x) {
-      const double v = nd_load(ra, 8u * (unsigned)(col * na.dld), 8u * (unsigned)x);
-      U[x] = y < ncol ? v : 0.0;
-      if ((x & 15) == 15) {
-        pin8(U, x - 15);
-        pin8(U, x - 7);
+      for (int s = 0; s < 8; ++s) {
+        const int ys = c0 + 8 * s + yq;
+        const int cs = ys < C ? ys : (ys < ncol ? C + ebase + (ys - C) : -1);
+        ro[s] = cs >= 0 ? 8u * (unsigned)(cs * na.dld) : kNdOob;
+      }
+#pragma unroll
+      for (int b = 0; b < C / 8; ++b) {
+        double v[8];
+#pragma unroll
+        for (int s = 0; s < 8; ++s)
+          v[s] = nd_load(ra, ro[s] == kNdOob ? kNdOob : ro[s] + 8u * (unsigned)(8 * b + xq), 0);
+#pragma unroll
+        for (int s = 0; s < 8; ++s) tw[xq * TBL + 8 * s + yq] = v[s];
+        wave_sync();
+#pragma unroll
+        for (int i = 0; i < 8; ++i) U[8 * b + i] = tw[i * TBL + lane];
+        pin8(U, 8 * b);
+        wave_sync();   // read before the next batch is written
+      }
+    } else {
+#pragma unroll
+      for (int x = 0; x < C; ++x) {
+        const double v = nd_load(ra, 8u * (unsigned)(col * na.dld), 8u * (unsigned)x);
+        U[x] = y < ncol ? v : 0.0;
+        if ((x & 15) == 15) {
+          pin8(U, x - 15);
+          pin8(U, x - 7);
+        }
       }
     }
   } else if constexpr (FINAL) {
