@@ -325,6 +325,18 @@ __device__ __forceinline__ double rowbcast_d(double v, int k) {
   }
 }
 
+// The region kernel's LDS matrices (row stride ein, lds_mat(ein) apart)
+// hold a zero in the slot after their last entry, index ein * ein.  A
+// column's key: its port, or a large negative number when the port is
+// absent (computed once per column).
+__device__ __forceinline__ int col_key(int s) { return s < 0 ? -(1 << 20) : s; }
+// Entry (r, column key sk) of such a matrix: an absent row port (r < 0) or
+// column port makes the index negative, and the unsigned minimum turns it
+// into the zero slot, so neither case needs a select of the value.
+__device__ __forceinline__ double pick(const double* c, int r, int sk, int ein) {
+  return c[min((unsigned)(r * ein + sk), (unsigned)(ein * ein))];
+}
+
 // The eight 2 x 2 -> 4 x 2 merges of a wave's 8 x 8 block (children
 // lds_mat(8) apart in `in`, results lds_mat(12) apart in `out`), in two
 // passes of four, a group of 16 lanes per merge: lane y holds column y of
@@ -348,15 +360,10 @@ __device__ __forceinline__ void level2_dpp(int T, int I0, int J0, const short* t
     const short* t1 = t0 + 64;
     const double* c0 = in + cm0 * lds_mat(EIN);
     const double* c1 = in + cm1 * lds_mat(EIN);
-    const int s0 = t0[yl], s1 = t1[yl];
+    const int k0 = col_key(t0[yl]), k1 = col_key(t1[yl]);
     double U[LD];
 #pragma unroll
-    for (int x = 0; x < LD; ++x) {
-      const int r0 = t0[x], r1 = t1[x];
-      const double a = c0[max(r0, 0) * EIN + max(s0, 0)];
-      const double b = c1[max(r1, 0) * EIN + max(s1, 0)];
-      U[x] = ((r0 >= 0 && s0 >= 0) ? a : 0.0) + ((r1 >= 0 && s1 >= 0) ? b : 0.0);
-    }
+    for (int x = 0; x < LD; ++x) U[x] = pick(c0, t0[x], k0, EIN) + pick(c1, t1[x], k1, EIN);
 #pragma unroll
     for (int k = 0; k < C; ++k) {
       const double t = U[k] * recip(rowbcast_d(U[k], k));
@@ -368,6 +375,7 @@ __device__ __forceinline__ void level2_dpp(int T, int I0, int J0, const short* t
       for (int x = C; x < LD; ++x)
         if (x < ld) out[m * lds_mat(EM) + (x - C) * EM + (yl - C)] = U[x];
     }
+    if (yl == 0) out[m * lds_mat(EM) + EM * EM] = 0.0;   // the zero slot
   }
   wave_sync();
 }
@@ -529,6 +537,7 @@ __global__ __launch_bounds__(64 * BWAVES) void k_nd_block(NdArgs na) {
         const double v = p >= q ? X[2 + p][2 + q] : X[2 + q][2 + p];
         if (pos[p] >= 0 && pos[q] >= 0) o[pos[p] * 8 + pos[q]] = v;
       }
+    o[64] = 0.0;   // the zero slot
   }
   wave_sync();
   level2_dpp(T, I0, J0, tab, A, B, lane);
@@ -1041,15 +1050,10 @@ __device__ __forceinline__ void merge_mfma(int T, int i0, int j0, const short* t
   const int E = NH + (rn ? NH : 0) + (tn ? NW : 0) + NW;   // ports of the merged block
   const short* t0 = tab + (((L * 4) + (rn ? 2 : 0) + (tn ? 1 : 0)) * 2) * 64;
   const short* t1 = t0 + 64;
-  const int s0 = t0[lane], s1 = t1[lane];
+  const int k0 = col_key(t0[lane]), k1 = col_key(t1[lane]);
   double U[C];
 #pragma unroll
-  for (int x = 0; x < C; ++x) {
-    const int r0 = t0[x], r1 = t1[x];
-    const double a = c0[max(r0, 0) * EIN + max(s0, 0)];
-    const double b = c1[max(r1, 0) * EIN + max(s1, 0)];
-    U[x] = ((r0 >= 0 && s0 >= 0) ? a : 0.0) + ((r1 >= 0 && s1 >= 0) ? b : 0.0);
-  }
+  for (int x = 0; x < C; ++x) U[x] = pick(c0, t0[x], k0, EIN) + pick(c1, t1[x], k1, EIN);
   double sq[C];
 #pragma unroll
   for (int k = 0; k < C; ++k) {
@@ -1077,7 +1081,7 @@ __device__ __forceinline__ void merge_mfma(int T, int i0, int j0, const short* t
     for (int bj = 0; bj < NB; ++bj) {
       if (SPLIT && (bi * NB + bj < (NB * NB + 1) / 2) != (part == 0)) continue;
       const int yy = 16 * bj + lc;
-      const int pb0 = t0[C + yy], pb1 = t1[C + yy];
+      const int kb0 = col_key(t0[C + yy]), kb1 = col_key(t1[C + yy]);
       f64x4 acc = f64x4{0.0, 0.0, 0.0, 0.0};
 #pragma unroll
       for (int k4 = 0; k4 < CK; k4 += 4) {
@@ -1088,11 +1092,8 @@ __device__ __forceinline__ void merge_mfma(int T, int i0, int j0, const short* t
 #pragma unroll
       for (int v = 0; v < 4; ++v) {
         const int xx = 16 * bi + lr + 4 * v;
-        const int pa0 = t0[C + xx], pa1 = t1[C + xx];
-        const double a = c0[max(pa0, 0) * EIN + max(pb0, 0)];
-        const double b = c1[max(pa1, 0) * EIN + max(pb1, 0)];
         const double r =
-            ((pa0 >= 0 && pb0 >= 0) ? a : 0.0) + ((pa1 >= 0 && pb1 >= 0) ? b : 0.0) - acc[v];
+            pick(c0, t0[C + xx], kb0, EIN) + pick(c1, t1[C + xx], kb1, EIN) - acc[v];
         if (bi + 1 < NB) {
           if (xx < E && yy < E) out[xx * EM + yy] = r;
         } else {
@@ -1112,6 +1113,7 @@ __device__ __forceinline__ void merge_mfma(int T, int i0, int j0, const short* t
       if (xx < E && yy < E) out[xx * EM + yy] = res[bj][v];
     }
   }
+  if (lane == 0 && (!SPLIT || part == 0)) out[EM * EM] = 0.0;   // the zero slot
   wave_sync();
 }
 
@@ -1145,15 +1147,10 @@ __device__ void region_merge16(int T, int RI, int RJ, const double* ch, double* 
   const int wv = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
   if (wv < 2) {
     const int y = lane < C ? lane : C + 48 * wv + (lane - C);   // combined column
-    const int pb0 = y < C + E ? invt[y] : -1, pb1 = y < C + E ? invt[80 + y] : -1;
+    const int kb0 = col_key(y < C + E ? invt[y] : -1), kb1 = col_key(y < C + E ? invt[80 + y] : -1);
     double U[C];
 #pragma unroll
-    for (int x = 0; x < C; ++x) {
-      const int pa0 = invt[x], pa1 = invt[80 + x];
-      const double a = ch[max(pa0, 0) * EIN + max(pb0, 0)];
-      const double b = ch[CH1 + max(pa1, 0) * EIN + max(pb1, 0)];
-      U[x] = ((pa0 >= 0 && pb0 >= 0) ? a : 0.0) + ((pa1 >= 0 && pb1 >= 0) ? b : 0.0);
-    }
+    for (int x = 0; x < C; ++x) U[x] = pick(ch, invt[x], kb0, EIN) + pick(ch + CH1, invt[80 + x], kb1, EIN);
     double sq[C];
 #pragma unroll
     for (int k = 0; k < C; ++k) {
@@ -1175,16 +1172,13 @@ __device__ void region_merge16(int T, int RI, int RJ, const double* ch, double* 
 #pragma unroll
   for (int j = 0; j < 2; ++j) {
     const int yy = min(mt.col(j), E - 1);
-    const int qb0 = invt[C + yy], qb1 = invt[80 + C + yy];
+    const int kb0 = col_key(invt[C + yy]), kb1 = col_key(invt[80 + C + yy]);
 #pragma unroll
     for (int i = 0; i < 2; ++i)
 #pragma unroll
       for (int v = 0; v < 4; ++v) {
         const int x = min(mt.row(i, v), E - 1);
-        const int qa0 = invt[C + x], qa1 = invt[80 + C + x];
-        const double a = ch[max(qa0, 0) * EIN + max(qb0, 0)];
-        const double b = ch[CH1 + max(qa1, 0) * EIN + max(qb1, 0)];
-        vv[i][j][v] = ((qa0 >= 0 && qb0 >= 0) ? a : 0.0) + ((qa1 >= 0 && qb1 >= 0) ? b : 0.0);
+        vv[i][j][v] = pick(ch, invt[C + x], kb0, EIN) + pick(ch + CH1, invt[80 + C + x], kb1, EIN);
       }
   }
   mt.step_ld(zl, zl, ZL, C, E, E);
@@ -1839,6 +1833,11 @@ __global__ __launch_bounds__(256) void k_nd_dense0(NdArgs na) {
   const int64_t la = blockIdx.x / nrb;
   const int x0 = (int)(blockIdx.x % nrb) * 16;
   double* B = na.dB + la * na.out_stride;
+  // the 16 rows share their lower tiles' column range [0, ylim); for a merge
+  // 64 threads take an 8 x 8 block (lane l: row l % 8, column l / 8), so
+  // that eight lanes read 64 contiguous bytes whichever mirror position of
+  // the entry the child stores, and write 64 contiguous bytes of a row
+  const int ylim = min(n, (x0 / 64 + 1) * 64), nyb = (ylim + 7) / 8;
   if constexpr (FINAL) {
     const int T = na.T, M = na.ms.M, Ein = 4 * T;
     const double* Y = na.buf_in + la * na.in_stride;
@@ -1846,7 +1845,7 @@ __global__ __launch_bounds__(256) void k_nd_dense0(NdArgs na) {
     auto port = [&](int i) { return i < T ? i : (i < T + M ? -1 : T + (i - T - M)); };
     for (int x = x0; x < min(x0 + 16, n); ++x) {
       const int px = port(x);
-      for (int y = threadIdx.x; y < min(n, (x / 64 + 1) * 64); y += 256) {
+      for (int y = threadIdx.x; y < ylim; y += 256) {
         if (dead_pair(na, x, y)) continue;
         const int py = port(y);
         double v = (px >= 0 && py >= 0) ? Y[sym_at(px, py, Ein)] : 0.0;
@@ -1861,16 +1860,15 @@ __global__ __launch_bounds__(256) void k_nd_dense0(NdArgs na) {
     inverse_tables<MAXSLOT2>(na, g, invt, 256);
     const double* Y0 = na.buf_in + la * na.in_stride + (int64_t)g.cm0 * g.Ein * g.Ein;
     const double* Y1 = na.buf_in + la * na.in_stride + (int64_t)g.cm1 * g.Ein * g.Ein;
-    for (int x = x0; x < min(x0 + 16, n); ++x) {
+    for (int e = threadIdx.x; e < 2 * nyb * 64; e += 256) {
+      const int x = x0 + 8 * (e / (nyb * 64)) + (e & 7), y = 8 * ((e >> 6) % nyb) + ((e >> 3) & 7);
+      if (x >= n || y >= ylim || dead_pair(na, x, y)) continue;
       const int pa0 = invt[0][x], pa1 = invt[1][x];
-      for (int y = threadIdx.x; y < min(n, (x / 64 + 1) * 64); y += 256) {
-        if (dead_pair(na, x, y)) continue;
-        const int pb0 = invt[0][y], pb1 = invt[1][y];
-        double v = 0.0;
-        if (pa0 >= 0 && pb0 >= 0) v += Y0[sym_at(pa0, pb0, g.Ein)];
-        if (pa1 >= 0 && pb1 >= 0) v += Y1[sym_at(pa1, pb1, g.Ein)];
-        B[(int64_t)x * ld + y] = v;
-      }
+      const int pb0 = invt[0][y], pb1 = invt[1][y];
+      double v = 0.0;
+      if (pa0 >= 0 && pb0 >= 0) v += Y0[sym_at(pa0, pb0, g.Ein)];
+      if (pa1 >= 0 && pb1 >= 0) v += Y1[sym_at(pa1, pb1, g.Ein)];
+      B[(int64_t)x * ld + y] = v;
     }
   }
 }
