@@ -1435,8 +1435,14 @@ __global__ __launch_bounds__(512) void k_nd_cut(NdArgs na) {
       }
       __syncthreads();
       double* ext = na.buf_out + la * na.out_stride + (int64_t)g.m * Emax * Emax;
-      const unsigned cbf = (unsigned)(g.Ein * g.Ein * 8);
-      const __amdgpu_buffer_rsrc_t r0f = nd_rsrc(Y0, cbf), r1f = nd_rsrc(Y1, cbf);
+      // an entry of V is one child's (an external port is a port of one
+      // child only): one load per entry over both children's blocks
+      const int cml = min(g.cm0, g.cm1);
+      const unsigned e2 = (unsigned)(g.Ein * g.Ein);
+      const unsigned o0 = (unsigned)(g.cm0 - cml) * e2, o1 = (unsigned)(g.cm1 - cml) * e2;
+      const __amdgpu_buffer_rsrc_t ry =
+          nd_rsrc(na.buf_in + la * na.in_stride + (int64_t)cml * e2,
+                  (unsigned)(abs(g.cm1 - g.cm0) + 1) * e2 * 8u);
       const int nt = (E + 63) / 64;
       // ext = V - Z^T Z on the 64 x 64 tiles of its lower triangle (ext is
       // symmetric; readers take the mirror of an entry above); the children's
@@ -1464,11 +1470,11 @@ __global__ __launch_bounds__(512) void k_nd_cut(NdArgs na) {
             for (int v = 0; v < 4; ++v) {
               const int x = min(x0 + mt.row(i, v), E - 1);
               const int pa0 = invt[0][C + x], pa1 = invt[1][C + x];
-              const double v0 = nd_load(r0f, (pa0 >= 0 && pb0 >= 0)
-                                                 ? 8u * (unsigned)sym_at(pa0, pb0, g.Ein) : kNdOob, 0);
-              const double v1 = nd_load(r1f, (pa1 >= 0 && pb1 >= 0)
-                                                 ? 8u * (unsigned)sym_at(pa1, pb1, g.Ein) : kNdOob, 0);
-              vv[i][j][v] = v0 + v1;
+              const unsigned off =
+                  (pa0 >= 0 && pb0 >= 0)   ? 8u * (o0 + (unsigned)sym_at(pa0, pb0, g.Ein))
+                  : (pa1 >= 0 && pb1 >= 0) ? 8u * (o1 + (unsigned)sym_at(pa1, pb1, g.Ein))
+                                           : kNdOob;
+              vv[i][j][v] = nd_load(ry, off, 0);
             }
         }
         mt.step_ld(zl + x0, zl + y0, ZLD, C, E - x0, E - y0);
@@ -2053,10 +2059,15 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(5))) void k
   }
   // ext = V - Z^T Z, V the children's external entries: per block column,
   // this lane's 8 entries are loaded together, then written
-  const double* Y0 = na.buf_in + g.la * na.in_stride + (int64_t)g.cm0 * g.Ein * g.Ein;
-  const double* Y1 = na.buf_in + g.la * na.in_stride + (int64_t)g.cm1 * g.Ein * g.Ein;
-  const unsigned cb = (unsigned)(g.Ein * g.Ein * 8);
-  const __amdgpu_buffer_rsrc_t r0 = nd_rsrc(Y0, cb), r1 = nd_rsrc(Y1, cb);
+  // an external port is a port of one child only, so an entry of V is one
+  // child's entry (or none): one load per entry, over both children's
+  // blocks of the level buffer
+  const int cml = min(g.cm0, g.cm1);
+  const unsigned e2 = (unsigned)(g.Ein * g.Ein);
+  const unsigned o0 = (unsigned)(g.cm0 - cml) * e2, o1 = (unsigned)(g.cm1 - cml) * e2;
+  const __amdgpu_buffer_rsrc_t ry =
+      nd_rsrc(na.buf_in + g.la * na.in_stride + (int64_t)cml * e2,
+              (unsigned)(abs(g.cm1 - g.cm0) + 1) * e2 * 8u);
   double* ext = na.buf_out + g.la * na.out_stride + (int64_t)g.m * Emax * Emax;
 #pragma unroll
   for (int j = 0; j < 2; ++j) {
@@ -2070,12 +2081,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(5))) void k
       for (int v = 0; v < 4; ++v) {
         const int x = min(x0 + mt.row(i, v), E - 1);
         const int pa0 = invt[0][c + x], pa1 = invt[1][c + x];
-        // an entry that a child does not hold reads 0 without a memory access
-        const double v0 = nd_load(r0, (pa0 >= 0 && pb0 >= 0) ? 8u * (unsigned)sym_at(pa0, pb0, g.Ein)
-                                                             : kNdOob, 0);
-        const double v1 = nd_load(r1, (pa1 >= 0 && pb1 >= 0) ? 8u * (unsigned)sym_at(pa1, pb1, g.Ein)
-                                                             : kNdOob, 0);
-        vv[i][v] = v0 + v1;
+        // an entry that no child holds reads 0 without a memory access
+        const unsigned off = (pa0 >= 0 && pb0 >= 0) ? 8u * (o0 + (unsigned)sym_at(pa0, pb0, g.Ein))
+                             : (pa1 >= 0 && pb1 >= 0) ? 8u * (o1 + (unsigned)sym_at(pa1, pb1, g.Ein))
+                                                      : kNdOob;
+        vv[i][v] = nd_load(ry, off, 0);
       }
 #pragma unroll
     for (int i = 0; i < 2; ++i)
