@@ -162,14 +162,14 @@ __device__ __forceinline__ double recip(double a) {
   return r;
 }
 
-// 1 / sqrt(a) for a > 0: the hardware estimate and three Newton steps
-// (r <- r + r (1 - a r^2) / 2), each squaring the relative error, to fp64
-// accuracy; a dozen instructions instead of a correctly rounded square root
-// and division.
+// 1 / sqrt(a) for a > 0: the hardware estimate and two Newton steps
+// (r <- r + r (1 - a r^2) / 2), each squaring the relative error: from any
+// estimate good to 14 bits or more that reaches fp64 accuracy; nine
+// instructions instead of a correctly rounded square root and division.
 __device__ __forceinline__ double rsqrt_nr(double a) {
   double r = __builtin_amdgcn_rsq(a);
 #pragma unroll
-  for (int i = 0; i < 3; ++i) r = fma(0.5 * r, fma(-a * r, r, 1.0), r);
+  for (int i = 0; i < 2; ++i) r = fma(0.5 * r, fma(-a * r, r, 1.0), r);
   return r;
 }
 
