@@ -699,8 +699,11 @@ struct BatchState {
   int64_t ent_cap = 0;
   double* ws = nullptr;
   int64_t ws_cap = 0;          // doubles
+  int* d_start = nullptr;      // the layers' first blocks of the batched w_max reduction
+  int64_t start_cap = 0;
   std::vector<NdBatchLayer> h_layers;
   std::vector<int2> h_ent;
+  std::vector<int> h_start;
 };
 constexpr size_t kBatchBudget = (size_t)24 << 30;
 BatchState g_batch[kMaxDevices];
@@ -757,11 +760,15 @@ rxnn_status rxnn_remap_layers(rxnn_layer* const* layers, const float* const* W, 
   BatchState& bs = g_batch[dev];
   bs.h_layers.resize((size_t)n);
   bs.h_ent.clear();
+  bs.h_start.resize((size_t)n + 1);
+  bs.h_start[0] = 0;
   for (int32_t i = 0; i < n; ++i) {
     rxnn_layer* L = layers[i];
     bs.h_layers[(size_t)i] = NdBatchLayer{L->ms, W[i], L->gpt};
     const int64_t na = (int64_t)L->ms.R * L->ms.C * L->ms.A;
     for (int64_t a = 0; a < na; ++a) bs.h_ent.push_back(make_int2(i, (int)a));
+    bs.h_start[(size_t)i + 1] =
+        bs.h_start[(size_t)i] + (L->ms.wmax_fixed > 0.0f ? 1 : absmax_blocks(L->ms.P * L->ms.Q));
   }
   const int64_t total = (int64_t)bs.h_ent.size();
   const MapScalars& ms0 = layers[0]->ms;
@@ -777,14 +784,19 @@ rxnn_status rxnn_remap_layers(rxnn_layer* const* layers, const float* const* W, 
   if ((st = grow_dev(&bs.d_layers, &bs.layers_cap, n, "batch layer table"))) return st;
   if ((st = grow_dev(&bs.d_ent, &bs.ent_cap, total, "batch array table"))) return st;
   if ((st = grow_dev(&bs.ws, &bs.ws_cap, chunk * per, "batch build workspace"))) return st;
+  if ((st = grow_dev(&bs.d_start, &bs.start_cap, (int64_t)n + 1, "batch w_max table"))) return st;
   // the tables go over on the stream (from pageable memory: staged before return)
   HIP_TRY(hipMemcpyAsync(bs.d_layers, bs.h_layers.data(), (size_t)n * sizeof(NdBatchLayer),
                          hipMemcpyHostToDevice, s));
   HIP_TRY(hipMemcpyAsync(bs.d_ent, bs.h_ent.data(), (size_t)total * sizeof(int2),
                          hipMemcpyHostToDevice, s));
-  for (int32_t i = 0; i < n; ++i) {
-    layers[i]->gload_valid = false;   // the row loads follow G'
-    hipError_t e = launch_wmax(layers[i], W[i], s);
+  HIP_TRY(hipMemcpyAsync(bs.d_start, bs.h_start.data(), ((size_t)n + 1) * sizeof(int),
+                         hipMemcpyHostToDevice, s));
+  for (int32_t i = 0; i < n; ++i) layers[i]->gload_valid = false;   // the row loads follow G'
+  {
+    // every layer's w_max at once
+    ProfScope t("wmax", s);
+    hipError_t e = launch_absmax_batch(bs.d_layers, bs.d_start, n, bs.h_start[(size_t)n], s);
     if (e != hipSuccess) return fail(RXNN_EHIP, "w_max launch failed: %s", hipGetErrorString(e));
   }
   const NdBatch batch{bs.d_layers, bs.d_ent};

@@ -129,6 +129,11 @@ struct NdBatch {
 hipError_t launch_nd_build(const MapScalars& ms, const float* W, float* gpt, int64_t arr0,
                            int64_t n, int bs, double* ws, hipStream_t s,
                            const NdBatch* batch = nullptr);
+// blocks of the w_max reduction of n weights; w_max of every layer of a batch
+// in two launches (layer l: blocks [start[l], start[l + 1]), start on the device)
+int absmax_blocks(int64_t n);
+hipError_t launch_absmax_batch(const NdBatchLayer* layers, const int* start, int n_layers,
+                               int total_blocks, hipStream_t s);
 
 struct VmmLaunch {
   const float* V;       // DAC output: FC Bv x ldx rows (ldx = fc_ldv); conv the padded NCHW tensor

@@ -267,6 +267,57 @@ __global__ __launch_bounds__(256) void k_absmax(const float* __restrict__ W, int
   }
 }
 
+// w_max of every layer of a batch in two launches.  k_wmax_init sets each
+// layer's w_max to its fixed value or to 0; k_absmax_batch then gives layer l
+// the blocks [start[l], start[l + 1]) (as many as its own reduction would
+// launch), and each block folds its max |W| into w_max by one atomic max on
+// the bits (|w| as unsigned bits orders as |w| does), without fences or a
+// last-block step.
+__global__ void k_wmax_init(const NdBatchLayer* __restrict__ layers, int n_layers) {
+  const int l = (int)(blockIdx.x * blockDim.x + threadIdx.x);
+  if (l >= n_layers) return;
+  const MapScalars& ms = layers[l].ms;
+  unsigned* out = reinterpret_cast<unsigned*>(const_cast<float*>(ms.d_wmax));
+  out[0] = ms.wmax_fixed > 0.0f ? __float_as_uint(ms.wmax_fixed) : 0u;
+}
+
+__global__ __launch_bounds__(256) void k_absmax_batch(const NdBatchLayer* __restrict__ layers,
+                                                      const int* __restrict__ start,
+                                                      int n_layers) {
+  __shared__ unsigned wm[4];
+  __shared__ int sl;
+  // the layer whose block range holds this block: the ranges partition the
+  // grid, so exactly one thread finds it (one round of loads, not a chain)
+  for (int base = 0; base < n_layers; base += (int)blockDim.x) {
+    const int t = base + (int)threadIdx.x;
+    if (t < n_layers && start[t] <= (int)blockIdx.x && (int)blockIdx.x < start[t + 1]) sl = t;
+  }
+  __syncthreads();
+  const int l = sl;
+  const MapScalars& ms = layers[l].ms;
+  if (ms.wmax_fixed > 0.0f) return;
+  unsigned* out = reinterpret_cast<unsigned*>(const_cast<float*>(ms.d_wmax));
+  const int b = (int)blockIdx.x - start[l], nb = start[l + 1] - start[l];
+  const float* W = layers[l].W;
+  const int64_t n = ms.P * ms.Q;
+  unsigned m = 0;
+  const int64_t stride = (int64_t)nb * blockDim.x;
+  for (int64_t i0 = (int64_t)b * blockDim.x + threadIdx.x; i0 < n; i0 += 8 * stride) {
+    unsigned v[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int64_t i = i0 + j * stride;
+      v[j] = i < n ? __float_as_uint(fabsf(W[i])) : 0u;
+    }
+#pragma unroll
+    for (int j = 0; j < 8; ++j) m = max(m, v[j]);
+  }
+  for (int off = 32; off > 0; off >>= 1) m = max(m, (unsigned)__shfl_xor((int)m, off, 64));
+  if ((threadIdx.x & 63) == 0) wm[threadIdx.x >> 6] = m;
+  __syncthreads();
+  if (threadIdx.x == 0) atomicMax(&out[0], max(max(wm[0], wm[1]), max(wm[2], wm[3])));
+}
+
 __global__ void k_fill_u32(unsigned* p, int64_t n, unsigned v) {
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
        i += (int64_t)gridDim.x * blockDim.x)
@@ -276,10 +327,23 @@ __global__ void k_fill_u32(unsigned* p, int64_t n, unsigned v) {
 }  // namespace
 
 hipError_t launch_absmax(const float* W, int64_t n, unsigned* out, hipStream_t s) {
+  hipLaunchKernelGGL(k_absmax, dim3((unsigned)absmax_blocks(n)), dim3(256), 0, s, W, n, out);
+  return hipGetLastError();
+}
+
+int absmax_blocks(int64_t n) {
   int64_t blocks = (n + 2047) / 2048;   // at least 8 elements per thread
   if (blocks > 1024) blocks = 1024;
   if (blocks < 1) blocks = 1;
-  hipLaunchKernelGGL(k_absmax, dim3((unsigned)blocks), dim3(256), 0, s, W, n, out);
+  return (int)blocks;
+}
+
+hipError_t launch_absmax_batch(const NdBatchLayer* layers, const int* start, int n_layers,
+                               int total_blocks, hipStream_t s) {
+  hipLaunchKernelGGL(k_wmax_init, dim3((unsigned)((n_layers + 255) / 256)), dim3(256), 0, s, layers,
+                     n_layers);
+  hipLaunchKernelGGL(k_absmax_batch, dim3((unsigned)total_blocks), dim3(256), 0, s, layers, start,
+                     n_layers);
   return hipGetLastError();
 }
 
