@@ -33,16 +33,16 @@
 // region's block.  Merges with 8 to 64 shared nodes: one workgroup per
 // merge eliminates them with the shared rows in registers (k_nd_cut; each
 // lane reads one multiplier per 16 rows from LDS, the FMAs take them by DPP
-// row broadcast), and the Schur update of the external block runs on 64 x 64 fp64 MFMA tiles of
-// its lower triangle, in the same workgroup for small merges, else in
-// k_nd_schur; the final step with at most 64 row inputs likewise.  Merges
-// with 128 shared nodes: k_nd_cut2 (panels of 256 external columns), then
-// k_nd_schur.  The merge of the two halves of a large grid and its final
-// step: the combined matrix is built dense (k_nd_dense0) and eliminated in
-// stages of 64 pivots (k_nd_cut<64, 2>, k_nd_dschur).  Other sizes run on one
-// workgroup with the shared rows in global memory, eliminated in blocks
-// of 16 (Cholesky of the 16 x 16 pivot block, triangular solve of its rows,
-// rank-16 update of the rest).  All arithmetic is fp64; wire conductances
+// row broadcast), and the Schur update of the external block runs on 64 x 64
+// fp64 MFMA tiles of its lower triangle, in the same workgroup for small
+// merges, else in k_nd_schur; the final step with at most 64 row inputs
+// likewise.  Merges with 128 shared nodes: k_nd_cut2 (panels of 256 external
+// columns), then k_nd_schur.  The merge of the two halves of a large grid
+// and its final step: the combined matrix is built dense (k_nd_dense0) and
+// eliminated in stages of 64 pivots (k_nd_cut<64, 2>, k_nd_dschur).  Other
+// sizes run on one workgroup with the shared rows in global memory,
+// eliminated in blocks of 16 (Cholesky of the 16 x 16 pivot block,
+// triangular solve of its rows, rank-16 update of the rest).  All arithmetic is fp64; wire conductances
 // exceed device conductances by about four orders of magnitude, and the
 // elimination of series wires loses about that many digits, leaving G'
 // accurate to ~1e-12.  Every wire, driver and sense resistance must be
@@ -1150,7 +1150,8 @@ __device__ void region_merge16(int T, int RI, int RJ, const double* ch, double* 
     const int kb0 = col_key(y < C + E ? invt[y] : -1), kb1 = col_key(y < C + E ? invt[80 + y] : -1);
     double U[C];
 #pragma unroll
-    for (int x = 0; x < C; ++x) U[x] = pick(ch, invt[x], kb0, EIN) + pick(ch + CH1, invt[80 + x], kb1, EIN);
+    for (int x = 0; x < C; ++x)
+      U[x] = pick(ch, invt[x], kb0, EIN) + pick(ch + CH1, invt[80 + x], kb1, EIN);
     double sq[C];
 #pragma unroll
     for (int k = 0; k < C; ++k) {
@@ -1562,10 +1563,11 @@ __global__ __launch_bounds__(512) void k_nd_cut(NdArgs na) {
 // unchanged); chunks of 8 rows wholly at or above the pivot are skipped.
 // Every lane reads one multiplier per 16 rows from LDS and the FMAs take them
 // by DPP row broadcast (the LDS traffic of every lane reading every
-// multiplier would bound the loop).  The pivot loop runs over blocks of 8
-// pivots unrolled, which keeps the code small.  Z (the eliminated rows scaled
-// by D^-1/2, over this panel's externals) goes to scratch for k_nd_schur or,
-// for the final step, for k_nd_gprod.
+// multiplier would bound the loop).  The pivots go in pairs, one barrier per
+// pair (below); the loop runs over blocks of 8 pivots unrolled, which keeps
+// the code small.  The gather takes 8 x 8 blocks through LDS (below).  Z
+// (the eliminated rows scaled by D^-1/2, over this panel's externals) goes
+// to scratch for k_nd_schur or, for the final step, for k_nd_gprod.
 // ---------------------------------------------------------------------------
 constexpr int C2 = 128;              // cut nodes
 constexpr int P2 = 256;              // external columns per panel
