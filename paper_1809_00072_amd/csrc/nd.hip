@@ -42,11 +42,12 @@
 // eliminated in stages of 64 pivots (k_nd_cut<64, 2>, k_nd_dschur).  Other
 // sizes run on one workgroup with the shared rows in global memory,
 // eliminated in blocks of 16 (Cholesky of the 16 x 16 pivot block,
-// triangular solve of its rows, rank-16 update of the rest).  All arithmetic is fp64; wire conductances
-// exceed device conductances by about four orders of magnitude, and the
-// elimination of series wires loses about that many digits, leaving G'
-// accurate to ~1e-12.  Every wire, driver and sense resistance must be
-// positive (zero resistances take the row sweep instead).
+// triangular solve of its rows, rank-16 update of the rest).  All
+// arithmetic is fp64; wire conductances exceed device conductances by about
+// four orders of magnitude, and the elimination of series wires loses about
+// that many digits, leaving G' accurate to ~1e-12.  Every wire, driver and
+// sense resistance must be positive (zero resistances take the row sweep
+// instead).
 
 #include <algorithm>
 #include <utility>
