@@ -236,7 +236,7 @@ constexpr int BUFA = 16 * 65, BUFB = 8 * 145;
 // externals), per level and per boundary variant (bit 1: the merged block
 // has ports on its right, bit 0: on its top) - the only geometry on which
 // the port maps of a merge depend.
-struct BlkTab {
+struct alignas(16) BlkTab {
   short s[BLEVELS][4][2][64];
 };
 
@@ -476,11 +476,17 @@ __device__ __forceinline__ void merge_mfma(int T, int i0, int j0, const short* t
 // those into the region's 16 x 16 block, which goes to the level buffer.
 // LDS (78 KB) allows two workgroups per CU.
 __global__ __launch_bounds__(64 * BWAVES) void k_nd_block(NdArgs na) {
-  __shared__ short tab[BLEVELS * 4 * 2 * 64];
+  __shared__ __attribute__((aligned(16))) short tab[BLEVELS * 4 * 2 * 64];
   __shared__ double bufA[BWAVES][BUFA];
   __shared__ double bufB[BWAVES][BUFB];
-  const short* ct = &kBlkTab.s[0][0][0][0];
-  for (int e = threadIdx.x; e < BLEVELS * 4 * 2 * 64; e += 64 * BWAVES) tab[e] = ct[e];
+  {
+    // the port tables to LDS, 16 bytes per thread and load
+    constexpr int NV = BLEVELS * 4 * 2 * 64 * (int)sizeof(short) / 16;
+    static_assert(BLEVELS * 4 * 2 * 64 * sizeof(short) % 16 == 0, "whole 16-byte pieces");
+    const uint4* ct = reinterpret_cast<const uint4*>(&kBlkTab.s[0][0][0][0]);
+    uint4* lt = reinterpret_cast<uint4*>(&tab[0]);
+    for (int e = threadIdx.x; e < NV; e += 64 * BWAVES) lt[e] = ct[e];
+  }
   __syncthreads();
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
   const int T = na.T;
