@@ -926,7 +926,11 @@ template <int NS>
 __device__ void inverse_tables(const NdArgs& na, const MergeGeom& g, short (*invt)[NS], int NT) {
   const int tid = threadIdx.x;
   const bool vert = na.vert != 0;
-  for (int t = tid; t < 2 * NS; t += NT) invt[t / NS][t % NS] = -1;
+  // every slot -1 (no port), 16 bytes per store
+  static_assert(2 * NS * sizeof(short) % 16 == 0, "whole 16-byte pieces");
+  uint4* iv = reinterpret_cast<uint4*>(&invt[0][0]);
+  for (int t = tid; t < 2 * NS * (int)sizeof(short) / 16; t += NT)
+    iv[t] = make_uint4(~0u, ~0u, ~0u, ~0u);
   __syncthreads();
   for (int t = tid; t < 2 * g.Ein; t += NT) {
     const int ch = t / g.Ein, p = t - ch * g.Ein;
@@ -1208,7 +1212,7 @@ template <int C, int MODE>
 __global__ __launch_bounds__(512) void k_nd_cut(NdArgs na) {
   static_assert(C <= 64, "at most 64 cut rows");
   constexpr bool FINAL = MODE == 1;
-  __shared__ short invt[2][MAXSLOT];
+  __shared__ __attribute__((aligned(16))) short invt[2][MAXSLOT];
   __shared__ double rowb[2][64];
   __shared__ double isq[64];
   // final step: the eliminated rows' sink and source columns for G'
@@ -1583,7 +1587,7 @@ constexpr int MAXSLOT2 = 1024;       // slots of a merge with 128 cut nodes (<= 
 
 template <bool FINAL>
 __global__ __launch_bounds__(2 * CP2) void k_nd_cut2(NdArgs na) {
-  __shared__ short invt[2][FINAL ? 1 : MAXSLOT2];
+  __shared__ __attribute__((aligned(16))) short invt[2][FINAL ? 1 : MAXSLOT2];
   __shared__ double rowb[2][2][CP2];   // [pair parity][row of the pair][column]
   __shared__ double pivs[2][3];
   __shared__ double dg[C2];
@@ -1842,7 +1846,7 @@ __device__ __forceinline__ bool dead_tile(const NdArgs& na, int x, int y) {
 // lower tiles).
 template <bool FINAL>
 __global__ __launch_bounds__(256) void k_nd_dense0(NdArgs na) {
-  __shared__ short invt[2][MAXSLOT2];
+  __shared__ __attribute__((aligned(16))) short invt[2][MAXSLOT2];
   const int n = na.dn, ld = na.dldo;
   const int nrb = (n + 15) / 16;
   const int64_t la = blockIdx.x / nrb;
@@ -2007,7 +2011,7 @@ __global__ __launch_bounds__(256) void k_nd_dschur(NdArgs na) {
 // above.
 // Five waves per SIMD (96 VGPRs): its gathers need many waves in flight.
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(5))) void k_nd_schur(NdArgs na) {
-  __shared__ short invt[2][MAXSLOT2];
+  __shared__ __attribute__((aligned(16))) short invt[2][MAXSLOT2];
   __shared__ __attribute__((aligned(16))) double zab[2 * KC64 * KLD];
   double* za = zab;
   double* zb = zab + KC64 * KLD;
