@@ -208,8 +208,9 @@ rxnn_status rxnn_remap_layer(rxnn_layer* layer, const float* W, void* stream);
  *           r_col and r_sense (the nested-dissection build); weights, sizes,
  *           w_max, slicing, device table and variation may differ.
  *   W       host array of n device pointers.
- * The library keeps, per device, the batch's layer and array tables (copied
- * from host memory on `stream`) and one build workspace of at most 24 GiB,
+ * The library keeps, per device, the batch's layer, array and w_max-block
+ * tables (copied from host memory on `stream`; every layer's w_max is
+ * reduced in one pass) and one build workspace of at most 24 GiB,
  * grown on demand and held until the process ends; batches whose workspace
  * would exceed it are built in chunks.  Calls that overlap on one device
  * (different streams) race on these.  RXNN_EINVAL for a bad argument or a
